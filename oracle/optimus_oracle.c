@@ -1,0 +1,192 @@
+/*
+ * Optimus grouped-operator ORACLE -- test infrastructure only.
+ *
+ * This file is the plain, slow, obviously-correct CPU reference that the GPU
+ * library is checked against. Only the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark may load it; the product path never does.
+ * It shares no code, header, table or helper with the HIP library.
+ *
+ * Everything is fp64 and written one member (one operator instance) at a
+ * time, exactly as the unfused program would compute it:
+ *
+ *  - Horizontal optimization, group fusion (paper Sec. 3.2, item 1): a group
+ *    of independent operators run in one launch must give the same outputs as
+ *    running each operator on its own (the rewrite is semantics-preserving,
+ *    Sec. 2.2; inputs and outputs map one-to-one, Sec. 3.3 item 2). So the
+ *    oracle of a group is a loop over members calling the single-operator
+ *    definition below.
+ *  - Vertical optimization, split-concat elimination (Sec. 3.2, item 2;
+ *    appendix Sec. 8.1 listings): the oracle materialises every split piece
+ *    in its own array, applies the per-piece operator, then concatenates
+ *    along dim 1 into a fresh output -- the unoptimised program, step by step.
+ *  - The chained example of Sec. 3.2 (LayerNorm per split piece, then an
+ *    activation per piece, then the concat) is split_op_cat() below.
+ *
+ * The paper names the operators (Table 1: batch_linear, batch_layernorm,
+ * batch_tanh / sigmoid / relu, batch_aten_mul) but not their formulas; the
+ * formulas here are the standard definitions of those PyTorch operators:
+ *   Linear      y[m][n] = sum_k x[m][k] * w[n][k] + b[n]   (w is [N, K])
+ *   LayerNorm   over the last dim, biased variance, eps inside the sqrt
+ *   relu / sigmoid / tanh / silu(x) = x * sigmoid(x)
+ *
+ * Parity pins for every function are in the CPU test suite (library
+ * routines, closed forms, invariants, brute force, the appendix example).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORC_ACT_NONE = 0, ORC_ACT_RELU = 1, ORC_ACT_SIGMOID = 2, ORC_ACT_TANH = 3, ORC_ACT_SILU = 4 };
+
+/* ---------------------------------------------------------------- scalars */
+
+/* Logistic function 1 / (1 + e^-x), evaluated on the side where the
+ * exponential cannot overflow: for x < 0 it is written as e^x / (1 + e^x). */
+static double orc_sigmoid(double x) {
+  if (x >= 0.0) return 1.0 / (1.0 + exp(-x));
+  double e = exp(x);
+  return e / (1.0 + e);
+}
+
+/* One activation applied to one value (Table 1 pointwise patterns). */
+double oracle_act_scalar(double x, int act) {
+  switch (act) {
+    case ORC_ACT_NONE: return x;
+    case ORC_ACT_RELU: return x > 0.0 ? x : 0.0;
+    case ORC_ACT_SIGMOID: return orc_sigmoid(x);
+    case ORC_ACT_TANH: return tanh(x);
+    case ORC_ACT_SILU: return x * orc_sigmoid(x); /* the x * sigmoid(x) product */
+    default: return NAN;
+  }
+}
+
+/* ---------------------------------------------------------------- Linear */
+
+/* One Linear operator: Y[M][N] = X[M][K] . W[N][K]^T (+ bias[N]), then the
+ * optional activation. Row-major, unit inner stride, row strides ldx/ldw/ldy.
+ * The sum runs over k in ascending order, in fp64. */
+void oracle_linear(const double* x, int64_t ldx, const double* w, int64_t ldw,
+                   const double* bias, double* y, int64_t ldy,
+                   int64_t M, int64_t N, int64_t K, int act) {
+#pragma omp parallel for schedule(static)
+  for (int64_t m = 0; m < M; ++m) {
+    for (int64_t n = 0; n < N; ++n) {
+      double s = 0.0;
+      for (int64_t k = 0; k < K; ++k) s += x[m * ldx + k] * w[n * ldw + k];
+      if (bias) s += bias[n];
+      y[m * ldy + n] = oracle_act_scalar(s, act);
+    }
+  }
+}
+
+/* Only the listed rows of the same Linear (rows[i] for i < nrows), written to
+ * y[i][*]. Used to check outputs of groups too large for the full oracle. */
+void oracle_linear_rows(const double* x, int64_t ldx, const double* w, int64_t ldw,
+                        const double* bias, double* y, int64_t ldy,
+                        const int64_t* rows, int64_t nrows, int64_t N, int64_t K, int act) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < nrows; ++i) {
+    const double* xr = x + rows[i] * ldx;
+    for (int64_t n = 0; n < N; ++n) {
+      double s = 0.0;
+      for (int64_t k = 0; k < K; ++k) s += xr[k] * w[n * ldw + k];
+      if (bias) s += bias[n];
+      y[i * ldy + n] = oracle_act_scalar(s, act);
+    }
+  }
+}
+
+/* ------------------------------------------------------------- LayerNorm */
+
+/* One row of LayerNorm over `cols` values:
+ *   mu = (1/n) sum x,  var = (1/n) sum (x - mu)^2  (biased, two passes),
+ *   y  = (x - mu) / sqrt(var + eps) * gamma + beta, then the activation.
+ * gamma == NULL means 1, beta == NULL means 0. */
+static void orc_ln_row(const double* x, double* y, int64_t cols, const double* gamma,
+                       const double* beta, double eps, int act) {
+  double mu = 0.0;
+  for (int64_t c = 0; c < cols; ++c) mu += x[c];
+  mu /= (double)cols;
+  double var = 0.0;
+  for (int64_t c = 0; c < cols; ++c) {
+    double d = x[c] - mu;
+    var += d * d;
+  }
+  var /= (double)cols;
+  double inv = 1.0 / sqrt(var + eps);
+  for (int64_t c = 0; c < cols; ++c) {
+    double v = (x[c] - mu) * inv;
+    if (gamma) v *= gamma[c];
+    if (beta) v += beta[c];
+    y[c] = oracle_act_scalar(v, act);
+  }
+}
+
+/* One LayerNorm operator over a [rows, cols] member (normalised dim = last). */
+void oracle_layernorm(const double* x, int64_t ldx, double* y, int64_t ldy,
+                      int64_t rows, int64_t cols, const double* gamma, const double* beta,
+                      double eps, int act) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) orc_ln_row(x + r * ldx, y + r * ldy, cols, gamma, beta, eps, act);
+}
+
+/* ------------------------------------------------------------- pointwise */
+
+/* One pointwise operator over a [rows, cols] member. */
+void oracle_pointwise(const double* x, int64_t ldx, double* y, int64_t ldy,
+                      int64_t rows, int64_t cols, int act) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t c = 0; c < cols; ++c) y[r * ldy + c] = oracle_act_scalar(x[r * ldx + c], act);
+}
+
+/* ------------------------------------------------------- split-op-concat */
+
+/* The unoptimised split -> per-piece op -> concat program along dim 1 of a
+ * [rows, D] tensor (Sec. 3.2 chained example; appendix Sec. 8.1 listing):
+ *   1. split: copy piece j, columns [o_j, o_j + w_j) with o_j = sum_{i<j} w_i,
+ *      into its own contiguous [rows, w_j] array;
+ *   2. per piece: LayerNorm_j (if apply_ln; gamma[j] / beta[j] may be NULL)
+ *      then the activation, into a second array;
+ *   3. concat along dim 1: copy each result back at column offset o_j of out.
+ * Returns 0 on success, -1 if the widths do not sum to D or allocation fails. */
+int oracle_split_op_cat(const double* in, int64_t ldin, double* out, int64_t ldout,
+                        int64_t rows, int64_t D, int32_t n_pieces, const int64_t* widths,
+                        const double* const* gamma, const double* const* beta,
+                        int32_t apply_ln, double eps, int act) {
+  int64_t total = 0;
+  for (int32_t j = 0; j < n_pieces; ++j) total += widths[j];
+  if (total != D) return -1;
+  int64_t off = 0;
+  for (int32_t j = 0; j < n_pieces; ++j) {
+    int64_t w = widths[j];
+    double* piece = (double*)malloc(sizeof(double) * (size_t)(rows * w + 1));
+    double* res = (double*)malloc(sizeof(double) * (size_t)(rows * w + 1));
+    if (!piece || !res) { free(piece); free(res); return -1; }
+    for (int64_t r = 0; r < rows; ++r)                      /* 1. split */
+      for (int64_t c = 0; c < w; ++c) piece[r * w + c] = in[r * ldin + off + c];
+    if (apply_ln)                                           /* 2. per-piece op */
+      oracle_layernorm(piece, w, res, w, rows, w, gamma ? gamma[j] : NULL,
+                       beta ? beta[j] : NULL, eps, act);
+    else
+      oracle_pointwise(piece, w, res, w, rows, w, act);
+    for (int64_t r = 0; r < rows; ++r)                      /* 3. concat */
+      for (int64_t c = 0; c < w; ++c) out[r * ldout + off + c] = res[r * w + c];
+    free(piece);
+    free(res);
+    off += w;
+  }
+  return 0;
+}
+
+/* Number of OpenMP threads the oracle's parallel loops use (1 without OpenMP). */
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  extern int omp_get_max_threads(void);
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

@@ -1,0 +1,235 @@
+"""Seeded synthetic operator groups shaped like the paper's recommendation workloads.
+
+This module only draws inputs: shapes, random values, and the one rounding of
+each drawn fp64 value to its storage dtype. It holds none of the grouped
+operators' arithmetic, and it is the only code the GPU path and the CPU oracle
+share: tests draw a workload here, hand the storage tensors to the GPU and the
+exact fp64 images of the same values to the oracle.
+
+Every generator uses ``numpy.random.Generator(PCG64(seed))`` and a fixed draw
+order: shapes first, then per member in the order (W, b, gamma, beta, X).
+``N(mu, v)`` takes v as the VARIANCE. Sizes can be scaled down (for parity
+tests) without changing the recipe.
+
+The five workload families (paper Sec. 5: DLRM-style recommendation models;
+Sec. 5.2: many small bf16 operators; Sec. 3.2: split -> LayerNorm -> act -> cat):
+  tiny_group        G=8 fp32 Linear members, shared batch 512, -> LayerNorm -> tanh
+  launch_bound      G=256 tiny bf16 Linear members, batch 2048, -> sigmoid
+  split_op_cat      [8192, 4096] bf16 split into 32 Dirichlet widths, LN_j -> silu, cat
+  towers            26 bf16 MLP towers Linear(in_g->512)+relu+Linear(512->256)+LayerNorm, batch 4096
+  large_group       G=32 bf16 Linear members, batch 16384, K=1024 -> LayerNorm -> tanh
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+DTYPES = {"fp32": torch.float32, "bf16": torch.bfloat16}
+
+
+def rng(seed: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def to_storage(a: np.ndarray, dtype: str) -> torch.Tensor:
+    """Round an fp64 draw once to the storage dtype (CPU tensor)."""
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64)).to(DTYPES[dtype]).contiguous()
+
+
+def exact64(t: Optional[torch.Tensor]) -> Optional[np.ndarray]:
+    """The exact fp64 image of a stored tensor (widening is exact)."""
+    if t is None:
+        return None
+    return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+def _normal(g: np.random.Generator, shape, var: float) -> np.ndarray:
+    return g.standard_normal(shape) * np.sqrt(var)
+
+
+@dataclass
+class LinearMember:
+    x: torch.Tensor                 # [M, K]
+    w: torch.Tensor                 # [N, K]
+    b: Optional[torch.Tensor]       # [N]
+
+    @property
+    def M(self): return self.x.shape[0]
+
+    @property
+    def K(self): return self.x.shape[1]
+
+    @property
+    def N(self): return self.w.shape[0]
+
+
+@dataclass
+class LinearLNGroup:
+    """Group of Linear members, each optionally followed by LayerNorm and an activation."""
+    name: str
+    dtype: str
+    members: List[LinearMember]
+    act: str                                     # activation after the last op
+    ln: bool = False
+    gammas: List[torch.Tensor] = field(default_factory=list)
+    betas: List[torch.Tensor] = field(default_factory=list)
+    eps: float = 1e-5
+
+    @property
+    def G(self): return len(self.members)
+
+
+@dataclass
+class SplitOpCatInput:
+    name: str
+    dtype: str
+    x: torch.Tensor                              # [rows, D]
+    widths: List[int]
+    gammas: List[torch.Tensor]
+    betas: List[torch.Tensor]
+    eps: float
+    act: str
+
+
+@dataclass
+class Tower:
+    x: torch.Tensor       # [B, in_g]
+    w1: torch.Tensor      # [512, in_g]
+    b1: torch.Tensor
+    w2: torch.Tensor      # [256, 512]
+    b2: torch.Tensor
+    gamma: torch.Tensor   # [256]
+    beta: torch.Tensor
+
+
+@dataclass
+class TowersInput:
+    name: str
+    dtype: str
+    towers: List[Tower]
+    eps: float = 1e-5
+
+    @property
+    def G(self): return len(self.towers)
+
+
+# ------------------------------------------------------------------ helpers
+def dirichlet_widths(g: np.random.Generator, n_pieces: int, D: int, unit: int = 16) -> List[int]:
+    """Widths that are multiples of ``unit`` summing to D, from a Dirichlet(1) draw.
+
+    Each piece gets one unit; the remaining units are shared by largest remainder
+    of (remaining * p), ties to the lower index.
+    """
+    total_units = D // unit
+    assert total_units * unit == D and total_units >= n_pieces
+    p = g.dirichlet(np.ones(n_pieces))
+    spare = total_units - n_pieces
+    q = spare * p
+    base = np.floor(q).astype(np.int64)
+    left = spare - int(base.sum())
+    frac = q - base
+    order = sorted(range(n_pieces), key=lambda i: (-frac[i], i))
+    for i in order[:left]:
+        base[i] += 1
+    return [int(unit * (1 + b)) for b in base]
+
+
+def xavier_uniform(g, n_out: int, n_in: int) -> np.ndarray:
+    a = np.sqrt(6.0 / (n_in + n_out))
+    return g.uniform(-a, a, size=(n_out, n_in))
+
+
+def kaiming_normal_relu(g, n_out: int, n_in: int) -> np.ndarray:
+    return _normal(g, (n_out, n_in), 2.0 / n_in)
+
+
+# ------------------------------------------------------------------ workloads
+def tiny_group(seed: int = 0, G: int = 8, M: int = 512) -> LinearLNGroup:
+    """G fp32 Linear members on a shared batch M; K in {64,128,256}, N in {64,128};
+    X, W ~ N(0, 1/K), b ~ N(0, 0.01); then LayerNorm(eps 1e-5, gamma 1, beta 0) and tanh."""
+    g = rng(seed)
+    Ks = g.choice([64, 128, 256], size=G)
+    Ns = g.choice([64, 128], size=G)
+    members, gammas, betas = [], [], []
+    for K, N in zip(Ks.tolist(), Ns.tolist()):
+        w = to_storage(_normal(g, (N, K), 1.0 / K), "fp32")
+        b = to_storage(_normal(g, (N,), 0.01), "fp32")
+        gammas.append(to_storage(np.ones(N), "fp32"))
+        betas.append(to_storage(np.zeros(N), "fp32"))
+        x = to_storage(_normal(g, (M, K), 1.0 / K), "fp32")
+        members.append(LinearMember(x, w, b))
+    return LinearLNGroup("tiny_group", "fp32", members, "tanh", True, gammas, betas, 1e-5)
+
+
+def launch_bound(seed: int = 0, G: int = 256, M: int = 2048) -> LinearLNGroup:
+    """G bf16 Linear members, batch M, K and N in {16,32,48,64}; X ~ N(0,1),
+    W Xavier-uniform, b ~ N(0, 0.01); then sigmoid."""
+    g = rng(seed)
+    Ks = g.choice([16, 32, 48, 64], size=G)
+    Ns = g.choice([16, 32, 48, 64], size=G)
+    members = []
+    for K, N in zip(Ks.tolist(), Ns.tolist()):
+        w = to_storage(xavier_uniform(g, N, K), "bf16")
+        b = to_storage(_normal(g, (N,), 0.01), "bf16")
+        x = to_storage(g.standard_normal((M, K)), "bf16")
+        members.append(LinearMember(x, w, b))
+    return LinearLNGroup("launch_bound", "bf16", members, "sigmoid")
+
+
+def split_op_cat(seed: int = 0, rows: int = 8192, D: int = 4096, n_pieces: int = 32) -> SplitOpCatInput:
+    """[rows, D] bf16 ~ N(0,1) split along dim 1 into Dirichlet widths (multiples
+    of 16); per piece LayerNorm(gamma ~ U(0.5,1.5), beta ~ N(0,0.1), eps 1e-5) then silu."""
+    g = rng(seed)
+    widths = dirichlet_widths(g, n_pieces, D)
+    gammas, betas = [], []
+    for w in widths:
+        gammas.append(to_storage(g.uniform(0.5, 1.5, size=w), "bf16"))
+        betas.append(to_storage(_normal(g, (w,), 0.1), "bf16"))
+    x = to_storage(g.standard_normal((rows, D)), "bf16")
+    return SplitOpCatInput("split_op_cat", "bf16", x, widths, gammas, betas, 1e-5, "silu")
+
+
+def towers(seed: int = 0, G: int = 26, M: int = 4096, hidden: int = 512, out: int = 256) -> TowersInput:
+    """G bf16 towers: Linear(in_g->hidden)+relu+Linear(hidden->out)+LayerNorm(gamma 1, beta 0);
+    in_g in {64,128,256,512}; X ~ N(0,1); Kaiming-normal (fan_in, relu) weights; b ~ N(0, 0.01)."""
+    g = rng(seed)
+    ins = g.choice([64, 128, 256, 512], size=G)
+    ts = []
+    for K in ins.tolist():
+        w1 = to_storage(kaiming_normal_relu(g, hidden, K), "bf16")
+        b1 = to_storage(_normal(g, (hidden,), 0.01), "bf16")
+        w2 = to_storage(kaiming_normal_relu(g, out, hidden), "bf16")
+        b2 = to_storage(_normal(g, (out,), 0.01), "bf16")
+        gamma = to_storage(np.ones(out), "bf16")
+        beta = to_storage(np.zeros(out), "bf16")
+        x = to_storage(g.standard_normal((M, K)), "bf16")
+        ts.append(Tower(x, w1, b1, w2, b2, gamma, beta))
+    return TowersInput("towers", "bf16", ts, 1e-5)
+
+
+def large_group(seed: int = 0, G: int = 32, M: int = 16384, K: int = 1024) -> LinearLNGroup:
+    """G bf16 Linear members, batch M, K in-features, N in {256,512,1024};
+    X ~ N(0,1), W ~ N(0, 1/K), b ~ N(0, 0.01); then LayerNorm(gamma 1, beta 0) and tanh."""
+    g = rng(seed)
+    Ns = g.choice([256, 512, 1024], size=G)
+    members, gammas, betas = [], [], []
+    for N in Ns.tolist():
+        w = to_storage(_normal(g, (N, K), 1.0 / K), "bf16")
+        b = to_storage(_normal(g, (N,), 0.01), "bf16")
+        gammas.append(to_storage(np.ones(N), "bf16"))
+        betas.append(to_storage(np.zeros(N), "bf16"))
+        x = to_storage(g.standard_normal((M, K)), "bf16")
+        members.append(LinearMember(x, w, b))
+    return LinearLNGroup("large_group", "bf16", members, "tanh", True, gammas, betas, 1e-5)
+
+
+WORKLOADS = {
+    "tiny_group": tiny_group,
+    "launch_bound": launch_bound,
+    "split_op_cat": split_op_cat,
+    "towers": towers,
+    "large_group": large_group,
+}

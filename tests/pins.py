@@ -1,0 +1,262 @@
+"""Pins for the fp64 oracle: every check compares the oracle with something other
+than itself -- a library routine (numpy BLAS, torch fp64 ops), a closed form, an
+invariant, brute force in exact integer arithmetic, or the paper's appendix
+split-concat example. Each check raises AssertionError on a mismatch.
+
+Kept as plain functions taking an ``Oracle`` so that the mutant test can run the
+same checks against copies of the oracle with planted mistakes.
+"""
+from __future__ import annotations
+
+import itertools
+import json
+import os
+
+import numpy as np
+import torch
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def _nrm(a, b):
+    """inf-normwise relative difference."""
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    return np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-300)
+
+
+# ---------------------------------------------------------------- Linear
+def linear_vs_blas(orc):
+    """Y = X W^T + b against numpy's float64 matmul (BLAS dgemm) and torch's F.linear."""
+    g = _rng(1)
+    for (M, N, K) in [(7, 5, 3), (33, 17, 64), (64, 48, 16), (5, 129, 31)]:
+        x, w, b = g.standard_normal((M, K)), g.standard_normal((N, K)), g.standard_normal(N)
+        y = orc.linear(x, w, b)
+        assert y.shape == (M, N)
+        assert _nrm(y, x @ w.T + b) < 1e-13, (M, N, K)
+        t = torch.nn.functional.linear(torch.from_numpy(x), torch.from_numpy(w), torch.from_numpy(b))
+        assert _nrm(y, t.numpy()) < 1e-13
+        assert _nrm(orc.linear(x, w, None), x @ w.T) < 1e-13
+
+
+def linear_special_cases(orc):
+    """Zero weights give the bias exactly; identity weights give the input exactly."""
+    g = _rng(2)
+    x, b = g.standard_normal((9, 6)), g.standard_normal(4)
+    y = orc.linear(x, np.zeros((4, 6)), b)
+    assert np.array_equal(y, np.broadcast_to(b, (9, 4)))
+    x = g.standard_normal((11, 8))
+    assert np.array_equal(orc.linear(x, np.eye(8), np.zeros(8)), x)
+    assert np.array_equal(orc.linear(x, np.eye(8), None), x)
+
+
+def linear_brute_force(orc):
+    """Tiny groups of small integers: exact integer sums by brute force (every
+    M, N, K in 1..4), so the oracle must match bit for bit."""
+    g = _rng(3)
+    for M, N, K in itertools.product(range(1, 5), repeat=3):
+        x = g.integers(-4, 5, size=(M, K))
+        w = g.integers(-4, 5, size=(N, K))
+        b = g.integers(-8, 9, size=N)
+        want = [[sum(int(x[m, k]) * int(w[n, k]) for k in range(K)) + int(b[n]) for n in range(N)]
+                for m in range(M)]
+        got = orc.linear(x.astype(np.float64), w.astype(np.float64), b.astype(np.float64))
+        assert np.array_equal(got, np.array(want, dtype=np.float64)), (M, N, K)
+
+
+def linear_epilogue(orc):
+    """Linear followed by an activation equals the activation of the Linear."""
+    g = _rng(4)
+    x, w, b = g.standard_normal((13, 24)), g.standard_normal((10, 24)), g.standard_normal(10)
+    z = x @ w.T + b
+    want = {"relu": np.maximum(z, 0), "sigmoid": 1 / (1 + np.exp(-z)), "tanh": np.tanh(z),
+            "silu": z / (1 + np.exp(-z)), "none": z}
+    for a, v in want.items():
+        assert _nrm(orc.linear(x, w, b, a), v) < 1e-13, a
+
+
+def linear_rows_subset(orc):
+    """Selected rows equal the same rows of the full Linear."""
+    g = _rng(5)
+    x, w, b = g.standard_normal((40, 20)), g.standard_normal((7, 20)), g.standard_normal(7)
+    rows = np.array([39, 0, 17, 17, 3])
+    assert np.array_equal(orc.linear_rows(x, w, b, rows, "tanh"), orc.linear(x, w, b, "tanh")[rows])
+    assert _nrm(orc.linear_rows(x, w, b, rows), (x @ w.T + b)[rows]) < 1e-13
+
+
+def linear_batch_fusion(orc):
+    """Paper Sec. 3.2 batch fusion: equal-shape members stacked into one batched
+    matmul (then unbound) give the grouped per-member results."""
+    g = _rng(6)
+    G, M, N, K = 5, 12, 8, 16
+    xs, ws, bs = g.standard_normal((G, M, K)), g.standard_normal((G, N, K)), g.standard_normal((G, N))
+    stacked = np.matmul(xs, np.transpose(ws, (0, 2, 1))) + bs[:, None, :]
+    got = orc.grouped_linear(list(xs), list(ws), list(bs))
+    for i in range(G):
+        assert _nrm(got[i], stacked[i]) < 1e-13
+
+
+# ---------------------------------------------------------------- LayerNorm
+def layernorm_vs_torch(orc):
+    """Row LayerNorm against torch.nn.functional.layer_norm in fp64."""
+    g = _rng(7)
+    for rows, cols in [(5, 16), (9, 48), (3, 1000), (4, 1)]:
+        x = g.standard_normal((rows, cols)) * 3 + 1
+        gm, bt = g.uniform(0.5, 1.5, cols), g.standard_normal(cols)
+        t = torch.nn.functional.layer_norm(torch.from_numpy(x), (cols,), torch.from_numpy(gm),
+                                           torch.from_numpy(bt), eps=1e-5).numpy()
+        assert _nrm(orc.layernorm(x, gm, bt, 1e-5), t) < 1e-12, (rows, cols)
+        t0 = torch.nn.functional.layer_norm(torch.from_numpy(x), (cols,), eps=1e-3).numpy()
+        assert _nrm(orc.layernorm(x, None, None, 1e-3), t0) < 1e-12
+
+
+def layernorm_invariants(orc):
+    """gamma=1, beta=0: per-row mean 0 and per-row (biased) variance equal to
+    s2/(s2+eps) in closed form, where s2 is the row's biased variance."""
+    g = _rng(8)
+    x = g.standard_normal((20, 64)) * g.uniform(0.01, 10, (20, 1)) + g.standard_normal((20, 1))
+    for eps in (1e-5, 0.5):
+        y = orc.layernorm(x, np.ones(64), np.zeros(64), eps)
+        s2 = x.var(axis=1)
+        assert np.max(np.abs(y.mean(axis=1))) < 1e-12
+        assert np.max(np.abs(y.var(axis=1) - s2 / (s2 + eps))) < 1e-12
+
+
+def layernorm_constant_row(orc):
+    """A constant row has zero variance, so the output is beta exactly, with no NaN."""
+    bt = np.linspace(-2, 2, 32)
+    x = np.full((3, 32), 0.75)
+    y = orc.layernorm(x, np.full(32, 3.0), bt, 1e-5)
+    assert np.array_equal(y, np.broadcast_to(bt, (3, 32)))
+
+
+def layernorm_affine(orc):
+    """The affine step is elementwise: LN(x; gamma, beta) = gamma * LN(x; 1, 0) + beta."""
+    g = _rng(9)
+    x = g.standard_normal((6, 40))
+    gm, bt = g.uniform(-2, 2, 40), g.standard_normal(40)
+    plain = orc.layernorm(x, None, None, 1e-5)
+    assert _nrm(orc.layernorm(x, gm, bt, 1e-5), plain * gm + bt) < 1e-14
+
+
+def layernorm_epilogue_and_batch(orc):
+    """LN followed by an activation; equal-width members equal one LN over the stack."""
+    g = _rng(10)
+    x = g.standard_normal((4, 8, 24))
+    stack = torch.nn.functional.layer_norm(torch.from_numpy(x), (24,), eps=1e-5).numpy()
+    got = orc.grouped_layernorm(list(x), [None] * 4, [None] * 4, 1e-5, "tanh")
+    for i in range(4):
+        assert _nrm(got[i], np.tanh(stack[i])) < 1e-12
+
+
+# ---------------------------------------------------------------- pointwise
+def pointwise_closed_forms(orc):
+    """Values at 0, symmetries, the tanh/sigmoid identity, saturation, numpy forms."""
+    a = orc.act_scalar
+    assert a(0.0, "sigmoid") == 0.5 and a(0.0, "tanh") == 0.0 and a(0.0, "silu") == 0.0
+    assert a(-3.5, "relu") == 0.0 and a(2.25, "relu") == 2.25 and a(-7.0, "none") == -7.0
+    assert abs(a(30.0, "sigmoid") - 1.0) < 1e-13 and 0.0 <= a(-30.0, "sigmoid") < 1e-13
+    assert a(-800.0, "sigmoid") == 0.0 and a(800.0, "sigmoid") == 1.0   # no overflow
+    assert a(-800.0, "silu") == 0.0
+    x = np.linspace(-12, 12, 97)
+    for v in x:
+        s, t = a(v, "sigmoid"), a(v, "tanh")
+        assert abs(a(-v, "sigmoid") - (1.0 - s)) < 1e-15
+        assert a(-v, "tanh") == -t
+        assert abs(t - (2.0 * a(2.0 * v, "sigmoid") - 1.0)) < 1e-14
+        assert abs(a(v, "silu") - v * s) < 1e-14
+    g = _rng(11)
+    z = g.standard_normal((7, 33)) * 4
+    assert _nrm(orc.pointwise(z, "tanh"), np.tanh(z)) < 1e-15
+    assert _nrm(orc.pointwise(z, "sigmoid"), 1 / (1 + np.exp(-z))) < 1e-14
+    assert _nrm(orc.pointwise(z, "silu"), z / (1 + np.exp(-z))) < 1e-14
+    assert np.array_equal(orc.pointwise(z, "relu"), np.maximum(z, 0))
+    assert np.array_equal(orc.pointwise(z, "none"), z)
+
+
+# ---------------------------------------------------------------- split-op-cat
+def split_concat_appendix_example(orc):
+    """Appendix Sec. 8.1 listing: split [2,4] on dim 1, split the second piece
+    [2,2], cat the three pieces on dim 1 -- the optimized program returns x."""
+    with open(os.path.join(GOLDEN, "appendix_split_concat.json")) as f:
+        ex = json.load(f)
+    shape = tuple(ex["input_shape"])
+    first = ex["first_split_sizes"]
+    nested = ex["nested_split_sizes"]
+    flat = first[:ex["nested_split_of_piece"]] + nested + first[ex["nested_split_of_piece"] + 1:]
+    assert flat == ex["flattened_widths"]
+    x = _rng(12).standard_normal(shape)
+    y = orc.split_op_cat(x, flat, apply_ln=False, act="none")
+    assert np.array_equal(y, x)
+    # the same program written with torch on the CPU gives the same tensor
+    t = torch.from_numpy(x)
+    fs = torch.split(t, first, dim=1)
+    pieces = [fs[0]] + list(fs[1].split(tuple(nested), 1))
+    assert np.array_equal(torch.cat(pieces, dim=1).numpy(), y)
+
+
+def split_concat_identity_random(orc):
+    """split o cat is the identity for any widths (bit-exact)."""
+    g = _rng(13)
+    for D, n in [(64, 4), (4096, 32), (48, 3)]:
+        cuts = np.sort(g.choice(np.arange(1, D), size=n - 1, replace=False))
+        widths = np.diff(np.concatenate([[0], cuts, [D]]))
+        x = g.standard_normal((5, D))
+        assert np.array_equal(orc.split_op_cat(x, widths, apply_ln=False, act="none"), x)
+
+
+def split_op_cat_pieces(orc):
+    """Each output piece equals torch's LayerNorm + activation of that input piece,
+    placed at its column offset; one piece of full width is a plain row LayerNorm;
+    equal widths equal one LayerNorm over the stacked pieces (batch fusion)."""
+    g = _rng(14)
+    widths = [16, 48, 32, 160]
+    D = sum(widths)
+    x = g.standard_normal((6, D)) * 2 + 0.5
+    gms = [g.uniform(0.5, 1.5, w) for w in widths]
+    bts = [g.standard_normal(w) * 0.3 for w in widths]
+    y = orc.split_op_cat(x, widths, gms, bts, True, 1e-5, "silu")
+    o = 0
+    for w, gm, bt in zip(widths, gms, bts):
+        ref = torch.nn.functional.layer_norm(torch.from_numpy(x[:, o:o + w]), (w,), torch.from_numpy(gm),
+                                             torch.from_numpy(bt), eps=1e-5)
+        ref = torch.nn.functional.silu(ref).numpy()
+        assert _nrm(y[:, o:o + w], ref) < 1e-12, (o, w)
+        o += w
+    one = orc.split_op_cat(x, [D], None, None, True, 1e-5, "none")
+    assert _nrm(one, torch.nn.functional.layer_norm(torch.from_numpy(x), (D,), eps=1e-5).numpy()) < 1e-12
+    xe = g.standard_normal((3, 8 * 16))
+    ye = orc.split_op_cat(xe, [16] * 8, None, None, True, 1e-5, "tanh")
+    st = torch.nn.functional.layer_norm(torch.from_numpy(xe.reshape(3, 8, 16)), (16,), eps=1e-5)
+    assert _nrm(ye, torch.tanh(st).numpy().reshape(3, 128)) < 1e-12
+
+
+def split_op_cat_tag(orc):
+    """gamma_j = 0, beta_j = j: every element of piece j must equal j, so piece j
+    lands exactly at its offset."""
+    widths = [2, 5, 1, 8, 16]
+    x = _rng(15).standard_normal((4, sum(widths)))
+    y = orc.split_op_cat(x, widths, [np.zeros(w) for w in widths],
+                         [np.full(w, float(j)) for j, w in enumerate(widths)], True, 1e-5, "none")
+    want = np.concatenate([np.full((4, w), float(j)) for j, w in enumerate(widths)], axis=1)
+    assert np.array_equal(y, want)
+
+
+def split_op_cat_bad_widths(orc):
+    try:
+        orc.split_op_cat(np.zeros((2, 6)), [2, 2], apply_ln=False)
+    except ValueError:
+        return
+    raise AssertionError("widths not summing to D must be rejected")
+
+
+ALL_PINS = [
+    linear_vs_blas, linear_special_cases, linear_brute_force, linear_epilogue, linear_rows_subset,
+    linear_batch_fusion, layernorm_vs_torch, layernorm_invariants, layernorm_constant_row,
+    layernorm_affine, layernorm_epilogue_and_batch, pointwise_closed_forms,
+    split_concat_appendix_example, split_concat_identity_random, split_op_cat_pieces, split_op_cat_tag,
+    split_op_cat_bad_widths,
+]

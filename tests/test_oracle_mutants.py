@@ -1,0 +1,54 @@
+"""Plant plausible mistakes in copies of the oracle's C source (on the CPU) and
+check that the pins catch every one of them: a dropped term, a wrong sign, a
+wrong index, a transposed operand, a wrong offset."""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+import oracle
+from tests import pins
+
+SRC = open(oracle.SOURCE).read()
+
+# (name, exact text in optimus_oracle.c, replacement)
+MUTANTS = [
+    ("transposed_weight", "s += x[m * ldx + k] * w[n * ldw + k];", "s += x[m * ldx + k] * w[k * ldw + n];"),
+    ("dropped_last_k_term", "for (int64_t k = 0; k < K; ++k) s += x[m * ldx + k]",
+     "for (int64_t k = 0; k + 1 < K; ++k) s += x[m * ldx + k]"),
+    ("dropped_bias", "      if (bias) s += bias[n];\n      y[m * ldy + n]", "      y[m * ldy + n]"),
+    ("bias_wrong_index", "if (bias) s += bias[n];\n      y[m * ldy", "if (bias) s += bias[m % N];\n      y[m * ldy"),
+    ("rows_wrong_row", "const double* xr = x + rows[i] * ldx;", "const double* xr = x + i * ldx;"),
+    ("unbiased_variance", "var /= (double)cols;", "var /= (double)(cols > 1 ? cols - 1 : 1);"),
+    ("eps_outside_sqrt", "double inv = 1.0 / sqrt(var + eps);", "double inv = 1.0 / (sqrt(var) + eps);"),
+    ("mean_not_subtracted", "double v = (x[c] - mu) * inv;", "double v = x[c] * inv;"),
+    ("beta_dropped", "if (beta) v += beta[c];", ""),
+    ("gamma_beta_swapped", "if (gamma) v *= gamma[c];\n    if (beta) v += beta[c];",
+     "if (beta) v *= beta[c];\n    if (gamma) v += gamma[c];"),
+    ("sigmoid_wrong_sign", "return 1.0 / (1.0 + exp(-x));", "return 1.0 / (1.0 + exp(x));"),
+    ("silu_without_x", "return x * orc_sigmoid(x);", "return orc_sigmoid(x);"),
+    ("relu_leaky", "return x > 0.0 ? x : 0.0;", "return x > 0.0 ? x : 0.01 * x;"),
+    ("tanh_half_arg", "return tanh(x);", "return tanh(0.5 * x);"),
+    ("split_offset_dropped", "piece[r * w + c] = in[r * ldin + off + c];", "piece[r * w + c] = in[r * ldin + c];"),
+    ("cat_offset_dropped", "out[r * ldout + off + c] = res[r * w + c];", "out[r * ldout + c] = res[r * w + c];"),
+    ("piece_params_shifted", "gamma ? gamma[j] : NULL,\n                       beta ? beta[j] : NULL",
+     "gamma ? gamma[0] : NULL,\n                       beta ? beta[0] : NULL"),
+]
+
+
+@pytest.mark.parametrize("name,find,repl", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, find, repl):
+    assert SRC.count(find) == 1, f"mutation site for {name} not found exactly once"
+    src = tmp_path / "mutant.c"
+    src.write_text(SRC.replace(find, repl))
+    lib = str(tmp_path / "libmutant.so")
+    oracle.compile_library(str(src), lib)
+    orc = oracle.Oracle(lib)
+    caught = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(orc)
+        except AssertionError:
+            caught.append(pin.__name__)
+    assert caught, f"no pin catches the planted mistake {name}"
