@@ -1,0 +1,323 @@
+"""Benchmark: microseconds per op-group of the grouped launches vs the per-op launch chain.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload launch_bound]
+
+One step = one pass of the workload's op-group (every grouped launch of the
+group, e.g. grouped Linear + fused sigmoid for `launch_bound`) over one batch
+of seeded synthetic input that is already resident in HBM. Inputs are
+rotated over enough copies that each step reads data no longer held in the
+256 MB last-level cache. Prints one JSON line.
+
+Workloads (the seeded groups of paper_2607_02945_amd.synth): launch_bound
+(default; G=256 bf16 Linear + sigmoid, B=2048), tiny_group, split_op_cat,
+towers, large_group.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "µs per op-group + achieved TFLOP/s or HBM GB/s vs per-op launch chain"
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
+CACHE_BYTES = 512 << 20  # rotate inputs over at least this much memory per step cycle
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="launch_bound",
+                    choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-chain", action="store_true", help="skip timing the per-op launch chain")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU-baseline duration")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------- op-groups
+class OpGroup:
+    """Plans for one copy of a workload: `grouped` runs the optimized program,
+    `chain` the per-op launch chain; `dominant` is the plan of the kernel that
+    dominates the grouped time."""
+
+    def __init__(self):
+        self.grouped = []      # list of (plan, mode)
+        self.chain = []        # list of (plan, mode)
+        self.horizontal = []   # split-op-cat only: horizontal fusion without the vertical rewrite
+        self.dominant = None
+
+    def run(self, which, stream=None, ev=None):
+        seq = getattr(self, which)
+        for plan, mode in seq:
+            if ev is not None and plan is self.dominant:
+                ev[0].record()
+                plan.execute(mode, stream)
+                ev[1].record()
+            else:
+                plan.execute(mode, stream)
+
+
+def build_copy(name, wl, torch, B):
+    """Device copy of the workload's inputs and outputs plus its plans."""
+    og = OpGroup()
+    cu = lambda t: t.to("cuda")
+    bf = torch.bfloat16
+    if name in ("launch_bound", "tiny_group", "large_group"):
+        xs = [cu(m.x) for m in wl.members]
+        ws = [cu(m.w) for m in wl.members]
+        bs = [cu(m.b) for m in wl.members]
+        dt = xs[0].dtype
+        ys = [torch.empty((m.M, m.N), dtype=dt, device="cuda") for m in wl.members]
+        if not wl.ln:
+            lin = B.optimus_plan_linear(xs, ws, bs, ys, wl.act)
+            og.grouped = [(lin, "grouped")]
+            y1 = [torch.empty_like(y) for y in ys]
+            lin0 = B.optimus_plan_linear(xs, ws, bs, y1, "none")
+            pw = B.optimus_plan_pointwise(y1, ys, wl.act)
+            og.chain = [(lin0, "chain"), (pw, "chain")]
+            og.dominant = lin
+            og.keep = (xs, ws, bs, ys, y1)
+        else:
+            zs = [torch.empty_like(y) for y in ys]
+            gs = [cu(g) for g in wl.gammas]
+            be = [cu(b) for b in wl.betas]
+            lin = B.optimus_plan_linear(xs, ws, bs, ys, "none")
+            ln = B.optimus_plan_layernorm(ys, zs, gs, be, wl.eps, wl.act)
+            og.grouped = [(lin, "grouped"), (ln, "grouped")]
+            z1 = [torch.empty_like(y) for y in ys]
+            ln0 = B.optimus_plan_layernorm(ys, z1, gs, be, wl.eps, "none")
+            pw = B.optimus_plan_pointwise(z1, zs, wl.act)
+            og.chain = [(lin, "chain"), (ln0, "chain"), (pw, "chain")]
+            og.dominant = lin
+            og.keep = (xs, ws, bs, ys, zs, gs, be, z1)
+        og.plans = [lin]
+    elif name == "split_op_cat":
+        x = cu(wl.x)
+        y = torch.empty_like(x)
+        gs = [cu(g) for g in wl.gammas]
+        bs = [cu(b) for b in wl.betas]
+        soc = B.optimus_plan_split_op_cat(x, y, wl.widths, gs, bs, True, wl.eps, wl.act)
+        og.grouped = [(soc, "grouped")]
+        og.chain = [(soc, "chain")]
+        og.horizontal = [(soc, "horizontal")]
+        og.dominant = soc
+        og.keep = (x, y, gs, bs)
+    elif name == "towers":
+        T = wl.towers
+        xs = [cu(t.x) for t in T]
+        h = [torch.empty((t.x.shape[0], t.w1.shape[0]), dtype=bf, device="cuda") for t in T]
+        o = [torch.empty((t.x.shape[0], t.w2.shape[0]), dtype=bf, device="cuda") for t in T]
+        z = [torch.empty_like(v) for v in o]
+        w1, b1, w2, b2 = ([cu(getattr(t, a)) for t in T] for a in ("w1", "b1", "w2", "b2"))
+        gm, be = [cu(t.gamma) for t in T], [cu(t.beta) for t in T]
+        l1 = B.optimus_plan_linear(xs, w1, b1, h, "relu")
+        l2 = B.optimus_plan_linear(h, w2, b2, o, "none")
+        ln = B.optimus_plan_layernorm(o, z, gm, be, wl.eps, "none")
+        og.grouped = [(l1, "grouped"), (l2, "grouped"), (ln, "grouped")]
+        h0 = [torch.empty_like(v) for v in h]
+        l1n = B.optimus_plan_linear(xs, w1, b1, h0, "none")
+        relu = B.optimus_plan_pointwise(h0, h, "relu")
+        og.chain = [(l1n, "chain"), (relu, "chain"), (l2, "chain"), (ln, "chain")]
+        og.dominant = l1
+        og.keep = (xs, h, o, z, w1, b1, w2, b2, gm, be, h0)
+    return og
+
+
+def workload_bytes(name, wl):
+    """Bytes of device memory one copy of the workload touches."""
+    if name == "split_op_cat":
+        return 2 * wl.x.numel() * 2
+    if name == "towers":
+        return sum(t.x.numel() * 2 + (512 + 256 + 256) * t.x.shape[0] * 2 for t in wl.towers)
+    s = 4 if wl.dtype == "fp32" else 2
+    return sum((m.x.numel() + m.w.numel() + 2 * m.M * m.N) * s for m in wl.members)
+
+
+def describe(name, wl):
+    if name == "split_op_cat":
+        return {"workload": name, "rows": wl.x.shape[0], "D": wl.x.shape[1], "pieces": len(wl.widths),
+                "per_piece": "LayerNorm(affine) + silu", "seed": 0}
+    if name == "towers":
+        return {"workload": name, "towers": wl.G, "batch": wl.towers[0].x.shape[0],
+                "layers": "Linear(in_g->512)+relu, Linear(512->256), LayerNorm", "seed": 0}
+    return {"workload": name, "G": wl.G, "batch": wl.members[0].M,
+            "K": sorted({m.K for m in wl.members}), "N": sorted({m.N for m in wl.members}),
+            "epilogue": ("LayerNorm+" if wl.ln else "") + wl.act, "seed": 0}
+
+
+# ---------------------------------------------------------------------- CPU baseline
+def cpu_baseline(name, wl, target_s):
+    """The oracle as it stands, on the host cores, on a bounded sample of the
+    same workload, scaled to microseconds per op-group."""
+    import oracle
+    from paper_2607_02945_amd import synth
+    orc = oracle.get()
+    e = synth.exact64
+    t_total, frac_total, reps = 0.0, 0.0, 0
+    if name == "split_op_cat":
+        rows = min(wl.x.shape[0], 1024)
+        xs = e(wl.x[:rows])
+        gs, bs = [e(g) for g in wl.gammas], [e(b) for b in wl.betas]
+        frac, sample = rows / wl.x.shape[0], f"first {rows} of {wl.x.shape[0]} rows"
+        work = lambda: orc.split_op_cat(xs, wl.widths, gs, bs, True, wl.eps, wl.act)
+    elif name == "towers":
+        rows = 64
+        ins = [(e(t.x[:rows]), e(t.w1), e(t.b1), e(t.w2), e(t.b2), e(t.gamma), e(t.beta)) for t in wl.towers]
+        frac, sample = rows / wl.towers[0].x.shape[0], f"first {rows} rows of every tower"
+        work = lambda: [orc.layernorm(orc.linear(orc.linear(x, w1, b1, "relu"), w2, b2), g, b, wl.eps)
+                        for x, w1, b1, w2, b2, g, b in ins]
+    else:
+        M = wl.members[0].M
+        rows = M if name != "large_group" else 64
+        ins = [(e(m.x[:rows]), e(m.w), e(m.b)) for m in wl.members]
+        lns = [(e(g), e(b)) for g, b in zip(wl.gammas, wl.betas)] if wl.ln else None
+        frac = rows / M
+        sample = "whole group" if rows == M else f"first {rows} of {M} rows of every member"
+
+        def work():
+            for i, (x, w, b) in enumerate(ins):
+                if lns is None:
+                    orc.linear(x, w, b, wl.act)
+                else:
+                    orc.layernorm(orc.linear(x, w, b), lns[i][0], lns[i][1], wl.eps, wl.act)
+    while t_total < target_s or reps == 0:
+        t0 = time.perf_counter()
+        work()
+        t_total += time.perf_counter() - t0
+        frac_total += frac
+        reps += 1
+        if t_total > 3 * target_s:
+            break
+    us = t_total / frac_total * 1e6
+    return {"value": round(us, 1), "unit": "µs per op-group", "cores": orc.num_threads(), "kind": "oracle",
+            "sample": f"{sample}, {reps} pass(es), {t_total:.1f} s, fp64 C loops, scaled to one op-group"}
+
+
+# ---------------------------------------------------------------------- rocprofv3 traffic
+def traffic_from_profile(kernel, name):
+    """HBM bytes per launch from the committed counter summary, when it was
+    taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}__{name}.pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        pmc = json.load(f)
+    if pmc.get("sources_sha256") != sources_hash():
+        return None
+    return pmc.get("hbm_bytes_per_launch")
+
+
+def sources_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_02945_amd", "csrc")
+    for fn in sorted(os.listdir(csrc)):
+        if fn.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, fn), "rb") as f:
+                h.update(fn.encode() + f.read())
+    return h.hexdigest()
+
+
+# ---------------------------------------------------------------------- main
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build measures one GPU only (the grouped path needs no exchange "
+              "between GPUs; see the sharding design); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2607_02945_amd import binding as B
+    from paper_2607_02945_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    B.lib()  # loud failure if the HIP library is missing
+    wl = synth.WORKLOADS[args.workload](args.seed)
+    dtype = "fp32" if getattr(wl, "dtype", "bf16") == "fp32" else "bf16"
+    per_copy = workload_bytes(args.workload, wl)
+    copies = max(1, min(16, math.ceil(CACHE_BYTES / per_copy)))
+    ogs = [build_copy(args.workload, wl, torch, B) for _ in range(copies)]
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def timed(which, steps, warmup, with_events):
+        for i in range(warmup):
+            ogs[i % copies].run(which, stream)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)] \
+            if with_events else None
+        t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        t_start.record()
+        for i in range(steps):
+            ogs[i % copies].run(which, stream, evs[i] if evs else None)
+        t_end.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        total_ms = t_start.elapsed_time(t_end)
+        kern_ms = [a.elapsed_time(b) for a, b in evs] if evs else None
+        return total_ms, wall, kern_ms
+
+    total_ms, wall, kern_ms = timed("grouped", args.steps, args.warmup, True)
+    ms_step = total_ms / args.steps
+    info = ogs[0].dominant.info()
+    launches = sum(p.info()["launches"] for p, _ in ogs[0].grouped)
+    out = {
+        "metric": METRIC, "value": round(ms_step * 1000.0, 3), "unit": "µs", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 6),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+        "data": "synthetic (seeded PCG64 draws of the workload's shapes and distributions)",
+        "config": describe(args.workload, wl),
+        "launches_per_group": launches, "input_copies": copies, "wall_ms_per_step": round(wall * 1e3 / args.steps, 6),
+    }
+    # achieved throughput of the whole op-group
+    flops = sum(p.info()["flops"] for p, _ in ogs[0].grouped)
+    nbytes = sum(p.info()["bytes"] for p, _ in ogs[0].grouped)
+    out["group_tflops"] = round(flops / (ms_step * 1e-3) / 1e12, 3)
+    out["group_hbm_gbs"] = round(nbytes / (ms_step * 1e-3) / 1e9, 1)
+    # roofline of the dominant kernel: algorithmic work per launch / mean launch duration
+    k_ms = float(np.mean(kern_ms))
+    ai = info["flops"] / max(info["bytes"], 1.0)
+    ridge = PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if info["flops"] > 0 and ai >= ridge:
+        ach = info["flops"] / (k_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
+                "frac": round(ach / PEAK_TFLOPS[dtype], 4)}
+    else:
+        ach = info["bytes"] / (k_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
+    roof.update({"kernel": info["kernel"], "kernel_us": round(k_ms * 1000.0, 3),
+                 "algorithmic_bytes": info["bytes"], "algorithmic_flops": info["flops"],
+                 "traffic": traffic_from_profile(info["kernel"], args.workload)})
+    out["roofline"] = roof
+    if not args.no_chain:
+        csteps = max(5, min(args.steps, 50))
+        c_ms, _, _ = timed("chain", csteps, max(2, args.warmup // 4), False)
+        c_step = c_ms / csteps
+        out["chain"] = {"us_per_group": round(c_step * 1000.0, 3),
+                        "launches_per_group": sum(p.info()["chain_launches"] for p, m in ogs[0].chain
+                                                  if m == "chain") + sum(1 for p, m in ogs[0].chain if m != "chain"),
+                        "speedup": round(c_step / ms_step, 2)}
+    if ogs[0].horizontal:
+        hsteps = max(5, min(args.steps, 50))
+        h_ms, _, _ = timed("horizontal", hsteps, 2, False)
+        out["horizontal_only"] = {"us_per_group": round(h_ms / hsteps * 1000.0, 3), "launches_per_group": 3}
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(args.workload, wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,255 @@
+/*
+ * liboptimus -- grouped execution of many independent, same-type small
+ * operators on one MI355X (gfx950): one kernel launch per operator type
+ * instead of one launch per operator instance.
+ *
+ * The operation is the runtime effect of the horizontal and vertical graph
+ * rewrites of "Optimus: A Generic Operator-Level PyTorch Model
+ * Transformation Framework" (KDD '26):
+ *   - horizontal group fusion (Sec. 3.2, item 1): independent operator
+ *     instances, without data dependency between them (Sec. 4.1), executed
+ *     in a single launch with their tensor layouts unchanged and their sizes
+ *     free to differ;
+ *   - vertical split-concat elimination (Sec. 3.2, item 2; appendix Sec. 8.1)
+ *     chained with per-piece LayerNorm and activation (Sec. 3.2, chained
+ *     example): no split copy and no concat kernel;
+ *   - the patterns of Table 1 that these entry points cover: batch_linear /
+ *     batch_linear_post_grad (grouped Linear), batch_layernorm (grouped
+ *     LayerNorm), batch_relu / sigmoid / tanh and their ATen forms, with
+ *     x*sigmoid(x) as the activation product of batch_aten_mul (grouped
+ *     pointwise), and split_cat / merge_splits / split_cat_to_slices
+ *     (split-op-cat);
+ *   - inputs and outputs map one-to-one (Sec. 3.3, item 2): every member
+ *     reads its own input tensors and writes its own caller-owned output.
+ *
+ * Conventions for every entry point
+ *   Ownership   The caller owns every tensor (device memory, e.g. from
+ *               PyTorch). The library never frees a caller pointer.
+ *               Descriptor arrays and the host arrays inside descriptors
+ *               (widths, gamma/beta pointer arrays) are read during the call
+ *               only and may be freed when it returns.
+ *   Layout      2-D row-major tensors with unit inner stride; `ld*` is the
+ *               row stride in ELEMENTS (>= the row length). All members of
+ *               one call share one dtype (the group key: operator, dtype,
+ *               activation); their shapes may differ.
+ *   Streams     Work is enqueued on `stream` (a hipStream_t; NULL = the
+ *               default stream) and the call returns before it completes.
+ *               Device buffers must stay valid until the stream has run it.
+ *   Errors      No exception crosses the ABI. On any non-OK status nothing
+ *               is launched and optimus_last_error() (thread-local) says why.
+ *               G == 0 is a valid no-op (the rewrite's no-op fallback,
+ *               Sec. 3.3).
+ *               OPTIMUS_ERR_INVALID_ARG  null required pointer, a size < 1,
+ *                                        ld < row length, widths not summing
+ *                                        to D, G < 0, size above 2^31-1 rows
+ *               OPTIMUS_ERR_UNSUPPORTED  unknown dtype or activation
+ *               OPTIMUS_ERR_ALIASING     an output overlaps an input or
+ *                                        another output (members must be
+ *                                        independent, Sec. 4.1); exact
+ *                                        in-place (y == x with equal strides)
+ *                                        is allowed for LayerNorm, pointwise
+ *                                        and split-op-cat
+ *               OPTIMUS_ERR_HIP          a HIP runtime call failed
+ *               OPTIMUS_ERR_OOM          device allocation failed
+ *   Alignment   Pointers or strides that are not 16-byte aligned, or row
+ *               lengths that are not a multiple of 16 bytes, take a
+ *               per-element path. This is not an error.
+ *   Arithmetic  bf16 members: bf16 storage, fp32 accumulation and
+ *               statistics, outputs rounded to nearest-even bf16. fp32
+ *               members: fp32 throughout (no reduced-precision products).
+ */
+#ifndef OPTIMUS_H
+#define OPTIMUS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* optimus_stream_t; /* the same type as hipStream_t */
+
+typedef enum { OPTIMUS_F32 = 0, OPTIMUS_BF16 = 1 } optimus_dtype;
+
+/* Activations of Table 1: relu, sigmoid, tanh, and silu = x * sigmoid(x). */
+typedef enum {
+  OPTIMUS_ACT_NONE = 0,
+  OPTIMUS_ACT_RELU = 1,
+  OPTIMUS_ACT_SIGMOID = 2,
+  OPTIMUS_ACT_TANH = 3,
+  OPTIMUS_ACT_SILU = 4
+} optimus_act;
+
+typedef enum {
+  OPTIMUS_OK = 0,
+  OPTIMUS_ERR_INVALID_ARG = -1,
+  OPTIMUS_ERR_UNSUPPORTED = -2,
+  OPTIMUS_ERR_ALIASING = -3,
+  OPTIMUS_ERR_HIP = -4,
+  OPTIMUS_ERR_OOM = -5
+} optimus_status;
+
+/* One Linear member (torch nn.Linear convention):
+ *   y[M][N] = act( x[M][K] . w[N][K]^T + bias[N] )
+ * x, w, y: device pointers of the group's dtype; bias may be NULL (no bias). */
+typedef struct {
+  const void* x;
+  int64_t ldx;
+  const void* w;
+  int64_t ldw;
+  const void* bias;
+  void* y;
+  int64_t ldy;
+  int64_t M, N, K;
+} optimus_linear_desc;
+
+/* One LayerNorm member over the last dim of x[rows][cols]:
+ *   y = act( (x - mean) / sqrt(var + eps) * gamma + beta ),
+ * mean and biased variance per row. gamma/beta: device [cols] of the group's
+ * dtype, or NULL for 1 / 0. */
+typedef struct {
+  const void* x;
+  int64_t ldx;
+  void* y;
+  int64_t ldy;
+  const void* gamma;
+  const void* beta;
+  int64_t rows, cols;
+  float eps;
+} optimus_layernorm_desc;
+
+/* One pointwise member: y[rows][cols] = act(x[rows][cols]). */
+typedef struct {
+  const void* x;
+  int64_t ldx;
+  void* y;
+  int64_t ldy;
+  int64_t rows, cols;
+} optimus_pointwise_desc;
+
+/* split along dim 1 of in[rows][D] into n_slices pieces of widths[j]
+ * (sum == D, piece j starts at column o_j = sum_{i<j} widths[i]); per piece
+ *   out[:, o_j : o_j+w_j] = act( LayerNorm_j(in[:, o_j : o_j+w_j]) )  if apply_layernorm
+ *   out[:, o_j : o_j+w_j] = act( in[:, o_j : o_j+w_j] )               otherwise
+ * then concat along dim 1 into out[rows][D] -- performed in place in `out`,
+ * no split copy and no concat. widths: host array [n_slices]. gamma, beta:
+ * host arrays of n_slices device pointers (each [w_j], or NULL entries for
+ * 1 / 0), or NULL arrays. LayerNorm off and ACT_NONE is a plain copy.
+ * out == in (same ld) is allowed: each row is read whole before it is written. */
+typedef struct {
+  const void* in;
+  int64_t ldin;
+  void* out;
+  int64_t ldout;
+  int64_t rows, D;
+  int32_t n_slices;
+  const int64_t* widths;
+  const void* const* gamma;
+  const void* const* beta;
+  int32_t apply_layernorm;
+  float eps;
+  optimus_act act;
+} optimus_split_op_cat_desc;
+
+/* ---------------------------------------------------------------- one-shot
+ * Validate, build the launch schedule, upload it (stream-ordered) and launch
+ * ONE kernel for the whole group on `stream`. */
+
+/* Grouped Linear (Table 1 batch_linear; Sec. 3.2 group fusion): G members
+ * d[0..G-1], optional fused epilogue activation. */
+optimus_status optimus_grouped_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
+                                      optimus_act epilogue, optimus_stream_t stream);
+
+/* Grouped row-wise LayerNorm (Table 1 batch_layernorm), optional fused activation. */
+optimus_status optimus_grouped_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
+                                         optimus_act epilogue, optimus_stream_t stream);
+
+/* Grouped pointwise activation (Table 1 batch_tanh / sigmoid / relu, and x*sigmoid(x)). */
+optimus_status optimus_grouped_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt,
+                                         optimus_act op, optimus_stream_t stream);
+
+/* Fused split -> per-piece LayerNorm/activation -> concat (Sec. 3.2 chained
+ * example; split_cat patterns of Table 1), one launch. */
+optimus_status optimus_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
+                                    optimus_stream_t stream);
+
+/* ---------------------------------------------------------------- plans
+ * A plan validates once and keeps the group's descriptor table and launch
+ * schedule resident in device memory (allocated with hipMalloc on the current
+ * device at plan time, freed by optimus_plan_destroy), so that executing it is
+ * a single kernel launch with no host work: the compile-once / run-many split
+ * of the paper's rewrite-then-recompile flow (Sec. 3.2). The device pointers
+ * captured in the plan must stay valid while the plan is executed. */
+typedef struct optimus_plan_s* optimus_plan;
+
+optimus_status optimus_plan_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
+                                   optimus_act epilogue, optimus_plan* out);
+optimus_status optimus_plan_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
+                                      optimus_act epilogue, optimus_plan* out);
+optimus_status optimus_plan_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt,
+                                      optimus_act op, optimus_plan* out);
+optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
+                                         optimus_plan* out);
+
+/* Execution modes of a plan.
+ *   GROUPED     one launch for the whole group (the optimized program).
+ *   CHAIN       the unfused program: one launch per member and per operator
+ *               (the "fragmented" execution of Sec. 2.2 / Sec. 5.2), built
+ *               from the same kernels run with a group of one. For a
+ *               split-op-cat plan: a LayerNorm launch per piece into its own
+ *               temporary, an activation launch per piece, and one concat
+ *               launch (2 * n_slices + 1 launches).
+ *   HORIZONTAL  split-op-cat plans only: horizontal fusion without the
+ *               vertical rewrite -- one grouped LayerNorm launch over the
+ *               pieces into temporaries, one grouped activation launch, one
+ *               concat launch (3 launches).
+ * CHAIN and HORIZONTAL on a split-op-cat plan use plan-owned temporaries of
+ * rows*D elements, allocated on their first use. */
+typedef enum {
+  OPTIMUS_EXEC_GROUPED = 0,
+  OPTIMUS_EXEC_CHAIN = 1,
+  OPTIMUS_EXEC_HORIZONTAL = 2
+} optimus_exec_mode;
+
+optimus_status optimus_plan_execute(optimus_plan plan, optimus_stream_t stream);
+optimus_status optimus_plan_execute_mode(optimus_plan plan, optimus_exec_mode mode, optimus_stream_t stream);
+void optimus_plan_destroy(optimus_plan plan);
+
+/* What a plan launches, for measurement. `flops` and `bytes` are the
+ * algorithmic work of the group: GEMM flops 2*sum(M*N*K); HBM bytes counted
+ * once per tensor element read or written (inputs, weights, bias, gamma/beta,
+ * outputs), never padding, re-reads or temporaries. */
+typedef struct {
+  int32_t kind;            /* 0 linear, 1 layernorm, 2 pointwise, 3 split_op_cat */
+  int32_t group_size;      /* G, or n_slices */
+  int32_t launches;        /* kernel launches per GROUPED execute (1) */
+  int32_t chain_launches;  /* kernel launches per CHAIN execute */
+  int64_t work_items;      /* GEMM tiles / row tiles of the grouped launch */
+  int32_t grid;            /* workgroups of the grouped launch */
+  int32_t block;           /* threads per workgroup */
+  double flops;
+  double bytes;
+  const char* kernel;      /* name of the grouped kernel variant */
+} optimus_plan_info;
+
+optimus_status optimus_plan_get_info(optimus_plan plan, optimus_plan_info* out);
+
+/* ---------------------------------------------------------------- host-only
+ * Descriptor validation with no device access (no HIP call is made): the
+ * same checks the entry points above run before launching. */
+optimus_status optimus_validate_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
+optimus_status optimus_validate_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
+optimus_status optimus_validate_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
+optimus_status optimus_validate_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* optimus_last_error(void);
+
+/* Library version string. */
+const char* optimus_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OPTIMUS_H */

@@ -1,0 +1,301 @@
+"""ctypes binding of liboptimus (include/optimus.h): argument marshalling only.
+
+Every entry point here has the name of the C function it calls. Tensors are
+torch tensors on the GPU (device memory and streams come from PyTorch); every
+step of the work runs in the library's HIP kernels. If liboptimus.so is not
+built this module raises -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIBPATH = os.path.join(_PKG, "liboptimus.so")
+
+F32, BF16 = 0, 1
+ACTS = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "silu": 4}
+EXEC_MODES = {"grouped": 0, "chain": 1, "horizontal": 2}
+STATUS = {0: "OK", -1: "INVALID_ARG", -2: "UNSUPPORTED", -3: "ALIASING", -4: "HIP", -5: "OOM"}
+
+c_i64, c_i32, c_vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+
+
+class LinearDesc(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("ldx", c_i64), ("w", c_vp), ("ldw", c_i64), ("bias", c_vp), ("y", c_vp),
+                ("ldy", c_i64), ("M", c_i64), ("N", c_i64), ("K", c_i64)]
+
+
+class LayerNormDesc(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("ldx", c_i64), ("y", c_vp), ("ldy", c_i64), ("gamma", c_vp), ("beta", c_vp),
+                ("rows", c_i64), ("cols", c_i64), ("eps", ctypes.c_float)]
+
+
+class PointwiseDesc(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("ldx", c_i64), ("y", c_vp), ("ldy", c_i64), ("rows", c_i64), ("cols", c_i64)]
+
+
+class SplitOpCatDesc(ctypes.Structure):
+    _fields_ = [("in_", c_vp), ("ldin", c_i64), ("out", c_vp), ("ldout", c_i64), ("rows", c_i64), ("D", c_i64),
+                ("n_slices", c_i32), ("widths", ctypes.POINTER(c_i64)), ("gamma", ctypes.POINTER(c_vp)),
+                ("beta", ctypes.POINTER(c_vp)), ("apply_layernorm", c_i32), ("eps", ctypes.c_float),
+                ("act", ctypes.c_int)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("kind", c_i32), ("group_size", c_i32), ("launches", c_i32), ("chain_launches", c_i32),
+                ("work_items", c_i64), ("grid", c_i32), ("block", c_i32), ("flops", ctypes.c_double),
+                ("bytes", ctypes.c_double), ("kernel", ctypes.c_char_p)]
+
+
+# Every symbol include/optimus.h declares.
+EXPORTS = [
+    "optimus_grouped_linear", "optimus_grouped_layernorm", "optimus_grouped_pointwise", "optimus_split_op_cat",
+    "optimus_plan_linear", "optimus_plan_layernorm", "optimus_plan_pointwise", "optimus_plan_split_op_cat",
+    "optimus_plan_execute", "optimus_plan_execute_mode", "optimus_plan_destroy", "optimus_plan_get_info",
+    "optimus_validate_linear", "optimus_validate_layernorm", "optimus_validate_pointwise",
+    "optimus_validate_split_op_cat", "optimus_last_error", "optimus_version",
+]
+
+
+class OptimusError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded liboptimus.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIBPATH):
+            raise RuntimeError(f"{LIBPATH} is missing: build it with `python -m paper_2607_02945_amd.build`")
+        L = ctypes.CDLL(LIBPATH)
+        P = ctypes.POINTER
+        st = ctypes.c_int
+        sig = {
+            "optimus_grouped_linear": (st, [P(LinearDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
+            "optimus_grouped_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
+            "optimus_grouped_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
+            "optimus_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int, c_vp]),
+            "optimus_plan_linear": (st, [P(LinearDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
+            "optimus_plan_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
+            "optimus_plan_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
+            "optimus_plan_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int, P(c_vp)]),
+            "optimus_plan_execute": (st, [c_vp, c_vp]),
+            "optimus_plan_execute_mode": (st, [c_vp, ctypes.c_int, c_vp]),
+            "optimus_plan_destroy": (None, [c_vp]),
+            "optimus_plan_get_info": (st, [c_vp, P(PlanInfo)]),
+            "optimus_validate_linear": (st, [P(LinearDesc), c_i32, ctypes.c_int, ctypes.c_int]),
+            "optimus_validate_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int]),
+            "optimus_validate_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int]),
+            "optimus_validate_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int]),
+            "optimus_last_error": (ctypes.c_char_p, []),
+            "optimus_version": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def check(status: int) -> None:
+    if status != 0:
+        raise OptimusError(status, lib().optimus_last_error().decode())
+
+
+# ------------------------------------------------------------------ marshalling
+def dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _act(a) -> int:
+    return ACTS[a] if isinstance(a, str) else int(a)
+
+
+def _mat(t: torch.Tensor, name: str):
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name}: need a 2-D tensor with unit inner stride, got shape {tuple(t.shape)} "
+                         f"strides {t.stride()}")
+    return t.data_ptr(), max(t.stride(0), t.shape[1])
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def linear_descs(xs, ws, biases, ys) -> ctypes.Array:
+    G = len(xs)
+    arr = (LinearDesc * max(G, 1))()
+    for g in range(G):
+        x, ldx = _mat(xs[g], "x")
+        w, ldw = _mat(ws[g], "w")
+        y, ldy = _mat(ys[g], "y")
+        arr[g] = LinearDesc(x, ldx, w, ldw, _ptr(biases[g] if biases is not None else None), y, ldy,
+                            xs[g].shape[0], ws[g].shape[0], xs[g].shape[1])
+    return arr
+
+
+def layernorm_descs(xs, ys, gammas, betas, eps) -> ctypes.Array:
+    G = len(xs)
+    arr = (LayerNormDesc * max(G, 1))()
+    for g in range(G):
+        x, ldx = _mat(xs[g], "x")
+        y, ldy = _mat(ys[g], "y")
+        arr[g] = LayerNormDesc(x, ldx, y, ldy, _ptr(gammas[g] if gammas is not None else None),
+                               _ptr(betas[g] if betas is not None else None), xs[g].shape[0], xs[g].shape[1],
+                               float(eps))
+    return arr
+
+
+def pointwise_descs(xs, ys) -> ctypes.Array:
+    G = len(xs)
+    arr = (PointwiseDesc * max(G, 1))()
+    for g in range(G):
+        x, ldx = _mat(xs[g], "x")
+        y, ldy = _mat(ys[g], "y")
+        arr[g] = PointwiseDesc(x, ldx, y, ldy, xs[g].shape[0], xs[g].shape[1])
+    return arr
+
+
+class _SocArgs:
+    """Keeps the host arrays a split-op-cat descriptor points to alive."""
+
+    def __init__(self, inp, out, widths, gammas, betas, apply_layernorm, eps, act):
+        i, ldin = _mat(inp, "in")
+        o, ldout = _mat(out, "out")
+        n = len(widths)
+        self.widths = (c_i64 * n)(*[int(w) for w in widths])
+        self.gamma = None if gammas is None else (c_vp * n)(*[_ptr(g) for g in gammas])
+        self.beta = None if betas is None else (c_vp * n)(*[_ptr(b) for b in betas])
+        self.desc = SplitOpCatDesc(i, ldin, o, ldout, inp.shape[0], inp.shape[1], n, self.widths,
+                                   self.gamma, self.beta, int(bool(apply_layernorm)), float(eps), _act(act))
+
+
+# ------------------------------------------------------------------ one-shot entry points
+def optimus_grouped_linear(xs: Sequence[torch.Tensor], ws, biases, ys, act="none", stream=None) -> None:
+    """y_g = act(x_g w_g^T + b_g) for every member, one launch."""
+    d = linear_descs(xs, ws, biases, ys)
+    check(lib().optimus_grouped_linear(d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act), _stream(stream)))
+
+
+def optimus_grouped_layernorm(xs, ys, gammas=None, betas=None, eps=1e-5, act="none", stream=None) -> None:
+    d = layernorm_descs(xs, ys, gammas, betas, eps)
+    check(lib().optimus_grouped_layernorm(d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act), _stream(stream)))
+
+
+def optimus_grouped_pointwise(xs, ys, act, stream=None) -> None:
+    d = pointwise_descs(xs, ys)
+    check(lib().optimus_grouped_pointwise(d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act), _stream(stream)))
+
+
+def optimus_split_op_cat(inp, out, widths, gammas=None, betas=None, apply_layernorm=True, eps=1e-5, act="none",
+                         stream=None) -> None:
+    a = _SocArgs(inp, out, widths, gammas, betas, apply_layernorm, eps, act)
+    check(lib().optimus_split_op_cat(ctypes.byref(a.desc), dtype_code(inp), _stream(stream)))
+
+
+# ------------------------------------------------------------------ plans
+class Plan:
+    """A validated group with its device table resident; execute() is one launch."""
+
+    def __init__(self, handle: int, keep):
+        self._h = ctypes.c_void_p(handle)
+        self._keep = keep  # tensors the plan points to stay alive with it
+
+    def execute(self, mode: str = "grouped", stream=None) -> None:
+        check(lib().optimus_plan_execute_mode(self._h, EXEC_MODES[mode], _stream(stream)))
+
+    def info(self) -> dict:
+        pi = PlanInfo()
+        check(lib().optimus_plan_get_info(self._h, ctypes.byref(pi)))
+        return {"kind": pi.kind, "group_size": pi.group_size, "launches": pi.launches,
+                "chain_launches": pi.chain_launches, "work_items": pi.work_items, "grid": pi.grid,
+                "block": pi.block, "flops": pi.flops, "bytes": pi.bytes,
+                "kernel": pi.kernel.decode() if pi.kernel else ""}
+
+    def close(self) -> None:
+        if self._h:
+            lib().optimus_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _plan(fn, *args, keep=None) -> Plan:
+    h = ctypes.c_void_p()
+    check(fn(*args, ctypes.byref(h)))
+    return Plan(h.value, keep)
+
+
+def optimus_plan_linear(xs, ws, biases, ys, act="none") -> Plan:
+    d = linear_descs(xs, ws, biases, ys)
+    return _plan(lib().optimus_plan_linear, d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
+                 keep=(list(xs), list(ws), biases, list(ys)))
+
+
+def optimus_plan_layernorm(xs, ys, gammas=None, betas=None, eps=1e-5, act="none") -> Plan:
+    d = layernorm_descs(xs, ys, gammas, betas, eps)
+    return _plan(lib().optimus_plan_layernorm, d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
+                 keep=(list(xs), list(ys), gammas, betas))
+
+
+def optimus_plan_pointwise(xs, ys, act) -> Plan:
+    d = pointwise_descs(xs, ys)
+    return _plan(lib().optimus_plan_pointwise, d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
+                 keep=(list(xs), list(ys)))
+
+
+def optimus_plan_split_op_cat(inp, out, widths, gammas=None, betas=None, apply_layernorm=True, eps=1e-5,
+                              act="none") -> Plan:
+    a = _SocArgs(inp, out, widths, gammas, betas, apply_layernorm, eps, act)
+    return _plan(lib().optimus_plan_split_op_cat, ctypes.byref(a.desc), dtype_code(inp),
+                 keep=(inp, out, gammas, betas))
+
+
+# ------------------------------------------------------------------ host-only validation
+def optimus_validate_linear(descs: ctypes.Array, G: int, dtype: int, act="none") -> int:
+    return lib().optimus_validate_linear(descs, G, dtype, _act(act))
+
+
+def optimus_validate_layernorm(descs: ctypes.Array, G: int, dtype: int, act="none") -> int:
+    return lib().optimus_validate_layernorm(descs, G, dtype, _act(act))
+
+
+def optimus_validate_pointwise(descs: ctypes.Array, G: int, dtype: int, act="none") -> int:
+    return lib().optimus_validate_pointwise(descs, G, dtype, _act(act))
+
+
+def optimus_validate_split_op_cat(desc: SplitOpCatDesc, dtype: int) -> int:
+    return lib().optimus_validate_split_op_cat(ctypes.byref(desc), dtype)
+
+
+def optimus_last_error() -> str:
+    return lib().optimus_last_error().decode()
+
+
+def optimus_version() -> str:
+    return lib().optimus_version().decode()

@@ -1,0 +1,912 @@
+// liboptimus C ABI: descriptor validation, the host planner (device descriptor
+// tables and tile schedules), plans, and the one-shot entry points.
+//
+// A group is a set of independent operator instances of one type, dtype and
+// activation (paper Sec. 3.2 group fusion; Sec. 4.1: instances are independent
+// when no data dependency exists between them; the grouping key of Alg. 1
+// encodes such metadata). The planner turns the caller's per-member
+// descriptors into one device table plus a list of work items, so that the
+// whole group runs as ONE kernel launch; the same tables also drive the
+// unfused per-member launch chain used as the baseline.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <cstddef>
+#include <string>
+#include <vector>
+
+#include "optimus.h"
+#include "optimus_internal.h"
+
+using namespace optimus;
+
+// ===================================================================== errors
+static thread_local std::string g_last_error;
+
+static optimus_status fail(optimus_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+static optimus_status hip_fail(hipError_t e, const char* what) {
+  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+    return fail(OPTIMUS_ERR_OOM, "%s: %s", what, hipGetErrorString(e));
+  return fail(OPTIMUS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(call, what)                 \
+  do {                                      \
+    hipError_t e_ = (call);                 \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+extern "C" const char* optimus_last_error(void) { return g_last_error.c_str(); }
+extern "C" const char* optimus_version(void) { return "liboptimus 0.1 (gfx950)"; }
+
+namespace optimus {
+int device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+}  // namespace optimus
+
+// ===================================================================== validation
+static size_t dtype_size(optimus_dtype dt) { return dt == OPTIMUS_F32 ? 4 : 2; }
+static bool dtype_ok(optimus_dtype dt) { return dt == OPTIMUS_F32 || dt == OPTIMUS_BF16; }
+static bool act_ok(optimus_act a) { return (int)a >= OPTIMUS_ACT_NONE && (int)a <= OPTIMUS_ACT_SILU; }
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+static const int64_t kMaxDim = 0x7fffffff;
+
+// A 2-D memory region: `rows` runs of `row_bytes` bytes, `ld_bytes` apart.
+struct Region {
+  uintptr_t base;
+  int64_t ld_bytes, rows, row_bytes;
+  int member;
+  bool output;
+  uintptr_t lo() const { return base; }
+  uintptr_t hi() const { return base + (uintptr_t)((rows - 1) * ld_bytes + row_bytes); }
+  bool same(const Region& o) const {
+    return base == o.base && ld_bytes == o.ld_bytes && rows == o.rows && row_bytes == o.row_bytes;
+  }
+};
+
+// Exact test for two regions with a common row stride whose runs fit inside
+// one stride (slices of one buffer); bounding-range test otherwise.
+static bool regions_overlap(const Region& a, const Region& b) {
+  if (a.hi() <= b.lo() || b.hi() <= a.lo()) return false;
+  if (a.ld_bytes != b.ld_bytes || a.row_bytes > a.ld_bytes || b.row_bytes > b.ld_bytes || a.ld_bytes <= 0) return true;
+  const int64_t l = a.ld_bytes;
+  const int64_t delta = (int64_t)(b.base - a.base);  // may be negative (two's complement)
+  // runs a_i = [i l, i l + ra) and b_j = [delta + j l, delta + j l + rb) meet iff for k = j - i:
+  // -rb < delta + k l < ra; k ranges over [-(a.rows-1), b.rows-1]
+  const int64_t ra = a.row_bytes, rb = b.row_bytes;
+  auto floor_div = [](int64_t p, int64_t q) { return p >= 0 ? p / q : -((-p + q - 1) / q); };
+  int64_t k_lo = floor_div(-rb - delta, l) + 1;  // smallest k with k l > -rb - delta
+  int64_t k_hi = floor_div(ra - delta - 1, l);   // largest k with k l < ra - delta
+  k_lo = std::max(k_lo, -(a.rows - 1));
+  k_hi = std::min(k_hi, b.rows - 1);
+  return k_lo <= k_hi;
+}
+
+// Members must be independent: no output may overlap any input or any other
+// output. Exact in-place (an output identical to the same member's input) is
+// permitted when `allow_inplace`.
+static optimus_status check_aliasing(std::vector<Region>& regs, bool allow_inplace, const char* what) {
+  std::sort(regs.begin(), regs.end(), [](const Region& a, const Region& b) { return a.lo() < b.lo(); });
+  for (size_t i = 0; i < regs.size(); ++i) {
+    for (size_t j = i + 1; j < regs.size() && regs[j].lo() < regs[i].hi(); ++j) {
+      const Region& a = regs[i];
+      const Region& b = regs[j];
+      if (!a.output && !b.output) continue;
+      if (allow_inplace && a.member == b.member && a.output != b.output && a.same(b)) continue;
+      if (regions_overlap(a, b))
+        return fail(OPTIMUS_ERR_ALIASING, "%s: member %d %s overlaps member %d %s (members must be independent)", what,
+                    a.member, a.output ? "output" : "input", b.member, b.output ? "output" : "input");
+    }
+  }
+  return OPTIMUS_OK;
+}
+
+static Region region(const void* p, int64_t ld, int64_t rows, int64_t cols, size_t s, int member, bool out) {
+  return Region{(uintptr_t)p, ld * (int64_t)s, rows, cols * (int64_t)s, member, out};
+}
+
+extern "C" optimus_status optimus_validate_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
+                                                  optimus_act act) {
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: G = %d < 0", G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_linear: unknown dtype %d", (int)dt);
+  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_linear: unknown activation %d", (int)act);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: descriptor array is NULL");
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 4);
+  for (int g = 0; g < G; ++g) {
+    const optimus_linear_desc& m = d[g];
+    if (!m.x || !m.w || !m.y) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: member %d has a NULL x/w/y", g);
+    if (m.M < 1 || m.N < 1 || m.K < 1 || m.M > kMaxDim || m.N > kMaxDim || m.K > kMaxDim)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: member %d has M=%lld N=%lld K=%lld (need 1..2^31-1)", g,
+                  (long long)m.M, (long long)m.N, (long long)m.K);
+    if (m.ldx < m.K || m.ldw < m.K || m.ldy < m.N)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: member %d has a row stride below its row length", g);
+    regs.push_back(region(m.x, m.ldx, m.M, m.K, s, g, false));
+    regs.push_back(region(m.w, m.ldw, m.N, m.K, s, g, false));
+    if (m.bias) regs.push_back(region(m.bias, m.N, 1, m.N, s, g, false));
+    regs.push_back(region(m.y, m.ldy, m.M, m.N, s, g, true));
+  }
+  return check_aliasing(regs, false, "grouped_linear");
+}
+
+extern "C" optimus_status optimus_validate_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
+                                                     optimus_act act) {
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_layernorm: G = %d < 0", G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_layernorm: unknown dtype %d", (int)dt);
+  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_layernorm: unknown activation %d", (int)act);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_layernorm: descriptor array is NULL");
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 4);
+  for (int g = 0; g < G; ++g) {
+    const optimus_layernorm_desc& m = d[g];
+    if (!m.x || !m.y) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_layernorm: member %d has a NULL x/y", g);
+    if (m.rows < 1 || m.cols < 1 || m.rows > kMaxDim || m.cols > kMaxDim)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_layernorm: member %d has rows=%lld cols=%lld", g,
+                  (long long)m.rows, (long long)m.cols);
+    if (m.ldx < m.cols || m.ldy < m.cols)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_layernorm: member %d has a row stride below cols", g);
+    if (!(m.eps >= 0.f) || !std::isfinite(m.eps))
+      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_layernorm: member %d has eps=%g", g, (double)m.eps);
+    regs.push_back(region(m.x, m.ldx, m.rows, m.cols, s, g, false));
+    if (m.gamma) regs.push_back(region(m.gamma, m.cols, 1, m.cols, s, g, false));
+    if (m.beta) regs.push_back(region(m.beta, m.cols, 1, m.cols, s, g, false));
+    regs.push_back(region(m.y, m.ldy, m.rows, m.cols, s, g, true));
+  }
+  return check_aliasing(regs, true, "grouped_layernorm");
+}
+
+extern "C" optimus_status optimus_validate_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt,
+                                                     optimus_act act) {
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_pointwise: G = %d < 0", G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_pointwise: unknown dtype %d", (int)dt);
+  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_pointwise: unknown activation %d", (int)act);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_pointwise: descriptor array is NULL");
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 2);
+  for (int g = 0; g < G; ++g) {
+    const optimus_pointwise_desc& m = d[g];
+    if (!m.x || !m.y) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_pointwise: member %d has a NULL x/y", g);
+    if (m.rows < 1 || m.cols < 1 || m.rows > kMaxDim || m.cols > kMaxDim)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_pointwise: member %d has rows=%lld cols=%lld", g,
+                  (long long)m.rows, (long long)m.cols);
+    if (m.ldx < m.cols || m.ldy < m.cols)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_pointwise: member %d has a row stride below cols", g);
+    regs.push_back(region(m.x, m.ldx, m.rows, m.cols, s, g, false));
+    regs.push_back(region(m.y, m.ldy, m.rows, m.cols, s, g, true));
+  }
+  return check_aliasing(regs, true, "grouped_pointwise");
+}
+
+extern "C" optimus_status optimus_validate_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt) {
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: descriptor is NULL");
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "split_op_cat: unknown dtype %d", (int)dt);
+  if (!act_ok(d->act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "split_op_cat: unknown activation %d", (int)d->act);
+  if (!d->in || !d->out) return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: NULL in/out");
+  if (d->rows < 1 || d->D < 1 || d->rows > kMaxDim || d->D > kMaxDim)
+    return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: rows=%lld D=%lld", (long long)d->rows, (long long)d->D);
+  if (d->ldin < d->D || d->ldout < d->D) return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: row stride below D");
+  if (d->n_slices < 1 || !d->widths) return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: need n_slices >= 1 and widths");
+  int64_t total = 0;
+  for (int j = 0; j < d->n_slices; ++j) {
+    if (d->widths[j] < 1) return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: width[%d] = %lld < 1", j, (long long)d->widths[j]);
+    total += d->widths[j];
+  }
+  if (total != d->D)
+    return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: widths sum to %lld, not D = %lld", (long long)total, (long long)d->D);
+  if (d->apply_layernorm && (!(d->eps >= 0.f) || !std::isfinite(d->eps)))
+    return fail(OPTIMUS_ERR_INVALID_ARG, "split_op_cat: eps=%g", (double)d->eps);
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.push_back(region(d->in, d->ldin, d->rows, d->D, s, 0, false));
+  regs.push_back(region(d->out, d->ldout, d->rows, d->D, s, 0, true));
+  if (d->apply_layernorm) {
+    for (int j = 0; j < d->n_slices; ++j) {
+      if (d->gamma && d->gamma[j]) regs.push_back(region(d->gamma[j], d->widths[j], 1, d->widths[j], s, 0, false));
+      if (d->beta && d->beta[j]) regs.push_back(region(d->beta[j], d->widths[j], 1, d->widths[j], s, 0, false));
+    }
+  }
+  return check_aliasing(regs, true, "split_op_cat");
+}
+
+// ===================================================================== host plans
+// A HostPlan is everything a launch needs, built on the host: a byte blob that
+// becomes the device table, offsets into it, device-to-device copies to run
+// after the upload (packing per-piece gamma/beta), and launch parameters.
+enum Kind { KIND_LINEAR = 0, KIND_LN = 1, KIND_PW = 2, KIND_SOC = 3 };
+
+struct Blob {
+  std::vector<char> bytes;
+  size_t add(const void* p, size_t n) {
+    size_t off = (bytes.size() + 255) & ~(size_t)255;
+    bytes.resize(off + n);
+    if (p && n) memcpy(bytes.data() + off, p, n);
+    return off;
+  }
+};
+
+struct D2DCopy {
+  size_t dst_off;
+  const void* src;
+  size_t bytes;
+};
+
+// One kernel launch over a row-wise table (grouped or one member of a chain).
+struct RowLaunch {
+  size_t descs_off, tiles_off;
+  int32_t first_tile, num_tiles, grid;
+};
+
+struct HostPlan {
+  Kind kind;
+  optimus_dtype dt;
+  optimus_act act;
+  int32_t G = 0;
+  Blob blob;
+  std::vector<D2DCopy> copies;
+  // GEMM
+  GemmConfig gcfg{};
+  size_t g_descs_off = 0, g_tiles_off = 0;
+  int32_t g_num_tiles = 0, g_grid = 0;
+  std::vector<RowLaunch> g_chain;  // per member: tiles range of the same table
+  // row-wise (LN / PW, or the split-op-cat fallbacks)
+  int row_kernel = KIND_LN;  // which row kernel the grouped launch uses
+  optimus_act row_act = OPTIMUS_ACT_NONE;
+  RowLaunch rows{};
+  std::vector<RowLaunch> rows_chain;
+  // fused split-op-cat
+  bool soc_fused = false;
+  size_t soc_off = 0;
+  int32_t soc_rows = 0, soc_nchunks = 0, soc_pieces = 0, soc_tasks = 0, soc_grid = 0;
+  // split-op-cat unfused programs (CHAIN / HORIZONTAL) over plan-owned temporaries
+  bool soc_has_unfused = false;
+  bool soc_apply_ln = false;
+  int64_t soc_temp_elems = 0;
+  size_t soc_ln_descs = 0, soc_act_descs = 0, soc_cat_descs = 0, soc_tiles = 0;
+  std::vector<int32_t> soc_piece_first, soc_piece_count;  // per piece: tile range in soc_tiles
+  int32_t soc_piece_tiles_total = 0;
+  std::vector<size_t> soc_temp_fixups;  // blob offsets of DevRows pointers relative to the temp base
+  // measurement
+  int32_t launches = 1, chain_launches = 0, grid = 0, block = 0;
+  int64_t work_items = 0;
+  double flops = 0, bytes = 0;
+  std::string kernel;
+};
+
+static int pow2ceil(int v) {
+  int p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+// Row-wise member: lanes per row and the 16-byte path.
+static DevRows make_rows(const void* x, int64_t ldx, void* y, int64_t ldy, const void* gamma, const void* beta,
+                         int64_t rows, int64_t cols, float eps, optimus_dtype dt, bool layernorm) {
+  const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
+  DevRows r{};
+  r.x = x; r.y = y; r.gamma = gamma; r.beta = beta;
+  r.ldx = ldx; r.ldy = ldy;
+  r.rows = (int32_t)rows; r.cols = (int32_t)cols;
+  r.eps = eps;
+  r.inv_cols = (float)(1.0 / (double)cols);
+  const bool vec = cols % VEC == 0 && ldx % VEC == 0 && ldy % VEC == 0 && aligned16(x) && aligned16(y) &&
+                   (!gamma || aligned16(gamma)) && (!beta || aligned16(beta));
+  const int cpr = (int)(cols / VEC);
+  r.vec = 0;
+  r.lanes = 0;
+  if (vec) {
+    if (layernorm) {
+      const int maxc = 4;  // chunks per lane held in registers by the LayerNorm kernel
+      if (cpr <= 64 * maxc) {
+        r.vec = 1;
+        r.lanes = pow2ceil((cpr + maxc - 1) / maxc);
+      }
+    } else {
+      r.vec = 1;
+      r.lanes = std::min(64, pow2ceil(cpr));
+    }
+  }
+  return r;
+}
+
+// Row tiles of one member: about 32 KB of input per tile, a whole number of
+// the block's row slots.
+static void add_row_tiles(std::vector<RowTile>& tiles, int member, const DevRows& r, size_t s) {
+  const int rpb = r.vec ? 4 * (64 / r.lanes) : 4;
+  const int64_t row_bytes = std::max<int64_t>(1, (int64_t)r.cols * (int64_t)s);
+  int64_t per = std::max<int64_t>(1, 32768 / row_bytes);
+  per = std::max<int64_t>(rpb, (per / rpb) * rpb);
+  for (int64_t r0 = 0; r0 < r.rows; r0 += per)
+    tiles.push_back(RowTile{member, (int32_t)r0, (int32_t)std::min<int64_t>(per, r.rows - r0), 0});
+}
+
+static int32_t row_grid(int64_t tiles) {
+  const int64_t cap = (int64_t)device_cu_count() * 8;
+  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(tiles, cap));
+}
+
+// Row-wise plan over `members` (LayerNorm or pointwise), member-major tiles.
+static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool layernorm, size_t s) {
+  std::vector<RowTile> tiles;
+  hp.rows_chain.clear();
+  for (size_t g = 0; g < members.size(); ++g) {
+    const int first = (int)tiles.size();
+    add_row_tiles(tiles, (int)g, members[g], s);
+    hp.rows_chain.push_back(RowLaunch{0, 0, first, (int)tiles.size() - first, 0});
+  }
+  const size_t doff = hp.blob.add(members.data(), members.size() * sizeof(DevRows));
+  const size_t toff = hp.blob.add(tiles.data(), tiles.size() * sizeof(RowTile));
+  for (auto& c : hp.rows_chain) {
+    c.descs_off = doff;
+    c.tiles_off = toff;
+    c.grid = row_grid(c.num_tiles);
+  }
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
+  hp.row_kernel = layernorm ? KIND_LN : KIND_PW;
+  hp.work_items = (int64_t)tiles.size();
+  hp.grid = hp.rows.grid;
+  hp.block = kRowThreads;
+  hp.chain_launches = (int32_t)members.size();
+}
+
+static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
+                                   HostPlan& hp) {
+  optimus_status st = optimus_validate_linear(d, G, dt, act);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_LINEAR; hp.dt = dt; hp.act = act; hp.G = G;
+  const size_t s = dtype_size(dt);
+  const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
+  hp.gcfg = gemm_pick_config(dt, d, G);
+  std::vector<DevLinear> descs(G);
+  for (int g = 0; g < G; ++g) {
+    const optimus_linear_desc& m = d[g];
+    DevLinear& o = descs[g];
+    o.x = m.x; o.w = m.w; o.bias = m.bias; o.y = m.y;
+    o.ldx = m.ldx; o.ldw = m.ldw; o.ldy = m.ldy;
+    o.M = (int32_t)m.M; o.N = (int32_t)m.N; o.K = (int32_t)m.K;
+    const bool vin = m.K % VEC == 0 && m.ldx % VEC == 0 && m.ldw % VEC == 0 && aligned16(m.x) && aligned16(m.w);
+    const bool vout = m.ldy % VEC == 0 && aligned16(m.y);
+    o.vec = (vin ? 1 : 0) | (vout ? 2 : 0);
+    hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
+    hp.bytes += (double)s * ((double)m.M * m.K + (double)m.N * m.K + (m.bias ? (double)m.N : 0.0) + (double)m.M * m.N);
+  }
+  // heavy members first (tile cost grows with K), member-major, M-blocks then N-blocks
+  std::vector<int> order(G);
+  for (int g = 0; g < G; ++g) order[g] = g;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return d[a].K > d[b].K; });
+  std::vector<GemmTile> tiles;
+  hp.g_chain.assign(G, RowLaunch{});
+  const int bm = hp.gcfg.bm, bn = hp.gcfg.bn;
+  for (int g : order) {
+    const int first = (int)tiles.size();
+    const int64_t mbs = (d[g].M + bm - 1) / bm, nbs = (d[g].N + bn - 1) / bn;
+    for (int64_t mb = 0; mb < mbs; ++mb)
+      for (int64_t nb = 0; nb < nbs; ++nb) tiles.push_back(GemmTile{g, (int32_t)mb, (int32_t)nb, 0});
+    hp.g_chain[g].first_tile = first;
+    hp.g_chain[g].num_tiles = (int)tiles.size() - first;
+  }
+  const int64_t real_tiles = (int64_t)tiles.size();
+  while (tiles.size() % 8) tiles.push_back(GemmTile{-1, 0, 0, 0});
+  hp.g_descs_off = hp.blob.add(descs.data(), descs.size() * sizeof(DevLinear));
+  hp.g_tiles_off = hp.blob.add(tiles.data(), tiles.size() * sizeof(GemmTile));
+  hp.g_num_tiles = (int32_t)tiles.size();
+  // workgroups resident per CU for each variant (LDS / register bound)
+  static const int occ[] = {4, 2, 1, 4};
+  const int64_t cap = (int64_t)device_cu_count() * occ[hp.gcfg.variant];
+  int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
+  if (grid >= 8) grid -= grid % 8;
+  hp.g_grid = (int32_t)std::max<int64_t>(1, grid);
+  for (auto& c : hp.g_chain) {
+    c.descs_off = hp.g_descs_off;
+    c.tiles_off = hp.g_tiles_off;
+    c.grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(c.num_tiles, cap));
+  }
+  hp.work_items = real_tiles;
+  hp.grid = hp.g_grid;
+  hp.block = hp.gcfg.threads;
+  hp.chain_launches = G;
+  hp.kernel = hp.gcfg.name;
+  return OPTIMUS_OK;
+}
+
+static optimus_status build_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
+                                      HostPlan& hp) {
+  optimus_status st = optimus_validate_layernorm(d, G, dt, act);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_LN; hp.dt = dt; hp.act = act; hp.G = G; hp.row_act = act;
+  const size_t s = dtype_size(dt);
+  std::vector<DevRows> members;
+  for (int g = 0; g < G; ++g) {
+    const optimus_layernorm_desc& m = d[g];
+    members.push_back(make_rows(m.x, m.ldx, m.y, m.ldy, m.gamma, m.beta, m.rows, m.cols, m.eps, dt, true));
+    hp.bytes += (double)s * (2.0 * m.rows * m.cols + (m.gamma ? m.cols : 0) + (m.beta ? m.cols : 0));
+  }
+  build_rows(hp, members, true, s);
+  hp.kernel = dt == OPTIMUS_F32 ? "grouped_layernorm_f32" : "grouped_layernorm_bf16";
+  return OPTIMUS_OK;
+}
+
+static optimus_status build_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
+                                      HostPlan& hp) {
+  optimus_status st = optimus_validate_pointwise(d, G, dt, act);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_PW; hp.dt = dt; hp.act = act; hp.G = G; hp.row_act = act;
+  const size_t s = dtype_size(dt);
+  std::vector<DevRows> members;
+  for (int g = 0; g < G; ++g) {
+    const optimus_pointwise_desc& m = d[g];
+    members.push_back(make_rows(m.x, m.ldx, m.y, m.ldy, nullptr, nullptr, m.rows, m.cols, 0.f, dt, false));
+    hp.bytes += (double)s * 2.0 * m.rows * m.cols;
+  }
+  build_rows(hp, members, false, s);
+  hp.kernel = dt == OPTIMUS_F32 ? "grouped_pointwise_f32" : "grouped_pointwise_bf16";
+  return OPTIMUS_OK;
+}
+
+static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt, HostPlan& hp) {
+  optimus_status st = optimus_validate_split_op_cat(d, dt);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_SOC; hp.dt = dt; hp.act = d->act; hp.G = d->n_slices;
+  const size_t s = dtype_size(dt);
+  const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
+  const int n = d->n_slices;
+  const int64_t rows = d->rows, D = d->D;
+  std::vector<int64_t> off(n + 1, 0);
+  for (int j = 0; j < n; ++j) off[j + 1] = off[j] + d->widths[j];
+  hp.bytes = (double)s * 2.0 * rows * D;
+  if (d->apply_layernorm)
+    for (int j = 0; j < n; ++j)
+      hp.bytes += (double)s * ((d->gamma && d->gamma[j] ? d->widths[j] : 0) + (d->beta && d->beta[j] ? d->widths[j] : 0));
+
+  // ---- the optimized program
+  bool widths_vec = true;
+  for (int j = 0; j < n; ++j) widths_vec = widths_vec && d->widths[j] % VEC == 0;
+  const bool vec = widths_vec && d->ldin % VEC == 0 && d->ldout % VEC == 0 && aligned16(d->in) && aligned16(d->out);
+  const int64_t nchunks = D / VEC;
+  if (!d->apply_layernorm) {
+    // same activation on every piece: split and concat vanish into one pointwise pass over [rows, D]
+    std::vector<DevRows> m{make_rows(d->in, d->ldin, d->out, d->ldout, nullptr, nullptr, rows, D, 0.f, dt, false)};
+    build_rows(hp, m, false, s);
+    hp.row_act = d->act;
+    hp.kernel = "split_op_cat_as_pointwise";
+  } else if (vec && nchunks <= kSocMaxChunks && n <= kSocMaxPieces && n <= kSocMaxTasks) {
+    // reduction runs: each piece's chunk range cut into runs of at most `run` chunks, <= 128 runs
+    int run = 1;
+    auto count_tasks = [&](int r) {
+      int64_t t = 0;
+      for (int j = 0; j < n; ++j) t += (d->widths[j] / VEC + r - 1) / r;
+      return t;
+    };
+    while (count_tasks(run) > kSocMaxTasks) ++run;  // ends: n <= kSocMaxTasks pieces need n tasks at most
+    std::vector<uint8_t> cp((size_t)nchunks);
+    std::vector<SocPiece> pieces(n);
+    std::vector<SocTask> tasks;
+    for (int j = 0; j < n; ++j) {
+      const int c0 = (int)(off[j] / VEC), c1 = (int)(off[j + 1] / VEC);
+      pieces[j] = SocPiece{c0, c1, (float)(1.0 / (double)d->widths[j]), 0};
+      for (int c = c0; c < c1; ++c) cp[c] = (uint8_t)j;
+      for (int c = c0; c < c1; c += run)
+        tasks.push_back(SocTask{(int16_t)c, (int16_t)std::min(c1, c + run), (int16_t)j, 0});
+    }
+    DevSoc soc{};
+    soc.in = d->in; soc.out = d->out;
+    soc.ldin = d->ldin; soc.ldout = d->ldout;
+    soc.rows = (int32_t)rows; soc.D = (int32_t)D; soc.nchunks = (int32_t)nchunks;
+    soc.n_pieces = n; soc.n_tasks = (int32_t)tasks.size();
+    soc.apply_ln = 1; soc.eps = d->eps;
+    const size_t gam_off = hp.blob.add(nullptr, (size_t)D * s);
+    const size_t bet_off = hp.blob.add(nullptr, (size_t)D * s);
+    // identity affine where a piece has none: packed arrays start as 1 / 0
+    {
+      std::vector<char> ones((size_t)D * s), zeros((size_t)D * s, 0);
+      for (int64_t i = 0; i < D; ++i) {
+        if (dt == OPTIMUS_F32) { float one = 1.f; memcpy(&ones[i * 4], &one, 4); }
+        else { uint16_t one = 0x3f80; memcpy(&ones[i * 2], &one, 2); }
+      }
+      memcpy(hp.blob.bytes.data() + gam_off, ones.data(), ones.size());
+      memcpy(hp.blob.bytes.data() + bet_off, zeros.data(), zeros.size());
+    }
+    for (int j = 0; j < n; ++j) {
+      if (d->gamma && d->gamma[j]) hp.copies.push_back(D2DCopy{gam_off + (size_t)off[j] * s, d->gamma[j], (size_t)d->widths[j] * s});
+      if (d->beta && d->beta[j]) hp.copies.push_back(D2DCopy{bet_off + (size_t)off[j] * s, d->beta[j], (size_t)d->widths[j] * s});
+    }
+    const size_t cp_off = hp.blob.add(cp.data(), cp.size());
+    const size_t pc_off = hp.blob.add(pieces.data(), pieces.size() * sizeof(SocPiece));
+    const size_t tk_off = hp.blob.add(tasks.data(), tasks.size() * sizeof(SocTask));
+    // device pointers inside DevSoc are filled in at upload (relative offsets kept here)
+    soc.gamma = (const void*)(uintptr_t)gam_off;
+    soc.beta = (const void*)(uintptr_t)bet_off;
+    soc.chunk_piece = (const uint8_t*)(uintptr_t)cp_off;
+    soc.pieces = (const SocPiece*)(uintptr_t)pc_off;
+    soc.tasks = (const SocTask*)(uintptr_t)tk_off;
+    hp.soc_off = hp.blob.add(&soc, sizeof soc);
+    hp.soc_fused = true;
+    hp.soc_rows = (int32_t)rows;
+    hp.soc_nchunks = (int32_t)nchunks;
+    hp.soc_pieces = n;
+    hp.soc_tasks = (int32_t)tasks.size();
+    hp.soc_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((rows + 3) / 4, (int64_t)device_cu_count() * 4));
+    hp.work_items = rows;
+    hp.grid = hp.soc_grid;
+    hp.block = kSocThreads;
+    hp.kernel = dt == OPTIMUS_F32 ? "split_op_cat_fused_f32" : "split_op_cat_fused_bf16";
+  } else {
+    // any other shape: the pieces become the members of one grouped LayerNorm
+    // launch that reads and writes them in place (still no split copy, no concat)
+    std::vector<DevRows> m;
+    for (int j = 0; j < n; ++j)
+      m.push_back(make_rows((const char*)d->in + off[j] * s, d->ldin, (char*)d->out + off[j] * s, d->ldout,
+                            d->gamma ? d->gamma[j] : nullptr, d->beta ? d->beta[j] : nullptr, rows, d->widths[j],
+                            d->eps, dt, true));
+    build_rows(hp, m, true, s);
+    hp.row_act = d->act;
+    hp.kernel = "split_op_cat_as_grouped_layernorm";
+  }
+  hp.launches = 1;
+
+  // ---- the unfused programs, for measurement (CHAIN and HORIZONTAL modes):
+  // piece j lives in the temporaries at element offset rows * off[j] as a
+  // contiguous [rows, w_j] array. Pointers into the temporaries are stored as
+  // offsets and rebased when the temporaries exist.
+  hp.soc_has_unfused = true;
+  hp.soc_apply_ln = d->apply_layernorm != 0;
+  hp.soc_temp_elems = rows * D;
+  std::vector<DevRows> ln(n), act(n), cat(n);
+  for (int j = 0; j < n; ++j) {
+    const int64_t w = d->widths[j];
+    const uintptr_t t1 = (uintptr_t)(rows * off[j]) * s;                 // offset in temp 1
+    const uintptr_t t2 = (uintptr_t)(rows * D + rows * off[j]) * s;      // offset in temp 2
+    if (d->apply_layernorm)
+      ln[j] = make_rows((const char*)d->in + off[j] * s, d->ldin, (void*)t1, w, d->gamma ? d->gamma[j] : nullptr,
+                        d->beta ? d->beta[j] : nullptr, rows, w, d->eps, dt, true);
+    else
+      ln[j] = make_rows((const char*)d->in + off[j] * s, d->ldin, (void*)t1, w, nullptr, nullptr, rows, w, 0.f, dt,
+                        false);
+    act[j] = make_rows((const void*)t1, w, (void*)t2, w, nullptr, nullptr, rows, w, 0.f, dt, false);
+    cat[j] = make_rows((const void*)t2, w, (char*)d->out + off[j] * s, d->ldout, nullptr, nullptr, rows, w, 0.f, dt, false);
+  }
+  // make_rows sees temporary offsets in place of pointers; the temporaries are
+  // 256-byte aligned, so an offset's alignment is the pointer's alignment.
+  std::vector<RowTile> tl;
+  hp.soc_piece_first.assign(n, 0);
+  hp.soc_piece_count.assign(n, 0);
+  for (int j = 0; j < n; ++j) {
+    hp.soc_piece_first[j] = (int32_t)tl.size();
+    add_row_tiles(tl, j, ln[j], s);  // same row count for every piece: one tile list serves all three
+    hp.soc_piece_count[j] = (int32_t)tl.size() - hp.soc_piece_first[j];
+  }
+  hp.soc_ln_descs = hp.blob.add(ln.data(), n * sizeof(DevRows));
+  hp.soc_act_descs = hp.blob.add(act.data(), n * sizeof(DevRows));
+  hp.soc_cat_descs = hp.blob.add(cat.data(), n * sizeof(DevRows));
+  hp.soc_tiles = hp.blob.add(tl.data(), tl.size() * sizeof(RowTile));
+  hp.soc_piece_tiles_total = (int32_t)tl.size();
+  for (int j = 0; j < n; ++j) {
+    hp.soc_temp_fixups.push_back(hp.soc_ln_descs + j * sizeof(DevRows) + offsetof(DevRows, y));
+    hp.soc_temp_fixups.push_back(hp.soc_act_descs + j * sizeof(DevRows) + offsetof(DevRows, x));
+    hp.soc_temp_fixups.push_back(hp.soc_act_descs + j * sizeof(DevRows) + offsetof(DevRows, y));
+    hp.soc_temp_fixups.push_back(hp.soc_cat_descs + j * sizeof(DevRows) + offsetof(DevRows, x));
+  }
+  hp.chain_launches = 2 * n + 1;
+  return OPTIMUS_OK;
+}
+
+// ===================================================================== device side of a plan
+struct optimus_plan_s {
+  HostPlan hp;
+  int device = 0;
+  char* table = nullptr;       // device copy of hp.blob
+  char* temps = nullptr;       // split-op-cat unfused temporaries (lazy)
+  bool temps_ready = false;
+};
+
+// Rebase the pointer fields that hold blob offsets (split-op-cat tables).
+static void rebase_soc(HostPlan& hp, char* table) {
+  if (!hp.soc_fused) return;
+  DevSoc* s = (DevSoc*)(hp.blob.bytes.data() + hp.soc_off);
+  s->gamma = table + (uintptr_t)s->gamma;
+  s->beta = table + (uintptr_t)s->beta;
+  s->chunk_piece = (const uint8_t*)(table + (uintptr_t)s->chunk_piece);
+  s->pieces = (const SocPiece*)(table + (uintptr_t)s->pieces);
+  s->tasks = (const SocTask*)(table + (uintptr_t)s->tasks);
+}
+
+template <typename P>
+static const P* at(char* table, size_t off) {
+  return (const P*)(table + off);
+}
+
+static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t stream) {
+  switch (hp.kind) {
+    case KIND_LINEAR:
+      return gemm_launch(hp.gcfg, hp.dt, hp.act, at<DevLinear>(table, hp.g_descs_off), at<GemmTile>(table, hp.g_tiles_off),
+                         hp.g_num_tiles, hp.g_grid, stream);
+    case KIND_LN:
+    case KIND_PW:
+    case KIND_SOC:
+      if (hp.kind == KIND_SOC && hp.soc_fused)
+        return soc_launch(hp.dt, hp.act, at<DevSoc>(table, hp.soc_off), hp.soc_rows, hp.soc_nchunks, hp.soc_pieces,
+                          hp.soc_tasks, hp.soc_grid, stream);
+      if (hp.row_kernel == KIND_LN)
+        return layernorm_launch(hp.dt, hp.row_act, at<DevRows>(table, hp.rows.descs_off),
+                                at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles, hp.rows.grid, stream);
+      return pointwise_launch(hp.dt, hp.row_act, at<DevRows>(table, hp.rows.descs_off),
+                              at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles, hp.rows.grid, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+static optimus_status upload_copies(const HostPlan& hp, char* table, hipStream_t stream, bool async) {
+  for (const D2DCopy& c : hp.copies) {
+    hipError_t e = async ? hipMemcpyAsync(table + c.dst_off, c.src, c.bytes, hipMemcpyDeviceToDevice, stream)
+                         : hipMemcpy(table + c.dst_off, c.src, c.bytes, hipMemcpyDeviceToDevice);
+    if (e != hipSuccess) return hip_fail(e, "packing per-piece gamma/beta");
+  }
+  return OPTIMUS_OK;
+}
+
+static optimus_status make_plan(HostPlan&& hp, optimus_plan* out) {
+  if (!out) return fail(OPTIMUS_ERR_INVALID_ARG, "plan: output pointer is NULL");
+  *out = nullptr;
+  optimus_plan p = new (std::nothrow) optimus_plan_s();
+  if (!p) return fail(OPTIMUS_ERR_OOM, "plan: host allocation failed");
+  p->hp = std::move(hp);
+  if (hipGetDevice(&p->device) != hipSuccess) p->device = 0;
+  const size_t n = std::max<size_t>(p->hp.blob.bytes.size(), 256);
+  hipError_t e = hipMalloc((void**)&p->table, n);
+  if (e != hipSuccess) {
+    delete p;
+    return hip_fail(e, "plan: device table allocation");
+  }
+  rebase_soc(p->hp, p->table);
+  e = hipMemcpy(p->table, p->hp.blob.bytes.data(), p->hp.blob.bytes.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess) {
+    optimus_status st = upload_copies(p->hp, p->table, nullptr, false);
+    if (st != OPTIMUS_OK) {
+      (void)hipFree(p->table);
+      delete p;
+      return st;
+    }
+  }
+  if (e != hipSuccess) {
+    (void)hipFree(p->table);
+    delete p;
+    return hip_fail(e, "plan: device table upload");
+  }
+  *out = p;
+  return OPTIMUS_OK;
+}
+
+extern "C" optimus_status optimus_plan_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
+                                              optimus_act epilogue, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_linear(d, G, dt, epilogue, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
+                                                 optimus_act epilogue, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_layernorm(d, G, dt, epilogue, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt,
+                                                 optimus_act op, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_pointwise(d, G, dt, op, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
+                                                    optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_split_op_cat(d, dt, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+
+extern "C" void optimus_plan_destroy(optimus_plan p) {
+  if (!p) return;
+  int cur = 0;
+  const bool switched = hipGetDevice(&cur) == hipSuccess && cur != p->device && hipSetDevice(p->device) == hipSuccess;
+  (void)hipFree(p->table);
+  if (p->temps) (void)hipFree(p->temps);
+  if (switched) (void)hipSetDevice(cur);
+  delete p;
+}
+
+// Temporaries of the unfused split-op-cat programs, with the descriptor
+// pointers that refer to them rebased and re-uploaded.
+static optimus_status soc_prepare_temps(optimus_plan p) {
+  if (p->temps_ready) return OPTIMUS_OK;
+  HostPlan& hp = p->hp;
+  const size_t bytes = (size_t)hp.soc_temp_elems * 2 * dtype_size(hp.dt);
+  HIP_TRY(hipMalloc((void**)&p->temps, std::max<size_t>(bytes, 256)), "split_op_cat: temporaries");
+  for (size_t off : hp.soc_temp_fixups) {
+    uintptr_t v;
+    memcpy(&v, hp.blob.bytes.data() + off, sizeof v);
+    v += (uintptr_t)p->temps;
+    HIP_TRY(hipMemcpy(p->table + off, &v, sizeof v, hipMemcpyHostToDevice), "split_op_cat: temporaries table");
+  }
+  p->temps_ready = true;
+  return OPTIMUS_OK;
+}
+
+extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec_mode mode, optimus_stream_t stream) {
+  if (!p) return fail(OPTIMUS_ERR_INVALID_ARG, "execute: plan is NULL");
+  HostPlan& hp = p->hp;
+  hipStream_t st = (hipStream_t)stream;
+  if (hp.G == 0) return OPTIMUS_OK;
+  if (mode == OPTIMUS_EXEC_GROUPED) {
+    hipError_t e = launch_grouped(hp, p->table, st);
+    return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "execute: grouped launch");
+  }
+  if (mode == OPTIMUS_EXEC_CHAIN && hp.kind != KIND_SOC) {
+    for (int g = 0; g < hp.G; ++g) {
+      hipError_t e;
+      if (hp.kind == KIND_LINEAR) {
+        const RowLaunch& c = hp.g_chain[g];
+        e = gemm_launch(hp.gcfg, hp.dt, hp.act, at<DevLinear>(p->table, hp.g_descs_off),
+                        at<GemmTile>(p->table, hp.g_tiles_off) + c.first_tile, c.num_tiles, c.grid, st);
+      } else {
+        const RowLaunch& c = hp.rows_chain[g];
+        const DevRows* ds = at<DevRows>(p->table, c.descs_off);
+        const RowTile* ts = at<RowTile>(p->table, c.tiles_off) + c.first_tile;
+        e = hp.row_kernel == KIND_LN ? layernorm_launch(hp.dt, hp.row_act, ds, ts, c.num_tiles, c.grid, st)
+                                     : pointwise_launch(hp.dt, hp.row_act, ds, ts, c.num_tiles, c.grid, st);
+      }
+      if (e != hipSuccess) return hip_fail(e, "execute: chain launch");
+    }
+    return OPTIMUS_OK;
+  }
+  if (hp.kind != KIND_SOC || (mode != OPTIMUS_EXEC_CHAIN && mode != OPTIMUS_EXEC_HORIZONTAL))
+    return fail(OPTIMUS_ERR_INVALID_ARG, "execute: mode %d does not apply to this plan", (int)mode);
+  optimus_status s = soc_prepare_temps(p);
+  if (s != OPTIMUS_OK) return s;
+  const DevRows* ln = at<DevRows>(p->table, hp.soc_ln_descs);
+  const DevRows* act = at<DevRows>(p->table, hp.soc_act_descs);
+  const DevRows* cat = at<DevRows>(p->table, hp.soc_cat_descs);
+  const RowTile* tl = at<RowTile>(p->table, hp.soc_tiles);
+  const bool ln_on = hp.soc_apply_ln;
+  const int n = hp.G;
+  hipError_t e = hipSuccess;
+  if (mode == OPTIMUS_EXEC_HORIZONTAL) {
+    const int32_t T = hp.soc_piece_tiles_total, grid = row_grid(T);
+    e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tl, T, grid, st)
+              : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tl, T, grid, st);
+    if (e == hipSuccess) e = pointwise_launch(hp.dt, hp.act, act, tl, T, grid, st);
+    if (e == hipSuccess) e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, grid, st);
+  } else {
+    for (int j = 0; j < n && e == hipSuccess; ++j) {
+      const RowTile* tj = tl + hp.soc_piece_first[j];
+      const int32_t cnt = hp.soc_piece_count[j];
+      e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt), st)
+                : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt), st);
+    }
+    for (int j = 0; j < n && e == hipSuccess; ++j) {
+      const RowTile* tj = tl + hp.soc_piece_first[j];
+      const int32_t cnt = hp.soc_piece_count[j];
+      e = pointwise_launch(hp.dt, hp.act, act, tj, cnt, row_grid(cnt), st);
+    }
+    if (e == hipSuccess) {
+      const int32_t T = hp.soc_piece_tiles_total;
+      e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, row_grid(T), st);
+    }
+  }
+  return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "execute: split-op-cat unfused launch");
+}
+
+extern "C" optimus_status optimus_plan_execute(optimus_plan p, optimus_stream_t stream) {
+  return optimus_plan_execute_mode(p, OPTIMUS_EXEC_GROUPED, stream);
+}
+
+extern "C" optimus_status optimus_plan_get_info(optimus_plan p, optimus_plan_info* out) {
+  if (!p || !out) return fail(OPTIMUS_ERR_INVALID_ARG, "plan_get_info: NULL argument");
+  const HostPlan& hp = p->hp;
+  out->kind = (int32_t)hp.kind;
+  out->group_size = hp.G;
+  out->launches = hp.G ? hp.launches : 0;
+  out->chain_launches = hp.chain_launches;
+  out->work_items = hp.work_items;
+  out->grid = hp.grid;
+  out->block = hp.block;
+  out->flops = hp.flops;
+  out->bytes = hp.bytes;
+  out->kernel = hp.kernel.c_str();
+  return OPTIMUS_OK;
+}
+
+// ===================================================================== one-shot entry points
+// The table goes up through a pinned staging buffer (per thread, grow-only)
+// into stream-ordered device memory, the group is launched, and the device
+// memory is released in stream order; the call does not wait for the GPU.
+namespace {
+struct Staging {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+thread_local Staging* tl_stage = nullptr;  // intentionally never freed (process lifetime)
+}  // namespace
+
+static optimus_status run_oneshot(HostPlan& hp, hipStream_t stream) {
+  if (hp.G == 0) return OPTIMUS_OK;
+  if (!tl_stage) tl_stage = new Staging();
+  Staging& sg = *tl_stage;
+  const size_t n = std::max<size_t>(hp.blob.bytes.size(), 256);
+  char* table = nullptr;
+  HIP_TRY(hipMallocAsync((void**)&table, n, stream), "one-shot: device table");
+  if (!sg.ev) HIP_TRY(hipEventCreateWithFlags(&sg.ev, hipEventDisableTiming), "one-shot: event");
+  if (sg.pending) HIP_TRY(hipEventSynchronize(sg.ev), "one-shot: staging reuse");
+  if (sg.cap < n) {
+    if (sg.host) (void)hipHostFree(sg.host);
+    sg.host = nullptr;
+    sg.cap = 0;
+    HIP_TRY(hipHostMalloc(&sg.host, n, hipHostMallocDefault), "one-shot: pinned staging");
+    sg.cap = n;
+  }
+  rebase_soc(hp, table);
+  memcpy(sg.host, hp.blob.bytes.data(), hp.blob.bytes.size());
+  HIP_TRY(hipMemcpyAsync(table, sg.host, hp.blob.bytes.size(), hipMemcpyHostToDevice, stream), "one-shot: upload");
+  HIP_TRY(hipEventRecord(sg.ev, stream), "one-shot: event record");
+  sg.pending = true;
+  optimus_status st = upload_copies(hp, table, stream, true);
+  if (st != OPTIMUS_OK) return st;
+  hipError_t e = launch_grouped(hp, table, stream);
+  (void)hipFreeAsync(table, stream);
+  return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "one-shot: launch");
+}
+
+extern "C" optimus_status optimus_grouped_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
+                                                 optimus_act epilogue, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_linear(d, G, dt, epilogue, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
+                                                    optimus_act epilogue, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_layernorm(d, G, dt, epilogue, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt,
+                                                    optimus_act op, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_pointwise(d, G, dt, op, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
+                                               optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_split_op_cat(d, dt, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}

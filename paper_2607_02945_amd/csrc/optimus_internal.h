@@ -1,0 +1,110 @@
+// Internal types shared by the host planner and the gfx950 kernels of liboptimus.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "optimus.h"
+
+namespace optimus {
+
+// ------------------------------------------------------------------ device tables
+// Every grouped launch reads a device-resident table written once by the planner.
+
+// One Linear member as the GEMM kernel reads it (operand pointers, strides,
+// sizes, and a flag telling whether 16-byte vector access is legal).
+struct DevLinear {
+  const void* x;
+  const void* w;
+  const void* bias;
+  void* y;
+  int64_t ldx, ldw, ldy;
+  int32_t M, N, K;
+  int32_t vec;  // bit0: x/w rows 16-B loadable (K, ldx, ldw, pointers); bit1: y rows 16-B storable
+};
+
+// One GEMM work item: the BM x BN output tile (mb, nb) of member `member`;
+// member < 0 marks a padding entry that does no work.
+struct GemmTile {
+  int32_t member, mb, nb, pad;
+};
+
+// One row-wise member (LayerNorm or pointwise; a split-op-cat piece is a
+// member that points into the shared input/output at its column offset).
+struct DevRows {
+  const void* x;
+  void* y;
+  const void* gamma;
+  const void* beta;
+  int64_t ldx, ldy;
+  int32_t rows, cols;
+  int32_t lanes;   // lanes per row (power of two, 1..64) for the LayerNorm kernel
+  int32_t vec;     // 1 when rows are 16-B loadable/storable
+  float eps;
+  float inv_cols;
+};
+
+// One row-wise work item: rows [row0, row0 + nrows) of member `member`.
+struct RowTile {
+  int32_t member, row0, nrows, pad;
+};
+
+// Fused split-op-cat: per 16-byte chunk of a row, the piece it belongs to;
+// per reduction task, a run of chunks of one piece.
+struct SocPiece {
+  int32_t c0, c1;      // chunk range [c0, c1) of the piece
+  float inv_width;
+  int32_t pad;
+};
+
+struct SocTask {
+  int16_t c0, c1;      // chunk range summed by one lane
+  int16_t piece, pad;
+};
+
+struct DevSoc {
+  const void* in;
+  void* out;
+  const void* gamma;   // [D] packed per-piece gamma (device, plan-owned), or null
+  const void* beta;    // [D] packed per-piece beta, or null
+  const uint8_t* chunk_piece;   // [nchunks]
+  const SocPiece* pieces;       // [n_pieces]
+  const SocTask* tasks;         // [n_tasks]
+  int64_t ldin, ldout;
+  int32_t rows, D, nchunks, n_pieces, n_tasks;
+  int32_t apply_ln;
+  float eps;
+  int32_t pad;
+};
+
+// ------------------------------------------------------------------ launchers
+// Implemented in the kernel translation units; each enqueues exactly one
+// kernel launch on `stream` and returns the launch status.
+struct GemmConfig {
+  int bm, bn;          // tile
+  int variant;         // index into the kernel table
+  int threads;
+  const char* name;
+};
+
+GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G);
+hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, const DevLinear* descs,
+                       const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream);
+
+constexpr int kRowThreads = 256;
+hipError_t layernorm_launch(optimus_dtype dt, optimus_act act, const DevRows* descs, const RowTile* tiles,
+                            int32_t num_tiles, int32_t grid, hipStream_t stream);
+hipError_t pointwise_launch(optimus_dtype dt, optimus_act act, const DevRows* descs, const RowTile* tiles,
+                            int32_t num_tiles, int32_t grid, hipStream_t stream);
+
+constexpr int kSocThreads = 256;
+constexpr int kSocMaxChunks = 1024;  // 16-byte chunks per row held in registers by one wave (<= 64 * kSocSteps)
+constexpr int kSocSteps = 16;
+constexpr int kSocMaxPieces = 256;
+constexpr int kSocMaxTasks = 128;    // two per lane
+hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t rows, int32_t nchunks,
+                      int32_t n_pieces, int32_t n_tasks, int32_t grid, hipStream_t stream);
+
+int device_cu_count();
+
+}  // namespace optimus

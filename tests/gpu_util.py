@@ -1,0 +1,45 @@
+"""Helpers for the GPU parity tests: device transfer and the comparison metric."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from paper_2607_02945_amd import synth
+
+# Tolerances: fp32 members 1e-5, bf16 storage with fp32 accumulation 2e-2,
+# both as an inf-normwise relative error per member (or per piece): elementwise
+# relative error is unbounded where LayerNorm or tanh outputs pass near zero.
+TOL = {"fp32": 1e-5, "bf16": 2e-2}
+
+
+def say(*a):
+    """Name the case before a GPU step (flushed, so a fault still shows it)."""
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev(t):
+    return None if t is None else t.to("cuda", non_blocking=False)
+
+
+def host64(t: torch.Tensor) -> np.ndarray:
+    torch.cuda.synchronize()
+    return synth.exact64(t)
+
+
+def normwise(gpu: np.ndarray, ref: np.ndarray) -> float:
+    ref = np.asarray(ref, np.float64)
+    return float(np.max(np.abs(np.asarray(gpu, np.float64) - ref)) / max(float(np.max(np.abs(ref))), 1e-30))
+
+
+def assert_close(gpu, ref, dtype: str, what: str = ""):
+    e = normwise(gpu, ref)
+    assert np.all(np.isfinite(gpu)), f"{what}: non-finite output"
+    assert e <= TOL[dtype], f"{what}: normwise rel err {e:.3e} > {TOL[dtype]:.0e}"
+    return e
+
+
+def empty_like_rows(rows, cols, dtype, fill=float("nan")):
+    return torch.full((rows, cols), fill, dtype=synth.DTYPES[dtype], device="cuda")

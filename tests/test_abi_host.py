@@ -1,0 +1,148 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol, and
+its descriptor validation (no device access) accepts and rejects the right
+groups."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_02945_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+OK, INVALID, UNSUPPORTED, ALIASING = 0, -1, -2, -3
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIBPATH), reason="liboptimus.so not built")
+
+
+def test_exports_match_header():
+    hdr = open(os.path.join(ROOT, "include", "optimus.h")).read()
+    declared = set(re.findall(r"\b(optimus_[a-z_]+)\s*\(", hdr))
+    assert declared == set(B.EXPORTS)
+    lib = B.lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert "gfx950" in B.optimus_version()
+
+
+def lin(x, w, y, M=64, N=32, K=48, ldx=None, ldw=None, ldy=None, bias=None):
+    return B.LinearDesc(x, ldx or K, w, ldw or K, bias, y, ldy or N, M, N, K)
+
+
+def lin_arr(*descs):
+    a = (B.LinearDesc * len(descs))(*descs)
+    return a, len(descs)
+
+
+MB = 1 << 20
+
+
+def test_linear_validation():
+    a, G = lin_arr(lin(1 * MB, 2 * MB, 3 * MB), lin(4 * MB, 5 * MB, 6 * MB, M=7, N=5, K=3))
+    assert B.optimus_validate_linear(a, G, B.BF16) == OK
+    assert B.optimus_validate_linear(a, 0, B.BF16) == OK
+    assert B.optimus_validate_linear(a, -1, B.BF16) == INVALID
+    assert B.optimus_validate_linear(a, G, 7) == UNSUPPORTED
+    assert B.optimus_validate_linear(a, G, B.F32, 9) == UNSUPPORTED
+    for bad in [lin(0, 2 * MB, 3 * MB), lin(1 * MB, 0, 3 * MB), lin(1 * MB, 2 * MB, 0),
+                lin(1 * MB, 2 * MB, 3 * MB, M=0), lin(1 * MB, 2 * MB, 3 * MB, K=0),
+                lin(1 * MB, 2 * MB, 3 * MB, ldx=47), lin(1 * MB, 2 * MB, 3 * MB, ldy=31),
+                lin(1 * MB, 2 * MB, 3 * MB, M=1 << 31)]:
+        a, G = lin_arr(bad)
+        assert B.optimus_validate_linear(a, G, B.BF16) == INVALID
+        assert B.optimus_last_error()
+
+
+def test_linear_aliasing():
+    # output of member 1 lands inside member 0's input
+    a, G = lin_arr(lin(1 * MB, 2 * MB, 3 * MB), lin(4 * MB, 5 * MB, 1 * MB + 1024))
+    assert B.optimus_validate_linear(a, G, B.BF16) == ALIASING
+    assert "independent" in B.optimus_last_error()
+    # in place is never allowed for a GEMM
+    a, G = lin_arr(lin(1 * MB, 2 * MB, 1 * MB, M=8, N=8, K=8))
+    assert B.optimus_validate_linear(a, G, B.F32) == ALIASING
+    # two outputs overlapping
+    a, G = lin_arr(lin(1 * MB, 2 * MB, 3 * MB), lin(4 * MB, 5 * MB, 3 * MB + 64))
+    assert B.optimus_validate_linear(a, G, B.BF16) == ALIASING
+    # shared input and shared weights are fine (inputs may overlap inputs)
+    a, G = lin_arr(lin(1 * MB, 2 * MB, 3 * MB), lin(1 * MB, 2 * MB, 4 * MB))
+    assert B.optimus_validate_linear(a, G, B.BF16) == OK
+    # bias overlapping an output
+    a, G = lin_arr(lin(1 * MB, 2 * MB, 3 * MB, bias=3 * MB + 2))
+    assert B.optimus_validate_linear(a, G, B.BF16) == ALIASING
+
+
+def pw(x, y, rows, cols, ldx, ldy):
+    return B.PointwiseDesc(x, ldx, y, ldy, rows, cols)
+
+
+def test_column_slices_of_one_buffer_are_independent():
+    # 4 outputs: column slices [0,16) [16,48) [48,64) [64,128) of one [100, 128] bf16 buffer
+    out, inp = 8 * MB, 16 * MB
+    cuts = [0, 16, 48, 64, 128]
+    ds = [pw(inp + 2 * c0, out + 2 * c0, 100, c1 - c0, 128, 128) for c0, c1 in zip(cuts, cuts[1:])]
+    arr = (B.PointwiseDesc * 4)(*ds)
+    assert B.optimus_validate_pointwise(arr, 4, B.BF16) == OK
+    # exact in-place members are allowed
+    ds = [pw(out + 2 * c0, out + 2 * c0, 100, c1 - c0, 128, 128) for c0, c1 in zip(cuts, cuts[1:])]
+    arr = (B.PointwiseDesc * 4)(*ds)
+    assert B.optimus_validate_pointwise(arr, 4, B.BF16) == OK
+    # one column of overlap between neighbouring slices
+    ds = [pw(inp, out, 100, 17, 128, 128), pw(inp + 32, out + 32, 100, 16, 128, 128)]
+    arr = (B.PointwiseDesc * 2)(*ds)
+    assert B.optimus_validate_pointwise(arr, 2, B.BF16) == ALIASING
+    # disjoint columns but the second slice's rows wrap into the first (stride mismatch -> conservative)
+    ds = [pw(inp, out, 100, 16, 128, 128), pw(inp + 64, out + 64, 100, 16, 64, 64)]
+    arr = (B.PointwiseDesc * 2)(*ds)
+    assert B.optimus_validate_pointwise(arr, 2, B.BF16) == ALIASING
+    # an in-place member whose input is shifted by one row is not in place
+    ds = [pw(out, out + 256, 100, 128, 128, 128)]
+    arr = (B.PointwiseDesc * 1)(*ds)
+    assert B.optimus_validate_pointwise(arr, 1, B.BF16) == ALIASING
+
+
+def test_layernorm_validation():
+    d = B.LayerNormDesc(1 * MB, 64, 2 * MB, 64, 3 * MB, 3 * MB + 4096, 100, 64, 1e-5)
+    arr = (B.LayerNormDesc * 1)(d)
+    assert B.optimus_validate_layernorm(arr, 1, B.F32, "tanh") == OK
+    for field, val, want in [("rows", 0, INVALID), ("cols", 0, INVALID), ("ldx", 63, INVALID),
+                             ("eps", -1.0, INVALID), ("eps", float("nan"), INVALID), ("x", None, INVALID),
+                             ("gamma", 2 * MB + 128, ALIASING)]:
+        bad = B.LayerNormDesc(1 * MB, 64, 2 * MB, 64, 3 * MB, 3 * MB + 4096, 100, 64, 1e-5)
+        setattr(bad, field, val)
+        arr = (B.LayerNormDesc * 1)(bad)
+        assert B.optimus_validate_layernorm(arr, 1, B.F32) == want, field
+    # in place is allowed for LayerNorm
+    d = B.LayerNormDesc(1 * MB, 64, 1 * MB, 64, None, None, 100, 64, 1e-5)
+    assert B.optimus_validate_layernorm((B.LayerNormDesc * 1)(d), 1, B.BF16) == OK
+
+
+def soc(inp, out, widths, rows=10, ld=None, gam=None, bet=None, ln=1):
+    n = len(widths)
+    D = sum(widths)
+    w = (ctypes.c_int64 * n)(*widths)
+    g = None if gam is None else (ctypes.c_void_p * n)(*gam)
+    b = None if bet is None else (ctypes.c_void_p * n)(*bet)
+    d = B.SplitOpCatDesc(inp, ld or D, out, ld or D, rows, D, n, w, g, b, ln, 1e-5, 4)
+    return d, (w, g, b)
+
+
+def test_split_op_cat_validation():
+    d, keep = soc(1 * MB, 2 * MB, [2, 2, 2])
+    assert B.optimus_validate_split_op_cat(d, B.BF16) == OK
+    d, keep = soc(1 * MB, 1 * MB, [16, 48])   # in place
+    assert B.optimus_validate_split_op_cat(d, B.BF16) == OK
+    d, keep = soc(1 * MB, 1 * MB + 64, [16, 48])   # shifted: overlaps
+    assert B.optimus_validate_split_op_cat(d, B.BF16) == ALIASING
+    d, keep = soc(1 * MB, 2 * MB, [2, 0, 4])
+    assert B.optimus_validate_split_op_cat(d, B.BF16) == INVALID
+    d, keep = soc(1 * MB, 2 * MB, [2, 2, 2])
+    d.D = 7
+    d.ldin = d.ldout = 7
+    assert B.optimus_validate_split_op_cat(d, B.BF16) == INVALID
+    assert "sum" in B.optimus_last_error()
+    d, keep = soc(1 * MB, 2 * MB, [8, 8], gam=[3 * MB, 2 * MB + 8], bet=[None, None])
+    assert B.optimus_validate_split_op_cat(d, B.BF16) == ALIASING
+    d, keep = soc(1 * MB, 2 * MB, [8, 8])
+    d.act = 11
+    assert B.optimus_validate_split_op_cat(d, B.BF16) == UNSUPPORTED

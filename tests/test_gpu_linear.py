@@ -1,0 +1,166 @@
+"""Grouped Linear on the GPU against the fp64 oracle (through the C ABI)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_02945_amd import binding as B
+from paper_2607_02945_amd import synth
+from tests.gpu_util import TOL, assert_close, dev, host64, say
+
+pytestmark = pytest.mark.gpu
+ORC = oracle.get()
+ACTS = ["none", "relu", "sigmoid", "tanh", "silu"]
+
+
+def _members(shapes, dtype, seed, integer=False, strided=False, bias=True):
+    g = synth.rng(seed)
+    ms = []
+    for M, N, K in shapes:
+        if integer:
+            x = synth.to_storage(g.integers(-4, 5, size=(M, K)).astype(np.float64), dtype)
+            w = synth.to_storage(g.integers(-4, 5, size=(N, K)).astype(np.float64), dtype)
+            b = synth.to_storage(g.integers(-8, 9, size=N).astype(np.float64), dtype)
+        else:
+            x = synth.to_storage(g.standard_normal((M, K)), dtype)
+            w = synth.to_storage(g.standard_normal((N, K)) / np.sqrt(K), dtype)
+            b = synth.to_storage(g.standard_normal(N) * 0.1, dtype)
+        xd = dev(x)
+        if strided:  # x as a column view of a wider buffer
+            big = torch.zeros((M, K + 24), dtype=x.dtype, device="cuda")
+            big[:, 8:8 + K] = xd
+            xd = big[:, 8:8 + K]
+        ms.append((xd, dev(w), dev(b) if bias else None))
+    return ms
+
+
+def _run(ms, dtype, act, mode="oneshot", variant=None):
+    ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, _ in ms]
+    xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
+    old = os.environ.get("OPTIMUS_GEMM_VARIANT")
+    if variant is not None:
+        os.environ["OPTIMUS_GEMM_VARIANT"] = str(variant)
+    try:
+        if mode == "oneshot":
+            B.optimus_grouped_linear(xs, ws, bs, ys, act)
+        else:
+            p = B.optimus_plan_linear(xs, ws, bs, ys, act)
+            p.execute(mode)
+            torch.cuda.synchronize()
+            p.close()
+    finally:
+        if variant is not None:
+            if old is None:
+                del os.environ["OPTIMUS_GEMM_VARIANT"]
+            else:
+                os.environ["OPTIMUS_GEMM_VARIANT"] = old
+    return ys
+
+
+def _check(ms, ys, dtype, act, what):
+    for i, ((x, w, b), y) in enumerate(zip(ms, ys)):
+        ref = ORC.linear(host64(x), host64(w), None if b is None else host64(b), act)
+        assert_close(host64(y), ref, dtype, f"{what} member {i}")
+
+
+RAGGED = [(1, 1, 8), (37, 16, 16), (130, 65, 48), (300, 200, 264), (64, 64, 64), (257, 129, 100)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("act", ACTS)
+def test_ragged_group_all_acts(dtype, act):
+    say(f"[linear ragged] dtype={dtype} act={act}")
+    ms = _members(RAGGED, dtype, seed=10)
+    ys = _run(ms, dtype, act)
+    _check(ms, ys, dtype, act, f"ragged {dtype} {act}")
+
+
+@pytest.mark.parametrize("variant", [0, 1, 2])
+def test_every_bf16_tile_variant(variant):
+    say(f"[linear variant] {variant}")
+    shapes = [(513, 300, 72), (256, 256, 1024), (31, 7, 40), (700, 520, 136)]
+    ms = _members(shapes, "bf16", seed=11 + variant)
+    for mode in ["oneshot", "grouped", "chain"]:
+        ys = _run(ms, "bf16", "tanh", mode=mode, variant=variant)
+        _check(ms, ys, "bf16", "tanh", f"variant {variant} {mode}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_unaligned_k_and_strided_input(dtype):
+    say(f"[linear scalar path] {dtype}")
+    ms = _members([(50, 33, 5), (70, 17, 13), (129, 40, 3)], dtype, seed=12)
+    ys = _run(ms, dtype, "none")
+    _check(ms, ys, dtype, "none", "K not a multiple of the vector width")
+    ms = _members([(90, 48, 32), (65, 64, 56)], dtype, seed=13, strided=True)
+    ys = _run(ms, dtype, "sigmoid")
+    _check(ms, ys, dtype, "sigmoid", "strided x")
+    ms = _members([(90, 48, 32)], dtype, seed=14, bias=False)
+    ys = _run(ms, dtype, "relu")
+    _check(ms, ys, dtype, "relu", "no bias")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_brute_force_integer_groups_bit_exact(dtype):
+    """Small integers: every product and sum is exact in fp32 accumulation and the
+    results (|y| <= 100) are exact in bf16, so the GPU must equal the oracle bit for bit."""
+    say(f"[linear brute force] {dtype}")
+    shapes = [(M, N, K) for M in (1, 2, 5) for N in (1, 3, 5) for K in (1, 2, 4, 5)]
+    for s in range(0, len(shapes), 12):
+        ms = _members(shapes[s:s + 12], dtype, seed=100 + s, integer=True)
+        ys = _run(ms, dtype, "none")
+        for (x, w, b), y in zip(ms, ys):
+            ref = ORC.linear(host64(x), host64(w), host64(b))
+            assert np.array_equal(host64(y), ref)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_zero_and_identity_weights_bit_exact(dtype):
+    say(f"[linear zero/identity] {dtype}")
+    g = synth.rng(15)
+    x = dev(synth.to_storage(g.standard_normal((200, 64)), dtype))
+    b = dev(synth.to_storage(g.standard_normal(48), dtype))
+    w0 = torch.zeros((48, 64), dtype=x.dtype, device="cuda")
+    eye = torch.eye(64, dtype=x.dtype, device="cuda")
+    z = torch.zeros(64, dtype=x.dtype, device="cuda")
+    ys = _run([(x, w0, b), (x, eye, z)], dtype, "none")
+    assert np.array_equal(host64(ys[0]), np.broadcast_to(host64(b), (200, 48)))
+    assert np.array_equal(host64(ys[1]), host64(x))
+
+
+def test_batch_fusion_identity_equal_shapes():
+    """Equal-shape members (paper Sec. 3.2 batch fusion) against one batched
+    matmul of the stacked operands, computed by the oracle member by member and
+    by numpy on the stack."""
+    say("[linear batch fusion]")
+    ms = _members([(256, 64, 128)] * 6, "bf16", seed=16)
+    ys = _run(ms, "bf16", "none")
+    xs = np.stack([host64(m[0]) for m in ms])
+    ws = np.stack([host64(m[1]) for m in ms])
+    bs = np.stack([host64(m[2]) for m in ms])
+    st = np.matmul(xs, np.transpose(ws, (0, 2, 1))) + bs[:, None, :]
+    for i, y in enumerate(ys):
+        assert_close(host64(y), st[i], "bf16", f"stacked member {i}")
+
+
+def test_chain_equals_grouped_bitwise():
+    """The per-member launch chain runs the same kernel per member, so it must give
+    the grouped launch's bits exactly."""
+    say("[linear chain vs grouped]")
+    ms = _members(RAGGED, "bf16", seed=17)
+    a = _run(ms, "bf16", "silu", mode="grouped")
+    c = _run(ms, "bf16", "silu", mode="chain")
+    for ya, yc in zip(a, c):
+        assert torch.equal(ya, yc)
+
+
+def test_empty_group_and_errors():
+    say("[linear empty/errors]")
+    B.optimus_grouped_linear([], [], [], [], "none")
+    x = torch.zeros((8, 8), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((8, 8), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(B.OptimusError) as ei:
+        B.optimus_grouped_linear([x], [w], [None], [x], "none")
+    assert ei.value.name == "ALIASING"
+    assert torch.count_nonzero(x) == 0

@@ -1,0 +1,137 @@
+"""Fused split -> per-piece LayerNorm/activation -> concat on the GPU."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_02945_amd import binding as B
+from paper_2607_02945_amd import synth
+from tests.gpu_util import assert_close, dev, host64, say
+
+pytestmark = pytest.mark.gpu
+ORC = oracle.get()
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _case(rows, widths, dtype, seed):
+    g = synth.rng(seed)
+    D = sum(widths)
+    x = dev(synth.to_storage(g.standard_normal((rows, D)) * 1.5 + 0.3, dtype))
+    gms = [dev(synth.to_storage(g.uniform(0.5, 1.5, w), dtype)) for w in widths]
+    bts = [dev(synth.to_storage(g.standard_normal(w) * np.sqrt(0.1), dtype)) for w in widths]
+    return x, gms, bts
+
+
+def _check_pieces(y, x, widths, gms, bts, act, dtype, what):
+    ref = ORC.split_op_cat(host64(x), widths, [host64(g) for g in gms] if gms else None,
+                           [host64(b) for b in bts] if bts else None, True, 1e-5, act)
+    yh = host64(y)
+    o = 0
+    for j, w in enumerate(widths):
+        assert_close(yh[:, o:o + w], ref[:, o:o + w], dtype, f"{what} piece {j}")
+        o += w
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("act", ["silu", "tanh", "none"])
+def test_dirichlet_pieces_all_modes(dtype, act):
+    say(f"[soc dirichlet] dtype={dtype} act={act}")
+    widths = synth.dirichlet_widths(synth.rng(40), 32, 4096)
+    x, gms, bts = _case(777, widths, dtype, seed=41)
+    for mode in ["grouped", "horizontal", "chain"]:
+        y = torch.full_like(x, float("nan"))
+        p = B.optimus_plan_split_op_cat(x, y, widths, gms, bts, True, 1e-5, act)
+        p.execute(mode)
+        torch.cuda.synchronize()
+        info = p.info()
+        assert info["launches"] == 1 and info["chain_launches"] == 2 * len(widths) + 1
+        if mode == "grouped" and dtype == "bf16":
+            assert info["kernel"].startswith("split_op_cat_fused")
+        _check_pieces(y, x, widths, gms, bts, act, dtype, mode)
+        p.close()
+
+
+@pytest.mark.parametrize("widths", [[16] * 8, [8, 8, 16, 32, 64, 8], [4096], [2048, 2048], [128] * 32, [8] * 256])
+def test_piece_layouts(widths):
+    say(f"[soc layouts] n={len(widths)} D={sum(widths)}")
+    x, gms, bts = _case(65, widths, "bf16", seed=42)
+    y = torch.empty_like(x)
+    B.optimus_split_op_cat(x, y, widths, gms, bts, True, 1e-5, "silu")
+    _check_pieces(y, x, widths, gms, bts, "silu", "bf16", f"widths {widths[:4]}")
+
+
+def test_equal_widths_equal_stacked_layernorm():
+    """32 equal pieces == one LayerNorm over the stacked [rows, 32, 128] view (batch fusion)."""
+    say("[soc stacked]")
+    x, _, _ = _case(300, [128] * 32, "bf16", seed=43)
+    y = torch.empty_like(x)
+    B.optimus_split_op_cat(x, y, [128] * 32, None, None, True, 1e-5, "none")
+    xs = host64(x).reshape(300, 32, 128)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(xs), (128,), eps=1e-5).numpy().reshape(300, 4096)
+    assert_close(host64(y), ref, "bf16", "stacked")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_split_cat_identity_bit_exact(dtype):
+    """No LayerNorm and no activation: split o cat is the identity, bit for bit."""
+    say(f"[soc identity] {dtype}")
+    widths = synth.dirichlet_widths(synth.rng(44), 32, 4096)
+    x, _, _ = _case(513, widths, dtype, seed=45)
+    y = torch.full_like(x, float("nan"))
+    B.optimus_split_op_cat(x, y, widths, None, None, False, 1e-5, "none")
+    assert torch.equal(x, y)
+    y2 = torch.full_like(x, float("nan"))
+    B.optimus_split_op_cat(x, y2, [5, 11, 4000, 80], None, None, False, 1e-5, "none")
+    assert torch.equal(x, y2)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_tag_pieces_land_at_their_offsets(dtype):
+    """gamma_j = 0, beta_j = j: every element of piece j must read j exactly."""
+    say(f"[soc tag] {dtype}")
+    widths = synth.dirichlet_widths(synth.rng(46), 32, 4096)
+    x, _, _ = _case(129, widths, dtype, seed=47)
+    gms = [torch.zeros(w, dtype=x.dtype, device="cuda") for w in widths]
+    bts = [torch.full((w,), float(j), dtype=x.dtype, device="cuda") for j, w in enumerate(widths)]
+    y = torch.full_like(x, float("nan"))
+    B.optimus_split_op_cat(x, y, widths, gms, bts, True, 1e-5, "none")
+    want = np.concatenate([np.full((129, w), float(j)) for j, w in enumerate(widths)], axis=1)
+    assert np.array_equal(host64(y), want)
+
+
+def test_appendix_example_bit_exact():
+    """Appendix Sec. 8.1 split-concat listing, shape [2, 6], pieces [2] + [2, 2]."""
+    say("[soc appendix example]")
+    with open(os.path.join(GOLDEN, "appendix_split_concat.json")) as f:
+        ex = json.load(f)
+    for dtype in ["bf16", "fp32"]:
+        x = dev(synth.to_storage(synth.rng(48).standard_normal(tuple(ex["input_shape"])), dtype))
+        y = torch.full_like(x, float("nan"))
+        B.optimus_split_op_cat(x, y, ex["flattened_widths"], None, None, False, 1e-5, "none")
+        assert torch.equal(x, y)
+
+
+def test_in_place():
+    say("[soc in place]")
+    widths = synth.dirichlet_widths(synth.rng(49), 32, 4096)
+    x, gms, bts = _case(200, widths, "bf16", seed=50)
+    x0 = x.clone()
+    B.optimus_split_op_cat(x, x, widths, gms, bts, True, 1e-5, "silu")
+    _check_pieces(x, x0, widths, gms, bts, "silu", "bf16", "in place")
+
+
+def test_wide_row_falls_back_to_grouped_layernorm():
+    """A row wider than the fused kernel holds in registers runs as one grouped
+    LayerNorm launch over the pieces, still with no copies."""
+    say("[soc wide fallback]")
+    widths = [4096, 4096, 48, 16]
+    x, gms, bts = _case(20, widths, "bf16", seed=51)
+    y = torch.empty_like(x)
+    p = B.optimus_plan_split_op_cat(x, y, widths, gms, bts, True, 1e-5, "tanh")
+    p.execute()
+    assert p.info()["kernel"] == "split_op_cat_as_grouped_layernorm"
+    _check_pieces(y, x, widths, gms, bts, "tanh", "bf16", "wide")
+    p.close()

@@ -1,0 +1,154 @@
+"""The five synthetic workload groups, end to end, in the launch configuration the
+benchmark times (plans executed as one grouped launch per operator type).
+
+Small groups are compared element by element with the oracle; the large groups
+on sampled rows the oracle computes one by one. Each group is checked per
+operator (the oracle fed the GPU's own stored intermediate) and end to end (the
+fp64 chain from the original inputs, no intermediate rounding)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_02945_amd import binding as B
+from paper_2607_02945_amd import synth
+from tests.gpu_util import assert_close, dev, host64, say
+
+pytestmark = pytest.mark.gpu
+ORC = oracle.get()
+
+
+def _sample_rows(M, n, seed):
+    g = synth.rng(seed)
+    rows = np.unique(np.concatenate([[0, M - 1], g.choice(M, size=min(M, n), replace=False)]))
+    return rows.astype(np.int64)
+
+
+def test_tiny_group_fp32():
+    say("[workload tiny_group] G=8 B=512 fp32")
+    wl = synth.tiny_group(0)
+    xs = [dev(m.x) for m in wl.members]
+    ws = [dev(m.w) for m in wl.members]
+    bs = [dev(m.b) for m in wl.members]
+    ys = [torch.empty((m.M, m.N), dtype=torch.float32, device="cuda") for m in wl.members]
+    zs = [torch.empty_like(y) for y in ys]
+    gs = [dev(g) for g in wl.gammas]
+    be = [dev(b) for b in wl.betas]
+    p1 = B.optimus_plan_linear(xs, ws, bs, ys, "none")
+    p2 = B.optimus_plan_layernorm(ys, zs, gs, be, wl.eps, "tanh")
+    p1.execute()
+    p2.execute()
+    torch.cuda.synchronize()
+    for i, m in enumerate(wl.members):
+        x64, w64, b64 = synth.exact64(m.x), synth.exact64(m.w), synth.exact64(m.b)
+        lin = ORC.linear(x64, w64, b64)
+        assert_close(host64(ys[i]), lin, "fp32", f"linear {i}")
+        assert_close(host64(zs[i]), ORC.layernorm(host64(ys[i]), host64(gs[i]), host64(be[i]), wl.eps, "tanh"),
+                     "fp32", f"layernorm {i} (per op)")
+        assert_close(host64(zs[i]), ORC.layernorm(lin, host64(gs[i]), host64(be[i]), wl.eps, "tanh"),
+                     "fp32", f"end to end {i}")
+
+
+def test_launch_bound_group_bf16():
+    say("[workload launch_bound] G=256 B=2048 bf16")
+    wl = synth.launch_bound(0)
+    xs = [dev(m.x) for m in wl.members]
+    ws = [dev(m.w) for m in wl.members]
+    bs = [dev(m.b) for m in wl.members]
+    ys = [torch.empty((m.M, m.N), dtype=torch.bfloat16, device="cuda") for m in wl.members]
+    p = B.optimus_plan_linear(xs, ws, bs, ys, "sigmoid")
+    p.execute()
+    # the unfused form: Linear, then a grouped sigmoid launch
+    y1 = [torch.empty_like(y) for y in ys]
+    y2 = [torch.empty_like(y) for y in ys]
+    q1 = B.optimus_plan_linear(xs, ws, bs, y1, "none")
+    q2 = B.optimus_plan_pointwise(y1, y2, "sigmoid")
+    q1.execute()
+    q2.execute()
+    torch.cuda.synchronize()
+    assert p.info()["launches"] == 1 and p.info()["chain_launches"] == 256
+    for i, m in enumerate(wl.members):
+        ref = ORC.linear(synth.exact64(m.x), synth.exact64(m.w), synth.exact64(m.b), "sigmoid")
+        assert_close(host64(ys[i]), ref, "bf16", f"fused member {i}")
+        assert_close(host64(y2[i]), ORC.pointwise(host64(y1[i]), "sigmoid"), "bf16", f"sigmoid member {i} (per op)")
+        assert_close(host64(y2[i]), ref, "bf16", f"unfused member {i} (end to end)")
+
+
+def test_split_op_cat_full_size_sampled_rows():
+    say("[workload split_op_cat] [8192, 4096] bf16, 32 pieces")
+    wl = synth.split_op_cat(0)
+    x = dev(wl.x)
+    y = torch.empty_like(x)
+    gs = [dev(g) for g in wl.gammas]
+    bs = [dev(b) for b in wl.betas]
+    p = B.optimus_plan_split_op_cat(x, y, wl.widths, gs, bs, True, wl.eps, wl.act)
+    p.execute()
+    torch.cuda.synchronize()
+    assert p.info()["kernel"] == "split_op_cat_fused_bf16"
+    rows = _sample_rows(8192, 384, seed=60)
+    xh = synth.exact64(wl.x[torch.from_numpy(rows)])
+    ref = ORC.split_op_cat(xh, wl.widths, [synth.exact64(g) for g in wl.gammas],
+                           [synth.exact64(b) for b in wl.betas], True, wl.eps, wl.act)
+    yh = host64(y)[rows]
+    o = 0
+    for j, w in enumerate(wl.widths):
+        assert_close(yh[:, o:o + w], ref[:, o:o + w], "bf16", f"piece {j}")
+        o += w
+
+
+def test_towers_full_size_sampled_rows():
+    say("[workload towers] 26 towers B=4096 bf16")
+    wl = synth.towers(0)
+    T = wl.towers
+    xs = [dev(t.x) for t in T]
+    h = [torch.empty((4096, 512), dtype=torch.bfloat16, device="cuda") for _ in T]
+    o = [torch.empty((4096, 256), dtype=torch.bfloat16, device="cuda") for _ in T]
+    z = [torch.empty_like(v) for v in o]
+    w1, b1, w2, b2 = ([dev(getattr(t, a)) for t in T] for a in ("w1", "b1", "w2", "b2"))
+    gm, bt = [dev(t.gamma) for t in T], [dev(t.beta) for t in T]
+    plans = [B.optimus_plan_linear(xs, w1, b1, h, "relu"), B.optimus_plan_linear(h, w2, b2, o, "none"),
+             B.optimus_plan_layernorm(o, z, gm, bt, wl.eps, "none")]
+    for p in plans:
+        p.execute()
+    torch.cuda.synchronize()
+    rows = _sample_rows(4096, 96, seed=61)
+    for i, t in enumerate(T):
+        x64 = synth.exact64(t.x)
+        h_ref = ORC.linear_rows(x64, synth.exact64(t.w1), synth.exact64(t.b1), rows, "relu")
+        hh = host64(h[i])
+        assert_close(hh[rows], h_ref, "bf16", f"tower {i} layer 1")
+        o_ref = ORC.linear_rows(hh, synth.exact64(t.w2), synth.exact64(t.b2), rows)
+        oh = host64(o[i])
+        assert_close(oh[rows], o_ref, "bf16", f"tower {i} layer 2 (per op)")
+        z_ref = ORC.layernorm(oh[rows], synth.exact64(t.gamma), synth.exact64(t.beta), wl.eps)
+        assert_close(host64(z[i])[rows], z_ref, "bf16", f"tower {i} layernorm (per op)")
+        e2e = ORC.layernorm(ORC.linear(h_ref, synth.exact64(t.w2), synth.exact64(t.b2)),
+                            synth.exact64(t.gamma), synth.exact64(t.beta), wl.eps)
+        assert_close(host64(z[i])[rows], e2e, "bf16", f"tower {i} end to end")
+
+
+def test_large_group_full_size_sampled_rows():
+    say("[workload large_group] G=32 B=16384 K=1024 bf16")
+    wl = synth.large_group(0)
+    xs = [dev(m.x) for m in wl.members]
+    ws = [dev(m.w) for m in wl.members]
+    bs = [dev(m.b) for m in wl.members]
+    ys = [torch.empty((m.M, m.N), dtype=torch.bfloat16, device="cuda") for m in wl.members]
+    zs = [torch.empty_like(y) for y in ys]
+    gs = [dev(g) for g in wl.gammas]
+    be = [dev(b) for b in wl.betas]
+    p1 = B.optimus_plan_linear(xs, ws, bs, ys, "none")
+    p2 = B.optimus_plan_layernorm(ys, zs, gs, be, wl.eps, "tanh")
+    p1.execute()
+    p2.execute()
+    torch.cuda.synchronize()
+    rows = _sample_rows(16384, 48, seed=62)
+    for i, m in enumerate(wl.members):
+        lin = ORC.linear_rows(synth.exact64(m.x), synth.exact64(m.w), synth.exact64(m.b), rows)
+        yh = host64(ys[i])
+        assert_close(yh[rows], lin, "bf16", f"member {i} linear")
+        g64, b64 = synth.exact64(wl.gammas[i]), synth.exact64(wl.betas[i])
+        assert_close(host64(zs[i])[rows], ORC.layernorm(yh[rows], g64, b64, wl.eps, "tanh"), "bf16",
+                     f"member {i} layernorm+tanh (per op)")
+        assert_close(host64(zs[i])[rows], ORC.layernorm(lin, g64, b64, wl.eps, "tanh"), "bf16",
+                     f"member {i} end to end")
