@@ -14,7 +14,8 @@ from typing import List, Optional, Sequence
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIBPATH = os.path.join(_PKG, "liboptimus.so")
+# OPTIMUS_LIBRARY may name another build of the same library (tuning builds).
+LIBPATH = os.environ.get("OPTIMUS_LIBRARY") or os.path.join(_PKG, "liboptimus.so")
 
 F32, BF16 = 0, 1
 ACTS = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "silu": 4}

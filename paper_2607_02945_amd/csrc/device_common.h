@@ -19,6 +19,8 @@ struct bf16_t {
   uint16_t bits;
 };
 
+#define OPTIMUS_GLOBAL __attribute__((address_space(1)))
+
 // ------------------------------------------------------------------ conversions
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __builtin_bit_cast(float, u << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t u) { return __builtin_bit_cast(float, u & 0xffff0000u); }
@@ -52,8 +54,8 @@ struct Elem<float> {
     const f32x4 f = {v[0], v[1], v[2], v[3]};
     return __builtin_bit_cast(u32x4, f);
   }
-  __device__ static __forceinline__ float load1(const void* p, int64_t i) { return ((const float*)p)[i]; }
-  __device__ static __forceinline__ void store1(void* p, int64_t i, float v) { ((float*)p)[i] = v; }
+  __device__ static __forceinline__ float load1(const void* p, int64_t i) { return ((const OPTIMUS_GLOBAL float*)p)[i]; }
+  __device__ static __forceinline__ void store1(void* p, int64_t i, float v) { ((OPTIMUS_GLOBAL float*)p)[i] = v; }
 };
 template <>
 struct Elem<bf16_t> {
@@ -73,10 +75,31 @@ struct Elem<bf16_t> {
     return c;
   }
   __device__ static __forceinline__ float load1(const void* p, int64_t i) {
-    return bf16_to_f32(((const uint16_t*)p)[i]);
+    return bf16_to_f32(((const OPTIMUS_GLOBAL uint16_t*)p)[i]);
   }
-  __device__ static __forceinline__ void store1(void* p, int64_t i, float v) { ((uint16_t*)p)[i] = f32_to_bf16(v); }
+  __device__ static __forceinline__ void store1(void* p, int64_t i, float v) {
+    ((OPTIMUS_GLOBAL uint16_t*)p)[i] = f32_to_bf16(v);
+  }
 };
+
+// Sum of the values of one 16-byte chunk in fp32. bf16: four v_dot2 with
+// (1, 1) on the packed pairs (products by 1 are exact), no unpacking.
+template <typename T>
+__device__ __forceinline__ float chunk_sum(const u32x4& c);
+template <>
+__device__ __forceinline__ float chunk_sum<bf16_t>(const u32x4& c) {
+  const bf16x8 v = __builtin_bit_cast(bf16x8, c);
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 0, 1), one, 0.f, false);
+  a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 2, 3), one, a, false);
+  a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 4, 5), one, a, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 6, 7), one, a, false);
+}
+template <>
+__device__ __forceinline__ float chunk_sum<float>(const u32x4& c) {
+  const f32x4 f = __builtin_bit_cast(f32x4, c);
+  return (f[0] + f[1]) + (f[2] + f[3]);
+}
 
 // ------------------------------------------------------------------ activations
 // exp via the hardware base-2 exponential; reciprocal via the hardware
@@ -102,11 +125,33 @@ __device__ __forceinline__ float act_apply(float x) {
 }
 
 // ------------------------------------------------------------------ memory
-__device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
-__device__ __forceinline__ void st16(void* p, const u32x4& v) { *(u32x4*)p = v; }
+// Every tensor access goes through these helpers, which name the global
+// address space: pointers read from a descriptor table are otherwise generic,
+// and generic (flat) accesses also count against the LDS wait counter, which
+// would make every LDS wait drain the in-flight global loads too.
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *(const OPTIMUS_GLOBAL u32x4*)p; }
+__device__ __forceinline__ void st16(void* p, const u32x4& v) { *(OPTIMUS_GLOBAL u32x4*)p = v; }
 // Streaming variants: data touched once (nontemporal hint).
-__device__ __forceinline__ u32x4 ld16_nt(const void* p) { return __builtin_nontemporal_load((const u32x4*)p); }
-__device__ __forceinline__ void st16_nt(void* p, const u32x4& v) { __builtin_nontemporal_store(v, (u32x4*)p); }
+#ifndef OPTIMUS_NT_LOADS
+#define OPTIMUS_NT_LOADS 1
+#endif
+#ifndef OPTIMUS_NT_STORES
+#define OPTIMUS_NT_STORES 1
+#endif
+__device__ __forceinline__ u32x4 ld16_nt(const void* p) {
+#if OPTIMUS_NT_LOADS
+  return __builtin_nontemporal_load((const OPTIMUS_GLOBAL u32x4*)p);
+#else
+  return *(const OPTIMUS_GLOBAL u32x4*)p;
+#endif
+}
+__device__ __forceinline__ void st16_nt(void* p, const u32x4& v) {
+#if OPTIMUS_NT_STORES
+  __builtin_nontemporal_store(v, (OPTIMUS_GLOBAL u32x4*)p);
+#else
+  *(OPTIMUS_GLOBAL u32x4*)p = v;
+#endif
+}
 
 // ------------------------------------------------------------------ lane reductions
 template <int CTRL>

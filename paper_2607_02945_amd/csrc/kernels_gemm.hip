@@ -243,9 +243,9 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         } else {
           for (int e = 0; e < VEC && n + e < Nr; ++e) {
             if constexpr (sizeof(T) == 2)
-              ((uint16_t*)yp)[e] = ((const uint16_t*)sp)[e];
+              ((OPTIMUS_GLOBAL uint16_t*)yp)[e] = ((const uint16_t*)sp)[e];
             else
-              ((float*)yp)[e] = ((const float*)sp)[e];
+              ((OPTIMUS_GLOBAL float*)yp)[e] = ((const float*)sp)[e];
           }
         }
       }
@@ -256,18 +256,21 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
 
 // ===================================================================== configurations
 struct GemmVariant {
-  int bm, bn, threads;
+  int bm, bn, threads, occ;  // occ: workgroups resident per CU (LDS / register bound)
   const char* name;
 };
 
-// bf16 variants: 0 small (few-column members, single K step), 1 medium, 2 large.
-// fp32 variant: 3.
+// 0: members with N, K <= 64 (one K step); 1: 128x128; 2: 256x256 (8 waves);
+// 3: fp32; 4: 256x256 (4 waves); 5: 256x128 (4 waves).
 static const GemmVariant kVariants[] = {
-    {128, 64, 256, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
-    {128, 128, 256, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
-    {256, 256, 256, "grouped_gemm_bf16_256x256x64_w2x2_s2"},
-    {64, 64, 256, "grouped_gemm_f32_64x64x32_w2x2_s2"},
+    {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
+    {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
+    {256, 256, 512, 1, "grouped_gemm_bf16_256x256x64_w2x4_s2"},
+    {64, 64, 256, 4, "grouped_gemm_f32_64x64x32_w2x2_s2"},
+    {256, 256, 256, 1, "grouped_gemm_bf16_256x256x64_w2x2_s2"},
+    {256, 128, 256, 1, "grouped_gemm_bf16_256x128x64_w2x2_s2"},
 };
+static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
 
 GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G) {
   int v;
@@ -288,13 +291,13 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     else
       v = 1;
   }
-  // OPTIMUS_GEMM_VARIANT=<0..2> pins the bf16 tile shape (tests and tuning).
+  // OPTIMUS_GEMM_VARIANT=<n> pins the bf16 tile shape (tests and tuning).
   if (dt == OPTIMUS_BF16) {
     const char* f = getenv("OPTIMUS_GEMM_VARIANT");
-    if (f && f[0] >= '0' && f[0] <= '2' && f[1] == 0) v = f[0] - '0';
+    if (f && f[0] >= '0' && f[0] <= '9' && f[1] == 0 && f[0] - '0' < kNumVariants && f[0] != '3') v = f[0] - '0';
   }
   const GemmVariant& k = kVariants[v];
-  return GemmConfig{k.bm, k.bn, v, k.threads, k.name};
+  return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
 }
 
 template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
@@ -331,8 +334,10 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
   switch (cfg.variant) {
     case 0: return launch_shape<bf16_t, 128, 64, 64, 4, 1, 1>(act, descs, tiles, num_tiles, grid, stream);
     case 1: return launch_shape<bf16_t, 128, 128, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 2: return launch_shape<bf16_t, 256, 256, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 2: return launch_shape<bf16_t, 256, 256, 64, 2, 4, 2>(act, descs, tiles, num_tiles, grid, stream);
     case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 4: return launch_shape<bf16_t, 256, 256, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 5: return launch_shape<bf16_t, 256, 128, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     default: return hipErrorInvalidValue;
   }
 }

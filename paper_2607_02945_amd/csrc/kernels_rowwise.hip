@@ -7,6 +7,8 @@
 // Grouped kernels walk a device table of (member, row range) tiles written by
 // the planner, so one launch serves members of different shapes (Sec. 3.2
 // group fusion: instances keep their own layouts and sizes).
+#include <stdlib.h>
+
 #include "device_common.h"
 
 namespace optimus {
@@ -41,21 +43,24 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
   }
   const int rpb = 4 * rpw;
   const int end = rt.row0 + rt.nrows;
-  for (int base = rt.row0; base < end; base += rpb) {
-    const int r = base + wave * rpw + sub;
-    const bool valid = r < end;
-    float x[MAXC][VEC];
+  // The next row slot's chunks are loaded while the current one is computed.
+  u32x4 raw[MAXC];
+  auto fetch = [&](int r) {
     const char* xr = (const char*)d.x + (int64_t)r * d.ldx * sizeof(T);
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
       const int c = j * L + li;
-      if (valid && c < cpr) {
-        Elem<T>::unpack(ld16_nt(xr + (int64_t)c * 16), x[j]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) x[j][e] = 0.f;
-      }
+      raw[j] = (r < end && c < cpr) ? ld16_nt(xr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
     }
+  };
+  fetch(rt.row0 + wave * rpw + sub);
+  for (int base = rt.row0; base < end; base += rpb) {
+    const int r = base + wave * rpw + sub;
+    const bool valid = r < end;
+    float x[MAXC][VEC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) Elem<T>::unpack(raw[j], x[j]);  // zero where out of range
+    if (base + rpb < end) fetch(r + rpb);
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j)
@@ -68,8 +73,8 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
       const bool in = valid && (j * L + li) < cpr;
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float t = x[j][e] - mean;
-        q += in ? t * t : 0.f;
+        x[j][e] -= mean;
+        q += in ? x[j][e] * x[j][e] : 0.f;
       }
     }
     const float rstd = __builtin_amdgcn_rsqf(group_sum(q, L) * d.inv_cols + d.eps);
@@ -80,7 +85,7 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
       if (valid && c < cpr) {
         float o[VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>((x[j][e] - mean) * rstd * g[j][e] + b[j][e]);
+        for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>(x[j][e] * (rstd * g[j][e]) + b[j][e]);
         st16_nt(yr + (int64_t)c * 16, Elem<T>::pack(o));
       }
     }
@@ -112,19 +117,16 @@ __device__ __forceinline__ void ln_rows_scalar(const DevRows& d, const RowTile& 
   }
 }
 
-template <typename T>
-constexpr int ln_maxc() { return 4; }
-
 template <typename T, int ACT>
 __global__ __launch_bounds__(kRowThreads) void grouped_layernorm_kernel(const DevRows* __restrict__ descs,
                                                                         const RowTile* __restrict__ tiles,
                                                                         int32_t num_tiles) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
     const RowTile rt = tiles[t];
     const DevRows d = descs[rt.member];
     if (d.vec && d.lanes > 0)
-      ln_rows_vec<T, ACT, ln_maxc<T>()>(d, rt, lane, wave);
+      ln_rows_vec<T, ACT, kLnChunksPerLane>(d, rt, lane, wave);
     else
       ln_rows_scalar<T, ACT>(d, rt, lane, wave);
   }
@@ -138,7 +140,7 @@ __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const De
                                                                         const RowTile* __restrict__ tiles,
                                                                         int32_t num_tiles) {
   constexpr int VEC = Elem<T>::VEC;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
     const RowTile rt = tiles[t];
     const DevRows d = descs[rt.member];
@@ -167,129 +169,215 @@ __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const De
 }
 
 // ===================================================================== split-op-cat
-// One wave owns one whole row of the [rows, D] tensor: step j, lane l holds
-// 16-byte chunk c = 64 j + l, so every step reads 1 KB of the row contiguously
-// and writes it back at the same columns of `out` -- the split and the concat
-// are index arithmetic only. Piece statistics: chunk partial sums go to a
-// per-wave LDS array; each lane then sums one or two planner-built runs of
-// chunks that lie in a single piece and adds the run total into that piece's
-// LDS accumulator; every chunk then reads its piece's statistic back. Two
-// passes (mean, then centred squares) as in the row kernel above. Piece gamma
-// and beta are staged once per block in LDS.
-template <typename T, int ACT, int STEPS>
+// WPR waves share one row (a block of four waves works on 4 / WPR rows at a
+// time); in step j, lane l of the row's w-th wave holds the 16-byte chunk
+// c = 64 S w + 64 j + l, so every step of a wave reads 1 KB of the row
+// contiguously and writes it back at the same columns of `out` -- the split
+// and the concat are index arithmetic only. The next row is loaded while the
+// current one is computed.
+//
+// Piece statistics (two passes: sums, then centred squares): the chunk
+// partials of a row go to an LDS array in row order; each of the row's
+// 64 WPR lanes reads back the run of S consecutive chunks starting at chunk
+// (its index in the row) * S, adds them up piece by piece in registers, and
+// adds each piece's run total into that piece's LDS accumulator (ds_add_f32;
+// a piece spanning several lanes gets one add per lane). The lanes that own a
+// piece then turn its sum into the mean (or the centred sum of squares into
+// 1/sqrt(var + eps)) in place, and every chunk reads its piece's statistic
+// back. With one wave per row the row's LDS traffic is private to the wave and
+// needs no workgroup barrier. Piece gamma and beta are staged once per block
+// in LDS as fp32.
+template <typename T, int ACT, int S, int WPR, bool FULL>
 __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc* __restrict__ sp) {
   constexpr int VEC = Elem<T>::VEC;
+  constexpr int PACKS = (S + 3) / 4;    // piece ids packed four per register
+  constexpr int SLOTS = 4 / WPR;        // rows in flight per block
+  constexpr int RL = 64 * WPR;          // lanes per row
   extern __shared__ __align__(16) char smem[];
   const DevSoc s = *sp;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nch = s.nchunks, npc = s.n_pieces;
-  // LDS layout: gamma [nch * 16 B] | beta [nch * 16 B] | part [4][nch] f32 | stat [4][2][npc] f32
-  char* lg = smem;
-  char* lb = lg + (size_t)nch * 16;
-  float* part = (float*)(lb + (size_t)nch * 16) + wave * nch;
-  float* stat = (float*)(lb + (size_t)nch * 16) + 4 * nch + wave * 2 * npc;
+  // wave, slot and part are uniform across a wave: keep them (and row addresses) scalar
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int slot = wave / WPR, wr = wave % WPR;
+  // FULL: the row is exactly RL * S chunks, so no chunk needs a range check
+  const int nch = FULL ? RL * S : s.nchunks, npc = s.n_pieces;
+  // LDS: gamma [nch * VEC] f32 | beta [nch * VEC] f32 | part [SLOTS][RL * S] f32 | stat [SLOTS][2][npc] f32
+  float* lg = (float*)smem;
+  float* lb = lg + (size_t)nch * VEC;
+  float* part = lb + (size_t)nch * VEC + slot * (RL * S);
+  float* stat = lb + (size_t)nch * VEC + SLOTS * (RL * S) + slot * 2 * npc;
   for (int c = threadIdx.x; c < nch; c += kSocThreads) {
-    u32x4 gv, bv;
-    if (s.gamma) gv = ld16((const char*)s.gamma + (int64_t)c * 16);
-    if (s.beta) bv = ld16((const char*)s.beta + (int64_t)c * 16);
-    if (!s.gamma) { float one[VEC]; for (int e = 0; e < VEC; ++e) one[e] = 1.f; gv = Elem<T>::pack(one); }
-    if (!s.beta) { float z[VEC]; for (int e = 0; e < VEC; ++e) z[e] = 0.f; bv = Elem<T>::pack(z); }
-    *(u32x4*)(lg + (size_t)c * 16) = gv;
-    *(u32x4*)(lb + (size_t)c * 16) = bv;
+    float g[VEC], b[VEC];
+    if (s.gamma) {
+      Elem<T>::unpack(ld16((const char*)s.gamma + (int64_t)c * 16), g);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) g[e] = 1.f;
+    }
+    if (s.beta) {
+      Elem<T>::unpack(ld16((const char*)s.beta + (int64_t)c * 16), b);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) b[e] = 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; e += 4) {
+      *(f32x4*)(lg + (size_t)c * VEC + e) = f32x4{g[e], g[e + 1], g[e + 2], g[e + 3]};
+      *(f32x4*)(lb + (size_t)c * VEC + e) = f32x4{b[e], b[e + 1], b[e + 2], b[e + 3]};
+    }
   }
   __syncthreads();
+  // row-local LDS ordering: a wave-local wait with one wave per row, else a workgroup barrier
+  auto row_sync = [&]() {
+    if constexpr (WPR == 1)
+      lds_wave_sync();
+    else
+      __syncthreads();
+  };
 
-  // per-lane static data: piece of each owned chunk, its 1/width, the lane's runs
-  int pc[STEPS];
-  float invw[STEPS];
+  const int cbase = wr * 64 * S;  // first chunk of this wave's part of the row
+  const int ls = wr * 64 + lane;  // lane index within the row
+  const int run0 = ls * S;        // this lane's reduction run
+  // Per-lane static data: the piece of each chunk this lane holds and of each
+  // chunk of its reduction run, a byte each.
+  uint32_t pc[PACKS], rp[PACKS];
 #pragma unroll
-  for (int j = 0; j < STEPS; ++j) {
-    const int c = j * 64 + lane;
-    pc[j] = c < nch ? s.chunk_piece[c] : 0;
-    invw[j] = c < nch ? s.pieces[pc[j]].inv_width : 0.f;
+  for (int k = 0; k < PACKS; ++k) { pc[k] = 0u; rp[k] = 0u; }
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    const int c = cbase + j * 64 + lane, cr = run0 + j;
+    pc[j >> 2] |= (uint32_t)(c < nch ? s.chunk_piece[c] : 0) << (8 * (j & 3));
+    rp[j >> 2] |= (uint32_t)(cr < nch ? s.chunk_piece[cr] : 0) << (8 * (j & 3));
   }
-  SocTask tk0 = {0, 0, 0, 0}, tk1 = {0, 0, 0, 0};
-  if (lane < s.n_tasks) tk0 = s.tasks[lane];
-  if (lane + 64 < s.n_tasks) tk1 = s.tasks[lane + 64];
+  auto piece_of = [](const uint32_t* pk, int j) { return (int)((pk[j >> 2] >> (8 * (j & 3))) & 0xffu); };
+  // the pieces this lane finalises: ls, ls + RL (n_pieces <= 128)
+  const float iw0 = ls < npc ? s.pieces[ls].inv_width : 0.f;
+  const float iw1 = ls + RL < npc ? s.pieces[ls + RL].inv_width : 0.f;
 
-  for (int row = blockIdx.x * 4 + wave; row < s.rows; row += gridDim.x * 4) {
-    const char* xr = (const char*)s.in + (int64_t)row * s.ldin * sizeof(T);
-    char* yr = (char*)s.out + (int64_t)row * s.ldout * sizeof(T);
-    float x[STEPS][VEC];
+  // Reduce per-chunk partials t[] of the slot's row into per-piece accumulators acc[] (LDS).
+  auto piece_reduce = [&](const float* t, float* acc) {
 #pragma unroll
-    for (int j = 0; j < STEPS; ++j) {
-      const int c = j * 64 + lane;
-      if (c < nch) {
-        Elem<T>::unpack(ld16_nt(xr + (int64_t)c * 16), x[j]);
+    for (int j = 0; j < S; ++j) {
+      const int c = cbase + j * 64 + lane;
+      if (FULL || c < nch) part[c] = t[j];
+    }
+    row_sync();
+    if (run0 < nch) {
+      float run[S];
+      if constexpr (S % 4 == 0) {
+#pragma unroll
+        for (int k = 0; k < S / 4; ++k) {
+          const f32x4 v = *(const f32x4*)(part + run0 + 4 * k);
+          run[4 * k + 0] = v[0];
+          run[4 * k + 1] = v[1];
+          run[4 * k + 2] = v[2];
+          run[4 * k + 3] = v[3];
+        }
       } else {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) x[j][e] = 0.f;
+        for (int i = 0; i < S; ++i) run[i] = part[run0 + i];
       }
+      int cur = piece_of(rp, 0);
+      float a = 0.f;
+#pragma unroll
+      for (int i = 0; i < S; ++i) {
+        if (FULL || run0 + i < nch) {
+          const int p = piece_of(rp, i);
+          if (p != cur) {
+            atomicAdd(&acc[cur], a);
+            a = 0.f;
+            cur = p;
+          }
+          a += run[i];
+        }
+      }
+      atomicAdd(&acc[cur], a);
     }
-    float mean[STEPS], rstd[STEPS];
+    row_sync();
+  };
+
+  u32x4 raw[S];
+  auto fetch = [&](int row) {
+    const char* xr = (const char*)s.in + (int64_t)row * s.ldin * sizeof(T);
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const int c = cbase + j * 64 + lane;
+      raw[j] = (FULL || c < nch) ? ld16_nt(xr + c * 16) : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  const int row_step = gridDim.x * SLOTS;
+  int r0 = blockIdx.x * SLOTS;
+  if (r0 + slot < s.rows) fetch(r0 + slot);
+  // every wave of the block runs the same number of iterations (barriers inside when WPR > 1)
+  for (; r0 < s.rows; r0 += row_step) {
+    const int row = r0 + slot;
+    const bool valid = row < s.rows;
+    if (WPR == 1 && !valid) break;
+    u32x4 cur[S];
+#pragma unroll
+    for (int j = 0; j < S; ++j) cur[j] = raw[j];
+    if (row + row_step < s.rows) fetch(row + row_step);
+    char* yr = (char*)s.out + (int64_t)row * s.ldout * sizeof(T);
     if (s.apply_ln) {
-      for (int p = lane; p < 2 * npc; p += 64) stat[p] = 0.f;
-      // pass 1: sums
+      float t[S];
+      // pass 1: piece means
+      for (int p = ls; p < 2 * npc; p += RL) stat[p] = 0.f;
 #pragma unroll
-      for (int j = 0; j < STEPS; ++j) {
-        const int c = j * 64 + lane;
-        float t = 0.f;
+      for (int j = 0; j < S; ++j) t[j] = chunk_sum<T>(cur[j]);
+      piece_reduce(t, stat);
+      if (ls < npc) stat[ls] *= iw0;
+      if (ls + RL < npc) stat[ls + RL] *= iw1;
+      row_sync();
+      // pass 2: centred values, their squares -> 1/sqrt(var + eps)
+      float dx[S][VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) t += x[j][e];
-        if (c < nch) part[c] = t;
-      }
-      lds_wave_sync();
-      {
-        float a = 0.f, b2 = 0.f;
-        for (int c = tk0.c0; c < tk0.c1; ++c) a += part[c];
-        for (int c = tk1.c0; c < tk1.c1; ++c) b2 += part[c];
-        if (tk0.c1 > tk0.c0) atomicAdd(&stat[tk0.piece], a);
-        if (tk1.c1 > tk1.c0) atomicAdd(&stat[tk1.piece], b2);
-      }
-      lds_wave_sync();
-#pragma unroll
-      for (int j = 0; j < STEPS; ++j) mean[j] = stat[pc[j]] * invw[j];
-      // pass 2: centred squares
-#pragma unroll
-      for (int j = 0; j < STEPS; ++j) {
-        const int c = j * 64 + lane;
-        float t = 0.f;
+      for (int j = 0; j < S; ++j) {
+        const float m = stat[piece_of(pc, j)];
+        Elem<T>::unpack(cur[j], dx[j]);
+        float a = 0.f;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          const float u = x[j][e] - mean[j];
-          t += u * u;
+          dx[j][e] -= m;
+          a += dx[j][e] * dx[j][e];
         }
-        if (c < nch) part[c] = t;
+        t[j] = a;
       }
-      lds_wave_sync();
-      {
-        float a = 0.f, b2 = 0.f;
-        for (int c = tk0.c0; c < tk0.c1; ++c) a += part[c];
-        for (int c = tk1.c0; c < tk1.c1; ++c) b2 += part[c];
-        if (tk0.c1 > tk0.c0) atomicAdd(&stat[npc + tk0.piece], a);
-        if (tk1.c1 > tk1.c0) atomicAdd(&stat[npc + tk1.piece], b2);
-      }
-      lds_wave_sync();
+      piece_reduce(t, stat + npc);
+      if (ls < npc) stat[npc + ls] = __builtin_amdgcn_rsqf(stat[npc + ls] * iw0 + s.eps);
+      if (ls + RL < npc) stat[npc + ls + RL] = __builtin_amdgcn_rsqf(stat[npc + ls + RL] * iw1 + s.eps);
+      row_sync();
+      // normalise: y = (x - mean) * (rstd * gamma) + beta, then the activation
+      if (valid) {
 #pragma unroll
-      for (int j = 0; j < STEPS; ++j) rstd[j] = __builtin_amdgcn_rsqf(stat[npc + pc[j]] * invw[j] + s.eps);
-      lds_wave_sync();  // statistics read before the next row clears them
-    }
+        for (int j = 0; j < S; ++j) {
+          const int c = cbase + j * 64 + lane;
+          if (FULL || c < nch) {
+            const float rs = stat[npc + piece_of(pc, j)];
+            float o[VEC];
 #pragma unroll
-    for (int j = 0; j < STEPS; ++j) {
-      const int c = j * 64 + lane;
-      if (c < nch) {
-        float o[VEC];
-        if (s.apply_ln) {
-          float g[VEC], b[VEC];
-          Elem<T>::unpack(*(const u32x4*)(lg + (size_t)c * 16), g);
-          Elem<T>::unpack(*(const u32x4*)(lb + (size_t)c * 16), b);
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>((x[j][e] - mean[j]) * rstd[j] * g[e] + b[e]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>(x[j][e]);
+            for (int e = 0; e < VEC; e += 4) {
+              const f32x4 g = *(const f32x4*)(lg + (size_t)c * VEC + e);
+              const f32x4 b = *(const f32x4*)(lb + (size_t)c * VEC + e);
+              o[e + 0] = act_apply<ACT>(dx[j][e + 0] * (rs * g[0]) + b[0]);
+              o[e + 1] = act_apply<ACT>(dx[j][e + 1] * (rs * g[1]) + b[1]);
+              o[e + 2] = act_apply<ACT>(dx[j][e + 2] * (rs * g[2]) + b[2]);
+              o[e + 3] = act_apply<ACT>(dx[j][e + 3] * (rs * g[3]) + b[3]);
+            }
+            st16_nt(yr + c * 16, Elem<T>::pack(o));
+          }
         }
-        st16_nt(yr + (int64_t)c * 16, Elem<T>::pack(o));
+      }
+      row_sync();  // statistics read before the next row clears them
+    } else if (valid) {
+#pragma unroll
+      for (int j = 0; j < S; ++j) {
+        const int c = cbase + j * 64 + lane;
+        if (FULL || c < nch) {
+          float x[VEC], o[VEC];
+          Elem<T>::unpack(cur[j], x);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>(x[e]);
+          st16_nt(yr + c * 16, Elem<T>::pack(o));
+        }
       }
     }
   }
@@ -332,17 +420,91 @@ hipError_t pointwise_launch(optimus_dtype dt, optimus_act act, const DevRows* de
   return hipGetLastError();
 }
 
+template <typename T, int ACT, int S, int WPR, bool FULL>
+static const void* soc_kernel_ptr() {
+  return (const void*)split_op_cat_kernel<T, ACT, S, WPR, FULL>;
+}
+
+struct SocShape {
+  int steps, wpr;
+  bool full;
+  size_t smem;
+};
+
+// Waves per row: OPTIMUS_SOC_WPR=<1|2|4> pins it (tuning); otherwise 1 (no workgroup barriers).
+static int soc_wpr() {
+  const char* f = getenv("OPTIMUS_SOC_WPR");
+  if (f && (f[0] == '1' || f[0] == '2' || f[0] == '4') && f[1] == 0) return f[0] - '0';
+  return 1;
+}
+
+static SocShape soc_shape(int32_t nchunks, int32_t n_pieces, optimus_dtype dt) {
+  int wpr = soc_wpr();
+  // at most 8 chunks per lane in registers
+  while (wpr < 4 && (nchunks + 64 * wpr - 1) / (64 * wpr) > 8) wpr *= 2;
+  const int per = (nchunks + 64 * wpr - 1) / (64 * wpr);
+  const int st = per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : 8;
+  const int vec = dt == OPTIMUS_F32 ? 4 : 8;
+  const int slots = 4 / wpr;
+  return SocShape{st, wpr, nchunks == 64 * wpr * st,
+                  (size_t)nchunks * vec * 4 * 2 + (size_t)slots * 64 * wpr * st * 4 + (size_t)slots * 2 * n_pieces * 4};
+}
+
+template <typename T, int ACT, int WPR>
+static const void* soc_kernel_w(const SocShape& sh) {
+  switch (sh.steps) {
+    case 1: return sh.full ? soc_kernel_ptr<T, ACT, 1, WPR, true>() : soc_kernel_ptr<T, ACT, 1, WPR, false>();
+    case 2: return sh.full ? soc_kernel_ptr<T, ACT, 2, WPR, true>() : soc_kernel_ptr<T, ACT, 2, WPR, false>();
+    case 4: return sh.full ? soc_kernel_ptr<T, ACT, 4, WPR, true>() : soc_kernel_ptr<T, ACT, 4, WPR, false>();
+    default: return sh.full ? soc_kernel_ptr<T, ACT, 8, WPR, true>() : soc_kernel_ptr<T, ACT, 8, WPR, false>();
+  }
+}
+
 template <typename T, int ACT>
-static hipError_t soc_launch_t(const DevSoc* soc, int32_t nchunks, int32_t n_pieces, int32_t grid, hipStream_t stream) {
-  const size_t smem = (size_t)nchunks * 32 + (size_t)4 * nchunks * 4 + (size_t)4 * 2 * n_pieces * 4;
-  const int steps = (nchunks + 63) / 64;
-  if (steps <= 4)
-    hipLaunchKernelGGL((split_op_cat_kernel<T, ACT, 4>), dim3(grid), dim3(kSocThreads), smem, stream, soc);
-  else if (steps <= 8)
-    hipLaunchKernelGGL((split_op_cat_kernel<T, ACT, 8>), dim3(grid), dim3(kSocThreads), smem, stream, soc);
-  else
-    hipLaunchKernelGGL((split_op_cat_kernel<T, ACT, 16>), dim3(grid), dim3(kSocThreads), smem, stream, soc);
-  return hipGetLastError();
+static const void* soc_kernel_for(const SocShape& sh) {
+  if (sh.wpr == 1) return soc_kernel_w<T, ACT, 1>(sh);
+  if (sh.wpr == 2) return soc_kernel_w<T, ACT, 2>(sh);
+  return soc_kernel_w<T, ACT, 4>(sh);
+}
+
+static const void* soc_kernel(optimus_dtype dt, optimus_act act, const SocShape& sh) {
+  if (dt == OPTIMUS_BF16) {
+    switch (act) {
+      case OPTIMUS_ACT_NONE: return soc_kernel_for<bf16_t, 0>(sh);
+      case OPTIMUS_ACT_RELU: return soc_kernel_for<bf16_t, 1>(sh);
+      case OPTIMUS_ACT_SIGMOID: return soc_kernel_for<bf16_t, 2>(sh);
+      case OPTIMUS_ACT_TANH: return soc_kernel_for<bf16_t, 3>(sh);
+      case OPTIMUS_ACT_SILU: return soc_kernel_for<bf16_t, 4>(sh);
+      default: return nullptr;
+    }
+  }
+  switch (act) {
+    case OPTIMUS_ACT_NONE: return soc_kernel_for<float, 0>(sh);
+    case OPTIMUS_ACT_RELU: return soc_kernel_for<float, 1>(sh);
+    case OPTIMUS_ACT_SIGMOID: return soc_kernel_for<float, 2>(sh);
+    case OPTIMUS_ACT_TANH: return soc_kernel_for<float, 3>(sh);
+    case OPTIMUS_ACT_SILU: return soc_kernel_for<float, 4>(sh);
+    default: return nullptr;
+  }
+}
+
+// Kernels whose dynamic LDS exceeds the 64 KB default need the limit raised once.
+static hipError_t soc_allow_lds(const void* k, size_t smem) {
+  if (smem <= 65536) return hipSuccess;
+  return hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+}
+
+int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces) {
+  const SocShape sh = soc_shape(nchunks, n_pieces, dt);
+  const void* k = soc_kernel(dt, act, sh);
+  int n = 0;
+  if (k && soc_allow_lds(k, sh.smem) != hipSuccess) return 1;
+  if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kSocThreads, sh.smem) != hipSuccess || n < 1) n = 1;
+  return n;
+}
+
+int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces) {
+  return 4 / soc_shape(nchunks, n_pieces, dt).wpr;
 }
 
 hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t rows, int32_t nchunks,
@@ -350,12 +512,13 @@ hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int3
   (void)rows;
   (void)n_tasks;
   if (nchunks <= 0 || nchunks > kSocMaxChunks || n_pieces > kSocMaxPieces) return hipErrorInvalidValue;
-  if (dt == OPTIMUS_BF16) {
-    OPTIMUS_ACT_SWITCH(act, return soc_launch_t<bf16_t, A>(soc, nchunks, n_pieces, grid, stream));
-  } else {
-    OPTIMUS_ACT_SWITCH(act, return soc_launch_t<float, A>(soc, nchunks, n_pieces, grid, stream));
-  }
-  return hipSuccess;
+  const SocShape sh = soc_shape(nchunks, n_pieces, dt);
+  const void* k = soc_kernel(dt, act, sh);
+  if (!k) return hipErrorInvalidValue;
+  hipError_t e = soc_allow_lds(k, sh.smem);
+  if (e != hipSuccess) return e;
+  void* args[] = {(void*)&soc};
+  return hipLaunchKernel(k, dim3(grid), dim3(kSocThreads), args, sh.smem, stream);
 }
 
 }  // namespace optimus

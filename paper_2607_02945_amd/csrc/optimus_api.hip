@@ -324,7 +324,7 @@ static DevRows make_rows(const void* x, int64_t ldx, void* y, int64_t ldy, const
   r.lanes = 0;
   if (vec) {
     if (layernorm) {
-      const int maxc = 4;  // chunks per lane held in registers by the LayerNorm kernel
+      const int maxc = kLnChunksPerLane;  // chunks per lane held in registers by the LayerNorm kernel
       if (cpr <= 64 * maxc) {
         r.vec = 1;
         r.lanes = pow2ceil((cpr + maxc - 1) / maxc);
@@ -419,8 +419,7 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
   hp.g_tiles_off = hp.blob.add(tiles.data(), tiles.size() * sizeof(GemmTile));
   hp.g_num_tiles = (int32_t)tiles.size();
   // workgroups resident per CU for each variant (LDS / register bound)
-  static const int occ[] = {4, 2, 1, 4};
-  const int64_t cap = (int64_t)device_cu_count() * occ[hp.gcfg.variant];
+  const int64_t cap = (int64_t)device_cu_count() * hp.gcfg.occ;
   int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
   if (grid >= 8) grid -= grid % 8;
   hp.g_grid = (int32_t)std::max<int64_t>(1, grid);
@@ -553,7 +552,10 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
     hp.soc_nchunks = (int32_t)nchunks;
     hp.soc_pieces = n;
     hp.soc_tasks = (int32_t)tasks.size();
-    hp.soc_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((rows + 3) / 4, (int64_t)device_cu_count() * 4));
+    // persistent grid: exactly the workgroups that fit at once, each wave walking rows
+    const int64_t resident = (int64_t)device_cu_count() * soc_blocks_per_cu(dt, d->act, (int32_t)nchunks, n);
+    const int rpb = soc_rows_per_block(dt, (int32_t)nchunks, n);
+    hp.soc_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((rows + rpb - 1) / rpb, resident));
     hp.work_items = rows;
     hp.grid = hp.soc_grid;
     hp.block = kSocThreads;

@@ -84,6 +84,7 @@ struct GemmConfig {
   int bm, bn;          // tile
   int variant;         // index into the kernel table
   int threads;
+  int occ;             // workgroups resident per CU
   const char* name;
 };
 
@@ -92,18 +93,27 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream);
 
 constexpr int kRowThreads = 256;
+#ifndef OPTIMUS_LN_CHUNKS_PER_LANE
+#define OPTIMUS_LN_CHUNKS_PER_LANE 2
+#endif
+// 16-byte chunks of a row each lane of the LayerNorm kernel holds in registers
+// (rows up to 64 * this many chunks take the register path).
+constexpr int kLnChunksPerLane = OPTIMUS_LN_CHUNKS_PER_LANE;
 hipError_t layernorm_launch(optimus_dtype dt, optimus_act act, const DevRows* descs, const RowTile* tiles,
                             int32_t num_tiles, int32_t grid, hipStream_t stream);
 hipError_t pointwise_launch(optimus_dtype dt, optimus_act act, const DevRows* descs, const RowTile* tiles,
                             int32_t num_tiles, int32_t grid, hipStream_t stream);
 
 constexpr int kSocThreads = 256;
-constexpr int kSocMaxChunks = 1024;  // 16-byte chunks per row held in registers by one wave (<= 64 * kSocSteps)
-constexpr int kSocSteps = 16;
+constexpr int kSocMaxChunks = 1024;  // 16-byte chunks per row held in registers by two waves (8 per lane)
 constexpr int kSocMaxPieces = 256;
 constexpr int kSocMaxTasks = 128;    // two per lane
 hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t rows, int32_t nchunks,
                       int32_t n_pieces, int32_t n_tasks, int32_t grid, hipStream_t stream);
+// Workgroups of the fused split-op-cat kernel resident per CU (occupancy query)
+// and rows one workgroup works on at a time.
+int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces);
+int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces);
 
 int device_cu_count();
 
