@@ -93,6 +93,70 @@ __device__ __forceinline__ u32x4 load_chunk(const void* base, int64_t ld, int ro
   return v;
 }
 
+// Epilogue shared by the GEMM kernels: bias + activation + rounding into the
+// LDS staging tile sC ([BM][LDC], reusing the operand area), then whole
+// 16-byte pieces of y rows leave in coalesced stores, masked at the M/N tails.
+// acc[i][j][r] holds y row m = wm*TM + 32 i + (lane % 32) and column
+// n = wn*TN + 32 j + 8 (r / 4) + 4 (lane / 32) + (r % 4) (A operand = weights).
+template <typename T, int BM, int BN, int WM, int WN, int LDC, int ACT>
+__device__ __forceinline__ void gemm_epilogue(const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], T* sC,
+                                              const float* sBias, const DevLinear& d, int m0, int n0, int Mr,
+                                              int Nr) {
+  constexpr int VEC = Elem<T>::VEC, NT = WM * WN * 64, TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN, l32 = lane & 31, lh = lane >> 5;
+  // One base address per lane and compile-time offsets: per-(i, j, q)
+  // addresses would otherwise be kept live across the whole tile loop.
+  T* const cbase = sC + (wm * TM + l32) * LDC + wn * TN + lh * 4;
+  const float* const bbase = sBias + wn * TN + lh * 4;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 bv = *(const f32x4*)(bbase + j * 32 + q * 8);
+        float o[4];
+        o[0] = act_apply<ACT>(acc[i][j][q * 4 + 0] + bv.x);
+        o[1] = act_apply<ACT>(acc[i][j][q * 4 + 1] + bv.y);
+        o[2] = act_apply<ACT>(acc[i][j][q * 4 + 2] + bv.z);
+        o[3] = act_apply<ACT>(acc[i][j][q * 4 + 3] + bv.w);
+        T* const cp = cbase + i * 32 * LDC + j * 32 + q * 8;
+        if constexpr (sizeof(T) == 2) {
+          u32x2 pk = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+          *(u32x2*)cp = pk;
+        } else {
+          *(f32x4*)cp = f32x4{o[0], o[1], o[2], o[3]};
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const bool vout = (d.vec & 2) != 0;
+  constexpr int SCPR = BN / VEC;  // 16-byte pieces per staged row
+  static_assert(NT % SCPR == 0 && (BM * SCPR) % NT == 0, "store phase must divide evenly");
+  constexpr int RSTEP = NT / SCPR;  // rows covered per pass of the workgroup
+  const int r0 = tid / SCPR, n = (tid % SCPR) * VEC;
+  const T* sp = sC + r0 * LDC + n;
+  T* yp = (T*)d.y + (int64_t)(m0 + r0) * d.ldy + n0 + n;
+  const int64_t ystep = (int64_t)RSTEP * d.ldy;
+  if (n < Nr) {
+    for (int row = r0; row < BM && row < Mr; row += RSTEP, sp += RSTEP * LDC, yp += ystep) {
+      if (vout && n + VEC <= Nr) {
+        st16(yp, *(const u32x4*)sp);
+      } else {
+        for (int e = 0; e < VEC && n + e < Nr; ++e) {
+          if constexpr (sizeof(T) == 2)
+            ((OPTIMUS_GLOBAL uint16_t*)yp)[e] = ((const uint16_t*)sp)[e];
+          else
+            ((OPTIMUS_GLOBAL float*)yp)[e] = ((const float*)sp)[e];
+        }
+      }
+    }
+  }
+}
+
 template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES, int ACT>
 __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLinear* __restrict__ descs,
                                                                    const GemmTile* __restrict__ tiles,
@@ -201,56 +265,303 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       }
     }
 
-    // ---- epilogue: bias + activation + rounding into the LDS staging tile.
-    // acc[i][j][r] is y row m = wm*TM + 32 i + l32, column
-    // n = wn*TN + 32 j + 8 (r / 4) + 4 lh + (r % 4).
-#pragma unroll
-    for (int i = 0; i < S::FM; ++i) {
-      const int m = wm * S::TM + i * 32 + l32;
-#pragma unroll
-      for (int j = 0; j < S::FN; ++j) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int n = wn * S::TN + j * 32 + q * 8 + lh * 4;
-          const f32x4 bv = *(const f32x4*)(sBias + n);
-          float o[4];
-          o[0] = act_apply<ACT>(acc[i][j][q * 4 + 0] + bv.x);
-          o[1] = act_apply<ACT>(acc[i][j][q * 4 + 1] + bv.y);
-          o[2] = act_apply<ACT>(acc[i][j][q * 4 + 2] + bv.z);
-          o[3] = act_apply<ACT>(acc[i][j][q * 4 + 3] + bv.w);
-          if constexpr (sizeof(T) == 2) {
-            u32x2 pk = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-            *(u32x2*)(sC + m * S::LDC + n) = pk;
-          } else {
-            *(f32x4*)(sC + m * S::LDC + n) = f32x4{o[0], o[1], o[2], o[3]};
-          }
-        }
-      }
-    }
-    __syncthreads();
-    // ---- store: whole 16-byte pieces of y rows
-    const bool vout = (d.vec & 2) != 0;
-    constexpr int SCPR = BN / VEC;
-#pragma unroll
-    for (int i = 0; i < BM * SCPR / NT; ++i) {
-      const int idx = tid + i * NT, row = idx / SCPR, c = idx % SCPR;
-      const int n = c * VEC;
-      if (row < Mr && n < Nr) {
-        T* yp = (T*)d.y + (int64_t)(m0 + row) * d.ldy + n0 + n;
-        const T* sp = sC + row * S::LDC + n;
-        if (vout && n + VEC <= Nr) {
-          st16(yp, *(const u32x4*)sp);
-        } else {
-          for (int e = 0; e < VEC && n + e < Nr; ++e) {
-            if constexpr (sizeof(T) == 2)
-              ((OPTIMUS_GLOBAL uint16_t*)yp)[e] = ((const uint16_t*)sp)[e];
-            else
-              ((OPTIMUS_GLOBAL float*)yp)[e] = ((const float*)sp)[e];
-          }
-        }
-      }
-    }
+    gemm_epilogue<T, BM, BN, WM, WN, S::LDC, ACT>(acc, sC, sBias, d, m0, n0, Mr, Nr);
     __syncthreads();  // staging and bias reads done before the next tile overwrites them
+  }
+}
+
+// ===================================================================== direct-to-LDS variant
+// bf16 members whose x and w rows are 16-byte aligned with K % 8 == 0. The K
+// loop stages BK = 64 columns of the x and w tiles straight from global memory
+// into LDS with global_load_lds_dwordx4 (no register staging, no LDS write
+// instructions), two stages deep: the loads of step k+1 fly while step k is
+// multiplied. Each DMA instruction of a wave fills 1 KB of LDS = 8 staged rows
+// of 128 bytes; lane l brings the chunk that belongs at byte 16 l of it. A row
+// keeps its 8 chunks, XOR-swizzled by (row / 2) mod 8 so that the 16 lanes of
+// an MFMA operand read (16 consecutive rows, one chunk) hit distinct LDS banks.
+// Rows past M and chunks past K load from a zero page. One step further ahead,
+// every 128-byte line of the tiles of step k+2 is touched by a DMA into a
+// 1 KB sink, so that step's loads find their lines in L2 instead of waiting on
+// HBM.
+static __device__ __align__(16) const uint32_t kZeroChunk[4] = {0u, 0u, 0u, 0u};
+
+__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
+  // M0 holds the LDS destination of the wave; the compiler is not told that
+  // this writes LDS, so the K loop's waits are placed by hand below.
+  __asm__ volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                   :
+                   : "v"(gptr), "s"(lds_addr)
+                   : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  __asm__ volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
+template <int BM, int BN, int WM, int WN>
+struct DmaShape {
+  static constexpr int BK = 64, NW = WM * WN, NT = NW * 64;
+  static constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
+  static constexpr int XBYTES = BM * 128, WBYTES = BN * 128, STAGE = XBYTES + WBYTES;
+  static constexpr int XI = BM / (8 * NW), WI = BN / (8 * NW);  // DMA instructions per wave per stage
+  static constexpr int PF = (BM + BN + 64 * NW - 1) / (64 * NW);  // L2 prefetch instructions per wave per stage
+  static constexpr int LDC = BN + 8;
+  static constexpr size_t AB = 2 * (size_t)STAGE, CB = (size_t)BM * LDC * 2;
+  static constexpr size_t MAIN = AB > CB ? AB : CB;
+  static constexpr size_t SINK = MAIN + BN * sizeof(float);  // 1 KB the prefetch loads land in
+  static constexpr size_t LDS_BYTES = SINK + 1024;
+  static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "whole DMA instructions per wave");
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
+};
+
+template <int BM, int BN, int WM, int WN, int ACT>
+__global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const DevLinear* __restrict__ descs,
+                                                                       const GemmTile* __restrict__ tiles,
+                                                                       int32_t num_tiles) {
+  using S = DmaShape<BM, BN, WM, WN>;
+  constexpr int NW = S::NW;
+  extern __shared__ __align__(16) char smem[];
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+  bf16_t* sC = (bf16_t*)smem;
+  float* sBias = (float*)(smem + S::MAIN);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN, l32 = lane & 31, lh = lane >> 5;
+  const int lrow = lane >> 3, lslot = lane & 7;  // this lane's place in a DMA instruction's 8 x 8 chunks
+
+  int vb = blockIdx.x;
+  if ((gridDim.x & 7) == 0) vb = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+
+  for (int t = vb; t < num_tiles; t += gridDim.x) {
+    const GemmTile tile = tiles[t];
+    if (tile.member < 0) continue;
+    const DevLinear d = descs[tile.member];
+    const int m0 = tile.mb * BM, n0 = tile.nb * BN;
+    const int Mr = d.M - m0, Nr = d.N - n0, K = d.K;
+    const bf16_t* xb = (const bf16_t*)d.x + (int64_t)m0 * d.ldx;
+    const bf16_t* wb = (const bf16_t*)d.w + (int64_t)n0 * d.ldw;
+    if (tid < BN) sBias[tid] = (d.bias && tid < Nr) ? Elem<bf16_t>::load1(d.bias, n0 + tid) : 0.f;
+
+    f32x16 acc[S::FM][S::FN];
+#pragma unroll
+    for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // This lane's first staged row of x and w and its (swizzled) chunk; each
+    // further DMA instruction of the wave is NW * 8 rows further down. The
+    // swizzle depends on (row / 2) mod 8, which is the same for all of them.
+    const int lr = wave * 8 + lrow;
+    const int kch = (lslot ^ swz(lr)) << 3;
+    const bf16_t* xl = xb + (int64_t)lr * d.ldx + kch;
+    const bf16_t* wl = wb + (int64_t)lr * d.ldw + kch;
+    const int64_t xstep = (int64_t)NW * 8 * d.ldx, wstep = (int64_t)NW * 8 * d.ldw;
+    auto prefetch = [&](int k0) {
+      const uint32_t sink = lds_base + (uint32_t)S::SINK;
+#pragma unroll
+      for (int p = 0; p < S::PF; ++p) {
+        const int r = (p * NW + wave) * 64 + lane;  // x rows, then w rows
+        const void* src = kZeroChunk;
+        if (k0 < K) {
+          if (r < BM) {
+            if (r < Mr) src = xb + (int64_t)r * d.ldx + k0;
+          } else if (r - BM < Nr && r < BM + BN) {
+            src = wb + (int64_t)(r - BM) * d.ldw + k0;
+          }
+        }
+        lds_dma16(src, sink);
+      }
+    };
+    auto issue = [&](int stage, int k0) {
+      const uint32_t sb = lds_base + stage * S::STAGE + wave * 8 * 128;
+      const bool kin = k0 + kch < K;
+#pragma unroll
+      for (int q = 0; q < S::XI; ++q) {
+        const bool in = kin && lr + q * NW * 8 < Mr;
+        lds_dma16(in ? (const void*)(xl + q * xstep + k0) : (const void*)kZeroChunk, sb + q * NW * 8 * 128);
+      }
+#pragma unroll
+      for (int q = 0; q < S::WI; ++q) {
+        const bool in = kin && lr + q * NW * 8 < Nr;
+        lds_dma16(in ? (const void*)(wl + q * wstep + k0) : (const void*)kZeroChunk,
+                  sb + S::XBYTES + q * NW * 8 * 128);
+      }
+    };
+    // K step: the fragments of k-chunk kc + 1 are read from LDS while the
+    // MFMAs of kc run (two fragment sets); scheduling barriers keep the
+    // compiler from hoisting every read of the step up front (which would
+    // need four sets of fragment registers).
+    auto compute = [&](int stage) {
+      const char* sx = smem + stage * S::STAGE;
+      const char* sw = sx + S::XBYTES;
+      u32x4 a[2][S::FN], b[2][S::FM];
+      auto frag = [&](int kc, int set) {
+        const int lc = kc * 2 + lh;
+#pragma unroll
+        for (int j = 0; j < S::FN; ++j) {
+          const int row = wn * S::TN + j * 32 + l32;
+          a[set][j] = *(const u32x4*)(sw + row * 128 + ((lc ^ swz(row)) << 4));
+        }
+#pragma unroll
+        for (int i = 0; i < S::FM; ++i) {
+          const int row = wm * S::TM + i * 32 + l32;
+          b[set][i] = *(const u32x4*)(sx + row * 128 + ((lc ^ swz(row)) << 4));
+        }
+      };
+      frag(0, 0);
+#pragma unroll
+      for (int kc = 0; kc < S::BK / 16; ++kc) {
+        if (kc + 1 < S::BK / 16) frag(kc + 1, (kc + 1) & 1);
+#pragma unroll
+        for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < S::FN; ++j) Mfma<bf16_t>::run(a[kc & 1][j], b[kc & 1][i], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+
+    const int nk = (K + S::BK - 1) / S::BK;
+    issue(0, 0);
+    prefetch(S::BK);
+    for (int kb = 0; kb < nk; ++kb) {
+      if (kb + 1 < nk) {
+        issue((kb + 1) & 1, (kb + 1) * S::BK);
+        prefetch((kb + 2) * S::BK);
+        // this wave's loads of step kb have landed; the two prefetch groups and
+        // the loads of step kb + 1 issued after them may still be in flight
+        wait_vmcnt<S::XI + S::WI + 2 * S::PF>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      __syncthreads();  // ... and every other wave's
+      compute(kb & 1);
+      __syncthreads();  // step kb's stage is free for the loads of step kb + 2
+    }
+    gemm_epilogue<bf16_t, BM, BN, WM, WN, S::LDC, ACT>(acc, sC, sBias, d, m0, n0, Mr, Nr);
+    __syncthreads();  // staging and bias reads done before the next tile overwrites them
+  }
+}
+
+// ===================================================================== skinny members
+// bf16 members with N <= 64 and K <= 64, K % 8 == 0 (many tiny Linears on a
+// large batch): each is a stream of rows through a small weight matrix, bound
+// by HBM. Every wave works on its own item -- 256 rows of one member -- with no
+// workgroup barrier: it keeps the member's weight fragments and bias in
+// registers and streams the item's eight 32-row tiles with two tiles of x in
+// flight ahead of the one being multiplied; x fragments go straight from
+// global memory into MFMA operand registers (lane l holds row l % 32, k-chunk
+// l / 32 of each 16-wide k step) for v_mfma_f32_32x32x16_bf16, and each output
+// tile passes through a wave-private LDS staging tile so that rows leave in
+// whole 16-byte stores.
+#ifndef OPTIMUS_SKINNY_TILES
+#define OPTIMUS_SKINNY_TILES 2
+#endif
+constexpr int kSkinnyTiles = OPTIMUS_SKINNY_TILES;  // 32-row tiles per work item
+constexpr int kSkinnyRows = 32 * kSkinnyTiles;  // rows per work item
+constexpr int kSkinnyLdc = 72;                  // staging row (elements): 64 + 8
+#ifndef OPTIMUS_SKINNY_OCC
+#define OPTIMUS_SKINNY_OCC 4
+#endif
+
+template <int ACT>
+__global__ __launch_bounds__(256) void grouped_gemm_skinny_kernel(const DevLinear* __restrict__ descs,
+                                                                   const GemmTile* __restrict__ items,
+                                                                   int32_t num_items) {
+  __shared__ __align__(16) bf16_t stage[4][32 * kSkinnyLdc];
+  __shared__ __align__(16) float sbias[4][64];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l32 = lane & 31, lh = lane >> 5;
+  bf16_t* st = stage[wave];
+  float* sb = sbias[wave];
+  for (int it = blockIdx.x * 4 + wave; it < num_items; it += gridDim.x * 4) {
+    const GemmTile item = items[it];
+    if (item.member < 0) continue;
+    const DevLinear d = descs[item.member];
+    const int K = d.K, N = d.N;
+    const int r0 = item.mb * kSkinnyRows;
+    const int rows = min(kSkinnyRows, d.M - r0);
+    const int kfull = K >> 4;          // whole 16-wide k steps
+    const bool khalf = (K & 15) != 0;  // one more step with only k < K in the lower lane half
+    // x fragments of tile t: rows past the member are clamped to its last row
+    // (never stored); k steps past K are zero.
+    auto load_tile = [&](int t, u32x4 (&xf)[4]) {
+      const bf16_t* xr = (const bf16_t*)d.x + (int64_t)min(r0 + 32 * t + l32, d.M - 1) * d.ldx + 8 * lh;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s < kfull || (s == kfull && khalf && lh == 0))
+          xf[s] = ld16_nt(xr + 16 * s);
+        else
+          xf[s] = u32x4{0u, 0u, 0u, 0u};
+      }
+    };
+    u32x4 ring[3][4];
+    load_tile(0, ring[0]);
+    if (32 < rows) load_tile(1, ring[1]);
+    sb[lane] = (d.bias && lane < N) ? Elem<bf16_t>::load1(d.bias, lane) : 0.f;
+    // weights: a[f][s] = w[32 f + l32][16 s + 8 lh .. + 8], zero outside N x K
+    u32x4 a[2][4];
+    const bf16_t* wl = (const bf16_t*)d.w + (int64_t)l32 * d.ldw + 8 * lh;
+    const int64_t wf = (int64_t)32 * d.ldw;
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        a[f][s] = (32 * f + l32 < N && 16 * s + 8 * lh < K) ? ld16(wl + f * wf + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+    const bool vout = (d.vec & 2) && (N % 8 == 0);
+    const int cpr = (N + 7) / 8;
+    bf16_t* yl = (bf16_t*)d.y + (int64_t)(r0 + (lane >> 3)) * d.ldy + 8 * (lane & 7);
+    const int64_t y8 = (int64_t)8 * d.ldy;
+    lds_wave_sync();  // bias staged
+#pragma unroll
+    for (int t = 0; t < kSkinnyTiles; ++t) {
+      if (32 * t >= rows) break;
+      if (t + 2 < kSkinnyTiles && 32 * (t + 2) < rows) load_tile(t + 2, ring[(t + 2) % 3]);
+      const u32x4(&xf)[4] = ring[t % 3];
+      // both 32-column blocks are computed (the second is zero when N <= 32):
+      // the MFMAs cost nothing next to the row traffic
+      f32x16 acc0 = {}, acc1 = {};
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (16 * s < K) {
+          Mfma<bf16_t>::run(a[0][s], xf[s], acc0);
+          Mfma<bf16_t>::run(a[1][s], xf[s], acc1);
+        }
+      }
+      // acc_f[4 q + e] is y row 32 t + l32, column 32 f + 8 q + 4 lh + e
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 b0 = *(const f32x4*)(sb + 8 * q + 4 * lh);
+        const f32x4 b1 = *(const f32x4*)(sb + 32 + 8 * q + 4 * lh);
+        u32x2 p0 = {pack_bf16x2(act_apply<ACT>(acc0[4 * q + 0] + b0[0]), act_apply<ACT>(acc0[4 * q + 1] + b0[1])),
+                    pack_bf16x2(act_apply<ACT>(acc0[4 * q + 2] + b0[2]), act_apply<ACT>(acc0[4 * q + 3] + b0[3]))};
+        u32x2 p1 = {pack_bf16x2(act_apply<ACT>(acc1[4 * q + 0] + b1[0]), act_apply<ACT>(acc1[4 * q + 1] + b1[1])),
+                    pack_bf16x2(act_apply<ACT>(acc1[4 * q + 2] + b1[2]), act_apply<ACT>(acc1[4 * q + 3] + b1[3]))};
+        *(u32x2*)(st + l32 * kSkinnyLdc + 8 * q + 4 * lh) = p0;
+        *(u32x2*)(st + l32 * kSkinnyLdc + 32 + 8 * q + 4 * lh) = p1;
+      }
+      lds_wave_sync();
+      // 32 rows x N columns leave as 16-byte pieces: lane -> (row 8 p + lane / 8, piece lane % 8)
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int row = 8 * p + (lane >> 3), c = lane & 7;
+        if (32 * t + row < rows && c < cpr) {
+          bf16_t* yp = yl + (4 * t + p) * y8;
+          const bf16_t* sp = st + row * kSkinnyLdc + 8 * c;
+          if (vout) {
+            st16_nt(yp, *(const u32x4*)sp);
+          } else {
+#pragma unroll 1
+            for (int e = 0; e < 8 && 8 * c + e < N; ++e)
+              ((OPTIMUS_GLOBAL uint16_t*)yp)[e] = ((const uint16_t*)sp)[e];
+          }
+        }
+      }
+      lds_wave_sync();  // staging read before the next tile overwrites it
+    }
   }
 }
 
@@ -261,7 +572,10 @@ struct GemmVariant {
 };
 
 // 0: members with N, K <= 64 (one K step); 1: 128x128; 2: 256x256 (8 waves);
-// 3: fp32; 4: 256x256 (4 waves); 5: 256x128 (4 waves).
+// 3: fp32; 4: 256x256 (4 waves); 5: 256x128 (4 waves);
+// 6-9: direct-to-LDS (bf16, aligned rows, K % 8 == 0): 256x256 8 waves,
+// 256x256 4 waves, 256x128 4 waves, 128x128 4 waves;
+// 10: skinny members (bf16, N <= 64, K <= 64, K % 8 == 0, aligned rows).
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
     {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
@@ -269,8 +583,29 @@ static const GemmVariant kVariants[] = {
     {64, 64, 256, 4, "grouped_gemm_f32_64x64x32_w2x2_s2"},
     {256, 256, 256, 1, "grouped_gemm_bf16_256x256x64_w2x2_s2"},
     {256, 128, 256, 1, "grouped_gemm_bf16_256x128x64_w2x2_s2"},
+    {256, 256, 512, 1, "grouped_gemm_dma_bf16_256x256x64_w2x4"},
+    {256, 256, 256, 1, "grouped_gemm_dma_bf16_256x256x64_w2x2"},
+    {256, 128, 256, 1, "grouped_gemm_dma_bf16_256x128x64_w2x2"},
+    {128, 128, 256, 2, "grouped_gemm_dma_bf16_128x128x64_w2x2"},
+    {kSkinnyRows, 64, 256, OPTIMUS_SKINNY_OCC, "grouped_gemm_skinny_bf16"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
+
+static bool gemm_skinny_ok(const optimus_linear_desc* d, int32_t G) {
+  for (int g = 0; g < G; ++g) {
+    if (d[g].N > 64 || d[g].K > 64 || d[g].K % 8 || d[g].ldx % 8 || d[g].ldw % 8 || ((uintptr_t)d[g].x & 15) ||
+        ((uintptr_t)d[g].w & 15))
+      return false;
+  }
+  return true;
+}
+
+static bool gemm_dma_ok(const optimus_linear_desc* d, int32_t G) {
+  for (int g = 0; g < G; ++g) {
+    if (d[g].K % 8 || d[g].ldx % 8 || d[g].ldw % 8 || ((uintptr_t)d[g].x & 15) || ((uintptr_t)d[g].w & 15)) return false;
+  }
+  return true;
+}
 
 GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G) {
   int v;
@@ -287,14 +622,20 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     if (maxN <= 64 && maxK <= 64)
       v = 0;
     else if (tiles256 >= 2.0 * device_cu_count())
-      v = 2;
+      v = gemm_dma_ok(d, G) ? 6 : 2;
     else
       v = 1;
   }
-  // OPTIMUS_GEMM_VARIANT=<n> pins the bf16 tile shape (tests and tuning).
+  // OPTIMUS_GEMM_VARIANT=<n> pins the bf16 tile shape (tests and tuning); the
+  // direct-to-LDS variants need every member's x / w rows 16-byte aligned and K % 8 == 0.
   if (dt == OPTIMUS_BF16) {
     const char* f = getenv("OPTIMUS_GEMM_VARIANT");
-    if (f && f[0] >= '0' && f[0] <= '9' && f[1] == 0 && f[0] - '0' < kNumVariants && f[0] != '3') v = f[0] - '0';
+    char* end = nullptr;
+    const long want = f ? strtol(f, &end, 10) : -1;
+    if (f && end && *end == 0 && want >= 0 && want < kNumVariants && want != 3) {
+      const bool dma = want >= 6 && want <= 9, skinny = want == 10;
+      if ((!dma && !skinny) || (dma && gemm_dma_ok(d, G)) || (skinny && gemm_skinny_ok(d, G))) v = (int)want;
+    }
   }
   const GemmVariant& k = kVariants[v];
   return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
@@ -328,6 +669,34 @@ static hipError_t launch_shape(optimus_act act, const DevLinear* descs, const Ge
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WM, int WN>
+static hipError_t launch_dma(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
+                             hipStream_t stream) {
+  using S = DmaShape<BM, BN, WM, WN>;
+  const size_t smem = S::LDS_BYTES;
+#define OPTIMUS_DMA_LAUNCH(A)                                                                                      \
+  {                                                                                                                \
+    auto kfn = grouped_gemm_dma_kernel<BM, BN, WM, WN, A>;                                                         \
+    static bool attr_set = false;                                                                                  \
+    if (smem > 65536 && !attr_set) {                                                                               \
+      hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); \
+      if (e != hipSuccess) return e;                                                                               \
+      attr_set = true;                                                                                             \
+    }                                                                                                              \
+    hipLaunchKernelGGL(kfn, dim3(grid), dim3(S::NT), smem, stream, descs, tiles, n);                              \
+  }
+  switch (act) {
+    case OPTIMUS_ACT_NONE: OPTIMUS_DMA_LAUNCH(0); break;
+    case OPTIMUS_ACT_RELU: OPTIMUS_DMA_LAUNCH(1); break;
+    case OPTIMUS_ACT_SIGMOID: OPTIMUS_DMA_LAUNCH(2); break;
+    case OPTIMUS_ACT_TANH: OPTIMUS_DMA_LAUNCH(3); break;
+    case OPTIMUS_ACT_SILU: OPTIMUS_DMA_LAUNCH(4); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef OPTIMUS_DMA_LAUNCH
+  return hipGetLastError();
+}
+
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream) {
   if (num_tiles <= 0) return hipSuccess;
@@ -338,6 +707,21 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
     case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     case 4: return launch_shape<bf16_t, 256, 256, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     case 5: return launch_shape<bf16_t, 256, 128, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 6: return launch_dma<256, 256, 2, 4>(act, descs, tiles, num_tiles, grid, stream);
+    case 7: return launch_dma<256, 256, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 8: return launch_dma<256, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 9: return launch_dma<128, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 10: {
+      switch (act) {
+        case OPTIMUS_ACT_NONE: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<0>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
+        case OPTIMUS_ACT_RELU: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<1>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
+        case OPTIMUS_ACT_SIGMOID: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<2>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
+        case OPTIMUS_ACT_TANH: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<3>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
+        case OPTIMUS_ACT_SILU: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<4>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
+        default: return hipErrorInvalidValue;
+      }
+      return hipGetLastError();
+    }
     default: return hipErrorInvalidValue;
   }
 }
