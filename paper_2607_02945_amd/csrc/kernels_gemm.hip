@@ -273,24 +273,41 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
 // ===================================================================== direct-to-LDS variant
 // bf16 members whose x and w rows are 16-byte aligned with K % 8 == 0. The K
 // loop stages BK = 64 columns of the x and w tiles straight from global memory
-// into LDS with global_load_lds_dwordx4 (no register staging, no LDS write
-// instructions), two stages deep: the loads of step k+1 fly while step k is
-// multiplied. Each DMA instruction of a wave fills 1 KB of LDS = 8 staged rows
-// of 128 bytes; lane l brings the chunk that belongs at byte 16 l of it. A row
-// keeps its 8 chunks, XOR-swizzled by (row / 2) mod 8 so that the 16 lanes of
-// an MFMA operand read (16 consecutive rows, one chunk) hit distinct LDS banks.
-// Rows past M and chunks past K load from a zero page. One step further ahead,
-// every 128-byte line of the tiles of step k+2 is touched by a DMA into a
-// 1 KB sink, so that step's loads find their lines in L2 instead of waiting on
-// HBM.
-static __device__ __align__(16) const uint32_t kZeroChunk[4] = {0u, 0u, 0u, 0u};
+// into LDS with buffer_load_dwordx4 ... lds (no register staging, no LDS write
+// instructions), two stages deep. Each such instruction of a wave fills 1 KB
+// of LDS = 8 staged rows of 128 bytes; lane l brings the chunk that belongs at
+// byte 16 l of it. A row keeps its 8 chunks, XOR-swizzled by (row / 2) mod 8 so
+// that the 16 lanes of an MFMA operand read (16 consecutive rows, one chunk)
+// hit distinct LDS banks.
+//
+// Addressing goes through one buffer resource per operand and tile whose
+// record count ends at the tile's last valid row: rows past M (N) read as zero
+// in hardware, and chunks past K are sent to an offset beyond any record count.
+// The loads of step k+1 are issued in small groups between the MFMA groups of
+// step k, so the address unit works while the matrix cores do; one workgroup
+// barrier per step then makes step k+1's stage visible and frees step k's.
+// The K loop starts at a step that depends on the tile's coordinates, so the
+// tiles that share an x panel or a weight block (which run side by side on one
+// L2) do not request the same lines at the same moment.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
-  // M0 holds the LDS destination of the wave; the compiler is not told that
-  // this writes LDS, so the K loop's waits are placed by hand below.
-  __asm__ volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu));  // stride 0
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);                              // record count in bytes
+  r[3] = 0x00020000;                                                               // 32-bit data format
+  return r;
+}
+
+// One 16-byte chunk per lane into LDS at M0 + 16 * lane; an offset at or past
+// the record count returns zeros. The compiler is not told that this writes
+// LDS, so the K loop's waits are placed by hand.
+__device__ __forceinline__ void lds_dma16(const i32x4& rsrc, uint32_t voff, uint32_t lds_addr) {
+  __asm__ volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                    :
-                   : "v"(gptr), "s"(lds_addr)
+                   : "v"(voff), "s"(rsrc), "s"(lds_addr)
                    : "memory", "m0");
 }
 
@@ -301,21 +318,72 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
+constexpr uint32_t kOutOfRange = 0x80000000u;  // larger than any tile's record count
+
 template <int BM, int BN, int WM, int WN>
 struct DmaShape {
-  static constexpr int BK = 64, NW = WM * WN, NT = NW * 64;
+  static constexpr int BK = 64, KC = BK / 16, NW = WM * WN, NT = NW * 64;
   static constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
   static constexpr int XBYTES = BM * 128, WBYTES = BN * 128, STAGE = XBYTES + WBYTES;
   static constexpr int XI = BM / (8 * NW), WI = BN / (8 * NW);  // DMA instructions per wave per stage
-  static constexpr int PF = (BM + BN + 64 * NW - 1) / (64 * NW);  // L2 prefetch instructions per wave per stage
-  static constexpr int LDC = BN + 8;
-  static constexpr size_t AB = 2 * (size_t)STAGE, CB = (size_t)BM * LDC * 2;
-  static constexpr size_t MAIN = AB > CB ? AB : CB;
-  static constexpr size_t SINK = MAIN + BN * sizeof(float);  // 1 KB the prefetch loads land in
-  static constexpr size_t LDS_BYTES = SINK + 1024;
+  static constexpr int NQ = XI + WI, PER = (NQ + KC - 1) / KC;   // ... and per MFMA group
+  // epilogue: each wave stages HR rows of its TM x TN result at a time in its
+  // own slice of the stage buffer the last K step read
+  static constexpr int HR = 32, NH = TM / HR;  // one 32-row fragment row per pass
+  // staged rows are padded by 16 bytes (8 rows at one chunk fall in 8 distinct
+  // bank groups) so that every staging address is a lane base plus a constant
+  static constexpr int PITCH = TN * 2 + 16, CPRW = TN / 8;  // staged row bytes, 16-byte chunks per row
+  static constexpr size_t BIAS = 2 * (size_t)STAGE;        // fp32 bias of the current tile
+  static constexpr size_t LDS_BYTES = BIAS + BN * sizeof(float);
   static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "whole DMA instructions per wave");
+  static_assert((8 * NW) % 16 == 0, "the swizzle of a lane's rows must not change between instructions");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
+  static_assert(NW * HR * PITCH <= STAGE, "epilogue staging must fit in one stage buffer");
+  static_assert((HR * CPRW) % 64 == 0 && CPRW >= 8, "staged rows leave in whole 64-lane passes");
 };
+
+// What one K step's DMA instructions of a member tile need: the buffer
+// resources of its x and w rows, this lane's byte offsets (already sent out of
+// range for chunks past K), the bytes between a wave's consecutive
+// instructions, and the step's first column. k0 < 0: no loads.
+struct DmaLoads {
+  i32x4 rx, rw;
+  uint32_t sx, sw, xrow, wrow;
+  int k0;
+};
+
+// First K step of a tile, chosen from the tile's coordinates so that tiles
+// sharing an x panel (same mb) or a weight block (same nb) start apart.
+__device__ __forceinline__ int dma_rot(const GemmTile& tile, int nk) { return (4 * tile.nb + tile.mb) % nk; }
+
+template <int BM, int BN, int NW>
+__device__ __forceinline__ DmaLoads dma_loads(const DevLinear& d, int m0, int n0, int k0, int lr, int kch) {
+  DmaLoads L;
+  const int Mr = d.M - m0, Nr = d.N - n0;
+  L.rx = make_rsrc((const bf16_t*)d.x + (int64_t)m0 * d.ldx, (uint32_t)((Mr < BM ? Mr : BM) * d.ldx * 2));
+  L.rw = make_rsrc((const bf16_t*)d.w + (int64_t)n0 * d.ldw, (uint32_t)((Nr < BN ? Nr : BN) * d.ldw * 2));
+  const bool kin = k0 + kch < d.K;
+  L.sx = kin ? (uint32_t)((lr * d.ldx + kch) * 2) : kOutOfRange;
+  L.sw = kin ? (uint32_t)((lr * d.ldw + kch) * 2) : kOutOfRange;
+  L.xrow = (uint32_t)(NW * 8 * d.ldx * 2);
+  L.wrow = (uint32_t)(NW * 8 * d.ldw * 2);
+  L.k0 = k0;
+  return L;
+}
+
+// The first K step's loads of work item t (k0 < 0 past the end or for a padding entry).
+template <int BM, int BN, int NW>
+__device__ __forceinline__ DmaLoads dma_first(const DevLinear* __restrict__ descs, const GemmTile* __restrict__ tiles,
+                                              int t, int num_tiles, int lr, int kch) {
+  DmaLoads L;
+  L.k0 = -1;
+  if (t >= num_tiles) return L;
+  const GemmTile tile = tiles[t];
+  if (tile.member < 0) return L;
+  const DevLinear& d = descs[tile.member];
+  const int nk = (d.K + 63) / 64;
+  return dma_loads<BM, BN, NW>(d, tile.mb * BM, tile.nb * BN, dma_rot(tile, nk) * 64, lr, kch);
+}
 
 template <int BM, int BN, int WM, int WN, int ACT>
 __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const DevLinear* __restrict__ descs,
@@ -325,24 +393,47 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   constexpr int NW = S::NW;
   extern __shared__ __align__(16) char smem[];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
-  bf16_t* sC = (bf16_t*)smem;
-  float* sBias = (float*)(smem + S::MAIN);
+  float* sBias = (float*)(smem + S::BIAS);
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN, l32 = lane & 31, lh = lane >> 5;
-  const int lrow = lane >> 3, lslot = lane & 7;  // this lane's place in a DMA instruction's 8 x 8 chunks
+  // this lane's first staged row and its (swizzled) chunk; each further DMA
+  // instruction of the wave is NW * 8 rows further down, with the same swizzle
+  const int lr = wave * 8 + (lane >> 3);
+  const int kch = ((lane & 7) ^ swz(lr)) << 3;
 
-  int vb = blockIdx.x;
-  if ((gridDim.x & 7) == 0) vb = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+  int t = blockIdx.x;
+  if ((gridDim.x & 7) == 0) t = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
 
-  for (int t = vb; t < num_tiles; t += gridDim.x) {
+  // every DMA instruction of one K step into `stage` (q < XI: x rows, then w rows)
+  auto issue_all = [&](const DmaLoads& L, int stage) {
+    const uint32_t sb = lds_base + stage * S::STAGE + wave * 8 * 128;
+#pragma unroll
+    for (int q = 0; q < S::NQ; ++q) {
+      if (q < S::XI)
+        lds_dma16(L.rx, L.sx + q * L.xrow + L.k0 * 2, sb + q * NW * 8 * 128);
+      else
+        lds_dma16(L.rw, L.sw + (q - S::XI) * L.wrow + L.k0 * 2, sb + S::XBYTES + (q - S::XI) * NW * 8 * 128);
+    }
+  };
+
+  int sbase = 0;  // stage holding the current tile's first K step
+  {
+    const DmaLoads L = dma_first<BM, BN, NW>(descs, tiles, t, num_tiles, lr, kch);
+    if (L.k0 >= 0) issue_all(L, 0);
+  }
+
+  for (; t < num_tiles; t += gridDim.x) {
     const GemmTile tile = tiles[t];
-    if (tile.member < 0) continue;
-    const DevLinear d = descs[tile.member];
+    if (tile.member < 0) {
+      // padding (only at the end of the list): nothing was loaded for it
+      const DmaLoads L = dma_first<BM, BN, NW>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
+      if (L.k0 >= 0) issue_all(L, sbase);
+      continue;
+    }
+    const DevLinear& d = descs[tile.member];
     const int m0 = tile.mb * BM, n0 = tile.nb * BN;
-    const int Mr = d.M - m0, Nr = d.N - n0, K = d.K;
-    const bf16_t* xb = (const bf16_t*)d.x + (int64_t)m0 * d.ldx;
-    const bf16_t* wb = (const bf16_t*)d.w + (int64_t)n0 * d.ldw;
-    if (tid < BN) sBias[tid] = (d.bias && tid < Nr) ? Elem<bf16_t>::load1(d.bias, n0 + tid) : 0.f;
+    const int Mr = d.M - m0, Nr = d.N - n0;
+    const int nk = (d.K + S::BK - 1) / S::BK, rot = dma_rot(tile, nk);
 
     f32x16 acc[S::FM][S::FN];
 #pragma unroll
@@ -352,70 +443,42 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    // This lane's first staged row of x and w and its (swizzled) chunk; each
-    // further DMA instruction of the wave is NW * 8 rows further down. The
-    // swizzle depends on (row / 2) mod 8, which is the same for all of them.
-    const int lr = wave * 8 + lrow;
-    const int kch = (lslot ^ swz(lr)) << 3;
-    const bf16_t* xl = xb + (int64_t)lr * d.ldx + kch;
-    const bf16_t* wl = wb + (int64_t)lr * d.ldw + kch;
-    const int64_t xstep = (int64_t)NW * 8 * d.ldx, wstep = (int64_t)NW * 8 * d.ldw;
-    auto prefetch = [&](int k0) {
-      const uint32_t sink = lds_base + (uint32_t)S::SINK;
-#pragma unroll
-      for (int p = 0; p < S::PF; ++p) {
-        const int r = (p * NW + wave) * 64 + lane;  // x rows, then w rows
-        const void* src = kZeroChunk;
-        if (k0 < K) {
-          if (r < BM) {
-            if (r < Mr) src = xb + (int64_t)r * d.ldx + k0;
-          } else if (r - BM < Nr && r < BM + BN) {
-            src = wb + (int64_t)(r - BM) * d.ldw + k0;
-          }
-        }
-        lds_dma16(src, sink);
-      }
-    };
-    auto issue = [&](int stage, int k0) {
-      const uint32_t sb = lds_base + stage * S::STAGE + wave * 8 * 128;
-      const bool kin = k0 + kch < K;
-#pragma unroll
-      for (int q = 0; q < S::XI; ++q) {
-        const bool in = kin && lr + q * NW * 8 < Mr;
-        lds_dma16(in ? (const void*)(xl + q * xstep + k0) : (const void*)kZeroChunk, sb + q * NW * 8 * 128);
-      }
-#pragma unroll
-      for (int q = 0; q < S::WI; ++q) {
-        const bool in = kin && lr + q * NW * 8 < Nr;
-        lds_dma16(in ? (const void*)(wl + q * wstep + k0) : (const void*)kZeroChunk,
-                  sb + S::XBYTES + q * NW * 8 * 128);
-      }
-    };
-    // K step: the fragments of k-chunk kc + 1 are read from LDS while the
-    // MFMAs of kc run (two fragment sets); scheduling barriers keep the
-    // compiler from hoisting every read of the step up front (which would
-    // need four sets of fragment registers).
-    auto compute = [&](int stage) {
-      const char* sx = smem + stage * S::STAGE;
-      const char* sw = sx + S::XBYTES;
+    // one K step on `stage`; the fragments of k-chunk kc + 1 are read from LDS
+    // while the MFMAs of kc run, and the DMA instructions of the following
+    // step (of this tile, or the next tile's first; none when nk0 < 0) are
+    // spread over the first MFMA groups
+    auto step = [&](int stage, const i32x4& qrx, const i32x4& qrw, uint32_t sx, uint32_t sw, uint32_t xrow,
+                    uint32_t wrow, int nstage, int nk0) {
+      const char* sxp = smem + stage * S::STAGE;
+      const char* swp = sxp + S::XBYTES;
       u32x4 a[2][S::FN], b[2][S::FM];
       auto frag = [&](int kc, int set) {
         const int lc = kc * 2 + lh;
 #pragma unroll
         for (int j = 0; j < S::FN; ++j) {
           const int row = wn * S::TN + j * 32 + l32;
-          a[set][j] = *(const u32x4*)(sw + row * 128 + ((lc ^ swz(row)) << 4));
+          a[set][j] = *(const u32x4*)(swp + row * 128 + ((lc ^ swz(row)) << 4));
         }
 #pragma unroll
         for (int i = 0; i < S::FM; ++i) {
           const int row = wm * S::TM + i * 32 + l32;
-          b[set][i] = *(const u32x4*)(sx + row * 128 + ((lc ^ swz(row)) << 4));
+          b[set][i] = *(const u32x4*)(sxp + row * 128 + ((lc ^ swz(row)) << 4));
         }
       };
+      const uint32_t sb = lds_base + nstage * S::STAGE + wave * 8 * 128;
       frag(0, 0);
 #pragma unroll
-      for (int kc = 0; kc < S::BK / 16; ++kc) {
-        if (kc + 1 < S::BK / 16) frag(kc + 1, (kc + 1) & 1);
+      for (int kc = 0; kc < S::KC; ++kc) {
+        if (kc + 1 < S::KC) frag(kc + 1, (kc + 1) & 1);
+        if (nk0 >= 0) {
+#pragma unroll
+          for (int q = kc * S::PER; q < (kc + 1) * S::PER && q < S::NQ; ++q) {
+            if (q < S::XI)
+              lds_dma16(qrx, sx + q * xrow + nk0 * 2, sb + q * NW * 8 * 128);
+            else
+              lds_dma16(qrw, sw + (q - S::XI) * wrow + nk0 * 2, sb + S::XBYTES + (q - S::XI) * NW * 8 * 128);
+          }
+        }
 #pragma unroll
         for (int i = 0; i < S::FM; ++i)
 #pragma unroll
@@ -424,25 +487,80 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       }
     };
 
-    const int nk = (K + S::BK - 1) / S::BK;
-    issue(0, 0);
-    prefetch(S::BK);
     for (int kb = 0; kb < nk; ++kb) {
+      wait_vmcnt<0>();  // this wave's loads of step kb (and its earlier stores) are done
+      __syncthreads();  // ... and every other wave's; step kb - 1's stage is free
+      const int stage = (sbase + kb) & 1;
+      // the bias of this tile: the previous tile's epilogue read sBias before this barrier
+      float bv = 0.f;
+      if (kb == 0 && tid < BN) bv = (d.bias && tid < Nr) ? Elem<bf16_t>::load1(d.bias, n0 + tid) : 0.f;
+      // the following step of this tile, or at the last step the next tile's first
+      DmaLoads L;
       if (kb + 1 < nk) {
-        issue((kb + 1) & 1, (kb + 1) * S::BK);
-        prefetch((kb + 2) * S::BK);
-        // this wave's loads of step kb have landed; the two prefetch groups and
-        // the loads of step kb + 1 issued after them may still be in flight
-        wait_vmcnt<S::XI + S::WI + 2 * S::PF>();
+        const int q = kb + 1 + rot;
+        L = dma_loads<BM, BN, NW>(d, m0, n0, (q >= nk ? q - nk : q) * S::BK, lr, kch);
       } else {
-        wait_vmcnt<0>();
+        L = dma_first<BM, BN, NW>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
       }
-      __syncthreads();  // ... and every other wave's
-      compute(kb & 1);
-      __syncthreads();  // step kb's stage is free for the loads of step kb + 2
+      step(stage, L.rx, L.rw, L.sx, L.sw, L.xrow, L.wrow, stage ^ 1, L.k0);
+      if (kb == 0 && tid < BN) sBias[tid] = bv;
     }
-    gemm_epilogue<bf16_t, BM, BN, WM, WN, S::LDC, ACT>(acc, sC, sBias, d, m0, n0, Mr, Nr);
-    __syncthreads();  // staging and bias reads done before the next tile overwrites them
+    __syncthreads();  // every wave is done with the last stage (staging) and the bias is written
+
+    // epilogue: bias + activation + rounding into this wave's staging slice,
+    // then whole 16-byte pieces of y rows leave in coalesced stores. Every
+    // address is one lane base plus constants and every bound a per-tile
+    // scalar, so nothing lane-dependent stays live across the tile loop.
+    {
+      constexpr int RPP = 64 / S::CPRW;  // staged rows per store pass
+      // opaque copies: computed here, per tile, instead of being hoisted out
+      // of the tile loop and kept live across the K loop
+      int lane_o = lane, wrow0 = wm * S::TM, wcol0 = wn * S::TN;
+      __asm__ volatile("" : "+v"(lane_o));
+      __asm__ volatile("" : "+s"(wrow0), "+s"(wcol0));
+      const int lstage = (sbase + nk - 1) & 1;
+      char* wst = smem + lstage * S::STAGE + wave * S::HR * S::PITCH;
+      char* wput = wst + (lane_o & 31) * S::PITCH + (lane_o >> 5) * 8;
+      const int lrow = lane_o / S::CPRW, lc = lane_o % S::CPRW;
+      const char* wget = wst + lrow * S::PITCH + lc * 16;
+      const float* bput = sBias + wcol0 + (lane_o >> 5) * 4;
+      const int tc = wcol0 + lc * 8;  // tile column of this lane's stores
+      const bool col_in = tc < Nr, col_vec = (d.vec & 2) != 0 && tc + 8 <= Nr;
+      bf16_t* ybase = (bf16_t*)d.y + (int64_t)(m0 + wrow0) * d.ldy + n0 + tc + (int64_t)lrow * d.ldy;
+#pragma unroll
+      for (int h = 0; h < S::NH; ++h) {
+#pragma unroll
+        for (int j = 0; j < S::FN; ++j) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 bv = *(const f32x4*)(bput + j * 32 + q * 8);
+            const float o0 = act_apply<ACT>(acc[h][j][q * 4 + 0] + bv.x);
+            const float o1 = act_apply<ACT>(acc[h][j][q * 4 + 1] + bv.y);
+            const float o2 = act_apply<ACT>(acc[h][j][q * 4 + 2] + bv.z);
+            const float o3 = act_apply<ACT>(acc[h][j][q * 4 + 3] + bv.w);
+            *(u32x2*)(wput + (4 * j + q) * 16) = u32x2{pack_bf16x2(o0, o1), pack_bf16x2(o2, o3)};
+          }
+        }
+        lds_wave_sync();
+#pragma unroll
+        for (int r = 0; r < S::HR / RPP; ++r) {
+          const u32x4 v = *(const u32x4*)(wget + r * RPP * S::PITCH);
+          const int lim = Mr - (wrow0 + h * S::HR + r * RPP);  // rows of this pass inside the tile
+          if (lrow < lim && col_in) {
+            bf16_t* yp = ybase + (int64_t)(h * S::HR + r * RPP) * d.ldy;
+            if (col_vec) {
+              st16(yp, v);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                if (tc + e < Nr) ((OPTIMUS_GLOBAL uint16_t*)yp)[e] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+            }
+          }
+        }
+        lds_wave_sync();  // staging read before the next pass overwrites it
+      }
+    }
+    sbase = (sbase + nk) & 1;
   }
 }
 
@@ -600,9 +718,12 @@ static bool gemm_skinny_ok(const optimus_linear_desc* d, int32_t G) {
   return true;
 }
 
+// The direct-to-LDS kernels address a tile of at most 256 rows through 32-bit
+// buffer offsets below 2^31 (larger offsets mark out-of-range chunks).
 static bool gemm_dma_ok(const optimus_linear_desc* d, int32_t G) {
   for (int g = 0; g < G; ++g) {
     if (d[g].K % 8 || d[g].ldx % 8 || d[g].ldw % 8 || ((uintptr_t)d[g].x & 15) || ((uintptr_t)d[g].w & 15)) return false;
+    if (256 * d[g].ldx * 2 >= (int64_t)1 << 31 || 256 * d[g].ldw * 2 >= (int64_t)1 << 31) return false;
   }
   return true;
 }
