@@ -29,19 +29,29 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 CACHE_BYTES = 512 << 20  # rotate inputs over at least this much memory per step cycle
+COPY_BYTES = 1 << 30     # the calibration copy: 1 GiB read and 1 GiB written, far beyond the caches
+WARMUP_SECONDS = 0.3
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before timing (default: at least 20 and at least 0.3 s of work, "
+                         "so that the clocks have settled)")
     ap.add_argument("--workload", default="launch_bound",
                     choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-chain", action="store_true", help="skip timing the per-op launch chain")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU-baseline duration")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run only a plain device-to-device copy of COPY_BYTES, five times (counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="turn four rocprofv3 --pmc output folders (FETCH_SIZE and WRITE_SIZE of this workload's "
+                         "bench run and of --copy-probe) into profiles/<kernel>__<workload>.pmc.json; no GPU needed")
+    ap.add_argument("--pmc-command", default="", help="command line recorded in the --pmc-summary output")
     return ap.parse_args()
 
 
@@ -206,9 +216,10 @@ def cpu_baseline(name, wl, target_s):
 
 # ---------------------------------------------------------------------- rocprofv3 traffic
 def traffic_from_profile(kernel, name):
-    """HBM bytes per launch from the committed counter summary, when it was
-    taken on the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}__{name}.pmc.json")
+    """HBM bytes per launch from the committed counter summary of this
+    kernel and workload, when it was taken on the current kernel sources
+    (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_symbol(kernel)}__{name}.pmc.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -216,6 +227,85 @@ def traffic_from_profile(kernel, name):
     if pmc.get("sources_sha256") != sources_hash():
         return None
     return pmc.get("hbm_bytes_per_launch")
+
+
+def _pmc_per_dispatch(folder, counter, kernel_substr):
+    """Mean value of `counter` per dispatch of kernels whose name contains
+    `kernel_substr`, from a rocprofv3 --pmc csv output folder."""
+    import csv
+    import glob
+    vals = {}
+    for fn in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
+        with open(fn) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter and kernel_substr in r["Kernel_Name"]:
+                    vals[(fn, r["Dispatch_Id"])] = vals.get((fn, r["Dispatch_Id"]), 0.0) + float(r["Counter_Value"])
+    if not vals:
+        raise SystemExit(f"bench.py: no {counter} records for '{kernel_substr}' under {folder}")
+    return sum(vals.values()) / len(vals), len(vals)
+
+
+def pmc_summary(args):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the workload's dominant
+    kernel, each scaled by what the same counter reads for a copy of known
+    size, as HBM bytes per launch."""
+    name = args.workload
+    kernel = DOMINANT_KERNEL_NAME[name]
+    f_dir, w_dir, cf_dir, cw_dir = args.pmc_summary
+    fetch, nf = _pmc_per_dispatch(f_dir, "FETCH_SIZE", kernel)
+    write, nw = _pmc_per_dispatch(w_dir, "WRITE_SIZE", kernel)
+    cfetch, _ = _pmc_per_dispatch(cf_dir, "FETCH_SIZE", COPY_KERNEL)
+    cwrite, _ = _pmc_per_dispatch(cw_dir, "WRITE_SIZE", COPY_KERNEL)
+    fs, ws = COPY_BYTES / (cfetch * 1024.0), COPY_BYTES / (cwrite * 1024.0)
+    out = {"kernel": kernel, "workload": name, "fetch_kib_per_dispatch": round(fetch, 1),
+           "write_kib_per_dispatch": round(write, 1), "dispatches": [nf, nw],
+           "copy_bytes": COPY_BYTES, "copy_fetch_kib": round(cfetch, 1), "copy_write_kib": round(cwrite, 1),
+           "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+           "hbm_bytes_per_launch": round(fetch * 1024.0 * fs + write * 1024.0 * ws),
+           "sources_sha256": sources_hash(), "command": args.pmc_command}
+    path = os.path.join(ROOT, "profiles", f"{kernel}__{name}.pmc.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out))
+
+
+# The calibration copy is torch's elementwise kernel writing the bitwise
+# complement of a 1 GiB byte tensor (a device-to-device copy_ may run on a
+# DMA engine, which no shader counter sees).
+COPY_KERNEL = "bitwise_not"
+
+
+def copy_probe():
+    import torch
+    a = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)  # contents do not matter
+    torch.cuda.synchronize()
+    for _ in range(5):
+        torch.bitwise_not(a, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": COPY_BYTES, "copies": 5}))
+
+
+# The kernel whose launches the roofline is taken on, per workload: the
+# symbol name (up to its template arguments) of the kernel the plan picks.
+DOMINANT_KERNEL_NAME = {
+    "launch_bound": "grouped_gemm_kernel",
+    "tiny_group": "grouped_gemm_kernel",
+    "split_op_cat": "split_op_cat_kernel",
+    "towers": "grouped_gemm_dma_kernel",
+    "large_group": "grouped_gemm_dma_kernel",
+}
+
+
+def kernel_symbol(label):
+    """Symbol name of the kernel behind a plan's kernel label."""
+    for prefix, sym in (("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
+                        ("grouped_gemm", "grouped_gemm_kernel"), ("split_op_cat_fused", "split_op_cat_kernel"),
+                        ("grouped_layernorm", "grouped_layernorm_kernel"), ("grouped_pointwise", "grouped_pointwise_kernel")):
+        if label.startswith(prefix):
+            return sym
+    return label
 
 
 def sources_hash():
@@ -231,6 +321,12 @@ def sources_hash():
 # ---------------------------------------------------------------------- main
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(args)
+        return
+    if args.copy_probe:
+        copy_probe()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build measures one GPU only (the grouped path needs no exchange "
               "between GPUs; see the sharding design); run with --gpus 1", file=sys.stderr)
@@ -251,9 +347,23 @@ def main():
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
+    def warm(which, warmup):
+        """W untimed steps, or by default at least 20 and at least WARMUP_SECONDS
+        of work (the clocks ramp up over the first tens of milliseconds)."""
+        if warmup is not None:
+            for i in range(warmup):
+                ogs[i % copies].run(which, stream)
+            return warmup
+        n, t0 = 0, time.perf_counter()
+        while n < 20 or time.perf_counter() - t0 < WARMUP_SECONDS:
+            for _ in range(10):
+                ogs[n % copies].run(which, stream)
+                n += 1
+            torch.cuda.synchronize()
+        return n
+
     def timed(which, steps, warmup, with_events):
-        for i in range(warmup):
-            ogs[i % copies].run(which, stream)
+        warm(which, warmup)
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)] \
             if with_events else None
         t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -269,13 +379,14 @@ def main():
         kern_ms = [a.elapsed_time(b) for a, b in evs] if evs else None
         return total_ms, wall, kern_ms
 
-    total_ms, wall, kern_ms = timed("grouped", args.steps, args.warmup, True)
+    warmed = warm("grouped", args.warmup)
+    total_ms, wall, kern_ms = timed("grouped", args.steps, 0, True)
     ms_step = total_ms / args.steps
     info = ogs[0].dominant.info()
     launches = sum(p.info()["launches"] for p, _ in ogs[0].grouped)
     out = {
         "metric": METRIC, "value": round(ms_step * 1000.0, 3), "unit": "µs", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 6),
+        "steps": args.steps, "warmup": warmed, "ms_per_step": round(ms_step, 6),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
         "data": "synthetic (seeded PCG64 draws of the workload's shapes and distributions)",
         "config": describe(args.workload, wl),
@@ -304,7 +415,7 @@ def main():
     out["roofline"] = roof
     if not args.no_chain:
         csteps = max(5, min(args.steps, 50))
-        c_ms, _, _ = timed("chain", csteps, max(2, args.warmup // 4), False)
+        c_ms, _, _ = timed("chain", csteps, 5, False)
         c_step = c_ms / csteps
         out["chain"] = {"us_per_group": round(c_step * 1000.0, 3),
                         "launches_per_group": sum(p.info()["chain_launches"] for p, m in ogs[0].chain

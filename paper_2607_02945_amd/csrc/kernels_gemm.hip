@@ -283,9 +283,10 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
 // Addressing goes through one buffer resource per operand and tile whose
 // record count ends at the tile's last valid row: rows past M (N) read as zero
 // in hardware, and chunks past K are sent to an offset beyond any record count.
-// The loads of step k+1 are issued in small groups between the MFMA groups of
-// step k, so the address unit works while the matrix cores do; one workgroup
-// barrier per step then makes step k+1's stage visible and frees step k's.
+// The loads of step k+1 are issued in small groups between the first MFMA
+// groups of step k, so the address unit works while the matrix cores do; one
+// workgroup barrier per step then makes step k+1's stage visible and frees
+// step k's. The last step of a tile fetches the next tile's first step.
 // The K loop starts at a step that depends on the tile's coordinates, so the
 // tiles that share an x panel or a weight block (which run side by side on one
 // L2) do not request the same lines at the same moment.
@@ -326,7 +327,9 @@ struct DmaShape {
   static constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
   static constexpr int XBYTES = BM * 128, WBYTES = BN * 128, STAGE = XBYTES + WBYTES;
   static constexpr int XI = BM / (8 * NW), WI = BN / (8 * NW);  // DMA instructions per wave per stage
-  static constexpr int NQ = XI + WI, PER = (NQ + KC - 1) / KC;   // ... and per MFMA group
+  // ... issued over the first two MFMA groups of the step before (later ones
+  // would leave too little of the step to cover their latency)
+  static constexpr int NQ = XI + WI, PER = (NQ + 1) / 2;
   // epilogue: each wave stages HR rows of its TM x TN result at a time in its
   // own slice of the stage buffer the last K step read
   static constexpr int HR = 32, NH = TM / HR;  // one 32-row fragment row per pass
@@ -347,21 +350,26 @@ struct DmaShape {
 // range for chunks past K), the bytes between a wave's consecutive
 // instructions, and the step's first column. k0 < 0: no loads.
 struct DmaLoads {
-  i32x4 rx, rw;
+  const void* xp;          // first x / w row of the tile
+  const void* wp;
+  uint32_t xbytes, wbytes; // record counts: bytes up to the end of the tile's last valid row
   uint32_t sx, sw, xrow, wrow;
   int k0;
 };
 
-// First K step of a tile, chosen from the tile's coordinates so that tiles
-// sharing an x panel (same mb) or a weight block (same nb) start apart.
-__device__ __forceinline__ int dma_rot(const GemmTile& tile, int nk) { return (4 * tile.nb + tile.mb) % nk; }
+// First K step of a tile: tiles that share an x panel (same mb, run side by
+// side on one L2) walk K in step so that the panel is fetched once; tiles
+// that share a weight block (same nb) start apart.
+__device__ __forceinline__ int dma_rot(const GemmTile& tile, int nk) { return tile.mb % nk; }
 
 template <int BM, int BN, int NW>
 __device__ __forceinline__ DmaLoads dma_loads(const DevLinear& d, int m0, int n0, int k0, int lr, int kch) {
   DmaLoads L;
   const int Mr = d.M - m0, Nr = d.N - n0;
-  L.rx = make_rsrc((const bf16_t*)d.x + (int64_t)m0 * d.ldx, (uint32_t)((Mr < BM ? Mr : BM) * d.ldx * 2));
-  L.rw = make_rsrc((const bf16_t*)d.w + (int64_t)n0 * d.ldw, (uint32_t)((Nr < BN ? Nr : BN) * d.ldw * 2));
+  L.xp = (const bf16_t*)d.x + (int64_t)m0 * d.ldx;
+  L.wp = (const bf16_t*)d.w + (int64_t)n0 * d.ldw;
+  L.xbytes = (uint32_t)((Mr < BM ? Mr : BM) * d.ldx * 2);
+  L.wbytes = (uint32_t)((Nr < BN ? Nr : BN) * d.ldw * 2);
   const bool kin = k0 + kch < d.K;
   L.sx = kin ? (uint32_t)((lr * d.ldx + kch) * 2) : kOutOfRange;
   L.sw = kin ? (uint32_t)((lr * d.ldw + kch) * 2) : kOutOfRange;
@@ -385,7 +393,7 @@ __device__ __forceinline__ DmaLoads dma_first(const DevLinear* __restrict__ desc
   return dma_loads<BM, BN, NW>(d, tile.mb * BM, tile.nb * BN, dma_rot(tile, nk) * 64, lr, kch);
 }
 
-template <int BM, int BN, int WM, int WN, int ACT>
+template <int BM, int BN, int WM, int WN, bool REGS, int ACT>
 __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const DevLinear* __restrict__ descs,
                                                                        const GemmTile* __restrict__ tiles,
                                                                        int32_t num_tiles) {
@@ -404,15 +412,32 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   int t = blockIdx.x;
   if ((gridDim.x & 7) == 0) t = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
 
-  // every DMA instruction of one K step into `stage` (q < XI: x rows, then w rows)
+  // Load q of one K step (q < XI: x rows, then w rows) lands at byte lds_off(q)
+  // of the stage plus 16 * lane; with REGS it goes through registers.
+  auto lds_off = [&](int q) {
+    return q < S::XI ? wave * 8 * 128 + q * NW * 8 * 128 : S::XBYTES + wave * 8 * 128 + (q - S::XI) * NW * 8 * 128;
+  };
+  auto gofs = [&](const DmaLoads& L, int q) {
+    return q < S::XI ? L.sx + q * L.xrow + L.k0 * 2 : L.sw + (q - S::XI) * L.wrow + L.k0 * 2;
+  };
+  auto load_reg = [&](const DmaLoads& L, int q) {
+    const __amdgpu_buffer_rsrc_t r = q < S::XI ? __builtin_amdgcn_make_buffer_rsrc((void*)L.xp, 0, L.xbytes, 0x00020000)
+                                               : __builtin_amdgcn_make_buffer_rsrc((void*)L.wp, 0, L.wbytes, 0x00020000);
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)gofs(L, q), 0, 0));
+  };
+  auto put = [&](int stage, int q, const u32x4& v) { *(u32x4*)(smem + stage * S::STAGE + lds_off(q) + lane * 16) = v; };
+  // every load of one K step into `stage`
   auto issue_all = [&](const DmaLoads& L, int stage) {
-    const uint32_t sb = lds_base + stage * S::STAGE + wave * 8 * 128;
+    if constexpr (REGS) {
+      u32x4 R[S::NQ];
 #pragma unroll
-    for (int q = 0; q < S::NQ; ++q) {
-      if (q < S::XI)
-        lds_dma16(L.rx, L.sx + q * L.xrow + L.k0 * 2, sb + q * NW * 8 * 128);
-      else
-        lds_dma16(L.rw, L.sw + (q - S::XI) * L.wrow + L.k0 * 2, sb + S::XBYTES + (q - S::XI) * NW * 8 * 128);
+      for (int q = 0; q < S::NQ; ++q) R[q] = load_reg(L, q);
+#pragma unroll
+      for (int q = 0; q < S::NQ; ++q) put(stage, q, R[q]);
+    } else {
+      const i32x4 rx = make_rsrc(L.xp, L.xbytes), rw = make_rsrc(L.wp, L.wbytes);
+#pragma unroll
+      for (int q = 0; q < S::NQ; ++q) lds_dma16(q < S::XI ? rx : rw, gofs(L, q), lds_base + stage * S::STAGE + lds_off(q));
     }
   };
 
@@ -447,8 +472,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     // while the MFMAs of kc run, and the DMA instructions of the following
     // step (of this tile, or the next tile's first; none when nk0 < 0) are
     // spread over the first MFMA groups
-    auto step = [&](int stage, const i32x4& qrx, const i32x4& qrw, uint32_t sx, uint32_t sw, uint32_t xrow,
-                    uint32_t wrow, int nstage, int nk0) {
+    auto step = [&](int stage, const DmaLoads& L, int nstage) {
       const char* sxp = smem + stage * S::STAGE;
       const char* swp = sxp + S::XBYTES;
       u32x4 a[2][S::FN], b[2][S::FM];
@@ -465,18 +489,24 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
           b[set][i] = *(const u32x4*)(sxp + row * 128 + ((lc ^ swz(row)) << 4));
         }
       };
-      const uint32_t sb = lds_base + nstage * S::STAGE + wave * 8 * 128;
+      const bool go = L.k0 >= 0;
+      i32x4 rx, rw;
+      if constexpr (!REGS) {
+        rx = make_rsrc(L.xp, L.xbytes);
+        rw = make_rsrc(L.wp, L.wbytes);
+      }
+      u32x4 R[S::NQ];
       frag(0, 0);
 #pragma unroll
       for (int kc = 0; kc < S::KC; ++kc) {
         if (kc + 1 < S::KC) frag(kc + 1, (kc + 1) & 1);
-        if (nk0 >= 0) {
+        if (go) {
 #pragma unroll
           for (int q = kc * S::PER; q < (kc + 1) * S::PER && q < S::NQ; ++q) {
-            if (q < S::XI)
-              lds_dma16(qrx, sx + q * xrow + nk0 * 2, sb + q * NW * 8 * 128);
+            if constexpr (REGS)
+              R[q] = load_reg(L, q);
             else
-              lds_dma16(qrw, sw + (q - S::XI) * wrow + nk0 * 2, sb + S::XBYTES + (q - S::XI) * NW * 8 * 128);
+              lds_dma16(q < S::XI ? rx : rw, gofs(L, q), lds_base + nstage * S::STAGE + lds_off(q));
           }
         }
 #pragma unroll
@@ -485,11 +515,20 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
           for (int j = 0; j < S::FN; ++j) Mfma<bf16_t>::run(a[kc & 1][j], b[kc & 1][i], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
+      if constexpr (REGS) {
+        if (go) {
+#pragma unroll
+          for (int q = 0; q < S::NQ; ++q) put(nstage, q, R[q]);
+        }
+      }
     };
 
     for (int kb = 0; kb < nk; ++kb) {
-      wait_vmcnt<0>();  // this wave's loads of step kb (and its earlier stores) are done
-      __syncthreads();  // ... and every other wave's; step kb - 1's stage is free
+      // this wave's loads of step kb have landed (direct-to-LDS: and its
+      // earlier stores); the barrier extends that to every wave and frees
+      // step kb - 1's stage
+      if constexpr (!REGS) wait_vmcnt<0>();
+      __syncthreads();
       const int stage = (sbase + kb) & 1;
       // the bias of this tile: the previous tile's epilogue read sBias before this barrier
       float bv = 0.f;
@@ -502,7 +541,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       } else {
         L = dma_first<BM, BN, NW>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
       }
-      step(stage, L.rx, L.rw, L.sx, L.sw, L.xrow, L.wrow, stage ^ 1, L.k0);
+      step(stage, L, stage ^ 1);
       if (kb == 0 && tid < BN) sBias[tid] = bv;
     }
     __syncthreads();  // every wave is done with the last stage (staging) and the bias is written
@@ -549,7 +588,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
           if (lrow < lim && col_in) {
             bf16_t* yp = ybase + (int64_t)(h * S::HR + r * RPP) * d.ldy;
             if (col_vec) {
-              st16(yp, v);
+              st16_nt(yp, v);  // y is not read again by this launch
             } else {
 #pragma unroll
               for (int e = 0; e < 8; ++e)
@@ -691,8 +730,9 @@ struct GemmVariant {
 
 // 0: members with N, K <= 64 (one K step); 1: 128x128; 2: 256x256 (8 waves);
 // 3: fp32; 4: 256x256 (4 waves); 5: 256x128 (4 waves);
-// 6-9: direct-to-LDS (bf16, aligned rows, K % 8 == 0): 256x256 8 waves,
-// 256x256 4 waves, 256x128 4 waves, 128x128 4 waves;
+// 6-9: buffer-resource pipeline (bf16, aligned rows, K % 8 == 0): 256x256
+// 8 waves direct-to-LDS, 256x256 8 waves through registers, 256x128 and
+// 128x128 4 waves direct-to-LDS;
 // 10: skinny members (bf16, N <= 64, K <= 64, K % 8 == 0, aligned rows).
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
@@ -702,7 +742,7 @@ static const GemmVariant kVariants[] = {
     {256, 256, 256, 1, "grouped_gemm_bf16_256x256x64_w2x2_s2"},
     {256, 128, 256, 1, "grouped_gemm_bf16_256x128x64_w2x2_s2"},
     {256, 256, 512, 1, "grouped_gemm_dma_bf16_256x256x64_w2x4"},
-    {256, 256, 256, 1, "grouped_gemm_dma_bf16_256x256x64_w2x2"},
+    {256, 256, 512, 1, "grouped_gemm_rs_bf16_256x256x64_w2x4"},
     {256, 128, 256, 1, "grouped_gemm_dma_bf16_256x128x64_w2x2"},
     {128, 128, 256, 2, "grouped_gemm_dma_bf16_128x128x64_w2x2"},
     {kSkinnyRows, 64, 256, OPTIMUS_SKINNY_OCC, "grouped_gemm_skinny_bf16"},
@@ -790,14 +830,14 @@ static hipError_t launch_shape(optimus_act act, const DevLinear* descs, const Ge
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, bool REGS>
 static hipError_t launch_dma(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
                              hipStream_t stream) {
   using S = DmaShape<BM, BN, WM, WN>;
   const size_t smem = S::LDS_BYTES;
 #define OPTIMUS_DMA_LAUNCH(A)                                                                                      \
   {                                                                                                                \
-    auto kfn = grouped_gemm_dma_kernel<BM, BN, WM, WN, A>;                                                         \
+    auto kfn = grouped_gemm_dma_kernel<BM, BN, WM, WN, REGS, A>;                                                         \
     static bool attr_set = false;                                                                                  \
     if (smem > 65536 && !attr_set) {                                                                               \
       hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); \
@@ -828,10 +868,10 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
     case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     case 4: return launch_shape<bf16_t, 256, 256, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     case 5: return launch_shape<bf16_t, 256, 128, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 6: return launch_dma<256, 256, 2, 4>(act, descs, tiles, num_tiles, grid, stream);
-    case 7: return launch_dma<256, 256, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 8: return launch_dma<256, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 9: return launch_dma<128, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 6: return launch_dma<256, 256, 2, 4, false>(act, descs, tiles, num_tiles, grid, stream);
+    case 7: return launch_dma<256, 256, 2, 4, true>(act, descs, tiles, num_tiles, grid, stream);
+    case 8: return launch_dma<256, 128, 2, 2, false>(act, descs, tiles, num_tiles, grid, stream);
+    case 9: return launch_dma<128, 128, 2, 2, false>(act, descs, tiles, num_tiles, grid, stream);
     case 10: {
       switch (act) {
         case OPTIMUS_ACT_NONE: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<0>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
