@@ -8,6 +8,14 @@ of seeded synthetic input that is already resident in HBM. Inputs are
 rotated over enough copies that each step reads data no longer held in the
 256 MB last-level cache. Prints one JSON line.
 
+`value` is the mean time of the timed steps between one pair of HIP events.
+The roofline is taken on the op-group's dominant kernel: its plan is then
+launched `--steps` times back to back over the same rotating inputs between
+one more pair of events, and the mean launch duration divides the kernel's
+algorithmic flops or bytes. `traffic` is the HBM bytes per launch from the
+committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary when that was taken on
+the current kernel sources.
+
 Workloads (the seeded groups of paper_2607_02945_amd.synth): launch_bound
 (default; G=256 bf16 Linear + sigmoid, B=2048), tiny_group, split_op_cat,
 towers, large_group.
@@ -22,7 +30,6 @@ import os
 import sys
 import time
 
-import numpy as np
 
 METRIC = "µs per op-group + achieved TFLOP/s or HBM GB/s vs per-op launch chain"
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -67,15 +74,12 @@ class OpGroup:
         self.horizontal = []   # split-op-cat only: horizontal fusion without the vertical rewrite
         self.dominant = None
 
-    def run(self, which, stream=None, ev=None):
-        seq = getattr(self, which)
-        for plan, mode in seq:
-            if ev is not None and plan is self.dominant:
-                ev[0].record()
-                plan.execute(mode, stream)
-                ev[1].record()
-            else:
-                plan.execute(mode, stream)
+    def run(self, which, stream=None):
+        for plan, mode in getattr(self, which):
+            plan.execute(mode, stream)
+
+    def run_dominant(self, stream=None):
+        self.dominant.execute("grouped", stream)
 
 
 def build_copy(name, wl, torch, B):
@@ -347,40 +351,47 @@ def main():
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
+    def one(i, which):
+        if which == "dominant":
+            ogs[i % copies].run_dominant(stream)
+        else:
+            ogs[i % copies].run(which, stream)
+
     def warm(which, warmup):
         """W untimed steps, or by default at least 20 and at least WARMUP_SECONDS
         of work (the clocks ramp up over the first tens of milliseconds)."""
         if warmup is not None:
             for i in range(warmup):
-                ogs[i % copies].run(which, stream)
+                one(i, which)
             return warmup
         n, t0 = 0, time.perf_counter()
         while n < 20 or time.perf_counter() - t0 < WARMUP_SECONDS:
             for _ in range(10):
-                ogs[n % copies].run(which, stream)
+                one(n, which)
                 n += 1
             torch.cuda.synchronize()
         return n
 
-    def timed(which, steps, warmup, with_events):
+    def timed(which, steps, warmup):
+        """(ms, wall s) of `steps` back-to-back steps between one pair of HIP
+        events recorded on the launch stream."""
         warm(which, warmup)
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)] \
-            if with_events else None
         t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         w0 = time.perf_counter()
-        t_start.record()
+        t_start.record(stream)
         for i in range(steps):
-            ogs[i % copies].run(which, stream, evs[i] if evs else None)
-        t_end.record()
+            one(i, which)
+        t_end.record(stream)
         torch.cuda.synchronize()
-        wall = time.perf_counter() - w0
-        total_ms = t_start.elapsed_time(t_end)
-        kern_ms = [a.elapsed_time(b) for a, b in evs] if evs else None
-        return total_ms, wall, kern_ms
+        return t_start.elapsed_time(t_end), time.perf_counter() - w0
 
     warmed = warm("grouped", args.warmup)
-    total_ms, wall, kern_ms = timed("grouped", args.steps, 0, True)
+    total_ms, wall = timed("grouped", args.steps, 0)
+    # the dominant kernel alone, launched back to back over the same inputs:
+    # its mean launch duration (one event pair, so no per-launch event cost)
+    k_total_ms, _ = timed("dominant", args.steps, 10)
+    k_ms = k_total_ms / args.steps
     ms_step = total_ms / args.steps
     info = ogs[0].dominant.info()
     launches = sum(p.info()["launches"] for p, _ in ogs[0].grouped)
@@ -398,7 +409,6 @@ def main():
     out["group_tflops"] = round(flops / (ms_step * 1e-3) / 1e12, 3)
     out["group_hbm_gbs"] = round(nbytes / (ms_step * 1e-3) / 1e9, 1)
     # roofline of the dominant kernel: algorithmic work per launch / mean launch duration
-    k_ms = float(np.mean(kern_ms))
     ai = info["flops"] / max(info["bytes"], 1.0)
     ridge = PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
     if info["flops"] > 0 and ai >= ridge:
@@ -415,7 +425,7 @@ def main():
     out["roofline"] = roof
     if not args.no_chain:
         csteps = max(5, min(args.steps, 50))
-        c_ms, _, _ = timed("chain", csteps, 5, False)
+        c_ms, _ = timed("chain", csteps, 5)
         c_step = c_ms / csteps
         out["chain"] = {"us_per_group": round(c_step * 1000.0, 3),
                         "launches_per_group": sum(p.info()["chain_launches"] for p, m in ogs[0].chain
@@ -423,7 +433,7 @@ def main():
                         "speedup": round(c_step / ms_step, 2)}
     if ogs[0].horizontal:
         hsteps = max(5, min(args.steps, 50))
-        h_ms, _, _ = timed("horizontal", hsteps, 2, False)
+        h_ms, _ = timed("horizontal", hsteps, 2)
         out["horizontal_only"] = {"us_per_group": round(h_ms / hsteps * 1000.0, 3), "launches_per_group": 3}
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(args.workload, wl, args.cpu_seconds)

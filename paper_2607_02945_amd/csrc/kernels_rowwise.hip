@@ -30,15 +30,18 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
   const int li = lane & (L - 1);
   const int cpr = d.cols / VEC;
 
-  float g[MAXC][VEC], b[MAXC][VEC];
+  // gamma / beta stay packed (unpacked where used): registers set the occupancy
+  u32x4 gp[MAXC], bp[MAXC];
+  {
+    float one[VEC], zero[VEC];
 #pragma unroll
-  for (int j = 0; j < MAXC; ++j) {
-    const int c = j * L + li;
+    for (int e = 0; e < VEC; ++e) { one[e] = 1.f; zero[e] = 0.f; }
+    const u32x4 ones = Elem<T>::pack(one), zeros = Elem<T>::pack(zero);
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) { g[j][e] = 1.f; b[j][e] = 0.f; }
-    if (c < cpr) {
-      if (d.gamma) Elem<T>::unpack(ld16((const char*)d.gamma + (int64_t)c * 16), g[j]);
-      if (d.beta) Elem<T>::unpack(ld16((const char*)d.beta + (int64_t)c * 16), b[j]);
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = j * L + li;
+      gp[j] = (d.gamma && c < cpr) ? ld16((const char*)d.gamma + (int64_t)c * 16) : ones;
+      bp[j] = (d.beta && c < cpr) ? ld16((const char*)d.beta + (int64_t)c * 16) : zeros;
     }
   }
   const int rpb = 4 * rpw;
@@ -83,9 +86,13 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
     for (int j = 0; j < MAXC; ++j) {
       const int c = j * L + li;
       if (valid && c < cpr) {
-        float o[VEC];
+        float g[VEC], b[VEC], o[VEC];
+        u32x4 gj = gp[j], bj = bp[j];
+        __asm__ volatile("" : "+v"(gj), "+v"(bj));  // unpack here, not hoisted out of the row loop
+        Elem<T>::unpack(gj, g);
+        Elem<T>::unpack(bj, b);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>(x[j][e] * (rstd * g[j][e]) + b[j][e]);
+        for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>(x[j][e] * (rstd * g[e]) + b[e]);
         st16_nt(yr + (int64_t)c * 16, Elem<T>::pack(o));
       }
     }
@@ -134,7 +141,8 @@ __global__ __launch_bounds__(kRowThreads) void grouped_layernorm_kernel(const De
 
 // ===================================================================== pointwise
 // Same row/lane mapping as the LayerNorm kernel, without the reductions; a
-// lane group loops over the row's chunks (any row length).
+// lane group loops over the row's chunks (any row length), four loads in
+// flight per lane.
 template <typename T, int ACT>
 __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const DevRows* __restrict__ descs,
                                                                         const RowTile* __restrict__ tiles,
@@ -151,7 +159,22 @@ __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const De
       for (int r = rt.row0 + wave * rpw + sub; r < end; r += 4 * rpw) {
         const char* xr = (const char*)d.x + (int64_t)r * d.ldx * sizeof(T);
         char* yr = (char*)d.y + (int64_t)r * d.ldy * sizeof(T);
-        for (int c = li; c < cpr; c += L) {
+        // four chunks per lane in flight, then the rest one at a time
+        int c = li;
+        for (; c + 3 * L < cpr; c += 4 * L) {
+          u32x4 rv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) rv[u] = ld16_nt(xr + (int64_t)(c + u * L) * 16);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            float v[VEC];
+            Elem<T>::unpack(rv[u], v);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) v[e] = act_apply<ACT>(v[e]);
+            st16_nt(yr + (int64_t)(c + u * L) * 16, Elem<T>::pack(v));
+          }
+        }
+        for (; c < cpr; c += L) {
           float v[VEC];
           Elem<T>::unpack(ld16_nt(xr + (int64_t)c * 16), v);
 #pragma unroll
@@ -327,17 +350,19 @@ __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc*
       if (ls < npc) stat[ls] *= iw0;
       if (ls + RL < npc) stat[ls + RL] *= iw1;
       row_sync();
-      // pass 2: centred values, their squares -> 1/sqrt(var + eps)
-      float dx[S][VEC];
+      // pass 2: centred squares -> 1/sqrt(var + eps) (the centred values are
+      // recomputed from the packed row below rather than held: registers
+      // decide how many rows are in flight)
 #pragma unroll
       for (int j = 0; j < S; ++j) {
         const float m = stat[piece_of(pc, j)];
-        Elem<T>::unpack(cur[j], dx[j]);
+        float dx[VEC];
+        Elem<T>::unpack(cur[j], dx);
         float a = 0.f;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          dx[j][e] -= m;
-          a += dx[j][e] * dx[j][e];
+          dx[e] -= m;
+          a += dx[e] * dx[e];
         }
         t[j] = a;
       }
@@ -351,16 +376,20 @@ __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc*
         for (int j = 0; j < S; ++j) {
           const int c = cbase + j * 64 + lane;
           if (FULL || c < nch) {
-            const float rs = stat[npc + piece_of(pc, j)];
-            float o[VEC];
+            const int pj = piece_of(pc, j);
+            const float m = stat[pj], rs = stat[npc + pj];
+            float dx[VEC], o[VEC];
+            u32x4 cj = cur[j];
+            __asm__ volatile("" : "+v"(cj));  // unpack again here instead of keeping pass 2's floats live
+            Elem<T>::unpack(cj, dx);
 #pragma unroll
             for (int e = 0; e < VEC; e += 4) {
               const f32x4 g = *(const f32x4*)(lg + (size_t)c * VEC + e);
               const f32x4 b = *(const f32x4*)(lb + (size_t)c * VEC + e);
-              o[e + 0] = act_apply<ACT>(dx[j][e + 0] * (rs * g[0]) + b[0]);
-              o[e + 1] = act_apply<ACT>(dx[j][e + 1] * (rs * g[1]) + b[1]);
-              o[e + 2] = act_apply<ACT>(dx[j][e + 2] * (rs * g[2]) + b[2]);
-              o[e + 3] = act_apply<ACT>(dx[j][e + 3] * (rs * g[3]) + b[3]);
+              o[e + 0] = act_apply<ACT>((dx[e + 0] - m) * (rs * g[0]) + b[0]);
+              o[e + 1] = act_apply<ACT>((dx[e + 1] - m) * (rs * g[1]) + b[1]);
+              o[e + 2] = act_apply<ACT>((dx[e + 2] - m) * (rs * g[2]) + b[2]);
+              o[e + 3] = act_apply<ACT>((dx[e + 3] - m) * (rs * g[3]) + b[3]);
             }
             st16_nt(yr + c * 16, Elem<T>::pack(o));
           }

@@ -337,12 +337,16 @@ static DevRows make_rows(const void* x, int64_t ldx, void* y, int64_t ldy, const
   return r;
 }
 
-// Row tiles of one member: about 32 KB of input per tile, a whole number of
-// the block's row slots.
+// Row tiles of one member: about kRowTileBytes of input per tile, a whole
+// number of the block's row slots.
+#ifndef OPTIMUS_ROW_TILE_BYTES
+#define OPTIMUS_ROW_TILE_BYTES 32768
+#endif
+static constexpr int64_t kRowTileBytes = OPTIMUS_ROW_TILE_BYTES;
 static void add_row_tiles(std::vector<RowTile>& tiles, int member, const DevRows& r, size_t s) {
   const int rpb = r.vec ? 4 * (64 / r.lanes) : 4;
   const int64_t row_bytes = std::max<int64_t>(1, (int64_t)r.cols * (int64_t)s);
-  int64_t per = std::max<int64_t>(1, 32768 / row_bytes);
+  int64_t per = std::max<int64_t>(1, kRowTileBytes / row_bytes);
   per = std::max<int64_t>(rpb, (per / rpb) * rpb);
   for (int64_t r0 = 0; r0 < r.rows; r0 += per)
     tiles.push_back(RowTile{member, (int32_t)r0, (int32_t)std::min<int64_t>(per, r.rows - r0), 0});
