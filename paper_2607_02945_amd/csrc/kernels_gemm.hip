@@ -110,13 +110,21 @@ __device__ __forceinline__ void gemm_epilogue(const f32x16 (&acc)[BM / WM / 32][
   // addresses would otherwise be kept live across the whole tile loop.
   T* const cbase = sC + (wm * TM + l32) * LDC + wn * TN + lh * 4;
   const float* const bbase = sBias + wn * TN + lh * 4;
+  // this lane's bias values, read before any staging write (the compiler
+  // cannot tell that those writes miss the bias, so reads placed after them
+  // would each wait for their own LDS round trip)
+  f32x4 bias[FN][4];
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)(bbase + j * 32 + q * 8);
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const f32x4 bv = *(const f32x4*)(bbase + j * 32 + q * 8);
+        const f32x4 bv = bias[j][q];
         float o[4];
         o[0] = act_apply<ACT>(acc[i][j][q * 4 + 0] + bv.x);
         o[1] = act_apply<ACT>(acc[i][j][q * 4 + 1] + bv.y);
@@ -566,13 +574,19 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       const int tc = wcol0 + lc * 8;  // tile column of this lane's stores
       const bool col_in = tc < Nr, col_vec = (d.vec & 2) != 0 && tc + 8 <= Nr;
       bf16_t* ybase = (bf16_t*)d.y + (int64_t)(m0 + wrow0) * d.ldy + n0 + tc + (int64_t)lrow * d.ldy;
+      // this lane's bias values, all read before the first staging write
+      f32x4 bias[S::FN][4];
+#pragma unroll
+      for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)(bput + j * 32 + q * 8);
 #pragma unroll
       for (int h = 0; h < S::NH; ++h) {
 #pragma unroll
         for (int j = 0; j < S::FN; ++j) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const f32x4 bv = *(const f32x4*)(bput + j * 32 + q * 8);
+            const f32x4 bv = bias[j][q];
             const float o0 = act_apply<ACT>(acc[h][j][q * 4 + 0] + bv.x);
             const float o1 = act_apply<ACT>(acc[h][j][q * 4 + 1] + bv.y);
             const float o2 = act_apply<ACT>(acc[h][j][q * 4 + 2] + bv.z);
