@@ -12,7 +12,8 @@ rotated over enough copies that each step reads data no longer held in the
 The roofline is taken on the op-group's dominant kernel: its plan is then
 launched `--steps` times back to back over the same rotating inputs between
 one more pair of events, and the mean launch duration divides the kernel's
-algorithmic flops or bytes. `traffic` is the HBM bytes per launch from the
+algorithmic flops or bytes; `other_kernels` does the same for every other
+launch of the op-group (e.g. the grouped LayerNorm after a grouped Linear). `traffic` is the HBM bytes per launch from the
 committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary when that was taken on
 the current kernel sources.
 
@@ -80,6 +81,9 @@ class OpGroup:
 
     def run_dominant(self, stream=None):
         self.dominant.execute("grouped", stream)
+
+    def run_plan(self, k, stream=None):
+        self.grouped[k][0].execute(self.grouped[k][1], stream)
 
 
 def build_copy(name, wl, torch, B):
@@ -354,6 +358,8 @@ def main():
     def one(i, which):
         if which == "dominant":
             ogs[i % copies].run_dominant(stream)
+        elif isinstance(which, int):
+            ogs[i % copies].run_plan(which, stream)
         else:
             ogs[i % copies].run(which, stream)
 
@@ -409,20 +415,35 @@ def main():
     out["group_tflops"] = round(flops / (ms_step * 1e-3) / 1e12, 3)
     out["group_hbm_gbs"] = round(nbytes / (ms_step * 1e-3) / 1e9, 1)
     # roofline of the dominant kernel: algorithmic work per launch / mean launch duration
-    ai = info["flops"] / max(info["bytes"], 1.0)
     ridge = PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
-    if info["flops"] > 0 and ai >= ridge:
-        ach = info["flops"] / (k_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
-                "frac": round(ach / PEAK_TFLOPS[dtype], 4)}
-    else:
-        ach = info["bytes"] / (k_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+
+    def roofline(pinfo, ms):
+        if pinfo["flops"] > 0 and pinfo["flops"] / max(pinfo["bytes"], 1.0) >= ridge:
+            ach = pinfo["flops"] / (ms * 1e-3) / 1e12
+            return {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
+                    "frac": round(ach / PEAK_TFLOPS[dtype], 4)}
+        ach = pinfo["bytes"] / (ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+    roof = roofline(info, k_ms)
     roof.update({"kernel": info["kernel"], "kernel_us": round(k_ms * 1000.0, 3),
                  "algorithmic_bytes": info["bytes"], "algorithmic_flops": info["flops"],
                  "traffic": traffic_from_profile(info["kernel"], args.workload)})
     out["roofline"] = roof
+    # the op-group's other kernels, each launched back to back the same way
+    others = []
+    for k, (plan, mode) in enumerate(ogs[0].grouped):
+        if plan is ogs[0].dominant:
+            continue
+        o_ms = timed(k, args.steps, 10)[0] / args.steps
+        pinfo = plan.info()
+        entry = roofline(pinfo, o_ms)
+        entry.update({"kernel": pinfo["kernel"], "kernel_us": round(o_ms * 1000.0, 3),
+                      "algorithmic_bytes": pinfo["bytes"], "algorithmic_flops": pinfo["flops"]})
+        others.append(entry)
+    if others:
+        out["other_kernels"] = others
     if not args.no_chain:
         csteps = max(5, min(args.steps, 50))
         c_ms, _ = timed("chain", csteps, 5)

@@ -99,6 +99,22 @@ def linear_batch_fusion(orc):
         assert _nrm(got[i], stacked[i]) < 1e-13
 
 
+def linear_shared_input(orc):
+    """Paper Table 1 batch_linear_lhs: members that share one input equal a
+    single matmul of that input with the members' weights concatenated along N
+    (numpy BLAS), split back into the members' columns."""
+    g = _rng(16)
+    M, K, Ns = 14, 24, [3, 9, 1, 6]
+    x = g.standard_normal((M, K))
+    ws = [g.standard_normal((n, K)) for n in Ns]
+    bs = [g.standard_normal(n) for n in Ns]
+    whole = x @ np.concatenate(ws).T + np.concatenate(bs)
+    got = orc.grouped_linear([x] * len(Ns), ws, bs)
+    offs = np.cumsum([0] + Ns)
+    for i in range(len(Ns)):
+        assert _nrm(got[i], whole[:, offs[i]:offs[i + 1]]) < 1e-13
+
+
 # ---------------------------------------------------------------- LayerNorm
 def layernorm_vs_torch(orc):
     """Row LayerNorm against torch.nn.functional.layer_norm in fp64."""
@@ -255,7 +271,7 @@ def split_op_cat_bad_widths(orc):
 
 ALL_PINS = [
     linear_vs_blas, linear_special_cases, linear_brute_force, linear_epilogue, linear_rows_subset,
-    linear_batch_fusion, layernorm_vs_torch, layernorm_invariants, layernorm_constant_row,
+    linear_batch_fusion, linear_shared_input, layernorm_vs_torch, layernorm_invariants, layernorm_constant_row,
     layernorm_affine, layernorm_epilogue_and_batch, pointwise_closed_forms,
     split_concat_appendix_example, split_concat_identity_random, split_op_cat_pieces, split_op_cat_tag,
     split_op_cat_bad_widths,

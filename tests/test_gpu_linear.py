@@ -164,3 +164,23 @@ def test_empty_group_and_errors():
         B.optimus_grouped_linear([x], [w], [None], [x], "none")
     assert ei.value.name == "ALIASING"
     assert torch.count_nonzero(x) == 0
+
+
+def test_shared_input_members():
+    """Members that share one input tensor (paper Table 1 batch_linear_lhs): the
+    descriptors point at the same x; outputs against the oracle and against one
+    matmul with the weights concatenated (inputs may alias each other)."""
+    say("[linear shared input]")
+    g = synth.rng(18)
+    M, K, Ns = 1000, 256, [256, 512, 64, 256]
+    x = dev(synth.to_storage(g.standard_normal((M, K)), "bf16"))
+    ws = [dev(synth.to_storage(g.standard_normal((n, K)) / np.sqrt(K), "bf16")) for n in Ns]
+    bs = [dev(synth.to_storage(g.standard_normal(n) * 0.1, "bf16")) for n in Ns]
+    ms = [(x, w, b) for w, b in zip(ws, bs)]
+    ys = _run(ms, "bf16", "relu")
+    _check(ms, ys, "bf16", "relu", "shared input")
+    whole = ORC.linear(host64(x), np.concatenate([host64(w) for w in ws]),
+                       np.concatenate([host64(b) for b in bs]), "relu")
+    offs = np.cumsum([0] + Ns)
+    for i, y in enumerate(ys):
+        assert_close(host64(y), whole[:, offs[i]:offs[i + 1]], "bf16", f"shared input member {i} vs concatenated W")
