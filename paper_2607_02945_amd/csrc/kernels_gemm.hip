@@ -401,7 +401,7 @@ __device__ __forceinline__ DmaLoads dma_first(const DevLinear* __restrict__ desc
   return dma_loads<BM, BN, NW>(d, tile.mb * BM, tile.nb * BN, dma_rot(tile, nk) * 64, lr, kch);
 }
 
-template <int BM, int BN, int WM, int WN, bool REGS, int ACT>
+template <int BM, int BN, int WM, int WN, int ACT>
 __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const DevLinear* __restrict__ descs,
                                                                        const GemmTile* __restrict__ tiles,
                                                                        int32_t num_tiles) {
@@ -421,32 +421,18 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   if ((gridDim.x & 7) == 0) t = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
 
   // Load q of one K step (q < XI: x rows, then w rows) lands at byte lds_off(q)
-  // of the stage plus 16 * lane; with REGS it goes through registers.
+  // of the stage plus 16 * lane.
   auto lds_off = [&](int q) {
     return q < S::XI ? wave * 8 * 128 + q * NW * 8 * 128 : S::XBYTES + wave * 8 * 128 + (q - S::XI) * NW * 8 * 128;
   };
   auto gofs = [&](const DmaLoads& L, int q) {
     return q < S::XI ? L.sx + q * L.xrow + L.k0 * 2 : L.sw + (q - S::XI) * L.wrow + L.k0 * 2;
   };
-  auto load_reg = [&](const DmaLoads& L, int q) {
-    const __amdgpu_buffer_rsrc_t r = q < S::XI ? __builtin_amdgcn_make_buffer_rsrc((void*)L.xp, 0, L.xbytes, 0x00020000)
-                                               : __builtin_amdgcn_make_buffer_rsrc((void*)L.wp, 0, L.wbytes, 0x00020000);
-    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)gofs(L, q), 0, 0));
-  };
-  auto put = [&](int stage, int q, const u32x4& v) { *(u32x4*)(smem + stage * S::STAGE + lds_off(q) + lane * 16) = v; };
   // every load of one K step into `stage`
   auto issue_all = [&](const DmaLoads& L, int stage) {
-    if constexpr (REGS) {
-      u32x4 R[S::NQ];
+    const i32x4 rx = make_rsrc(L.xp, L.xbytes), rw = make_rsrc(L.wp, L.wbytes);
 #pragma unroll
-      for (int q = 0; q < S::NQ; ++q) R[q] = load_reg(L, q);
-#pragma unroll
-      for (int q = 0; q < S::NQ; ++q) put(stage, q, R[q]);
-    } else {
-      const i32x4 rx = make_rsrc(L.xp, L.xbytes), rw = make_rsrc(L.wp, L.wbytes);
-#pragma unroll
-      for (int q = 0; q < S::NQ; ++q) lds_dma16(q < S::XI ? rx : rw, gofs(L, q), lds_base + stage * S::STAGE + lds_off(q));
-    }
+    for (int q = 0; q < S::NQ; ++q) lds_dma16(q < S::XI ? rx : rw, gofs(L, q), lds_base + stage * S::STAGE + lds_off(q));
   };
 
   int sbase = 0;  // stage holding the current tile's first K step
@@ -498,24 +484,15 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
         }
       };
       const bool go = L.k0 >= 0;
-      i32x4 rx, rw;
-      if constexpr (!REGS) {
-        rx = make_rsrc(L.xp, L.xbytes);
-        rw = make_rsrc(L.wp, L.wbytes);
-      }
-      u32x4 R[S::NQ];
+      const i32x4 rx = make_rsrc(L.xp, L.xbytes), rw = make_rsrc(L.wp, L.wbytes);
       frag(0, 0);
 #pragma unroll
       for (int kc = 0; kc < S::KC; ++kc) {
         if (kc + 1 < S::KC) frag(kc + 1, (kc + 1) & 1);
         if (go) {
 #pragma unroll
-          for (int q = kc * S::PER; q < (kc + 1) * S::PER && q < S::NQ; ++q) {
-            if constexpr (REGS)
-              R[q] = load_reg(L, q);
-            else
-              lds_dma16(q < S::XI ? rx : rw, gofs(L, q), lds_base + nstage * S::STAGE + lds_off(q));
-          }
+          for (int q = kc * S::PER; q < (kc + 1) * S::PER && q < S::NQ; ++q)
+            lds_dma16(q < S::XI ? rx : rw, gofs(L, q), lds_base + nstage * S::STAGE + lds_off(q));
         }
 #pragma unroll
         for (int i = 0; i < S::FM; ++i)
@@ -523,19 +500,12 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
           for (int j = 0; j < S::FN; ++j) Mfma<bf16_t>::run(a[kc & 1][j], b[kc & 1][i], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
-      if constexpr (REGS) {
-        if (go) {
-#pragma unroll
-          for (int q = 0; q < S::NQ; ++q) put(nstage, q, R[q]);
-        }
-      }
     };
 
     for (int kb = 0; kb < nk; ++kb) {
-      // this wave's loads of step kb have landed (direct-to-LDS: and its
-      // earlier stores); the barrier extends that to every wave and frees
-      // step kb - 1's stage
-      if constexpr (!REGS) wait_vmcnt<0>();
+      // this wave's loads of step kb (and its earlier stores) have landed;
+      // the barrier extends that to every wave and frees step kb - 1's stage
+      wait_vmcnt<0>();
       __syncthreads();
       const int stage = (sbase + kb) & 1;
       // the bias of this tile: the previous tile's epilogue read sBias before this barrier
@@ -617,125 +587,6 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   }
 }
 
-// ===================================================================== skinny members
-// bf16 members with N <= 64 and K <= 64, K % 8 == 0 (many tiny Linears on a
-// large batch): each is a stream of rows through a small weight matrix, bound
-// by HBM. Every wave works on its own item -- 256 rows of one member -- with no
-// workgroup barrier: it keeps the member's weight fragments and bias in
-// registers and streams the item's eight 32-row tiles with two tiles of x in
-// flight ahead of the one being multiplied; x fragments go straight from
-// global memory into MFMA operand registers (lane l holds row l % 32, k-chunk
-// l / 32 of each 16-wide k step) for v_mfma_f32_32x32x16_bf16, and each output
-// tile passes through a wave-private LDS staging tile so that rows leave in
-// whole 16-byte stores.
-#ifndef OPTIMUS_SKINNY_TILES
-#define OPTIMUS_SKINNY_TILES 2
-#endif
-constexpr int kSkinnyTiles = OPTIMUS_SKINNY_TILES;  // 32-row tiles per work item
-constexpr int kSkinnyRows = 32 * kSkinnyTiles;  // rows per work item
-constexpr int kSkinnyLdc = 72;                  // staging row (elements): 64 + 8
-#ifndef OPTIMUS_SKINNY_OCC
-#define OPTIMUS_SKINNY_OCC 4
-#endif
-
-template <int ACT>
-__global__ __launch_bounds__(256) void grouped_gemm_skinny_kernel(const DevLinear* __restrict__ descs,
-                                                                   const GemmTile* __restrict__ items,
-                                                                   int32_t num_items) {
-  __shared__ __align__(16) bf16_t stage[4][32 * kSkinnyLdc];
-  __shared__ __align__(16) float sbias[4][64];
-  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int l32 = lane & 31, lh = lane >> 5;
-  bf16_t* st = stage[wave];
-  float* sb = sbias[wave];
-  for (int it = blockIdx.x * 4 + wave; it < num_items; it += gridDim.x * 4) {
-    const GemmTile item = items[it];
-    if (item.member < 0) continue;
-    const DevLinear d = descs[item.member];
-    const int K = d.K, N = d.N;
-    const int r0 = item.mb * kSkinnyRows;
-    const int rows = min(kSkinnyRows, d.M - r0);
-    const int kfull = K >> 4;          // whole 16-wide k steps
-    const bool khalf = (K & 15) != 0;  // one more step with only k < K in the lower lane half
-    // x fragments of tile t: rows past the member are clamped to its last row
-    // (never stored); k steps past K are zero.
-    auto load_tile = [&](int t, u32x4 (&xf)[4]) {
-      const bf16_t* xr = (const bf16_t*)d.x + (int64_t)min(r0 + 32 * t + l32, d.M - 1) * d.ldx + 8 * lh;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (s < kfull || (s == kfull && khalf && lh == 0))
-          xf[s] = ld16_nt(xr + 16 * s);
-        else
-          xf[s] = u32x4{0u, 0u, 0u, 0u};
-      }
-    };
-    u32x4 ring[3][4];
-    load_tile(0, ring[0]);
-    if (32 < rows) load_tile(1, ring[1]);
-    sb[lane] = (d.bias && lane < N) ? Elem<bf16_t>::load1(d.bias, lane) : 0.f;
-    // weights: a[f][s] = w[32 f + l32][16 s + 8 lh .. + 8], zero outside N x K
-    u32x4 a[2][4];
-    const bf16_t* wl = (const bf16_t*)d.w + (int64_t)l32 * d.ldw + 8 * lh;
-    const int64_t wf = (int64_t)32 * d.ldw;
-#pragma unroll
-    for (int f = 0; f < 2; ++f)
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        a[f][s] = (32 * f + l32 < N && 16 * s + 8 * lh < K) ? ld16(wl + f * wf + 16 * s) : u32x4{0u, 0u, 0u, 0u};
-    const bool vout = (d.vec & 2) && (N % 8 == 0);
-    const int cpr = (N + 7) / 8;
-    bf16_t* yl = (bf16_t*)d.y + (int64_t)(r0 + (lane >> 3)) * d.ldy + 8 * (lane & 7);
-    const int64_t y8 = (int64_t)8 * d.ldy;
-    lds_wave_sync();  // bias staged
-#pragma unroll
-    for (int t = 0; t < kSkinnyTiles; ++t) {
-      if (32 * t >= rows) break;
-      if (t + 2 < kSkinnyTiles && 32 * (t + 2) < rows) load_tile(t + 2, ring[(t + 2) % 3]);
-      const u32x4(&xf)[4] = ring[t % 3];
-      // both 32-column blocks are computed (the second is zero when N <= 32):
-      // the MFMAs cost nothing next to the row traffic
-      f32x16 acc0 = {}, acc1 = {};
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (16 * s < K) {
-          Mfma<bf16_t>::run(a[0][s], xf[s], acc0);
-          Mfma<bf16_t>::run(a[1][s], xf[s], acc1);
-        }
-      }
-      // acc_f[4 q + e] is y row 32 t + l32, column 32 f + 8 q + 4 lh + e
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const f32x4 b0 = *(const f32x4*)(sb + 8 * q + 4 * lh);
-        const f32x4 b1 = *(const f32x4*)(sb + 32 + 8 * q + 4 * lh);
-        u32x2 p0 = {pack_bf16x2(act_apply<ACT>(acc0[4 * q + 0] + b0[0]), act_apply<ACT>(acc0[4 * q + 1] + b0[1])),
-                    pack_bf16x2(act_apply<ACT>(acc0[4 * q + 2] + b0[2]), act_apply<ACT>(acc0[4 * q + 3] + b0[3]))};
-        u32x2 p1 = {pack_bf16x2(act_apply<ACT>(acc1[4 * q + 0] + b1[0]), act_apply<ACT>(acc1[4 * q + 1] + b1[1])),
-                    pack_bf16x2(act_apply<ACT>(acc1[4 * q + 2] + b1[2]), act_apply<ACT>(acc1[4 * q + 3] + b1[3]))};
-        *(u32x2*)(st + l32 * kSkinnyLdc + 8 * q + 4 * lh) = p0;
-        *(u32x2*)(st + l32 * kSkinnyLdc + 32 + 8 * q + 4 * lh) = p1;
-      }
-      lds_wave_sync();
-      // 32 rows x N columns leave as 16-byte pieces: lane -> (row 8 p + lane / 8, piece lane % 8)
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int row = 8 * p + (lane >> 3), c = lane & 7;
-        if (32 * t + row < rows && c < cpr) {
-          bf16_t* yp = yl + (4 * t + p) * y8;
-          const bf16_t* sp = st + row * kSkinnyLdc + 8 * c;
-          if (vout) {
-            st16_nt(yp, *(const u32x4*)sp);
-          } else {
-#pragma unroll 1
-            for (int e = 0; e < 8 && 8 * c + e < N; ++e)
-              ((OPTIMUS_GLOBAL uint16_t*)yp)[e] = ((const uint16_t*)sp)[e];
-          }
-        }
-      }
-      lds_wave_sync();  // staging read before the next tile overwrites it
-    }
-  }
-}
-
 // ===================================================================== configurations
 struct GemmVariant {
   int bm, bn, threads, occ;  // occ: workgroups resident per CU (LDS / register bound)
@@ -744,10 +595,8 @@ struct GemmVariant {
 
 // 0: members with N, K <= 64 (one K step); 1: 128x128; 2: 256x256 (8 waves);
 // 3: fp32; 4: 256x256 (4 waves); 5: 256x128 (4 waves);
-// 6-9: buffer-resource pipeline (bf16, aligned rows, K % 8 == 0): 256x256
-// 8 waves direct-to-LDS, 256x256 8 waves through registers, 256x128 and
-// 128x128 4 waves direct-to-LDS;
-// 10: skinny members (bf16, N <= 64, K <= 64, K % 8 == 0, aligned rows).
+// 6-8: direct-to-LDS (bf16, aligned rows, K % 8 == 0): 256x256 8 waves,
+// 256x128 4 waves, 128x128 4 waves.
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
     {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
@@ -756,21 +605,10 @@ static const GemmVariant kVariants[] = {
     {256, 256, 256, 1, "grouped_gemm_bf16_256x256x64_w2x2_s2"},
     {256, 128, 256, 1, "grouped_gemm_bf16_256x128x64_w2x2_s2"},
     {256, 256, 512, 1, "grouped_gemm_dma_bf16_256x256x64_w2x4"},
-    {256, 256, 512, 1, "grouped_gemm_rs_bf16_256x256x64_w2x4"},
     {256, 128, 256, 1, "grouped_gemm_dma_bf16_256x128x64_w2x2"},
     {128, 128, 256, 2, "grouped_gemm_dma_bf16_128x128x64_w2x2"},
-    {kSkinnyRows, 64, 256, OPTIMUS_SKINNY_OCC, "grouped_gemm_skinny_bf16"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
-
-static bool gemm_skinny_ok(const optimus_linear_desc* d, int32_t G) {
-  for (int g = 0; g < G; ++g) {
-    if (d[g].N > 64 || d[g].K > 64 || d[g].K % 8 || d[g].ldx % 8 || d[g].ldw % 8 || ((uintptr_t)d[g].x & 15) ||
-        ((uintptr_t)d[g].w & 15))
-      return false;
-  }
-  return true;
-}
 
 // The direct-to-LDS kernels address a tile of at most 256 rows through 32-bit
 // buffer offsets below 2^31 (larger offsets mark out-of-range chunks).
@@ -808,8 +646,7 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     char* end = nullptr;
     const long want = f ? strtol(f, &end, 10) : -1;
     if (f && end && *end == 0 && want >= 0 && want < kNumVariants && want != 3) {
-      const bool dma = want >= 6 && want <= 9, skinny = want == 10;
-      if ((!dma && !skinny) || (dma && gemm_dma_ok(d, G)) || (skinny && gemm_skinny_ok(d, G))) v = (int)want;
+      if (want < 6 || gemm_dma_ok(d, G)) v = (int)want;
     }
   }
   const GemmVariant& k = kVariants[v];
@@ -844,14 +681,14 @@ static hipError_t launch_shape(optimus_act act, const DevLinear* descs, const Ge
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, bool REGS>
+template <int BM, int BN, int WM, int WN>
 static hipError_t launch_dma(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
                              hipStream_t stream) {
   using S = DmaShape<BM, BN, WM, WN>;
   const size_t smem = S::LDS_BYTES;
 #define OPTIMUS_DMA_LAUNCH(A)                                                                                      \
   {                                                                                                                \
-    auto kfn = grouped_gemm_dma_kernel<BM, BN, WM, WN, REGS, A>;                                                         \
+    auto kfn = grouped_gemm_dma_kernel<BM, BN, WM, WN, A>;                                                         \
     static bool attr_set = false;                                                                                  \
     if (smem > 65536 && !attr_set) {                                                                               \
       hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); \
@@ -882,21 +719,9 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
     case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     case 4: return launch_shape<bf16_t, 256, 256, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     case 5: return launch_shape<bf16_t, 256, 128, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 6: return launch_dma<256, 256, 2, 4, false>(act, descs, tiles, num_tiles, grid, stream);
-    case 7: return launch_dma<256, 256, 2, 4, true>(act, descs, tiles, num_tiles, grid, stream);
-    case 8: return launch_dma<256, 128, 2, 2, false>(act, descs, tiles, num_tiles, grid, stream);
-    case 9: return launch_dma<128, 128, 2, 2, false>(act, descs, tiles, num_tiles, grid, stream);
-    case 10: {
-      switch (act) {
-        case OPTIMUS_ACT_NONE: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<0>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
-        case OPTIMUS_ACT_RELU: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<1>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
-        case OPTIMUS_ACT_SIGMOID: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<2>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
-        case OPTIMUS_ACT_TANH: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<3>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
-        case OPTIMUS_ACT_SILU: hipLaunchKernelGGL((grouped_gemm_skinny_kernel<4>), dim3(grid), dim3(256), 0, stream, descs, tiles, num_tiles); break;
-        default: return hipErrorInvalidValue;
-      }
-      return hipGetLastError();
-    }
+    case 6: return launch_dma<256, 256, 2, 4>(act, descs, tiles, num_tiles, grid, stream);
+    case 7: return launch_dma<256, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 8: return launch_dma<128, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -424,15 +424,13 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
   hp.g_num_tiles = (int32_t)tiles.size();
   // workgroups resident per CU for each variant (LDS / register bound)
   const int64_t cap = (int64_t)device_cu_count() * hp.gcfg.occ;
-  // the skinny kernel hands one work item to each wave (four per workgroup)
-  const int64_t per_block = hp.gcfg.variant == 10 ? 4 : 1;
-  int64_t grid = std::min<int64_t>(((int64_t)tiles.size() + per_block - 1) / per_block, cap);
+  int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
   if (grid >= 8) grid -= grid % 8;
   hp.g_grid = (int32_t)std::max<int64_t>(1, grid);
   for (auto& c : hp.g_chain) {
     c.descs_off = hp.g_descs_off;
     c.tiles_off = hp.g_tiles_off;
-    c.grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((c.num_tiles + per_block - 1) / per_block, cap));
+    c.grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(c.num_tiles, cap));
   }
   hp.work_items = real_tiles;
   hp.grid = hp.g_grid;
