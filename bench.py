@@ -308,7 +308,7 @@ DOMINANT_KERNEL_NAME = {
 
 def kernel_symbol(label):
     """Symbol name of the kernel behind a plan's kernel label."""
-    for prefix, sym in (("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
+    for prefix, sym in (("grouped_gemm_dma", "grouped_gemm_dma_kernel"),
                         ("grouped_gemm", "grouped_gemm_kernel"), ("split_op_cat_fused", "split_op_cat_kernel"),
                         ("grouped_layernorm", "grouped_layernorm_kernel"), ("grouped_pointwise", "grouped_pointwise_kernel")):
         if label.startswith(prefix):
