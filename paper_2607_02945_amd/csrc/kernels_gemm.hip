@@ -632,12 +632,16 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
       maxK = d[g].K > maxK ? d[g].K : maxK;
       tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
     }
+    // measured over groups of 64 to 4096 256x256 tiles: the 256x256 tile wins
+    // from half a tile per CU on; smaller groups need the 128x128 tile to
+    // spread over the CUs
+    const bool dma = gemm_dma_ok(d, G);
     if (maxN <= 64 && maxK <= 64)
       v = 0;
-    else if (tiles256 >= 2.0 * device_cu_count())
-      v = gemm_dma_ok(d, G) ? 6 : 2;
+    else if (tiles256 >= 0.5 * device_cu_count())
+      v = dma ? 6 : 2;
     else
-      v = 1;
+      v = dma ? 8 : 1;
   }
   // OPTIMUS_GEMM_VARIANT=<n> pins the bf16 tile shape (tests and tuning); the
   // direct-to-LDS variants need every member's x / w rows 16-byte aligned and K % 8 == 0.
