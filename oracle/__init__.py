@@ -164,6 +164,13 @@ class Oracle:
             raise ValueError("oracle_split_op_cat: widths do not sum to D")
         return y
 
+    def linear_layernorm(self, x, w, bias, gamma=None, beta=None, eps=1e-5, act="none") -> np.ndarray:
+        """A Linear and the row-wise LayerNorm that consumes its output, fused
+        (paper Sec. 3.2, vertical optimization of consecutive operators): the
+        plain composition LN(X W^T + bias) over each output row, then act, in
+        fp64 with no rounding of the intermediate."""
+        return self.layernorm(self.linear(x, w, bias, "none"), gamma, beta, eps, act)
+
     def num_threads(self) -> int:
         return self.lib.oracle_num_threads()
 
@@ -175,6 +182,10 @@ class Oracle:
 
     def grouped_layernorm(self, xs, gammas, betas, eps=1e-5, act="none"):
         return [self.layernorm(x, g, b, eps, act) for x, g, b in zip(xs, gammas, betas)]
+
+    def grouped_linear_layernorm(self, xs, ws, biases, gammas, betas, eps=1e-5, act="none"):
+        return [self.linear_layernorm(x, w, b, g, be, eps, act)
+                for x, w, b, g, be in zip(xs, ws, biases, gammas, betas)]
 
     def grouped_pointwise(self, xs, act):
         return [self.pointwise(x, act) for x in xs]

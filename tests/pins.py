@@ -168,6 +168,44 @@ def layernorm_epilogue_and_batch(orc):
         assert _nrm(got[i], np.tanh(stack[i])) < 1e-12
 
 
+# ---------------------------------------------------------------- Linear + LayerNorm
+def linear_layernorm_reductions(orc):
+    """The fused Linear + LayerNorm reduces to a plain LayerNorm when W is the
+    identity: with bias 0 it equals LN(x) (+ act), with a bias it equals
+    LN(x + bias); the activation comes after the normalisation, not before."""
+    g = _rng(17)
+    x = g.standard_normal((12, 20)) * 2 + 0.5
+    eye = np.eye(20)
+    gm, bt = g.uniform(0.5, 1.5, 20), g.standard_normal(20)
+    for act in ("none", "tanh", "silu"):
+        got = orc.linear_layernorm(x, eye, np.zeros(20), gm, bt, 1e-5, act)
+        assert _nrm(got, orc.layernorm(x, gm, bt, 1e-5, act)) < 1e-14, act
+    b = g.standard_normal(20)
+    assert _nrm(orc.linear_layernorm(x, eye, b, gm, bt, 1e-5), orc.layernorm(x + b, gm, bt, 1e-5)) < 1e-14
+    t = torch.nn.functional.layer_norm(torch.from_numpy(x @ eye.T + b), (20,), torch.from_numpy(gm),
+                                       torch.from_numpy(bt), eps=1e-5).numpy()
+    assert _nrm(orc.linear_layernorm(x, eye, b, gm, bt, 1e-5), t) < 1e-12
+
+
+def linear_layernorm_invariants(orc):
+    """gamma=1, beta=0 over a real Linear: each output row has mean 0 and biased
+    variance s2/(s2+eps), s2 the variance of the Linear's row (numpy BLAS);
+    a weight matrix whose rows are all equal (and a constant bias) makes every
+    output row constant, so the result is beta exactly."""
+    g = _rng(18)
+    x, w, b = g.standard_normal((9, 16)), g.standard_normal((24, 16)), g.standard_normal(24)
+    y = orc.linear_layernorm(x, w, b, np.ones(24), np.zeros(24), 1e-5)
+    s2 = (x @ w.T + b).var(axis=1)
+    assert np.max(np.abs(y.mean(axis=1))) < 1e-12
+    assert np.max(np.abs(y.var(axis=1) - s2 / (s2 + 1e-5))) < 1e-12
+    # integer x and w: every dot product, sum and mean of a row is exact
+    x = g.integers(-3, 4, (9, 16)).astype(np.float64)
+    wc = np.broadcast_to(g.integers(-3, 4, 16).astype(np.float64), (24, 16))
+    bt = np.linspace(-1, 1, 24)
+    yc = orc.linear_layernorm(x, wc, np.full(24, 0.25), np.full(24, 2.0), bt, 1e-5)
+    assert np.array_equal(yc, np.broadcast_to(bt, (9, 24)))
+
+
 # ---------------------------------------------------------------- pointwise
 def pointwise_closed_forms(orc):
     """Values at 0, symmetries, the tanh/sigmoid identity, saturation, numpy forms."""
@@ -272,7 +310,8 @@ def split_op_cat_bad_widths(orc):
 ALL_PINS = [
     linear_vs_blas, linear_special_cases, linear_brute_force, linear_epilogue, linear_rows_subset,
     linear_batch_fusion, linear_shared_input, layernorm_vs_torch, layernorm_invariants, layernorm_constant_row,
-    layernorm_affine, layernorm_epilogue_and_batch, pointwise_closed_forms,
+    layernorm_affine, layernorm_epilogue_and_batch, linear_layernorm_reductions, linear_layernorm_invariants,
+    pointwise_closed_forms,
     split_concat_appendix_example, split_concat_identity_random, split_op_cat_pieces, split_op_cat_tag,
     split_op_cat_bad_widths,
 ]

@@ -52,3 +52,27 @@ def test_pins_catch_mutant(tmp_path, name, find, repl):
         except AssertionError:
             caught.append(pin.__name__)
     assert caught, f"no pin catches the planted mistake {name}"
+
+
+# Plausible mistakes in the fused Linear + LayerNorm composition.
+COMPOSITION_MUTANTS = {
+    "act_before_layernorm": lambda o, x, w, b, g, be, eps, act: o.layernorm(o.linear(x, w, b, act), g, be, eps),
+    "bias_dropped": lambda o, x, w, b, g, be, eps, act: o.layernorm(o.linear(x, w, None), g, be, eps, act),
+    "gamma_beta_swapped": lambda o, x, w, b, g, be, eps, act: o.layernorm(o.linear(x, w, b), be, g, eps, act),
+    "no_normalisation": lambda o, x, w, b, g, be, eps, act: o.pointwise(o.linear(x, w, b) * (1 if g is None else g)
+                                                                         + (0 if be is None else be), act),
+}
+
+
+@pytest.mark.parametrize("name", list(COMPOSITION_MUTANTS))
+def test_pins_catch_composition_mutant(name):
+    orc = oracle.Oracle()
+    bad = COMPOSITION_MUTANTS[name]
+    orc.linear_layernorm = lambda x, w, b, g=None, be=None, eps=1e-5, act="none": bad(orc, x, w, b, g, be, eps, act)
+    caught = []
+    for pin in (pins.linear_layernorm_reductions, pins.linear_layernorm_invariants):
+        try:
+            pin(orc)
+        except AssertionError:
+            caught.append(pin.__name__)
+    assert caught, f"no pin catches the planted mistake {name}"
