@@ -9,13 +9,13 @@ rotated over enough copies that each step reads data no longer held in the
 256 MB last-level cache. Prints one JSON line.
 
 `value` is the mean time of the timed steps between one pair of HIP events.
-The roofline is taken on the op-group's dominant kernel: its plan is then
-launched `--steps` times back to back over the same rotating inputs between
-one more pair of events, and the mean launch duration divides the kernel's
-algorithmic flops or bytes; `other_kernels` does the same for every other
-launch of the op-group (e.g. the grouped LayerNorm after a grouped Linear). `traffic` is the HBM bytes per launch from the
-committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary when that was taken on
-the current kernel sources.
+Then every launch of the op-group is run `--steps` times back to back over
+the same rotating inputs between one more pair of events; the slowest is the
+dominant kernel, whose mean launch duration divides its algorithmic flops or
+bytes for `roofline`, and `other_kernels` lists the rest (e.g. the grouped
+LayerNorm after a grouped Linear). `traffic` is the HBM bytes per launch from
+the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary when that was taken
+on the current kernel sources.
 
 Workloads (the seeded groups of paper_2607_02945_amd.synth): launch_bound
 (default; G=256 bf16 Linear + sigmoid, B=2048), tiny_group, split_op_cat,
@@ -39,6 +39,7 @@ PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 CACHE_BYTES = 512 << 20  # rotate inputs over at least this much memory per step cycle
 COPY_BYTES = 1 << 30     # the calibration copy: 1 GiB read and 1 GiB written, far beyond the caches
 WARMUP_SECONDS = 0.3
+LN_FUSE_MAX_N = {"fp32": 128, "bf16": 256}  # widest row the GEMM epilogue can normalise
 
 
 def parse():
@@ -60,27 +61,25 @@ def parse():
                     help="turn four rocprofv3 --pmc output folders (FETCH_SIZE and WRITE_SIZE of this workload's "
                          "bench run and of --copy-probe) into profiles/<kernel>__<workload>.pmc.json; no GPU needed")
     ap.add_argument("--pmc-command", default="", help="command line recorded in the --pmc-summary output")
+    ap.add_argument("--only-plan", type=int, default=None, metavar="K",
+                    help="time only launch K of the op-group (roofline.plan_index of a bench line picks the "
+                         "dominant one), for profiler runs")
     return ap.parse_args()
 
 
 # ---------------------------------------------------------------------- op-groups
 class OpGroup:
     """Plans for one copy of a workload: `grouped` runs the optimized program,
-    `chain` the per-op launch chain; `dominant` is the plan of the kernel that
-    dominates the grouped time."""
+    `chain` the per-op launch chain."""
 
     def __init__(self):
         self.grouped = []      # list of (plan, mode)
         self.chain = []        # list of (plan, mode)
         self.horizontal = []   # split-op-cat only: horizontal fusion without the vertical rewrite
-        self.dominant = None
 
     def run(self, which, stream=None):
         for plan, mode in getattr(self, which):
             plan.execute(mode, stream)
-
-    def run_dominant(self, stream=None):
-        self.dominant.execute("grouped", stream)
 
     def run_plan(self, k, stream=None):
         self.grouped[k][0].execute(self.grouped[k][1], stream)
@@ -104,7 +103,6 @@ def build_copy(name, wl, torch, B):
             lin0 = B.optimus_plan_linear(xs, ws, bs, y1, "none")
             pw = B.optimus_plan_pointwise(y1, ys, wl.act)
             og.chain = [(lin0, "chain"), (pw, "chain")]
-            og.dominant = lin
             og.keep = (xs, ws, bs, ys, y1)
         else:
             zs = [torch.empty_like(y) for y in ys]
@@ -112,14 +110,16 @@ def build_copy(name, wl, torch, B):
             be = [cu(b) for b in wl.betas]
             lin = B.optimus_plan_linear(xs, ws, bs, ys, "none")
             ln = B.optimus_plan_layernorm(ys, zs, gs, be, wl.eps, wl.act)
-            og.grouped = [(lin, "grouped"), (ln, "grouped")]
+            if max(m.N for m in wl.members) <= LN_FUSE_MAX_N[wl.dtype]:
+                # the LayerNorm rides in the GEMM epilogue: one launch
+                og.grouped = [(B.optimus_plan_linear_layernorm(xs, ws, bs, zs, gs, be, wl.eps, wl.act), "grouped")]
+            else:
+                og.grouped = [(lin, "grouped"), (ln, "grouped")]
             z1 = [torch.empty_like(y) for y in ys]
             ln0 = B.optimus_plan_layernorm(ys, z1, gs, be, wl.eps, "none")
             pw = B.optimus_plan_pointwise(z1, zs, wl.act)
             og.chain = [(lin, "chain"), (ln0, "chain"), (pw, "chain")]
-            og.dominant = lin
             og.keep = (xs, ws, bs, ys, zs, gs, be, z1)
-        og.plans = [lin]
     elif name == "split_op_cat":
         x = cu(wl.x)
         y = torch.empty_like(x)
@@ -129,7 +129,6 @@ def build_copy(name, wl, torch, B):
         og.grouped = [(soc, "grouped")]
         og.chain = [(soc, "chain")]
         og.horizontal = [(soc, "horizontal")]
-        og.dominant = soc
         og.keep = (x, y, gs, bs)
     elif name == "towers":
         T = wl.towers
@@ -142,12 +141,13 @@ def build_copy(name, wl, torch, B):
         l1 = B.optimus_plan_linear(xs, w1, b1, h, "relu")
         l2 = B.optimus_plan_linear(h, w2, b2, o, "none")
         ln = B.optimus_plan_layernorm(o, z, gm, be, wl.eps, "none")
-        og.grouped = [(l1, "grouped"), (l2, "grouped"), (ln, "grouped")]
+        # layer 2 (N = 256) with the LayerNorm in its epilogue: two launches
+        l2ln = B.optimus_plan_linear_layernorm(h, w2, b2, z, gm, be, wl.eps, "none")
+        og.grouped = [(l1, "grouped"), (l2ln, "grouped")]
         h0 = [torch.empty_like(v) for v in h]
         l1n = B.optimus_plan_linear(xs, w1, b1, h0, "none")
         relu = B.optimus_plan_pointwise(h0, h, "relu")
         og.chain = [(l1n, "chain"), (relu, "chain"), (l2, "chain"), (ln, "chain")]
-        og.dominant = l1
         og.keep = (xs, h, o, z, w1, b1, w2, b2, gm, be, h0)
     return og
 
@@ -255,10 +255,13 @@ def _pmc_per_dispatch(folder, counter, kernel_substr):
 
 def pmc_summary(args):
     """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the workload's dominant
-    kernel, each scaled by what the same counter reads for a copy of known
-    size, as HBM bytes per launch."""
+    kernel (the one the committed bench line names; the counter runs launch
+    only its plan, --only-plan), each scaled by what the same counter reads for
+    a copy of known size, as HBM bytes per launch."""
     name = args.workload
-    kernel = DOMINANT_KERNEL_NAME[name]
+    line = os.path.join(ROOT, "profiles", "bench", f"bench_{name}.json")
+    with open(line) as f:
+        kernel = kernel_symbol(json.loads(f.read().splitlines()[-1])["roofline"]["kernel"])
     f_dir, w_dir, cf_dir, cw_dir = args.pmc_summary
     fetch, nf = _pmc_per_dispatch(f_dir, "FETCH_SIZE", kernel)
     write, nw = _pmc_per_dispatch(w_dir, "WRITE_SIZE", kernel)
@@ -293,17 +296,6 @@ def copy_probe():
         torch.bitwise_not(a, out=b)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes": COPY_BYTES, "copies": 5}))
-
-
-# The kernel whose launches the roofline is taken on, per workload: the
-# symbol name (up to its template arguments) of the kernel the plan picks.
-DOMINANT_KERNEL_NAME = {
-    "launch_bound": "grouped_gemm_kernel",
-    "tiny_group": "grouped_gemm_kernel",
-    "split_op_cat": "split_op_cat_kernel",
-    "towers": "grouped_gemm_dma_kernel",
-    "large_group": "grouped_gemm_dma_kernel",
-}
 
 
 def kernel_symbol(label):
@@ -356,9 +348,7 @@ def main():
     torch.cuda.synchronize()
 
     def one(i, which):
-        if which == "dominant":
-            ogs[i % copies].run_dominant(stream)
-        elif isinstance(which, int):
+        if isinstance(which, int):
             ogs[i % copies].run_plan(which, stream)
         else:
             ogs[i % copies].run(which, stream)
@@ -392,14 +382,26 @@ def main():
         torch.cuda.synchronize()
         return t_start.elapsed_time(t_end), time.perf_counter() - w0
 
+    if args.only_plan is not None:
+        # one launch of the op-group alone (for rocprofv3 runs that must see
+        # only the dominant kernel): default warm-up, then --steps launches
+        k = args.only_plan
+        warm(k, args.warmup)
+        k_ms = timed(k, args.steps, 0)[0] / args.steps
+        print(json.dumps({"workload": args.workload, "plan_index": k, "kernel": ogs[0].grouped[k][0].info()["kernel"],
+                          "steps": args.steps, "kernel_us": round(k_ms * 1000.0, 3)}), flush=True)
+        return
+
     warmed = warm("grouped", args.warmup)
     total_ms, wall = timed("grouped", args.steps, 0)
-    # the dominant kernel alone, launched back to back over the same inputs:
-    # its mean launch duration (one event pair, so no per-launch event cost)
-    k_total_ms, _ = timed("dominant", args.steps, 10)
-    k_ms = k_total_ms / args.steps
+    # every launch of the op-group alone, launched back to back over the same
+    # inputs: its mean launch duration (one event pair, so no per-launch event
+    # cost); the slowest is the dominant kernel
+    plan_ms = [timed(k, args.steps, 10)[0] / args.steps for k in range(len(ogs[0].grouped))]
+    kd = max(range(len(plan_ms)), key=lambda k: plan_ms[k])
+    k_ms = plan_ms[kd]
     ms_step = total_ms / args.steps
-    info = ogs[0].dominant.info()
+    info = ogs[0].grouped[kd][0].info()
     launches = sum(p.info()["launches"] for p, _ in ogs[0].grouped)
     out = {
         "metric": METRIC, "value": round(ms_step * 1000.0, 3), "unit": "µs", "n_gpus": 1,
@@ -427,16 +429,16 @@ def main():
                 "frac": round(ach / HBM_PEAK_GBS, 4)}
 
     roof = roofline(info, k_ms)
-    roof.update({"kernel": info["kernel"], "kernel_us": round(k_ms * 1000.0, 3),
+    roof.update({"kernel": info["kernel"], "plan_index": kd, "kernel_us": round(k_ms * 1000.0, 3),
                  "algorithmic_bytes": info["bytes"], "algorithmic_flops": info["flops"],
                  "traffic": traffic_from_profile(info["kernel"], args.workload)})
     out["roofline"] = roof
     # the op-group's other kernels, each launched back to back the same way
     others = []
     for k, (plan, mode) in enumerate(ogs[0].grouped):
-        if plan is ogs[0].dominant:
+        if k == kd:
             continue
-        o_ms = timed(k, args.steps, 10)[0] / args.steps
+        o_ms = plan_ms[k]
         pinfo = plan.info()
         entry = roofline(pinfo, o_ms)
         entry.update({"kernel": pinfo["kernel"], "kernel_us": round(o_ms * 1000.0, 3),

@@ -160,6 +160,21 @@ typedef struct {
 optimus_status optimus_grouped_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
                                       optimus_act epilogue, optimus_stream_t stream);
 
+/* Grouped Linear with the row-wise LayerNorm that consumes each member's
+ * output fused into the same launch (Sec. 3.2: vertical optimization of two
+ * consecutive operators, applied to a horizontally fused group):
+ *   y[M][N] = act( LN_row( x . w^T + bias ) * gamma + beta )
+ * mean and biased variance of each output row over its N values, in fp32 on
+ * the unrounded accumulator; x . w^T + bias is never written out. gamma,
+ * beta: host arrays of G device pointers ([N_g] each, the group's dtype; a
+ * NULL entry means 1 / 0), or NULL arrays. One output tile holds whole rows,
+ * so N_g <= 256 for bf16 and N_g <= 128 for fp32; a wider member returns
+ * OPTIMUS_ERR_UNSUPPORTED (use optimus_grouped_linear then
+ * optimus_grouped_layernorm). eps >= 0 and finite, else INVALID_ARG. */
+optimus_status optimus_grouped_linear_layernorm(const optimus_linear_desc* d, const void* const* gamma,
+                                                const void* const* beta, int32_t G, optimus_dtype dt, float eps,
+                                                optimus_act epilogue, optimus_stream_t stream);
+
 /* Grouped row-wise LayerNorm (Table 1 batch_layernorm), optional fused activation. */
 optimus_status optimus_grouped_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
                                          optimus_act epilogue, optimus_stream_t stream);
@@ -184,6 +199,9 @@ typedef struct optimus_plan_s* optimus_plan;
 
 optimus_status optimus_plan_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
                                    optimus_act epilogue, optimus_plan* out);
+optimus_status optimus_plan_linear_layernorm(const optimus_linear_desc* d, const void* const* gamma,
+                                             const void* const* beta, int32_t G, optimus_dtype dt, float eps,
+                                             optimus_act epilogue, optimus_plan* out);
 optimus_status optimus_plan_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
                                       optimus_act epilogue, optimus_plan* out);
 optimus_status optimus_plan_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt,
@@ -220,7 +238,7 @@ void optimus_plan_destroy(optimus_plan plan);
  * once per tensor element read or written (inputs, weights, bias, gamma/beta,
  * outputs), never padding, re-reads or temporaries. */
 typedef struct {
-  int32_t kind;            /* 0 linear, 1 layernorm, 2 pointwise, 3 split_op_cat */
+  int32_t kind;            /* 0 linear, 1 layernorm, 2 pointwise, 3 split_op_cat, 4 linear_layernorm */
   int32_t group_size;      /* G, or n_slices */
   int32_t launches;        /* kernel launches per GROUPED execute (1) */
   int32_t chain_launches;  /* kernel launches per CHAIN execute */
@@ -238,6 +256,9 @@ optimus_status optimus_plan_get_info(optimus_plan plan, optimus_plan_info* out);
  * Descriptor validation with no device access (no HIP call is made): the
  * same checks the entry points above run before launching. */
 optimus_status optimus_validate_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
+optimus_status optimus_validate_linear_layernorm(const optimus_linear_desc* d, const void* const* gamma,
+                                                 const void* const* beta, int32_t G, optimus_dtype dt, float eps,
+                                                 optimus_act act);
 optimus_status optimus_validate_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
 optimus_status optimus_validate_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
 optimus_status optimus_validate_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt);

@@ -54,10 +54,13 @@ class PlanInfo(ctypes.Structure):
 
 # Every symbol include/optimus.h declares.
 EXPORTS = [
-    "optimus_grouped_linear", "optimus_grouped_layernorm", "optimus_grouped_pointwise", "optimus_split_op_cat",
-    "optimus_plan_linear", "optimus_plan_layernorm", "optimus_plan_pointwise", "optimus_plan_split_op_cat",
+    "optimus_grouped_linear", "optimus_grouped_linear_layernorm", "optimus_grouped_layernorm",
+    "optimus_grouped_pointwise", "optimus_split_op_cat",
+    "optimus_plan_linear", "optimus_plan_linear_layernorm", "optimus_plan_layernorm", "optimus_plan_pointwise",
+    "optimus_plan_split_op_cat",
     "optimus_plan_execute", "optimus_plan_execute_mode", "optimus_plan_destroy", "optimus_plan_get_info",
-    "optimus_validate_linear", "optimus_validate_layernorm", "optimus_validate_pointwise",
+    "optimus_validate_linear", "optimus_validate_linear_layernorm", "optimus_validate_layernorm",
+    "optimus_validate_pointwise",
     "optimus_validate_split_op_cat", "optimus_last_error", "optimus_version",
 ]
 
@@ -83,10 +86,14 @@ def lib() -> ctypes.CDLL:
         st = ctypes.c_int
         sig = {
             "optimus_grouped_linear": (st, [P(LinearDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
+            "optimus_grouped_linear_layernorm": (st, [P(LinearDesc), P(c_vp), P(c_vp), c_i32, ctypes.c_int,
+                                                      ctypes.c_float, ctypes.c_int, c_vp]),
             "optimus_grouped_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
             "optimus_grouped_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
             "optimus_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int, c_vp]),
             "optimus_plan_linear": (st, [P(LinearDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
+            "optimus_plan_linear_layernorm": (st, [P(LinearDesc), P(c_vp), P(c_vp), c_i32, ctypes.c_int,
+                                                   ctypes.c_float, ctypes.c_int, P(c_vp)]),
             "optimus_plan_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
             "optimus_plan_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
             "optimus_plan_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int, P(c_vp)]),
@@ -95,6 +102,8 @@ def lib() -> ctypes.CDLL:
             "optimus_plan_destroy": (None, [c_vp]),
             "optimus_plan_get_info": (st, [c_vp, P(PlanInfo)]),
             "optimus_validate_linear": (st, [P(LinearDesc), c_i32, ctypes.c_int, ctypes.c_int]),
+            "optimus_validate_linear_layernorm": (st, [P(LinearDesc), P(c_vp), P(c_vp), c_i32, ctypes.c_int,
+                                                       ctypes.c_float, ctypes.c_int]),
             "optimus_validate_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int]),
             "optimus_validate_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int]),
             "optimus_validate_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int]),
@@ -199,6 +208,21 @@ def optimus_grouped_linear(xs: Sequence[torch.Tensor], ws, biases, ys, act="none
     check(lib().optimus_grouped_linear(d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act), _stream(stream)))
 
 
+def _ptrs(ts, G):
+    """Host array of G device pointers (None entries -> NULL), or None."""
+    return None if ts is None else (c_vp * max(G, 1))(*[_ptr(t) for t in ts])
+
+
+def optimus_grouped_linear_layernorm(xs, ws, biases, ys, gammas=None, betas=None, eps=1e-5, act="none",
+                                     stream=None) -> None:
+    """y_g = act(LayerNorm_row(x_g w_g^T + b_g) * gamma_g + beta_g) for every member, one launch."""
+    d = linear_descs(xs, ws, biases, ys)
+    G = len(xs)
+    check(lib().optimus_grouped_linear_layernorm(d, _ptrs(gammas, G), _ptrs(betas, G), G,
+                                                 dtype_code(xs[0]) if xs else BF16, float(eps), _act(act),
+                                                 _stream(stream)))
+
+
 def optimus_grouped_layernorm(xs, ys, gammas=None, betas=None, eps=1e-5, act="none", stream=None) -> None:
     d = layernorm_descs(xs, ys, gammas, betas, eps)
     check(lib().optimus_grouped_layernorm(d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act), _stream(stream)))
@@ -258,6 +282,14 @@ def optimus_plan_linear(xs, ws, biases, ys, act="none") -> Plan:
                  keep=(list(xs), list(ws), biases, list(ys)))
 
 
+def optimus_plan_linear_layernorm(xs, ws, biases, ys, gammas=None, betas=None, eps=1e-5, act="none") -> Plan:
+    d = linear_descs(xs, ws, biases, ys)
+    G = len(xs)
+    return _plan(lib().optimus_plan_linear_layernorm, d, _ptrs(gammas, G), _ptrs(betas, G), G,
+                 dtype_code(xs[0]) if xs else BF16, float(eps), _act(act),
+                 keep=(list(xs), list(ws), biases, list(ys), gammas, betas))
+
+
 def optimus_plan_layernorm(xs, ys, gammas=None, betas=None, eps=1e-5, act="none") -> Plan:
     d = layernorm_descs(xs, ys, gammas, betas, eps)
     return _plan(lib().optimus_plan_layernorm, d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
@@ -280,6 +312,12 @@ def optimus_plan_split_op_cat(inp, out, widths, gammas=None, betas=None, apply_l
 # ------------------------------------------------------------------ host-only validation
 def optimus_validate_linear(descs: ctypes.Array, G: int, dtype: int, act="none") -> int:
     return lib().optimus_validate_linear(descs, G, dtype, _act(act))
+
+
+def optimus_validate_linear_layernorm(descs: ctypes.Array, gammas, betas, G: int, dtype: int, eps=1e-5,
+                                      act="none") -> int:
+    """gammas / betas: host arrays of device pointers (ctypes c_void_p arrays) or None."""
+    return lib().optimus_validate_linear_layernorm(descs, gammas, betas, G, dtype, float(eps), _act(act))
 
 
 def optimus_validate_layernorm(descs: ctypes.Array, G: int, dtype: int, act="none") -> int:

@@ -66,7 +66,11 @@ struct GemmShape {
   static constexpr int STAGE_ELEMS = (BM + BN) * LDK;
   static constexpr size_t LDS_BYTES_AB = (size_t)STAGES * STAGE_ELEMS * sizeof(T);
   static constexpr size_t LDS_BYTES_C = (size_t)BM * LDC * sizeof(T);
-  static constexpr size_t LDS_BYTES = (LDS_BYTES_AB > LDS_BYTES_C ? LDS_BYTES_AB : LDS_BYTES_C) + BN * sizeof(float);
+  static constexpr size_t LDS_MAIN = LDS_BYTES_AB > LDS_BYTES_C ? LDS_BYTES_AB : LDS_BYTES_C;
+  // then fp32 [BN] bias; with a fused LayerNorm also [BN] gamma, [BN] beta and
+  // two [BM][WN] row-partial buffers
+  static constexpr size_t LDS_BYTES = LDS_MAIN + BN * sizeof(float);
+  static constexpr size_t LDS_BYTES_LN = LDS_MAIN + 3 * BN * sizeof(float) + 2 * BM * WN * sizeof(float);
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
   static_assert((BM * CPR) % NT == 0 && (BN * CPR) % NT == 0, "staging must divide evenly");
   static_assert(BK % (2 * VEC) == 0, "BK must hold whole chunk pairs");
@@ -93,15 +97,141 @@ __device__ __forceinline__ u32x4 load_chunk(const void* base, int64_t ld, int ro
   return v;
 }
 
+// Fused LayerNorm over each output row of a tile that holds whole rows
+// (BN >= N, so n0 = 0): adds the bias to the accumulators, takes every row's
+// mean and biased variance in two passes -- lane pair, then the WN waves that
+// share the row, through `red` ([2][BM][WN]) -- and leaves
+// (v - mean) / sqrt(var + eps) * gamma + beta in acc, in fp32 on the unrounded
+// accumulator. Columns past N hold exact zeros (zero weights and bias), so
+// they add nothing to the sum and are masked out of the centred squares.
+// acc[i][j][r] holds row wm*TM + 32 i + (lane % 32), column
+// wn*TN + 32 j + 8 (r / 4) + 4 (lane / 32) + (r % 4).
+template <int BM, int BN, int WM, int WN>
+__device__ __forceinline__ void ln_rows(f32x16 (&acc)[BM / WM / 32][BN / WN / 32], const float* sBias,
+                                        const float* sGamma, const float* sBeta, float* red, const DevLinear& d) {
+  constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN, l32 = lane & 31, lh = lane >> 5;
+  const int c0 = wn * TN + lh * 4;  // this lane's first column
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 bv = *(const f32x4*)(sBias + c0 + j * 32 + q * 8);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        acc[i][j][q * 4 + 0] += bv.x;
+        acc[i][j][q * 4 + 1] += bv.y;
+        acc[i][j][q * 4 + 2] += bv.z;
+        acc[i][j][q * 4 + 3] += bv.w;
+      }
+    }
+  float* red1 = red;
+  float* red2 = red + BM * WN;
+  float part[FM], mu[FM], rs[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    float t = 0.f;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) t += acc[i][j][r];
+    part[i] = t + __shfl_xor(t, 32);
+  }
+  if (lh == 0)
+#pragma unroll
+    for (int i = 0; i < FM; ++i) red1[(wm * TM + i * 32 + l32) * WN + wn] = part[i];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < WN; ++w) t += red1[(wm * TM + i * 32 + l32) * WN + w];
+    mu[i] = t * d.inv_n;
+  }
+  if (d.N >= BN) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      float t = 0.f;
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float c = acc[i][j][r] - mu[i];
+          t += c * c;
+        }
+      part[i] = t;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      float t = 0.f;
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float c = c0 + j * 32 + (r >> 2) * 8 + (r & 3) < d.N ? acc[i][j][r] - mu[i] : 0.f;
+          t += c * c;
+        }
+      part[i] = t;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < FM; ++i) part[i] += __shfl_xor(part[i], 32);
+  if (lh == 0)
+#pragma unroll
+    for (int i = 0; i < FM; ++i) red2[(wm * TM + i * 32 + l32) * WN + wn] = part[i];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < WN; ++w) t += red2[(wm * TM + i * 32 + l32) * WN + w];
+    rs[i] = __builtin_amdgcn_rsqf(t * d.inv_n + d.eps);
+  }
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 gv = *(const f32x4*)(sGamma + c0 + j * 32 + q * 8);
+      const f32x4 bv = *(const f32x4*)(sBeta + c0 + j * 32 + q * 8);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        acc[i][j][q * 4 + 0] = (acc[i][j][q * 4 + 0] - mu[i]) * rs[i] * gv.x + bv.x;
+        acc[i][j][q * 4 + 1] = (acc[i][j][q * 4 + 1] - mu[i]) * rs[i] * gv.y + bv.y;
+        acc[i][j][q * 4 + 2] = (acc[i][j][q * 4 + 2] - mu[i]) * rs[i] * gv.z + bv.z;
+        acc[i][j][q * 4 + 3] = (acc[i][j][q * 4 + 3] - mu[i]) * rs[i] * gv.w + bv.w;
+      }
+    }
+}
+
+// The fp32 per-column parameters of a tile: bias and, for a fused LayerNorm,
+// gamma (1 when absent) and beta (0), zero past the member's last column.
+template <typename T, int BN, bool LN>
+__device__ __forceinline__ void load_col_params(float* sBias, float* sGamma, float* sBeta, const DevLinear& d, int n0,
+                                                int Nr) {
+  const int tid = threadIdx.x;
+  if (tid < BN) {
+    sBias[tid] = (d.bias && tid < Nr) ? Elem<T>::load1(d.bias, n0 + tid) : 0.f;
+    if constexpr (LN) {
+      sGamma[tid] = tid < Nr ? (d.gamma ? Elem<T>::load1(d.gamma, tid) : 1.f) : 0.f;
+      sBeta[tid] = (d.beta && tid < Nr) ? Elem<T>::load1(d.beta, tid) : 0.f;
+    }
+  }
+}
+
 // Epilogue shared by the GEMM kernels: bias + activation + rounding into the
 // LDS staging tile sC ([BM][LDC], reusing the operand area), then whole
 // 16-byte pieces of y rows leave in coalesced stores, masked at the M/N tails.
+// ACT bit 3 set: the bias was added and the row LayerNorm applied in acc.
 // acc[i][j][r] holds y row m = wm*TM + 32 i + (lane % 32) and column
 // n = wn*TN + 32 j + 8 (r / 4) + 4 (lane / 32) + (r % 4) (A operand = weights).
-template <typename T, int BM, int BN, int WM, int WN, int LDC, int ACT>
+template <typename T, int BM, int BN, int WM, int WN, int LDC, int ACTX>
 __device__ __forceinline__ void gemm_epilogue(const f32x16 (&acc)[BM / WM / 32][BN / WN / 32], T* sC,
                                               const float* sBias, const DevLinear& d, int m0, int n0, int Mr,
                                               int Nr) {
+  constexpr int ACT = ACTX & 7;
+  constexpr bool LN = (ACTX & 8) != 0;
   constexpr int VEC = Elem<T>::VEC, NT = WM * WN * 64, TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -114,22 +244,31 @@ __device__ __forceinline__ void gemm_epilogue(const f32x16 (&acc)[BM / WM / 32][
   // cannot tell that those writes miss the bias, so reads placed after them
   // would each wait for their own LDS round trip)
   f32x4 bias[FN][4];
+  if constexpr (!LN) {
 #pragma unroll
-  for (int j = 0; j < FN; ++j)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)(bbase + j * 32 + q * 8);
+      for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)(bbase + j * 32 + q * 8);
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const f32x4 bv = bias[j][q];
         float o[4];
-        o[0] = act_apply<ACT>(acc[i][j][q * 4 + 0] + bv.x);
-        o[1] = act_apply<ACT>(acc[i][j][q * 4 + 1] + bv.y);
-        o[2] = act_apply<ACT>(acc[i][j][q * 4 + 2] + bv.z);
-        o[3] = act_apply<ACT>(acc[i][j][q * 4 + 3] + bv.w);
+        if constexpr (LN) {
+          o[0] = act_apply<ACT>(acc[i][j][q * 4 + 0]);
+          o[1] = act_apply<ACT>(acc[i][j][q * 4 + 1]);
+          o[2] = act_apply<ACT>(acc[i][j][q * 4 + 2]);
+          o[3] = act_apply<ACT>(acc[i][j][q * 4 + 3]);
+        } else {
+          const f32x4 bv = bias[j][q];
+          o[0] = act_apply<ACT>(acc[i][j][q * 4 + 0] + bv.x);
+          o[1] = act_apply<ACT>(acc[i][j][q * 4 + 1] + bv.y);
+          o[2] = act_apply<ACT>(acc[i][j][q * 4 + 2] + bv.z);
+          o[3] = act_apply<ACT>(acc[i][j][q * 4 + 3] + bv.w);
+        }
         T* const cp = cbase + i * 32 * LDC + j * 32 + q * 8;
         if constexpr (sizeof(T) == 2) {
           u32x2 pk = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
@@ -174,7 +313,11 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
   extern __shared__ __align__(16) char smem[];
   T* sAB = (T*)smem;                                       // [STAGES][(BM + BN) * LDK]: x rows then w rows
   T* sC = (T*)smem;                                        // [BM][LDC] staging, reuses the A/B area
-  float* sBias = (float*)(smem + (S::LDS_BYTES - BN * sizeof(float)));
+  float* sBias = (float*)(smem + S::LDS_MAIN);             // [BN], then (fused LayerNorm) gamma, beta, partials
+  float* sGamma = sBias + BN;
+  float* sBeta = sGamma + BN;
+  float* red = sBeta + BN;
+  constexpr bool LN = (ACT & 8) != 0;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -197,7 +340,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
     const T* xb = (const T*)d.x + (int64_t)m0 * d.ldx;
     const T* wb = (const T*)d.w + (int64_t)n0 * d.ldw;
 
-    if (tid < BN) sBias[tid] = (d.bias && tid < Nr) ? Elem<T>::load1(d.bias, n0 + tid) : 0.f;
+    load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
 
     f32x16 acc[S::FM][S::FN];
 #pragma unroll
@@ -273,6 +416,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       }
     }
 
+    if constexpr (LN) ln_rows<BM, BN, WM, WN>(acc, sBias, sGamma, sBeta, red, d);
     gemm_epilogue<T, BM, BN, WM, WN, S::LDC, ACT>(acc, sC, sBias, d, m0, n0, Mr, Nr);
     __syncthreads();  // staging and bias reads done before the next tile overwrites them
   }
@@ -346,6 +490,8 @@ struct DmaShape {
   static constexpr int PITCH = TN * 2 + 16, CPRW = TN / 8;  // staged row bytes, 16-byte chunks per row
   static constexpr size_t BIAS = 2 * (size_t)STAGE;        // fp32 bias of the current tile
   static constexpr size_t LDS_BYTES = BIAS + BN * sizeof(float);
+  // a fused LayerNorm adds [BN] gamma, [BN] beta and two [BM][WN] row-partial buffers
+  static constexpr size_t LDS_BYTES_LN = BIAS + 3 * BN * sizeof(float) + 2 * BM * WN * sizeof(float);
   static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "whole DMA instructions per wave");
   static_assert((8 * NW) % 16 == 0, "the swizzle of a lane's rows must not change between instructions");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
@@ -406,10 +552,14 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
                                                                        const GemmTile* __restrict__ tiles,
                                                                        int32_t num_tiles) {
   using S = DmaShape<BM, BN, WM, WN>;
-  constexpr int NW = S::NW;
+  constexpr int NW = S::NW, A = ACT & 7;
+  constexpr bool LN = (ACT & 8) != 0;  // the row LayerNorm is fused into the epilogue
   extern __shared__ __align__(16) char smem[];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
   float* sBias = (float*)(smem + S::BIAS);
+  float* sGamma = sBias + BN;
+  float* sBeta = sGamma + BN;
+  float* red = sBeta + BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN, l32 = lane & 31, lh = lane >> 5;
   // this lane's first staged row and its (swizzled) chunk; each further DMA
@@ -509,8 +659,14 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       __syncthreads();
       const int stage = (sbase + kb) & 1;
       // the bias of this tile: the previous tile's epilogue read sBias before this barrier
-      float bv = 0.f;
-      if (kb == 0 && tid < BN) bv = (d.bias && tid < Nr) ? Elem<bf16_t>::load1(d.bias, n0 + tid) : 0.f;
+      float bv = 0.f, gv = 0.f, ev = 0.f;
+      if (kb == 0 && tid < BN) {
+        bv = (d.bias && tid < Nr) ? Elem<bf16_t>::load1(d.bias, n0 + tid) : 0.f;
+        if constexpr (LN) {
+          gv = tid < Nr ? (d.gamma ? Elem<bf16_t>::load1(d.gamma, tid) : 1.f) : 0.f;
+          ev = (d.beta && tid < Nr) ? Elem<bf16_t>::load1(d.beta, tid) : 0.f;
+        }
+      }
       // the following step of this tile, or at the last step the next tile's first
       DmaLoads L;
       if (kb + 1 < nk) {
@@ -520,9 +676,16 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
         L = dma_first<BM, BN, NW>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
       }
       step(stage, L, stage ^ 1);
-      if (kb == 0 && tid < BN) sBias[tid] = bv;
+      if (kb == 0 && tid < BN) {
+        sBias[tid] = bv;
+        if constexpr (LN) {
+          sGamma[tid] = gv;
+          sBeta[tid] = ev;
+        }
+      }
     }
     __syncthreads();  // every wave is done with the last stage (staging) and the bias is written
+    if constexpr (LN) ln_rows<BM, BN, WM, WN>(acc, sBias, sGamma, sBeta, red, d);
 
     // epilogue: bias + activation + rounding into this wave's staging slice,
     // then whole 16-byte pieces of y rows leave in coalesced stores. Every
@@ -545,22 +708,33 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       const bool col_in = tc < Nr, col_vec = (d.vec & 2) != 0 && tc + 8 <= Nr;
       bf16_t* ybase = (bf16_t*)d.y + (int64_t)(m0 + wrow0) * d.ldy + n0 + tc + (int64_t)lrow * d.ldy;
       // this lane's bias values, all read before the first staging write
+      // (a fused LayerNorm has already added them)
       f32x4 bias[S::FN][4];
+      if constexpr (!LN) {
 #pragma unroll
-      for (int j = 0; j < S::FN; ++j)
+        for (int j = 0; j < S::FN; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)(bput + j * 32 + q * 8);
+          for (int q = 0; q < 4; ++q) bias[j][q] = *(const f32x4*)(bput + j * 32 + q * 8);
+      }
 #pragma unroll
       for (int h = 0; h < S::NH; ++h) {
 #pragma unroll
         for (int j = 0; j < S::FN; ++j) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const f32x4 bv = bias[j][q];
-            const float o0 = act_apply<ACT>(acc[h][j][q * 4 + 0] + bv.x);
-            const float o1 = act_apply<ACT>(acc[h][j][q * 4 + 1] + bv.y);
-            const float o2 = act_apply<ACT>(acc[h][j][q * 4 + 2] + bv.z);
-            const float o3 = act_apply<ACT>(acc[h][j][q * 4 + 3] + bv.w);
+            const f32x4 bv = LN ? f32x4{0.f, 0.f, 0.f, 0.f} : bias[j][q];
+            float o0 = acc[h][j][q * 4 + 0], o1 = acc[h][j][q * 4 + 1];
+            float o2 = acc[h][j][q * 4 + 2], o3 = acc[h][j][q * 4 + 3];
+            if constexpr (!LN) {
+              o0 += bv.x;
+              o1 += bv.y;
+              o2 += bv.z;
+              o3 += bv.w;
+            }
+            o0 = act_apply<A>(o0);
+            o1 = act_apply<A>(o1);
+            o2 = act_apply<A>(o2);
+            o3 = act_apply<A>(o3);
             *(u32x2*)(wput + (4 * j + q) * 16) = u32x2{pack_bf16x2(o0, o1), pack_bf16x2(o2, o3)};
           }
         }
@@ -594,19 +768,17 @@ struct GemmVariant {
 };
 
 // 0: members with N, K <= 64 (one K step); 1: 128x128; 2: 256x256 (8 waves);
-// 3: fp32; 4: 256x256 (4 waves); 5: 256x128 (4 waves);
-// 6-8: direct-to-LDS (bf16, aligned rows, K % 8 == 0): 256x256 8 waves,
-// 256x128 4 waves, 128x128 4 waves.
+// 3: fp32 64x64; 4-5: direct-to-LDS (bf16, aligned rows, K % 8 == 0):
+// 256x256 8 waves, 128x128 4 waves; 6: fp32 64x128 (a fused LayerNorm over
+// fp32 rows of 65 to 128 columns).
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
     {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
     {256, 256, 512, 1, "grouped_gemm_bf16_256x256x64_w2x4_s2"},
     {64, 64, 256, 4, "grouped_gemm_f32_64x64x32_w2x2_s2"},
-    {256, 256, 256, 1, "grouped_gemm_bf16_256x256x64_w2x2_s2"},
-    {256, 128, 256, 1, "grouped_gemm_bf16_256x128x64_w2x2_s2"},
     {256, 256, 512, 1, "grouped_gemm_dma_bf16_256x256x64_w2x4"},
-    {256, 128, 256, 1, "grouped_gemm_dma_bf16_256x128x64_w2x2"},
     {128, 128, 256, 2, "grouped_gemm_dma_bf16_128x128x64_w2x2"},
+    {64, 128, 256, 1, "grouped_gemm_f32_64x128x64_w2x2_s2"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
 
@@ -620,59 +792,67 @@ static bool gemm_dma_ok(const optimus_linear_desc* d, int32_t G) {
   return true;
 }
 
-GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G) {
+int gemm_ln_max_n(optimus_dtype dt) { return dt == OPTIMUS_F32 ? 128 : 256; }
+
+GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln) {
+  int64_t maxN = 0, maxK = 0;
+  double tiles256 = 0.0;
+  for (int g = 0; g < G; ++g) {
+    maxN = d[g].N > maxN ? d[g].N : maxN;
+    maxK = d[g].K > maxK ? d[g].K : maxK;
+    tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
+  }
   int v;
+  const bool dma = dt == OPTIMUS_BF16 && gemm_dma_ok(d, G);
   if (dt == OPTIMUS_F32) {
-    v = 3;
-  } else {
-    int64_t maxN = 0, maxK = 0;
-    double tiles256 = 0.0;
-    for (int g = 0; g < G; ++g) {
-      maxN = d[g].N > maxN ? d[g].N : maxN;
-      maxK = d[g].K > maxK ? d[g].K : maxK;
-      tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
-    }
+    v = (ln && maxN > 64) ? 6 : 3;
+  } else if (maxN <= 64 && maxK <= 64) {
+    v = 0;
+  } else if (tiles256 >= 0.5 * device_cu_count() || (ln && maxN > 128)) {
     // measured over groups of 64 to 4096 256x256 tiles: the 256x256 tile wins
-    // from half a tile per CU on; smaller groups need the 128x128 tile to
-    // spread over the CUs
-    const bool dma = gemm_dma_ok(d, G);
-    if (maxN <= 64 && maxK <= 64)
-      v = 0;
-    else if (tiles256 >= 0.5 * device_cu_count())
-      v = dma ? 6 : 2;
-    else
-      v = dma ? 8 : 1;
+    // from half a tile per CU on (and is the one that holds rows past 128)
+    v = dma ? 4 : 2;
+  } else {
+    // smaller groups need the 128x128 tile to spread over the CUs
+    v = dma ? 5 : 1;
   }
   // OPTIMUS_GEMM_VARIANT=<n> pins the bf16 tile shape (tests and tuning); the
-  // direct-to-LDS variants need every member's x / w rows 16-byte aligned and K % 8 == 0.
+  // direct-to-LDS variants need every member's x / w rows 16-byte aligned and
+  // K % 8 == 0, and a fused LayerNorm a tile as wide as the widest row.
   if (dt == OPTIMUS_BF16) {
     const char* f = getenv("OPTIMUS_GEMM_VARIANT");
     char* end = nullptr;
     const long want = f ? strtol(f, &end, 10) : -1;
-    if (f && end && *end == 0 && want >= 0 && want < kNumVariants && want != 3) {
-      if (want < 6 || gemm_dma_ok(d, G)) v = (int)want;
+    if (f && end && *end == 0 && want >= 0 && want < kNumVariants && want != 3 && want != 6) {
+      if ((want < 4 || dma) && (!ln || kVariants[want].bn >= maxN)) v = (int)want;
     }
   }
   const GemmVariant& k = kVariants[v];
   return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
 }
 
-template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
-static hipError_t launch_shape(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
-                               hipStream_t stream) {
-  using S = GemmShape<T, BM, BN, BK, WM, WN, STAGES>;
-  const size_t smem = S::LDS_BYTES;
-#define OPTIMUS_GEMM_LAUNCH(A)                                                                                      \
+// One kernel instance: the dynamic LDS limit is raised once per instance.
+#define OPTIMUS_LAUNCH_ONE(KFN, SMEM, NT)                                                                          \
   {                                                                                                                \
-    auto kfn = grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, A>;                                              \
-    static bool attr_set = false; /* per device-independent kernel; setting it twice is harmless */               \
-    if (smem > 65536 && !attr_set) {                                                                               \
-      hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); \
+    auto kfn = KFN;                                                                                                \
+    static bool attr_set = false; /* the attribute is device-independent; setting it twice is harmless */         \
+    if ((SMEM) > 65536 && !attr_set) {                                                                             \
+      hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)(SMEM)); \
       if (e != hipSuccess) return e;                                                                               \
       attr_set = true;                                                                                             \
     }                                                                                                              \
-    hipLaunchKernelGGL(kfn, dim3(grid), dim3(S::NT), smem, stream, descs, tiles, n);                              \
+    hipLaunchKernelGGL(kfn, dim3(grid), dim3(NT), (SMEM), stream, descs, tiles, n);                                \
   }
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
+static hipError_t launch_shape(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
+                               int32_t grid, hipStream_t stream) {
+  using S = GemmShape<T, BM, BN, BK, WM, WN, STAGES>;
+#define OPTIMUS_GEMM_LAUNCH(A)                                                                     \
+  if (ln)                                                                                          \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, (A) | 8>), S::LDS_BYTES_LN, S::NT) \
+  else                                                                                             \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, (A)>), S::LDS_BYTES, S::NT)
   switch (act) {
     case OPTIMUS_ACT_NONE: OPTIMUS_GEMM_LAUNCH(0); break;
     case OPTIMUS_ACT_RELU: OPTIMUS_GEMM_LAUNCH(1); break;
@@ -686,21 +866,14 @@ static hipError_t launch_shape(optimus_act act, const DevLinear* descs, const Ge
 }
 
 template <int BM, int BN, int WM, int WN>
-static hipError_t launch_dma(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
-                             hipStream_t stream) {
+static hipError_t launch_dma(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
+                             int32_t grid, hipStream_t stream) {
   using S = DmaShape<BM, BN, WM, WN>;
-  const size_t smem = S::LDS_BYTES;
-#define OPTIMUS_DMA_LAUNCH(A)                                                                                      \
-  {                                                                                                                \
-    auto kfn = grouped_gemm_dma_kernel<BM, BN, WM, WN, A>;                                                         \
-    static bool attr_set = false;                                                                                  \
-    if (smem > 65536 && !attr_set) {                                                                               \
-      hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem); \
-      if (e != hipSuccess) return e;                                                                               \
-      attr_set = true;                                                                                             \
-    }                                                                                                              \
-    hipLaunchKernelGGL(kfn, dim3(grid), dim3(S::NT), smem, stream, descs, tiles, n);                              \
-  }
+#define OPTIMUS_DMA_LAUNCH(A)                                                                      \
+  if (ln)                                                                                          \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, (A) | 8>), S::LDS_BYTES_LN, S::NT) \
+  else                                                                                             \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, (A)>), S::LDS_BYTES, S::NT)
   switch (act) {
     case OPTIMUS_ACT_NONE: OPTIMUS_DMA_LAUNCH(0); break;
     case OPTIMUS_ACT_RELU: OPTIMUS_DMA_LAUNCH(1); break;
@@ -712,20 +885,20 @@ static hipError_t launch_dma(optimus_act act, const DevLinear* descs, const Gemm
 #undef OPTIMUS_DMA_LAUNCH
   return hipGetLastError();
 }
+#undef OPTIMUS_LAUNCH_ONE
 
-hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, const DevLinear* descs,
+hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream) {
   if (num_tiles <= 0) return hipSuccess;
+  const int32_t n = num_tiles;
   switch (cfg.variant) {
-    case 0: return launch_shape<bf16_t, 128, 64, 64, 4, 1, 1>(act, descs, tiles, num_tiles, grid, stream);
-    case 1: return launch_shape<bf16_t, 128, 128, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 2: return launch_shape<bf16_t, 256, 256, 64, 2, 4, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 4: return launch_shape<bf16_t, 256, 256, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 5: return launch_shape<bf16_t, 256, 128, 64, 2, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 6: return launch_dma<256, 256, 2, 4>(act, descs, tiles, num_tiles, grid, stream);
-    case 7: return launch_dma<256, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
-    case 8: return launch_dma<128, 128, 2, 2>(act, descs, tiles, num_tiles, grid, stream);
+    case 0: return launch_shape<bf16_t, 128, 64, 64, 4, 1, 1>(act, ln, descs, tiles, n, grid, stream);
+    case 1: return launch_shape<bf16_t, 128, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream);
+    case 2: return launch_shape<bf16_t, 256, 256, 64, 2, 4, 2>(act, ln, descs, tiles, n, grid, stream);
+    case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream);
+    case 4: return launch_dma<256, 256, 2, 4>(act, ln, descs, tiles, n, grid, stream);
+    case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream);
+    case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream);
     default: return hipErrorInvalidValue;
   }
 }

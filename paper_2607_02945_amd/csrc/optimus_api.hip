@@ -128,30 +128,50 @@ static Region region(const void* p, int64_t ld, int64_t rows, int64_t cols, size
   return Region{(uintptr_t)p, ld * (int64_t)s, rows, cols * (int64_t)s, member, out};
 }
 
-extern "C" optimus_status optimus_validate_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
-                                                  optimus_act act) {
-  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: G = %d < 0", G);
-  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_linear: unknown dtype %d", (int)dt);
-  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_linear: unknown activation %d", (int)act);
+// Linear members, and with `ln` the LayerNorm fused over their output rows
+// (gamma / beta: host arrays of G device pointers, or NULL).
+static optimus_status validate_linear_impl(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
+                                           bool ln, const void* const* gamma, const void* const* beta, float eps) {
+  const char* what = ln ? "grouped_linear_layernorm" : "grouped_linear";
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: G = %d < 0", what, G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown dtype %d", what, (int)dt);
+  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown activation %d", what, (int)act);
+  if (ln && (!(eps >= 0.f) || !std::isfinite(eps))) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: eps=%g", what, (double)eps);
   if (G == 0) return OPTIMUS_OK;
-  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: descriptor array is NULL");
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: descriptor array is NULL", what);
   const size_t s = dtype_size(dt);
   std::vector<Region> regs;
-  regs.reserve((size_t)G * 4);
+  regs.reserve((size_t)G * 6);
   for (int g = 0; g < G; ++g) {
     const optimus_linear_desc& m = d[g];
-    if (!m.x || !m.w || !m.y) return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: member %d has a NULL x/w/y", g);
+    if (!m.x || !m.w || !m.y) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a NULL x/w/y", what, g);
     if (m.M < 1 || m.N < 1 || m.K < 1 || m.M > kMaxDim || m.N > kMaxDim || m.K > kMaxDim)
-      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: member %d has M=%lld N=%lld K=%lld (need 1..2^31-1)", g,
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has M=%lld N=%lld K=%lld (need 1..2^31-1)", what, g,
                   (long long)m.M, (long long)m.N, (long long)m.K);
     if (m.ldx < m.K || m.ldw < m.K || m.ldy < m.N)
-      return fail(OPTIMUS_ERR_INVALID_ARG, "grouped_linear: member %d has a row stride below its row length", g);
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a row stride below its row length", what, g);
+    if (ln && m.N > gemm_ln_max_n(dt))
+      return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: member %d has N=%lld; a fused LayerNorm takes rows of at most %d",
+                  what, g, (long long)m.N, gemm_ln_max_n(dt));
     regs.push_back(region(m.x, m.ldx, m.M, m.K, s, g, false));
     regs.push_back(region(m.w, m.ldw, m.N, m.K, s, g, false));
     if (m.bias) regs.push_back(region(m.bias, m.N, 1, m.N, s, g, false));
+    if (ln && gamma && gamma[g]) regs.push_back(region(gamma[g], m.N, 1, m.N, s, g, false));
+    if (ln && beta && beta[g]) regs.push_back(region(beta[g], m.N, 1, m.N, s, g, false));
     regs.push_back(region(m.y, m.ldy, m.M, m.N, s, g, true));
   }
-  return check_aliasing(regs, false, "grouped_linear");
+  return check_aliasing(regs, false, what);
+}
+
+extern "C" optimus_status optimus_validate_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
+                                                  optimus_act act) {
+  return validate_linear_impl(d, G, dt, act, false, nullptr, nullptr, 0.f);
+}
+
+extern "C" optimus_status optimus_validate_linear_layernorm(const optimus_linear_desc* d, const void* const* gamma,
+                                                            const void* const* beta, int32_t G, optimus_dtype dt,
+                                                            float eps, optimus_act act) {
+  return validate_linear_impl(d, G, dt, act, true, gamma, beta, eps);
 }
 
 extern "C" optimus_status optimus_validate_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
@@ -274,6 +294,7 @@ struct HostPlan {
   std::vector<D2DCopy> copies;
   // GEMM
   GemmConfig gcfg{};
+  bool g_ln = false;  // the row LayerNorm is fused into the GEMM epilogue
   size_t g_descs_off = 0, g_tiles_off = 0;
   int32_t g_num_tiles = 0, g_grid = 0;
   std::vector<RowLaunch> g_chain;  // per member: tiles range of the same table
@@ -382,13 +403,14 @@ static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool l
 }
 
 static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
-                                   HostPlan& hp) {
-  optimus_status st = optimus_validate_linear(d, G, dt, act);
+                                   HostPlan& hp, bool ln = false, const void* const* gamma = nullptr,
+                                   const void* const* beta = nullptr, float eps = 0.f) {
+  optimus_status st = validate_linear_impl(d, G, dt, act, ln, gamma, beta, eps);
   if (st != OPTIMUS_OK) return st;
-  hp.kind = KIND_LINEAR; hp.dt = dt; hp.act = act; hp.G = G;
+  hp.kind = KIND_LINEAR; hp.dt = dt; hp.act = act; hp.G = G; hp.g_ln = ln;
   const size_t s = dtype_size(dt);
   const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
-  hp.gcfg = gemm_pick_config(dt, d, G);
+  hp.gcfg = gemm_pick_config(dt, d, G, ln);
   std::vector<DevLinear> descs(G);
   for (int g = 0; g < G; ++g) {
     const optimus_linear_desc& m = d[g];
@@ -399,8 +421,13 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
     const bool vin = m.K % VEC == 0 && m.ldx % VEC == 0 && m.ldw % VEC == 0 && aligned16(m.x) && aligned16(m.w);
     const bool vout = m.ldy % VEC == 0 && aligned16(m.y);
     o.vec = (vin ? 1 : 0) | (vout ? 2 : 0);
+    o.gamma = ln && gamma ? gamma[g] : nullptr;
+    o.beta = ln && beta ? beta[g] : nullptr;
+    o.eps = eps;
+    o.inv_n = 1.0f / (float)m.N;
     hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
     hp.bytes += (double)s * ((double)m.M * m.K + (double)m.N * m.K + (m.bias ? (double)m.N : 0.0) + (double)m.M * m.N);
+    if (ln) hp.bytes += (double)s * ((o.gamma ? (double)m.N : 0.0) + (o.beta ? (double)m.N : 0.0));
   }
   // heavy members first (tile cost grows with K), member-major, M-blocks then N-blocks
   std::vector<int> order(G);
@@ -436,7 +463,7 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
   hp.grid = hp.g_grid;
   hp.block = hp.gcfg.threads;
   hp.chain_launches = G;
-  hp.kernel = hp.gcfg.name;
+  hp.kernel = std::string(hp.gcfg.name) + (ln ? "_layernorm" : "");
   return OPTIMUS_OK;
 }
 
@@ -652,7 +679,7 @@ static const P* at(char* table, size_t off) {
 static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t stream) {
   switch (hp.kind) {
     case KIND_LINEAR:
-      return gemm_launch(hp.gcfg, hp.dt, hp.act, at<DevLinear>(table, hp.g_descs_off), at<GemmTile>(table, hp.g_tiles_off),
+      return gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(table, hp.g_descs_off), at<GemmTile>(table, hp.g_tiles_off),
                          hp.g_num_tiles, hp.g_grid, stream);
     case KIND_LN:
     case KIND_PW:
@@ -714,6 +741,14 @@ extern "C" optimus_status optimus_plan_linear(const optimus_linear_desc* d, int3
                                               optimus_act epilogue, optimus_plan* out) {
   HostPlan hp;
   optimus_status st = build_linear(d, G, dt, epilogue, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_linear_layernorm(const optimus_linear_desc* d, const void* const* gamma,
+                                                        const void* const* beta, int32_t G, optimus_dtype dt,
+                                                        float eps, optimus_act epilogue, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_linear(d, G, dt, epilogue, hp, true, gamma, beta, eps);
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
@@ -780,7 +815,7 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
       hipError_t e;
       if (hp.kind == KIND_LINEAR) {
         const RowLaunch& c = hp.g_chain[g];
-        e = gemm_launch(hp.gcfg, hp.dt, hp.act, at<DevLinear>(p->table, hp.g_descs_off),
+        e = gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(p->table, hp.g_descs_off),
                         at<GemmTile>(p->table, hp.g_tiles_off) + c.first_tile, c.num_tiles, c.grid, st);
       } else {
         const RowLaunch& c = hp.rows_chain[g];
@@ -837,7 +872,7 @@ extern "C" optimus_status optimus_plan_execute(optimus_plan p, optimus_stream_t 
 extern "C" optimus_status optimus_plan_get_info(optimus_plan p, optimus_plan_info* out) {
   if (!p || !out) return fail(OPTIMUS_ERR_INVALID_ARG, "plan_get_info: NULL argument");
   const HostPlan& hp = p->hp;
-  out->kind = (int32_t)hp.kind;
+  out->kind = hp.kind == KIND_LINEAR && hp.g_ln ? 4 : (int32_t)hp.kind;
   out->group_size = hp.G;
   out->launches = hp.G ? hp.launches : 0;
   out->chain_launches = hp.chain_launches;
@@ -896,6 +931,13 @@ extern "C" optimus_status optimus_grouped_linear(const optimus_linear_desc* d, i
                                                  optimus_act epilogue, optimus_stream_t stream) {
   HostPlan hp;
   optimus_status st = build_linear(d, G, dt, epilogue, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_linear_layernorm(const optimus_linear_desc* d, const void* const* gamma,
+                                                           const void* const* beta, int32_t G, optimus_dtype dt,
+                                                           float eps, optimus_act epilogue, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_linear(d, G, dt, epilogue, hp, true, gamma, beta, eps);
   return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
 }
 extern "C" optimus_status optimus_grouped_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,

@@ -21,6 +21,10 @@ struct DevLinear {
   int64_t ldx, ldw, ldy;
   int32_t M, N, K;
   int32_t vec;  // bit0: x/w rows 16-B loadable (K, ldx, ldw, pointers); bit1: y rows 16-B storable
+  // fused LayerNorm over each output row (used by the LN kernel instances only)
+  const void* gamma;  // [N] or NULL (1)
+  const void* beta;   // [N] or NULL (0)
+  float eps, inv_n;   // inv_n = 1 / N
 };
 
 // One GEMM work item: the BM x BN output tile (mb, nb) of member `member`;
@@ -88,8 +92,12 @@ struct GemmConfig {
   const char* name;
 };
 
-GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G);
-hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, const DevLinear* descs,
+// ln: the group's LayerNorm is fused into the epilogue, so one tile must hold
+// a whole output row (the picked variant has bn >= every member's N).
+GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln);
+// Widest output row a fused LayerNorm can take for the dtype.
+int gemm_ln_max_n(optimus_dtype dt);
+hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream);
 
 constexpr int kRowThreads = 256;

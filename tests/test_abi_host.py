@@ -72,6 +72,36 @@ def test_linear_aliasing():
     assert B.optimus_validate_linear(a, G, B.BF16) == ALIASING
 
 
+def ptrs(*vals):
+    return (ctypes.c_void_p * len(vals))(*vals)
+
+
+def test_linear_layernorm_validation():
+    """The fused Linear + LayerNorm: the Linear checks, a finite eps >= 0, rows
+    that fit one output tile (bf16 256, fp32 128), gamma/beta never overlapping
+    an output."""
+    a, G = lin_arr(lin(1 * MB, 2 * MB, 3 * MB, N=256), lin(4 * MB, 5 * MB, 6 * MB, N=17))
+    g, b = ptrs(7 * MB, 8 * MB), ptrs(9 * MB, None)
+    V = B.optimus_validate_linear_layernorm
+    assert V(a, g, b, G, B.BF16) == OK
+    assert V(a, None, None, G, B.BF16) == OK
+    assert V(a, g, b, 0, B.BF16) == OK
+    assert V(a, g, b, G, B.BF16, eps=-1.0) == INVALID
+    assert V(a, g, b, G, B.BF16, eps=float("inf")) == INVALID
+    assert V(a, g, b, G, B.BF16, act=9) == UNSUPPORTED
+    assert V(a, g, b, G, B.F32) == UNSUPPORTED  # N = 256 > 128 for fp32
+    assert "at most 128" in B.optimus_last_error()
+    a1, G1 = lin_arr(lin(1 * MB, 2 * MB, 3 * MB, N=257))
+    assert V(a1, None, None, G1, B.BF16) == UNSUPPORTED
+    a2, G2 = lin_arr(lin(1 * MB, 2 * MB, 3 * MB, N=128))
+    assert V(a2, None, None, G2, B.F32) == OK
+    # gamma inside member 1's output
+    assert V(a, ptrs(7 * MB, 6 * MB + 8), b, G, B.BF16) == ALIASING
+    # the plain Linear rule still holds (no in place)
+    a3, G3 = lin_arr(lin(1 * MB, 2 * MB, 1 * MB, M=8, N=8, K=8))
+    assert V(a3, None, None, G3, B.BF16) == ALIASING
+
+
 def pw(x, y, rows, cols, ldx, ldy):
     return B.PointwiseDesc(x, ldx, y, ldy, rows, cols)
 

@@ -77,7 +77,7 @@ def test_ragged_group_all_acts(dtype, act):
     _check(ms, ys, dtype, act, f"ragged {dtype} {act}")
 
 
-@pytest.mark.parametrize("variant", [0, 1, 2, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("variant", [0, 1, 2, 4, 5])
 def test_every_bf16_tile_variant(variant):
     say(f"[linear variant] {variant}")
     shapes = [(513, 300, 72), (256, 256, 1024), (31, 7, 40), (700, 520, 136)]

@@ -36,9 +36,14 @@ def test_tiny_group_fp32():
     be = [dev(b) for b in wl.betas]
     p1 = B.optimus_plan_linear(xs, ws, bs, ys, "none")
     p2 = B.optimus_plan_layernorm(ys, zs, gs, be, wl.eps, "tanh")
+    # the op-group the benchmark times: LayerNorm + tanh in the GEMM epilogue, one launch
+    fz = [torch.empty_like(y) for y in ys]
+    p3 = B.optimus_plan_linear_layernorm(xs, ws, bs, fz, gs, be, wl.eps, "tanh")
     p1.execute()
     p2.execute()
+    p3.execute()
     torch.cuda.synchronize()
+    assert p3.info()["launches"] == 1 and p3.info()["kernel"].endswith("_layernorm")
     for i, m in enumerate(wl.members):
         x64, w64, b64 = synth.exact64(m.x), synth.exact64(m.w), synth.exact64(m.b)
         lin = ORC.linear(x64, w64, b64)
@@ -47,6 +52,8 @@ def test_tiny_group_fp32():
                      "fp32", f"layernorm {i} (per op)")
         assert_close(host64(zs[i]), ORC.layernorm(lin, host64(gs[i]), host64(be[i]), wl.eps, "tanh"),
                      "fp32", f"end to end {i}")
+        assert_close(host64(fz[i]), ORC.linear_layernorm(x64, w64, b64, host64(gs[i]), host64(be[i]), wl.eps, "tanh"),
+                     "fp32", f"fused linear+layernorm {i}")
 
 
 def test_launch_bound_group_bf16():
@@ -106,8 +113,12 @@ def test_towers_full_size_sampled_rows():
     z = [torch.empty_like(v) for v in o]
     w1, b1, w2, b2 = ([dev(getattr(t, a)) for t in T] for a in ("w1", "b1", "w2", "b2"))
     gm, bt = [dev(t.gamma) for t in T], [dev(t.beta) for t in T]
+    # layer 2 with its LayerNorm in the GEMM epilogue (the op-group the
+    # benchmark times) next to the three-launch form
+    fz = [torch.empty_like(v) for v in o]
     plans = [B.optimus_plan_linear(xs, w1, b1, h, "relu"), B.optimus_plan_linear(h, w2, b2, o, "none"),
-             B.optimus_plan_layernorm(o, z, gm, bt, wl.eps, "none")]
+             B.optimus_plan_layernorm(o, z, gm, bt, wl.eps, "none"),
+             B.optimus_plan_linear_layernorm(h, w2, b2, fz, gm, bt, wl.eps, "none")]
     for p in plans:
         p.execute()
     torch.cuda.synchronize()
@@ -125,6 +136,11 @@ def test_towers_full_size_sampled_rows():
         e2e = ORC.layernorm(ORC.linear(h_ref, synth.exact64(t.w2), synth.exact64(t.b2)),
                             synth.exact64(t.gamma), synth.exact64(t.beta), wl.eps)
         assert_close(host64(z[i])[rows], e2e, "bf16", f"tower {i} end to end")
+        fzh = host64(fz[i])[rows]
+        f_ref = ORC.linear_layernorm(hh[rows], synth.exact64(t.w2), synth.exact64(t.b2), synth.exact64(t.gamma),
+                                     synth.exact64(t.beta), wl.eps)
+        assert_close(fzh, f_ref, "bf16", f"tower {i} fused layer 2 + layernorm (per op)")
+        assert_close(fzh, e2e, "bf16", f"tower {i} fused end to end")
 
 
 def test_large_group_full_size_sampled_rows():
