@@ -50,7 +50,7 @@ def parse():
                     help="untimed steps before timing (default: at least 20 and at least 0.3 s of work, "
                          "so that the clocks have settled)")
     ap.add_argument("--workload", default="launch_bound",
-                    choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group"])
+                    choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group", "decompose_mm"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-chain", action="store_true", help="skip timing the per-op launch chain")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -76,6 +76,7 @@ class OpGroup:
         self.grouped = []      # list of (plan, mode)
         self.chain = []        # list of (plan, mode)
         self.horizontal = []   # split-op-cat only: horizontal fusion without the vertical rewrite
+        self.tiled = []        # decompose_mm only: the group through the tiled GEMM kernel
 
     def run(self, which, stream=None):
         for plan, mode in getattr(self, which):
@@ -90,19 +91,30 @@ def build_copy(name, wl, torch, B):
     og = OpGroup()
     cu = lambda t: t.to("cuda")
     bf = torch.bfloat16
-    if name in ("launch_bound", "tiny_group", "large_group"):
+    if name in ("launch_bound", "tiny_group", "large_group", "decompose_mm"):
         xs = [cu(m.x) for m in wl.members]
         ws = [cu(m.w) for m in wl.members]
-        bs = [cu(m.b) for m in wl.members]
+        bs = [None if m.b is None else cu(m.b) for m in wl.members]
         dt = xs[0].dtype
         ys = [torch.empty((m.M, m.N), dtype=dt, device="cuda") for m in wl.members]
         if not wl.ln:
             lin = B.optimus_plan_linear(xs, ws, bs, ys, wl.act)
             og.grouped = [(lin, "grouped")]
-            y1 = [torch.empty_like(y) for y in ys]
-            lin0 = B.optimus_plan_linear(xs, ws, bs, y1, "none")
-            pw = B.optimus_plan_pointwise(y1, ys, wl.act)
-            og.chain = [(lin0, "chain"), (pw, "chain")]
+            if wl.act == "none":
+                og.chain = [(lin, "chain")]
+                y1 = None
+            else:
+                y1 = [torch.empty_like(y) for y in ys]
+                lin0 = B.optimus_plan_linear(xs, ws, bs, y1, "none")
+                pw = B.optimus_plan_pointwise(y1, ys, wl.act)
+                og.chain = [(lin0, "chain"), (pw, "chain")]
+            if name == "decompose_mm":
+                # the same group through the tiled MFMA GEMM (the paper's "before")
+                os.environ["OPTIMUS_GEMM_VARIANT"] = "3"
+                try:
+                    og.tiled = [(B.optimus_plan_linear(xs, ws, bs, ys, wl.act), "grouped")]
+                finally:
+                    del os.environ["OPTIMUS_GEMM_VARIANT"]
             og.keep = (xs, ws, bs, ys, y1)
         else:
             zs = [torch.empty_like(y) for y in ys]
@@ -169,6 +181,9 @@ def describe(name, wl):
     if name == "towers":
         return {"workload": name, "towers": wl.G, "batch": wl.towers[0].x.shape[0],
                 "layers": "Linear(in_g->512)+relu, Linear(512->256), LayerNorm", "seed": 0}
+    if name == "decompose_mm":
+        return {"workload": name, "G": wl.G, "M": [m.M for m in wl.members], "K": [m.K for m in wl.members],
+                "N": [m.N for m in wl.members], "bias": False, "seed": 0}
     return {"workload": name, "G": wl.G, "batch": wl.members[0].M,
             "K": sorted({m.K for m in wl.members}), "N": sorted({m.N for m in wl.members}),
             "epilogue": ("LayerNorm+" if wl.ln else "") + wl.act, "seed": 0}
@@ -197,11 +212,12 @@ def cpu_baseline(name, wl, target_s):
                         for x, w1, b1, w2, b2, g, b in ins]
     else:
         M = wl.members[0].M
-        rows = M if name != "large_group" else 64
+        rows = {"large_group": 64, "decompose_mm": 65536}.get(name, M)
         ins = [(e(m.x[:rows]), e(m.w), e(m.b)) for m in wl.members]
         lns = [(e(g), e(b)) for g, b in zip(wl.gammas, wl.betas)] if wl.ln else None
-        frac = rows / M
-        sample = "whole group" if rows == M else f"first {rows} of {M} rows of every member"
+        # share of the group's work (flops) the sample covers
+        frac = (sum(min(rows, m.M) * m.N * m.K for m in wl.members) / sum(m.M * m.N * m.K for m in wl.members))
+        sample = "whole group" if rows == M else f"first {rows} rows of every member"
 
         def work():
             for i, (x, w, b) in enumerate(ins):
@@ -454,6 +470,12 @@ def main():
                         "launches_per_group": sum(p.info()["chain_launches"] for p, m in ogs[0].chain
                                                   if m == "chain") + sum(1 for p, m in ogs[0].chain if m != "chain"),
                         "speedup": round(c_step / ms_step, 2)}
+    if ogs[0].tiled:
+        tsteps = max(5, min(args.steps, 20))
+        t_ms, _ = timed("tiled", tsteps, 2)
+        t_step = t_ms / tsteps
+        out["tiled_gemm"] = {"us_per_group": round(t_step * 1000.0, 3), "kernel": ogs[0].tiled[0][0].info()["kernel"],
+                             "speedup": round(t_step / ms_step, 2)}
     if ogs[0].horizontal:
         hsteps = max(5, min(args.steps, 50))
         h_ms, _ = timed("horizontal", hsteps, 2)

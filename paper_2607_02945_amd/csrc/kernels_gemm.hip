@@ -761,6 +761,259 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   }
 }
 
+// ===================================================================== skinny members
+// Every member has K <= 8 and N <= 8: a tall-skinny matrix product such as
+// [2e7, 8] x [8, 8], which the paper's decompose_mm rewrite (appendix Sec. 8.2)
+// turns into pointwise products and a reduction over K because a tiled GEMM
+// wastes nearly all of its work on such shapes. Here it is one streaming
+// kernel with no MFMA: each lane owns whole rows, multiplies a row's K values
+// by the member's weights (fp32 FMAs, ascending k) and writes the row's N
+// outputs. A work item is kSkinnyRows rows of one member, walked in passes
+// of RPL rows per lane (8 for the small classes, 4 for 8 x 8), and a lane
+// loads all of a pass's rows before it uses any. A member's weights and bias are staged in LDS as fp32 when a
+// workgroup's items reach it (while its first rows are in flight) and read
+// back as broadcasts. A uniform branch per item picks the smallest shape class
+// (KV, NV) that holds the member, so the paper's [*, 4] x [4, 2] and
+// [*, 8] x [8, 8] members pay no padded FMAs.
+constexpr int kSkinnyMax = 8;      // largest K and N of the path
+constexpr int kSkinnyRows = 2048;  // rows per work item (4 waves)
+
+template <typename T, int KV>
+__device__ __forceinline__ void skinny_load(const T* p, int K, bool vec, float (&v)[KV]) {
+  if constexpr (sizeof(T) == 4) {
+    if (vec && KV % 4 == 0) {  // K == KV, 16-byte aligned rows
+#pragma unroll
+      for (int c = 0; c < KV / 4; ++c) {
+        const f32x4 q = __builtin_bit_cast(f32x4, ld16_nt(p + 4 * c));
+        v[4 * c + 0] = q.x;
+        v[4 * c + 1] = q.y;
+        v[4 * c + 2] = q.z;
+        v[4 * c + 3] = q.w;
+      }
+      return;
+    }
+  } else {
+    if (vec && KV % 8 == 0) {
+      float f[8];
+      Elem<bf16_t>::unpack(ld16_nt(p), f);
+#pragma unroll
+      for (int e = 0; e < KV; ++e) v[e] = f[e];
+      return;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < KV; ++k) v[k] = k < K ? Elem<T>::load1(p, k) : 0.f;
+}
+
+template <typename T, int NV>
+__device__ __forceinline__ void skinny_store(T* p, int N, bool vec, const float (&o)[NV]) {
+  // vec: N == NV and rows aligned to their size (16 bytes, or 8 / 4 for narrower rows)
+  if constexpr (sizeof(T) == 4) {
+    if (vec && NV % 4 == 0) {
+#pragma unroll
+      for (int c = 0; c < NV / 4; ++c)
+        st16_nt(p + 4 * c, __builtin_bit_cast(u32x4, f32x4{o[4 * c], o[4 * c + 1], o[4 * c + 2], o[4 * c + 3]}));
+      return;
+    }
+    if (vec && NV == 2) {
+      __builtin_nontemporal_store(u32x2{__builtin_bit_cast(uint32_t, o[0]), __builtin_bit_cast(uint32_t, o[1])},
+                                  (OPTIMUS_GLOBAL u32x2*)p);
+      return;
+    }
+  } else {
+    if (vec && NV % 8 == 0) {
+      st16_nt(p, u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+                       pack_bf16x2(o[6], o[7])});
+      return;
+    }
+    if (vec && NV == 4) {
+      __builtin_nontemporal_store(u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])}, (OPTIMUS_GLOBAL u32x2*)p);
+      return;
+    }
+    if (vec && NV == 2) {
+      __builtin_nontemporal_store(pack_bf16x2(o[0], o[1]), (OPTIMUS_GLOBAL uint32_t*)p);
+      return;
+    }
+  }
+#pragma unroll
+  for (int n = 0; n < NV; ++n)
+    if (n < N) Elem<T>::store1(p, n, o[n]);
+}
+
+// The lane's rows of one pass: rows base + 64 i of [r0, r0 + count).
+template <typename T, int KV, int RPL>
+__device__ __forceinline__ void skinny_rows_load(const DevLinear& d, int r0, int count, float (&x)[RPL][KV]) {
+  const bool vin = (d.vec & 1) && d.K == KV;
+  const int base = (threadIdx.x >> 6) * 64 * RPL + (threadIdx.x & 63);
+#pragma unroll
+  for (int i = 0; i < RPL; ++i) {
+    const int r = base + 64 * i;
+    if (r < count) skinny_load<T, KV>((const T*)d.x + (int64_t)(r0 + r) * d.ldx, d.K, vin, x[i]);
+  }
+}
+
+// Products, bias, activation and stores of the loaded rows; weights sW[n][k]
+// (kSkinnyMax x kSkinnyMax, zero outside N x K) and bias sB in LDS.
+template <typename T, int KV, int NV, int ACT, int RPL>
+__device__ __forceinline__ void skinny_rows_out(const DevLinear& d, int r0, int count, const float (&x)[RPL][KV],
+                                                const float* sW, const float* sB) {
+  // rows of NV elements aligned to their size: 16-byte pieces, or one 8- / 4-byte piece
+  constexpr int ROWB = NV * (int)sizeof(T);
+  const bool vout = d.N == NV && ((ROWB >= 16) ? (d.vec & 2) != 0
+                                               : ((uintptr_t)d.y % ROWB == 0 && (d.ldy * sizeof(T)) % ROWB == 0));
+  const int base = (threadIdx.x >> 6) * 64 * RPL + (threadIdx.x & 63);
+  float o[RPL][NV];
+#pragma unroll
+  for (int n = 0; n < NV; ++n) {
+    float w[KV];
+#pragma unroll
+    for (int k = 0; k < KV; ++k) w[k] = sW[n * kSkinnyMax + k];
+    const float b = sB[n];
+#pragma unroll
+    for (int i = 0; i < RPL; ++i) {
+      float s = 0.f;
+#pragma unroll
+      for (int k = 0; k < KV; ++k) s = fmaf(x[i][k], w[k], s);
+      o[i][n] = act_apply<ACT>(s + b);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < RPL; ++i) {
+    const int r = base + 64 * i;
+    if (r < count) skinny_store<T, NV>((T*)d.y + (int64_t)(r0 + r) * d.ldy, d.N, vout, o[i]);
+  }
+}
+
+// One work item in shape class (KV, NV), in passes of 256 * RPL rows: the
+// first pass's loads go out first, then (only when the member changed) the
+// weights are staged while they fly.
+template <typename T, int KV, int NV, int ACT, int RPL>
+__device__ __forceinline__ void skinny_item(const DevLinear& d, int r0, int count, bool restage, float* sW, float* sB) {
+  constexpr int PASS = 256 * RPL;
+  static_assert(kSkinnyRows % PASS == 0, "whole passes per item");
+  float x[RPL][KV];
+  skinny_rows_load<T, KV, RPL>(d, r0, count, x);
+  if (restage) {
+    __syncthreads();  // every wave is done with the previous member's weights
+    const int tid = threadIdx.x;
+    if (tid < kSkinnyMax * kSkinnyMax) {
+      const int n = tid / kSkinnyMax, k = tid % kSkinnyMax;
+      sW[tid] = (n < d.N && k < d.K) ? Elem<T>::load1(d.w, (int64_t)n * d.ldw + k) : 0.f;
+    }
+    if (tid < kSkinnyMax) sB[tid] = (d.bias && tid < d.N) ? Elem<T>::load1(d.bias, tid) : 0.f;
+    __syncthreads();
+  }
+  skinny_rows_out<T, KV, NV, ACT, RPL>(d, r0, count, x, sW, sB);
+#pragma unroll 1
+  for (int p = PASS; p < kSkinnyRows && p < count; p += PASS) {
+    skinny_rows_load<T, KV, RPL>(d, r0 + p, count - p, x);
+    skinny_rows_out<T, KV, NV, ACT, RPL>(d, r0 + p, count - p, x, sW, sB);
+  }
+}
+
+// fp32 members with K = N = 8 and contiguous rows (32 bytes each): a lane pair
+// per row, so that every load and store instruction moves consecutive 16-byte
+// chunks. Thread t takes chunks t + 256 j of the item (chunk c is half c % 2
+// of row c / 2; the two halves of a row sit in adjacent lanes), forms the
+// partial products of its four k for all eight outputs, adds its partner's
+// partials (DPP lane ^ 1 swap), and stores its half of the row's outputs,
+// which is the same chunk index of y.
+constexpr int kSkinnyChunks = 8;  // chunks per thread per pass (a pass is 1024 rows)
+template <int ACT>
+__device__ __forceinline__ void skinny_pairs_pass(const float* xb, float* yb, int nchunks, const f32x4 (&w)[8],
+                                                  const f32x4& b, f32x4 (&x)[kSkinnyChunks], bool loaded) {
+  const int tid = threadIdx.x, half = tid & 1;
+  if (!loaded) {
+#pragma unroll
+    for (int j = 0; j < kSkinnyChunks; ++j) {
+      const int c = tid + 256 * j;
+      x[j] = c < nchunks ? __builtin_bit_cast(f32x4, ld16_nt(xb + 4 * c)) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kSkinnyChunks; ++j) {
+    float p[8];
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+      float t = x[j].x * w[n].x;
+      t = fmaf(x[j].y, w[n].y, t);
+      t = fmaf(x[j].z, w[n].z, t);
+      t = fmaf(x[j].w, w[n].w, t);
+      p[n] = t;
+    }
+    float o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      // outputs q and 4 + q: this lane keeps one, its partner the other
+      const float mine = half ? p[4 + q] : p[q], theirs = half ? p[q] : p[4 + q];
+      o[q] = mine + dpp_f<0xB1>(theirs);  // partner's partial of the same output
+    }
+    const int c = tid + 256 * j;
+    if (c < nchunks)
+      st16_nt(yb + 4 * c, __builtin_bit_cast(u32x4, f32x4{act_apply<ACT>(o[0] + b.x), act_apply<ACT>(o[1] + b.y),
+                                                           act_apply<ACT>(o[2] + b.z), act_apply<ACT>(o[3] + b.w)}));
+  }
+}
+
+template <int ACT>
+__device__ __forceinline__ void skinny_item_pairs(const DevLinear& d, int r0, int count, bool restage, float* sW,
+                                                  float* sB) {
+  constexpr int PASS = 256 * kSkinnyChunks / 2;  // rows per pass
+  static_assert(kSkinnyRows % PASS == 0, "whole passes per item");
+  const int tid = threadIdx.x, half = tid & 1;
+  const float* xb = (const float*)d.x + (int64_t)r0 * 8;
+  float* yb = (float*)d.y + (int64_t)r0 * 8;
+  f32x4 x[kSkinnyChunks];
+#pragma unroll
+  for (int j = 0; j < kSkinnyChunks; ++j) {
+    const int c = tid + 256 * j;
+    x[j] = c < 2 * count ? __builtin_bit_cast(f32x4, ld16_nt(xb + 4 * c)) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  if (restage) {
+    __syncthreads();
+    if (tid < kSkinnyMax * kSkinnyMax) sW[tid] = Elem<float>::load1(d.w, (int64_t)(tid / 8) * d.ldw + tid % 8);
+    if (tid < kSkinnyMax) sB[tid] = d.bias ? Elem<float>::load1(d.bias, tid) : 0.f;
+    __syncthreads();
+  }
+  // this lane's four k of every output row, and the bias of its four outputs
+  f32x4 w[8];
+#pragma unroll
+  for (int n = 0; n < 8; ++n) w[n] = *(const f32x4*)(sW + n * 8 + half * 4);
+  const f32x4 b = *(const f32x4*)(sB + half * 4);
+  skinny_pairs_pass<ACT>(xb, yb, 2 * count, w, b, x, true);
+#pragma unroll 1
+  for (int p = PASS; p < kSkinnyRows && p < count; p += PASS)
+    skinny_pairs_pass<ACT>(xb + (int64_t)p * 8, yb + (int64_t)p * 8, 2 * (count - p), w, b, x, false);
+}
+
+template <typename T, int ACT>
+__global__ __launch_bounds__(256) void grouped_gemm_skinny_kernel(const DevLinear* __restrict__ descs,
+                                                                  const GemmTile* __restrict__ tiles,
+                                                                  int32_t num_tiles) {
+  __shared__ __align__(16) float sW[kSkinnyMax * kSkinnyMax];
+  __shared__ __align__(16) float sB[kSkinnyMax];
+  int staged = -1;  // member whose weights sW / sB hold
+  for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
+    const GemmTile tile = tiles[t];
+    if (tile.member < 0) continue;
+    const DevLinear& d = descs[tile.member];
+    const bool restage = tile.member != staged;
+    staged = tile.member;
+    const int r0 = tile.mb * kSkinnyRows;
+    const int count = min(kSkinnyRows, d.M - r0);
+    bool pairs = false;
+    if constexpr (sizeof(T) == 4) pairs = d.K == 8 && d.N == 8 && d.ldx == 8 && d.ldy == 8 && (d.vec & 3) == 3;
+    if (pairs)
+      skinny_item_pairs<ACT>(d, r0, count, restage, sW, sB);
+    else if (d.K <= 4 && d.N <= 2)
+      skinny_item<T, 4, 2, ACT, 8>(d, r0, count, restage, sW, sB);
+    else if (d.K <= 4 && d.N <= 4)
+      skinny_item<T, 4, 4, ACT, 8>(d, r0, count, restage, sW, sB);
+    else
+      skinny_item<T, 8, 8, ACT, 4>(d, r0, count, restage, sW, sB);
+  }
+}
+
 // ===================================================================== configurations
 struct GemmVariant {
   int bm, bn, threads, occ;  // occ: workgroups resident per CU (LDS / register bound)
@@ -770,7 +1023,8 @@ struct GemmVariant {
 // 0: members with N, K <= 64 (one K step); 1: 128x128; 2: 256x256 (8 waves);
 // 3: fp32 64x64; 4-5: direct-to-LDS (bf16, aligned rows, K % 8 == 0):
 // 256x256 8 waves, 128x128 4 waves; 6: fp32 64x128 (a fused LayerNorm over
-// fp32 rows of 65 to 128 columns).
+// fp32 rows of 65 to 128 columns); 7: skinny members (every K, N <= 8), fp32 or
+// bf16, streamed with no MFMA.
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
     {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
@@ -779,6 +1033,7 @@ static const GemmVariant kVariants[] = {
     {256, 256, 512, 1, "grouped_gemm_dma_bf16_256x256x64_w2x4"},
     {128, 128, 256, 2, "grouped_gemm_dma_bf16_128x128x64_w2x2"},
     {64, 128, 256, 1, "grouped_gemm_f32_64x128x64_w2x2_s2"},
+    {kSkinnyRows, kSkinnyMax, 256, 4, "grouped_gemm_skinny"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
 
@@ -804,7 +1059,10 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
   }
   int v;
   const bool dma = dt == OPTIMUS_BF16 && gemm_dma_ok(d, G);
-  if (dt == OPTIMUS_F32) {
+  const bool skinny = !ln && maxN <= kSkinnyMax && maxK <= kSkinnyMax;
+  if (skinny) {
+    v = 7;
+  } else if (dt == OPTIMUS_F32) {
     v = (ln && maxN > 64) ? 6 : 3;
   } else if (maxN <= 64 && maxK <= 64) {
     v = 0;
@@ -816,22 +1074,42 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     // smaller groups need the 128x128 tile to spread over the CUs
     v = dma ? 5 : 1;
   }
-  // OPTIMUS_GEMM_VARIANT=<n> pins the bf16 tile shape (tests and tuning); the
+  // OPTIMUS_GEMM_VARIANT=<n> pins the tile shape (tests and tuning); the
   // direct-to-LDS variants need every member's x / w rows 16-byte aligned and
   // K % 8 == 0, and a fused LayerNorm a tile as wide as the widest row.
-  if (dt == OPTIMUS_BF16) {
+  // fp32: 3 and 6 (tiled) and 7 (skinny) in the same way.
+  {
     const char* f = getenv("OPTIMUS_GEMM_VARIANT");
     char* end = nullptr;
     const long want = f ? strtol(f, &end, 10) : -1;
-    if (f && end && *end == 0 && want >= 0 && want < kNumVariants && want != 3 && want != 6) {
-      if ((want < 4 || dma) && (!ln || kVariants[want].bn >= maxN)) v = (int)want;
+    if (f && end && *end == 0 && want >= 0 && want < kNumVariants) {
+      const bool is_f32 = want == 3 || want == 6;
+      bool ok;
+      if (want == 7)
+        ok = skinny;
+      else if ((dt == OPTIMUS_F32) != is_f32)
+        ok = false;
+      else
+        ok = (dt == OPTIMUS_F32 || want < 4 || dma) && (!ln || kVariants[want].bn >= maxN);
+      if (ok) v = (int)want;
     }
   }
   const GemmVariant& k = kVariants[v];
   return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
 }
 
-// One kernel instance: the dynamic LDS limit is raised once per instance.
+// Workgroups of one kernel instance that fit on a CU at once (registers, LDS).
+static hipError_t resident_of(const void* kfn, int threads, size_t smem, int* out) {
+  int b = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, kfn, threads, smem);
+  if (e != hipSuccess) return e;
+  *out = b;
+  return hipSuccess;
+}
+
+// One kernel instance: the dynamic LDS limit is raised once per instance; with
+// `occ` set the instance is not launched and its resident workgroups per CU
+// are reported instead.
 #define OPTIMUS_LAUNCH_ONE(KFN, SMEM, NT)                                                                          \
   {                                                                                                                \
     auto kfn = KFN;                                                                                                \
@@ -841,12 +1119,27 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
       if (e != hipSuccess) return e;                                                                               \
       attr_set = true;                                                                                             \
     }                                                                                                              \
+    if (occ) return resident_of((const void*)kfn, (NT), (SMEM), occ);                                              \
     hipLaunchKernelGGL(kfn, dim3(grid), dim3(NT), (SMEM), stream, descs, tiles, n);                                \
   }
 
+template <typename T>
+static hipError_t launch_skinny(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n,
+                                int32_t grid, hipStream_t stream, int* occ) {
+  switch (act) {
+    case OPTIMUS_ACT_NONE: OPTIMUS_LAUNCH_ONE((grouped_gemm_skinny_kernel<T, 0>), 0, 256); break;
+    case OPTIMUS_ACT_RELU: OPTIMUS_LAUNCH_ONE((grouped_gemm_skinny_kernel<T, 1>), 0, 256); break;
+    case OPTIMUS_ACT_SIGMOID: OPTIMUS_LAUNCH_ONE((grouped_gemm_skinny_kernel<T, 2>), 0, 256); break;
+    case OPTIMUS_ACT_TANH: OPTIMUS_LAUNCH_ONE((grouped_gemm_skinny_kernel<T, 3>), 0, 256); break;
+    case OPTIMUS_ACT_SILU: OPTIMUS_LAUNCH_ONE((grouped_gemm_skinny_kernel<T, 4>), 0, 256); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
 static hipError_t launch_shape(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
-                               int32_t grid, hipStream_t stream) {
+                               int32_t grid, hipStream_t stream, int* occ) {
   using S = GemmShape<T, BM, BN, BK, WM, WN, STAGES>;
 #define OPTIMUS_GEMM_LAUNCH(A)                                                                     \
   if (ln)                                                                                          \
@@ -867,7 +1160,7 @@ static hipError_t launch_shape(optimus_act act, bool ln, const DevLinear* descs,
 
 template <int BM, int BN, int WM, int WN>
 static hipError_t launch_dma(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
-                             int32_t grid, hipStream_t stream) {
+                             int32_t grid, hipStream_t stream, int* occ) {
   using S = DmaShape<BM, BN, WM, WN>;
 #define OPTIMUS_DMA_LAUNCH(A)                                                                      \
   if (ln)                                                                                          \
@@ -887,20 +1180,38 @@ static hipError_t launch_dma(optimus_act act, bool ln, const DevLinear* descs, c
 }
 #undef OPTIMUS_LAUNCH_ONE
 
+static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln,
+                                const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
+                                hipStream_t stream, int* occ) {
+  switch (cfg.variant) {
+    case 0: return launch_shape<bf16_t, 128, 64, 64, 4, 1, 1>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 1: return launch_shape<bf16_t, 128, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 2: return launch_shape<bf16_t, 256, 256, 64, 2, 4, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 4: return launch_dma<256, 256, 2, 4>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 7:
+      if (ln) return hipErrorInvalidValue;
+      return dt == OPTIMUS_F32 ? launch_skinny<float>(act, descs, tiles, n, grid, stream, occ)
+                               : launch_skinny<bf16_t>(act, descs, tiles, n, grid, stream, occ);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream) {
   if (num_tiles <= 0) return hipSuccess;
-  const int32_t n = num_tiles;
-  switch (cfg.variant) {
-    case 0: return launch_shape<bf16_t, 128, 64, 64, 4, 1, 1>(act, ln, descs, tiles, n, grid, stream);
-    case 1: return launch_shape<bf16_t, 128, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream);
-    case 2: return launch_shape<bf16_t, 256, 256, 64, 2, 4, 2>(act, ln, descs, tiles, n, grid, stream);
-    case 3: return launch_shape<float, 64, 64, 32, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream);
-    case 4: return launch_dma<256, 256, 2, 4>(act, ln, descs, tiles, n, grid, stream);
-    case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream);
-    case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream);
-    default: return hipErrorInvalidValue;
+  return gemm_dispatch(cfg, dt, act, ln, descs, tiles, num_tiles, grid, stream, nullptr);
+}
+
+int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln) {
+  int occ = 0;
+  if (gemm_dispatch(cfg, dt, act, ln, nullptr, nullptr, 0, 0, nullptr, &occ) != hipSuccess || occ < 1) {
+    (void)hipGetLastError();
+    return cfg.occ;
   }
+  return occ;
 }
 
 }  // namespace optimus

@@ -450,7 +450,9 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
   hp.g_tiles_off = hp.blob.add(tiles.data(), tiles.size() * sizeof(GemmTile));
   hp.g_num_tiles = (int32_t)tiles.size();
   // workgroups resident per CU for each variant (LDS / register bound)
-  const int64_t cap = (int64_t)device_cu_count() * hp.gcfg.occ;
+  // a persistent grid no larger than what is resident at once: a workgroup
+  // that had to wait for a free slot would start its whole share late
+  const int64_t cap = (int64_t)device_cu_count() * gemm_resident_per_cu(hp.gcfg, dt, act, ln);
   int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
   if (grid >= 8) grid -= grid % 8;
   hp.g_grid = (int32_t)std::max<int64_t>(1, grid);

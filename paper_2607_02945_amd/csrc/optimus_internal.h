@@ -99,6 +99,9 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
 int gemm_ln_max_n(optimus_dtype dt);
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream);
+// Workgroups of the instance gemm_launch would run that fit on one CU at once
+// (the HIP runtime's occupancy of its registers and LDS; cfg.occ if the query fails).
+int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln);
 
 constexpr int kRowThreads = 256;
 #ifndef OPTIMUS_LN_CHUNKS_PER_LANE

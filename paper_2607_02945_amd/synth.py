@@ -18,6 +18,8 @@ Sec. 5.2: many small bf16 operators; Sec. 3.2: split -> LayerNorm -> act -> cat)
   split_op_cat      [8192, 4096] bf16 split into 32 Dirichlet widths, LN_j -> silu, cat
   towers            26 bf16 MLP towers Linear(in_g->512)+relu+Linear(512->256)+LayerNorm, batch 4096
   large_group       G=32 bf16 Linear members, batch 16384, K=1024 -> LayerNorm -> tanh
+  decompose_mm      the four tall-skinny mm members of the appendix decompose_mm case
+                    study ([~2e7, K] x [K, N], K, N in {(8, 8), (4, 2)}), fp32, no bias
 """
 from __future__ import annotations
 
@@ -226,10 +228,29 @@ def large_group(seed: int = 0, G: int = 32, M: int = 16384, K: int = 1024) -> Li
     return LinearLNGroup("large_group", "bf16", members, "tanh", True, gammas, betas, 1e-5)
 
 
+# The four aten.mm shapes of the decompose_mm case study (appendix Sec. 8.2):
+# (M, K, N) of [M, K] x [K, N]; as Linear members the weight is W = [N, K].
+DECOMPOSE_MM_SHAPES = [(18583840, 8, 8), (25247936, 4, 2), (22502112, 8, 8), (17980096, 4, 2)]
+
+
+def decompose_mm(seed: int = 0, scale: float = 1.0, dtype: str = "fp32") -> LinearLNGroup:
+    """The four tall-skinny mm members of the decompose_mm case study (no bias),
+    M scaled by `scale` for parity tests; X ~ N(0, 1), W ~ N(0, 1/K). The paper
+    states no dtype for them: fp32 (PyTorch's default) is the reading."""
+    g = rng(seed)
+    members = []
+    for M, K, N in DECOMPOSE_MM_SHAPES:
+        w = to_storage(_normal(g, (N, K), 1.0 / K), dtype)
+        x = to_storage(g.standard_normal((max(1, int(round(M * scale))), K)), dtype)
+        members.append(LinearMember(x, w, None))
+    return LinearLNGroup("decompose_mm", dtype, members, "none")
+
+
 WORKLOADS = {
     "tiny_group": tiny_group,
     "launch_bound": launch_bound,
     "split_op_cat": split_op_cat,
     "towers": towers,
     "large_group": large_group,
+    "decompose_mm": decompose_mm,
 }

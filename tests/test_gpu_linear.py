@@ -184,3 +184,51 @@ def test_shared_input_members():
     offs = np.cumsum([0] + Ns)
     for i, y in enumerate(ys):
         assert_close(host64(y), whole[:, offs[i]:offs[i + 1]], "bf16", f"shared input member {i} vs concatenated W")
+
+
+# Skinny members (every K, N <= 8: the decompose_mm shapes): the streaming
+# kernel, one shape class per member, items of 1024 rows with a ragged last one.
+SKINNY = [(1000, 8, 8), (1025, 2, 4), (5000, 4, 4), (300, 1, 3), (777, 5, 8), (64, 8, 7), (3, 3, 1), (2049, 6, 2), (4500, 8, 6), (6000, 2, 2)]
+
+
+def _plan_kernel(ms, act):
+    xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
+    ys = [torch.empty((x.shape[0], w.shape[0]), dtype=x.dtype, device="cuda") for x, w, _ in ms]
+    p = B.optimus_plan_linear(xs, ws, bs, ys, act)
+    name = p.info()["kernel"]
+    p.close()
+    return name
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("act", ACTS)
+def test_skinny_members(dtype, act):
+    say(f"[linear skinny] {dtype} {act}")
+    ms = _members(SKINNY, dtype, seed=30)
+    assert _plan_kernel(ms, act) == "grouped_gemm_skinny"
+    for mode in ["oneshot", "chain"]:
+        ys = _run(ms, dtype, act, mode=mode)
+        _check(ms, ys, dtype, act, f"skinny {dtype} {act} {mode}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_skinny_strided_rows_and_no_bias(dtype):
+    """Rows that are not 16-byte pieces (x a column view of a wider buffer; K or
+    N not the class size) take the element path."""
+    say(f"[linear skinny strided] {dtype}")
+    ms = _members([(900, 8, 8), (513, 2, 4), (300, 7, 5)], dtype, seed=31, strided=True)
+    ys = _run(ms, dtype, "none")
+    _check(ms, ys, dtype, "none", f"skinny strided {dtype}")
+    ms = _members([(900, 8, 8), (513, 2, 4)], dtype, seed=32, bias=False)
+    ys = _run(ms, dtype, "tanh")
+    _check(ms, ys, dtype, "tanh", f"skinny no bias {dtype}")
+
+
+def test_skinny_against_tiled_kernel():
+    """The same fp32 group through the tiled MFMA kernel (variant 3) and the
+    streaming kernel: both against the oracle."""
+    say("[linear skinny vs tiled]")
+    ms = _members([(4000, 8, 8), (3000, 4, 2)], "fp32", seed=33, bias=False)
+    for v in (3, 7):
+        ys = _run(ms, "fp32", "none", variant=v)
+        _check(ms, ys, "fp32", "none", f"variant {v}")

@@ -168,3 +168,23 @@ def test_large_group_full_size_sampled_rows():
                      f"member {i} layernorm+tanh (per op)")
         assert_close(host64(zs[i])[rows], ORC.layernorm(lin, g64, b64, wl.eps, "tanh"), "bf16",
                      f"member {i} end to end")
+
+
+def test_decompose_mm_full_size_sampled_rows():
+    """The four tall-skinny mm members of the decompose_mm case study at full
+    size (84 M rows, fp32) in one launch of the streaming kernel, on sampled rows."""
+    say("[workload decompose_mm] 4 members, 84 M rows, fp32")
+    wl = synth.decompose_mm(0)
+    xs = [dev(m.x) for m in wl.members]
+    ws = [dev(m.w) for m in wl.members]
+    ys = [torch.empty((m.M, m.N), dtype=torch.float32, device="cuda") for m in wl.members]
+    p = B.optimus_plan_linear(xs, ws, [None] * 4, ys, "none")
+    assert p.info()["kernel"] == "grouped_gemm_skinny" and p.info()["launches"] == 1
+    p.execute()
+    torch.cuda.synchronize()
+    for i, m in enumerate(wl.members):
+        rows = _sample_rows(m.M, 2000, seed=70 + i)
+        x64 = synth.exact64(m.x[torch.from_numpy(rows)])
+        ref = ORC.linear(x64, synth.exact64(m.w), None)
+        got = synth.exact64(ys[i][torch.from_numpy(rows).to("cuda")])
+        assert_close(got, ref, "fp32", f"member {i} {tuple(m.x.shape)} x {tuple(m.w.shape)}")
