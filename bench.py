@@ -248,7 +248,7 @@ def traffic_from_profile(kernel, name):
         return None
     with open(path) as f:
         pmc = json.load(f)
-    if pmc.get("sources_sha256") != sources_hash():
+    if pmc.get("sources_sha256") != sources_hash(kernel_symbol(kernel)):
         return None
     return pmc.get("hbm_bytes_per_launch")
 
@@ -289,7 +289,7 @@ def pmc_summary(args):
            "copy_bytes": COPY_BYTES, "copy_fetch_kib": round(cfetch, 1), "copy_write_kib": round(cwrite, 1),
            "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
            "hbm_bytes_per_launch": round(fetch * 1024.0 * fs + write * 1024.0 * ws),
-           "sources_sha256": sources_hash(), "command": args.pmc_command}
+           "sources_sha256": sources_hash(kernel), "command": args.pmc_command}
     path = os.path.join(ROOT, "profiles", f"{kernel}__{name}.pmc.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
@@ -316,7 +316,7 @@ def copy_probe():
 
 def kernel_symbol(label):
     """Symbol name of the kernel behind a plan's kernel label."""
-    for prefix, sym in (("grouped_gemm_dma", "grouped_gemm_dma_kernel"),
+    for prefix, sym in (("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
                         ("grouped_gemm", "grouped_gemm_kernel"), ("split_op_cat_fused", "split_op_cat_kernel"),
                         ("grouped_layernorm", "grouped_layernorm_kernel"), ("grouped_pointwise", "grouped_pointwise_kernel")):
         if label.startswith(prefix):
@@ -324,13 +324,21 @@ def kernel_symbol(label):
     return label
 
 
-def sources_hash():
+# The source files a kernel is built from (its translation unit and the shared
+# headers): a counter summary is used only while these are unchanged.
+KERNEL_SOURCES = {
+    "grouped_gemm_kernel": "kernels_gemm.hip", "grouped_gemm_dma_kernel": "kernels_gemm.hip",
+    "grouped_gemm_skinny_kernel": "kernels_gemm.hip", "split_op_cat_kernel": "kernels_rowwise.hip",
+    "grouped_layernorm_kernel": "kernels_rowwise.hip", "grouped_pointwise_kernel": "kernels_rowwise.hip",
+}
+
+
+def sources_hash(kernel):
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_02945_amd", "csrc")
-    for fn in sorted(os.listdir(csrc)):
-        if fn.endswith((".hip", ".h")):
-            with open(os.path.join(csrc, fn), "rb") as f:
-                h.update(fn.encode() + f.read())
+    for fn in sorted([KERNEL_SOURCES[kernel], "device_common.h", "optimus_internal.h"]):
+        with open(os.path.join(csrc, fn), "rb") as f:
+            h.update(fn.encode() + f.read())
     return h.hexdigest()
 
 
