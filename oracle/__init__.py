@@ -85,6 +85,17 @@ class Oracle:
                                           ctypes.c_int64, ctypes.c_int32, _i64p,
                                           ctypes.POINTER(_dp), ctypes.POINTER(_dp),
                                           ctypes.c_int32, ctypes.c_double, ctypes.c_int]
+        L.oracle_fp8e4m3_decode.restype = ctypes.c_double
+        L.oracle_fp8e4m3_decode.argtypes = [ctypes.c_int]
+        L.oracle_fp8e4m3_encode.restype = ctypes.c_int
+        L.oracle_fp8e4m3_encode.argtypes = [ctypes.c_double, ctypes.c_int]
+        _u8p = ctypes.POINTER(ctypes.c_uint8)
+        L.oracle_quantize_fp8.restype = None
+        L.oracle_quantize_fp8.argtypes = [_dp, ctypes.c_int64, _u8p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+        L.oracle_dequantize_fp8.restype = None
+        L.oracle_dequantize_fp8.argtypes = [_u8p, ctypes.c_int64, _dp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                            ctypes.c_float]
         L.oracle_num_threads.restype = ctypes.c_int
         L.oracle_num_threads.argtypes = []
 
@@ -170,6 +181,34 @@ class Oracle:
         plain composition LN(X W^T + bias) over each output row, then act, in
         fp64 with no rounding of the intermediate."""
         return self.layernorm(self.linear(x, w, bias, "none"), gamma, beta, eps, act)
+
+    # ------------------------------------------------------------ fp8 codec
+    def fp8_decode(self, code: int) -> float:
+        """Value of an OCP E4M3 code."""
+        return self.lib.oracle_fp8e4m3_decode(int(code))
+
+    def fp8_encode(self, v: float, saturate: bool = False) -> int:
+        """OCP E4M3 code of v (round to nearest even; overflow -> NaN or +-448)."""
+        return self.lib.oracle_fp8e4m3_encode(float(v), int(bool(saturate)))
+
+    def quantize_fp8(self, x, use_scaling=True):
+        """(codes uint8 [rows, cols], fp32 scale) of one tensor of fp32-exact values."""
+        x = _c64(x)
+        rows, cols = x.shape
+        q = np.empty((rows, cols), dtype=np.uint8)
+        sc = ctypes.c_float(1.0)
+        self.lib.oracle_quantize_fp8(_ptr(x), cols, q.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), cols, rows,
+                                     cols, int(bool(use_scaling)), ctypes.byref(sc))
+        return q, np.float32(sc.value)
+
+    def dequantize_fp8(self, q, scale=1.0) -> np.ndarray:
+        """fp32(decode(code) * scale), as fp64 values."""
+        q = np.ascontiguousarray(q, dtype=np.uint8)
+        rows, cols = q.shape
+        y = np.empty((rows, cols), dtype=np.float64)
+        self.lib.oracle_dequantize_fp8(q.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), cols, _ptr(y), cols, rows,
+                                       cols, float(np.float32(scale)))
+        return y
 
     def num_threads(self) -> int:
         return self.lib.oracle_num_threads()

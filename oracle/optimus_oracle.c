@@ -181,6 +181,93 @@ int oracle_split_op_cat(const double* in, int64_t ldin, double* out, int64_t ldo
   return 0;
 }
 
+/* ------------------------------------------------------- fp8 activation codec
+ *
+ * The activation-quantization rewrite (paper Sec. 5 memory results; appendix
+ * Sec. 8.2, peak memory usage reduction) stores saved activations in FP8 in
+ * the forward pass and restores them before use in the backward pass, with
+ * or without a per-tensor scale; without the scale, values that overflow FP8
+ * become NaN. FP8 here is the OCP E4M3 format: sign, 4 exponent bits (bias 7),
+ * 3 mantissa bits, no infinities, S.1111.111 = NaN, largest finite 448,
+ * smallest normal 2^-6, subnormals m * 2^-9 (m = 1..7). Rounding is to
+ * nearest, ties to even.
+ *
+ * Scaled mode: amax = max |x| over the tensor (NaN ignored), scale = amax/448
+ * and inv = 448/amax in fp32 (1 and 1 when amax is 0); code = E4M3(fp32(x *
+ * inv)), clamped to +-448. Unscaled mode: code = E4M3(x), magnitudes that
+ * round above 448 (|x| >= 464, the midpoint to the next power-of-two step)
+ * give NaN. Decode: the code's value times scale in fp32. Every fp32 step is
+ * written in fp32 (float) arithmetic, so a quantised code is decided in the
+ * same precision on every implementation. */
+
+/* Value of an E4M3 code (NaN for S.1111.111). */
+double oracle_fp8e4m3_decode(int code) {
+  const int s = (code >> 7) & 1, e = (code >> 3) & 15, m = code & 7;
+  if (e == 15 && m == 7) return NAN;
+  const double mag = e == 0 ? ldexp((double)m, -9) : ldexp(1.0 + m / 8.0, e - 7);
+  return s ? -mag : mag;
+}
+
+/* E4M3 code of a finite or non-finite value; saturate: clamp overflow to
+ * +-448 instead of NaN. */
+int oracle_fp8e4m3_encode(double v, int saturate) {
+  if (isnan(v)) return 0x7F;
+  const int s = signbit(v) ? 0x80 : 0;
+  double a = fabs(v);
+  if (a >= 464.0) return saturate ? (s | 0x7E) : (s | 0x7F); /* infinities too */
+  int code;
+  if (a < ldexp(1.0, -6)) {
+    /* subnormal range: steps of 2^-9; 8 steps is the smallest normal (code 8) */
+    code = (int)nearbyint(a / ldexp(1.0, -9));
+  } else {
+    int e2;
+    frexp(a, &e2);                              /* a = f * 2^e2, f in [0.5, 1) */
+    const int e = e2 - 1;                       /* a in [2^e, 2^(e+1)) */
+    long q = (long)nearbyint(a / ldexp(1.0, e - 3)); /* 8 ..16 mantissa steps */
+    int ef = e;
+    if (q == 16) { q = 8; ef = e + 1; }
+    code = ((ef + 7) << 3) | (int)(q - 8);
+  }
+  if (code > 0x7E) code = saturate ? 0x7E : 0x7F;
+  return s | code;
+}
+
+/* One tensor x[rows][cols] (fp32 values given exactly as doubles) to codes
+ * q[rows][ldq]; *scale_out receives the fp32 scale (scaled mode only). */
+void oracle_quantize_fp8(const double* x, int64_t ldx, uint8_t* q, int64_t ldq, int64_t rows, int64_t cols,
+                         int use_scaling, float* scale_out) {
+  float inv = 1.0f, scale = 1.0f;
+  if (use_scaling) {
+    float amax = 0.0f;
+    for (int64_t r = 0; r < rows; ++r)
+      for (int64_t c = 0; c < cols; ++c) {
+        const float a = fabsf((float)x[r * ldx + c]);
+        if (a > amax) amax = a; /* NaN compares false: ignored */
+      }
+    if (amax > 0.0f) {
+      scale = amax / 448.0f;
+      inv = 448.0f / amax;
+    }
+    if (scale_out) *scale_out = scale;
+  }
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t c = 0; c < cols; ++c) {
+      const float xv = (float)x[r * ldx + c];
+      const float v = use_scaling ? xv * inv : xv;
+      q[r * ldq + c] = (uint8_t)oracle_fp8e4m3_encode((double)v, use_scaling);
+    }
+}
+
+/* Codes q[rows][ldq] back to values y = fp32(decode(code) * scale). */
+void oracle_dequantize_fp8(const uint8_t* q, int64_t ldq, double* y, int64_t ldy, int64_t rows, int64_t cols,
+                           float scale) {
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t c = 0; c < cols; ++c) {
+      const float v = (float)oracle_fp8e4m3_decode(q[r * ldq + c]);
+      y[r * ldy + c] = (double)(v * scale);
+    }
+}
+
 /* Number of OpenMP threads the oracle's parallel loops use (1 without OpenMP). */
 int oracle_num_threads(void) {
 #ifdef _OPENMP

@@ -206,6 +206,84 @@ def linear_layernorm_invariants(orc):
     assert np.array_equal(yc, np.broadcast_to(bt, (9, 24)))
 
 
+# ---------------------------------------------------------------- fp8 codec
+def _torch_e4m3_value(codes):
+    """Values of E4M3 codes through torch's own float8_e4m3fn type."""
+    return torch.tensor(np.asarray(codes, np.uint8)).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+
+
+def _torch_e4m3_code(values):
+    return torch.tensor(np.asarray(values, np.float32)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def fp8_decode_all_codes(orc):
+    """Every one of the 256 codes decodes to torch's float8_e4m3fn value (NaN
+    at S.1111.111 only); the largest finite is 448 and the smallest subnormal 2^-9."""
+    got = np.array([orc.fp8_decode(c) for c in range(256)])
+    ref = _torch_e4m3_value(range(256))
+    assert np.array_equal(np.isnan(got), np.isnan(ref)) and np.isnan(got).sum() == 2
+    fin = ~np.isnan(ref)
+    assert np.array_equal(got[fin], ref[fin]) and np.array_equal(np.signbit(got[fin]), np.signbit(ref[fin]))
+    assert np.nanmax(got) == 448.0 and got[1] == 2.0 ** -9
+
+
+def fp8_encode_round_trip_and_ties(orc):
+    """encode(decode(c)) == c for every finite code (both modes), and every
+    midpoint between adjacent codes of one sign goes to the even mantissa."""
+    for sat in (False, True):
+        for c in range(256):
+            if c & 0x7F == 0x7F:
+                continue
+            assert orc.fp8_encode(orc.fp8_decode(c), sat) == c, (c, sat)
+    for c in range(0, 0x7E):
+        lo, hi = orc.fp8_decode(c), orc.fp8_decode(c + 1)
+        mid = (lo + hi) / 2
+        want = c if c % 2 == 0 else c + 1
+        assert orc.fp8_encode(mid) == want and orc.fp8_encode(-mid) == want | 0x80, c
+        assert orc.fp8_encode(np.nextafter(mid, 0)) == c and orc.fp8_encode(np.nextafter(mid, 1e9)) == c + 1
+
+
+def fp8_encode_vs_torch(orc):
+    """Every bf16 value and 20000 random fp32 values of every magnitude, within
+    the finite range, encode as torch's float8_e4m3fn conversion does."""
+    bits = np.arange(65536, dtype=np.uint32) << 16
+    vals = bits.view(np.float32)
+    g = _rng(19)
+    rnd = (g.standard_normal(20000) * np.exp2(g.uniform(-14, 9, 20000))).astype(np.float32)
+    for v in (vals, rnd):
+        v = v[np.isfinite(v) & (np.abs(v) <= 448)]
+        got = np.array([orc.fp8_encode(float(t)) for t in v], dtype=np.uint8)
+        assert np.array_equal(got, _torch_e4m3_code(v))
+
+
+def fp8_overflow_and_scaling(orc):
+    """Unscaled: |x| >= 464 (the round-up midpoint past 448) and non-finite
+    values give NaN, just below stays 448. Scaled: the largest magnitude lands
+    exactly on +-448, every code is finite, and decode(code) * scale is within
+    half a code step of x."""
+    assert orc.fp8_encode(463.99) == 0x7E and orc.fp8_encode(464.0) == 0x7F and orc.fp8_encode(-464.0) == 0xFF
+    assert orc.fp8_encode(float("inf")) == 0x7F and orc.fp8_encode(float("nan")) & 0x7F == 0x7F
+    assert orc.fp8_encode(1e6, True) == 0x7E and orc.fp8_encode(-1e6, True) == 0xFE
+    g = _rng(20)
+    x = (g.standard_normal((40, 33)) * 37.0).astype(np.float32).astype(np.float64)
+    q, scale = orc.quantize_fp8(x, True)
+    assert np.float32(scale) == np.float32(np.float32(np.abs(x).max()) / np.float32(448.0))
+    i = np.unravel_index(np.argmax(np.abs(x)), x.shape)
+    assert q[i] in (0x7E, 0xFE) and np.all((q & 0x7F) != 0x7F)
+    y = orc.dequantize_fp8(q, scale)
+    step = np.exp2(np.floor(np.log2(np.maximum(np.abs(x) / scale, 2.0 ** -6))) - 3) * scale
+    assert np.all(np.abs(y - x) <= step / 2 * (1 + 1e-6))
+    # torch: the same codes decode to the same values, times the fp32 scale
+    ref = (torch.tensor(q).view(torch.float8_e4m3fn).to(torch.float32) * torch.tensor(scale)).to(torch.float64)
+    assert np.array_equal(y, ref.numpy())
+    # unscaled: in-range values keep torch's codes; 500 -> NaN
+    x[0, 0] = 500.0
+    qu, _ = orc.quantize_fp8(x, False)
+    assert qu[0, 0] == 0x7F
+    fin = np.abs(x) < 448
+    assert np.array_equal(qu[fin], _torch_e4m3_code(x[fin].astype(np.float32)))
+
+
 # ---------------------------------------------------------------- pointwise
 def pointwise_closed_forms(orc):
     """Values at 0, symmetries, the tanh/sigmoid identity, saturation, numpy forms."""
@@ -311,6 +389,7 @@ ALL_PINS = [
     linear_vs_blas, linear_special_cases, linear_brute_force, linear_epilogue, linear_rows_subset,
     linear_batch_fusion, linear_shared_input, layernorm_vs_torch, layernorm_invariants, layernorm_constant_row,
     layernorm_affine, layernorm_epilogue_and_batch, linear_layernorm_reductions, linear_layernorm_invariants,
+    fp8_decode_all_codes, fp8_encode_round_trip_and_ties, fp8_encode_vs_torch, fp8_overflow_and_scaling,
     pointwise_closed_forms,
     split_concat_appendix_example, split_concat_identity_random, split_op_cat_pieces, split_op_cat_tag,
     split_op_cat_bad_widths,

@@ -34,6 +34,14 @@ MUTANTS = [
     ("cat_offset_dropped", "out[r * ldout + off + c] = res[r * w + c];", "out[r * ldout + c] = res[r * w + c];"),
     ("piece_params_shifted", "gamma ? gamma[j] : NULL,\n                       beta ? beta[j] : NULL",
      "gamma ? gamma[0] : NULL,\n                       beta ? beta[0] : NULL"),
+    ("fp8_bias_off", "ldexp(1.0 + m / 8.0, e - 7)", "ldexp(1.0 + m / 8.0, e - 8)"),
+    ("fp8_truncate", "long q = (long)nearbyint(a / ldexp(1.0, e - 3));", "long q = (long)floor(a / ldexp(1.0, e - 3));"),
+    ("fp8_subnormal_truncate", "code = (int)nearbyint(a / ldexp(1.0, -9));", "code = (int)floor(a / ldexp(1.0, -9));"),
+    ("fp8_sign_dropped", "const int s = signbit(v) ? 0x80 : 0;", "const int s = 0;"),
+    ("fp8_overflow_threshold", "if (a >= 464.0)", "if (a > 448.0)"),
+    ("fp8_scale_inverted", "inv = 448.0f / amax;", "inv = amax / 448.0f;"),
+    ("fp8_no_carry", "if (q == 16) { q = 8; ef = e + 1; }", ""),
+    ("fp8_dequant_no_scale", "y[r * ldy + c] = (double)(v * scale);", "y[r * ldy + c] = (double)v;"),
 ]
 
 
