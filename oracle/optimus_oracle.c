@@ -195,8 +195,9 @@ int oracle_split_op_cat(const double* in, int64_t ldin, double* out, int64_t ldo
  * Scaled mode: amax = max |x| over the tensor (NaN ignored), scale = amax/448
  * and inv = 448/amax in fp32 (1 and 1 when amax is 0); code = E4M3(fp32(x *
  * inv)), clamped to +-448. Unscaled mode: code = E4M3(x), magnitudes that
- * round above 448 (|x| >= 464, the midpoint to the next power-of-two step)
- * give NaN. Decode: the code's value times scale in fp32. Every fp32 step is
+ * round above 448 (|x| > 464; 464 itself is a tie that goes to the even 448)
+ * give NaN. A NaN input gives the NaN code with the input's sign in both
+ * modes. Decode: the code's value times scale in fp32. Every fp32 step is
  * written in fp32 (float) arithmetic, so a quantised code is decided in the
  * same precision on every implementation. */
 
@@ -211,10 +212,13 @@ double oracle_fp8e4m3_decode(int code) {
 /* E4M3 code of a finite or non-finite value; saturate: clamp overflow to
  * +-448 instead of NaN. */
 int oracle_fp8e4m3_encode(double v, int saturate) {
-  if (isnan(v)) return 0x7F;
   const int s = signbit(v) ? 0x80 : 0;
+  if (isnan(v)) return s | 0x7F; /* NaN keeps its sign, in both modes */
   double a = fabs(v);
-  if (a >= 464.0) return saturate ? (s | 0x7E) : (s | 0x7F); /* infinities too */
+  /* 464 is halfway between 448 (mantissa 110) and the next step 480 (111,
+   * the NaN pattern): ties-to-even takes 448, so only larger magnitudes
+   * overflow (infinities too). */
+  if (a > 464.0) return saturate ? (s | 0x7E) : (s | 0x7F);
   int code;
   if (a < ldexp(1.0, -6)) {
     /* subnormal range: steps of 2^-9; 8 steps is the smallest normal (code 8) */

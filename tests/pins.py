@@ -244,26 +244,35 @@ def fp8_encode_round_trip_and_ties(orc):
 
 
 def fp8_encode_vs_torch(orc):
-    """Every bf16 value and 20000 random fp32 values of every magnitude, within
-    the finite range, encode as torch's float8_e4m3fn conversion does."""
+    """Every bf16 value (overflow, infinities and NaNs of both signs included)
+    and 20000 random fp32 values of every magnitude encode, unsaturated, as
+    torch's float8_e4m3fn conversion does; the fp32 neighbours of the overflow
+    tie 464 too."""
     bits = np.arange(65536, dtype=np.uint32) << 16
     vals = bits.view(np.float32)
     g = _rng(19)
-    rnd = (g.standard_normal(20000) * np.exp2(g.uniform(-14, 9, 20000))).astype(np.float32)
-    for v in (vals, rnd):
-        v = v[np.isfinite(v) & (np.abs(v) <= 448)]
+    rnd = (g.standard_normal(20000) * np.exp2(g.uniform(-14, 10, 20000))).astype(np.float32)
+    edge = np.array([464.0, np.nextafter(np.float32(464), np.float32(0)), np.nextafter(np.float32(464), np.float32(1e9)),
+                     447.99, 448.0, 456.0, 472.0, 479.99, 480.0], np.float32)
+    for v in (vals, rnd, edge, -edge):
         got = np.array([orc.fp8_encode(float(t)) for t in v], dtype=np.uint8)
         assert np.array_equal(got, _torch_e4m3_code(v))
 
 
 def fp8_overflow_and_scaling(orc):
-    """Unscaled: |x| >= 464 (the round-up midpoint past 448) and non-finite
-    values give NaN, just below stays 448. Scaled: the largest magnitude lands
-    exactly on +-448, every code is finite, and decode(code) * scale is within
-    half a code step of x."""
-    assert orc.fp8_encode(463.99) == 0x7E and orc.fp8_encode(464.0) == 0x7F and orc.fp8_encode(-464.0) == 0xFF
-    assert orc.fp8_encode(float("inf")) == 0x7F and orc.fp8_encode(float("nan")) & 0x7F == 0x7F
+    """Unscaled: |x| > 464 and infinities give NaN; the tie 464 itself rounds
+    to the even mantissa, 448. Saturated: overflow and infinities give +-448,
+    NaN stays NaN with its sign. Scaled: the largest magnitude lands exactly
+    on +-448, every code is finite, and decode(code) * scale is within half a
+    code step of x."""
+    above = float(np.nextafter(464.0, 1e9))
+    assert orc.fp8_encode(463.99) == 0x7E and orc.fp8_encode(464.0) == 0x7E and orc.fp8_encode(-464.0) == 0xFE
+    assert orc.fp8_encode(above) == 0x7F and orc.fp8_encode(-above) == 0xFF
+    assert orc.fp8_encode(float("inf")) == 0x7F and orc.fp8_encode(-float("inf")) == 0xFF
+    assert orc.fp8_encode(float("nan")) == 0x7F and orc.fp8_encode(-float("nan")) == 0xFF
     assert orc.fp8_encode(1e6, True) == 0x7E and orc.fp8_encode(-1e6, True) == 0xFE
+    assert orc.fp8_encode(above, True) == 0x7E and orc.fp8_encode(-float("inf"), True) == 0xFE
+    assert orc.fp8_encode(float("nan"), True) == 0x7F and orc.fp8_encode(-float("nan"), True) == 0xFF
     g = _rng(20)
     x = (g.standard_normal((40, 33)) * 37.0).astype(np.float32).astype(np.float64)
     q, scale = orc.quantize_fp8(x, True)

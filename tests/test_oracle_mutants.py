@@ -38,7 +38,8 @@ MUTANTS = [
     ("fp8_truncate", "long q = (long)nearbyint(a / ldexp(1.0, e - 3));", "long q = (long)floor(a / ldexp(1.0, e - 3));"),
     ("fp8_subnormal_truncate", "code = (int)nearbyint(a / ldexp(1.0, -9));", "code = (int)floor(a / ldexp(1.0, -9));"),
     ("fp8_sign_dropped", "const int s = signbit(v) ? 0x80 : 0;", "const int s = 0;"),
-    ("fp8_overflow_threshold", "if (a >= 464.0)", "if (a > 448.0)"),
+    ("fp8_overflow_threshold", "if (a > 464.0)", "if (a >= 464.0)"),
+    ("fp8_nan_unsigned", "if (isnan(v)) return s | 0x7F;", "if (isnan(v)) return 0x7F;"),
     ("fp8_scale_inverted", "inv = 448.0f / amax;", "inv = amax / 448.0f;"),
     ("fp8_no_carry", "if (q == 16) { q = 8; ef = e + 1; }", ""),
     ("fp8_dequant_no_scale", "y[r * ldy + c] = (double)(v * scale);", "y[r * ldy + c] = (double)v;"),
