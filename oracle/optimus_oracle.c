@@ -197,7 +197,9 @@ int oracle_split_op_cat(const double* in, int64_t ldin, double* out, int64_t ldo
  * inv)), clamped to +-448. Unscaled mode: code = E4M3(x), magnitudes that
  * round above 448 (|x| > 464; 464 itself is a tie that goes to the even 448)
  * give NaN. A NaN input gives the NaN code with the input's sign in both
- * modes. Decode: the code's value times scale in fp32. Every fp32 step is
+ * modes; so does an infinite input in scaled mode (amax is then infinite,
+ * inv is 0 and x * inv is NaN). Decode: the code's value times scale in
+ * fp32. Every fp32 step is
  * written in fp32 (float) arithmetic, so a quantised code is decided in the
  * same precision on every implementation. */
 
@@ -258,7 +260,11 @@ void oracle_quantize_fp8(const double* x, int64_t ldx, uint8_t* q, int64_t ldq, 
     for (int64_t c = 0; c < cols; ++c) {
       const float xv = (float)x[r * ldx + c];
       const float v = use_scaling ? xv * inv : xv;
-      q[r * ldq + c] = (uint8_t)oracle_fp8e4m3_encode((double)v, use_scaling);
+      /* A NaN value takes the sign of x itself: the sign of the NaN that
+       * +-inf * 0 yields (amax infinite, so inv = 0) differs between
+       * platforms. */
+      q[r * ldq + c] = isnan(v) ? (uint8_t)(signbit(xv) ? 0xFF : 0x7F)
+                                : (uint8_t)oracle_fp8e4m3_encode((double)v, use_scaling);
     }
 }
 

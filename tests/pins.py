@@ -285,6 +285,11 @@ def fp8_overflow_and_scaling(orc):
     # torch: the same codes decode to the same values, times the fp32 scale
     ref = (torch.tensor(q).view(torch.float8_e4m3fn).to(torch.float32) * torch.tensor(scale)).to(torch.float64)
     assert np.array_equal(y, ref.numpy())
+    # an infinite element makes amax infinite: inv = 0, finite values give
+    # (signed) zero codes, the infinities NaN codes with their own sign
+    xi = np.array([[1.5, -2.0, np.inf], [-np.inf, 0.0, 3.0]])
+    qi, si = orc.quantize_fp8(xi, True)
+    assert np.isinf(si) and qi.tolist() == [[0x00, 0x80, 0x7F], [0xFF, 0x00, 0x00]]
     # unscaled: in-range values keep torch's codes; 500 -> NaN
     x[0, 0] = 500.0
     qu, _ = orc.quantize_fp8(x, False)

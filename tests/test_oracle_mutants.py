@@ -40,6 +40,7 @@ MUTANTS = [
     ("fp8_sign_dropped", "const int s = signbit(v) ? 0x80 : 0;", "const int s = 0;"),
     ("fp8_overflow_threshold", "if (a > 464.0)", "if (a >= 464.0)"),
     ("fp8_nan_unsigned", "if (isnan(v)) return s | 0x7F;", "if (isnan(v)) return 0x7F;"),
+    ("fp8_nan_sign_of_product", "isnan(v) ? (uint8_t)(signbit(xv) ? 0xFF : 0x7F)", "isnan(v) ? (uint8_t)(signbit(v) ? 0xFF : 0x7F)"),
     ("fp8_scale_inverted", "inv = 448.0f / amax;", "inv = amax / 448.0f;"),
     ("fp8_no_carry", "if (q == 16) { q = 8; ef = e + 1; }", ""),
     ("fp8_dequant_no_scale", "y[r * ldy + c] = (double)(v * scale);", "y[r * ldy + c] = (double)v;"),
