@@ -48,7 +48,8 @@
  *                                        independent, Sec. 4.1); exact
  *                                        in-place (y == x with equal strides)
  *                                        is allowed for LayerNorm, pointwise
- *                                        and split-op-cat
+ *                                        and split-op-cat (never for the fp8
+ *                                        codec)
  *               OPTIMUS_ERR_HIP          a HIP runtime call failed
  *               OPTIMUS_ERR_OOM          device allocation failed
  *   Alignment   Pointers or strides that are not 16-byte aligned, or row
@@ -151,6 +152,31 @@ typedef struct {
   optimus_act act;
 } optimus_split_op_cat_desc;
 
+/* One member of the fp8 activation codec (paper Sec. 5, peak memory usage
+ * reduction; appendix Sec. 8.2, activation quantization: saved activations
+ * are stored in FP8 in the forward pass and restored to their own dtype
+ * before use in the backward pass, with or without a per-tensor scale).
+ * FP8 is OCP E4M3: one byte per value, bias 7, largest finite 448, no
+ * infinities, S.1111.111 = NaN. x: values [rows][ldx] of the group's dtype;
+ * q: codes [rows][ldq] (uint8); scale: ONE device fp32 value. */
+typedef struct {
+  const void* x;
+  int64_t ldx;
+  void* q;
+  int64_t ldq;
+  float* scale;  /* written by a scaled quantize; unused (may be NULL) unscaled */
+  int64_t rows, cols;
+} optimus_fp8_quant_desc;
+
+typedef struct {
+  const void* q;
+  int64_t ldq;
+  const float* scale;  /* read; NULL means 1 */
+  void* y;
+  int64_t ldy;
+  int64_t rows, cols;
+} optimus_fp8_dequant_desc;
+
 /* ---------------------------------------------------------------- one-shot
  * Validate, build the launch schedule, upload it (stream-ordered) and launch
  * ONE kernel for the whole group on `stream`. */
@@ -188,6 +214,28 @@ optimus_status optimus_grouped_pointwise(const optimus_pointwise_desc* d, int32_
 optimus_status optimus_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
                                     optimus_stream_t stream);
 
+/* Grouped fp8 quantize of G activation tensors, one launch (Sec. 3.2 group
+ * fusion applied to the activation-quantization rewrite, Sec. 5).
+ *   use_scaling = 1: amax = max |x| over the member (NaN values skipped),
+ *     scale = amax / 448 and inv = 448 / amax in fp32 (both 1 if amax is 0),
+ *     *scale is written, q = E4M3(fp32(x * inv)) with magnitudes saturated
+ *     to 448 (no code is NaN unless x holds NaN, or an infinity, which makes
+ *     amax infinite, inv 0 and x * inv NaN for the infinities).
+ *   use_scaling = 0: q = E4M3(x); magnitudes above 464 (448 plus half a
+ *     step; 464 itself rounds to the even 448) and infinities give the NaN
+ *     code -- the overflow the paper warns about when scaling is disabled.
+ * Rounding is to nearest, ties to even; a NaN value gives S.1111.111 with
+ * the sign of x. use_scaling other than 0/1 -> INVALID_ARG; scaled members
+ * need a non-NULL scale. The scaled form is one launch: per-member amax
+ * partials are combined inside the kernel (see optimus_plan_quantize_fp8). */
+optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                            int32_t use_scaling, optimus_stream_t stream);
+
+/* Grouped fp8 dequantize: y = fp32(value(q) * scale) rounded to the group's
+ * dtype (nearest even for bf16); NaN codes give NaN. */
+optimus_status optimus_grouped_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
+                                              optimus_stream_t stream);
+
 /* ---------------------------------------------------------------- plans
  * A plan validates once and keeps the group's descriptor table and launch
  * schedule resident in device memory (allocated with hipMalloc on the current
@@ -208,6 +256,16 @@ optimus_status optimus_plan_pointwise(const optimus_pointwise_desc* d, int32_t G
                                       optimus_act op, optimus_plan* out);
 optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
                                          optimus_plan* out);
+/* A scaled quantize plan also owns a small control block (ticket and done
+ * counters, a launch generation) and one 8-byte amax partial per amax tile
+ * per member; the kernel resets the counters when it finishes, so the plan
+ * can be executed again. Executions of one quantize plan must not overlap
+ * (use one stream, or order them with events); one-shot calls each get
+ * their own control block. */
+optimus_status optimus_plan_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                         int32_t use_scaling, optimus_plan* out);
+optimus_status optimus_plan_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
+                                           optimus_plan* out);
 
 /* Execution modes of a plan.
  *   GROUPED     one launch for the whole group (the optimized program).
@@ -238,7 +296,8 @@ void optimus_plan_destroy(optimus_plan plan);
  * once per tensor element read or written (inputs, weights, bias, gamma/beta,
  * outputs), never padding, re-reads or temporaries. */
 typedef struct {
-  int32_t kind;            /* 0 linear, 1 layernorm, 2 pointwise, 3 split_op_cat, 4 linear_layernorm */
+  int32_t kind;            /* 0 linear, 1 layernorm, 2 pointwise, 3 split_op_cat, 4 linear_layernorm,
+                              5 quantize_fp8, 6 dequantize_fp8 */
   int32_t group_size;      /* G, or n_slices */
   int32_t launches;        /* kernel launches per GROUPED execute (1) */
   int32_t chain_launches;  /* kernel launches per CHAIN execute */
@@ -262,6 +321,9 @@ optimus_status optimus_validate_linear_layernorm(const optimus_linear_desc* d, c
 optimus_status optimus_validate_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
 optimus_status optimus_validate_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
 optimus_status optimus_validate_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt);
+optimus_status optimus_validate_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                             int32_t use_scaling);
+optimus_status optimus_validate_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt);
 
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char* optimus_last_error(void);

@@ -46,6 +46,16 @@ class SplitOpCatDesc(ctypes.Structure):
                 ("act", ctypes.c_int)]
 
 
+class Fp8QuantDesc(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("ldx", c_i64), ("q", c_vp), ("ldq", c_i64), ("scale", c_vp), ("rows", c_i64),
+                ("cols", c_i64)]
+
+
+class Fp8DequantDesc(ctypes.Structure):
+    _fields_ = [("q", c_vp), ("ldq", c_i64), ("scale", c_vp), ("y", c_vp), ("ldy", c_i64), ("rows", c_i64),
+                ("cols", c_i64)]
+
+
 class PlanInfo(ctypes.Structure):
     _fields_ = [("kind", c_i32), ("group_size", c_i32), ("launches", c_i32), ("chain_launches", c_i32),
                 ("work_items", c_i64), ("grid", c_i32), ("block", c_i32), ("flops", ctypes.c_double),
@@ -55,13 +65,14 @@ class PlanInfo(ctypes.Structure):
 # Every symbol include/optimus.h declares.
 EXPORTS = [
     "optimus_grouped_linear", "optimus_grouped_linear_layernorm", "optimus_grouped_layernorm",
-    "optimus_grouped_pointwise", "optimus_split_op_cat",
+    "optimus_grouped_pointwise", "optimus_split_op_cat", "optimus_grouped_quantize_fp8",
+    "optimus_grouped_dequantize_fp8",
     "optimus_plan_linear", "optimus_plan_linear_layernorm", "optimus_plan_layernorm", "optimus_plan_pointwise",
-    "optimus_plan_split_op_cat",
+    "optimus_plan_split_op_cat", "optimus_plan_quantize_fp8", "optimus_plan_dequantize_fp8",
     "optimus_plan_execute", "optimus_plan_execute_mode", "optimus_plan_destroy", "optimus_plan_get_info",
     "optimus_validate_linear", "optimus_validate_linear_layernorm", "optimus_validate_layernorm",
-    "optimus_validate_pointwise",
-    "optimus_validate_split_op_cat", "optimus_last_error", "optimus_version",
+    "optimus_validate_pointwise", "optimus_validate_split_op_cat", "optimus_validate_quantize_fp8",
+    "optimus_validate_dequantize_fp8", "optimus_last_error", "optimus_version",
 ]
 
 
@@ -97,6 +108,12 @@ def lib() -> ctypes.CDLL:
             "optimus_plan_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
             "optimus_plan_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
             "optimus_plan_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int, P(c_vp)]),
+            "optimus_grouped_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32, c_vp]),
+            "optimus_grouped_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int, c_vp]),
+            "optimus_plan_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32, P(c_vp)]),
+            "optimus_plan_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int, P(c_vp)]),
+            "optimus_validate_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32]),
+            "optimus_validate_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int]),
             "optimus_plan_execute": (st, [c_vp, c_vp]),
             "optimus_plan_execute_mode": (st, [c_vp, ctypes.c_int, c_vp]),
             "optimus_plan_destroy": (None, [c_vp]),
@@ -187,6 +204,30 @@ def pointwise_descs(xs, ys) -> ctypes.Array:
     return arr
 
 
+def fp8_quant_descs(xs, qs, scales) -> ctypes.Array:
+    """xs: values (bf16 / fp32), qs: uint8 codes of the same shapes, scales:
+    one-element fp32 device tensors, or None (unscaled)."""
+    G = len(xs)
+    arr = (Fp8QuantDesc * max(G, 1))()
+    for g in range(G):
+        x, ldx = _mat(xs[g], "x")
+        q, ldq = _mat(qs[g], "q")
+        arr[g] = Fp8QuantDesc(x, ldx, q, ldq, _ptr(scales[g] if scales is not None else None), xs[g].shape[0],
+                              xs[g].shape[1])
+    return arr
+
+
+def fp8_dequant_descs(qs, scales, ys) -> ctypes.Array:
+    G = len(qs)
+    arr = (Fp8DequantDesc * max(G, 1))()
+    for g in range(G):
+        q, ldq = _mat(qs[g], "q")
+        y, ldy = _mat(ys[g], "y")
+        arr[g] = Fp8DequantDesc(q, ldq, _ptr(scales[g] if scales is not None else None), y, ldy, qs[g].shape[0],
+                                qs[g].shape[1])
+    return arr
+
+
 class _SocArgs:
     """Keeps the host arrays a split-op-cat descriptor points to alive."""
 
@@ -237,6 +278,19 @@ def optimus_split_op_cat(inp, out, widths, gammas=None, betas=None, apply_layern
                          stream=None) -> None:
     a = _SocArgs(inp, out, widths, gammas, betas, apply_layernorm, eps, act)
     check(lib().optimus_split_op_cat(ctypes.byref(a.desc), dtype_code(inp), _stream(stream)))
+
+
+def optimus_grouped_quantize_fp8(xs, qs, scales=None, use_scaling=True, stream=None) -> None:
+    """q_g = E4M3 codes of x_g (scaled: x_g * 448 / amax_g, with scale_g = amax_g / 448 written), one launch."""
+    d = fp8_quant_descs(xs, qs, scales)
+    check(lib().optimus_grouped_quantize_fp8(d, len(xs), dtype_code(xs[0]) if xs else BF16, int(use_scaling),
+                                             _stream(stream)))
+
+
+def optimus_grouped_dequantize_fp8(qs, scales, ys, stream=None) -> None:
+    """y_g = value(q_g) * scale_g in the dtype of y_g, one launch; scales None (or None entries) mean 1."""
+    d = fp8_dequant_descs(qs, scales, ys)
+    check(lib().optimus_grouped_dequantize_fp8(d, len(qs), dtype_code(ys[0]) if ys else BF16, _stream(stream)))
 
 
 # ------------------------------------------------------------------ plans
@@ -309,6 +363,18 @@ def optimus_plan_split_op_cat(inp, out, widths, gammas=None, betas=None, apply_l
                  keep=(inp, out, gammas, betas))
 
 
+def optimus_plan_quantize_fp8(xs, qs, scales=None, use_scaling=True) -> Plan:
+    d = fp8_quant_descs(xs, qs, scales)
+    return _plan(lib().optimus_plan_quantize_fp8, d, len(xs), dtype_code(xs[0]) if xs else BF16, int(use_scaling),
+                 keep=(list(xs), list(qs), scales))
+
+
+def optimus_plan_dequantize_fp8(qs, scales, ys) -> Plan:
+    d = fp8_dequant_descs(qs, scales, ys)
+    return _plan(lib().optimus_plan_dequantize_fp8, d, len(qs), dtype_code(ys[0]) if ys else BF16,
+                 keep=(list(qs), scales, list(ys)))
+
+
 # ------------------------------------------------------------------ host-only validation
 def optimus_validate_linear(descs: ctypes.Array, G: int, dtype: int, act="none") -> int:
     return lib().optimus_validate_linear(descs, G, dtype, _act(act))
@@ -330,6 +396,14 @@ def optimus_validate_pointwise(descs: ctypes.Array, G: int, dtype: int, act="non
 
 def optimus_validate_split_op_cat(desc: SplitOpCatDesc, dtype: int) -> int:
     return lib().optimus_validate_split_op_cat(ctypes.byref(desc), dtype)
+
+
+def optimus_validate_quantize_fp8(descs: ctypes.Array, G: int, dtype: int, use_scaling=1) -> int:
+    return lib().optimus_validate_quantize_fp8(descs, G, dtype, int(use_scaling))
+
+
+def optimus_validate_dequantize_fp8(descs: ctypes.Array, G: int, dtype: int) -> int:
+    return lib().optimus_validate_dequantize_fp8(descs, G, dtype)
 
 
 def optimus_last_error() -> str:

@@ -257,11 +257,68 @@ extern "C" optimus_status optimus_validate_split_op_cat(const optimus_split_op_c
   return check_aliasing(regs, true, "split_op_cat");
 }
 
+static optimus_status validate_fp8_member(const char* what, int g, const void* a, int64_t lda, size_t sa,
+                                          const void* b, int64_t ldb, size_t sb, int64_t rows, int64_t cols) {
+  if (!a || !b) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a NULL tensor", what, g);
+  if (rows < 1 || cols < 1 || rows > kMaxDim || cols > kMaxDim)
+    return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has rows=%lld cols=%lld", what, g, (long long)rows,
+                (long long)cols);
+  if (lda < cols || ldb < cols) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a row stride below cols", what, g);
+  (void)sa;
+  (void)sb;
+  return OPTIMUS_OK;
+}
+
+extern "C" optimus_status optimus_validate_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                                        int32_t use_scaling) {
+  const char* what = "grouped_quantize_fp8";
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: G = %d < 0", what, G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown dtype %d", what, (int)dt);
+  if (use_scaling != 0 && use_scaling != 1)
+    return fail(OPTIMUS_ERR_INVALID_ARG, "%s: use_scaling = %d (0 or 1)", what, (int)use_scaling);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: descriptor array is NULL", what);
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 3);
+  for (int g = 0; g < G; ++g) {
+    const optimus_fp8_quant_desc& m = d[g];
+    optimus_status st = validate_fp8_member(what, g, m.x, m.ldx, s, m.q, m.ldq, 1, m.rows, m.cols);
+    if (st != OPTIMUS_OK) return st;
+    if (use_scaling && !m.scale) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d needs a scale pointer", what, g);
+    regs.push_back(region(m.x, m.ldx, m.rows, m.cols, s, g, false));
+    regs.push_back(region(m.q, m.ldq, m.rows, m.cols, 1, g, true));
+    if (use_scaling) regs.push_back(region(m.scale, 1, 1, 1, sizeof(float), g, true));
+  }
+  return check_aliasing(regs, false, what);
+}
+
+extern "C" optimus_status optimus_validate_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G,
+                                                          optimus_dtype dt) {
+  const char* what = "grouped_dequantize_fp8";
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: G = %d < 0", what, G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown dtype %d", what, (int)dt);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: descriptor array is NULL", what);
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 3);
+  for (int g = 0; g < G; ++g) {
+    const optimus_fp8_dequant_desc& m = d[g];
+    optimus_status st = validate_fp8_member(what, g, m.q, m.ldq, 1, m.y, m.ldy, s, m.rows, m.cols);
+    if (st != OPTIMUS_OK) return st;
+    regs.push_back(region(m.q, m.ldq, m.rows, m.cols, 1, g, false));
+    if (m.scale) regs.push_back(region(m.scale, 1, 1, 1, sizeof(float), g, false));
+    regs.push_back(region(m.y, m.ldy, m.rows, m.cols, s, g, true));
+  }
+  return check_aliasing(regs, false, what);
+}
+
 // ===================================================================== host plans
 // A HostPlan is everything a launch needs, built on the host: a byte blob that
 // becomes the device table, offsets into it, device-to-device copies to run
 // after the upload (packing per-piece gamma/beta), and launch parameters.
-enum Kind { KIND_LINEAR = 0, KIND_LN = 1, KIND_PW = 2, KIND_SOC = 3 };
+enum Kind { KIND_LINEAR = 0, KIND_LN = 1, KIND_PW = 2, KIND_SOC = 3, KIND_Q8 = 5, KIND_DQ8 = 6 };
 
 struct Blob {
   std::vector<char> bytes;
@@ -315,6 +372,13 @@ struct HostPlan {
   std::vector<int32_t> soc_piece_first, soc_piece_count;  // per piece: tile range in soc_tiles
   int32_t soc_piece_tiles_total = 0;
   std::vector<size_t> soc_temp_fixups;  // blob offsets of DevRows pointers relative to the temp base
+  // fp8 codec: member table, item list (the grouped list, then per member
+  // the items of its CHAIN launch), and for scaled quantize the control
+  // block, amax partial slots and per-member amax words
+  bool q_scaled = false;
+  size_t q_descs_off = 0, q_items_off = 0, q_ctl_off = 0, q_slots_off = 0, q_mamax_off = 0;
+  RowLaunch q_grouped{};
+  std::vector<RowLaunch> q_chain;
   // measurement
   int32_t launches = 1, chain_launches = 0, grid = 0, block = 0;
   int64_t work_items = 0;
@@ -653,6 +717,181 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
   return OPTIMUS_OK;
 }
 
+// ===================================================================== fp8 codec plans
+// Value-side bytes of a convert / dequantize item; an amax item covers
+// OPTIMUS_FP8_AMAX_TILES of them; a member's convert items start
+// OPTIMUS_FP8_LAG_PCT percent of a grid of items after its last amax item.
+#ifndef OPTIMUS_FP8_TILE_BYTES
+#define OPTIMUS_FP8_TILE_BYTES 32768
+#endif
+#ifndef OPTIMUS_FP8_AMAX_TILES
+#define OPTIMUS_FP8_AMAX_TILES 4
+#endif
+#ifndef OPTIMUS_FP8_LAG_PCT
+#define OPTIMUS_FP8_LAG_PCT 100
+#endif
+
+// Item geometry of one member: the 16-byte path needs value rows made of
+// 16-byte chunks (16-byte aligned) and code rows of as many bytes (aligned
+// to that many); a unit is then one chunk, else one value.
+struct Fp8Geom {
+  bool vec;
+  int64_t units;       // units per row
+  int64_t unit_bytes;  // value-side bytes of a unit
+  int64_t seg;         // widest row segment of a convert item, in units
+  int lanes;           // threads per row
+};
+
+static Fp8Geom fp8_geom(const void* vals, int64_t ldv, const void* codes, int64_t ldc, int64_t cols, optimus_dtype dt) {
+  const int64_t s = (int64_t)dtype_size(dt), VEC = 16 / s;
+  Fp8Geom g{};
+  g.vec = cols % VEC == 0 && ldv % VEC == 0 && ldc % VEC == 0 && aligned16(vals) && ((uintptr_t)codes % VEC) == 0;
+  g.units = g.vec ? cols / VEC : cols;
+  g.unit_bytes = g.vec ? 16 : s;
+  g.seg = std::max<int64_t>(256, (OPTIMUS_FP8_TILE_BYTES / g.unit_bytes) / 256 * 256);
+  g.lanes = std::min(256, pow2ceil((int)std::min<int64_t>(g.units, g.seg)));
+  return g;
+}
+
+// Items covering one member: whole-row tiles of about `budget` value bytes
+// when a row fits in `seg` units, else single-row segments of `seg` units.
+// slot >= 0: amax items, numbered from `slot`.
+static void fp8_items(const Fp8Geom& g, int member, int64_t rows, int64_t budget, int64_t seg, int32_t slot,
+                      std::vector<Fp8Item>& out) {
+  const int64_t row_bytes = g.units * g.unit_bytes;
+  if (g.units <= seg) {
+    const int64_t rpb = 256 / g.lanes;
+    int64_t per = std::max<int64_t>(1, budget / row_bytes);
+    per = std::max<int64_t>(rpb, per / rpb * rpb);
+    for (int64_t r0 = 0; r0 < rows; r0 += per)
+      out.push_back(Fp8Item{member, (int32_t)r0, (int32_t)std::min<int64_t>(per, rows - r0), 0, (int32_t)g.units,
+                            slot < 0 ? -1 : slot++});
+  } else {
+    for (int64_t r = 0; r < rows; ++r)
+      for (int64_t c0 = 0; c0 < g.units; c0 += seg)
+        out.push_back(Fp8Item{member, (int32_t)r, 1, (int32_t)c0, (int32_t)std::min<int64_t>(c0 + seg, g.units),
+                              slot < 0 ? -1 : slot++});
+  }
+}
+
+static int32_t fp8_grid(int64_t items, optimus_dtype dt, int kernel) {
+  const int64_t cap = (int64_t)device_cu_count() * fp8_blocks_per_cu(dt, kernel);
+  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(items, cap));
+}
+
+// Shared by quantize and dequantize: the member table, the grouped item list
+// and the per-member CHAIN lists. `scaled` adds amax items, interleaved.
+static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vector<Fp8Geom>& geo, bool scaled,
+                      int kernel) {
+  const int G = (int)members.size();
+  std::vector<std::vector<Fp8Item>> conv(G), amax(G);
+  int32_t nslots = 0;
+  for (int g = 0; g < G; ++g) {
+    DevFp8& m = members[g];
+    m.lanes = geo[g].vec ? geo[g].lanes : 0;
+    m.lanes_scalar = geo[g].vec ? 0 : geo[g].lanes;
+    fp8_items(geo[g], g, m.rows, OPTIMUS_FP8_TILE_BYTES, geo[g].seg, -1, conv[g]);
+    if (scaled) {
+      m.slot0 = nslots;
+      fp8_items(geo[g], g, m.rows, (int64_t)OPTIMUS_FP8_TILE_BYTES * OPTIMUS_FP8_AMAX_TILES,
+                geo[g].seg * OPTIMUS_FP8_AMAX_TILES, nslots, amax[g]);
+      m.nslots = (int32_t)amax[g].size();
+      nslots += m.nslots;
+    }
+  }
+  std::vector<Fp8Item> items;
+  if (!scaled) {
+    for (int g = 0; g < G; ++g) items.insert(items.end(), conv[g].begin(), conv[g].end());
+  } else {
+    int64_t total = 0;
+    for (int g = 0; g < G; ++g) total += (int64_t)conv[g].size() + (int64_t)amax[g].size();
+    const int64_t lag = (int64_t)fp8_grid(total, hp.dt, kernel) * OPTIMUS_FP8_LAG_PCT / 100;
+    // A member's convert items follow its last amax item by `lag` items (or
+    // come at the end): every convert item comes after all amax items of its
+    // member, which is what makes the in-kernel waits finite.
+    std::vector<int64_t> a_end(G, 0);
+    int next = 0;
+    for (int g = 0; g < G; ++g) {
+      for (const Fp8Item& it : amax[g]) {
+        items.push_back(it);
+        while (next < g && (int64_t)items.size() >= a_end[next] + lag) {
+          items.insert(items.end(), conv[next].begin(), conv[next].end());
+          ++next;
+        }
+      }
+      a_end[g] = (int64_t)items.size();
+    }
+    for (; next < G; ++next) items.insert(items.end(), conv[next].begin(), conv[next].end());
+  }
+  const int32_t grouped_n = (int32_t)items.size();
+  hp.q_chain.clear();
+  for (int g = 0; g < G; ++g) {
+    const int32_t first = (int32_t)items.size();
+    items.insert(items.end(), amax[g].begin(), amax[g].end());
+    items.insert(items.end(), conv[g].begin(), conv[g].end());
+    const int32_t n = (int32_t)items.size() - first;
+    hp.q_chain.push_back(RowLaunch{0, 0, first, n, fp8_grid(n, hp.dt, kernel)});
+  }
+  hp.q_scaled = scaled;
+  hp.q_descs_off = hp.blob.add(members.data(), members.size() * sizeof(DevFp8));
+  hp.q_items_off = hp.blob.add(items.data(), items.size() * sizeof(Fp8Item));
+  if (scaled) {
+    hp.q_ctl_off = hp.blob.add(nullptr, sizeof(Fp8Ctl));
+    hp.q_slots_off = hp.blob.add(nullptr, (size_t)std::max(nslots, 1) * sizeof(uint64_t));
+    hp.q_mamax_off = hp.blob.add(nullptr, (size_t)G * sizeof(uint64_t));
+  }
+  hp.q_grouped = RowLaunch{0, 0, 0, grouped_n, fp8_grid(grouped_n, hp.dt, kernel)};
+  hp.work_items = grouped_n;
+  hp.grid = hp.q_grouped.grid;
+  hp.block = 256;
+  hp.chain_launches = G;
+}
+
+static optimus_status build_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                         int32_t use_scaling, HostPlan& hp) {
+  optimus_status st = optimus_validate_quantize_fp8(d, G, dt, use_scaling);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_Q8; hp.dt = dt; hp.G = G;
+  const size_t s = dtype_size(dt);
+  std::vector<DevFp8> members;
+  std::vector<Fp8Geom> geo;
+  for (int g = 0; g < G; ++g) {
+    const optimus_fp8_quant_desc& m = d[g];
+    DevFp8 r{};
+    r.x = m.x; r.y = m.q; r.scale = use_scaling ? m.scale : nullptr;
+    r.ldx = m.ldx; r.ldy = m.ldq; r.rows = (int32_t)m.rows; r.cols = (int32_t)m.cols;
+    members.push_back(r);
+    geo.push_back(fp8_geom(m.x, m.ldx, m.q, m.ldq, m.cols, dt));
+    hp.bytes += (double)m.rows * m.cols * (double)(s + 1) + (use_scaling ? 4.0 : 0.0);
+  }
+  build_fp8(hp, members, geo, use_scaling != 0, use_scaling ? 1 : 0);
+  hp.kernel = std::string(use_scaling ? "grouped_quantize_fp8_scaled_" : "grouped_quantize_fp8_") +
+              (dt == OPTIMUS_F32 ? "f32" : "bf16");
+  return OPTIMUS_OK;
+}
+
+static optimus_status build_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
+                                           HostPlan& hp) {
+  optimus_status st = optimus_validate_dequantize_fp8(d, G, dt);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_DQ8; hp.dt = dt; hp.G = G;
+  const size_t s = dtype_size(dt);
+  std::vector<DevFp8> members;
+  std::vector<Fp8Geom> geo;
+  for (int g = 0; g < G; ++g) {
+    const optimus_fp8_dequant_desc& m = d[g];
+    DevFp8 r{};
+    r.x = m.q; r.y = m.y; r.scale = const_cast<float*>(m.scale);
+    r.ldx = m.ldq; r.ldy = m.ldy; r.rows = (int32_t)m.rows; r.cols = (int32_t)m.cols;
+    members.push_back(r);
+    geo.push_back(fp8_geom(m.y, m.ldy, m.q, m.ldq, m.cols, dt));
+    hp.bytes += (double)m.rows * m.cols * (double)(s + 1) + (m.scale ? 4.0 : 0.0);
+  }
+  build_fp8(hp, members, geo, false, 2);
+  hp.kernel = std::string("grouped_dequantize_fp8_") + (dt == OPTIMUS_F32 ? "f32" : "bf16");
+  return OPTIMUS_OK;
+}
+
 // ===================================================================== device side of a plan
 struct optimus_plan_s {
   HostPlan hp;
@@ -678,8 +917,21 @@ static const P* at(char* table, size_t off) {
   return (const P*)(table + off);
 }
 
+static hipError_t launch_fp8(const HostPlan& hp, char* table, const RowLaunch& l, hipStream_t stream) {
+  const DevFp8* descs = at<DevFp8>(table, hp.q_descs_off);
+  const Fp8Item* items = at<Fp8Item>(table, hp.q_items_off) + l.first_tile;
+  if (hp.kind == KIND_DQ8) return fp8_dequantize_launch(hp.dt, descs, items, l.num_tiles, l.grid, stream);
+  return fp8_quantize_launch(hp.dt, hp.q_scaled, descs, items, l.num_tiles, l.grid,
+                             hp.q_scaled ? (Fp8Ctl*)(table + hp.q_ctl_off) : nullptr,
+                             hp.q_scaled ? (uint64_t*)(table + hp.q_slots_off) : nullptr,
+                             hp.q_scaled ? (uint64_t*)(table + hp.q_mamax_off) : nullptr, stream);
+}
+
 static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t stream) {
   switch (hp.kind) {
+    case KIND_Q8:
+    case KIND_DQ8:
+      return launch_fp8(hp, table, hp.q_grouped, stream);
     case KIND_LINEAR:
       return gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(table, hp.g_descs_off), at<GemmTile>(table, hp.g_tiles_off),
                          hp.g_num_tiles, hp.g_grid, stream);
@@ -775,6 +1027,20 @@ extern "C" optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_d
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
+extern "C" optimus_status optimus_plan_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                                    int32_t use_scaling, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_quantize_fp8(d, G, dt, use_scaling, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
+                                                      optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_dequantize_fp8(d, G, dt, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
 
 extern "C" void optimus_plan_destroy(optimus_plan p) {
   if (!p) return;
@@ -815,7 +1081,9 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
   if (mode == OPTIMUS_EXEC_CHAIN && hp.kind != KIND_SOC) {
     for (int g = 0; g < hp.G; ++g) {
       hipError_t e;
-      if (hp.kind == KIND_LINEAR) {
+      if (hp.kind == KIND_Q8 || hp.kind == KIND_DQ8) {
+        e = launch_fp8(hp, p->table, hp.q_chain[g], st);
+      } else if (hp.kind == KIND_LINEAR) {
         const RowLaunch& c = hp.g_chain[g];
         e = gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(p->table, hp.g_descs_off),
                         at<GemmTile>(p->table, hp.g_tiles_off) + c.first_tile, c.num_tiles, c.grid, st);
@@ -958,5 +1226,17 @@ extern "C" optimus_status optimus_split_op_cat(const optimus_split_op_cat_desc* 
                                                optimus_stream_t stream) {
   HostPlan hp;
   optimus_status st = build_split_op_cat(d, dt, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                                       int32_t use_scaling, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_quantize_fp8(d, G, dt, use_scaling, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G,
+                                                         optimus_dtype dt, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_dequantize_fp8(d, G, dt, hp);
   return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
 }

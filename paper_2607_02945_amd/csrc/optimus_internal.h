@@ -126,6 +126,49 @@ hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int3
 int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces);
 int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces);
 
+// ------------------------------------------------------------------ fp8 codec
+// One member of the fp8 activation codec. Quantize: x = values of the group's
+// dtype, y = codes (one byte each); dequantize: x = codes, y = values.
+// Strides in elements of each side. With lanes > 0 the member takes the
+// 16-byte path: its item columns count chunks of 16 bytes of the wide (value)
+// side, i.e. 16 / sizeof(value) values and as many codes; otherwise
+// (lanes_scalar > 0) they count single values.
+struct DevFp8 {
+  const void* x;
+  void* y;
+  float* scale;        // quantize, scaled: written; dequantize: read, or null (1)
+  int64_t ldx, ldy;
+  int32_t rows, cols;
+  int32_t lanes;         // threads per row of the 16-byte path (power of two, 1..256), or 0
+  int32_t lanes_scalar;  // threads per row of the per-value path
+  int32_t slot0, nslots; // the member's amax partial slots (scaled quantize)
+};
+
+// One work item: rows [row0, row0 + nrows) x item columns [c0, c1) of
+// `member`. slot >= 0 marks an amax item (its partial slot); -1 a convert item.
+struct Fp8Item {
+  int32_t member, row0, nrows, c0, c1, slot;
+};
+
+// Control block of a scaled quantize launch (plan-owned, zero at upload).
+struct Fp8Ctl {
+  uint32_t ticket;  // next item to draw
+  uint32_t done;    // workgroups finished
+  uint32_t gen;     // launches completed: partial slots of this launch carry gen + 1
+  uint32_t err;     // set if a bounded wait ran out (never in a correct schedule)
+};
+// Iterations (each a short sleep) of the bounded wait for an amax slot.
+constexpr uint32_t kFp8SpinLimit = 1u << 24;
+
+hipError_t fp8_quantize_launch(optimus_dtype dt, bool scaled, const DevFp8* descs, const Fp8Item* items,
+                               int32_t num_items, int32_t grid, Fp8Ctl* ctl, uint64_t* slots, uint64_t* mamax,
+                               hipStream_t stream);
+hipError_t fp8_dequantize_launch(optimus_dtype dt, const DevFp8* descs, const Fp8Item* items, int32_t num_items,
+                                 int32_t grid, hipStream_t stream);
+// Workgroups of a codec kernel resident per CU (occupancy query); kernel:
+// 0 quantize, 1 scaled quantize, 2 dequantize.
+int fp8_blocks_per_cu(optimus_dtype dt, int kernel);
+
 int device_cu_count();
 
 }  // namespace optimus

@@ -11,7 +11,7 @@ order: shapes first, then per member in the order (W, b, gamma, beta, X).
 ``N(mu, v)`` takes v as the VARIANCE. Sizes can be scaled down (for parity
 tests) without changing the recipe.
 
-The five workload families (paper Sec. 5: DLRM-style recommendation models;
+The workload families (paper Sec. 5: DLRM-style recommendation models;
 Sec. 5.2: many small bf16 operators; Sec. 3.2: split -> LayerNorm -> act -> cat):
   tiny_group        G=8 fp32 Linear members, shared batch 512, -> LayerNorm -> tanh
   launch_bound      G=256 tiny bf16 Linear members, batch 2048, -> sigmoid
@@ -20,6 +20,8 @@ Sec. 5.2: many small bf16 operators; Sec. 3.2: split -> LayerNorm -> act -> cat)
   large_group       G=32 bf16 Linear members, batch 16384, K=1024 -> LayerNorm -> tanh
   decompose_mm      the four tall-skinny mm members of the appendix decompose_mm case
                     study ([~2e7, K] x [K, N], K, N in {(8, 8), (4, 2)}), fp32, no bias
+  act_quant         G=32 bf16 saved activations [16384, N_g] (large_group's Linear outputs)
+                    for the fp8 activation codec, per-member scale 2^U(-6, 6)
 """
 from __future__ import annotations
 
@@ -116,6 +118,18 @@ class TowersInput:
 
     @property
     def G(self): return len(self.towers)
+
+
+@dataclass
+class ActQuantInput:
+    """Saved activations handed to the fp8 activation codec."""
+    name: str
+    dtype: str
+    xs: List[torch.Tensor]                       # [M, N_g] each
+    sigmas: List[float]
+
+    @property
+    def G(self): return len(self.xs)
 
 
 # ------------------------------------------------------------------ helpers
@@ -246,6 +260,24 @@ def decompose_mm(seed: int = 0, scale: float = 1.0, dtype: str = "fp32") -> Line
     return LinearLNGroup("decompose_mm", dtype, members, "none")
 
 
+def act_quant(seed: int = 0, G: int = 32, M: int = 16384, dtype: str = "bf16") -> ActQuantInput:
+    """G activation tensors shaped like large_group's Linear outputs ([M, N_g],
+    N_g in {256, 512, 1024}): the saved activations the activation-quantization
+    rewrite stores in FP8 (paper Sec. 5, appendix Sec. 8.2). Member g ~ N(0,
+    s_g^2) with log2 s_g ~ U(-6, 6), so the per-tensor scales span four orders
+    of magnitude and, unscaled, the widest members overflow E4M3 (|x| > 464)."""
+    g = rng(seed)
+    Ns = g.choice([256, 512, 1024], size=G)
+    sig = np.exp2(g.uniform(-6.0, 6.0, size=G))
+    xs = [to_storage(g.standard_normal((M, int(N))) * float(s), dtype) for N, s in zip(Ns.tolist(), sig.tolist())]
+    return ActQuantInput("act_quant", dtype, xs, sig.tolist())
+
+
+def fp8_codes(seed: int, rows: int, cols: int) -> torch.Tensor:
+    """Uniform random bytes: every E4M3 code, NaN codes included (uint8 [rows, cols])."""
+    return torch.from_numpy(rng(seed).integers(0, 256, size=(rows, cols), dtype=np.uint8))
+
+
 WORKLOADS = {
     "tiny_group": tiny_group,
     "launch_bound": launch_bound,
@@ -253,4 +285,5 @@ WORKLOADS = {
     "towers": towers,
     "large_group": large_group,
     "decompose_mm": decompose_mm,
+    "act_quant": act_quant,
 }

@@ -17,7 +17,7 @@ pytestmark = pytest.mark.skipif(not os.path.exists(B.LIBPATH), reason="liboptimu
 
 def test_exports_match_header():
     hdr = open(os.path.join(ROOT, "include", "optimus.h")).read()
-    declared = set(re.findall(r"\b(optimus_[a-z_]+)\s*\(", hdr))
+    declared = set(re.findall(r"\b(optimus_[a-z0-9_]+)\s*\(", hdr))
     assert declared == set(B.EXPORTS)
     lib = B.lib()
     for name in declared:
@@ -176,3 +176,60 @@ def test_split_op_cat_validation():
     d, keep = soc(1 * MB, 2 * MB, [8, 8])
     d.act = 11
     assert B.optimus_validate_split_op_cat(d, B.BF16) == UNSUPPORTED
+
+
+def q8(x, q, scale=None, rows=64, cols=48, ldx=None, ldq=None):
+    return B.Fp8QuantDesc(x, ldx or cols, q, ldq or cols, scale, rows, cols)
+
+
+def dq8(q, y, scale=None, rows=64, cols=48, ldq=None, ldy=None):
+    return B.Fp8DequantDesc(q, ldq or cols, scale, y, ldy or cols, rows, cols)
+
+
+def test_fp8_codec_validation():
+    arr = lambda T, *ds: ((T * len(ds))(*ds), len(ds))
+    a, G = arr(B.Fp8QuantDesc, q8(1 * MB, 2 * MB, 3 * MB), q8(4 * MB, 5 * MB, 3 * MB + 4, rows=7, cols=5))
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 1) == OK
+    assert B.optimus_validate_quantize_fp8(a, G, B.F32, 0) == OK
+    assert B.optimus_validate_quantize_fp8(a, 0, B.BF16, 1) == OK
+    assert B.optimus_validate_quantize_fp8(a, -1, B.BF16, 1) == INVALID
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 2) == INVALID
+    assert "use_scaling" in B.optimus_last_error()
+    assert B.optimus_validate_quantize_fp8(a, G, 5, 1) == UNSUPPORTED
+    # scaled needs a scale pointer; unscaled does not
+    a, G = arr(B.Fp8QuantDesc, q8(1 * MB, 2 * MB))
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 1) == INVALID
+    assert "scale" in B.optimus_last_error()
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 0) == OK
+    for bad in [q8(0, 2 * MB), q8(1 * MB, 0), q8(1 * MB, 2 * MB, rows=0), q8(1 * MB, 2 * MB, cols=0),
+                q8(1 * MB, 2 * MB, ldx=47), q8(1 * MB, 2 * MB, ldq=40), q8(1 * MB, 2 * MB, rows=1 << 31)]:
+        a, G = arr(B.Fp8QuantDesc, bad)
+        assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 0) == INVALID, bad
+    # codes over the values (bf16 values take 2 bytes each: 64 x 48 x 2 = 6 KiB)
+    a, G = arr(B.Fp8QuantDesc, q8(1 * MB, 1 * MB + 4096))
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 0) == ALIASING
+    a, G = arr(B.Fp8QuantDesc, q8(1 * MB, 1 * MB + 6144))
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 0) == OK
+    # no in-place, even at equal pointers and strides
+    a, G = arr(B.Fp8QuantDesc, q8(1 * MB, 1 * MB))
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 0) == ALIASING
+    # two members writing one scale, or a scale inside a member's codes
+    a, G = arr(B.Fp8QuantDesc, q8(1 * MB, 2 * MB, 3 * MB), q8(4 * MB, 5 * MB, 3 * MB))
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 1) == ALIASING
+    a, G = arr(B.Fp8QuantDesc, q8(1 * MB, 2 * MB, 2 * MB + 100))
+    assert B.optimus_validate_quantize_fp8(a, G, B.BF16, 1) == ALIASING
+
+    a, G = arr(B.Fp8DequantDesc, dq8(1 * MB, 2 * MB, 3 * MB), dq8(4 * MB, 5 * MB))
+    assert B.optimus_validate_dequantize_fp8(a, G, B.BF16) == OK
+    assert B.optimus_validate_dequantize_fp8(a, G, 9) == UNSUPPORTED
+    # members may share one read-only scale
+    a, G = arr(B.Fp8DequantDesc, dq8(1 * MB, 2 * MB, 3 * MB), dq8(4 * MB, 5 * MB, 3 * MB))
+    assert B.optimus_validate_dequantize_fp8(a, G, B.F32) == OK
+    for bad in [dq8(0, 2 * MB), dq8(1 * MB, 0), dq8(1 * MB, 2 * MB, cols=-3), dq8(1 * MB, 2 * MB, ldy=47)]:
+        a, G = arr(B.Fp8DequantDesc, bad)
+        assert B.optimus_validate_dequantize_fp8(a, G, B.BF16) == INVALID, bad
+    # the output over another member's codes, or over the scale
+    a, G = arr(B.Fp8DequantDesc, dq8(1 * MB, 2 * MB), dq8(2 * MB + 512, 5 * MB))
+    assert B.optimus_validate_dequantize_fp8(a, G, B.BF16) == ALIASING
+    a, G = arr(B.Fp8DequantDesc, dq8(1 * MB, 2 * MB, 2 * MB + 8))
+    assert B.optimus_validate_dequantize_fp8(a, G, B.BF16) == ALIASING
