@@ -19,7 +19,8 @@ on the current kernel sources.
 
 Workloads (the seeded groups of paper_2607_02945_amd.synth): launch_bound
 (default; G=256 bf16 Linear + sigmoid, B=2048), tiny_group, split_op_cat,
-towers, large_group.
+towers, large_group, decompose_mm, act_quant (fp8 quantize of 32 saved
+activations, then dequantize).
 """
 from __future__ import annotations
 
@@ -50,7 +51,8 @@ def parse():
                     help="untimed steps before timing (default: at least 20 and at least 0.3 s of work, "
                          "so that the clocks have settled)")
     ap.add_argument("--workload", default="launch_bound",
-                    choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group", "decompose_mm"])
+                    choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group", "decompose_mm",
+                             "act_quant"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-chain", action="store_true", help="skip timing the per-op launch chain")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -77,6 +79,7 @@ class OpGroup:
         self.chain = []        # list of (plan, mode)
         self.horizontal = []   # split-op-cat only: horizontal fusion without the vertical rewrite
         self.tiled = []        # decompose_mm only: the group through the tiled GEMM kernel
+        self.unscaled = []     # act_quant only: quantize without the per-tensor scale
 
     def run(self, which, stream=None):
         for plan, mode in getattr(self, which):
@@ -142,6 +145,20 @@ def build_copy(name, wl, torch, B):
         og.chain = [(soc, "chain")]
         og.horizontal = [(soc, "horizontal")]
         og.keep = (x, y, gs, bs)
+    elif name == "act_quant":
+        # forward: the saved activations to E4M3 codes with per-tensor scales;
+        # backward: the codes back to bf16 before use
+        xs = [cu(x) for x in wl.xs]
+        qs = [torch.empty(x.shape, dtype=torch.uint8, device="cuda") for x in xs]
+        sc = [torch.ones(1, dtype=torch.float32, device="cuda") for _ in xs]
+        ys = [torch.empty_like(x) for x in xs]
+        quant = B.optimus_plan_quantize_fp8(xs, qs, sc, True)
+        dequant = B.optimus_plan_dequantize_fp8(qs, sc, ys)
+        og.grouped = [(quant, "grouped"), (dequant, "grouped")]
+        og.chain = [(quant, "chain"), (dequant, "chain")]
+        qs_u = [torch.empty_like(q) for q in qs]
+        og.unscaled = [(B.optimus_plan_quantize_fp8(xs, qs_u, None, False), "grouped")]
+        og.keep = (xs, qs, sc, ys, qs_u)
     elif name == "towers":
         T = wl.towers
         xs = [cu(t.x) for t in T]
@@ -170,6 +187,8 @@ def workload_bytes(name, wl):
         return 2 * wl.x.numel() * 2
     if name == "towers":
         return sum(t.x.numel() * 2 + (512 + 256 + 256) * t.x.shape[0] * 2 for t in wl.towers)
+    if name == "act_quant":
+        return sum(x.numel() * (2 + 1 + 2 + 1) for x in wl.xs)
     s = 4 if wl.dtype == "fp32" else 2
     return sum((m.x.numel() + m.w.numel() + 2 * m.M * m.N) * s for m in wl.members)
 
@@ -181,6 +200,9 @@ def describe(name, wl):
     if name == "towers":
         return {"workload": name, "towers": wl.G, "batch": wl.towers[0].x.shape[0],
                 "layers": "Linear(in_g->512)+relu, Linear(512->256), LayerNorm", "seed": 0}
+    if name == "act_quant":
+        return {"workload": name, "G": wl.G, "batch": wl.xs[0].shape[0], "N": sorted({x.shape[1] for x in wl.xs}),
+                "codec": "bf16 -> OCP E4M3 with per-tensor amax scale -> bf16", "seed": 0}
     if name == "decompose_mm":
         return {"workload": name, "G": wl.G, "M": [m.M for m in wl.members], "K": [m.K for m in wl.members],
                 "N": [m.N for m in wl.members], "bias": False, "seed": 0}
@@ -204,6 +226,16 @@ def cpu_baseline(name, wl, target_s):
         gs, bs = [e(g) for g in wl.gammas], [e(b) for b in wl.betas]
         frac, sample = rows / wl.x.shape[0], f"first {rows} of {wl.x.shape[0]} rows"
         work = lambda: orc.split_op_cat(xs, wl.widths, gs, bs, True, wl.eps, wl.act)
+    elif name == "act_quant":
+        rows = 1024
+        ins = [e(x[:rows]) for x in wl.xs]
+        frac = rows / wl.xs[0].shape[0]
+        sample = f"first {rows} of {wl.xs[0].shape[0]} rows of every member (scale from the sample)"
+
+        def work():
+            for x in ins:
+                q, sc = orc.quantize_fp8(x, True)
+                orc.dequantize_fp8(q, sc)
     elif name == "towers":
         rows = 64
         ins = [(e(t.x[:rows]), e(t.w1), e(t.b1), e(t.w2), e(t.b2), e(t.gamma), e(t.beta)) for t in wl.towers]
@@ -316,7 +348,10 @@ def copy_probe():
 
 def kernel_symbol(label):
     """Symbol name of the kernel behind a plan's kernel label."""
-    for prefix, sym in (("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
+    for prefix, sym in (("grouped_quantize_fp8_scaled", "grouped_quantize_fp8_scaled_kernel"),
+                        ("grouped_quantize_fp8", "grouped_quantize_fp8_kernel"),
+                        ("grouped_dequantize_fp8", "grouped_dequantize_fp8_kernel"),
+                        ("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
                         ("grouped_gemm", "grouped_gemm_kernel"), ("split_op_cat_fused", "split_op_cat_kernel"),
                         ("grouped_layernorm", "grouped_layernorm_kernel"), ("grouped_pointwise", "grouped_pointwise_kernel")):
         if label.startswith(prefix):
@@ -330,6 +365,8 @@ KERNEL_SOURCES = {
     "grouped_gemm_kernel": "kernels_gemm.hip", "grouped_gemm_dma_kernel": "kernels_gemm.hip",
     "grouped_gemm_skinny_kernel": "kernels_gemm.hip", "split_op_cat_kernel": "kernels_rowwise.hip",
     "grouped_layernorm_kernel": "kernels_rowwise.hip", "grouped_pointwise_kernel": "kernels_rowwise.hip",
+    "grouped_quantize_fp8_scaled_kernel": "kernels_fp8.hip", "grouped_quantize_fp8_kernel": "kernels_fp8.hip",
+    "grouped_dequantize_fp8_kernel": "kernels_fp8.hip",
 }
 
 
@@ -484,6 +521,13 @@ def main():
         t_step = t_ms / tsteps
         out["tiled_gemm"] = {"us_per_group": round(t_step * 1000.0, 3), "kernel": ogs[0].tiled[0][0].info()["kernel"],
                              "speedup": round(t_step / ms_step, 2)}
+    if ogs[0].unscaled:
+        usteps = max(5, min(args.steps, 50))
+        u_ms, _ = timed("unscaled", usteps, 5)
+        pinfo = ogs[0].unscaled[0][0].info()
+        entry = roofline(pinfo, u_ms / usteps)
+        entry.update({"kernel": pinfo["kernel"], "kernel_us": round(u_ms / usteps * 1000.0, 3)})
+        out["unscaled_quantize"] = entry
     if ogs[0].horizontal:
         hsteps = max(5, min(args.steps, 50))
         h_ms, _ = timed("horizontal", hsteps, 2)

@@ -226,8 +226,9 @@ optimus_status optimus_split_op_cat(const optimus_split_op_cat_desc* d, optimus_
  *     code -- the overflow the paper warns about when scaling is disabled.
  * Rounding is to nearest, ties to even; a NaN value gives S.1111.111 with
  * the sign of x. use_scaling other than 0/1 -> INVALID_ARG; scaled members
- * need a non-NULL scale. The scaled form is one launch: per-member amax
- * partials are combined inside the kernel (see optimus_plan_quantize_fp8). */
+ * need a non-NULL scale. Unscaled is one launch; scaled is two for the whole
+ * group: an amax pass that writes one partial per tile into plan-owned
+ * memory, then the conversion, which reads its member's partials. */
 optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
                                             int32_t use_scaling, optimus_stream_t stream);
 
@@ -256,12 +257,10 @@ optimus_status optimus_plan_pointwise(const optimus_pointwise_desc* d, int32_t G
                                       optimus_act op, optimus_plan* out);
 optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
                                          optimus_plan* out);
-/* A scaled quantize plan also owns a small control block (ticket and done
- * counters, a launch generation) and one 8-byte amax partial per amax tile
- * per member; the kernel resets the counters when it finishes, so the plan
- * can be executed again. Executions of one quantize plan must not overlap
- * (use one stream, or order them with events); one-shot calls each get
- * their own control block. */
+/* A scaled quantize plan also owns the 4-byte amax partials of its members
+ * (about 256 per member at most), written by its first launch and read by
+ * its second: executions of one scaled plan must not overlap (use one
+ * stream, or order them with events); one-shot calls each get their own. */
 optimus_status optimus_plan_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
                                          int32_t use_scaling, optimus_plan* out);
 optimus_status optimus_plan_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
@@ -299,7 +298,7 @@ typedef struct {
   int32_t kind;            /* 0 linear, 1 layernorm, 2 pointwise, 3 split_op_cat, 4 linear_layernorm,
                               5 quantize_fp8, 6 dequantize_fp8 */
   int32_t group_size;      /* G, or n_slices */
-  int32_t launches;        /* kernel launches per GROUPED execute (1) */
+  int32_t launches;        /* kernel launches per GROUPED execute (1; 2 for a scaled quantize) */
   int32_t chain_launches;  /* kernel launches per CHAIN execute */
   int64_t work_items;      /* GEMM tiles / row tiles of the grouped launch */
   int32_t grid;            /* workgroups of the grouped launch */

@@ -14,25 +14,18 @@
 // overflow tie 464 goes to 448, larger magnitudes and infinities to the NaN
 // code) and v_cvt_pk_f32_fp8 (exact).
 //
-// Scaled quantize is ONE launch per group. Its work list holds two kinds of
-// items, in an order fixed by the planner:
-//   amax items    a large tile of one member: the tile's max |x| goes into
-//                 the member's partial slot for that tile
-//   convert items a smaller tile: read the member's amax (all of its partial
-//                 slots), convert, store the codes
-// Workgroups draw items from a global ticket counter in list order, and a
-// member's convert items come after all of its amax items, so a convert item
-// waits only on amax items that were drawn before it and that are held by
-// running workgroups which never wait themselves: the waits always end, at
-// any grid size and residency. The planner places a member's convert items
-// about one grid of items after its last amax item, so they find the slots
-// written and re-read the tile while it is still in the memory-side cache.
-//
-// Every partial slot is written once per launch by one atomic store of
-// (generation << 32 | nan flag << 31 | amax bits); a reader checks the
-// generation, so the slots are never cleared. The control block (ticket,
-// done count, generation) is reset by the last workgroup to finish, so a plan
-// can be executed again (executions of one plan must be stream-ordered).
+// Scaled quantize is two launches per group, whatever G is:
+//   amax     every member in tiles of at most 1/256 of it (and at least
+//            128 KB): each tile's max |x| (and whether it holds a NaN) goes to
+//            the tile's own slot -- one writer per slot, no atomics
+//   convert  tiles of 32 KB: a tile reduces its member's slots (a few hundred
+//            bytes, cached), derives scale and inv, converts and stores; it
+//            walks the group in reverse order, so that the tiles the amax
+//            pass read last -- still in the memory-side cache -- come first
+// A single launch would need workgroups to wait for other workgroups' amax
+// tiles; handing work out through a global counter, the one schedule whose
+// waits provably end, costs a same-address device atomic per tile, and those
+// serialize at about 12 ns each on this GPU -- more than the second pass.
 #include <type_traits>
 
 #include "device_common.h"
@@ -41,20 +34,6 @@ namespace optimus {
 
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-
-// ------------------------------------------------------------------ atomics
-__device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t ld_agent(const uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_agent(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Block barrier that orders LDS only: global loads in flight stay in flight.
 __device__ __forceinline__ void lds_barrier() {
@@ -96,7 +75,10 @@ __device__ __forceinline__ uint32_t encode1(float v, uint32_t xbits) {
 // row's chunks are strided by 256. Chunks are visited U at a time so that U
 // loads per lane are in flight; `body(r, c, ok)` gets U (row, chunk) pairs.
 constexpr int kFp8Threads = 256;
-constexpr int kFp8U = 4;
+#ifndef OPTIMUS_FP8_U
+#define OPTIMUS_FP8_U 4
+#endif
+constexpr int kFp8U = OPTIMUS_FP8_U;
 
 template <int U, class Body>
 __device__ __forceinline__ void walk_tile(const Fp8Item& it, int L, int tid, Body&& body) {
@@ -307,7 +289,7 @@ __device__ __forceinline__ void tile_convert(const DevFp8& d, const Fp8Item& it,
 }
 
 // ------------------------------------------------------------------ quantize kernels
-// Unscaled: every item converts; a grid-stride loop over the items.
+// Unscaled: every item converts.
 template <typename T>
 __global__ __launch_bounds__(kFp8Threads) void grouped_quantize_fp8_kernel(const DevFp8* __restrict__ descs,
                                                                            const Fp8Item* __restrict__ items,
@@ -319,105 +301,66 @@ __global__ __launch_bounds__(kFp8Threads) void grouped_quantize_fp8_kernel(const
   }
 }
 
-// Member amax from its partial slots (wave 0 of the block), cached in the
-// member's word once known. Returns (nan flag << 31 | amax bits).
-__device__ __forceinline__ uint32_t member_amax(const DevFp8& d, int member, uint64_t* slots, uint64_t* mamax,
-                                                uint32_t tag, Fp8Ctl* ctl, int lane) {
-  const uint64_t cached = ld_agent(&mamax[member]);
-  if ((uint32_t)(cached >> 32) == tag) return (uint32_t)cached;
-  uint32_t m = 0, nan = 0;
-  for (int i = lane; i < d.nslots; i += 64) {
-    uint64_t v = ld_agent(&slots[d.slot0 + i]);
-    // Bounded wait: the slot's amax item was drawn before this item and its
-    // workgroup never waits, so the slot is written within microseconds; the
-    // bound only keeps a broken schedule from hanging the device.
-    for (uint32_t spin = 0; (uint32_t)(v >> 32) != tag; ++spin) {
-      if (spin >= kFp8SpinLimit) {
-        st_agent(&ctl->err, 1u);
-        break;
+// Scaled, first launch: per amax tile, (nan flag << 31 | max |x| bits) into
+// slots[it.slot].
+template <typename T>
+__global__ __launch_bounds__(kFp8Threads) void grouped_fp8_amax_kernel(const DevFp8* __restrict__ descs,
+                                                                       const Fp8Item* __restrict__ items,
+                                                                       int32_t num_items, uint32_t* __restrict__ slots) {
+  __shared__ uint32_t s_red[kFp8Threads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int t = blockIdx.x; t < num_items; t += gridDim.x) {
+    const Fp8Item it = items[t];
+    bool nan;
+    const uint32_t m = tile_amax<T>(descs[it.member], it, tid, &nan);
+    const uint32_t wm = wave_max_u32(m) | (wave_max_u32(nan ? 1u : 0u) << 31);
+    if (lane == 0) s_red[wave] = wm;
+    lds_barrier();
+    if (tid == 0) {
+      uint32_t a = 0, n = 0;
+#pragma unroll
+      for (int w = 0; w < kFp8Threads / 64; ++w) {
+        a = max(a, s_red[w] & 0x7FFFFFFFu);
+        n |= s_red[w] & 0x80000000u;
       }
-      __builtin_amdgcn_s_sleep(2);
-      v = ld_agent(&slots[d.slot0 + i]);
+      slots[it.slot] = n | a;
     }
-    m = max(m, (uint32_t)v & 0x7FFFFFFFu);
-    nan |= (uint32_t)v & 0x80000000u;
+    lds_barrier();  // s_red is reused by the next item
   }
-  const uint32_t r = wave_max_u32(m) | wave_max_u32(nan);
-  if (lane == 0) st_agent(&mamax[member], ((uint64_t)tag << 32) | r);
-  return r;
 }
 
+// Scaled, second launch: every wave reduces the member's slots itself (no
+// block barrier), then the tile is converted; the member's first tile also
+// writes the scale.
 template <typename T>
 __global__ __launch_bounds__(kFp8Threads) void grouped_quantize_fp8_scaled_kernel(
-    const DevFp8* __restrict__ descs, const Fp8Item* __restrict__ items, int32_t num_items, Fp8Ctl* ctl,
-    uint64_t* slots, uint64_t* mamax) {
-  __shared__ int32_t s_ticket;
-  __shared__ uint32_t s_gen, s_red[kFp8Threads / 64], s_amax;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) {
-    s_gen = ld_agent(&ctl->gen);
-    s_ticket = (int32_t)__hip_atomic_fetch_add(&ctl->ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  lds_barrier();
-  const uint32_t tag = s_gen + 1u;
-  int t = s_ticket;
-  while (t < num_items) {
-    int32_t next = 0;
-    if (tid == 0)  // the next ticket is drawn while this item runs
-      next = (int32_t)__hip_atomic_fetch_add(&ctl->ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const DevFp8* __restrict__ descs, const Fp8Item* __restrict__ items, int32_t num_items,
+    const uint32_t* __restrict__ slots) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  for (int t = blockIdx.x; t < num_items; t += gridDim.x) {
     const Fp8Item it = items[t];
     const DevFp8 d = descs[it.member];
-    if (it.slot >= 0) {
-      bool nan;
-      const uint32_t m = tile_amax<T>(d, it, tid, &nan);
-      const uint32_t wm = wave_max_u32(m) | (wave_max_u32(nan ? 1u : 0u) << 31);
-      if (lane == 0) s_red[wave] = wm;
-      lds_barrier();
-      if (tid == 0) {
-        uint32_t a = 0, n = 0;
-#pragma unroll
-        for (int w = 0; w < kFp8Threads / 64; ++w) {
-          a = max(a, s_red[w] & 0x7FFFFFFFu);
-          n |= s_red[w] & 0x80000000u;
-        }
-        st_agent(&slots[it.slot], ((uint64_t)tag << 32) | n | a);
-      }
-    } else {
-      if (wave == 0) {
-        const uint32_t r = member_amax(d, it.member, slots, mamax, tag, ctl, lane);
-        if (lane == 0) s_amax = r;
-      }
-      lds_barrier();
-      const uint32_t r = s_amax;
-      const float amax = __builtin_bit_cast(float, r & 0x7FFFFFFFu);
-      float scale = 1.0f, inv = 1.0f;
-      if (amax > 0.0f) {
-        scale = amax / 448.0f;
-        inv = 448.0f / amax;
-      }
-      if (tid == 0 && it.row0 == 0 && it.c0 == 0) ((OPTIMUS_GLOBAL float*)d.scale)[0] = scale;
-      // The fast path needs every x * inv finite and within 464: no NaN in
-      // the member, amax finite, and inv finite (a tiny amax overflows it).
-      if ((r & 0x80000000u) || !(amax < __builtin_inff()) || !(inv < __builtin_inff()))
-        tile_convert<T, 2>(d, it, tid, inv);
-      else
-        tile_convert<T, 1>(d, it, tid, inv);
+    uint32_t m = 0, nan = 0;
+    for (int i = lane; i < d.nslots; i += 64) {
+      const uint32_t v = slots[d.slot0 + i];
+      m = max(m, v & 0x7FFFFFFFu);
+      nan |= v & 0x80000000u;
     }
-    lds_barrier();  // every thread is done with s_red / s_amax / s_ticket
-    if (tid == 0) s_ticket = next;
-    lds_barrier();
-    t = s_ticket;
-  }
-  if (tid == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(&ctl->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == gridDim.x - 1) {
-      // The last workgroup: every other one has drawn its final ticket and
-      // finished its items, so the control block can be reset for the next
-      // launch.
-      st_agent(&ctl->ticket, 0u);
-      st_agent(&ctl->done, 0u);
-      st_agent(&ctl->gen, tag);
+    m = wave_max_u32(m);
+    nan = wave_max_u32(nan);
+    const float amax = __builtin_bit_cast(float, m);
+    float scale = 1.0f, inv = 1.0f;
+    if (amax > 0.0f) {
+      scale = amax / 448.0f;
+      inv = 448.0f / amax;
     }
+    if (tid == 0 && it.row0 == 0 && it.c0 == 0) ((OPTIMUS_GLOBAL float*)d.scale)[0] = scale;
+    // The fast path needs every x * inv finite and within 464: no NaN in the
+    // member, amax finite, and inv finite (a tiny amax overflows it).
+    if (nan || !(amax < __builtin_inff()) || !(inv < __builtin_inff()))
+      tile_convert<T, 2>(d, it, tid, inv);
+    else
+      tile_convert<T, 1>(d, it, tid, inv);
   }
 }
 
@@ -476,17 +419,28 @@ __global__ __launch_bounds__(kFp8Threads) void grouped_dequantize_fp8_kernel(con
 }
 
 // ------------------------------------------------------------------ launchers
-hipError_t fp8_quantize_launch(optimus_dtype dt, bool scaled, const DevFp8* descs, const Fp8Item* items,
-                               int32_t num_items, int32_t grid, Fp8Ctl* ctl, uint64_t* slots, uint64_t* mamax,
-                               hipStream_t stream) {
+hipError_t fp8_amax_launch(optimus_dtype dt, const DevFp8* descs, const Fp8Item* items, int32_t num_items,
+                           int32_t grid, uint32_t* slots, hipStream_t stream) {
   if (num_items <= 0) return hipSuccess;
-  if (scaled) {
+  if (dt == OPTIMUS_BF16)
+    hipLaunchKernelGGL(grouped_fp8_amax_kernel<bf16_t>, dim3(grid), dim3(kFp8Threads), 0, stream, descs, items,
+                       num_items, slots);
+  else
+    hipLaunchKernelGGL(grouped_fp8_amax_kernel<float>, dim3(grid), dim3(kFp8Threads), 0, stream, descs, items,
+                       num_items, slots);
+  return hipGetLastError();
+}
+
+hipError_t fp8_quantize_launch(optimus_dtype dt, const DevFp8* descs, const Fp8Item* items, int32_t num_items,
+                               int32_t grid, const uint32_t* slots, hipStream_t stream) {
+  if (num_items <= 0) return hipSuccess;
+  if (slots) {
     if (dt == OPTIMUS_BF16)
       hipLaunchKernelGGL(grouped_quantize_fp8_scaled_kernel<bf16_t>, dim3(grid), dim3(kFp8Threads), 0, stream, descs,
-                         items, num_items, ctl, slots, mamax);
+                         items, num_items, slots);
     else
       hipLaunchKernelGGL(grouped_quantize_fp8_scaled_kernel<float>, dim3(grid), dim3(kFp8Threads), 0, stream, descs,
-                         items, num_items, ctl, slots, mamax);
+                         items, num_items, slots);
   } else {
     if (dt == OPTIMUS_BF16)
       hipLaunchKernelGGL(grouped_quantize_fp8_kernel<bf16_t>, dim3(grid), dim3(kFp8Threads), 0, stream, descs, items,
@@ -516,6 +470,8 @@ int fp8_blocks_per_cu(optimus_dtype dt, int kernel) {
                                      : (const void*)grouped_quantize_fp8_scaled_kernel<float>)
                   : kernel == 0 ? (b ? (const void*)grouped_quantize_fp8_kernel<bf16_t>
                                      : (const void*)grouped_quantize_fp8_kernel<float>)
+                  : kernel == 3 ? (b ? (const void*)grouped_fp8_amax_kernel<bf16_t>
+                                     : (const void*)grouped_fp8_amax_kernel<float>)
                                 : (b ? (const void*)grouped_dequantize_fp8_kernel<bf16_t>
                                      : (const void*)grouped_dequantize_fp8_kernel<float>);
   int n = 0;

@@ -372,13 +372,12 @@ struct HostPlan {
   std::vector<int32_t> soc_piece_first, soc_piece_count;  // per piece: tile range in soc_tiles
   int32_t soc_piece_tiles_total = 0;
   std::vector<size_t> soc_temp_fixups;  // blob offsets of DevRows pointers relative to the temp base
-  // fp8 codec: member table, item list (the grouped list, then per member
-  // the items of its CHAIN launch), and for scaled quantize the control
-  // block, amax partial slots and per-member amax words
+  // fp8 codec: member table, item lists (grouped launches, then per member
+  // the items of its CHAIN launches), and for scaled quantize the amax slots
   bool q_scaled = false;
-  size_t q_descs_off = 0, q_items_off = 0, q_ctl_off = 0, q_slots_off = 0, q_mamax_off = 0;
-  RowLaunch q_grouped{};
-  std::vector<RowLaunch> q_chain;
+  size_t q_descs_off = 0, q_items_off = 0, q_slots_off = 0;
+  RowLaunch q_grouped{}, q_amax{};                    // q_amax: scaled quantize only
+  std::vector<RowLaunch> q_chain, q_chain_amax;
   // measurement
   int32_t launches = 1, chain_launches = 0, grid = 0, block = 0;
   int64_t work_items = 0;
@@ -719,17 +718,15 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
 
 // ===================================================================== fp8 codec plans
 // Value-side bytes of a convert / dequantize item; an amax item covers
-// OPTIMUS_FP8_AMAX_TILES of them; a member's convert items start
-// OPTIMUS_FP8_LAG_PCT percent of a grid of items after its last amax item.
+// OPTIMUS_FP8_AMAX_TILES of them, or 1/kFp8MaxSlots of its member if that is
+// more, so a convert item reduces at most about kFp8MaxSlots slots.
 #ifndef OPTIMUS_FP8_TILE_BYTES
 #define OPTIMUS_FP8_TILE_BYTES 32768
 #endif
 #ifndef OPTIMUS_FP8_AMAX_TILES
 #define OPTIMUS_FP8_AMAX_TILES 4
 #endif
-#ifndef OPTIMUS_FP8_LAG_PCT
-#define OPTIMUS_FP8_LAG_PCT 100
-#endif
+static constexpr int64_t kFp8MaxSlots = 256;
 
 // Item geometry of one member: the 16-byte path needs value rows made of
 // 16-byte chunks (16-byte aligned) and code rows of as many bytes (aligned
@@ -738,9 +735,14 @@ struct Fp8Geom {
   bool vec;
   int64_t units;       // units per row
   int64_t unit_bytes;  // value-side bytes of a unit
-  int64_t seg;         // widest row segment of a convert item, in units
   int lanes;           // threads per row
 };
+
+// Widest row segment of an item of about `budget` value bytes, in units (a
+// multiple of the 256 threads of a block).
+static int64_t fp8_seg(const Fp8Geom& g, int64_t budget) {
+  return std::max<int64_t>(256, (budget / g.unit_bytes) / 256 * 256);
+}
 
 static Fp8Geom fp8_geom(const void* vals, int64_t ldv, const void* codes, int64_t ldc, int64_t cols, optimus_dtype dt) {
   const int64_t s = (int64_t)dtype_size(dt), VEC = 16 / s;
@@ -748,17 +750,19 @@ static Fp8Geom fp8_geom(const void* vals, int64_t ldv, const void* codes, int64_
   g.vec = cols % VEC == 0 && ldv % VEC == 0 && ldc % VEC == 0 && aligned16(vals) && ((uintptr_t)codes % VEC) == 0;
   g.units = g.vec ? cols / VEC : cols;
   g.unit_bytes = g.vec ? 16 : s;
-  g.seg = std::max<int64_t>(256, (OPTIMUS_FP8_TILE_BYTES / g.unit_bytes) / 256 * 256);
-  g.lanes = std::min(256, pow2ceil((int)std::min<int64_t>(g.units, g.seg)));
+  g.lanes = std::min(256, pow2ceil((int)std::min<int64_t>(g.units, fp8_seg(g, OPTIMUS_FP8_TILE_BYTES))));
   return g;
 }
 
-// Items covering one member: whole-row tiles of about `budget` value bytes
-// when a row fits in `seg` units, else single-row segments of `seg` units.
-// slot >= 0: amax items, numbered from `slot`.
-static void fp8_items(const Fp8Geom& g, int member, int64_t rows, int64_t budget, int64_t seg, int32_t slot,
+// Items covering one member with tiles of about `budget` value bytes: whole
+// rows (a multiple of the block's row slots) when a row fits, else
+// single-row segments. slot >= 0: amax items, slots numbered from `slot`.
+// Every item is at least as wide as the member's lanes cover or is a whole
+// row, so the block walk of the kernels fits any of them.
+static void fp8_items(const Fp8Geom& g, int member, int64_t rows, int64_t budget, int32_t slot,
                       std::vector<Fp8Item>& out) {
   const int64_t row_bytes = g.units * g.unit_bytes;
+  const int64_t seg = fp8_seg(g, budget);
   if (g.units <= seg) {
     const int64_t rpb = 256 / g.lanes;
     int64_t per = std::max<int64_t>(1, budget / row_bytes);
@@ -779,8 +783,10 @@ static int32_t fp8_grid(int64_t items, optimus_dtype dt, int kernel) {
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(items, cap));
 }
 
-// Shared by quantize and dequantize: the member table, the grouped item list
-// and the per-member CHAIN lists. `scaled` adds amax items, interleaved.
+// Shared by quantize and dequantize: the member table and item lists.
+// Grouped: (scaled: the amax items, member order, then) the convert items --
+// in reverse order when scaled, so the data the amax launch read last is
+// converted first. CHAIN: per member, its own items.
 static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vector<Fp8Geom>& geo, bool scaled,
                       int kernel) {
   const int G = (int)members.size();
@@ -790,61 +796,45 @@ static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vec
     DevFp8& m = members[g];
     m.lanes = geo[g].vec ? geo[g].lanes : 0;
     m.lanes_scalar = geo[g].vec ? 0 : geo[g].lanes;
-    fp8_items(geo[g], g, m.rows, OPTIMUS_FP8_TILE_BYTES, geo[g].seg, -1, conv[g]);
+    fp8_items(geo[g], g, m.rows, OPTIMUS_FP8_TILE_BYTES, -1, conv[g]);
     if (scaled) {
+      const int64_t bytes = (int64_t)m.rows * geo[g].units * geo[g].unit_bytes;
+      const int64_t budget = std::max<int64_t>((int64_t)OPTIMUS_FP8_TILE_BYTES * OPTIMUS_FP8_AMAX_TILES,
+                                               (bytes + kFp8MaxSlots - 1) / kFp8MaxSlots);
       m.slot0 = nslots;
-      fp8_items(geo[g], g, m.rows, (int64_t)OPTIMUS_FP8_TILE_BYTES * OPTIMUS_FP8_AMAX_TILES,
-                geo[g].seg * OPTIMUS_FP8_AMAX_TILES, nslots, amax[g]);
+      fp8_items(geo[g], g, m.rows, budget, nslots, amax[g]);
       m.nslots = (int32_t)amax[g].size();
       nslots += m.nslots;
+      std::reverse(conv[g].begin(), conv[g].end());
     }
   }
   std::vector<Fp8Item> items;
-  if (!scaled) {
-    for (int g = 0; g < G; ++g) items.insert(items.end(), conv[g].begin(), conv[g].end());
-  } else {
-    int64_t total = 0;
-    for (int g = 0; g < G; ++g) total += (int64_t)conv[g].size() + (int64_t)amax[g].size();
-    const int64_t lag = (int64_t)fp8_grid(total, hp.dt, kernel) * OPTIMUS_FP8_LAG_PCT / 100;
-    // A member's convert items follow its last amax item by `lag` items (or
-    // come at the end): every convert item comes after all amax items of its
-    // member, which is what makes the in-kernel waits finite.
-    std::vector<int64_t> a_end(G, 0);
-    int next = 0;
-    for (int g = 0; g < G; ++g) {
-      for (const Fp8Item& it : amax[g]) {
-        items.push_back(it);
-        while (next < g && (int64_t)items.size() >= a_end[next] + lag) {
-          items.insert(items.end(), conv[next].begin(), conv[next].end());
-          ++next;
-        }
-      }
-      a_end[g] = (int64_t)items.size();
-    }
-    for (; next < G; ++next) items.insert(items.end(), conv[next].begin(), conv[next].end());
-  }
-  const int32_t grouped_n = (int32_t)items.size();
-  hp.q_chain.clear();
-  for (int g = 0; g < G; ++g) {
+  auto add = [&](const std::vector<Fp8Item>& v, int kern) {
     const int32_t first = (int32_t)items.size();
-    items.insert(items.end(), amax[g].begin(), amax[g].end());
-    items.insert(items.end(), conv[g].begin(), conv[g].end());
-    const int32_t n = (int32_t)items.size() - first;
-    hp.q_chain.push_back(RowLaunch{0, 0, first, n, fp8_grid(n, hp.dt, kernel)});
+    items.insert(items.end(), v.begin(), v.end());
+    return RowLaunch{0, 0, first, (int32_t)v.size(), fp8_grid((int64_t)v.size(), hp.dt, kern)};
+  };
+  std::vector<Fp8Item> all_a, all_c;
+  for (int g = 0; g < G; ++g) all_a.insert(all_a.end(), amax[g].begin(), amax[g].end());
+  for (int g = scaled ? G - 1 : 0; scaled ? g >= 0 : g < G; g += scaled ? -1 : 1)
+    all_c.insert(all_c.end(), conv[g].begin(), conv[g].end());
+  hp.q_amax = scaled ? add(all_a, 3) : RowLaunch{};
+  hp.q_grouped = add(all_c, kernel);
+  hp.q_chain.clear();
+  hp.q_chain_amax.clear();
+  for (int g = 0; g < G; ++g) {
+    if (scaled) hp.q_chain_amax.push_back(add(amax[g], 3));
+    hp.q_chain.push_back(add(conv[g], kernel));
   }
   hp.q_scaled = scaled;
   hp.q_descs_off = hp.blob.add(members.data(), members.size() * sizeof(DevFp8));
   hp.q_items_off = hp.blob.add(items.data(), items.size() * sizeof(Fp8Item));
-  if (scaled) {
-    hp.q_ctl_off = hp.blob.add(nullptr, sizeof(Fp8Ctl));
-    hp.q_slots_off = hp.blob.add(nullptr, (size_t)std::max(nslots, 1) * sizeof(uint64_t));
-    hp.q_mamax_off = hp.blob.add(nullptr, (size_t)G * sizeof(uint64_t));
-  }
-  hp.q_grouped = RowLaunch{0, 0, 0, grouped_n, fp8_grid(grouped_n, hp.dt, kernel)};
-  hp.work_items = grouped_n;
+  if (scaled) hp.q_slots_off = hp.blob.add(nullptr, (size_t)std::max(nslots, 1) * sizeof(uint32_t));
+  hp.work_items = (int64_t)all_a.size() + (int64_t)all_c.size();
   hp.grid = hp.q_grouped.grid;
   hp.block = 256;
-  hp.chain_launches = G;
+  hp.launches = scaled ? 2 : 1;
+  hp.chain_launches = scaled ? 2 * G : G;
 }
 
 static optimus_status build_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
@@ -917,21 +907,28 @@ static const P* at(char* table, size_t off) {
   return (const P*)(table + off);
 }
 
-static hipError_t launch_fp8(const HostPlan& hp, char* table, const RowLaunch& l, hipStream_t stream) {
+// One execution of a codec plan over the given item ranges: for scaled
+// quantize the amax launch, then the convert launch.
+static hipError_t launch_fp8(const HostPlan& hp, char* table, const RowLaunch* amax, const RowLaunch& conv,
+                             hipStream_t stream) {
   const DevFp8* descs = at<DevFp8>(table, hp.q_descs_off);
-  const Fp8Item* items = at<Fp8Item>(table, hp.q_items_off) + l.first_tile;
-  if (hp.kind == KIND_DQ8) return fp8_dequantize_launch(hp.dt, descs, items, l.num_tiles, l.grid, stream);
-  return fp8_quantize_launch(hp.dt, hp.q_scaled, descs, items, l.num_tiles, l.grid,
-                             hp.q_scaled ? (Fp8Ctl*)(table + hp.q_ctl_off) : nullptr,
-                             hp.q_scaled ? (uint64_t*)(table + hp.q_slots_off) : nullptr,
-                             hp.q_scaled ? (uint64_t*)(table + hp.q_mamax_off) : nullptr, stream);
+  const Fp8Item* items = at<Fp8Item>(table, hp.q_items_off);
+  if (hp.kind == KIND_DQ8)
+    return fp8_dequantize_launch(hp.dt, descs, items + conv.first_tile, conv.num_tiles, conv.grid, stream);
+  uint32_t* slots = nullptr;
+  if (hp.q_scaled) {
+    slots = (uint32_t*)(table + hp.q_slots_off);
+    hipError_t e = fp8_amax_launch(hp.dt, descs, items + amax->first_tile, amax->num_tiles, amax->grid, slots, stream);
+    if (e != hipSuccess) return e;
+  }
+  return fp8_quantize_launch(hp.dt, descs, items + conv.first_tile, conv.num_tiles, conv.grid, slots, stream);
 }
 
 static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t stream) {
   switch (hp.kind) {
     case KIND_Q8:
     case KIND_DQ8:
-      return launch_fp8(hp, table, hp.q_grouped, stream);
+      return launch_fp8(hp, table, &hp.q_amax, hp.q_grouped, stream);
     case KIND_LINEAR:
       return gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(table, hp.g_descs_off), at<GemmTile>(table, hp.g_tiles_off),
                          hp.g_num_tiles, hp.g_grid, stream);
@@ -1082,7 +1079,7 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
     for (int g = 0; g < hp.G; ++g) {
       hipError_t e;
       if (hp.kind == KIND_Q8 || hp.kind == KIND_DQ8) {
-        e = launch_fp8(hp, p->table, hp.q_chain[g], st);
+        e = launch_fp8(hp, p->table, hp.q_scaled ? &hp.q_chain_amax[g] : nullptr, hp.q_chain[g], st);
       } else if (hp.kind == KIND_LINEAR) {
         const RowLaunch& c = hp.g_chain[g];
         e = gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(p->table, hp.g_descs_off),

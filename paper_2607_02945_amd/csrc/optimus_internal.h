@@ -141,32 +141,26 @@ struct DevFp8 {
   int32_t rows, cols;
   int32_t lanes;         // threads per row of the 16-byte path (power of two, 1..256), or 0
   int32_t lanes_scalar;  // threads per row of the per-value path
-  int32_t slot0, nslots; // the member's amax partial slots (scaled quantize)
+  int32_t slot0, nslots; // the member's amax slots (scaled quantize)
 };
 
 // One work item: rows [row0, row0 + nrows) x item columns [c0, c1) of
-// `member`. slot >= 0 marks an amax item (its partial slot); -1 a convert item.
+// `member`; slot: the amax slot an amax item writes (-1 for other items).
 struct Fp8Item {
   int32_t member, row0, nrows, c0, c1, slot;
 };
 
-// Control block of a scaled quantize launch (plan-owned, zero at upload).
-struct Fp8Ctl {
-  uint32_t ticket;  // next item to draw
-  uint32_t done;    // workgroups finished
-  uint32_t gen;     // launches completed: partial slots of this launch carry gen + 1
-  uint32_t err;     // set if a bounded wait ran out (never in a correct schedule)
-};
-// Iterations (each a short sleep) of the bounded wait for an amax slot.
-constexpr uint32_t kFp8SpinLimit = 1u << 24;
-
-hipError_t fp8_quantize_launch(optimus_dtype dt, bool scaled, const DevFp8* descs, const Fp8Item* items,
-                               int32_t num_items, int32_t grid, Fp8Ctl* ctl, uint64_t* slots, uint64_t* mamax,
-                               hipStream_t stream);
+// Scaled quantize: amax launch (one slot per amax item: nan flag << 31 |
+// max |x| bits), then the convert launch, which reads the member's slots.
+hipError_t fp8_amax_launch(optimus_dtype dt, const DevFp8* descs, const Fp8Item* items, int32_t num_items,
+                           int32_t grid, uint32_t* slots, hipStream_t stream);
+// slots == nullptr: unscaled quantize; else the scaled convert launch.
+hipError_t fp8_quantize_launch(optimus_dtype dt, const DevFp8* descs, const Fp8Item* items, int32_t num_items,
+                               int32_t grid, const uint32_t* slots, hipStream_t stream);
 hipError_t fp8_dequantize_launch(optimus_dtype dt, const DevFp8* descs, const Fp8Item* items, int32_t num_items,
                                  int32_t grid, hipStream_t stream);
 // Workgroups of a codec kernel resident per CU (occupancy query); kernel:
-// 0 quantize, 1 scaled quantize, 2 dequantize.
+// 0 quantize, 1 scaled convert, 2 dequantize, 3 amax.
 int fp8_blocks_per_cu(optimus_dtype dt, int kernel);
 
 int device_cu_count();

@@ -36,7 +36,8 @@ def _quantize(ms, scaled, mode="oneshot", plan=None):
     else:
         p = B.optimus_plan_quantize_fp8(xs, qs, scales, scaled)
         info = p.info()
-        assert info["kind"] == 5 and info["launches"] == 1 and info["chain_launches"] == len(ms)
+        launches = 2 if scaled else 1
+        assert info["kind"] == 5 and info["launches"] == launches and info["chain_launches"] == launches * len(ms)
         assert info["kernel"].startswith("grouped_quantize_fp8_scaled" if scaled else "grouped_quantize_fp8_")
         p.execute(mode)
         torch.cuda.synchronize()
@@ -103,7 +104,7 @@ def test_every_finite_bf16_value_scaled(dtype):
 
 # ------------------------------------------------------------------ random groups
 SHAPES = [(1000, 256, 1.0), (333, 520, 0.01), (64, 8, 100.0), (1, 4096, 3.0), (2, 40000, 0.5), (4097, 24, 50.0),
-          (130, 1024, 2.0 ** -7)]
+          (130, 1024, 2.0 ** -7), (2, 100000, 30.0)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
@@ -138,8 +139,7 @@ def test_strided_and_unaligned(dtype, scaled):
 
 
 def test_many_small_members():
-    """300 small members: many members per grid of items, so the convert items
-    of one member sit among other members' amax items."""
+    """300 small members, one amax slot each, in one launch pair."""
     say("[fp8 many members]")
     g = synth.rng(303)
     rows = g.integers(1, 200, size=300)
@@ -147,6 +147,18 @@ def test_many_small_members():
     sig = np.exp2(g.uniform(-10, 10, size=300))
     ms = [_member(g.standard_normal((int(r), int(c))) * s, "bf16") for r, c, s in zip(rows, cols, sig)]
     _check_codes(ms, _quantize(ms, True, "grouped"), True, "many members")
+
+
+def test_large_member_amax_tiles():
+    """An 80 MB member: its amax tiles grow past the default so that a
+    convert item reduces at most about 256 partials; a small member beside it."""
+    say("[fp8 large member]")
+    g = synth.rng(309)
+    ms = [_member(g.standard_normal((40000, 1024)) * 3.0, "bf16"), _member(g.standard_normal((10, 64)), "bf16")]
+    ms[0]["x"][12345, 678] = 1000.0   # the amax sits in one tile only
+    ms[0]["x64"][12345, 678] = 1000.0
+    for mode in ["grouped", "chain"]:
+        _check_codes(ms, _quantize(ms, True, mode), True, f"large member {mode}")
 
 
 def test_special_members():
@@ -171,7 +183,7 @@ def test_special_members():
 def test_plan_executes_again():
     """A scaled plan run several times, grouped and chain interleaved, with
     the inputs changed in place between runs: every run matches the oracle on
-    the inputs it saw (the launch generation keeps stale amax partials out)."""
+    the inputs it saw (no amax partial of an earlier run survives)."""
     say("[fp8 plan re-execution]")
     g = synth.rng(305)
     ms = [_member(g.standard_normal((r, c)) * s, "bf16") for r, c, s in SHAPES[:4]]
