@@ -12,7 +12,8 @@ rotated over enough copies that each step reads data no longer held in the
 Then every launch of the op-group is run `--steps` times back to back over
 the same rotating inputs between one more pair of events; the slowest is the
 dominant kernel, whose mean launch duration divides its algorithmic flops or
-bytes for `roofline`, and `other_kernels` lists the rest (e.g. the grouped
+bytes for `roofline` (a plan of several launches -- the scaled fp8 quantize --
+counts them together, `roofline.kernels`), and `other_kernels` lists the rest (e.g. the grouped
 LayerNorm after a grouped Linear). `traffic` is the HBM bytes per launch from
 the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary when that was taken
 on the current kernel sources.
@@ -309,19 +310,30 @@ def pmc_summary(args):
     name = args.workload
     line = os.path.join(ROOT, "profiles", "bench", f"bench_{name}.json")
     with open(line) as f:
-        kernel = kernel_symbol(json.loads(f.read().splitlines()[-1])["roofline"]["kernel"])
+        label = json.loads(f.read().splitlines()[-1])["roofline"]["kernel"]
+    kernel, kernels = kernel_symbol(label), kernel_symbols(label)
     f_dir, w_dir, cf_dir, cw_dir = args.pmc_summary
-    fetch, nf = _pmc_per_dispatch(f_dir, "FETCH_SIZE", kernel)
-    write, nw = _pmc_per_dispatch(w_dir, "WRITE_SIZE", kernel)
     cfetch, _ = _pmc_per_dispatch(cf_dir, "FETCH_SIZE", COPY_KERNEL)
     cwrite, _ = _pmc_per_dispatch(cw_dir, "WRITE_SIZE", COPY_KERNEL)
     fs, ws = COPY_BYTES / (cfetch * 1024.0), COPY_BYTES / (cwrite * 1024.0)
-    out = {"kernel": kernel, "workload": name, "fetch_kib_per_dispatch": round(fetch, 1),
-           "write_kib_per_dispatch": round(write, 1), "dispatches": [nf, nw],
+    # per execution of the plan: the per-dispatch means of each of its kernels, summed
+    per = {}
+    for k in kernels:
+        fetch, nf = _pmc_per_dispatch(f_dir, "FETCH_SIZE", k)
+        write, nw = _pmc_per_dispatch(w_dir, "WRITE_SIZE", k)
+        per[k] = {"fetch_kib_per_dispatch": round(fetch, 1), "write_kib_per_dispatch": round(write, 1),
+                  "dispatches": [nf, nw], "hbm_bytes": round(fetch * 1024.0 * fs + write * 1024.0 * ws)}
+    out = {"kernel": kernel, "workload": name,
+           "fetch_kib_per_dispatch": round(sum(v["fetch_kib_per_dispatch"] for v in per.values()), 1),
+           "write_kib_per_dispatch": round(sum(v["write_kib_per_dispatch"] for v in per.values()), 1),
+           "dispatches": per[kernel]["dispatches"],
            "copy_bytes": COPY_BYTES, "copy_fetch_kib": round(cfetch, 1), "copy_write_kib": round(cwrite, 1),
            "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
-           "hbm_bytes_per_launch": round(fetch * 1024.0 * fs + write * 1024.0 * ws),
+           "hbm_bytes_per_launch": sum(v["hbm_bytes"] for v in per.values()),
            "sources_sha256": sources_hash(kernel), "command": args.pmc_command}
+    if len(kernels) > 1:
+        out["per_kernel"] = per
+        out["note"] = "one execution of the plan is these launches; hbm_bytes_per_launch is their sum"
     path = os.path.join(ROOT, "profiles", f"{kernel}__{name}.pmc.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
@@ -346,8 +358,16 @@ def copy_probe():
     print(json.dumps({"copy_probe_bytes": COPY_BYTES, "copies": 5}))
 
 
+def kernel_symbols(label):
+    """Symbols of every kernel one execution of a plan launches, in order (a
+    scaled fp8 quantize is an amax launch, then the convert launch)."""
+    if label.startswith("grouped_quantize_fp8_scaled"):
+        return ["grouped_fp8_amax_kernel", "grouped_quantize_fp8_scaled_kernel"]
+    return [kernel_symbol(label)]
+
+
 def kernel_symbol(label):
-    """Symbol name of the kernel behind a plan's kernel label."""
+    """Symbol name of the (last) kernel behind a plan's kernel label."""
     for prefix, sym in (("grouped_quantize_fp8_scaled", "grouped_quantize_fp8_scaled_kernel"),
                         ("grouped_quantize_fp8", "grouped_quantize_fp8_kernel"),
                         ("grouped_dequantize_fp8", "grouped_dequantize_fp8_kernel"),
@@ -366,7 +386,7 @@ KERNEL_SOURCES = {
     "grouped_gemm_skinny_kernel": "kernels_gemm.hip", "split_op_cat_kernel": "kernels_rowwise.hip",
     "grouped_layernorm_kernel": "kernels_rowwise.hip", "grouped_pointwise_kernel": "kernels_rowwise.hip",
     "grouped_quantize_fp8_scaled_kernel": "kernels_fp8.hip", "grouped_quantize_fp8_kernel": "kernels_fp8.hip",
-    "grouped_dequantize_fp8_kernel": "kernels_fp8.hip",
+    "grouped_dequantize_fp8_kernel": "kernels_fp8.hip", "grouped_fp8_amax_kernel": "kernels_fp8.hip",
 }
 
 
@@ -490,6 +510,10 @@ def main():
                 "frac": round(ach / HBM_PEAK_GBS, 4)}
 
     roof = roofline(info, k_ms)
+    if info["launches"] > 1:
+        # the plan is several launches; kernel_us and traffic cover all of them
+        roof["launches"] = info["launches"]
+        roof["kernels"] = kernel_symbols(info["kernel"])
     roof.update({"kernel": info["kernel"], "plan_index": kd, "kernel_us": round(k_ms * 1000.0, 3),
                  "algorithmic_bytes": info["bytes"], "algorithmic_flops": info["flops"],
                  "traffic": traffic_from_profile(info["kernel"], args.workload)})

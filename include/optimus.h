@@ -19,6 +19,9 @@
  *     x*sigmoid(x) as the activation product of batch_aten_mul (grouped
  *     pointwise), and split_cat / merge_splits / split_cat_to_slices
  *     (split-op-cat);
+ *   - the activation-quantization rewrite (Sec. 5; appendix Sec. 8.2):
+ *     saved activations stored as one-byte FP8 codes and restored before
+ *     use, grouped over many tensors (fp8 codec below);
  *   - inputs and outputs map one-to-one (Sec. 3.3, item 2): every member
  *     reads its own input tensors and writes its own caller-owned output.
  *

@@ -19,13 +19,13 @@
 //            128 KB): each tile's max |x| (and whether it holds a NaN) goes to
 //            the tile's own slot -- one writer per slot, no atomics
 //   convert  tiles of 32 KB: a tile reduces its member's slots (a few hundred
-//            bytes, cached), derives scale and inv, converts and stores; it
-//            walks the group in reverse order, so that the tiles the amax
-//            pass read last -- still in the memory-side cache -- come first
-// A single launch would need workgroups to wait for other workgroups' amax
-// tiles; handing work out through a global counter, the one schedule whose
-// waits provably end, costs a same-address device atomic per tile, and those
-// serialize at about 12 ns each on this GPU -- more than the second pass.
+//            bytes, cached), derives scale and inv, converts and stores
+// x is read twice. A single launch would need workgroups to wait for other
+// workgroups' amax tiles; handing work out through a global counter, the one
+// schedule whose waits provably end, costs a same-address device atomic per
+// tile, and those serialize at about 12 ns each on this GPU -- more than the
+// second pass. Both passes stream (nontemporal loads): the memory-side cache
+// gives too little on a re-read for the amax pass to leave x in it.
 #include <type_traits>
 
 #include "device_common.h"
@@ -79,6 +79,13 @@ constexpr int kFp8Threads = 256;
 #define OPTIMUS_FP8_U 4
 #endif
 constexpr int kFp8U = OPTIMUS_FP8_U;
+// Load policy of the two passes over x (1: nontemporal, streaming).
+#ifndef OPTIMUS_FP8_AMAX_NT
+#define OPTIMUS_FP8_AMAX_NT 1
+#endif
+#ifndef OPTIMUS_FP8_CONVERT_NT
+#define OPTIMUS_FP8_CONVERT_NT 1
+#endif
 
 template <int U, class Body>
 __device__ __forceinline__ void walk_tile(const Fp8Item& it, int L, int tid, Body&& body) {
@@ -214,7 +221,8 @@ __device__ __forceinline__ uint32_t tile_amax(const DevFp8& d, const Fp8Item& it
       u32x4 v[U];
 #pragma unroll
       for (int u = 0; u < U; ++u)
-        v[u] = ok[u] ? ld16((const char*)d.x + ((int64_t)r[u] * d.ldx + (int64_t)c[u] * VEC) * s) : u32x4{0u, 0u, 0u, 0u};
+        v[u] = ok[u] ? (OPTIMUS_FP8_AMAX_NT ? ld16_nt : ld16)((const char*)d.x + ((int64_t)r[u] * d.ldx + (int64_t)c[u] * VEC) * s)
+                     : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
       for (int u = 0; u < U; ++u) amax_chunk(acc, v[u]);
     });
@@ -258,7 +266,7 @@ __device__ __forceinline__ void tile_convert(const DevFp8& d, const Fp8Item& it,
       u32x4 v[U];
 #pragma unroll
       for (int u = 0; u < U; ++u)
-        v[u] = ok[u] ? ld16_nt((const char*)d.x + ((int64_t)r[u] * d.ldx + (int64_t)c[u] * VEC) * s)
+        v[u] = ok[u] ? (OPTIMUS_FP8_CONVERT_NT ? ld16_nt : ld16)((const char*)d.x + ((int64_t)r[u] * d.ldx + (int64_t)c[u] * VEC) * s)
                      : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
       for (int u = 0; u < U; ++u) {

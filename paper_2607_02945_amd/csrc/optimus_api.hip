@@ -784,9 +784,8 @@ static int32_t fp8_grid(int64_t items, optimus_dtype dt, int kernel) {
 }
 
 // Shared by quantize and dequantize: the member table and item lists.
-// Grouped: (scaled: the amax items, member order, then) the convert items --
-// in reverse order when scaled, so the data the amax launch read last is
-// converted first. CHAIN: per member, its own items.
+// Grouped: (scaled: the amax items, then) the convert items, member order.
+// CHAIN: per member, its own items.
 static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vector<Fp8Geom>& geo, bool scaled,
                       int kernel) {
   const int G = (int)members.size();
@@ -805,7 +804,6 @@ static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vec
       fp8_items(geo[g], g, m.rows, budget, nslots, amax[g]);
       m.nslots = (int32_t)amax[g].size();
       nslots += m.nslots;
-      std::reverse(conv[g].begin(), conv[g].end());
     }
   }
   std::vector<Fp8Item> items;
@@ -816,8 +814,7 @@ static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vec
   };
   std::vector<Fp8Item> all_a, all_c;
   for (int g = 0; g < G; ++g) all_a.insert(all_a.end(), amax[g].begin(), amax[g].end());
-  for (int g = scaled ? G - 1 : 0; scaled ? g >= 0 : g < G; g += scaled ? -1 : 1)
-    all_c.insert(all_c.end(), conv[g].begin(), conv[g].end());
+  for (int g = 0; g < G; ++g) all_c.insert(all_c.end(), conv[g].begin(), conv[g].end());
   hp.q_amax = scaled ? add(all_a, 3) : RowLaunch{};
   hp.q_grouped = add(all_c, kernel);
   hp.q_chain.clear();
