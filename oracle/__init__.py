@@ -96,6 +96,18 @@ class Oracle:
         L.oracle_dequantize_fp8.restype = None
         L.oracle_dequantize_fp8.argtypes = [_u8p, ctypes.c_int64, _dp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                             ctypes.c_float]
+        L.oracle_linear_backward.restype = None
+        L.oracle_linear_backward.argtypes = [_dp, ctypes.c_int64, _dp, ctypes.c_int64, _dp, ctypes.c_int64,
+                                             _dp, ctypes.c_int64, _dp, ctypes.c_int64, _dp,
+                                             ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
+        L.oracle_act_grad_scalar.restype = ctypes.c_double
+        L.oracle_act_grad_scalar.argtypes = [ctypes.c_double, ctypes.c_int]
+        L.oracle_act_backward.restype = None
+        L.oracle_act_backward.argtypes = [_dp, ctypes.c_int64, _dp, ctypes.c_int64, _dp, ctypes.c_int64,
+                                          ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
+        L.oracle_layernorm_backward.restype = None
+        L.oracle_layernorm_backward.argtypes = [_dp, ctypes.c_int64, _dp, _dp, ctypes.c_int64, _dp, ctypes.c_int64,
+                                                _dp, _dp, ctypes.c_int64, ctypes.c_int64, ctypes.c_double]
         L.oracle_num_threads.restype = ctypes.c_int
         L.oracle_num_threads.argtypes = []
 
@@ -209,6 +221,39 @@ class Oracle:
         self.lib.oracle_dequantize_fp8(q.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), cols, _ptr(y), cols, rows,
                                        cols, float(np.float32(scale)))
         return y
+
+    # ------------------------------------------------------------ backward
+    def linear_backward(self, x, w, dy):
+        """(dX [M,K], dW [N,K], db [N]) of Y = X W^T + b given dY [M,N]."""
+        x, w, dy = _c64(x), _c64(w), _c64(dy)
+        M, K = x.shape
+        N = w.shape[0]
+        assert w.shape[1] == K and dy.shape == (M, N)
+        dx = np.empty((M, K)); dw = np.empty((N, K)); db = np.empty(N)
+        self.lib.oracle_linear_backward(_ptr(x), K, _ptr(w), K, _ptr(dy), N, _ptr(dx), K, _ptr(dw), K, _ptr(db),
+                                        M, N, K)
+        return dx, dw, db
+
+    def act_grad_scalar(self, x: float, act) -> float:
+        return self.lib.oracle_act_grad_scalar(float(x), _act(act))
+
+    def act_backward(self, x, dy, act) -> np.ndarray:
+        """dX = dY * act'(X), X the activation's input."""
+        x, dy = _c64(x), _c64(dy)
+        rows, cols = x.shape
+        dx = np.empty_like(x)
+        self.lib.oracle_act_backward(_ptr(x), cols, _ptr(dy), cols, _ptr(dx), cols, rows, cols, _act(act))
+        return dx
+
+    def layernorm_backward(self, x, gamma, dy, eps=1e-5):
+        """(dX, dgamma, dbeta) of the row LayerNorm (gamma None = 1)."""
+        x, dy = _c64(x), _c64(dy)
+        rows, cols = x.shape
+        g = None if gamma is None else _c64(gamma)
+        dx = np.empty_like(x); dg = np.empty(cols); dbt = np.empty(cols)
+        self.lib.oracle_layernorm_backward(_ptr(x), cols, _ptr(g), _ptr(dy), cols, _ptr(dx), cols, _ptr(dg),
+                                           _ptr(dbt), rows, cols, float(eps))
+        return dx, dg, dbt
 
     def num_threads(self) -> int:
         return self.lib.oracle_num_threads()

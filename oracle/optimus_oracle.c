@@ -181,6 +181,125 @@ int oracle_split_op_cat(const double* in, int64_t ldin, double* out, int64_t ldo
   return 0;
 }
 
+/* ---------------------------------------------------------------- backward
+ *
+ * Training runs the gradients of the grouped operators too (the training
+ * column of Table 3; batch_linear_post_grad in Table 1 groups the Linears of
+ * the backward graph). They are the derivatives of the forward definitions
+ * above, each sum in fp64 in ascending index order. */
+
+/* Linear, given dY = dL/dY of the Linear's output (before any activation):
+ *   dX[m][k] = sum_n dY[m][n] W[n][k]
+ *   dW[n][k] = sum_m dY[m][n] X[m][k]
+ *   db[n]    = sum_m dY[m][n]
+ * dx, dw or db may be NULL (not wanted). */
+void oracle_linear_backward(const double* x, int64_t ldx, const double* w, int64_t ldw,
+                            const double* dy, int64_t lddy, double* dx, int64_t lddx,
+                            double* dw, int64_t lddw, double* db, int64_t M, int64_t N, int64_t K) {
+  if (dx) {
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m)
+      for (int64_t k = 0; k < K; ++k) {
+        double s = 0.0;
+        for (int64_t n = 0; n < N; ++n) s += dy[m * lddy + n] * w[n * ldw + k];
+        dx[m * lddx + k] = s;
+      }
+  }
+  if (dw) {
+#pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < N; ++n)
+      for (int64_t k = 0; k < K; ++k) {
+        double s = 0.0;
+        for (int64_t m = 0; m < M; ++m) s += dy[m * lddy + n] * x[m * ldx + k];
+        dw[n * lddw + k] = s;
+      }
+  }
+  if (db) {
+    for (int64_t n = 0; n < N; ++n) {
+      double s = 0.0;
+      for (int64_t m = 0; m < M; ++m) s += dy[m * lddy + n];
+      db[n] = s;
+    }
+  }
+}
+
+/* Derivative of one activation at its input x. relu' is 0 at x = 0 (the
+ * gradient passes where x > 0, as torch's threshold backward does). */
+double oracle_act_grad_scalar(double x, int act) {
+  switch (act) {
+    case ORC_ACT_NONE: return 1.0;
+    case ORC_ACT_RELU: return x > 0.0 ? 1.0 : 0.0;
+    case ORC_ACT_SIGMOID: {
+      const double s = orc_sigmoid(x);
+      return s * (1.0 - s);
+    }
+    case ORC_ACT_TANH: {
+      const double t = tanh(x);
+      return 1.0 - t * t;
+    }
+    case ORC_ACT_SILU: { /* d/dx x s(x) = s + x s (1 - s) */
+      const double s = orc_sigmoid(x);
+      return s + x * s * (1.0 - s);
+    }
+    default: return NAN;
+  }
+}
+
+/* Activation backward over a [rows, cols] member: dX = dY * act'(X). */
+void oracle_act_backward(const double* x, int64_t ldx, const double* dy, int64_t lddy, double* dx,
+                         int64_t lddx, int64_t rows, int64_t cols, int act) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t c = 0; c < cols; ++c)
+      dx[r * lddx + c] = dy[r * lddy + c] * oracle_act_grad_scalar(x[r * ldx + c], act);
+}
+
+/* LayerNorm backward over a [rows, cols] member, the statistics recomputed
+ * from x as the forward takes them (two-pass biased variance). Per row, with
+ * xhat = (x - mu) / sqrt(var + eps) and g = dY * gamma:
+ *   dX = (g - mean(g) - xhat * mean(g * xhat)) / sqrt(var + eps)
+ * and over all rows dgamma[c] = sum dY * xhat, dbeta[c] = sum dY. gamma
+ * NULL means 1; dx, dgamma or dbeta may be NULL. */
+void oracle_layernorm_backward(const double* x, int64_t ldx, const double* gamma, const double* dy,
+                               int64_t lddy, double* dx, int64_t lddx, double* dgamma, double* dbeta,
+                               int64_t rows, int64_t cols, double eps) {
+  if (dgamma)
+    for (int64_t c = 0; c < cols; ++c) dgamma[c] = 0.0;
+  if (dbeta)
+    for (int64_t c = 0; c < cols; ++c) dbeta[c] = 0.0;
+  for (int64_t r = 0; r < rows; ++r) {
+    const double* xr = x + r * ldx;
+    const double* gr = dy + r * lddy;
+    double mu = 0.0;
+    for (int64_t c = 0; c < cols; ++c) mu += xr[c];
+    mu /= (double)cols;
+    double var = 0.0;
+    for (int64_t c = 0; c < cols; ++c) {
+      const double d = xr[c] - mu;
+      var += d * d;
+    }
+    var /= (double)cols;
+    const double rstd = 1.0 / sqrt(var + eps);
+    double mg = 0.0, mgx = 0.0;
+    for (int64_t c = 0; c < cols; ++c) {
+      const double xhat = (xr[c] - mu) * rstd;
+      const double g = gr[c] * (gamma ? gamma[c] : 1.0);
+      mg += g;
+      mgx += g * xhat;
+      if (dgamma) dgamma[c] += gr[c] * xhat;
+      if (dbeta) dbeta[c] += gr[c];
+    }
+    mg /= (double)cols;
+    mgx /= (double)cols;
+    if (dx)
+      for (int64_t c = 0; c < cols; ++c) {
+        const double xhat = (xr[c] - mu) * rstd;
+        const double g = gr[c] * (gamma ? gamma[c] : 1.0);
+        dx[r * lddx + c] = (g - mg - xhat * mgx) * rstd;
+      }
+  }
+}
+
 /* ------------------------------------------------------- fp8 activation codec
  *
  * The activation-quantization rewrite (paper Sec. 5 memory results; appendix

@@ -399,11 +399,102 @@ def split_op_cat_bad_widths(orc):
     raise AssertionError("widths not summing to D must be rejected")
 
 
+# ---------------------------------------------------------------- backward
+def _autograd(fn, inputs, dy):
+    """Gradients of sum(fn(*inputs) * dy) with torch autograd in fp64."""
+    ts = [torch.tensor(a, dtype=torch.float64, requires_grad=True) for a in inputs]
+    out = fn(*ts)
+    out.backward(torch.tensor(dy, dtype=torch.float64))
+    return [t.grad.numpy() for t in ts]
+
+
+def linear_backward_vs_autograd(orc):
+    """dX, dW, db of Y = X W^T + b against torch autograd (fp64) on ragged shapes."""
+    g = _rng(40)
+    for (M, N, K) in [(7, 5, 3), (33, 17, 64), (1, 9, 4), (65, 1, 2)]:
+        x, w, b = g.standard_normal((M, K)), g.standard_normal((N, K)), g.standard_normal(N)
+        dy = g.standard_normal((M, N))
+        ref = _autograd(torch.nn.functional.linear, [x, w, b], dy)
+        got = orc.linear_backward(x, w, dy)
+        for a, r, name in zip(got, ref, ("dx", "dw", "db")):
+            assert a.shape == r.shape and _nrm(a, r) < 1e-13, (M, N, K, name)
+
+
+def linear_backward_integer_and_fd(orc):
+    """Small integers: exact against numpy's int64 products; and a central
+    difference of the oracle's own forward along a random direction matches
+    the oracle's gradient (ties the backward to the forward definition)."""
+    g = _rng(41)
+    x = g.integers(-4, 5, (6, 3)); w = g.integers(-4, 5, (4, 3)); dy = g.integers(-3, 4, (6, 4))
+    dx, dw, db = orc.linear_backward(x.astype(float), w.astype(float), dy.astype(float))
+    assert np.array_equal(dx, (dy @ w).astype(float)) and np.array_equal(dw, (dy.T @ x).astype(float))
+    assert np.array_equal(db, dy.sum(0).astype(float))
+    x, w, b, dy = g.standard_normal((5, 4)), g.standard_normal((3, 4)), g.standard_normal(3), g.standard_normal((5, 3))
+    vx, vw = g.standard_normal(x.shape), g.standard_normal(w.shape)
+    L = lambda xx, ww: float(np.sum(orc.linear(xx, ww, b) * dy))
+    h = 1e-6
+    fd = (L(x + h * vx, w + h * vw) - L(x - h * vx, w - h * vw)) / (2 * h)
+    dx, dw, _ = orc.linear_backward(x, w, dy)
+    assert abs(fd - (np.sum(dx * vx) + np.sum(dw * vw))) < 1e-7
+
+
+def act_backward_vs_autograd(orc):
+    """act'(x) for every activation against torch autograd (fp64), including
+    x = 0 exactly (relu passes no gradient there) and large |x|."""
+    x = np.concatenate([np.linspace(-9, 9, 37), [0.0, -0.0, 30.0, -30.0, 1e-8]]).reshape(1, -1)
+    dy = _rng(42).standard_normal(x.shape)
+    fns = {"none": lambda t: t, "relu": torch.relu, "sigmoid": torch.sigmoid, "tanh": torch.tanh,
+           "silu": torch.nn.functional.silu}
+    for act, fn in fns.items():
+        ref = _autograd(fn, [x], dy)[0]
+        got = orc.act_backward(x, dy, act)
+        assert np.max(np.abs(got - ref)) < 1e-14, act
+    assert orc.act_grad_scalar(0.0, "sigmoid") == 0.25 and orc.act_grad_scalar(0.0, "tanh") == 1.0
+    assert orc.act_grad_scalar(0.0, "silu") == 0.5 and orc.act_grad_scalar(0.0, "relu") == 0.0
+
+
+def layernorm_backward_vs_autograd(orc):
+    """dX, dgamma, dbeta of the row LayerNorm against torch autograd (fp64),
+    with and without gamma, several eps."""
+    g = _rng(43)
+    for (R, C, eps) in [(5, 8, 1e-5), (17, 33, 1e-3), (1, 3, 0.0), (9, 64, 0.5)]:
+        x, gm, bt = g.standard_normal((R, C)) * 3 + 1, g.uniform(0.5, 1.5, C), g.standard_normal(C)
+        dy = g.standard_normal((R, C))
+        fn = lambda xx, gg, bb: torch.nn.functional.layer_norm(xx, (C,), gg, bb, eps)
+        ref = _autograd(fn, [x, gm, bt], dy)
+        got = orc.layernorm_backward(x, gm, dy, eps)
+        for a, r, name in zip(got, ref, ("dx", "dgamma", "dbeta")):
+            assert _nrm(a, r) < 1e-12, (R, C, eps, name)
+        ref1 = _autograd(lambda xx: torch.nn.functional.layer_norm(xx, (C,), None, None, eps), [x], dy)[0]
+        assert _nrm(orc.layernorm_backward(x, None, dy, eps)[0], ref1) < 1e-12
+
+
+def layernorm_backward_invariants(orc):
+    """With eps = 0 the output is invariant to shifting and scaling an input
+    row, so each row gradient is orthogonal to 1 and to x; dbeta = column
+    sums of dY, dgamma = column sums of dY * xhat; a central difference of the
+    oracle's forward (eps = 1e-5, with gamma)."""
+    g = _rng(44)
+    x, dy = g.standard_normal((12, 40)) * 2, g.standard_normal((12, 40))
+    dx, dg, dbt = orc.layernorm_backward(x, None, dy, 0.0)
+    xhat = orc.layernorm(x, None, None, 0.0)
+    assert np.max(np.abs(dx.sum(1))) < 1e-12 and np.max(np.abs((dx * x).sum(1))) < 1e-11
+    assert np.max(np.abs(dbt - dy.sum(0))) < 1e-12 and np.max(np.abs(dg - (dy * xhat).sum(0))) < 1e-12
+    gm = g.uniform(0.5, 1.5, 40)
+    v = g.standard_normal(x.shape)
+    L = lambda xx: float(np.sum(orc.layernorm(xx, gm, None, 1e-5) * dy))
+    h = 1e-6
+    fd = (L(x + h * v) - L(x - h * v)) / (2 * h)
+    assert abs(fd - np.sum(orc.layernorm_backward(x, gm, dy, 1e-5)[0] * v)) < 1e-6
+
+
 ALL_PINS = [
     linear_vs_blas, linear_special_cases, linear_brute_force, linear_epilogue, linear_rows_subset,
     linear_batch_fusion, linear_shared_input, layernorm_vs_torch, layernorm_invariants, layernorm_constant_row,
     layernorm_affine, layernorm_epilogue_and_batch, linear_layernorm_reductions, linear_layernorm_invariants,
     fp8_decode_all_codes, fp8_encode_round_trip_and_ties, fp8_encode_vs_torch, fp8_overflow_and_scaling,
+    linear_backward_vs_autograd, linear_backward_integer_and_fd, act_backward_vs_autograd,
+    layernorm_backward_vs_autograd, layernorm_backward_invariants,
     pointwise_closed_forms,
     split_concat_appendix_example, split_concat_identity_random, split_op_cat_pieces, split_op_cat_tag,
     split_op_cat_bad_widths,

@@ -20,7 +20,9 @@ MUTANTS = [
     ("dropped_bias", "      if (bias) s += bias[n];\n      y[m * ldy + n]", "      y[m * ldy + n]"),
     ("bias_wrong_index", "if (bias) s += bias[n];\n      y[m * ldy", "if (bias) s += bias[m % N];\n      y[m * ldy"),
     ("rows_wrong_row", "const double* xr = x + rows[i] * ldx;", "const double* xr = x + i * ldx;"),
-    ("unbiased_variance", "var /= (double)cols;", "var /= (double)(cols > 1 ? cols - 1 : 1);"),
+    ("unbiased_variance", "var /= (double)cols;\n  double inv", "var /= (double)(cols > 1 ? cols - 1 : 1);\n  double inv"),
+    ("bwd_ln_unbiased_variance", "var /= (double)cols;\n    const double rstd",
+     "var /= (double)(cols > 1 ? cols - 1 : 1);\n    const double rstd"),
     ("eps_outside_sqrt", "double inv = 1.0 / sqrt(var + eps);", "double inv = 1.0 / (sqrt(var) + eps);"),
     ("mean_not_subtracted", "double v = (x[c] - mu) * inv;", "double v = x[c] * inv;"),
     ("beta_dropped", "if (beta) v += beta[c];", ""),
@@ -40,6 +42,20 @@ MUTANTS = [
     ("fp8_sign_dropped", "const int s = signbit(v) ? 0x80 : 0;", "const int s = 0;"),
     ("fp8_overflow_threshold", "if (a > 464.0)", "if (a >= 464.0)"),
     ("fp8_nan_unsigned", "if (isnan(v)) return s | 0x7F;", "if (isnan(v)) return 0x7F;"),
+    ("bwd_dw_uses_w", "for (int64_t m = 0; m < M; ++m) s += dy[m * lddy + n] * x[m * ldx + k];",
+     "for (int64_t m = 0; m < M; ++m) s += dy[m * lddy + n] * w[n * ldw + k];"),
+    ("bwd_dx_transposed_w", "for (int64_t n = 0; n < N; ++n) s += dy[m * lddy + n] * w[n * ldw + k];",
+     "for (int64_t n = 0; n < N; ++n) s += dy[m * lddy + n] * w[k * ldw + n];"),
+    ("bwd_db_first_row", "for (int64_t m = 0; m < M; ++m) s += dy[m * lddy + n];\n      db[n] = s;",
+     "s = dy[n];\n      db[n] = s;"),
+    ("bwd_relu_at_zero", "case ORC_ACT_RELU: return x > 0.0 ? 1.0 : 0.0;", "case ORC_ACT_RELU: return x >= 0.0 ? 1.0 : 0.0;"),
+    ("bwd_sigmoid_grad_s", "return s * (1.0 - s);\n    }\n    case ORC_ACT_TANH:", "return s;\n    }\n    case ORC_ACT_TANH:"),
+    ("bwd_tanh_grad_linear", "return 1.0 - t * t;", "return 1.0 - t;"),
+    ("bwd_silu_no_x_term", "return s + x * s * (1.0 - s);", "return s;"),
+    ("bwd_ln_no_mean_g", "dx[r * lddx + c] = (g - mg - xhat * mgx) * rstd;", "dx[r * lddx + c] = (g - xhat * mgx) * rstd;"),
+    ("bwd_ln_no_xhat_term", "dx[r * lddx + c] = (g - mg - xhat * mgx) * rstd;", "dx[r * lddx + c] = (g - mg) * rstd;"),
+    ("bwd_ln_gamma_ignored", "const double g = gr[c] * (gamma ? gamma[c] : 1.0);\n        dx[", "const double g = gr[c];\n        dx["),
+    ("bwd_ln_dgamma_no_xhat", "if (dgamma) dgamma[c] += gr[c] * xhat;", "if (dgamma) dgamma[c] += gr[c];"),
     ("fp8_nan_sign_of_product", "isnan(v) ? (uint8_t)(signbit(xv) ? 0xFF : 0x7F)", "isnan(v) ? (uint8_t)(signbit(v) ? 0xFF : 0x7F)"),
     ("fp8_scale_inverted", "inv = 448.0f / amax;", "inv = amax / 448.0f;"),
     ("fp8_no_carry", "if (q == 16) { q = 8; ef = e + 1; }", ""),
