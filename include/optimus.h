@@ -155,6 +155,60 @@ typedef struct {
   optimus_act act;
 } optimus_split_op_cat_desc;
 
+/* One member of the grouped Linear backward (training; the backward graph's
+ * grouped Linear, Table 1 batch_linear_post_grad, and the training column of
+ * Table 3). Given the forward's X [M][K], W [N][K] and dY = dL/dY [M][N] of
+ * the Linear's output (before any activation; apply the activation's
+ * backward first):
+ *   dX[M][K] = dY . W,   dW[N][K] = dY^T . X,   db[N] = sum over rows of dY
+ * Outputs left NULL are not computed; db needs dw (it is summed while the dW
+ * launch streams dY). Sums in fp32, outputs rounded to the group's dtype. */
+typedef struct {
+  const void* x;
+  int64_t ldx;
+  const void* w;
+  int64_t ldw;
+  const void* dy;
+  int64_t lddy;
+  void* dx;
+  int64_t lddx;
+  void* dw;
+  int64_t lddw;
+  void* db;
+  int64_t M, N, K;
+} optimus_linear_grad_desc;
+
+/* One member of the grouped LayerNorm backward: x [rows][cols] is the
+ * forward's input (the statistics are recomputed from it), gamma [cols] or
+ * NULL (1), dy = dL/dy [rows][cols] of the LayerNorm's output (apply any
+ * activation's backward first). Writes dx [rows][cols] and, if not NULL,
+ * dgamma and dbeta [cols] (sums over rows). */
+typedef struct {
+  const void* x;
+  int64_t ldx;
+  const void* gamma;
+  const void* dy;
+  int64_t lddy;
+  void* dx;
+  int64_t lddx;
+  void* dgamma;
+  void* dbeta;
+  int64_t rows, cols;
+  float eps;
+} optimus_layernorm_grad_desc;
+
+/* One member of the grouped activation backward: dx = dy * act'(x), x the
+ * activation's input [rows][cols] (relu passes no gradient at x = 0). */
+typedef struct {
+  const void* x;
+  int64_t ldx;
+  const void* dy;
+  int64_t lddy;
+  void* dx;
+  int64_t lddx;
+  int64_t rows, cols;
+} optimus_act_grad_desc;
+
 /* One member of the fp8 activation codec (paper Sec. 5, peak memory usage
  * reduction; appendix Sec. 8.2, activation quantization: saved activations
  * are stored in FP8 in the forward pass and restored to their own dtype
@@ -240,6 +294,23 @@ optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_desc* d, int
 optimus_status optimus_grouped_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
                                               optimus_stream_t stream);
 
+/* Grouped Linear backward: two launches for the whole group -- every dX,
+ * then every dW (with db) -- on the register-staged grouped GEMM, whose
+ * loads transpose W, X and dY through registers into the tile layout the
+ * forward uses. */
+optimus_status optimus_grouped_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
+                                               optimus_stream_t stream);
+
+/* Grouped LayerNorm backward: one launch for dx and per-tile column
+ * partials of dgamma / dbeta, one small launch that sums the partials.
+ * Exact in-place (dx == dy, equal strides) is allowed. */
+optimus_status optimus_grouped_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
+                                                  optimus_stream_t stream);
+
+/* Grouped activation backward, one launch. Exact in-place (dx == dy) is allowed. */
+optimus_status optimus_grouped_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt,
+                                            optimus_act act, optimus_stream_t stream);
+
 /* ---------------------------------------------------------------- plans
  * A plan validates once and keeps the group's descriptor table and launch
  * schedule resident in device memory (allocated with hipMalloc on the current
@@ -264,6 +335,12 @@ optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_desc* d, opt
  * (about 256 per member at most), written by its first launch and read by
  * its second: executions of one scaled plan must not overlap (use one
  * stream, or order them with events); one-shot calls each get their own. */
+optimus_status optimus_plan_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
+                                            optimus_plan* out);
+optimus_status optimus_plan_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
+                                               optimus_plan* out);
+optimus_status optimus_plan_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
+                                         optimus_plan* out);
 optimus_status optimus_plan_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
                                          int32_t use_scaling, optimus_plan* out);
 optimus_status optimus_plan_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
@@ -299,9 +376,11 @@ void optimus_plan_destroy(optimus_plan plan);
  * outputs), never padding, re-reads or temporaries. */
 typedef struct {
   int32_t kind;            /* 0 linear, 1 layernorm, 2 pointwise, 3 split_op_cat, 4 linear_layernorm,
-                              5 quantize_fp8, 6 dequantize_fp8 */
+                              5 quantize_fp8, 6 dequantize_fp8, 7 linear_backward,
+                              8 layernorm_backward, 9 act_backward */
   int32_t group_size;      /* G, or n_slices */
-  int32_t launches;        /* kernel launches per GROUPED execute (1; 2 for a scaled quantize) */
+  int32_t launches;        /* kernel launches per GROUPED execute (1; 2 for a scaled quantize, a
+                              Linear backward with dX and dW, a LayerNorm backward with dgamma/dbeta) */
   int32_t chain_launches;  /* kernel launches per CHAIN execute */
   int64_t work_items;      /* GEMM tiles / row tiles of the grouped launch */
   int32_t grid;            /* workgroups of the grouped launch */
@@ -323,6 +402,9 @@ optimus_status optimus_validate_linear_layernorm(const optimus_linear_desc* d, c
 optimus_status optimus_validate_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
 optimus_status optimus_validate_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
 optimus_status optimus_validate_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt);
+optimus_status optimus_validate_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt);
+optimus_status optimus_validate_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt);
+optimus_status optimus_validate_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt, optimus_act act);
 optimus_status optimus_validate_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
                                              int32_t use_scaling);
 optimus_status optimus_validate_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt);

@@ -46,6 +46,23 @@ class SplitOpCatDesc(ctypes.Structure):
                 ("act", ctypes.c_int)]
 
 
+class LinearGradDesc(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("ldx", c_i64), ("w", c_vp), ("ldw", c_i64), ("dy", c_vp), ("lddy", c_i64),
+                ("dx", c_vp), ("lddx", c_i64), ("dw", c_vp), ("lddw", c_i64), ("db", c_vp), ("M", c_i64),
+                ("N", c_i64), ("K", c_i64)]
+
+
+class LayerNormGradDesc(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("ldx", c_i64), ("gamma", c_vp), ("dy", c_vp), ("lddy", c_i64), ("dx", c_vp),
+                ("lddx", c_i64), ("dgamma", c_vp), ("dbeta", c_vp), ("rows", c_i64), ("cols", c_i64),
+                ("eps", ctypes.c_float)]
+
+
+class ActGradDesc(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("ldx", c_i64), ("dy", c_vp), ("lddy", c_i64), ("dx", c_vp), ("lddx", c_i64),
+                ("rows", c_i64), ("cols", c_i64)]
+
+
 class Fp8QuantDesc(ctypes.Structure):
     _fields_ = [("x", c_vp), ("ldx", c_i64), ("q", c_vp), ("ldq", c_i64), ("scale", c_vp), ("rows", c_i64),
                 ("cols", c_i64)]
@@ -66,7 +83,10 @@ class PlanInfo(ctypes.Structure):
 EXPORTS = [
     "optimus_grouped_linear", "optimus_grouped_linear_layernorm", "optimus_grouped_layernorm",
     "optimus_grouped_pointwise", "optimus_split_op_cat", "optimus_grouped_quantize_fp8",
-    "optimus_grouped_dequantize_fp8",
+    "optimus_grouped_dequantize_fp8", "optimus_grouped_linear_backward", "optimus_grouped_layernorm_backward",
+    "optimus_grouped_act_backward", "optimus_plan_linear_backward", "optimus_plan_layernorm_backward",
+    "optimus_plan_act_backward", "optimus_validate_linear_backward", "optimus_validate_layernorm_backward",
+    "optimus_validate_act_backward",
     "optimus_plan_linear", "optimus_plan_linear_layernorm", "optimus_plan_layernorm", "optimus_plan_pointwise",
     "optimus_plan_split_op_cat", "optimus_plan_quantize_fp8", "optimus_plan_dequantize_fp8",
     "optimus_plan_execute", "optimus_plan_execute_mode", "optimus_plan_destroy", "optimus_plan_get_info",
@@ -108,6 +128,15 @@ def lib() -> ctypes.CDLL:
             "optimus_plan_layernorm": (st, [P(LayerNormDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
             "optimus_plan_pointwise": (st, [P(PointwiseDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
             "optimus_plan_split_op_cat": (st, [P(SplitOpCatDesc), ctypes.c_int, P(c_vp)]),
+            "optimus_grouped_linear_backward": (st, [P(LinearGradDesc), c_i32, ctypes.c_int, c_vp]),
+            "optimus_grouped_layernorm_backward": (st, [P(LayerNormGradDesc), c_i32, ctypes.c_int, c_vp]),
+            "optimus_grouped_act_backward": (st, [P(ActGradDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
+            "optimus_plan_linear_backward": (st, [P(LinearGradDesc), c_i32, ctypes.c_int, P(c_vp)]),
+            "optimus_plan_layernorm_backward": (st, [P(LayerNormGradDesc), c_i32, ctypes.c_int, P(c_vp)]),
+            "optimus_plan_act_backward": (st, [P(ActGradDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
+            "optimus_validate_linear_backward": (st, [P(LinearGradDesc), c_i32, ctypes.c_int]),
+            "optimus_validate_layernorm_backward": (st, [P(LayerNormGradDesc), c_i32, ctypes.c_int]),
+            "optimus_validate_act_backward": (st, [P(ActGradDesc), c_i32, ctypes.c_int, ctypes.c_int]),
             "optimus_grouped_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32, c_vp]),
             "optimus_grouped_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int, c_vp]),
             "optimus_plan_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32, P(c_vp)]),
@@ -204,6 +233,52 @@ def pointwise_descs(xs, ys) -> ctypes.Array:
     return arr
 
 
+def _opt_mat(t, name):
+    return (None, 0) if t is None else _mat(t, name)
+
+
+def linear_grad_descs(xs, ws, dys, dxs=None, dws=None, dbs=None) -> ctypes.Array:
+    """Members of a Linear backward: forward X [M,K], W [N,K], dY [M,N]; the
+    wanted gradients dX, dW, db (lists with None entries, or None)."""
+    G = len(dys)
+    arr = (LinearGradDesc * max(G, 1))()
+    pick = lambda v, g: None if v is None else v[g]
+    for g in range(G):
+        dy, lddy = _mat(dys[g], "dy")
+        x, ldx = _opt_mat(pick(xs, g), "x")
+        w, ldw = _opt_mat(pick(ws, g), "w")
+        dx, lddx = _opt_mat(pick(dxs, g), "dx")
+        dw, lddw = _opt_mat(pick(dws, g), "dw")
+        M, N = dys[g].shape
+        K = (pick(xs, g) if pick(xs, g) is not None else pick(ws, g)).shape[1]
+        arr[g] = LinearGradDesc(x, ldx, w, ldw, dy, lddy, dx, lddx, dw, lddw, _ptr(pick(dbs, g)), M, N, K)
+    return arr
+
+
+def layernorm_grad_descs(xs, dys, dxs, gammas=None, dgammas=None, dbetas=None, eps=1e-5) -> ctypes.Array:
+    G = len(xs)
+    arr = (LayerNormGradDesc * max(G, 1))()
+    pick = lambda v, g: None if v is None else v[g]
+    for g in range(G):
+        x, ldx = _mat(xs[g], "x")
+        dy, lddy = _mat(dys[g], "dy")
+        dx, lddx = _mat(dxs[g], "dx")
+        arr[g] = LayerNormGradDesc(x, ldx, _ptr(pick(gammas, g)), dy, lddy, dx, lddx, _ptr(pick(dgammas, g)),
+                                   _ptr(pick(dbetas, g)), xs[g].shape[0], xs[g].shape[1], float(eps))
+    return arr
+
+
+def act_grad_descs(xs, dys, dxs) -> ctypes.Array:
+    G = len(xs)
+    arr = (ActGradDesc * max(G, 1))()
+    for g in range(G):
+        x, ldx = _mat(xs[g], "x")
+        dy, lddy = _mat(dys[g], "dy")
+        dx, lddx = _mat(dxs[g], "dx")
+        arr[g] = ActGradDesc(x, ldx, dy, lddy, dx, lddx, xs[g].shape[0], xs[g].shape[1])
+    return arr
+
+
 def fp8_quant_descs(xs, qs, scales) -> ctypes.Array:
     """xs: values (bf16 / fp32), qs: uint8 codes of the same shapes, scales:
     one-element fp32 device tensors, or None (unscaled)."""
@@ -293,6 +368,24 @@ def optimus_grouped_dequantize_fp8(qs, scales, ys, stream=None) -> None:
     check(lib().optimus_grouped_dequantize_fp8(d, len(qs), dtype_code(ys[0]) if ys else BF16, _stream(stream)))
 
 
+def optimus_grouped_linear_backward(xs, ws, dys, dxs=None, dws=None, dbs=None, stream=None) -> None:
+    """dX = dY W, dW = dY^T X, db = column sums of dY, for every member; two launches for the group."""
+    d = linear_grad_descs(xs, ws, dys, dxs, dws, dbs)
+    check(lib().optimus_grouped_linear_backward(d, len(dys), dtype_code(dys[0]) if dys else BF16, _stream(stream)))
+
+
+def optimus_grouped_layernorm_backward(xs, dys, dxs, gammas=None, dgammas=None, dbetas=None, eps=1e-5,
+                                       stream=None) -> None:
+    d = layernorm_grad_descs(xs, dys, dxs, gammas, dgammas, dbetas, eps)
+    check(lib().optimus_grouped_layernorm_backward(d, len(xs), dtype_code(xs[0]) if xs else BF16, _stream(stream)))
+
+
+def optimus_grouped_act_backward(xs, dys, dxs, act, stream=None) -> None:
+    d = act_grad_descs(xs, dys, dxs)
+    check(lib().optimus_grouped_act_backward(d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
+                                             _stream(stream)))
+
+
 # ------------------------------------------------------------------ plans
 class Plan:
     """A validated group with its device table resident; execute() is one launch."""
@@ -363,6 +456,24 @@ def optimus_plan_split_op_cat(inp, out, widths, gammas=None, betas=None, apply_l
                  keep=(inp, out, gammas, betas))
 
 
+def optimus_plan_linear_backward(xs, ws, dys, dxs=None, dws=None, dbs=None) -> Plan:
+    d = linear_grad_descs(xs, ws, dys, dxs, dws, dbs)
+    return _plan(lib().optimus_plan_linear_backward, d, len(dys), dtype_code(dys[0]) if dys else BF16,
+                 keep=(xs, ws, list(dys), dxs, dws, dbs))
+
+
+def optimus_plan_layernorm_backward(xs, dys, dxs, gammas=None, dgammas=None, dbetas=None, eps=1e-5) -> Plan:
+    d = layernorm_grad_descs(xs, dys, dxs, gammas, dgammas, dbetas, eps)
+    return _plan(lib().optimus_plan_layernorm_backward, d, len(xs), dtype_code(xs[0]) if xs else BF16,
+                 keep=(list(xs), list(dys), list(dxs), gammas, dgammas, dbetas))
+
+
+def optimus_plan_act_backward(xs, dys, dxs, act) -> Plan:
+    d = act_grad_descs(xs, dys, dxs)
+    return _plan(lib().optimus_plan_act_backward, d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
+                 keep=(list(xs), list(dys), list(dxs)))
+
+
 def optimus_plan_quantize_fp8(xs, qs, scales=None, use_scaling=True) -> Plan:
     d = fp8_quant_descs(xs, qs, scales)
     return _plan(lib().optimus_plan_quantize_fp8, d, len(xs), dtype_code(xs[0]) if xs else BF16, int(use_scaling),
@@ -396,6 +507,18 @@ def optimus_validate_pointwise(descs: ctypes.Array, G: int, dtype: int, act="non
 
 def optimus_validate_split_op_cat(desc: SplitOpCatDesc, dtype: int) -> int:
     return lib().optimus_validate_split_op_cat(ctypes.byref(desc), dtype)
+
+
+def optimus_validate_linear_backward(descs: ctypes.Array, G: int, dtype: int) -> int:
+    return lib().optimus_validate_linear_backward(descs, G, dtype)
+
+
+def optimus_validate_layernorm_backward(descs: ctypes.Array, G: int, dtype: int) -> int:
+    return lib().optimus_validate_layernorm_backward(descs, G, dtype)
+
+
+def optimus_validate_act_backward(descs: ctypes.Array, G: int, dtype: int, act="none") -> int:
+    return lib().optimus_validate_act_backward(descs, G, dtype, _act(act))
 
 
 def optimus_validate_quantize_fp8(descs: ctypes.Array, G: int, dtype: int, use_scaling=1) -> int:

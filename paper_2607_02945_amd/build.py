@@ -18,7 +18,7 @@ OBJDIR = os.path.join(PKG, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["optimus_api.hip", "kernels_rowwise.hip", "kernels_gemm.hip", "kernels_fp8.hip"]
+SOURCES = ["optimus_api.hip", "kernels_rowwise.hip", "kernels_gemm.hip", "kernels_fp8.hip", "kernels_backward.hip"]
 
 # Packed-fp32 VALU instructions are kept out of every kernel.
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-munsafe-fp-atomics",

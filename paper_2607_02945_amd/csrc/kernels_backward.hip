@@ -1,0 +1,352 @@
+// Row-wise backward kernels of liboptimus for gfx950 (training: the
+// gradients of the grouped operators, the training column of Table 3):
+//   - grouped activation backward   dx = dy * act'(x)
+//   - grouped LayerNorm backward    dx = rstd (g - mean(g) - xhat mean(g xhat)),
+//                                   g = dy * gamma, xhat = (x - mean) rstd,
+//                                   dgamma = sum_rows dy xhat, dbeta = sum_rows dy
+//   - the finalize of dgamma / dbeta over the per-tile column partials
+// The row mapping is the forward's: L lanes per row, a wave 64 / L rows, a
+// block of four waves consecutive row slots, 16-byte chunks; the statistics
+// are recomputed from x in fp32 (two passes) as the forward takes them.
+#include "device_common.h"
+
+namespace optimus {
+
+// Derivative of one activation at its input, in the same hardware
+// exponential / reciprocal forms as the forward activations.
+template <int ACT>
+__device__ __forceinline__ float act_grad(float x) {
+  if constexpr (ACT == OPTIMUS_ACT_RELU) {
+    return x > 0.f ? 1.f : 0.f;
+  } else if constexpr (ACT == OPTIMUS_ACT_SIGMOID) {
+    const float s = fast_rcp(1.f + fast_exp(-x));
+    return s * (1.f - s);
+  } else if constexpr (ACT == OPTIMUS_ACT_TANH) {
+    const float t = 1.f - 2.f * fast_rcp(fast_exp(2.f * x) + 1.f);
+    return 1.f - t * t;
+  } else if constexpr (ACT == OPTIMUS_ACT_SILU) {
+    const float s = fast_rcp(1.f + fast_exp(-x));
+    return s + x * s * (1.f - s);
+  } else {
+    return 1.f;
+  }
+}
+
+// ===================================================================== activation
+template <typename T, int ACT>
+__global__ __launch_bounds__(kRowThreads) void grouped_act_backward_kernel(const DevRowsGrad* __restrict__ descs,
+                                                                           const RowTile* __restrict__ tiles,
+                                                                           int32_t num_tiles) {
+  constexpr int VEC = Elem<T>::VEC;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
+    const RowTile rt = tiles[t];
+    const DevRowsGrad d = descs[rt.member];
+    const int end = rt.row0 + rt.nrows;
+    if (d.vec) {
+      const int L = d.lanes, rpw = 64 / L, sub = lane / L, li = lane & (L - 1);
+      const int cpr = d.cols / VEC;
+      for (int r = rt.row0 + wave * rpw + sub; r < end; r += 4 * rpw) {
+        const char* xr = (const char*)d.x + (int64_t)r * d.ldx * sizeof(T);
+        const char* gr = (const char*)d.dy + (int64_t)r * d.lddy * sizeof(T);
+        char* orow = (char*)d.dx + (int64_t)r * d.lddx * sizeof(T);
+        int c = li;
+        for (; c + L < cpr; c += 2 * L) {
+          u32x4 xv[2], gv[2];
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            xv[u] = ld16_nt(xr + (int64_t)(c + u * L) * 16);
+            gv[u] = ld16_nt(gr + (int64_t)(c + u * L) * 16);
+          }
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            float a[VEC], g[VEC];
+            Elem<T>::unpack(xv[u], a);
+            Elem<T>::unpack(gv[u], g);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) a[e] = g[e] * act_grad<ACT>(a[e]);
+            st16_nt(orow + (int64_t)(c + u * L) * 16, Elem<T>::pack(a));
+          }
+        }
+        for (; c < cpr; c += L) {
+          float a[VEC], g[VEC];
+          Elem<T>::unpack(ld16_nt(xr + (int64_t)c * 16), a);
+          Elem<T>::unpack(ld16_nt(gr + (int64_t)c * 16), g);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) a[e] = g[e] * act_grad<ACT>(a[e]);
+          st16_nt(orow + (int64_t)c * 16, Elem<T>::pack(a));
+        }
+      }
+    } else {
+      for (int r = rt.row0 + wave; r < end; r += 4) {
+        const int64_t xo = (int64_t)r * d.ldx, go = (int64_t)r * d.lddy, oo = (int64_t)r * d.lddx;
+        for (int c = lane; c < d.cols; c += 64)
+          Elem<T>::store1(d.dx, oo + c, Elem<T>::load1(d.dy, go + c) * act_grad<ACT>(Elem<T>::load1(d.x, xo + c)));
+      }
+    }
+  }
+}
+
+// ===================================================================== LayerNorm
+// 16-byte path: the row's chunks in registers (MAXC per lane), as the forward.
+// Each lane keeps its columns' dgamma / dbeta sums over the rows it handles;
+// at the end of the tile they are added into sPart ([2][cols] in LDS) and the
+// tile's partial row leaves in one coalesced pass.
+template <typename T, int MAXC>
+__device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile& rt, int lane, int wave,
+                                             float* sPart) {
+  constexpr int VEC = Elem<T>::VEC;
+  const int L = d.lanes;
+  const int rpw = 64 / L;
+  const int sub = lane / L;
+  const int li = lane & (L - 1);
+  const int cpr = d.cols / VEC;
+  const bool params = d.want_params != 0;
+  float gm[MAXC][VEC];
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int c = j * L + li;
+    if (d.gamma && c < cpr) {
+      Elem<T>::unpack(ld16((const char*)d.gamma + (int64_t)c * 16), gm[j]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) gm[j][e] = 1.f;
+    }
+  }
+  float accG[MAXC][VEC], accB[MAXC][VEC];
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) accG[j][e] = accB[j][e] = 0.f;
+  const int end = rt.row0 + rt.nrows;
+  for (int r = rt.row0 + wave * rpw + sub; r - sub - wave * rpw < end; r += 4 * rpw) {
+    // every lane of the wave runs the loop the same number of times (the
+    // lane-group sums need all 64); rows past the tile contribute nothing
+    const bool valid = r < end;
+    const char* xr = (const char*)d.x + (int64_t)r * d.ldx * sizeof(T);
+    const char* gr = (const char*)d.dy + (int64_t)r * d.lddy * sizeof(T);
+    float x[MAXC][VEC], g[MAXC][VEC];
+    {
+      u32x4 rx[MAXC], rg[MAXC];
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        const int c = j * L + li;
+        const bool in = valid && c < cpr;
+        rx[j] = in ? ld16_nt(xr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
+        rg[j] = in ? ld16_nt(gr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        Elem<T>::unpack(rx[j], x[j]);
+        Elem<T>::unpack(rg[j], g[j]);
+      }
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) s += x[j][e];
+    const float mean = group_sum(s, L) * d.inv_cols;
+    float q = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const bool in = valid && (j * L + li) < cpr;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        x[j][e] -= mean;
+        q += in ? x[j][e] * x[j][e] : 0.f;
+      }
+    }
+    const float rstd = __builtin_amdgcn_rsqf(group_sum(q, L) * d.inv_cols + d.eps);
+    float sg = 0.f, sgx = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const bool in = valid && (j * L + li) < cpr;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float xh = x[j][e] * rstd;
+        const float gg = g[j][e] * gm[j][e];
+        x[j][e] = xh;
+        sg += in ? gg : 0.f;
+        sgx += in ? gg * xh : 0.f;
+      }
+    }
+    const float mg = group_sum(sg, L) * d.inv_cols;
+    const float mgx = group_sum(sgx, L) * d.inv_cols;
+    char* orow = (char*)d.dx + (int64_t)r * d.lddx * sizeof(T);
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = j * L + li;
+      if (valid && c < cpr) {
+        float o[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          o[e] = rstd * (g[j][e] * gm[j][e] - mg - x[j][e] * mgx);
+          accG[j][e] += g[j][e] * x[j][e];
+          accB[j][e] += g[j][e];
+        }
+        st16_nt(orow + (int64_t)c * 16, Elem<T>::pack(o));
+      }
+    }
+  }
+  if (params) {
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = j * L + li;
+      if (c < cpr) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          atomicAdd(&sPart[c * VEC + e], accG[j][e]);
+          atomicAdd(&sPart[d.cols + c * VEC + e], accB[j][e]);
+        }
+      }
+    }
+  }
+}
+
+// Any shape, any alignment: one wave per row, four passes over global memory;
+// the wave's dgamma / dbeta sums go to its own partial row (written by its
+// first row, added to by the next ones: only this wave touches it).
+template <typename T>
+__device__ __forceinline__ void lnb_rows_scalar(const DevRowsGrad& d, const RowTile& rt, int lane, int wave) {
+  const int end = rt.row0 + rt.nrows;
+  const bool params = d.want_params != 0;
+  float* pg = d.part + (int64_t)(d.part0 + rt.pad * kGradWavesPerBlock + wave) * 2 * d.cols;
+  float* pb = pg + d.cols;
+  bool first = true;
+  for (int r = rt.row0 + wave; r < end; r += 4) {
+    const int64_t xo = (int64_t)r * d.ldx, go = (int64_t)r * d.lddy, oo = (int64_t)r * d.lddx;
+    float s = 0.f;
+    for (int c = lane; c < d.cols; c += 64) s += Elem<T>::load1(d.x, xo + c);
+    const float mean = group_sum(s, 64) * d.inv_cols;
+    float q = 0.f;
+    for (int c = lane; c < d.cols; c += 64) {
+      const float t = Elem<T>::load1(d.x, xo + c) - mean;
+      q += t * t;
+    }
+    const float rstd = __builtin_amdgcn_rsqf(group_sum(q, 64) * d.inv_cols + d.eps);
+    float sg = 0.f, sgx = 0.f;
+    for (int c = lane; c < d.cols; c += 64) {
+      const float gg = Elem<T>::load1(d.dy, go + c) * (d.gamma ? Elem<T>::load1(d.gamma, c) : 1.f);
+      sg += gg;
+      sgx += gg * (Elem<T>::load1(d.x, xo + c) - mean) * rstd;
+    }
+    const float mg = group_sum(sg, 64) * d.inv_cols;
+    const float mgx = group_sum(sgx, 64) * d.inv_cols;
+    // every read of the row's dy is done (the sums above depend on them), so
+    // dx may overwrite dy in place
+    for (int c = lane; c < d.cols; c += 64) {
+      const float xh = (Elem<T>::load1(d.x, xo + c) - mean) * rstd;
+      const float gy = Elem<T>::load1(d.dy, go + c);
+      const float gg = gy * (d.gamma ? Elem<T>::load1(d.gamma, c) : 1.f);
+      Elem<T>::store1(d.dx, oo + c, rstd * (gg - mg - xh * mgx));
+      if (params) {
+        pg[c] = first ? gy * xh : pg[c] + gy * xh;
+        pb[c] = first ? gy : pb[c] + gy;
+      }
+    }
+    first = false;
+  }
+  if (params && first) {  // no row for this wave: its partial row is zero
+    for (int c = lane; c < d.cols; c += 64) {
+      pg[c] = 0.f;
+      pb[c] = 0.f;
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void grouped_layernorm_backward_kernel(
+    const DevRowsGrad* __restrict__ descs, const RowTile* __restrict__ tiles, int32_t num_tiles) {
+  // [2][cols] for the widest row the 16-byte path holds: 64 lanes x the
+  // chunks per lane x the values per chunk
+  constexpr int MAXCOLS = 64 * kLnChunksPerLane * Elem<T>::VEC;
+  __shared__ float sPart[2 * MAXCOLS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
+    const RowTile rt = tiles[t];
+    const DevRowsGrad d = descs[rt.member];
+    if (d.vec && d.lanes > 0) {
+      const bool params = d.want_params != 0;
+      if (params) {
+        for (int i = tid; i < 2 * d.cols; i += kRowThreads) sPart[i] = 0.f;
+        __syncthreads();
+      }
+      lnb_rows_vec<T, kLnChunksPerLane>(d, rt, lane, wave, sPart);
+      if (params) {
+        __syncthreads();
+        float* out = d.part + (int64_t)(d.part0 + rt.pad) * 2 * d.cols;
+        for (int i = tid; i < 2 * d.cols; i += kRowThreads) out[i] = sPart[i];
+        __syncthreads();  // sPart is cleared by the next tile
+      }
+    } else {
+      lnb_rows_scalar<T>(d, rt, lane, wave);
+    }
+  }
+}
+
+// ===================================================================== finalize
+template <typename T>
+__global__ __launch_bounds__(256) void grad_finalize_kernel(const GradFinItem* __restrict__ items, int32_t num_items) {
+  for (int t = blockIdx.x; t < num_items; t += gridDim.x) {
+    const GradFinItem it = items[t];
+    const int c = it.c0 + threadIdx.x;
+    if (c >= it.cols) continue;
+    float sg = 0.f, sb = 0.f;
+    for (int p = 0; p < it.nparts; ++p) {
+      const float* row = it.part + (int64_t)p * 2 * it.cols;
+      sg += row[c];
+      sb += row[it.cols + c];
+    }
+    if (it.dgamma) Elem<T>::store1(it.dgamma, c, sg);
+    if (it.dbeta) Elem<T>::store1(it.dbeta, c, sb);
+  }
+}
+
+// ===================================================================== launchers
+#define OPTIMUS_BWD_ACT_SWITCH(act, ...)                           \
+  switch (act) {                                                   \
+    case OPTIMUS_ACT_NONE: { constexpr int A = 0; __VA_ARGS__; } break;    \
+    case OPTIMUS_ACT_RELU: { constexpr int A = 1; __VA_ARGS__; } break;    \
+    case OPTIMUS_ACT_SIGMOID: { constexpr int A = 2; __VA_ARGS__; } break; \
+    case OPTIMUS_ACT_TANH: { constexpr int A = 3; __VA_ARGS__; } break;    \
+    case OPTIMUS_ACT_SILU: { constexpr int A = 4; __VA_ARGS__; } break;    \
+    default: return hipErrorInvalidValue;                          \
+  }
+
+hipError_t act_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs, const RowTile* tiles,
+                               int32_t num_tiles, int32_t grid, hipStream_t stream) {
+  if (num_tiles <= 0) return hipSuccess;
+  if (dt == OPTIMUS_BF16) {
+    OPTIMUS_BWD_ACT_SWITCH(act, hipLaunchKernelGGL((grouped_act_backward_kernel<bf16_t, A>), dim3(grid),
+                                                   dim3(kRowThreads), 0, stream, descs, tiles, num_tiles));
+  } else {
+    OPTIMUS_BWD_ACT_SWITCH(act, hipLaunchKernelGGL((grouped_act_backward_kernel<float, A>), dim3(grid),
+                                                   dim3(kRowThreads), 0, stream, descs, tiles, num_tiles));
+  }
+  return hipGetLastError();
+}
+
+hipError_t layernorm_backward_launch(optimus_dtype dt, const DevRowsGrad* descs, const RowTile* tiles,
+                                     int32_t num_tiles, int32_t grid, hipStream_t stream) {
+  if (num_tiles <= 0) return hipSuccess;
+  if (dt == OPTIMUS_BF16)
+    hipLaunchKernelGGL(grouped_layernorm_backward_kernel<bf16_t>, dim3(grid), dim3(kRowThreads), 0, stream, descs,
+                       tiles, num_tiles);
+  else
+    hipLaunchKernelGGL(grouped_layernorm_backward_kernel<float>, dim3(grid), dim3(kRowThreads), 0, stream, descs,
+                       tiles, num_tiles);
+  return hipGetLastError();
+}
+
+hipError_t grad_finalize_launch(optimus_dtype dt, const GradFinItem* items, int32_t num_items, int32_t grid,
+                                hipStream_t stream) {
+  if (num_items <= 0) return hipSuccess;
+  if (dt == OPTIMUS_BF16)
+    hipLaunchKernelGGL(grad_finalize_kernel<bf16_t>, dim3(grid), dim3(256), 0, stream, items, num_items);
+  else
+    hipLaunchKernelGGL(grad_finalize_kernel<float>, dim3(grid), dim3(256), 0, stream, items, num_items);
+  return hipGetLastError();
+}
+
+}  // namespace optimus

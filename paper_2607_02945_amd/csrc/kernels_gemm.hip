@@ -22,6 +22,8 @@
 
 namespace optimus {
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
 template <typename T>
 struct Mfma;
 
@@ -95,6 +97,74 @@ __device__ __forceinline__ u32x4 load_chunk(const void* base, int64_t ld, int ro
     }
   }
   return v;
+}
+
+// ----------------------------------------------------------------- transposed operands
+// An operand stored reduction-major (element (row, k) at base[k * ld + row]):
+// the gradients dX = dY . W and dW = dY^T . X read W and X, dY across their
+// rows. A thread loads KB reduction rows of one 16-byte chunk (VEC tile rows)
+// and writes VEC pieces of KB reduction-consecutive values into the same
+// [row][k] LDS layout the MFMA fragment reads use: for bf16 four rows, and the
+// 4 x 8 block is transposed with two byte permutes per output word.
+template <typename T>
+struct Trans;
+template <>
+struct Trans<bf16_t> {
+  static constexpr int KB = 4;
+};
+template <>
+struct Trans<float> {
+  static constexpr int KB = 2;
+};
+
+// One 16-byte chunk of tile rows row..row+VEC-1 at reduction index k, zero
+// past nrows or K. `vec`: the chunk is 16-byte aligned (ld % VEC == 0 and an
+// aligned base).
+template <typename T>
+__device__ __forceinline__ u32x4 load_chunk_t(const void* base, int64_t ld, int row, int nrows, int k, int K,
+                                              bool vec) {
+  constexpr int VEC = Elem<T>::VEC;
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (k < K && row < nrows) {
+    const T* p = (const T*)base + (int64_t)k * ld + row;
+    if (vec && row + VEC <= nrows) {
+      v = ld16(p);
+    } else {
+      float f[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) f[e] = (row + e < nrows) ? Elem<T>::load1(p, e) : 0.f;
+      v = Elem<T>::pack(f);
+    }
+  }
+  return v;
+}
+
+// v[j]: reduction row k0 + j of the chunk; dst: LDS element (row0, k0) of the
+// [row][k] layout with row pitch LDK. Also adds each tile row's KB values to
+// rs[] when `sum` (the row sums of the x operand: db for dW = dY^T X).
+__device__ __forceinline__ void store_trans(const u32x4 (&v)[4], bf16_t* dst, int LDK, bool sum, float (&rs)[8]) {
+  const uint32_t r0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, r1[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
+  const uint32_t r2[4] = {v[2].x, v[2].y, v[2].z, v[2].w}, r3[4] = {v[3].x, v[3].y, v[3].z, v[3].w};
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const u32x2 lo = {__builtin_amdgcn_perm(r1[p], r0[p], 0x05040100u), __builtin_amdgcn_perm(r3[p], r2[p], 0x05040100u)};
+    const u32x2 hi = {__builtin_amdgcn_perm(r1[p], r0[p], 0x07060302u), __builtin_amdgcn_perm(r3[p], r2[p], 0x07060302u)};
+    *(u32x2*)(dst + (2 * p) * LDK) = lo;
+    *(u32x2*)(dst + (2 * p + 1) * LDK) = hi;
+    if (sum) {
+      rs[2 * p] += (bf16_lo(r0[p]) + bf16_lo(r1[p])) + (bf16_lo(r2[p]) + bf16_lo(r3[p]));
+      rs[2 * p + 1] += (bf16_hi(r0[p]) + bf16_hi(r1[p])) + (bf16_hi(r2[p]) + bf16_hi(r3[p]));
+    }
+  }
+}
+__device__ __forceinline__ void store_trans(const u32x4 (&v)[2], float* dst, int LDK, bool sum, float (&rs)[4]) {
+  const f32x4 a = __builtin_bit_cast(f32x4, v[0]), b = __builtin_bit_cast(f32x4, v[1]);
+  const float fa[4] = {a[0], a[1], a[2], a[3]}, fb[4] = {b[0], b[1], b[2], b[3]};
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    *(f32x2*)(dst + c * LDK) = f32x2{fa[c], fb[c]};
+    if (sum) rs[c] += fa[c] + fb[c];
+  }
 }
 
 // Fused LayerNorm over each output row of a tile that holds whole rows
@@ -304,12 +374,24 @@ __device__ __forceinline__ void gemm_epilogue(const f32x16 (&acc)[BM / WM / 32][
   }
 }
 
-template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES, int ACT>
+// TR bit 0: x stored reduction-major; bit 1: w stored reduction-major (the
+// transposed operands of the backward GEMMs). With bit 0 set and d.xsum
+// given, the tiles of the first column block also write the row sums of x
+// over the whole reduction (db beside dW = dY^T X).
+template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES, int ACT, int TR = 0>
 __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLinear* __restrict__ descs,
                                                                    const GemmTile* __restrict__ tiles,
                                                                    int32_t num_tiles) {
   using S = GemmShape<T, BM, BN, BK, WM, WN, STAGES>;
   constexpr int VEC = S::VEC, NT = S::NT, CPR = S::CPR, LDK = S::LDK;
+  constexpr bool TX = (TR & 1) != 0, TW = (TR & 2) != 0;
+  constexpr int KB = Trans<T>::KB;
+  // transposed operands: (rows / VEC) x (BK / KB) blocks, whole blocks per thread
+  constexpr int LXT = (BM / VEC) * (BK / KB) / NT, LWT = (BN / VEC) * (BK / KB) / NT;
+  static_assert(!TX || (LXT >= 1 && LXT * NT == (BM / VEC) * (BK / KB)), "transposed x staging must divide evenly");
+  static_assert(!TW || (LWT >= 1 && LWT * NT == (BN / VEC) * (BK / KB)), "transposed w staging must divide evenly");
+  static_assert(!TX || (size_t)(BK / KB) * BM * sizeof(float) <= S::LDS_MAIN, "row-sum partials must fit");
+  constexpr int NRX = TX ? LXT * KB : S::LX, NRW = TW ? LWT * KB : S::LW;
   extern __shared__ __align__(16) char smem[];
   T* sAB = (T*)smem;                                       // [STAGES][(BM + BN) * LDK]: x rows then w rows
   T* sC = (T*)smem;                                        // [BM][LDC] staging, reuses the A/B area
@@ -337,8 +419,15 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
     const int m0 = tile.mb * BM, n0 = tile.nb * BN;
     const int Mr = d.M - m0, Nr = d.N - n0;  // rows / columns left in this tile (may exceed BM / BN)
     const bool vin = d.vec & 1;
-    const T* xb = (const T*)d.x + (int64_t)m0 * d.ldx;
-    const T* wb = (const T*)d.w + (int64_t)n0 * d.ldw;
+    const bool vw = TW ? (d.vec & 4) != 0 : vin;
+    const T* xb = TX ? (const T*)d.x + m0 : (const T*)d.x + (int64_t)m0 * d.ldx;
+    const T* wb = TW ? (const T*)d.w + n0 : (const T*)d.w + (int64_t)n0 * d.ldw;
+    const bool want_sum = TX && d.xsum && tile.nb == 0;
+    float xs[TX ? LXT : 1][VEC];
+#pragma unroll
+    for (int i = 0; i < (TX ? LXT : 1); ++i)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) xs[i][e] = 0.f;
 
     load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
 
@@ -350,31 +439,72 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    u32x4 rx[S::LX], rw[S::LW];
+    u32x4 rx[NRX], rw[NRW];
     auto gload = [&](int k0) {
+      if constexpr (TX) {
 #pragma unroll
-      for (int i = 0; i < S::LX; ++i) {
-        const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-        rx[i] = load_chunk<T>(xb, d.ldx, row, Mr, k0 + c * VEC, d.K, vin);
+        for (int i = 0; i < LXT; ++i) {
+          const int idx = tid + i * NT, rg = idx % (BM / VEC), kq = idx / (BM / VEC);
+#pragma unroll
+          for (int j = 0; j < KB; ++j) rx[i * KB + j] = load_chunk_t<T>(xb, d.ldx, rg * VEC, Mr, k0 + kq * KB + j, d.K, vin);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < S::LX; ++i) {
+          const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
+          rx[i] = load_chunk<T>(xb, d.ldx, row, Mr, k0 + c * VEC, d.K, vin);
+        }
       }
+      if constexpr (TW) {
 #pragma unroll
-      for (int i = 0; i < S::LW; ++i) {
-        const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-        rw[i] = load_chunk<T>(wb, d.ldw, row, Nr, k0 + c * VEC, d.K, vin);
+        for (int i = 0; i < LWT; ++i) {
+          const int idx = tid + i * NT, rg = idx % (BN / VEC), kq = idx / (BN / VEC);
+#pragma unroll
+          for (int j = 0; j < KB; ++j) rw[i * KB + j] = load_chunk_t<T>(wb, d.ldw, rg * VEC, Nr, k0 + kq * KB + j, d.K, vw);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < S::LW; ++i) {
+          const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
+          rw[i] = load_chunk<T>(wb, d.ldw, row, Nr, k0 + c * VEC, d.K, vin);
+        }
       }
     };
     auto lstore = [&](int stage) {
       T* sx = sAB + stage * S::STAGE_ELEMS;
       T* sw = sx + BM * LDK;
+      if constexpr (TX) {
 #pragma unroll
-      for (int i = 0; i < S::LX; ++i) {
-        const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-        *(u32x4*)(sx + row * LDK + c * VEC) = rx[i];
+        for (int i = 0; i < LXT; ++i) {
+          const int idx = tid + i * NT, rg = idx % (BM / VEC), kq = idx / (BM / VEC);
+          u32x4 blk[KB];
+#pragma unroll
+          for (int j = 0; j < KB; ++j) blk[j] = rx[i * KB + j];
+          store_trans(blk, sx + rg * VEC * LDK + kq * KB, LDK, want_sum, xs[i]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < S::LX; ++i) {
+          const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
+          *(u32x4*)(sx + row * LDK + c * VEC) = rx[i];
+        }
       }
+      if constexpr (TW) {
+        float unused[VEC];
 #pragma unroll
-      for (int i = 0; i < S::LW; ++i) {
-        const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-        *(u32x4*)(sw + row * LDK + c * VEC) = rw[i];
+        for (int i = 0; i < LWT; ++i) {
+          const int idx = tid + i * NT, rg = idx % (BN / VEC), kq = idx / (BN / VEC);
+          u32x4 blk[KB];
+#pragma unroll
+          for (int j = 0; j < KB; ++j) blk[j] = rw[i * KB + j];
+          store_trans(blk, sw + rg * VEC * LDK + kq * KB, LDK, false, unused);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < S::LW; ++i) {
+          const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
+          *(u32x4*)(sw + row * LDK + c * VEC) = rw[i];
+        }
       }
     };
     auto compute = [&](int stage) {
@@ -416,6 +546,25 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       }
     }
 
+    if constexpr (TX) {
+      if (want_sum) {
+        // row sums of x: per-thread partials over (kq, rows) -> LDS -> one sum per tile row
+        float* part = (float*)smem;  // [BK / KB][BM], the operand area is free after the K loop
+#pragma unroll
+        for (int i = 0; i < LXT; ++i) {
+          const int idx = tid + i * NT, rg = idx % (BM / VEC), kq = idx / (BM / VEC);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) part[kq * BM + rg * VEC + e] = xs[i][e];
+        }
+        __syncthreads();
+        for (int r = tid; r < BM && r < Mr; r += NT) {
+          float sum = 0.f;
+          for (int q = 0; q < BK / KB; ++q) sum += part[q * BM + r];
+          Elem<T>::store1(d.xsum, m0 + r, sum);
+        }
+        __syncthreads();
+      }
+    }
     if constexpr (LN) ln_rows<BM, BN, WM, WN>(acc, sBias, sGamma, sBeta, red, d);
     gemm_epilogue<T, BM, BN, WM, WN, S::LDC, ACT>(acc, sC, sBias, d, m0, n0, Mr, Nr);
     __syncthreads();  // staging and bias reads done before the next tile overwrites them
@@ -1158,6 +1307,20 @@ static hipError_t launch_shape(optimus_act act, bool ln, const DevLinear* descs,
   return hipGetLastError();
 }
 
+// Backward GEMM instances: no bias, no activation, no LayerNorm.
+template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
+static hipError_t launch_trans(int tr, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
+                               hipStream_t stream, int* occ) {
+  using S = GemmShape<T, BM, BN, BK, WM, WN, STAGES>;
+  if (tr == 2)
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, 0, 2>), S::LDS_BYTES, S::NT)
+  else if (tr == 3)
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, 0, 3>), S::LDS_BYTES, S::NT)
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int WM, int WN>
 static hipError_t launch_dma(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
                              int32_t grid, hipStream_t stream, int* occ) {
@@ -1180,9 +1343,19 @@ static hipError_t launch_dma(optimus_act act, bool ln, const DevLinear* descs, c
 }
 #undef OPTIMUS_LAUNCH_ONE
 
-static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln,
+static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, int tr,
                                 const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
                                 hipStream_t stream, int* occ) {
+  if (tr) {
+    if (ln || act != OPTIMUS_ACT_NONE) return hipErrorInvalidValue;
+    switch (cfg.variant) {
+      case 1: return launch_trans<bf16_t, 128, 128, 64, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
+      case 2: return launch_trans<bf16_t, 256, 256, 64, 2, 4, 2>(tr, descs, tiles, n, grid, stream, occ);
+      case 3: return launch_trans<float, 64, 64, 32, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
+      case 6: return launch_trans<float, 64, 128, 64, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (cfg.variant) {
     case 0: return launch_shape<bf16_t, 128, 64, 64, 4, 1, 1>(act, ln, descs, tiles, n, grid, stream, occ);
     case 1: return launch_shape<bf16_t, 128, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
@@ -1200,14 +1373,28 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
 }
 
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
-                       const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream) {
+                       const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream, int tr) {
   if (num_tiles <= 0) return hipSuccess;
-  return gemm_dispatch(cfg, dt, act, ln, descs, tiles, num_tiles, grid, stream, nullptr);
+  return gemm_dispatch(cfg, dt, act, ln, tr, descs, tiles, num_tiles, grid, stream, nullptr);
 }
 
-int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln) {
+// Backward GEMMs (transposed operands): the register-staged tiles -- 256x256
+// from half a tile per CU on, else 128x128; fp32 64x64.
+GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G) {
+  double tiles256 = 0.0;
+  for (int g = 0; g < G; ++g) tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
+  int v = dt == OPTIMUS_F32 ? 3 : (tiles256 >= 0.5 * device_cu_count() ? 2 : 1);
+  const char* f = getenv("OPTIMUS_GEMM_VARIANT");
+  char* end = nullptr;
+  const long want = f ? strtol(f, &end, 10) : -1;
+  if (f && end && *end == 0 && (dt == OPTIMUS_F32 ? (want == 3 || want == 6) : (want == 1 || want == 2))) v = (int)want;
+  const GemmVariant& k = kVariants[v];
+  return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
+}
+
+int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, int tr) {
   int occ = 0;
-  if (gemm_dispatch(cfg, dt, act, ln, nullptr, nullptr, 0, 0, nullptr, &occ) != hipSuccess || occ < 1) {
+  if (gemm_dispatch(cfg, dt, act, ln, tr, nullptr, nullptr, 0, 0, nullptr, &occ) != hipSuccess || occ < 1) {
     (void)hipGetLastError();
     return cfg.occ;
   }

@@ -257,6 +257,95 @@ extern "C" optimus_status optimus_validate_split_op_cat(const optimus_split_op_c
   return check_aliasing(regs, true, "split_op_cat");
 }
 
+extern "C" optimus_status optimus_validate_linear_backward(const optimus_linear_grad_desc* d, int32_t G,
+                                                          optimus_dtype dt) {
+  const char* what = "grouped_linear_backward";
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: G = %d < 0", what, G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown dtype %d", what, (int)dt);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: descriptor array is NULL", what);
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 6);
+  for (int g = 0; g < G; ++g) {
+    const optimus_linear_grad_desc& m = d[g];
+    if (!m.dy) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a NULL dy", what, g);
+    if (m.dx && !m.w) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d wants dx but has a NULL w", what, g);
+    if (m.dw && !m.x) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d wants dw but has a NULL x", what, g);
+    if (m.db && !m.dw)
+      return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: member %d wants db without dw (db is summed by the dW launch)", what, g);
+    if (m.M < 1 || m.N < 1 || m.K < 1 || m.M > kMaxDim || m.N > kMaxDim || m.K > kMaxDim)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has M=%lld N=%lld K=%lld (need 1..2^31-1)", what, g,
+                  (long long)m.M, (long long)m.N, (long long)m.K);
+    if (m.lddy < m.N || (m.dw && m.ldx < m.K) || (m.dx && m.ldw < m.K) || (m.dx && m.lddx < m.K) ||
+        (m.dw && m.lddw < m.K))
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a row stride below its row length", what, g);
+    regs.push_back(region(m.dy, m.lddy, m.M, m.N, s, g, false));
+    if (m.dw) regs.push_back(region(m.x, m.ldx, m.M, m.K, s, g, false));
+    if (m.dx) regs.push_back(region(m.w, m.ldw, m.N, m.K, s, g, false));
+    if (m.dx) regs.push_back(region(m.dx, m.lddx, m.M, m.K, s, g, true));
+    if (m.dw) regs.push_back(region(m.dw, m.lddw, m.N, m.K, s, g, true));
+    if (m.db) regs.push_back(region(m.db, m.N, 1, m.N, s, g, true));
+  }
+  return check_aliasing(regs, false, what);
+}
+
+extern "C" optimus_status optimus_validate_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G,
+                                                             optimus_dtype dt) {
+  const char* what = "grouped_layernorm_backward";
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: G = %d < 0", what, G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown dtype %d", what, (int)dt);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: descriptor array is NULL", what);
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 6);
+  for (int g = 0; g < G; ++g) {
+    const optimus_layernorm_grad_desc& m = d[g];
+    if (!m.x || !m.dy || !m.dx) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a NULL x/dy/dx", what, g);
+    if (m.rows < 1 || m.cols < 1 || m.rows > kMaxDim || m.cols > kMaxDim)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has rows=%lld cols=%lld", what, g, (long long)m.rows,
+                  (long long)m.cols);
+    if (m.ldx < m.cols || m.lddy < m.cols || m.lddx < m.cols)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a row stride below cols", what, g);
+    if (!(m.eps >= 0.f) || !std::isfinite(m.eps))
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has eps=%g", what, g, (double)m.eps);
+    regs.push_back(region(m.x, m.ldx, m.rows, m.cols, s, g, false));
+    regs.push_back(region(m.dy, m.lddy, m.rows, m.cols, s, g, false));
+    if (m.gamma) regs.push_back(region(m.gamma, m.cols, 1, m.cols, s, g, false));
+    regs.push_back(region(m.dx, m.lddx, m.rows, m.cols, s, g, true));
+    if (m.dgamma) regs.push_back(region(m.dgamma, m.cols, 1, m.cols, s, g, true));
+    if (m.dbeta) regs.push_back(region(m.dbeta, m.cols, 1, m.cols, s, g, true));
+  }
+  return check_aliasing(regs, true, what);
+}
+
+extern "C" optimus_status optimus_validate_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt,
+                                                        optimus_act act) {
+  const char* what = "grouped_act_backward";
+  if (G < 0) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: G = %d < 0", what, G);
+  if (!dtype_ok(dt)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown dtype %d", what, (int)dt);
+  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown activation %d", what, (int)act);
+  if (G == 0) return OPTIMUS_OK;
+  if (!d) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: descriptor array is NULL", what);
+  const size_t s = dtype_size(dt);
+  std::vector<Region> regs;
+  regs.reserve((size_t)G * 3);
+  for (int g = 0; g < G; ++g) {
+    const optimus_act_grad_desc& m = d[g];
+    if (!m.x || !m.dy || !m.dx) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a NULL x/dy/dx", what, g);
+    if (m.rows < 1 || m.cols < 1 || m.rows > kMaxDim || m.cols > kMaxDim)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has rows=%lld cols=%lld", what, g, (long long)m.rows,
+                  (long long)m.cols);
+    if (m.ldx < m.cols || m.lddy < m.cols || m.lddx < m.cols)
+      return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a row stride below cols", what, g);
+    regs.push_back(region(m.x, m.ldx, m.rows, m.cols, s, g, false));
+    regs.push_back(region(m.dy, m.lddy, m.rows, m.cols, s, g, false));
+    regs.push_back(region(m.dx, m.lddx, m.rows, m.cols, s, g, true));
+  }
+  return check_aliasing(regs, true, what);
+}
+
 static optimus_status validate_fp8_member(const char* what, int g, const void* a, int64_t lda, size_t sa,
                                           const void* b, int64_t ldb, size_t sb, int64_t rows, int64_t cols) {
   if (!a || !b) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d has a NULL tensor", what, g);
@@ -318,7 +407,10 @@ extern "C" optimus_status optimus_validate_dequantize_fp8(const optimus_fp8_dequ
 // A HostPlan is everything a launch needs, built on the host: a byte blob that
 // becomes the device table, offsets into it, device-to-device copies to run
 // after the upload (packing per-piece gamma/beta), and launch parameters.
-enum Kind { KIND_LINEAR = 0, KIND_LN = 1, KIND_PW = 2, KIND_SOC = 3, KIND_Q8 = 5, KIND_DQ8 = 6 };
+enum Kind {
+  KIND_LINEAR = 0, KIND_LN = 1, KIND_PW = 2, KIND_SOC = 3, KIND_Q8 = 5, KIND_DQ8 = 6, KIND_LINBWD = 7,
+  KIND_LNBWD = 8, KIND_ACTBWD = 9
+};
 
 struct Blob {
   std::vector<char> bytes;
@@ -342,6 +434,18 @@ struct RowLaunch {
   int32_t first_tile, num_tiles, grid;
 };
 
+// One grouped GEMM launch: tile shape, operand layout (tr: 0 forward, 2 / 3
+// the backward GEMMs), member table, tile list, grid, and per member of the
+// plan's group its tile range for a CHAIN launch (empty if it has none here).
+struct GemmSet {
+  GemmConfig cfg{};
+  int tr = 0;
+  size_t descs_off = 0, tiles_off = 0;
+  int32_t num_tiles = 0, grid = 0;
+  int64_t real_tiles = 0;
+  std::vector<RowLaunch> chain;
+};
+
 struct HostPlan {
   Kind kind;
   optimus_dtype dt;
@@ -350,11 +454,9 @@ struct HostPlan {
   Blob blob;
   std::vector<D2DCopy> copies;
   // GEMM
-  GemmConfig gcfg{};
+  GemmSet gs[2];       // forward: gs[0]; backward: dX in gs[0], dW (+ db) in gs[1]
+  int n_gs = 0;
   bool g_ln = false;  // the row LayerNorm is fused into the GEMM epilogue
-  size_t g_descs_off = 0, g_tiles_off = 0;
-  int32_t g_num_tiles = 0, g_grid = 0;
-  std::vector<RowLaunch> g_chain;  // per member: tiles range of the same table
   // row-wise (LN / PW, or the split-op-cat fallbacks)
   int row_kernel = KIND_LN;  // which row kernel the grouped launch uses
   optimus_act row_act = OPTIMUS_ACT_NONE;
@@ -372,6 +474,12 @@ struct HostPlan {
   std::vector<int32_t> soc_piece_first, soc_piece_count;  // per piece: tile range in soc_tiles
   int32_t soc_piece_tiles_total = 0;
   std::vector<size_t> soc_temp_fixups;  // blob offsets of DevRows pointers relative to the temp base
+  // pointer fields of the blob that hold a blob offset, rebased to the device table
+  std::vector<size_t> table_fixups;
+  // row-wise backward: the main launch (rows / rows_chain) and the dgamma /
+  // dbeta finalize of a LayerNorm backward
+  RowLaunch fin{};
+  std::vector<RowLaunch> fin_chain;
   // fp8 codec: member table, item lists (grouped launches, then per member
   // the items of its CHAIN launches), and for scaled quantize the amax slots
   bool q_scaled = false;
@@ -465,6 +573,46 @@ static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool l
   hp.chain_launches = (int32_t)members.size();
 }
 
+// Tile list of one grouped GEMM over `descs` (ids[i]: the plan-group member
+// descs[i] belongs to): heavy members first (tile cost grows with K),
+// member-major, M-blocks then N-blocks, padded to a multiple of 8; the
+// persistent grid is no larger than what is resident at once (a workgroup
+// that had to wait for a free slot would start its whole share late).
+static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int tr, const std::vector<DevLinear>& descs,
+                           const std::vector<int>& ids, int group_size, optimus_act act, bool ln) {
+  const int n = (int)descs.size();
+  gs.cfg = cfg;
+  gs.tr = tr;
+  std::vector<int> order(n);
+  for (int i = 0; i < n; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return descs[a].K > descs[b].K; });
+  std::vector<GemmTile> tiles;
+  gs.chain.assign(group_size, RowLaunch{});
+  const int bm = cfg.bm, bn = cfg.bn;
+  for (int i : order) {
+    const int first = (int)tiles.size();
+    const int64_t mbs = (descs[i].M + bm - 1) / bm, nbs = (descs[i].N + bn - 1) / bn;
+    for (int64_t mb = 0; mb < mbs; ++mb)
+      for (int64_t nb = 0; nb < nbs; ++nb) tiles.push_back(GemmTile{i, (int32_t)mb, (int32_t)nb, 0});
+    gs.chain[ids[i]].first_tile = first;
+    gs.chain[ids[i]].num_tiles = (int)tiles.size() - first;
+  }
+  gs.real_tiles = (int64_t)tiles.size();
+  while (tiles.size() % 8) tiles.push_back(GemmTile{-1, 0, 0, 0});
+  gs.descs_off = hp.blob.add(descs.data(), descs.size() * sizeof(DevLinear));
+  gs.tiles_off = hp.blob.add(tiles.data(), tiles.size() * sizeof(GemmTile));
+  gs.num_tiles = (int32_t)tiles.size();
+  const int64_t cap = (int64_t)device_cu_count() * gemm_resident_per_cu(cfg, hp.dt, act, ln, tr);
+  int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
+  if (grid >= 8) grid -= grid % 8;
+  gs.grid = (int32_t)std::max<int64_t>(1, grid);
+  for (auto& c : gs.chain) {
+    c.descs_off = gs.descs_off;
+    c.tiles_off = gs.tiles_off;
+    c.grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(c.num_tiles, cap));
+  }
+}
+
 static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
                                    HostPlan& hp, bool ln = false, const void* const* gamma = nullptr,
                                    const void* const* beta = nullptr, float eps = 0.f) {
@@ -473,7 +621,6 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
   hp.kind = KIND_LINEAR; hp.dt = dt; hp.act = act; hp.G = G; hp.g_ln = ln;
   const size_t s = dtype_size(dt);
   const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
-  hp.gcfg = gemm_pick_config(dt, d, G, ln);
   std::vector<DevLinear> descs(G);
   for (int g = 0; g < G; ++g) {
     const optimus_linear_desc& m = d[g];
@@ -492,43 +639,241 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
     hp.bytes += (double)s * ((double)m.M * m.K + (double)m.N * m.K + (m.bias ? (double)m.N : 0.0) + (double)m.M * m.N);
     if (ln) hp.bytes += (double)s * ((o.gamma ? (double)m.N : 0.0) + (o.beta ? (double)m.N : 0.0));
   }
-  // heavy members first (tile cost grows with K), member-major, M-blocks then N-blocks
-  std::vector<int> order(G);
-  for (int g = 0; g < G; ++g) order[g] = g;
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return d[a].K > d[b].K; });
-  std::vector<GemmTile> tiles;
-  hp.g_chain.assign(G, RowLaunch{});
-  const int bm = hp.gcfg.bm, bn = hp.gcfg.bn;
-  for (int g : order) {
-    const int first = (int)tiles.size();
-    const int64_t mbs = (d[g].M + bm - 1) / bm, nbs = (d[g].N + bn - 1) / bn;
-    for (int64_t mb = 0; mb < mbs; ++mb)
-      for (int64_t nb = 0; nb < nbs; ++nb) tiles.push_back(GemmTile{g, (int32_t)mb, (int32_t)nb, 0});
-    hp.g_chain[g].first_tile = first;
-    hp.g_chain[g].num_tiles = (int)tiles.size() - first;
-  }
-  const int64_t real_tiles = (int64_t)tiles.size();
-  while (tiles.size() % 8) tiles.push_back(GemmTile{-1, 0, 0, 0});
-  hp.g_descs_off = hp.blob.add(descs.data(), descs.size() * sizeof(DevLinear));
-  hp.g_tiles_off = hp.blob.add(tiles.data(), tiles.size() * sizeof(GemmTile));
-  hp.g_num_tiles = (int32_t)tiles.size();
-  // workgroups resident per CU for each variant (LDS / register bound)
-  // a persistent grid no larger than what is resident at once: a workgroup
-  // that had to wait for a free slot would start its whole share late
-  const int64_t cap = (int64_t)device_cu_count() * gemm_resident_per_cu(hp.gcfg, dt, act, ln);
-  int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
-  if (grid >= 8) grid -= grid % 8;
-  hp.g_grid = (int32_t)std::max<int64_t>(1, grid);
-  for (auto& c : hp.g_chain) {
-    c.descs_off = hp.g_descs_off;
-    c.tiles_off = hp.g_tiles_off;
-    c.grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(c.num_tiles, cap));
-  }
-  hp.work_items = real_tiles;
-  hp.grid = hp.g_grid;
-  hp.block = hp.gcfg.threads;
+  std::vector<int> ids(G);
+  for (int g = 0; g < G; ++g) ids[g] = g;
+  build_gemm_set(hp, hp.gs[0], gemm_pick_config(dt, d, G, ln), 0, descs, ids, G, act, ln);
+  hp.n_gs = 1;
+  hp.work_items = hp.gs[0].real_tiles;
+  hp.grid = hp.gs[0].grid;
+  hp.block = hp.gs[0].cfg.threads;
   hp.chain_launches = G;
-  hp.kernel = std::string(hp.gcfg.name) + (ln ? "_layernorm" : "");
+  hp.kernel = std::string(hp.gs[0].cfg.name) + (ln ? "_layernorm" : "");
+  return OPTIMUS_OK;
+}
+
+// Linear backward as two grouped GEMMs in the forward kernel's terms
+// (y[m][n] = sum_k x[m][k] w[n][k]):
+//   dX: x = dY (as stored), w[n'][k'] = W[k'][n'] (reduction-major), y = dX,
+//       M' = M, N' = K, K' = N
+//   dW: x[m'][k'] = dY[k'][m'] and w[n'][k'] = X[k'][n'] (both
+//       reduction-major), y = dW, M' = N, N' = K, K' = M; the row sums of x
+//       over k' are db.
+static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
+                                            HostPlan& hp) {
+  optimus_status st = optimus_validate_linear_backward(d, G, dt);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_LINBWD; hp.dt = dt; hp.act = OPTIMUS_ACT_NONE; hp.G = G;
+  const size_t s = dtype_size(dt);
+  const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
+  std::vector<DevLinear> dxs, dws;
+  std::vector<int> dx_ids, dw_ids;
+  std::vector<optimus_linear_desc> dx_shape, dw_shape;  // (M', N', K') for the tile picker
+  for (int g = 0; g < G; ++g) {
+    const optimus_linear_grad_desc& m = d[g];
+    if (m.dx) {
+      DevLinear o{};
+      o.x = m.dy; o.ldx = m.lddy; o.w = m.w; o.ldw = m.ldw; o.y = m.dx; o.ldy = m.lddx;
+      o.M = (int32_t)m.M; o.N = (int32_t)m.K; o.K = (int32_t)m.N;
+      const bool vx = m.N % VEC == 0 && m.lddy % VEC == 0 && aligned16(m.dy);
+      const bool vout = m.lddx % VEC == 0 && aligned16(m.dx);
+      const bool vw = m.ldw % VEC == 0 && aligned16(m.w);
+      o.vec = (vx ? 1 : 0) | (vout ? 2 : 0) | (vw ? 4 : 0);
+      o.inv_n = 1.0f / (float)m.K;
+      dxs.push_back(o);
+      dx_ids.push_back(g);
+      optimus_linear_desc sh{};
+      sh.M = m.M; sh.N = m.K; sh.K = m.N;
+      dx_shape.push_back(sh);
+      hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
+      hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K);
+    }
+    if (m.dw) {
+      DevLinear o{};
+      o.x = m.dy; o.ldx = m.lddy; o.w = m.x; o.ldw = m.ldx; o.y = m.dw; o.ldy = m.lddw; o.xsum = m.db;
+      o.M = (int32_t)m.N; o.N = (int32_t)m.K; o.K = (int32_t)m.M;
+      const bool vx = m.lddy % VEC == 0 && aligned16(m.dy);
+      const bool vout = m.lddw % VEC == 0 && aligned16(m.dw);
+      const bool vw = m.ldx % VEC == 0 && aligned16(m.x);
+      o.vec = (vx ? 1 : 0) | (vout ? 2 : 0) | (vw ? 4 : 0);
+      o.inv_n = 1.0f / (float)m.K;
+      dws.push_back(o);
+      dw_ids.push_back(g);
+      optimus_linear_desc sh{};
+      sh.M = m.N; sh.N = m.K; sh.K = m.M;
+      dw_shape.push_back(sh);
+      hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
+      hp.bytes += (double)s * ((double)m.M * m.N + (double)m.M * m.K + (double)m.N * m.K + (m.db ? (double)m.N : 0.0));
+    }
+  }
+  hp.n_gs = 0;
+  hp.work_items = 0;
+  hp.chain_launches = 0;
+  std::string name;
+  if (!dxs.empty()) {
+    GemmSet& gs = hp.gs[hp.n_gs++];
+    build_gemm_set(hp, gs, gemm_pick_config_trans(dt, dx_shape.data(), (int32_t)dx_shape.size()), 2, dxs, dx_ids, G,
+                   OPTIMUS_ACT_NONE, false);
+    name = std::string(gs.cfg.name) + "_dgrad";
+  }
+  if (!dws.empty()) {
+    GemmSet& gs = hp.gs[hp.n_gs++];
+    build_gemm_set(hp, gs, gemm_pick_config_trans(dt, dw_shape.data(), (int32_t)dw_shape.size()), 3, dws, dw_ids, G,
+                   OPTIMUS_ACT_NONE, false);
+    name += std::string(name.empty() ? "" : "+") + gs.cfg.name + "_wgrad";
+  }
+  for (int i = 0; i < hp.n_gs; ++i) {
+    hp.work_items += hp.gs[i].real_tiles;
+    for (const RowLaunch& c : hp.gs[i].chain) hp.chain_launches += c.num_tiles > 0 ? 1 : 0;
+  }
+  hp.launches = std::max(hp.n_gs, 1);
+  hp.grid = hp.n_gs ? hp.gs[0].grid : 0;
+  hp.block = hp.n_gs ? hp.gs[0].cfg.threads : 0;
+  hp.kernel = name.empty() ? "grouped_linear_backward_empty" : name;
+  return OPTIMUS_OK;
+}
+
+// Row-wise backward member: the forward's geometry (lanes per row, the
+// 16-byte path when x, dy, dx (and gamma) rows are 16-byte chunks).
+static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, int64_t lddy, void* dx, int64_t lddx,
+                                  const void* gamma, int64_t rows, int64_t cols, float eps, optimus_dtype dt,
+                                  bool layernorm) {
+  DevRows geo = make_rows(x, ldx, dx, lddx, gamma, nullptr, rows, cols, eps, dt, layernorm);
+  const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
+  const bool dy_ok = lddy % VEC == 0 && aligned16(dy);
+  DevRowsGrad r{};
+  r.x = x; r.dy = dy; r.dx = dx; r.gamma = gamma;
+  r.ldx = ldx; r.lddy = lddy; r.lddx = lddx;
+  r.rows = (int32_t)rows; r.cols = (int32_t)cols;
+  r.vec = geo.vec && dy_ok ? 1 : 0;
+  r.lanes = r.vec ? geo.lanes : 0;
+  r.eps = eps;
+  r.inv_cols = geo.inv_cols;
+  return r;
+}
+
+// Row tiles of every member (pad = the tile's index within its member), the
+// grouped launch and the per-member CHAIN ranges.
+static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
+                                           std::vector<int>& ntiles) {
+  std::vector<RowTile> tiles;
+  hp.rows_chain.clear();
+  ntiles.assign(members.size(), 0);
+  for (size_t g = 0; g < members.size(); ++g) {
+    DevRows geo{};
+    geo.rows = members[g].rows;
+    geo.cols = members[g].cols;
+    geo.vec = members[g].vec;
+    geo.lanes = members[g].vec ? members[g].lanes : 1;
+    const int first = (int)tiles.size();
+    add_row_tiles(tiles, (int)g, geo, s);
+    for (int t = first; t < (int)tiles.size(); ++t) tiles[t].pad = t - first;
+    ntiles[g] = (int)tiles.size() - first;
+    hp.rows_chain.push_back(RowLaunch{0, 0, first, ntiles[g], row_grid(ntiles[g])});
+  }
+  return tiles;
+}
+
+static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
+                                               HostPlan& hp) {
+  optimus_status st = optimus_validate_layernorm_backward(d, G, dt);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_LNBWD; hp.dt = dt; hp.act = OPTIMUS_ACT_NONE; hp.G = G;
+  const size_t s = dtype_size(dt);
+  std::vector<DevRowsGrad> members;
+  for (int g = 0; g < G; ++g) {
+    const optimus_layernorm_grad_desc& m = d[g];
+    members.push_back(make_rows_grad(m.x, m.ldx, m.dy, m.lddy, m.dx, m.lddx, m.gamma, m.rows, m.cols, m.eps, dt, true));
+    members.back().want_params = (m.dgamma || m.dbeta) ? 1 : 0;
+    hp.bytes += (double)s * (3.0 * m.rows * m.cols + (m.gamma ? m.cols : 0) + (m.dgamma ? m.cols : 0) +
+                             (m.dbeta ? m.cols : 0));
+  }
+  std::vector<int> ntiles;
+  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles);
+  // partial rows: one per tile (16-byte path) or per wave (per-value path)
+  int64_t part_rows = 0;
+  std::vector<int> nparts(G, 0);
+  for (int g = 0; g < G; ++g) {
+    if (!members[g].want_params) continue;
+    members[g].part0 = (int32_t)part_rows;
+    nparts[g] = ntiles[g] * (members[g].vec ? 1 : kGradWavesPerBlock);
+    part_rows += nparts[g];
+  }
+  int64_t part_floats = 0;  // offsets in floats of each member's first partial row
+  std::vector<int64_t> part_off(G, 0);
+  for (int g = 0; g < G; ++g) {
+    part_off[g] = part_floats;
+    if (members[g].want_params) part_floats += (int64_t)nparts[g] * 2 * members[g].cols;
+  }
+  // the kernel addresses partial row p of a member at part + p * 2 * cols: give
+  // each member its own base so rows of different widths do not overlap
+  const size_t part_off_blob = hp.blob.add(nullptr, (size_t)std::max<int64_t>(part_floats, 1) * sizeof(float));
+  for (int g = 0; g < G; ++g) {
+    members[g].part = (float*)(uintptr_t)(part_off_blob + (size_t)part_off[g] * sizeof(float));
+    members[g].part0 = 0;
+  }
+  const size_t doff = hp.blob.add(members.data(), members.size() * sizeof(DevRowsGrad));
+  for (int g = 0; g < G; ++g) hp.table_fixups.push_back(doff + g * sizeof(DevRowsGrad) + offsetof(DevRowsGrad, part));
+  const size_t toff = hp.blob.add(tiles.data(), tiles.size() * sizeof(RowTile));
+  for (auto& c : hp.rows_chain) {
+    c.descs_off = doff;
+    c.tiles_off = toff;
+  }
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
+  // finalize items: 256 columns each
+  std::vector<GradFinItem> fin;
+  hp.fin_chain.assign(G, RowLaunch{});
+  for (int g = 0; g < G; ++g) {
+    const int first = (int)fin.size();
+    if (members[g].want_params)
+      for (int c0 = 0; c0 < members[g].cols; c0 += 256)
+        fin.push_back(GradFinItem{(const float*)(uintptr_t)(part_off_blob + (size_t)part_off[g] * sizeof(float)),
+                                  d[g].dgamma, d[g].dbeta, members[g].cols, nparts[g], c0, 0});
+    hp.fin_chain[g] = RowLaunch{0, 0, first, (int)fin.size() - first, 0};
+  }
+  const size_t foff = hp.blob.add(fin.data(), fin.size() * sizeof(GradFinItem));
+  for (size_t i = 0; i < fin.size(); ++i) hp.table_fixups.push_back(foff + i * sizeof(GradFinItem) + offsetof(GradFinItem, part));
+  const int32_t fin_cap = device_cu_count() * 4;
+  hp.fin = RowLaunch{foff, foff, 0, (int32_t)fin.size(), (int32_t)std::max<int64_t>(1, std::min<int64_t>((int64_t)fin.size(), fin_cap))};
+  for (auto& c : hp.fin_chain) {
+    c.descs_off = c.tiles_off = foff;
+    c.grid = std::max(1, std::min(c.num_tiles, fin_cap));
+  }
+  hp.work_items = (int64_t)tiles.size();
+  hp.grid = hp.rows.grid;
+  hp.block = kRowThreads;
+  hp.launches = fin.empty() ? 1 : 2;
+  hp.chain_launches = 0;
+  for (int g = 0; g < G; ++g) hp.chain_launches += 1 + (hp.fin_chain[g].num_tiles > 0 ? 1 : 0);
+  hp.kernel = dt == OPTIMUS_F32 ? "grouped_layernorm_backward_f32" : "grouped_layernorm_backward_bf16";
+  return OPTIMUS_OK;
+}
+
+static optimus_status build_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
+                                         HostPlan& hp) {
+  optimus_status st = optimus_validate_act_backward(d, G, dt, act);
+  if (st != OPTIMUS_OK) return st;
+  hp.kind = KIND_ACTBWD; hp.dt = dt; hp.act = act; hp.G = G;
+  const size_t s = dtype_size(dt);
+  std::vector<DevRowsGrad> members;
+  for (int g = 0; g < G; ++g) {
+    const optimus_act_grad_desc& m = d[g];
+    members.push_back(make_rows_grad(m.x, m.ldx, m.dy, m.lddy, m.dx, m.lddx, nullptr, m.rows, m.cols, 0.f, dt, false));
+    hp.bytes += (double)s * 3.0 * m.rows * m.cols;
+  }
+  std::vector<int> ntiles;
+  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles);
+  const size_t doff = hp.blob.add(members.data(), members.size() * sizeof(DevRowsGrad));
+  const size_t toff = hp.blob.add(tiles.data(), tiles.size() * sizeof(RowTile));
+  for (auto& c : hp.rows_chain) {
+    c.descs_off = doff;
+    c.tiles_off = toff;
+  }
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
+  hp.work_items = (int64_t)tiles.size();
+  hp.grid = hp.rows.grid;
+  hp.block = kRowThreads;
+  hp.chain_launches = G;
+  hp.kernel = dt == OPTIMUS_F32 ? "grouped_act_backward_f32" : "grouped_act_backward_bf16";
   return OPTIMUS_OK;
 }
 
@@ -899,6 +1244,16 @@ static void rebase_soc(HostPlan& hp, char* table) {
   s->tasks = (const SocTask*)(table + (uintptr_t)s->tasks);
 }
 
+// Every pointer the planner stored as a blob offset, made a device address.
+static void rebase_fixups(HostPlan& hp, char* table) {
+  for (size_t off : hp.table_fixups) {
+    uintptr_t v;
+    memcpy(&v, hp.blob.bytes.data() + off, sizeof v);
+    v += (uintptr_t)table;
+    memcpy(hp.blob.bytes.data() + off, &v, sizeof v);
+  }
+}
+
 template <typename P>
 static const P* at(char* table, size_t off) {
   return (const P*)(table + off);
@@ -926,9 +1281,26 @@ static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t st
     case KIND_Q8:
     case KIND_DQ8:
       return launch_fp8(hp, table, &hp.q_amax, hp.q_grouped, stream);
+    case KIND_ACTBWD:
+      return act_backward_launch(hp.dt, hp.act, at<DevRowsGrad>(table, hp.rows.descs_off),
+                                 at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles, hp.rows.grid, stream);
+    case KIND_LNBWD: {
+      hipError_t e = layernorm_backward_launch(hp.dt, at<DevRowsGrad>(table, hp.rows.descs_off),
+                                               at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles,
+                                               hp.rows.grid, stream);
+      if (e != hipSuccess) return e;
+      return grad_finalize_launch(hp.dt, at<GradFinItem>(table, hp.fin.descs_off), hp.fin.num_tiles, hp.fin.grid,
+                                  stream);
+    }
     case KIND_LINEAR:
-      return gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(table, hp.g_descs_off), at<GemmTile>(table, hp.g_tiles_off),
-                         hp.g_num_tiles, hp.g_grid, stream);
+    case KIND_LINBWD:
+      for (int i = 0; i < hp.n_gs; ++i) {
+        const GemmSet& g = hp.gs[i];
+        hipError_t e = gemm_launch(g.cfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(table, g.descs_off),
+                                   at<GemmTile>(table, g.tiles_off), g.num_tiles, g.grid, stream, g.tr);
+        if (e != hipSuccess) return e;
+      }
+      return hipSuccess;
     case KIND_LN:
     case KIND_PW:
     case KIND_SOC:
@@ -967,6 +1339,7 @@ static optimus_status make_plan(HostPlan&& hp, optimus_plan* out) {
     return hip_fail(e, "plan: device table allocation");
   }
   rebase_soc(p->hp, p->table);
+  rebase_fixups(p->hp, p->table);
   e = hipMemcpy(p->table, p->hp.blob.bytes.data(), p->hp.blob.bytes.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) {
     optimus_status st = upload_copies(p->hp, p->table, nullptr, false);
@@ -1018,6 +1391,27 @@ extern "C" optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_d
                                                     optimus_plan* out) {
   HostPlan hp;
   optimus_status st = build_split_op_cat(d, dt, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
+                                                       optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_linear_backward(d, G, dt, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G,
+                                                          optimus_dtype dt, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_layernorm_backward(d, G, dt, hp);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
+extern "C" optimus_status optimus_plan_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt,
+                                                    optimus_act act, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_act_backward(d, G, dt, act, hp);
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
@@ -1075,12 +1469,30 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
   if (mode == OPTIMUS_EXEC_CHAIN && hp.kind != KIND_SOC) {
     for (int g = 0; g < hp.G; ++g) {
       hipError_t e;
-      if (hp.kind == KIND_Q8 || hp.kind == KIND_DQ8) {
+      if (hp.kind == KIND_ACTBWD || hp.kind == KIND_LNBWD) {
+        const RowLaunch& c = hp.rows_chain[g];
+        const DevRowsGrad* ds = at<DevRowsGrad>(p->table, c.descs_off);
+        const RowTile* ts = at<RowTile>(p->table, c.tiles_off) + c.first_tile;
+        if (hp.kind == KIND_ACTBWD) {
+          e = act_backward_launch(hp.dt, hp.act, ds, ts, c.num_tiles, c.grid, st);
+        } else {
+          e = layernorm_backward_launch(hp.dt, ds, ts, c.num_tiles, c.grid, st);
+          const RowLaunch& f = hp.fin_chain[g];
+          if (e == hipSuccess && f.num_tiles > 0)
+            e = grad_finalize_launch(hp.dt, at<GradFinItem>(p->table, f.descs_off) + f.first_tile, f.num_tiles, f.grid,
+                                     st);
+        }
+      } else if (hp.kind == KIND_Q8 || hp.kind == KIND_DQ8) {
         e = launch_fp8(hp, p->table, hp.q_scaled ? &hp.q_chain_amax[g] : nullptr, hp.q_chain[g], st);
-      } else if (hp.kind == KIND_LINEAR) {
-        const RowLaunch& c = hp.g_chain[g];
-        e = gemm_launch(hp.gcfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(p->table, hp.g_descs_off),
-                        at<GemmTile>(p->table, hp.g_tiles_off) + c.first_tile, c.num_tiles, c.grid, st);
+      } else if (hp.kind == KIND_LINEAR || hp.kind == KIND_LINBWD) {
+        e = hipSuccess;
+        for (int i = 0; i < hp.n_gs && e == hipSuccess; ++i) {
+          const GemmSet& gs = hp.gs[i];
+          const RowLaunch& c = gs.chain[g];
+          if (c.num_tiles > 0)
+            e = gemm_launch(gs.cfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(p->table, gs.descs_off),
+                            at<GemmTile>(p->table, gs.tiles_off) + c.first_tile, c.num_tiles, c.grid, st, gs.tr);
+        }
       } else {
         const RowLaunch& c = hp.rows_chain[g];
         const DevRows* ds = at<DevRows>(p->table, c.descs_off);
@@ -1180,6 +1592,7 @@ static optimus_status run_oneshot(HostPlan& hp, hipStream_t stream) {
     sg.cap = n;
   }
   rebase_soc(hp, table);
+  rebase_fixups(hp, table);
   memcpy(sg.host, hp.blob.bytes.data(), hp.blob.bytes.size());
   HIP_TRY(hipMemcpyAsync(table, sg.host, hp.blob.bytes.size(), hipMemcpyHostToDevice, stream), "one-shot: upload");
   HIP_TRY(hipEventRecord(sg.ev, stream), "one-shot: event record");
@@ -1220,6 +1633,24 @@ extern "C" optimus_status optimus_split_op_cat(const optimus_split_op_cat_desc* 
                                                optimus_stream_t stream) {
   HostPlan hp;
   optimus_status st = build_split_op_cat(d, dt, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_linear_backward(const optimus_linear_grad_desc* d, int32_t G,
+                                                          optimus_dtype dt, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_linear_backward(d, G, dt, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G,
+                                                             optimus_dtype dt, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_layernorm_backward(d, G, dt, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt,
+                                                       optimus_act act, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_act_backward(d, G, dt, act, hp);
   return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
 }
 extern "C" optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,

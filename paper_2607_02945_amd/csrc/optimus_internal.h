@@ -25,6 +25,9 @@ struct DevLinear {
   const void* gamma;  // [N] or NULL (1)
   const void* beta;   // [N] or NULL (0)
   float eps, inv_n;   // inv_n = 1 / N
+  // backward GEMMs: vec bit 2 = w 16-B loadable in its reduction-major layout;
+  // xsum [M] receives the row sums of x over K (db beside dW), or NULL
+  void* xsum;
 };
 
 // One GEMM work item: the BM x BN output tile (mb, nb) of member `member`;
@@ -97,11 +100,15 @@ struct GemmConfig {
 GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln);
 // Widest output row a fused LayerNorm can take for the dtype.
 int gemm_ln_max_n(optimus_dtype dt);
+// tr: 0 forward; 2 = w reduction-major (dX = dY . W); 3 = x and w
+// reduction-major (dW = dY^T . X, with db from d.xsum).
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
-                       const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream);
+                       const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream, int tr = 0);
+// Tile shape for the backward GEMMs (register-staged variants only).
+GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G);
 // Workgroups of the instance gemm_launch would run that fit on one CU at once
 // (the HIP runtime's occupancy of its registers and LDS; cfg.occ if the query fails).
-int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln);
+int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, int tr = 0);
 
 constexpr int kRowThreads = 256;
 #ifndef OPTIMUS_LN_CHUNKS_PER_LANE
@@ -125,6 +132,42 @@ hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int3
 // and rows one workgroup works on at a time.
 int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces);
 int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces);
+
+// ------------------------------------------------------------------ backward
+// One member of the LayerNorm / activation backward. Row mapping as for the
+// forward row kernels (lanes, vec). LayerNorm: every row tile writes column
+// partials of dgamma and dbeta (fp32, [2][cols] per partial row) into the
+// plan's partial buffer from row part0 + RowTile.pad (one partial row per
+// tile on the 16-byte path, one per wave on the per-value path).
+struct DevRowsGrad {
+  const void* x;
+  const void* dy;
+  void* dx;
+  const void* gamma;
+  float* part;      // the plan's partial buffer
+  int64_t ldx, lddy, lddx;
+  int32_t rows, cols;
+  int32_t lanes, vec;
+  float eps, inv_cols;
+  int32_t part0;    // this member's first partial row
+  int32_t want_params;  // dgamma / dbeta wanted
+};
+
+// Finalize: columns [c0, c0 + 256) of one member, the sum of its partial rows.
+struct GradFinItem {
+  const float* part;  // first partial row of the member ([2][cols] each)
+  void* dgamma;
+  void* dbeta;
+  int32_t cols, nparts, c0, pad;
+};
+
+constexpr int kGradWavesPerBlock = 4;  // partial rows per tile on the per-value path
+hipError_t act_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs, const RowTile* tiles,
+                               int32_t num_tiles, int32_t grid, hipStream_t stream);
+hipError_t layernorm_backward_launch(optimus_dtype dt, const DevRowsGrad* descs, const RowTile* tiles,
+                                     int32_t num_tiles, int32_t grid, hipStream_t stream);
+hipError_t grad_finalize_launch(optimus_dtype dt, const GradFinItem* items, int32_t num_items, int32_t grid,
+                                hipStream_t stream);
 
 // ------------------------------------------------------------------ fp8 codec
 // One member of the fp8 activation codec. Quantize: x = values of the group's

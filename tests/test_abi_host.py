@@ -233,3 +233,48 @@ def test_fp8_codec_validation():
     assert B.optimus_validate_dequantize_fp8(a, G, B.BF16) == ALIASING
     a, G = arr(B.Fp8DequantDesc, dq8(1 * MB, 2 * MB, 2 * MB + 8))
     assert B.optimus_validate_dequantize_fp8(a, G, B.BF16) == ALIASING
+
+
+def test_backward_validation():
+    arr = lambda T, *ds: ((T * len(ds))(*ds), len(ds))
+    # Linear: M=64, N=32, K=48
+    lg = lambda **kw: B.LinearGradDesc(*[kw.get(k, v) for k, v in [
+        ("x", 1 * MB), ("ldx", 48), ("w", 2 * MB), ("ldw", 48), ("dy", 3 * MB), ("lddy", 32), ("dx", 4 * MB),
+        ("lddx", 48), ("dw", 5 * MB), ("lddw", 48), ("db", 6 * MB), ("M", 64), ("N", 32), ("K", 48)]])
+    a, G = arr(B.LinearGradDesc, lg(), lg(x=7 * MB, w=8 * MB, dy=9 * MB, dx=10 * MB, dw=11 * MB, db=12 * MB))
+    assert B.optimus_validate_linear_backward(a, G, B.BF16) == OK
+    assert B.optimus_validate_linear_backward(a, -1, B.BF16) == INVALID
+    assert B.optimus_validate_linear_backward(a, G, 3) == UNSUPPORTED
+    for bad in [lg(dy=None), lg(w=None), lg(x=None), lg(M=0), lg(lddy=31), lg(lddx=40), lg(lddw=47), lg(ldx=47)]:
+        a, G = arr(B.LinearGradDesc, bad)
+        assert B.optimus_validate_linear_backward(a, G, B.BF16) == INVALID, bad
+    a, G = arr(B.LinearGradDesc, lg(dw=None))     # db without dw
+    assert B.optimus_validate_linear_backward(a, G, B.BF16) == UNSUPPORTED
+    a, G = arr(B.LinearGradDesc, lg(dw=None, db=None, x=None))   # dX only: x not needed
+    assert B.optimus_validate_linear_backward(a, G, B.F32) == OK
+    a, G = arr(B.LinearGradDesc, lg(dx=None, w=None))            # dW and db only: w not needed
+    assert B.optimus_validate_linear_backward(a, G, B.F32) == OK
+    a, G = arr(B.LinearGradDesc, lg(dx=3 * MB + 64))              # dX over dY
+    assert B.optimus_validate_linear_backward(a, G, B.BF16) == ALIASING
+    a, G = arr(B.LinearGradDesc, lg(), lg(x=7 * MB, w=8 * MB, dy=9 * MB, dx=10 * MB, dw=11 * MB, db=6 * MB))
+    assert B.optimus_validate_linear_backward(a, G, B.BF16) == ALIASING   # two members' db
+    # LayerNorm: rows 64, cols 48
+    ln = lambda **kw: B.LayerNormGradDesc(*[kw.get(k, v) for k, v in [
+        ("x", 1 * MB), ("ldx", 48), ("gamma", 2 * MB), ("dy", 3 * MB), ("lddy", 48), ("dx", 4 * MB), ("lddx", 48),
+        ("dgamma", 5 * MB), ("dbeta", 6 * MB), ("rows", 64), ("cols", 48), ("eps", 1e-5)]])
+    a, G = arr(B.LayerNormGradDesc, ln(), ln(x=7 * MB, gamma=None, dy=8 * MB, dx=8 * MB, dgamma=None, dbeta=None))
+    assert B.optimus_validate_layernorm_backward(a, G, B.BF16) == OK        # in place dx == dy allowed
+    for bad in [ln(x=None), ln(dy=None), ln(dx=None), ln(cols=0), ln(lddx=40), ln(eps=-1.0), ln(eps=float("inf"))]:
+        a, G = arr(B.LayerNormGradDesc, bad)
+        assert B.optimus_validate_layernorm_backward(a, G, B.BF16) == INVALID, bad
+    a, G = arr(B.LayerNormGradDesc, ln(dgamma=6 * MB + 8))
+    assert B.optimus_validate_layernorm_backward(a, G, B.BF16) == ALIASING
+    # activation
+    ag = lambda **kw: B.ActGradDesc(*[kw.get(k, v) for k, v in [
+        ("x", 1 * MB), ("ldx", 48), ("dy", 2 * MB), ("lddy", 48), ("dx", 2 * MB), ("lddx", 48), ("rows", 64),
+        ("cols", 48)]])
+    a, G = arr(B.ActGradDesc, ag())
+    assert B.optimus_validate_act_backward(a, G, B.BF16, "silu") == OK
+    assert B.optimus_validate_act_backward(a, G, B.BF16, 9) == UNSUPPORTED
+    a, G = arr(B.ActGradDesc, ag(dx=1 * MB + 2))
+    assert B.optimus_validate_act_backward(a, G, B.BF16, "relu") == ALIASING

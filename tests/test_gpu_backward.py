@@ -1,0 +1,301 @@
+"""Backward of the grouped operators on the GPU against the fp64 oracle,
+through the C ABI: Linear (dX, dW, db), activation, LayerNorm (dX, dgamma,
+dbeta); inf-normwise relative error per member and output, 1e-5 for fp32 and
+2e-2 for bf16 (fp32 sums, one rounding of each output)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_02945_amd import binding as B
+from paper_2607_02945_amd import synth
+from tests.gpu_util import assert_close, dev, host64, say
+
+pytestmark = pytest.mark.gpu
+ORC = oracle.get()
+ACTS = ["none", "relu", "sigmoid", "tanh", "silu"]
+
+
+def _t(a, dtype, pad=0, off=0):
+    """Device tensor of the values (rounded once to the dtype), optionally a
+    column slice of a wider buffer (row stride cols + pad + off, start off)."""
+    st = synth.to_storage(a, dtype)
+    if not pad and not off:
+        return dev(st), synth.exact64(st)
+    r, c = st.shape
+    base = torch.zeros((r, c + pad + off), dtype=st.dtype)
+    base[:, off:off + c] = st
+    return dev(base)[:, off:off + c], synth.exact64(st)
+
+
+def _empty(shape, dtype, pad=0):
+    t = torch.full((shape[0], shape[1] + pad), float("nan"), dtype=synth.DTYPES[dtype], device="cuda")
+    return t[:, :shape[1]] if pad else t
+
+
+def _with_variant(v, fn):
+    old = os.environ.get("OPTIMUS_GEMM_VARIANT")
+    if v is not None:
+        os.environ["OPTIMUS_GEMM_VARIANT"] = str(v)
+    try:
+        return fn()
+    finally:
+        if v is not None:
+            if old is None:
+                del os.environ["OPTIMUS_GEMM_VARIANT"]
+            else:
+                os.environ["OPTIMUS_GEMM_VARIANT"] = old
+
+
+# ------------------------------------------------------------------ Linear
+def _linear_members(shapes, dtype, seed, pad=0):
+    g = synth.rng(seed)
+    ms = []
+    for M, N, K in shapes:
+        x, x64 = _t(g.standard_normal((M, K)), dtype, pad)
+        w, w64 = _t(g.standard_normal((N, K)) / np.sqrt(K), dtype, pad)
+        dy, dy64 = _t(g.standard_normal((M, N)), dtype, pad)
+        ms.append({"x": x, "w": w, "dy": dy, "x64": x64, "w64": w64, "dy64": dy64, "M": M, "N": N, "K": K})
+    return ms
+
+
+def _run_linear_bwd(ms, dtype, mode="oneshot", want=("dx", "dw", "db"), variant=None, pad=0):
+    for m in ms:
+        m["dx"] = _empty((m["M"], m["K"]), dtype, pad) if "dx" in want else None
+        m["dw"] = _empty((m["N"], m["K"]), dtype, pad) if "dw" in want else None
+        m["db"] = torch.full((m["N"],), float("nan"), dtype=synth.DTYPES[dtype], device="cuda") if "db" in want else None
+    args = ([m["x"] for m in ms], [m["w"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms],
+            [m["dw"] for m in ms], [m["db"] for m in ms])
+
+    def go():
+        if mode == "oneshot":
+            B.optimus_grouped_linear_backward(*args)
+            return None
+        p = B.optimus_plan_linear_backward(*args)
+        info = p.info()
+        p.execute(mode)
+        torch.cuda.synchronize()
+        p.close()
+        return info
+    info = _with_variant(variant, go)
+    torch.cuda.synchronize()
+    return info
+
+
+def _check_linear_bwd(ms, dtype, what, want=("dx", "dw", "db")):
+    for i, m in enumerate(ms):
+        rdx, rdw, rdb = ORC.linear_backward(m["x64"], m["w64"], m["dy64"])
+        if "dx" in want:
+            assert_close(host64(m["dx"]), rdx, dtype, f"{what} member {i} dx")
+        if "dw" in want:
+            assert_close(host64(m["dw"]), rdw, dtype, f"{what} member {i} dw")
+        if "db" in want:
+            assert_close(host64(m["db"][None, :])[0], rdb, dtype, f"{what} member {i} db")
+
+
+SHAPES = [(1000, 256, 512), (300, 200, 136), (64, 17, 40), (513, 96, 8), (4097, 24, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
+def test_linear_backward(dtype, mode):
+    """Ragged members (tails in every dimension, K and N not multiples of the
+    16-byte chunk), every output."""
+    say(f"[linear bwd] {dtype} {mode}")
+    ms = _linear_members(SHAPES, dtype, seed=500)
+    info = _run_linear_bwd(ms, dtype, mode)
+    if info is not None:
+        assert info["kind"] == 7 and info["launches"] == 2 and info["chain_launches"] == 2 * len(ms)
+    _check_linear_bwd(ms, dtype, f"{dtype} {mode}")
+
+
+@pytest.mark.parametrize("variant", [1, 2, 3, 6])
+def test_linear_backward_every_tile(variant):
+    """Each tile shape of the backward GEMMs (bf16 128x128 and 256x256, fp32
+    64x64 and 64x128), grouped and chain."""
+    dtype = "fp32" if variant in (3, 6) else "bf16"
+    say(f"[linear bwd variant] {variant}")
+    ms = _linear_members([(700, 300, 260), (129, 64, 33), (257, 9, 520)], dtype, seed=510 + variant)
+    for mode in ["grouped", "chain"]:
+        _run_linear_bwd(ms, dtype, mode, variant=variant)
+        _check_linear_bwd(ms, dtype, f"variant {variant} {mode}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_linear_backward_strided_and_partial(dtype):
+    """Row strides above the row lengths everywhere (the 16-byte paths), then
+    only dX, only dW + db, dW without db."""
+    say(f"[linear bwd strided] {dtype}")
+    ms = _linear_members([(600, 128, 192), (77, 40, 56)], dtype, seed=520, pad=8)
+    _run_linear_bwd(ms, dtype, "grouped", pad=8)
+    _check_linear_bwd(ms, dtype, "strided")
+    for want in [("dx",), ("dw", "db"), ("dw",)]:
+        ms = _linear_members([(333, 64, 128), (65, 200, 8)], dtype, seed=521)
+        _run_linear_bwd(ms, dtype, "grouped", want=want)
+        _check_linear_bwd(ms, dtype, f"only {want}", want=want)
+
+
+def test_linear_backward_unaligned():
+    """A member starting one value off 16-byte alignment: every operand takes
+    the per-value loads."""
+    say("[linear bwd unaligned]")
+    ms = _linear_members([(300, 72, 40)], "bf16", seed=530)
+    g = synth.rng(531)
+    for key, shape in [("x", (300, 40)), ("w", (72, 40)), ("dy", (300, 72))]:
+        t, t64 = _t(g.standard_normal(shape) / (np.sqrt(40) if key == "w" else 1), "bf16", pad=3, off=1)
+        ms[0][key], ms[0][key + "64"] = t, t64
+    _run_linear_bwd(ms, "bf16", "grouped")
+    _check_linear_bwd(ms, "bf16", "unaligned")
+
+
+# ------------------------------------------------------------------ activation
+@pytest.mark.parametrize("act", ACTS)
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_act_backward(act, dtype):
+    say(f"[act bwd] {act} {dtype}")
+    g = synth.rng(540)
+    shapes = [(1000, 256), (300, 520), (17, 8), (64, 37)]
+    xs, dys, refs = [], [], []
+    for r, c in shapes:
+        x, x64 = _t(g.standard_normal((r, c)) * 3, dtype)
+        dy, dy64 = _t(g.standard_normal((r, c)), dtype)
+        xs.append(x); dys.append(dy); refs.append(ORC.act_backward(x64, dy64, act))
+    dxs = [_empty(x.shape, dtype) for x in xs]
+    B.optimus_grouped_act_backward(xs, dys, dxs, act)
+    for i, (dx, ref) in enumerate(zip(dxs, refs)):
+        assert_close(host64(dx), ref, dtype, f"act {act} member {i}")
+    # plan, chain, and in place (dx == dy)
+    p = B.optimus_plan_act_backward(xs, dys, dys, act)
+    p.execute("chain")
+    torch.cuda.synchronize()
+    p.close()
+    for i, (dy, ref) in enumerate(zip(dys, refs)):
+        assert_close(host64(dy), ref, dtype, f"act {act} in place member {i}")
+
+
+# ------------------------------------------------------------------ LayerNorm
+def _ln_members(shapes, dtype, seed, gamma=True, pad=0, off=0):
+    g = synth.rng(seed)
+    ms = []
+    for r, c in shapes:
+        x, x64 = _t(g.standard_normal((r, c)) * 2 + 0.5, dtype, pad, off)
+        dy, dy64 = _t(g.standard_normal((r, c)), dtype, pad, off)
+        gm, gm64 = _t(g.uniform(0.5, 1.5, (1, c)), dtype) if gamma else (None, None)
+        ms.append({"x": x, "dy": dy, "x64": x64, "dy64": dy64, "gamma": None if gm is None else gm[0],
+                   "g64": None if gm64 is None else gm64[0], "rows": r, "cols": c})
+    return ms
+
+
+def _run_ln_bwd(ms, dtype, mode="oneshot", params=True, inplace=False, eps=1e-5):
+    for m in ms:
+        m["dx"] = m["dy"] if inplace else _empty((m["rows"], m["cols"]), dtype)
+        m["dg"] = torch.full((m["cols"],), float("nan"), dtype=synth.DTYPES[dtype], device="cuda") if params else None
+        m["db"] = torch.full((m["cols"],), float("nan"), dtype=synth.DTYPES[dtype], device="cuda") if params else None
+    args = ([m["x"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms], [m["gamma"] for m in ms],
+            [m["dg"] for m in ms], [m["db"] for m in ms], eps)
+    if mode == "oneshot":
+        B.optimus_grouped_layernorm_backward(*args)
+    else:
+        p = B.optimus_plan_layernorm_backward(*args)
+        info = p.info()
+        assert info["kind"] == 8 and info["launches"] == (2 if params else 1)
+        p.execute(mode)
+        if not inplace:
+            p.execute(mode)   # a second run over the same partial buffer (in place, dy is gone)
+        torch.cuda.synchronize()
+        p.close()
+    torch.cuda.synchronize()
+
+
+def _check_ln_bwd(ms, dtype, what, params=True, eps=1e-5):
+    for i, m in enumerate(ms):
+        rdx, rdg, rdb = ORC.layernorm_backward(m["x64"], m["g64"], m["dy64"], eps)
+        assert_close(host64(m["dx"]), rdx, dtype, f"{what} member {i} dx")
+        if params:
+            assert_close(host64(m["dg"][None, :])[0], rdg, dtype, f"{what} member {i} dgamma")
+            assert_close(host64(m["db"][None, :])[0], rdb, dtype, f"{what} member {i} dbeta")
+
+
+LN_SHAPES = [(1000, 256), (300, 520), (4097, 24), (64, 1024), (3, 2000), (50, 37)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
+def test_layernorm_backward(dtype, mode):
+    """Rows held in registers (up to 1024 bf16 / 512 fp32 values) and wider or
+    odd rows on the per-value path, in one group."""
+    say(f"[ln bwd] {dtype} {mode}")
+    ms = _ln_members(LN_SHAPES, dtype, seed=550)
+    _run_ln_bwd(ms, dtype, mode)
+    _check_ln_bwd(ms, dtype, f"{dtype} {mode}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_layernorm_backward_variants(dtype):
+    """No gamma, no dgamma/dbeta, in place (dx == dy), strided and unaligned rows, eps 0.5."""
+    say(f"[ln bwd variants] {dtype}")
+    ms = _ln_members(LN_SHAPES[:3], dtype, seed=560, gamma=False)
+    _run_ln_bwd(ms, dtype, "grouped", eps=0.5)
+    _check_ln_bwd(ms, dtype, "no gamma", eps=0.5)
+    ms = _ln_members(LN_SHAPES[:3], dtype, seed=561)
+    _run_ln_bwd(ms, dtype, "grouped", params=False, inplace=True)
+    _check_ln_bwd(ms, dtype, "in place, no params", params=False)
+    ms = _ln_members([(500, 256), (77, 128)], dtype, seed=562, pad=8)
+    _run_ln_bwd(ms, dtype, "grouped")
+    _check_ln_bwd(ms, dtype, "strided")
+    ms = _ln_members([(500, 256), (77, 128)], dtype, seed=563, pad=3, off=1)
+    _run_ln_bwd(ms, dtype, "grouped")
+    _check_ln_bwd(ms, dtype, "unaligned")
+
+
+# ------------------------------------------------------------------ a training step's backward
+def test_towers_backward_chain_of_groups():
+    """The towers group's backward (LayerNorm, layer 2, relu, layer 1) as
+    grouped launches, against the fp64 oracle composition fed the same
+    stored intermediates: each operator per member within the bf16 bound."""
+    say("[towers bwd]")
+    wl = synth.towers(seed=3, G=6, M=512)
+    g = synth.rng(570)
+    T = wl.towers
+    # forward intermediates from the oracle (stored in bf16 as the forward would)
+    h_pre, h, o = [], [], []
+    for t in T:
+        hp = ORC.linear(synth.exact64(t.x), synth.exact64(t.w1), synth.exact64(t.b1))
+        hp_t, hp64 = _t(hp, "bf16")
+        h_t, h64 = _t(np.maximum(hp64, 0.0), "bf16")
+        o_t, o64 = _t(ORC.linear(h64, synth.exact64(t.w2), synth.exact64(t.b2)), "bf16")
+        h_pre.append((hp_t, hp64)); h.append((h_t, h64)); o.append((o_t, o64))
+    dz = [_t(g.standard_normal((512, 256)), "bf16") for _ in T]
+    gm = [dev(t.gamma) for t in T]
+    # LayerNorm backward
+    do = [_empty((512, 256), "bf16") for _ in T]
+    dgm = [torch.empty(256, dtype=torch.bfloat16, device="cuda") for _ in T]
+    dbt = [torch.empty(256, dtype=torch.bfloat16, device="cuda") for _ in T]
+    B.optimus_grouped_layernorm_backward([v[0] for v in o], [v[0] for v in dz], do, gm, dgm, dbt, wl.eps)
+    # layer 2 backward
+    dh = [_empty((512, 512), "bf16") for _ in T]
+    dw2 = [_empty((256, 512), "bf16") for _ in T]
+    db2 = [torch.empty(256, dtype=torch.bfloat16, device="cuda") for _ in T]
+    B.optimus_grouped_linear_backward([v[0] for v in h], [dev(t.w2) for t in T], do, dh, dw2, db2)
+    # relu backward (in place) and layer 1 backward
+    B.optimus_grouped_act_backward([v[0] for v in h_pre], dh, dh, "relu")
+    dw1 = [_empty((512, t.x.shape[1]), "bf16") for t in T]
+    db1 = [torch.empty(512, dtype=torch.bfloat16, device="cuda") for _ in T]
+    B.optimus_grouped_linear_backward([dev(t.x) for t in T], [dev(t.w1) for t in T], dh, None, dw1, db1)
+    torch.cuda.synchronize()
+    for i, t in enumerate(T):
+        r_do, r_dg, r_db = ORC.layernorm_backward(o[i][1], synth.exact64(t.gamma), dz[i][1], wl.eps)
+        assert_close(host64(do[i]), r_do, "bf16", f"tower {i} d(layer 2 out)")
+        assert_close(host64(dgm[i][None, :])[0], r_dg, "bf16", f"tower {i} dgamma")
+        do64 = host64(do[i])
+        r_dh, r_dw2, r_db2 = ORC.linear_backward(h[i][1], synth.exact64(t.w2), do64)
+        assert_close(host64(dw2[i]), r_dw2, "bf16", f"tower {i} dW2")
+        assert_close(host64(db2[i][None, :])[0], r_db2, "bf16", f"tower {i} db2")
+        dh64 = host64(dh[i])   # after the in-place relu backward
+        r_dhp = ORC.act_backward(h_pre[i][1], synth.exact64(synth.to_storage(r_dh, "bf16")), "relu")
+        assert_close(dh64, r_dhp, "bf16", f"tower {i} d(layer 1 out)")
+        _, r_dw1, r_db1 = ORC.linear_backward(synth.exact64(t.x), synth.exact64(t.w1), dh64)
+        assert_close(host64(dw1[i]), r_dw1, "bf16", f"tower {i} dW1")
+        assert_close(host64(db1[i][None, :])[0], r_db1, "bf16", f"tower {i} db1")
