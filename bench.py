@@ -21,7 +21,8 @@ on the current kernel sources.
 Workloads (the seeded groups of paper_2607_02945_amd.synth): launch_bound
 (default; G=256 bf16 Linear + sigmoid, B=2048), tiny_group, split_op_cat,
 towers, large_group, decompose_mm, act_quant (fp8 quantize of 32 saved
-activations, then dequantize).
+activations, then dequantize), towers_bwd and large_group_bwd (the training
+backward of the towers and large_group op-groups).
 """
 from __future__ import annotations
 
@@ -53,7 +54,7 @@ def parse():
                          "so that the clocks have settled)")
     ap.add_argument("--workload", default="launch_bound",
                     choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group", "decompose_mm",
-                             "act_quant"])
+                             "act_quant", "towers_bwd", "large_group_bwd"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-chain", action="store_true", help="skip timing the per-op launch chain")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -160,6 +161,59 @@ def build_copy(name, wl, torch, B):
         qs_u = [torch.empty_like(q) for q in qs]
         og.unscaled = [(B.optimus_plan_quantize_fp8(xs, qs_u, None, False), "grouped")]
         og.keep = (xs, qs, sc, ys, qs_u)
+    elif name == "towers_bwd":
+        # the towers' training backward: LayerNorm, layer 2, relu, layer 1
+        # (dX of the tower inputs too); the forward intermediates come from
+        # the forward plans, the incoming gradient is N(0, 1)
+        T = wl.towers
+        B_ = T[0].x.shape[0]
+        xs = [cu(t.x) for t in T]
+        w1, b1, w2, b2 = ([cu(getattr(t, a)) for t in T] for a in ("w1", "b1", "w2", "b2"))
+        gm = [cu(t.gamma) for t in T]
+        hp = [torch.empty((B_, 512), dtype=bf, device="cuda") for _ in T]
+        h = [torch.empty_like(v) for v in hp]
+        o = [torch.empty((B_, 256), dtype=bf, device="cuda") for _ in T]
+        B.optimus_plan_linear(xs, w1, b1, hp, "none").execute()
+        B.optimus_plan_pointwise(hp, h, "relu").execute()
+        B.optimus_plan_linear(h, w2, b2, o, "none").execute()
+        gen = torch.Generator(device="cuda").manual_seed(1)
+        dz = [torch.randn(v.shape, generator=gen, device="cuda").to(bf) for v in o]
+        do, dh = [torch.empty_like(v) for v in o], [torch.empty_like(v) for v in h]
+        dx = [torch.empty_like(x) for x in xs]
+        dw1, dw2 = [torch.empty_like(w) for w in w1], [torch.empty_like(w) for w in w2]
+        db1, db2 = [torch.empty_like(b) for b in b1], [torch.empty_like(b) for b in b2]
+        dgm, dbt = [torch.empty_like(g) for g in gm], [torch.empty_like(g) for g in gm]
+        torch.cuda.synchronize()
+        ln_b = B.optimus_plan_layernorm_backward(o, dz, do, gm, dgm, dbt, wl.eps)
+        l2_b = B.optimus_plan_linear_backward(h, w2, do, dh, dw2, db2)
+        relu_b = B.optimus_plan_act_backward(hp, dh, dh, "relu")
+        l1_b = B.optimus_plan_linear_backward(xs, w1, dh, dx, dw1, db1)
+        og.grouped = [(ln_b, "grouped"), (l2_b, "grouped"), (relu_b, "grouped"), (l1_b, "grouped")]
+        og.chain = [(ln_b, "chain"), (l2_b, "chain"), (relu_b, "chain"), (l1_b, "chain")]
+        og.keep = (xs, w1, b1, w2, b2, gm, hp, h, o, dz, do, dh, dx, dw1, dw2, db1, db2, dgm, dbt)
+    elif name == "large_group_bwd":
+        # backward of Linear -> LayerNorm -> tanh over the 32 wide members: tanh,
+        # LayerNorm, then dX, dW and db of the Linear (K = 1024 for dX, the
+        # batch of 16384 for dW)
+        ms = wl.members
+        xs, ws, bs = [cu(m.x) for m in ms], [cu(m.w) for m in ms], [cu(m.b) for m in ms]
+        gs, bes = [cu(g) for g in wl.gammas], [cu(b) for b in wl.betas]
+        y = [torch.empty((m.M, m.N), dtype=bf, device="cuda") for m in ms]
+        z = [torch.empty_like(v) for v in y]
+        B.optimus_plan_linear(xs, ws, bs, y, "none").execute()
+        B.optimus_plan_layernorm(y, z, gs, bes, wl.eps, "none").execute()
+        gen = torch.Generator(device="cuda").manual_seed(2)
+        dt_ = [torch.randn(v.shape, generator=gen, device="cuda").to(bf) for v in z]
+        dz, dy = [torch.empty_like(v) for v in z], [torch.empty_like(v) for v in y]
+        dx, dw, db = [torch.empty_like(x) for x in xs], [torch.empty_like(w) for w in ws], [torch.empty_like(b) for b in bs]
+        dgm, dbt = [torch.empty_like(g) for g in gs], [torch.empty_like(g) for g in gs]
+        torch.cuda.synchronize()
+        tanh_b = B.optimus_plan_act_backward(z, dt_, dz, "tanh")
+        ln_b = B.optimus_plan_layernorm_backward(y, dz, dy, gs, dgm, dbt, wl.eps)
+        lin_b = B.optimus_plan_linear_backward(xs, ws, dy, dx, dw, db)
+        og.grouped = [(tanh_b, "grouped"), (ln_b, "grouped"), (lin_b, "grouped")]
+        og.chain = [(tanh_b, "chain"), (ln_b, "chain"), (lin_b, "chain")]
+        og.keep = (xs, ws, bs, gs, bes, y, z, dt_, dz, dy, dx, dw, db, dgm, dbt)
     elif name == "towers":
         T = wl.towers
         xs = [cu(t.x) for t in T]
@@ -188,6 +242,10 @@ def workload_bytes(name, wl):
         return 2 * wl.x.numel() * 2
     if name == "towers":
         return sum(t.x.numel() * 2 + (512 + 256 + 256) * t.x.shape[0] * 2 for t in wl.towers)
+    if name == "towers_bwd":
+        return sum(2 * t.x.numel() * 2 + (4 * 512 + 4 * 256) * t.x.shape[0] * 2 for t in wl.towers)
+    if name == "large_group_bwd":
+        return sum((2 * m.x.numel() + 2 * m.w.numel() + 6 * m.M * m.N) * 2 for m in wl.members)
     if name == "act_quant":
         return sum(x.numel() * (2 + 1 + 2 + 1) for x in wl.xs)
     s = 4 if wl.dtype == "fp32" else 2
@@ -201,6 +259,14 @@ def describe(name, wl):
     if name == "towers":
         return {"workload": name, "towers": wl.G, "batch": wl.towers[0].x.shape[0],
                 "layers": "Linear(in_g->512)+relu, Linear(512->256), LayerNorm", "seed": 0}
+    if name == "towers_bwd":
+        return {"workload": name, "towers": wl.G, "batch": wl.towers[0].x.shape[0],
+                "backward_of": "Linear(in_g->512)+relu, Linear(512->256), LayerNorm",
+                "grads": "dX, dW, db of both layers, dgamma, dbeta", "seed": 0}
+    if name == "large_group_bwd":
+        return {"workload": name, "G": wl.G, "batch": wl.members[0].M, "K": sorted({m.K for m in wl.members}),
+                "N": sorted({m.N for m in wl.members}), "backward_of": "Linear -> LayerNorm -> tanh",
+                "grads": "dX, dW, db, dgamma, dbeta", "seed": 0}
     if name == "act_quant":
         return {"workload": name, "G": wl.G, "batch": wl.xs[0].shape[0], "N": sorted({x.shape[1] for x in wl.xs}),
                 "codec": "bf16 -> OCP E4M3 with per-tensor amax scale -> bf16", "seed": 0}
@@ -216,6 +282,8 @@ def describe(name, wl):
 def cpu_baseline(name, wl, target_s):
     """The oracle as it stands, on the host cores, on a bounded sample of the
     same workload, scaled to microseconds per op-group."""
+    import numpy as np
+
     import oracle
     from paper_2607_02945_amd import synth
     orc = oracle.get()
@@ -237,6 +305,42 @@ def cpu_baseline(name, wl, target_s):
             for x in ins:
                 q, sc = orc.quantize_fp8(x, True)
                 orc.dequantize_fp8(q, sc)
+    elif name in ("towers_bwd", "large_group_bwd"):
+        # the oracle's backward of the same operators on the first rows of every member
+        rows = 64
+        g = synth.rng(7)
+        if name == "towers_bwd":
+            M = wl.towers[0].x.shape[0]
+            ins = []
+            for t in wl.towers:
+                x, w1, b1, w2, b2 = (e(a) for a in (t.x[:rows], t.w1, t.b1, t.w2, t.b2))
+                hp = orc.linear(x, w1, b1)
+                h = np.maximum(hp, 0.0)
+                o = orc.linear(h, w2, b2)
+                ins.append((x, w1, w2, e(t.gamma), hp, h, o, g.standard_normal(o.shape)))
+
+            def work():
+                for x, w1, w2, gm, hp, h, o, dz in ins:
+                    do = orc.layernorm_backward(o, gm, dz, wl.eps)[0]
+                    dh = orc.linear_backward(h, w2, do)[0]
+                    dhp = orc.act_backward(hp, dh, "relu")
+                    orc.linear_backward(x, w1, dhp)
+        else:
+            M = wl.members[0].M
+            ins = []
+            for m, gm, be in zip(wl.members, wl.gammas, wl.betas):
+                x, w, b = e(m.x[:rows]), e(m.w), e(m.b)
+                y = orc.linear(x, w, b)
+                z = orc.layernorm(y, e(gm), e(be), wl.eps)
+                ins.append((x, w, y, z, e(gm), g.standard_normal(z.shape)))
+
+            def work():
+                for x, w, y, z, gm, dt_ in ins:
+                    dz = orc.act_backward(z, dt_, "tanh")
+                    dy = orc.layernorm_backward(y, gm, dz, wl.eps)[0]
+                    orc.linear_backward(x, w, dy)
+        frac = rows / M
+        sample = f"first {rows} of {M} rows of every member"
     elif name == "towers":
         rows = 64
         ins = [(e(t.x[:rows]), e(t.w1), e(t.b1), e(t.w2), e(t.b2), e(t.gamma), e(t.beta)) for t in wl.towers]
@@ -420,7 +524,7 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     B.lib()  # loud failure if the HIP library is missing
-    wl = synth.WORKLOADS[args.workload](args.seed)
+    wl = synth.WORKLOADS[args.workload.replace("_bwd", "")](args.seed)
     dtype = "fp32" if getattr(wl, "dtype", "bf16") == "fp32" else "bf16"
     per_copy = workload_bytes(args.workload, wl)
     copies = max(1, min(16, math.ceil(CACHE_BYTES / per_copy)))

@@ -119,28 +119,34 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
 #pragma unroll
     for (int e = 0; e < VEC; ++e) accG[j][e] = accB[j][e] = 0.f;
   const int end = rt.row0 + rt.nrows;
-  for (int r = rt.row0 + wave * rpw + sub; r - sub - wave * rpw < end; r += 4 * rpw) {
-    // every lane of the wave runs the loop the same number of times (the
-    // lane-group sums need all 64); rows past the tile contribute nothing
-    const bool valid = r < end;
+  const int rpb = 4 * rpw;
+  // The next row slot's x and dy chunks are loaded while the current one is
+  // computed (as the forward kernel does).
+  u32x4 rx[MAXC], rg[MAXC];
+  auto fetch = [&](int r) {
     const char* xr = (const char*)d.x + (int64_t)r * d.ldx * sizeof(T);
     const char* gr = (const char*)d.dy + (int64_t)r * d.lddy * sizeof(T);
-    float x[MAXC][VEC], g[MAXC][VEC];
-    {
-      u32x4 rx[MAXC], rg[MAXC];
 #pragma unroll
-      for (int j = 0; j < MAXC; ++j) {
-        const int c = j * L + li;
-        const bool in = valid && c < cpr;
-        rx[j] = in ? ld16_nt(xr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
-        rg[j] = in ? ld16_nt(gr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
-      }
-#pragma unroll
-      for (int j = 0; j < MAXC; ++j) {
-        Elem<T>::unpack(rx[j], x[j]);
-        Elem<T>::unpack(rg[j], g[j]);
-      }
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = j * L + li;
+      const bool in = r < end && c < cpr;
+      rx[j] = in ? ld16_nt(xr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
+      rg[j] = in ? ld16_nt(gr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
     }
+  };
+  fetch(rt.row0 + wave * rpw + sub);
+  // every lane of the wave runs the loop the same number of times (the
+  // lane-group sums need all 64); rows past the tile contribute nothing
+  for (int base = rt.row0; base < end; base += rpb) {
+    const int r = base + wave * rpw + sub;
+    const bool valid = r < end;
+    float x[MAXC][VEC], g[MAXC][VEC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      Elem<T>::unpack(rx[j], x[j]);
+      Elem<T>::unpack(rg[j], g[j]);
+    }
+    if (base + rpb < end) fetch(r + rpb);
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j)

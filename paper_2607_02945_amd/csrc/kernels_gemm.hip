@@ -105,7 +105,11 @@ __device__ __forceinline__ u32x4 load_chunk(const void* base, int64_t ld, int ro
 // rows. A thread loads KB reduction rows of one 16-byte chunk (VEC tile rows)
 // and writes VEC pieces of KB reduction-consecutive values into the same
 // [row][k] LDS layout the MFMA fragment reads use: for bf16 four rows, and the
-// 4 x 8 block is transposed with two byte permutes per output word.
+// 4 x 8 block is transposed with two byte permutes per output word. Lanes
+// take consecutive reduction blocks first: the 8-byte LDS writes of a wave
+// then fall on distinct bank pairs (consecutive row groups sit 8 rows apart,
+// a multiple of the bank period at the padded row pitch), while each global
+// load still reads 64 contiguous bytes per reduction row.
 template <typename T>
 struct Trans;
 template <>
@@ -444,7 +448,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       if constexpr (TX) {
 #pragma unroll
         for (int i = 0; i < LXT; ++i) {
-          const int idx = tid + i * NT, rg = idx % (BM / VEC), kq = idx / (BM / VEC);
+          const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
 #pragma unroll
           for (int j = 0; j < KB; ++j) rx[i * KB + j] = load_chunk_t<T>(xb, d.ldx, rg * VEC, Mr, k0 + kq * KB + j, d.K, vin);
         }
@@ -458,7 +462,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       if constexpr (TW) {
 #pragma unroll
         for (int i = 0; i < LWT; ++i) {
-          const int idx = tid + i * NT, rg = idx % (BN / VEC), kq = idx / (BN / VEC);
+          const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
 #pragma unroll
           for (int j = 0; j < KB; ++j) rw[i * KB + j] = load_chunk_t<T>(wb, d.ldw, rg * VEC, Nr, k0 + kq * KB + j, d.K, vw);
         }
@@ -476,7 +480,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       if constexpr (TX) {
 #pragma unroll
         for (int i = 0; i < LXT; ++i) {
-          const int idx = tid + i * NT, rg = idx % (BM / VEC), kq = idx / (BM / VEC);
+          const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
           u32x4 blk[KB];
 #pragma unroll
           for (int j = 0; j < KB; ++j) blk[j] = rx[i * KB + j];
@@ -493,7 +497,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         float unused[VEC];
 #pragma unroll
         for (int i = 0; i < LWT; ++i) {
-          const int idx = tid + i * NT, rg = idx % (BN / VEC), kq = idx / (BN / VEC);
+          const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
           u32x4 blk[KB];
 #pragma unroll
           for (int j = 0; j < KB; ++j) blk[j] = rw[i * KB + j];
@@ -552,7 +556,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         float* part = (float*)smem;  // [BK / KB][BM], the operand area is free after the K loop
 #pragma unroll
         for (int i = 0; i < LXT; ++i) {
-          const int idx = tid + i * NT, rg = idx % (BM / VEC), kq = idx / (BM / VEC);
+          const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
 #pragma unroll
           for (int e = 0; e < VEC; ++e) part[kq * BM + rg * VEC + e] = xs[i][e];
         }

@@ -752,20 +752,25 @@ static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, in
 }
 
 // Row tiles of every member (pad = the tile's index within its member), the
-// grouped launch and the per-member CHAIN ranges.
+// grouped launch and the per-member CHAIN ranges. With `max_tiles` a member
+// gets at most that many tiles (each LayerNorm-backward tile writes a
+// partial row of dgamma / dbeta that the finalize reads back).
+static constexpr int64_t kGradMaxTilesPerMember = 64;
 static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
-                                           std::vector<int>& ntiles) {
+                                           std::vector<int>& ntiles, int64_t max_tiles = 0) {
   std::vector<RowTile> tiles;
   hp.rows_chain.clear();
   ntiles.assign(members.size(), 0);
   for (size_t g = 0; g < members.size(); ++g) {
-    DevRows geo{};
-    geo.rows = members[g].rows;
-    geo.cols = members[g].cols;
-    geo.vec = members[g].vec;
-    geo.lanes = members[g].vec ? members[g].lanes : 1;
+    const DevRowsGrad& m = members[g];
+    const int rpb = m.vec ? 4 * (64 / m.lanes) : 4;
+    const int64_t row_bytes = std::max<int64_t>(1, (int64_t)m.cols * (int64_t)s);
+    int64_t per = std::max<int64_t>(1, kRowTileBytes / row_bytes);
+    if (max_tiles > 0) per = std::max<int64_t>(per, (m.rows + max_tiles - 1) / max_tiles);
+    per = (per + rpb - 1) / rpb * rpb;
     const int first = (int)tiles.size();
-    add_row_tiles(tiles, (int)g, geo, s);
+    for (int64_t r0 = 0; r0 < m.rows; r0 += per)
+      tiles.push_back(RowTile{(int)g, (int32_t)r0, (int32_t)std::min<int64_t>(per, m.rows - r0), 0});
     for (int t = first; t < (int)tiles.size(); ++t) tiles[t].pad = t - first;
     ntiles[g] = (int)tiles.size() - first;
     hp.rows_chain.push_back(RowLaunch{0, 0, first, ntiles[g], row_grid(ntiles[g])});
@@ -788,7 +793,7 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
                              (m.dbeta ? m.cols : 0));
   }
   std::vector<int> ntiles;
-  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles);
+  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember);
   // partial rows: one per tile (16-byte path) or per wave (per-value path)
   int64_t part_rows = 0;
   std::vector<int> nparts(G, 0);
