@@ -427,6 +427,14 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
     const T* xb = TX ? (const T*)d.x + m0 : (const T*)d.x + (int64_t)m0 * d.ldx;
     const T* wb = TW ? (const T*)d.w + n0 : (const T*)d.w + (int64_t)n0 * d.ldw;
     const bool want_sum = TX && d.xsum && tile.nb == 0;
+    // the reduction range: all of K, or one split of it
+    int kbeg = 0, kend = d.K;
+    if constexpr (TR != 0) {
+      if (d.ws) {
+        kbeg = tile.pad * d.kchunk;
+        kend = min(d.K, kbeg + d.kchunk);
+      }
+    }
     float xs[TX ? LXT : 1][VEC];
 #pragma unroll
     for (int i = 0; i < (TX ? LXT : 1); ++i)
@@ -450,13 +458,13 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         for (int i = 0; i < LXT; ++i) {
           const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
 #pragma unroll
-          for (int j = 0; j < KB; ++j) rx[i * KB + j] = load_chunk_t<T>(xb, d.ldx, rg * VEC, Mr, k0 + kq * KB + j, d.K, vin);
+          for (int j = 0; j < KB; ++j) rx[i * KB + j] = load_chunk_t<T>(xb, d.ldx, rg * VEC, Mr, k0 + kq * KB + j, kend, vin);
         }
       } else {
 #pragma unroll
         for (int i = 0; i < S::LX; ++i) {
           const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-          rx[i] = load_chunk<T>(xb, d.ldx, row, Mr, k0 + c * VEC, d.K, vin);
+          rx[i] = load_chunk<T>(xb, d.ldx, row, Mr, k0 + c * VEC, kend, vin);
         }
       }
       if constexpr (TW) {
@@ -464,13 +472,13 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         for (int i = 0; i < LWT; ++i) {
           const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
 #pragma unroll
-          for (int j = 0; j < KB; ++j) rw[i * KB + j] = load_chunk_t<T>(wb, d.ldw, rg * VEC, Nr, k0 + kq * KB + j, d.K, vw);
+          for (int j = 0; j < KB; ++j) rw[i * KB + j] = load_chunk_t<T>(wb, d.ldw, rg * VEC, Nr, k0 + kq * KB + j, kend, vw);
         }
       } else {
 #pragma unroll
         for (int i = 0; i < S::LW; ++i) {
           const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-          rw[i] = load_chunk<T>(wb, d.ldw, row, Nr, k0 + c * VEC, d.K, vin);
+          rw[i] = load_chunk<T>(wb, d.ldw, row, Nr, k0 + c * VEC, kend, vin);
         }
       }
     };
@@ -529,20 +537,20 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       }
     };
 
-    const int nk = (d.K + BK - 1) / BK;
+    const int nk = (kend - kbeg + BK - 1) / BK;
     if constexpr (STAGES == 2) {
-      gload(0);
+      gload(kbeg);
       lstore(0);
       __syncthreads();
       for (int kb = 0; kb < nk; ++kb) {
-        if (kb + 1 < nk) gload((kb + 1) * BK);
+        if (kb + 1 < nk) gload(kbeg + (kb + 1) * BK);
         compute(kb & 1);
         if (kb + 1 < nk) lstore((kb + 1) & 1);
         __syncthreads();
       }
     } else {
       for (int kb = 0; kb < nk; ++kb) {
-        gload(kb * BK);
+        gload(kbeg + kb * BK);
         lstore(0);
         __syncthreads();
         compute(0);
@@ -564,9 +572,41 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         for (int r = tid; r < BM && r < Mr; r += NT) {
           float sum = 0.f;
           for (int q = 0; q < BK / KB; ++q) sum += part[q * BM + r];
-          Elem<T>::store1(d.xsum, m0 + r, sum);
+          if (d.ws)  // this split's share of the row sums
+            d.ws[(int64_t)d.splits * d.M * d.N + (int64_t)tile.pad * d.M + m0 + r] = sum;
+          else
+            Elem<T>::store1(d.xsum, m0 + r, sum);
         }
         __syncthreads();
+      }
+    }
+    if constexpr (TR != 0) {
+      if (d.ws) {
+        // fp32 partial tile straight from the accumulators: each lane holds
+        // four consecutive columns of one row per (i, j, quad)
+        float* wb = d.ws + ((int64_t)tile.pad * d.M + m0) * d.N + n0;
+        const bool v4 = (d.N & 3) == 0;
+#pragma unroll
+        for (int i = 0; i < S::FM; ++i) {
+          const int row = wm * S::TM + i * 32 + l32;
+          if (row >= Mr) continue;
+#pragma unroll
+          for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int col = wn * S::TN + j * 32 + 8 * q + 4 * lh;
+              float* p = wb + (int64_t)row * d.N + col;
+              if (v4 && col + 3 < Nr) {
+                *(OPTIMUS_GLOBAL f32x4*)p = f32x4{acc[i][j][q * 4 + 0], acc[i][j][q * 4 + 1], acc[i][j][q * 4 + 2],
+                                                 acc[i][j][q * 4 + 3]};
+              } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  if (col + e < Nr) ((OPTIMUS_GLOBAL float*)p)[e] = acc[i][j][q * 4 + e];
+              }
+            }
+        }
+        continue;
       }
     }
     if constexpr (LN) ln_rows<BM, BN, WM, WN>(acc, sBias, sGamma, sBeta, red, d);
@@ -1167,6 +1207,104 @@ __global__ __launch_bounds__(256) void grouped_gemm_skinny_kernel(const DevLinea
   }
 }
 
+// ===================================================================== split reduction
+// y[m][n] = sum over the splits of the fp32 partials, rounded once; the row
+// sums likewise. An item is a run of rows; its (row, 4-column group) pairs
+// are spread over the workgroup's threads, so every thread has a few
+// independent loads per split in flight whatever the width.
+template <typename T>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const SplitReduceItem* __restrict__ items,
+                                                            int32_t num_items) {
+  const int tid = threadIdx.x;
+  for (int t = blockIdx.x; t < num_items; t += gridDim.x) {
+    const SplitReduceItem it = items[t];
+    const int64_t plane = (int64_t)it.M * it.N;
+    const int nc4 = (it.N + 3) >> 2;
+    const int total = it.nrows * nc4;
+    const bool v4 = (it.N & 3) == 0;
+    for (int e = tid; e < total; e += 256) {
+      const int r = it.row0 + e / nc4;
+      const int c = (e % nc4) * 4;
+      const float* src = it.ws + (int64_t)r * it.N + c;
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      if (v4) {
+        for (int s = 0; s < it.splits; ++s) {
+          const f32x4 v = *(const OPTIMUS_GLOBAL f32x4*)(src + s * plane);
+          acc[0] += v[0];
+          acc[1] += v[1];
+          acc[2] += v[2];
+          acc[3] += v[3];
+        }
+      } else {
+        for (int s = 0; s < it.splits; ++s)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (c + q < it.N) acc[q] += ((const OPTIMUS_GLOBAL float*)(src + s * plane))[q];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (c + q < it.N) Elem<T>::store1(it.y, (int64_t)r * it.ldy + c + q, acc[q]);
+    }
+    if (it.xsum) {
+      const float* sums = it.ws + (int64_t)it.splits * plane;
+      for (int r = it.row0 + tid; r < it.row0 + it.nrows; r += 256) {
+        float a = 0.f;
+        for (int s = 0; s < it.splits; ++s) a += sums[(int64_t)s * it.M + r];
+        Elem<T>::store1(it.xsum, r, a);
+      }
+    }
+  }
+}
+
+hipError_t splitk_reduce_launch(optimus_dtype dt, const SplitReduceItem* items, int32_t num_items, int32_t grid,
+                                hipStream_t stream) {
+  if (num_items <= 0) return hipSuccess;
+  if (dt == OPTIMUS_BF16)
+    hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3(grid), dim3(256), 0, stream, items, num_items);
+  else
+    hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(grid), dim3(256), 0, stream, items, num_items);
+  return hipGetLastError();
+}
+
+// ===================================================================== grouped transpose
+// W [N][K] -> W^T [K][N] for the dX GEMM of the Linear backward (W is small
+// next to the activations, so the copy costs little and dX then runs on the
+// forward's direct-to-LDS kernel). 64 x 64 tiles through LDS, rows padded by
+// one element; values moved as raw bits.
+template <typename U>
+__global__ __launch_bounds__(256) void grouped_transpose_kernel(const TransposeItem* __restrict__ items,
+                                                                int32_t num_items) {
+  __shared__ U tile[64][65];
+  const int tid = threadIdx.x, tc = tid & 63, tr = tid >> 6;
+  for (int t = blockIdx.x; t < num_items; t += gridDim.x) {
+    const TransposeItem it = items[t];
+    const OPTIMUS_GLOBAL U* src = (const OPTIMUS_GLOBAL U*)it.src;
+    OPTIMUS_GLOBAL U* dst = (OPTIMUS_GLOBAL U*)it.dst;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = it.r0 + tr + 4 * i, c = it.c0 + tc;
+      if (r < it.rows && c < it.cols) tile[tr + 4 * i][tc] = src[(int64_t)r * it.lds + c];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int c = it.c0 + tr + 4 * i, r = it.r0 + tc;  // dst row c, column r
+      if (r < it.rows && c < it.cols) dst[(int64_t)c * it.ldd + r] = tile[tc][tr + 4 * i];
+    }
+    __syncthreads();
+  }
+}
+
+hipError_t transpose_launch(optimus_dtype dt, const TransposeItem* items, int32_t num_items, int32_t grid,
+                            hipStream_t stream) {
+  if (num_items <= 0) return hipSuccess;
+  if (dt == OPTIMUS_BF16)
+    hipLaunchKernelGGL(grouped_transpose_kernel<uint16_t>, dim3(grid), dim3(256), 0, stream, items, num_items);
+  else
+    hipLaunchKernelGGL(grouped_transpose_kernel<float>, dim3(grid), dim3(256), 0, stream, items, num_items);
+  return hipGetLastError();
+}
+
 // ===================================================================== configurations
 struct GemmVariant {
   int bm, bn, threads, occ;  // occ: workgroups resident per CU (LDS / register bound)
@@ -1316,9 +1454,7 @@ template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
 static hipError_t launch_trans(int tr, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
                                hipStream_t stream, int* occ) {
   using S = GemmShape<T, BM, BN, BK, WM, WN, STAGES>;
-  if (tr == 2)
-    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, 0, 2>), S::LDS_BYTES, S::NT)
-  else if (tr == 3)
+  if (tr == 3)
     OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, 0, 3>), S::LDS_BYTES, S::NT)
   else
     return hipErrorInvalidValue;
@@ -1384,10 +1520,17 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
 
 // Backward GEMMs (transposed operands): the register-staged tiles -- 256x256
 // from half a tile per CU on, else 128x128; fp32 64x64.
-GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G) {
-  double tiles256 = 0.0;
-  for (int g = 0; g < G; ++g) tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
-  int v = dt == OPTIMUS_F32 ? 3 : (tiles256 >= 0.5 * device_cu_count() ? 2 : 1);
+GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k) {
+  double tiles256 = 0.0, area = 0.0;
+  for (int g = 0; g < G; ++g) {
+    tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
+    area += (double)d[g].M * (double)d[g].N;
+  }
+  // the share of the 256x256 tiles' area that holds output: narrow members
+  // (N of 64 or 128) leave most of a large tile idle
+  const double fill256 = area / (tiles256 * 65536.0);
+  // a split reduction fills the machine with the large tile's better per-tile rate
+  int v = dt == OPTIMUS_F32 ? 3 : (fill256 >= 0.75 && (split_k || tiles256 >= 0.5 * device_cu_count()) ? 2 : 1);
   const char* f = getenv("OPTIMUS_GEMM_VARIANT");
   char* end = nullptr;
   const long want = f ? strtol(f, &end, 10) : -1;

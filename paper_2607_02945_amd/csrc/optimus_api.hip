@@ -476,6 +476,14 @@ struct HostPlan {
   std::vector<size_t> soc_temp_fixups;  // blob offsets of DevRows pointers relative to the temp base
   // pointer fields of the blob that hold a blob offset, rebased to the device table
   std::vector<size_t> table_fixups;
+  // plan-owned device scratch (split-reduction partials), not part of the
+  // uploaded table: pointer fields holding an offset into it
+  size_t scratch_bytes = 0;
+  std::vector<size_t> scratch_fixups;
+  RowLaunch red{};                  // split reduction of the dW set
+  std::vector<RowLaunch> red_chain;
+  RowLaunch tp{};                   // transpose of W before the dX set
+  std::vector<RowLaunch> tp_chain;
   // row-wise backward: the main launch (rows / rows_chain) and the dgamma /
   // dbeta finalize of a LayerNorm backward
   RowLaunch fin{};
@@ -579,7 +587,7 @@ static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool l
 // persistent grid is no larger than what is resident at once (a workgroup
 // that had to wait for a free slot would start its whole share late).
 static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int tr, const std::vector<DevLinear>& descs,
-                           const std::vector<int>& ids, int group_size, optimus_act act, bool ln) {
+                           const std::vector<int>& ids, int group_size, optimus_act act, bool ln, int splits = 1) {
   const int n = (int)descs.size();
   gs.cfg = cfg;
   gs.tr = tr;
@@ -593,7 +601,8 @@ static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int
     const int first = (int)tiles.size();
     const int64_t mbs = (descs[i].M + bm - 1) / bm, nbs = (descs[i].N + bn - 1) / bn;
     for (int64_t mb = 0; mb < mbs; ++mb)
-      for (int64_t nb = 0; nb < nbs; ++nb) tiles.push_back(GemmTile{i, (int32_t)mb, (int32_t)nb, 0});
+      for (int64_t nb = 0; nb < nbs; ++nb)
+        for (int ks = 0; ks < splits; ++ks) tiles.push_back(GemmTile{i, (int32_t)mb, (int32_t)nb, ks});
     gs.chain[ids[i]].first_tile = first;
     gs.chain[ids[i]].num_tiles = (int)tiles.size() - first;
   }
@@ -668,21 +677,33 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
   std::vector<DevLinear> dxs, dws;
   std::vector<int> dx_ids, dw_ids;
   std::vector<optimus_linear_desc> dx_shape, dw_shape;  // (M', N', K') for the tile picker
+  std::vector<TransposeItem> tps;  // W -> W^T tiles, member by member
+  std::vector<int> tp_end;  // per dX member: end of its transpose tiles
   for (int g = 0; g < G; ++g) {
     const optimus_linear_grad_desc& m = d[g];
     if (m.dx) {
+      // dX = dY . W as a forward GEMM on W^T [K][N'] (N' = N rounded up to 8
+      // values), transposed into plan scratch by the first launch
       DevLinear o{};
-      o.x = m.dy; o.ldx = m.lddy; o.w = m.w; o.ldw = m.ldw; o.y = m.dx; o.ldy = m.lddx;
+      const int64_t ldt = (m.N + 7) / 8 * 8;
+      const size_t off = (hp.scratch_bytes + 255) & ~(size_t)255;
+      hp.scratch_bytes = off + (size_t)(m.K * ldt) * s;
+      o.x = m.dy; o.ldx = m.lddy; o.w = (const void*)(uintptr_t)off; o.ldw = ldt; o.y = m.dx; o.ldy = m.lddx;
       o.M = (int32_t)m.M; o.N = (int32_t)m.K; o.K = (int32_t)m.N;
-      const bool vx = m.N % VEC == 0 && m.lddy % VEC == 0 && aligned16(m.dy);
+      const bool vin = m.N % VEC == 0 && m.lddy % VEC == 0 && aligned16(m.dy);
       const bool vout = m.lddx % VEC == 0 && aligned16(m.dx);
-      const bool vw = m.ldw % VEC == 0 && aligned16(m.w);
-      o.vec = (vx ? 1 : 0) | (vout ? 2 : 0) | (vw ? 4 : 0);
+      o.vec = (vin ? 1 : 0) | (vout ? 2 : 0);
+      for (int64_t r0 = 0; r0 < m.N; r0 += 64)
+        for (int64_t c0 = 0; c0 < m.K; c0 += 64)
+          tps.push_back(TransposeItem{m.w, (void*)(uintptr_t)off, m.ldw, ldt, (int32_t)m.N, (int32_t)m.K,
+                                      (int32_t)r0, (int32_t)c0});
+      tp_end.push_back((int)tps.size());
       o.inv_n = 1.0f / (float)m.K;
       dxs.push_back(o);
       dx_ids.push_back(g);
       optimus_linear_desc sh{};
       sh.M = m.M; sh.N = m.K; sh.K = m.N;
+      sh.x = m.dy; sh.ldx = m.lddy; sh.w = (const void*)(uintptr_t)256; sh.ldw = ldt;  // W^T: 256-byte aligned
       dx_shape.push_back(sh);
       hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
       hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K);
@@ -709,23 +730,89 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
   hp.work_items = 0;
   hp.chain_launches = 0;
   std::string name;
+  hp.tp_chain.assign(G, RowLaunch{});
   if (!dxs.empty()) {
+    // the transposes of W, then dX on the forward kernels (direct-to-LDS when
+    // dY rows and N are 16-byte multiples)
+    const size_t toff = hp.blob.add(tps.data(), tps.size() * sizeof(TransposeItem));
+    for (size_t i = 0; i < tps.size(); ++i)
+      hp.scratch_fixups.push_back(toff + i * sizeof(TransposeItem) + offsetof(TransposeItem, dst));
+    const int32_t cap = device_cu_count() * 4;
+    hp.tp = RowLaunch{toff, toff, 0, (int32_t)tps.size(), std::max(1, std::min((int32_t)tps.size(), cap))};
+    int prev = 0;
+    for (size_t i = 0; i < dx_ids.size(); ++i) {
+      hp.tp_chain[dx_ids[i]] = RowLaunch{toff, toff, prev, tp_end[i] - prev, std::max(1, std::min(tp_end[i] - prev, cap))};
+      prev = tp_end[i];
+    }
     GemmSet& gs = hp.gs[hp.n_gs++];
-    build_gemm_set(hp, gs, gemm_pick_config_trans(dt, dx_shape.data(), (int32_t)dx_shape.size()), 2, dxs, dx_ids, G,
+    build_gemm_set(hp, gs, gemm_pick_config(dt, dx_shape.data(), (int32_t)dx_shape.size(), false), 0, dxs, dx_ids, G,
                    OPTIMUS_ACT_NONE, false);
+    for (size_t i = 0; i < dxs.size(); ++i)
+      hp.scratch_fixups.push_back(gs.descs_off + i * sizeof(DevLinear) + offsetof(DevLinear, w));
     name = std::string(gs.cfg.name) + "_dgrad";
   }
+  hp.red_chain.assign(G, RowLaunch{});
   if (!dws.empty()) {
     GemmSet& gs = hp.gs[hp.n_gs++];
-    build_gemm_set(hp, gs, gemm_pick_config_trans(dt, dw_shape.data(), (int32_t)dw_shape.size()), 3, dws, dw_ids, G,
-                   OPTIMUS_ACT_NONE, false);
-    name += std::string(name.empty() ? "" : "+") + gs.cfg.name + "_wgrad";
+    // dW reduces over the batch: few output tiles, a long K. Split K so that
+    // the work items fill the resident workgroups about twice; the splits'
+    // fp32 partials are summed by one more launch. A split writes and the sum
+    // reads 8 bytes per output element for 2 * kchunk flops on it, so a split
+    // keeps at least kSplitMinK of K (the MFMA work stays well above the
+    // partial traffic).
+    const GemmConfig cfg = gemm_pick_config_trans(dt, dw_shape.data(), (int32_t)dw_shape.size(), true);
+    const int bk = cfg.variant == 3 ? 32 : 64;
+    int64_t tiles = 0, kmin = INT64_MAX;
+    for (const auto& sh : dw_shape) {
+      tiles += ((sh.M + cfg.bm - 1) / cfg.bm) * ((sh.N + cfg.bn - 1) / cfg.bn);
+      kmin = std::min<int64_t>(kmin, sh.K);
+    }
+    const int64_t slots = (int64_t)device_cu_count() * gemm_resident_per_cu(cfg, dt, OPTIMUS_ACT_NONE, false, 3);
+    int splits = 1;
+    constexpr int64_t kSplitMinK = 1024;
+    while (splits < 16 && tiles * splits < 2 * slots && kmin / (2 * splits) >= kSplitMinK) splits *= 2;
+    if (splits > 1) {
+      std::vector<SplitReduceItem> red;
+      for (size_t i = 0; i < dws.size(); ++i) {
+        DevLinear& o = dws[i];
+        const int64_t kc = ((o.K + splits - 1) / splits + bk - 1) / bk * bk;
+        o.kchunk = (int32_t)kc;
+        o.splits = splits;
+        const int64_t floats = (int64_t)splits * o.M * o.N + (int64_t)splits * o.M;
+        const size_t off = (hp.scratch_bytes + 255) & ~(size_t)255;
+        o.ws = (float*)(uintptr_t)off;
+        hp.scratch_bytes = off + (size_t)floats * sizeof(float);
+        // about 1024 groups of 4 columns per item
+        const int rows_per = std::max<int32_t>(1, 4096 / std::max<int32_t>(o.N, 1));
+        const int first = (int)red.size();
+        for (int32_t r0 = 0; r0 < o.M; r0 += rows_per)
+          red.push_back(SplitReduceItem{(const float*)(uintptr_t)off, o.y, o.xsum, o.ldy, o.M, o.N, splits, r0,
+                                        std::min<int32_t>(rows_per, o.M - r0), 0});
+        hp.red_chain[dw_ids[i]] = RowLaunch{0, 0, first, (int)red.size() - first, 0};
+      }
+      const size_t roff = hp.blob.add(red.data(), red.size() * sizeof(SplitReduceItem));
+      for (size_t i = 0; i < red.size(); ++i)
+        hp.scratch_fixups.push_back(roff + i * sizeof(SplitReduceItem) + offsetof(SplitReduceItem, ws));
+      const int32_t cap = device_cu_count() * 4;
+      hp.red = RowLaunch{roff, roff, 0, (int32_t)red.size(), std::max(1, std::min((int32_t)red.size(), cap))};
+      for (auto& c : hp.red_chain) {
+        c.descs_off = c.tiles_off = roff;
+        c.grid = std::max(1, std::min(c.num_tiles, cap));
+      }
+    }
+    build_gemm_set(hp, gs, cfg, 3, dws, dw_ids, G, OPTIMUS_ACT_NONE, false, splits);
+    for (size_t i = 0; i < dws.size() && splits > 1; ++i)
+      hp.scratch_fixups.push_back(gs.descs_off + i * sizeof(DevLinear) + offsetof(DevLinear, ws));
+    name += std::string(name.empty() ? "" : "+") + gs.cfg.name + "_wgrad" +
+            (splits > 1 ? "_split" + std::to_string(splits) : "");
   }
   for (int i = 0; i < hp.n_gs; ++i) {
     hp.work_items += hp.gs[i].real_tiles;
     for (const RowLaunch& c : hp.gs[i].chain) hp.chain_launches += c.num_tiles > 0 ? 1 : 0;
   }
-  hp.launches = std::max(hp.n_gs, 1);
+  for (const RowLaunch& c : hp.red_chain) hp.chain_launches += c.num_tiles > 0 ? 1 : 0;
+  for (const RowLaunch& c : hp.tp_chain) hp.chain_launches += c.num_tiles > 0 ? 1 : 0;
+  hp.launches = std::max(hp.n_gs, 1) + (hp.red.num_tiles > 0 ? 1 : 0) + (hp.tp.num_tiles > 0 ? 1 : 0);
   hp.grid = hp.n_gs ? hp.gs[0].grid : 0;
   hp.block = hp.n_gs ? hp.gs[0].cfg.threads : 0;
   hp.kernel = name.empty() ? "grouped_linear_backward_empty" : name;
@@ -1235,6 +1322,7 @@ struct optimus_plan_s {
   int device = 0;
   char* table = nullptr;       // device copy of hp.blob
   char* temps = nullptr;       // split-op-cat unfused temporaries (lazy)
+  char* scratch = nullptr;     // hp.scratch_bytes of plan-owned scratch
   bool temps_ready = false;
 };
 
@@ -1249,13 +1337,17 @@ static void rebase_soc(HostPlan& hp, char* table) {
   s->tasks = (const SocTask*)(table + (uintptr_t)s->tasks);
 }
 
-// Every pointer the planner stored as a blob offset, made a device address.
-static void rebase_fixups(HostPlan& hp, char* table) {
-  for (size_t off : hp.table_fixups) {
-    uintptr_t v;
-    memcpy(&v, hp.blob.bytes.data() + off, sizeof v);
-    v += (uintptr_t)table;
-    memcpy(hp.blob.bytes.data() + off, &v, sizeof v);
+// Every pointer the planner stored as a blob (or scratch) offset, made a device address.
+static void rebase_fixups(HostPlan& hp, char* table, char* scratch = nullptr) {
+  for (int pass = 0; pass < 2; ++pass) {
+    const std::vector<size_t>& list = pass ? hp.scratch_fixups : hp.table_fixups;
+    char* base = pass ? scratch : table;
+    for (size_t off : list) {
+      uintptr_t v;
+      memcpy(&v, hp.blob.bytes.data() + off, sizeof v);
+      v += (uintptr_t)base;
+      memcpy(hp.blob.bytes.data() + off, &v, sizeof v);
+    }
   }
 }
 
@@ -1299,13 +1391,19 @@ static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t st
     }
     case KIND_LINEAR:
     case KIND_LINBWD:
+      if (hp.tp.num_tiles > 0) {
+        hipError_t e = transpose_launch(hp.dt, at<TransposeItem>(table, hp.tp.descs_off), hp.tp.num_tiles, hp.tp.grid,
+                                        stream);
+        if (e != hipSuccess) return e;
+      }
       for (int i = 0; i < hp.n_gs; ++i) {
         const GemmSet& g = hp.gs[i];
         hipError_t e = gemm_launch(g.cfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(table, g.descs_off),
                                    at<GemmTile>(table, g.tiles_off), g.num_tiles, g.grid, stream, g.tr);
         if (e != hipSuccess) return e;
       }
-      return hipSuccess;
+      return splitk_reduce_launch(hp.dt, at<SplitReduceItem>(table, hp.red.descs_off), hp.red.num_tiles, hp.red.grid,
+                                  stream);
     case KIND_LN:
     case KIND_PW:
     case KIND_SOC:
@@ -1343,8 +1441,16 @@ static optimus_status make_plan(HostPlan&& hp, optimus_plan* out) {
     delete p;
     return hip_fail(e, "plan: device table allocation");
   }
+  if (p->hp.scratch_bytes) {
+    e = hipMalloc((void**)&p->scratch, p->hp.scratch_bytes);
+    if (e != hipSuccess) {
+      (void)hipFree(p->table);
+      delete p;
+      return hip_fail(e, "plan: scratch allocation");
+    }
+  }
   rebase_soc(p->hp, p->table);
-  rebase_fixups(p->hp, p->table);
+  rebase_fixups(p->hp, p->table, p->scratch);
   e = hipMemcpy(p->table, p->hp.blob.bytes.data(), p->hp.blob.bytes.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess) {
     optimus_status st = upload_copies(p->hp, p->table, nullptr, false);
@@ -1441,6 +1547,7 @@ extern "C" void optimus_plan_destroy(optimus_plan p) {
   const bool switched = hipGetDevice(&cur) == hipSuccess && cur != p->device && hipSetDevice(p->device) == hipSuccess;
   (void)hipFree(p->table);
   if (p->temps) (void)hipFree(p->temps);
+  if (p->scratch) (void)hipFree(p->scratch);
   if (switched) (void)hipSetDevice(cur);
   delete p;
 }
@@ -1491,12 +1598,21 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
         e = launch_fp8(hp, p->table, hp.q_scaled ? &hp.q_chain_amax[g] : nullptr, hp.q_chain[g], st);
       } else if (hp.kind == KIND_LINEAR || hp.kind == KIND_LINBWD) {
         e = hipSuccess;
+        if (!hp.tp_chain.empty() && hp.tp_chain[g].num_tiles > 0) {
+          const RowLaunch& c = hp.tp_chain[g];
+          e = transpose_launch(hp.dt, at<TransposeItem>(p->table, c.descs_off) + c.first_tile, c.num_tiles, c.grid, st);
+        }
         for (int i = 0; i < hp.n_gs && e == hipSuccess; ++i) {
           const GemmSet& gs = hp.gs[i];
           const RowLaunch& c = gs.chain[g];
           if (c.num_tiles > 0)
             e = gemm_launch(gs.cfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(p->table, gs.descs_off),
                             at<GemmTile>(p->table, gs.tiles_off) + c.first_tile, c.num_tiles, c.grid, st, gs.tr);
+        }
+        if (e == hipSuccess && !hp.red_chain.empty() && hp.red_chain[g].num_tiles > 0) {
+          const RowLaunch& r = hp.red_chain[g];
+          e = splitk_reduce_launch(hp.dt, at<SplitReduceItem>(p->table, r.descs_off) + r.first_tile, r.num_tiles,
+                                   r.grid, st);
         }
       } else {
         const RowLaunch& c = hp.rows_chain[g];
@@ -1596,8 +1712,10 @@ static optimus_status run_oneshot(HostPlan& hp, hipStream_t stream) {
     HIP_TRY(hipHostMalloc(&sg.host, n, hipHostMallocDefault), "one-shot: pinned staging");
     sg.cap = n;
   }
+  char* scratch = nullptr;
+  if (hp.scratch_bytes) HIP_TRY(hipMallocAsync((void**)&scratch, hp.scratch_bytes, stream), "one-shot: scratch");
   rebase_soc(hp, table);
-  rebase_fixups(hp, table);
+  rebase_fixups(hp, table, scratch);
   memcpy(sg.host, hp.blob.bytes.data(), hp.blob.bytes.size());
   HIP_TRY(hipMemcpyAsync(table, sg.host, hp.blob.bytes.size(), hipMemcpyHostToDevice, stream), "one-shot: upload");
   HIP_TRY(hipEventRecord(sg.ev, stream), "one-shot: event record");
@@ -1606,6 +1724,7 @@ static optimus_status run_oneshot(HostPlan& hp, hipStream_t stream) {
   if (st != OPTIMUS_OK) return st;
   hipError_t e = launch_grouped(hp, table, stream);
   (void)hipFreeAsync(table, stream);
+  if (scratch) (void)hipFreeAsync(scratch, stream);
   return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "one-shot: launch");
 }
 

@@ -28,7 +28,36 @@ struct DevLinear {
   // backward GEMMs: vec bit 2 = w 16-B loadable in its reduction-major layout;
   // xsum [M] receives the row sums of x over K (db beside dW), or NULL
   void* xsum;
+  // split reduction (dW over a long batch): tile.pad is the split index, the
+  // split covers k in [pad * kchunk, pad * kchunk + kchunk) and writes fp32
+  // partials to ws ([splits][M][N], then the row sums [splits][M]); 0 / NULL
+  // when not split
+  float* ws;
+  int32_t kchunk, splits;
 };
+
+// Sum of the split partials of one member over rows [row0, row0 + nrows):
+// y = sum_s ws[s] (rounded to the dtype), and the row sums into xsum.
+struct SplitReduceItem {
+  const float* ws;
+  void* y;
+  void* xsum;
+  int64_t ldy;
+  int32_t M, N, splits, row0, nrows, pad;
+};
+hipError_t splitk_reduce_launch(optimus_dtype dt, const SplitReduceItem* items, int32_t num_items, int32_t grid,
+                                hipStream_t stream);
+
+// One 64 x 64 tile of a grouped transpose: dst[c][r] = src[r][c] for src rows
+// [r0, r0 + 64) and columns [c0, c0 + 64), clipped to rows x cols.
+struct TransposeItem {
+  const void* src;
+  void* dst;
+  int64_t lds, ldd;
+  int32_t rows, cols, r0, c0;
+};
+hipError_t transpose_launch(optimus_dtype dt, const TransposeItem* items, int32_t num_items, int32_t grid,
+                            hipStream_t stream);
 
 // One GEMM work item: the BM x BN output tile (mb, nb) of member `member`;
 // member < 0 marks a padding entry that does no work.
@@ -105,7 +134,8 @@ int gemm_ln_max_n(optimus_dtype dt);
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream, int tr = 0);
 // Tile shape for the backward GEMMs (register-staged variants only).
-GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G);
+// split_k: the set's K will be split (dW over the batch), so take the large tile.
+GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k = false);
 // Workgroups of the instance gemm_launch would run that fit on one CU at once
 // (the HIP runtime's occupancy of its registers and LDS; cfg.occ if the query fails).
 int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, int tr = 0);

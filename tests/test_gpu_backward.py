@@ -107,7 +107,8 @@ def test_linear_backward(dtype, mode):
     ms = _linear_members(SHAPES, dtype, seed=500)
     info = _run_linear_bwd(ms, dtype, mode)
     if info is not None:
-        assert info["kind"] == 7 and info["launches"] == 2 and info["chain_launches"] == 2 * len(ms)
+        # W transposed, dX, dW (+ db) -- no split at these batches
+        assert info["kind"] == 7 and info["launches"] == 3 and info["chain_launches"] == 3 * len(ms)
     _check_linear_bwd(ms, dtype, f"{dtype} {mode}")
 
 
@@ -121,6 +122,25 @@ def test_linear_backward_every_tile(variant):
     for mode in ["grouped", "chain"]:
         _run_linear_bwd(ms, dtype, mode, variant=variant)
         _check_linear_bwd(ms, dtype, f"variant {variant} {mode}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
+def test_linear_backward_split_reduction(dtype, mode):
+    """Members with long batches only: dW (and db) reduce over the batch in
+    fp32 splits summed by one more launch; ragged widths, one member without
+    db beside members with it."""
+    say(f"[linear bwd split] {dtype} {mode}")
+    ms = _linear_members([(8192, 256, 512), (4096, 100, 72), (6000, 64, 136)], dtype, seed=525)
+    info = _run_linear_bwd(ms, dtype, mode)
+    if info is not None:
+        assert "_split" in info["kernel"] and info["launches"] == 4, info   # + the split reduction
+    _check_linear_bwd(ms, dtype, f"split {dtype} {mode}")
+    for m in ms:
+        m["db"] = None
+    ms2 = _linear_members([(4096, 136, 264), (2500, 40, 8)], dtype, seed=526)   # 2 splits at most
+    _run_linear_bwd(ms2, dtype, mode, want=("dx", "dw"))
+    _check_linear_bwd(ms2, dtype, f"split, no db {dtype} {mode}", want=("dx", "dw"))
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
