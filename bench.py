@@ -385,7 +385,7 @@ def traffic_from_profile(kernel, name):
         return None
     with open(path) as f:
         pmc = json.load(f)
-    if pmc.get("sources_sha256") != sources_hash(kernel_symbol(kernel)):
+    if pmc.get("sources_sha256") != sources_hash(kernel):
         return None
     return pmc.get("hbm_bytes_per_launch")
 
@@ -416,6 +416,8 @@ def pmc_summary(args):
     with open(line) as f:
         label = json.loads(f.read().splitlines()[-1])["roofline"]["kernel"]
     kernel, kernels = kernel_symbol(label), kernel_symbols(label)
+    if len(set(kernels)) != len(kernels):
+        raise SystemExit(f"bench.py: the kernels of {label} are not told apart by name")
     f_dir, w_dir, cf_dir, cw_dir = args.pmc_summary
     cfetch, _ = _pmc_per_dispatch(cf_dir, "FETCH_SIZE", COPY_KERNEL)
     cwrite, _ = _pmc_per_dispatch(cw_dir, "WRITE_SIZE", COPY_KERNEL)
@@ -434,7 +436,7 @@ def pmc_summary(args):
            "copy_bytes": COPY_BYTES, "copy_fetch_kib": round(cfetch, 1), "copy_write_kib": round(cwrite, 1),
            "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
            "hbm_bytes_per_launch": sum(v["hbm_bytes"] for v in per.values()),
-           "sources_sha256": sources_hash(kernel), "command": args.pmc_command}
+           "plan": label, "sources_sha256": sources_hash(label), "command": args.pmc_command}
     if len(kernels) > 1:
         out["per_kernel"] = per
         out["note"] = "one execution of the plan is these launches; hbm_bytes_per_launch is their sum"
@@ -462,17 +464,43 @@ def copy_probe():
     print(json.dumps({"copy_probe_bytes": COPY_BYTES, "copies": 5}))
 
 
-def kernel_symbols(label):
-    """Symbols of every kernel one execution of a plan launches, in order (a
-    scaled fp8 quantize is an amax launch, then the convert launch)."""
+def plan_kernels(label):
+    """(a substring of the kernel's name, its source file) for every kernel one
+    execution of a plan launches, in order: the scaled fp8 quantize is an amax
+    launch then the convert launch; a Linear backward the transpose of W, the
+    dX GEMM, the dW GEMM (its transposing instance, template argument 3) and,
+    when its batch is split, the reduction; a LayerNorm backward its row kernel
+    then the finalize of dgamma / dbeta."""
     if label.startswith("grouped_quantize_fp8_scaled"):
-        return ["grouped_fp8_amax_kernel", "grouped_quantize_fp8_scaled_kernel"]
-    return [kernel_symbol(label)]
+        return [("grouped_fp8_amax_kernel", "kernels_fp8.hip"), ("grouped_quantize_fp8_scaled_kernel", "kernels_fp8.hip")]
+    if "_dgrad" in label or "_wgrad" in label:
+        ks = []
+        for part in label.split("+"):
+            if part.endswith("_dgrad"):
+                ks.append(("grouped_transpose_kernel", "kernels_gemm.hip"))
+                ks.append(("grouped_gemm_dma_kernel", "kernels_gemm.hip") if part.startswith("grouped_gemm_dma")
+                          else ("0, 0>(optimus::DevLinear", "kernels_gemm.hip"))
+            else:
+                ks.append(("0, 3>(optimus::DevLinear", "kernels_gemm.hip"))
+                if "_split" in part:
+                    ks.append(("splitk_reduce_kernel", "kernels_gemm.hip"))
+        return ks
+    if label.startswith("grouped_layernorm_backward"):
+        return [("grouped_layernorm_backward_kernel", "kernels_backward.hip"),
+                ("grad_finalize_kernel", "kernels_backward.hip")]
+    sym = kernel_symbol(label)
+    return [(sym, KERNEL_SOURCES[sym])]
+
+
+def kernel_symbols(label):
+    return [k for k, _ in plan_kernels(label)]
 
 
 def kernel_symbol(label):
     """Symbol name of the (last) kernel behind a plan's kernel label."""
-    for prefix, sym in (("grouped_quantize_fp8_scaled", "grouped_quantize_fp8_scaled_kernel"),
+    for prefix, sym in (("grouped_layernorm_backward", "grouped_layernorm_backward_kernel"),
+                        ("grouped_act_backward", "grouped_act_backward_kernel"),
+                        ("grouped_quantize_fp8_scaled", "grouped_quantize_fp8_scaled_kernel"),
                         ("grouped_quantize_fp8", "grouped_quantize_fp8_kernel"),
                         ("grouped_dequantize_fp8", "grouped_dequantize_fp8_kernel"),
                         ("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
@@ -491,13 +519,17 @@ KERNEL_SOURCES = {
     "grouped_layernorm_kernel": "kernels_rowwise.hip", "grouped_pointwise_kernel": "kernels_rowwise.hip",
     "grouped_quantize_fp8_scaled_kernel": "kernels_fp8.hip", "grouped_quantize_fp8_kernel": "kernels_fp8.hip",
     "grouped_dequantize_fp8_kernel": "kernels_fp8.hip", "grouped_fp8_amax_kernel": "kernels_fp8.hip",
+    "grouped_layernorm_backward_kernel": "kernels_backward.hip", "grouped_act_backward_kernel": "kernels_backward.hip",
 }
 
 
-def sources_hash(kernel):
+def sources_hash(label):
+    """sha256 of the sources of every kernel a plan launches (their
+    translation units and the shared headers)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_02945_amd", "csrc")
-    for fn in sorted([KERNEL_SOURCES[kernel], "device_common.h", "optimus_internal.h"]):
+    files = sorted({f for _, f in plan_kernels(label)} | {"device_common.h", "optimus_internal.h"})
+    for fn in files:
         with open(os.path.join(csrc, fn), "rb") as f:
             h.update(fn.encode() + f.read())
     return h.hexdigest()
