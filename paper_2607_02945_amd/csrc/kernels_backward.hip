@@ -196,14 +196,27 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
     }
   }
   if (params) {
+    // the rpw row slots of a wave hold the same columns (lanes li + k * L):
+    // add them up across the wave first, then one slot per wave goes to LDS
+    for (int off = L; off < 64; off <<= 1) {
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-      const int c = j * L + li;
-      if (c < cpr) {
+      for (int j = 0; j < MAXC; ++j)
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          atomicAdd(&sPart[c * VEC + e], accG[j][e]);
-          atomicAdd(&sPart[d.cols + c * VEC + e], accB[j][e]);
+          accG[j][e] += __shfl_xor(accG[j][e], off);
+          accB[j][e] += __shfl_xor(accB[j][e], off);
+        }
+    }
+    if (sub == 0) {
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        const int c = j * L + li;
+        if (c < cpr) {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            atomicAdd(&sPart[c * VEC + e], accG[j][e]);
+            atomicAdd(&sPart[d.cols + c * VEC + e], accB[j][e]);
+          }
         }
       }
     }
