@@ -477,9 +477,10 @@ def plan_kernels(label):
         ks = []
         for part in label.split("+"):
             if part.endswith("_dgrad"):
+                # both GEMM kernels end their template arguments with the
+                # operand layout: 0 for dX, 3 (both transposed) for dW
                 ks.append(("grouped_transpose_kernel", "kernels_gemm.hip"))
-                ks.append(("grouped_gemm_dma_kernel", "kernels_gemm.hip") if part.startswith("grouped_gemm_dma")
-                          else ("0, 0>(optimus::DevLinear", "kernels_gemm.hip"))
+                ks.append(("0, 0>(optimus::DevLinear", "kernels_gemm.hip"))
             else:
                 ks.append(("0, 3>(optimus::DevLinear", "kernels_gemm.hip"))
                 if "_split" in part:

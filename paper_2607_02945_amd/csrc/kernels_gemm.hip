@@ -651,9 +651,12 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes) {
 // the record count returns zeros. The compiler is not told that this writes
 // LDS, so the K loop's waits are placed by hand.
 __device__ __forceinline__ void lds_dma16(const i32x4& rsrc, uint32_t voff, uint32_t lds_addr) {
+  // the address is wave-uniform; readfirstlane only tells the compiler so
+  // where its analysis cannot see it
+  const uint32_t a = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_addr);
   __asm__ volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                    :
-                   : "v"(voff), "s"(rsrc), "s"(lds_addr)
+                   : "v"(voff), "s"(rsrc), "s"(a)
                    : "memory", "m0");
 }
 
@@ -690,7 +693,26 @@ struct DmaShape {
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be a multiple of 32");
   static_assert(NW * HR * PITCH <= STAGE, "epilogue staging must fit in one stage buffer");
   static_assert((HR * CPRW) % 64 == 0 && CPRW >= 8, "staged rows leave in whole 64-lane passes");
+  // Reduction-major operands (both stored [k][row]): a stage holds BK rows of
+  // BM (BN) values, RB bytes each; one DMA instruction fills RPI of them, CPR
+  // chunks per row. Chunk c of staged row r sits at position c ^ 4 (r mod 4),
+  // so the four rows one transposing fragment read touches fall in four
+  // distinct 64-byte bank windows; a wave's rows stay 0 mod 4 apart between
+  // its instructions, so the swizzle of a lane's chunk is fixed.
+  static constexpr int RB = BM * 2, RPI = 1024 / RB, CPR = RB / 16;
+  static_assert(RPI * RB == 1024 && (NW * RPI) % 4 == 0 && CPR >= 16, "reduction-major staging layout");
 };
+
+// Transposing LDS read (gfx950): in each group of 16 lanes, element r of lane
+// 4a + b is element b of the 8 bytes that lane a + 4r addressed. Lanes that
+// address four consecutive values of four consecutive reduction rows thus
+// receive four reduction values of one output row each.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2 lds_read_tr16(const char* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(
+      (__attribute__((address_space(3))) char*)p));
+  return __builtin_bit_cast(u32x2, v);
+}
 
 // What one K step's DMA instructions of a member tile need: the buffer
 // resources of its x and w rows, this lane's byte offsets (already sent out of
@@ -706,12 +728,34 @@ struct DmaLoads {
 
 // First K step of a tile: tiles that share an x panel (same mb, run side by
 // side on one L2) walk K in step so that the panel is fetched once; tiles
-// that share a weight block (same nb) start apart.
-__device__ __forceinline__ int dma_rot(const GemmTile& tile, int nk) { return tile.mb % nk; }
+// that share a weight block (same nb, a block that stays in L2) start apart.
+// With both operands reduction-major (the weight gradient) both panels are
+// long streams through the batch: every tile starts at step 0, so the tiles
+// of one member that run side by side share both.
+template <int TR>
+__device__ __forceinline__ int dma_rot(const GemmTile& tile, int nk) { return TR ? 0 : tile.mb % nk; }
 
-template <int BM, int BN, int NW>
-__device__ __forceinline__ DmaLoads dma_loads(const DevLinear& d, int m0, int n0, int k0, int lr, int kch) {
+template <int BM, int BN, int NW, int TR>
+__device__ __forceinline__ DmaLoads dma_loads(const DevLinear& d, int m0, int n0, int kbeg, int kend, int k0, int lr,
+                                              int kch) {
   DmaLoads L;
+  if constexpr (TR != 0) {
+    // rows are reduction steps [kbeg, kend) starting at the tile's first
+    // column; the record count ends at the last valid column of the last
+    // row, so rows past kend and chunks past the last column read as zero
+    constexpr int RPI = 1024 / (BM * 2);
+    const int rows = kend - kbeg;
+    L.xp = (const bf16_t*)d.x + (int64_t)kbeg * d.ldx + m0;
+    L.wp = (const bf16_t*)d.w + (int64_t)kbeg * d.ldw + n0;
+    L.xbytes = (uint32_t)(((int64_t)(rows - 1) * d.ldx + (d.M - m0)) * 2);
+    L.wbytes = (uint32_t)(((int64_t)(rows - 1) * d.ldw + (d.N - n0)) * 2);
+    L.sx = (uint32_t)(((int64_t)(k0 + lr) * d.ldx + kch) * 2);
+    L.sw = (uint32_t)(((int64_t)(k0 + lr) * d.ldw + kch) * 2);
+    L.xrow = (uint32_t)(NW * RPI * d.ldx * 2);
+    L.wrow = (uint32_t)(NW * RPI * d.ldw * 2);
+    L.k0 = k0;
+    return L;
+  }
   const int Mr = d.M - m0, Nr = d.N - n0;
   L.xp = (const bf16_t*)d.x + (int64_t)m0 * d.ldx;
   L.wp = (const bf16_t*)d.w + (int64_t)n0 * d.ldw;
@@ -726,8 +770,22 @@ __device__ __forceinline__ DmaLoads dma_loads(const DevLinear& d, int m0, int n0
   return L;
 }
 
+// The reduction range of a work item: all of K, or (transposed operands with
+// a split reduction) split tile.pad of it.
+template <int TR>
+__device__ __forceinline__ void dma_krange(const DevLinear& d, const GemmTile& tile, int& kbeg, int& kend) {
+  kbeg = 0;
+  kend = d.K;
+  if constexpr (TR != 0) {
+    if (d.ws) {
+      kbeg = tile.pad * d.kchunk;
+      kend = min(d.K, kbeg + d.kchunk);
+    }
+  }
+}
+
 // The first K step's loads of work item t (k0 < 0 past the end or for a padding entry).
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, int TR>
 __device__ __forceinline__ DmaLoads dma_first(const DevLinear* __restrict__ descs, const GemmTile* __restrict__ tiles,
                                               int t, int num_tiles, int lr, int kch) {
   DmaLoads L;
@@ -736,17 +794,22 @@ __device__ __forceinline__ DmaLoads dma_first(const DevLinear* __restrict__ desc
   const GemmTile tile = tiles[t];
   if (tile.member < 0) return L;
   const DevLinear& d = descs[tile.member];
-  const int nk = (d.K + 63) / 64;
-  return dma_loads<BM, BN, NW>(d, tile.mb * BM, tile.nb * BN, dma_rot(tile, nk) * 64, lr, kch);
+  int kbeg, kend;
+  dma_krange<TR>(d, tile, kbeg, kend);
+  const int nk = (kend - kbeg + 63) / 64;
+  return dma_loads<BM, BN, NW, TR>(d, tile.mb * BM, tile.nb * BN, kbeg, kend, dma_rot<TR>(tile, nk) * 64, lr, kch);
 }
 
-template <int BM, int BN, int WM, int WN, int ACT>
+template <int BM, int BN, int WM, int WN, int ACT, int TR = 0>
 __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const DevLinear* __restrict__ descs,
                                                                        const GemmTile* __restrict__ tiles,
                                                                        int32_t num_tiles) {
   using S = DmaShape<BM, BN, WM, WN>;
   constexpr int NW = S::NW, A = ACT & 7;
   constexpr bool LN = (ACT & 8) != 0;  // the row LayerNorm is fused into the epilogue
+  // TR = 3: x and w both stored reduction-major (the weight gradient
+  // dW = dY^T X: x = dY, w = X); no bias, activation or LayerNorm
+  static_assert(TR == 0 || (TR == 3 && ACT == 0 && BM == BN), "transposed instances: both operands, no epilogue ops");
   extern __shared__ __align__(16) char smem[];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
   float* sBias = (float*)(smem + S::BIAS);
@@ -756,9 +819,10 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN, l32 = lane & 31, lh = lane >> 5;
   // this lane's first staged row and its (swizzled) chunk; each further DMA
-  // instruction of the wave is NW * 8 rows further down, with the same swizzle
-  const int lr = wave * 8 + (lane >> 3);
-  const int kch = ((lane & 7) ^ swz(lr)) << 3;
+  // instruction of the wave is NW * 8 rows (reduction-major: NW * RPI rows)
+  // further down, with the same swizzle
+  const int lr = TR ? wave * S::RPI + lane / S::CPR : wave * 8 + (lane >> 3);
+  const int kch = TR ? ((lane % S::CPR) ^ (4 * (lr & 3))) << 3 : ((lane & 7) ^ swz(lr)) << 3;
 
   int t = blockIdx.x;
   if ((gridDim.x & 7) == 0) t = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
@@ -769,6 +833,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     return q < S::XI ? wave * 8 * 128 + q * NW * 8 * 128 : S::XBYTES + wave * 8 * 128 + (q - S::XI) * NW * 8 * 128;
   };
   auto gofs = [&](const DmaLoads& L, int q) {
+    if constexpr (TR != 0) return q < S::XI ? L.sx + q * L.xrow : L.sw + (q - S::XI) * L.wrow;
     return q < S::XI ? L.sx + q * L.xrow + L.k0 * 2 : L.sw + (q - S::XI) * L.wrow + L.k0 * 2;
   };
   // every load of one K step into `stage`
@@ -780,7 +845,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
 
   int sbase = 0;  // stage holding the current tile's first K step
   {
-    const DmaLoads L = dma_first<BM, BN, NW>(descs, tiles, t, num_tiles, lr, kch);
+    const DmaLoads L = dma_first<BM, BN, NW, TR>(descs, tiles, t, num_tiles, lr, kch);
     if (L.k0 >= 0) issue_all(L, 0);
   }
 
@@ -788,14 +853,23 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     const GemmTile tile = tiles[t];
     if (tile.member < 0) {
       // padding (only at the end of the list): nothing was loaded for it
-      const DmaLoads L = dma_first<BM, BN, NW>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
+      const DmaLoads L = dma_first<BM, BN, NW, TR>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
       if (L.k0 >= 0) issue_all(L, sbase);
       continue;
     }
     const DevLinear& d = descs[tile.member];
     const int m0 = tile.mb * BM, n0 = tile.nb * BN;
     const int Mr = d.M - m0, Nr = d.N - n0;
-    const int nk = (d.K + S::BK - 1) / S::BK, rot = dma_rot(tile, nk);
+    int kbeg, kend;
+    dma_krange<TR>(d, tile, kbeg, kend);
+    const int nk = (kend - kbeg + S::BK - 1) / S::BK, rot = dma_rot<TR>(tile, nk);
+    // reduction-major x: the tiles of the first column block also sum each x
+    // row over the reduction (db beside dW), from the fragments that the
+    // waves of the first wave column read anyway
+    const bool rsum = TR != 0 && d.xsum && tile.nb == 0 && wn == 0;
+    float rs[S::FM];
+#pragma unroll
+    for (int i = 0; i < S::FM; ++i) rs[i] = 0.f;
 
     f32x16 acc[S::FM][S::FN];
 #pragma unroll
@@ -814,16 +888,36 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       const char* swp = sxp + S::XBYTES;
       u32x4 a[2][S::FN], b[2][S::FM];
       auto frag = [&](int kc, int set) {
-        const int lc = kc * 2 + lh;
+        if constexpr (TR != 0) {
+          // lane 16 g + s: reduction rows 16 kc + 8 (g / 2) + s / 4 (+ 4 for
+          // the second read), values 4 (s mod 4) .. + 3 of the fragment's 16
+          // columns [16 (g mod 2), + 16); the reads hand lane l the eight
+          // reduction values 8 (l / 32) .. + 7 of fragment row l mod 32
+          const int s16 = lane & 15, t4 = s16 >> 2;
+          const int kr = kc * 16 + 8 * lh + t4;
+          const int cl = 2 * ((lane >> 4) & 1) + ((s16 & 3) >> 1);  // chunk within the 32-column fragment
+          const int lo = kr * S::RB + cl * 16 + 8 * (s16 & 1);
+          auto tr = [&](const char* base, int rowbase) {
+            const char* p = base + lo + (((rowbase >> 5) ^ t4) << 6);
+            const u32x2 v0 = lds_read_tr16(p), v1 = lds_read_tr16(p + 4 * S::RB);
+            return u32x4{v0.x, v0.y, v1.x, v1.y};
+          };
 #pragma unroll
-        for (int j = 0; j < S::FN; ++j) {
-          const int row = wn * S::TN + j * 32 + l32;
-          a[set][j] = *(const u32x4*)(swp + row * 128 + ((lc ^ swz(row)) << 4));
-        }
+          for (int j = 0; j < S::FN; ++j) a[set][j] = tr(swp, wn * S::TN + j * 32);
 #pragma unroll
-        for (int i = 0; i < S::FM; ++i) {
-          const int row = wm * S::TM + i * 32 + l32;
-          b[set][i] = *(const u32x4*)(sxp + row * 128 + ((lc ^ swz(row)) << 4));
+          for (int i = 0; i < S::FM; ++i) b[set][i] = tr(sxp, wm * S::TM + i * 32);
+        } else {
+          const int lc = kc * 2 + lh;
+#pragma unroll
+          for (int j = 0; j < S::FN; ++j) {
+            const int row = wn * S::TN + j * 32 + l32;
+            a[set][j] = *(const u32x4*)(swp + row * 128 + ((lc ^ swz(row)) << 4));
+          }
+#pragma unroll
+          for (int i = 0; i < S::FM; ++i) {
+            const int row = wm * S::TM + i * 32 + l32;
+            b[set][i] = *(const u32x4*)(sxp + row * 128 + ((lc ^ swz(row)) << 4));
+          }
         }
       };
       const bool go = L.k0 >= 0;
@@ -841,6 +935,17 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
         for (int i = 0; i < S::FM; ++i)
 #pragma unroll
           for (int j = 0; j < S::FN; ++j) Mfma<bf16_t>::run(a[kc & 1][j], b[kc & 1][i], acc[i][j]);
+        if constexpr (TR != 0) {
+          if (rsum) {
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t v = b[kc & 1][i][e];
+                rs[i] += __uint_as_float(v << 16) + __uint_as_float(v & 0xffff0000u);
+              }
+          }
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
     };
@@ -864,9 +969,9 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       DmaLoads L;
       if (kb + 1 < nk) {
         const int q = kb + 1 + rot;
-        L = dma_loads<BM, BN, NW>(d, m0, n0, (q >= nk ? q - nk : q) * S::BK, lr, kch);
+        L = dma_loads<BM, BN, NW, TR>(d, m0, n0, kbeg, kend, (q >= nk ? q - nk : q) * S::BK, lr, kch);
       } else {
-        L = dma_first<BM, BN, NW>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
+        L = dma_first<BM, BN, NW, TR>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
       }
       step(stage, L, stage ^ 1);
       if (kb == 0 && tid < BN) {
@@ -879,12 +984,55 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     }
     __syncthreads();  // every wave is done with the last stage (staging) and the bias is written
     if constexpr (LN) ln_rows<BM, BN, WM, WN>(acc, sBias, sGamma, sBeta, red, d);
+    if constexpr (TR != 0) {
+      if (rsum) {
+        // lanes l and l + 32 hold the two halves of row l mod 32's sum
+#pragma unroll
+        for (int i = 0; i < S::FM; ++i) {
+          const float v = rs[i] + __shfl_xor(rs[i], 32);
+          const int row = wm * S::TM + i * 32 + l32;
+          if (lh == 0 && row < Mr) {
+            if (d.ws)  // this split's share of the row sums
+              d.ws[(int64_t)d.splits * d.M * d.N + (int64_t)tile.pad * d.M + m0 + row] = v;
+            else
+              Elem<bf16_t>::store1(d.xsum, m0 + row, v);
+          }
+        }
+      }
+      if (d.ws) {
+        // fp32 partial tile straight from the accumulators: each lane holds
+        // four consecutive columns of one row per (i, j, quad)
+        float* wb = d.ws + ((int64_t)tile.pad * d.M + m0) * d.N + n0;
+        const bool v4 = (d.N & 3) == 0;
+#pragma unroll
+        for (int i = 0; i < S::FM; ++i) {
+          const int row = wm * S::TM + i * 32 + l32;
+          if (row >= Mr) continue;
+#pragma unroll
+          for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int col = wn * S::TN + j * 32 + 8 * q + 4 * lh;
+              float* p = wb + (int64_t)row * d.N + col;
+              if (v4 && col + 3 < Nr) {
+                *(OPTIMUS_GLOBAL f32x4*)p = f32x4{acc[i][j][q * 4 + 0], acc[i][j][q * 4 + 1], acc[i][j][q * 4 + 2],
+                                                 acc[i][j][q * 4 + 3]};
+              } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  if (col + e < Nr) ((OPTIMUS_GLOBAL float*)p)[e] = acc[i][j][q * 4 + e];
+              }
+            }
+        }
+      }
+    }
 
     // epilogue: bias + activation + rounding into this wave's staging slice,
     // then whole 16-byte pieces of y rows leave in coalesced stores. Every
     // address is one lane base plus constants and every bound a per-tile
     // scalar, so nothing lane-dependent stays live across the tile loop.
-    {
+    // (A split reduction has written its partial tile instead.)
+    if (!(TR != 0 && d.ws)) {
       constexpr int RPP = 64 / S::CPRW;  // staged rows per store pass
       // opaque copies: computed here, per tile, instead of being hoisted out
       // of the tile loop and kept live across the K loop
@@ -1338,6 +1486,21 @@ static bool gemm_dma_ok(const optimus_linear_desc* d, int32_t G) {
   return true;
 }
 
+// Transposed operands on the direct-to-LDS tiles: bf16 x and w stored
+// reduction-major ([K][M] and [K][N]) with 16-byte aligned rows, M and N
+// multiples of 8 (no chunk straddles a row's end), and the offsets of a
+// whole reduction range below 2^31.
+static bool gemm_dma_trans_ok(const optimus_linear_desc* d, int32_t G) {
+  for (int g = 0; g < G; ++g) {
+    if (d[g].M % 8 || d[g].N % 8 || d[g].ldx % 8 || d[g].ldw % 8 || ((uintptr_t)d[g].x & 15) ||
+        ((uintptr_t)d[g].w & 15))
+      return false;
+    if ((d[g].K + 128) * d[g].ldx * 2 >= (int64_t)1 << 31 || (d[g].K + 128) * d[g].ldw * 2 >= (int64_t)1 << 31)
+      return false;
+  }
+  return true;
+}
+
 int gemm_ln_max_n(optimus_dtype dt) { return dt == OPTIMUS_F32 ? 128 : 256; }
 
 GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln) {
@@ -1462,6 +1625,17 @@ static hipError_t launch_trans(int tr, const DevLinear* descs, const GemmTile* t
 }
 
 template <int BM, int BN, int WM, int WN>
+static hipError_t launch_dma_trans(int tr, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
+                                   hipStream_t stream, int* occ) {
+  using S = DmaShape<BM, BN, WM, WN>;
+  if (tr == 3)
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 0, 3>), S::LDS_BYTES, S::NT)
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN>
 static hipError_t launch_dma(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
                              int32_t grid, hipStream_t stream, int* occ) {
   using S = DmaShape<BM, BN, WM, WN>;
@@ -1492,6 +1666,8 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
       case 1: return launch_trans<bf16_t, 128, 128, 64, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
       case 2: return launch_trans<bf16_t, 256, 256, 64, 2, 4, 2>(tr, descs, tiles, n, grid, stream, occ);
       case 3: return launch_trans<float, 64, 64, 32, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
+      case 4: return launch_dma_trans<256, 256, 2, 4>(tr, descs, tiles, n, grid, stream, occ);
+      case 5: return launch_dma_trans<128, 128, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
       case 6: return launch_trans<float, 64, 128, 64, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
       default: return hipErrorInvalidValue;
     }
@@ -1518,9 +1694,11 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
   return gemm_dispatch(cfg, dt, act, ln, tr, descs, tiles, num_tiles, grid, stream, nullptr);
 }
 
-// Backward GEMMs (transposed operands): the register-staged tiles -- 256x256
-// from half a tile per CU on, else 128x128; fp32 64x64.
-GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k) {
+// Backward GEMMs (transposed operands): 256x256 from half a tile per CU on,
+// else 128x128, direct-to-LDS when every member allows it, else register-
+// staged; fp32 64x64.
+GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k,
+                                  int tile) {
   double tiles256 = 0.0, area = 0.0;
   for (int g = 0; g < G; ++g) {
     tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
@@ -1530,11 +1708,18 @@ GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d
   // (N of 64 or 128) leave most of a large tile idle
   const double fill256 = area / (tiles256 * 65536.0);
   // a split reduction fills the machine with the large tile's better per-tile rate
-  int v = dt == OPTIMUS_F32 ? 3 : (fill256 >= 0.75 && (split_k || tiles256 >= 0.5 * device_cu_count()) ? 2 : 1);
+  const bool dma = dt == OPTIMUS_BF16 && gemm_dma_trans_ok(d, G);
+  // tile = 256 or 128 asks for that bf16 tile edge; 0 chooses by the fill rule
+  const bool big = tile ? tile == 256 : fill256 >= 0.75 && (split_k || tiles256 >= 0.5 * device_cu_count());
+  int v = dt == OPTIMUS_F32 ? 3 : big ? (dma ? 4 : 2) : (dma ? 5 : 1);
+  // OPTIMUS_GEMM_VARIANT pins the tile as for the forward (1, 2 register-
+  // staged, 4, 5 direct-to-LDS where allowed; fp32 3, 6)
   const char* f = getenv("OPTIMUS_GEMM_VARIANT");
   char* end = nullptr;
   const long want = f ? strtol(f, &end, 10) : -1;
-  if (f && end && *end == 0 && (dt == OPTIMUS_F32 ? (want == 3 || want == 6) : (want == 1 || want == 2))) v = (int)want;
+  const bool ok = dt == OPTIMUS_F32 ? (want == 3 || want == 6)
+                                    : (want == 1 || want == 2 || ((want == 4 || want == 5) && dma));
+  if (f && end && *end == 0 && ok) v = (int)want;
   const GemmVariant& k = kVariants[v];
   return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
 }

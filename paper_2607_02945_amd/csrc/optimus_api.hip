@@ -721,6 +721,7 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       dw_ids.push_back(g);
       optimus_linear_desc sh{};
       sh.M = m.N; sh.N = m.K; sh.K = m.M;
+      sh.x = m.dy; sh.ldx = m.lddy; sh.w = m.x; sh.ldw = m.ldx;  // both reduction-major
       dw_shape.push_back(sh);
       hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
       hp.bytes += (double)s * ((double)m.M * m.N + (double)m.M * m.K + (double)m.N * m.K + (m.db ? (double)m.N : 0.0));
@@ -754,23 +755,79 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
   hp.red_chain.assign(G, RowLaunch{});
   if (!dws.empty()) {
     GemmSet& gs = hp.gs[hp.n_gs++];
-    // dW reduces over the batch: few output tiles, a long K. Split K so that
-    // the work items fill the resident workgroups about twice; the splits'
-    // fp32 partials are summed by one more launch. A split writes and the sum
-    // reads 8 bytes per output element for 2 * kchunk flops on it, so a split
-    // keeps at least kSplitMinK of K (the MFMA work stays well above the
-    // partial traffic).
-    const GemmConfig cfg = gemm_pick_config_trans(dt, dw_shape.data(), (int32_t)dw_shape.size(), true);
-    const int bk = cfg.variant == 3 ? 32 : 64;
-    int64_t tiles = 0, kmin = INT64_MAX;
-    for (const auto& sh : dw_shape) {
-      tiles += ((sh.M + cfg.bm - 1) / cfg.bm) * ((sh.N + cfg.bn - 1) / cfg.bn);
-      kmin = std::min<int64_t>(kmin, sh.K);
-    }
-    const int64_t slots = (int64_t)device_cu_count() * gemm_resident_per_cu(cfg, dt, OPTIMUS_ACT_NONE, false, 3);
+    // dW reduces over the batch: few output tiles, a long K. Splitting K into
+    // `splits` ranges multiplies the work items (split index fastest, as
+    // build_gemm_set lays them out); their fp32 partials cost one write by
+    // the GEMM and one read by the reduce launch, 8 bytes per output element
+    // and split. The tile edge (bf16: 256 or 128) and the split count are the
+    // pair with the least estimated time: the launch's makespan under its
+    // static schedule (item i on workgroup i mod grid) in K steps of one tile
+    // on one workgroup slot, plus the partial traffic and the reduce launch.
+    // Rates measured on MI355X: a direct-to-LDS K step at 4.6 TFLOP/s per CU
+    // (256x256) and 3.6 (128x128), the partials at 4.7 TB/s.
+    double out_elems = 0.0;
+    for (const auto& o : dws) out_elems += (double)o.M * o.N;
+    auto est_of = [&](const GemmConfig& c, int sp) {
+      const int bkc = c.variant == 3 ? 32 : 64;
+      const int occ = gemm_resident_per_cu(c, dt, OPTIMUS_ACT_NONE, false, 3);
+      const int64_t slots = (int64_t)device_cu_count() * occ;
+      const double cu_rate = c.variant == 4 ? 4.6e12 : c.variant == 5 ? 3.6e12
+                           : (c.variant == 3 || c.variant == 6) ? 0.4e12 : 3.0e12;
+      const double t_step = 2.0 * c.bm * c.bn * bkc / (cu_rate / occ);
+      std::vector<int64_t> steps;  // per work item, in list order
+      for (const auto& o : dws) {
+        const int64_t kc = ((o.K + sp - 1) / sp + bkc - 1) / bkc * bkc;
+        if ((int64_t)(sp - 1) * kc >= o.K) return -1.0;  // an empty split
+        const int64_t tiles = ((o.M + c.bm - 1) / c.bm) * ((o.N + c.bn - 1) / c.bn);
+        for (int64_t t = 0; t < tiles; ++t)
+          for (int k = 0; k < sp; ++k) steps.push_back((std::min<int64_t>(o.K, (k + 1) * kc) - k * kc + bkc - 1) / bkc);
+      }
+      const int64_t n8 = ((int64_t)steps.size() + 7) / 8 * 8;
+      int64_t grid = std::min<int64_t>(n8, slots);
+      if (grid >= 8) grid -= grid % 8;
+      grid = std::max<int64_t>(grid, 1);
+      std::vector<int64_t> load((size_t)grid, 0);
+      for (size_t i = 0; i < steps.size(); ++i) load[i % grid] += steps[i];
+      const int64_t makespan = *std::max_element(load.begin(), load.end());
+      // a split also costs the reduce launch (about 6 us of launch gap and ramp)
+      return (double)makespan * t_step + (sp > 1 ? sp * out_elems * 8.0 / 4.7e12 + 6e-6 : 0.0);
+    };
+    const int n_dw = (int32_t)dw_shape.size();
+    GemmConfig cfg = gemm_pick_config_trans(dt, dw_shape.data(), n_dw, true);
     int splits = 1;
-    constexpr int64_t kSplitMinK = 1024;
-    while (splits < 16 && tiles * splits < 2 * slots && kmin / (2 * splits) >= kSplitMinK) splits *= 2;
+    {
+      std::vector<GemmConfig> cands{cfg};
+      if (dt == OPTIMUS_BF16 && !getenv("OPTIMUS_GEMM_VARIANT"))
+        for (int edge : {256, 128}) {
+          const GemmConfig c = gemm_pick_config_trans(dt, dw_shape.data(), n_dw, true, edge);
+          if (c.variant != cfg.variant) cands.push_back(c);
+        }
+      double best = -1.0;
+      for (const GemmConfig& c : cands) {
+        int sp_best = 1;
+        double e_best = est_of(c, 1);
+        for (int sp = 2; sp <= 16; ++sp) {
+          const double e = est_of(c, sp);
+          if (e >= 0.0 && e < e_best * 0.99) {  // a split must pay for itself clearly
+            e_best = e;
+            sp_best = sp;
+          }
+        }
+        if (best < 0.0 || e_best < best * 0.99) {
+          best = e_best;
+          cfg = c;
+          splits = sp_best;
+        }
+      }
+    }
+    const int bk = cfg.variant == 3 ? 32 : 64;  // every split but the last a whole number of K steps
+    // OPTIMUS_WGRAD_SPLITS=<n> (1..16) pins the split count (tests and
+    // tuning) where no split comes out empty
+    if (const char* f = getenv("OPTIMUS_WGRAD_SPLITS")) {
+      char* end = nullptr;
+      const long want = strtol(f, &end, 10);
+      if (end && *end == 0 && want >= 1 && want <= 16 && est_of(cfg, (int)want) >= 0.0) splits = (int)want;
+    }
     if (splits > 1) {
       std::vector<SplitReduceItem> red;
       for (size_t i = 0; i < dws.size(); ++i) {

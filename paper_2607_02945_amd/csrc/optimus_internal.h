@@ -133,9 +133,12 @@ int gemm_ln_max_n(optimus_dtype dt);
 // reduction-major (dW = dY^T . X, with db from d.xsum).
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream, int tr = 0);
-// Tile shape for the backward GEMMs (register-staged variants only).
-// split_k: the set's K will be split (dW over the batch), so take the large tile.
-GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k = false);
+// Tile shape for the backward GEMMs with both operands reduction-major
+// (direct-to-LDS where every member allows it, else register-staged).
+// split_k: the set's K will be split (dW over the batch), so prefer the large
+// tile; tile = 256 or 128 asks for that bf16 tile edge instead of the rule.
+GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k = false,
+                                  int tile = 0);
 // Workgroups of the instance gemm_launch would run that fit on one CU at once
 // (the HIP runtime's occupancy of its registers and LDS; cfg.occ if the query fails).
 int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, int tr = 0);

@@ -107,34 +107,50 @@ def test_linear_backward(dtype, mode):
     ms = _linear_members(SHAPES, dtype, seed=500)
     info = _run_linear_bwd(ms, dtype, mode)
     if info is not None:
-        # W transposed, dX, dW (+ db) -- no split at these batches
-        assert info["kind"] == 7 and info["launches"] == 3 and info["chain_launches"] == 3 * len(ms)
+        # W transposed, dX, dW (+ db), and the reduction when dW's batch is split
+        n = 4 if "_split" in info["kernel"] else 3
+        assert info["kind"] == 7 and info["launches"] == n and info["chain_launches"] == n * len(ms), info
     _check_linear_bwd(ms, dtype, f"{dtype} {mode}")
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3, 6])
+def _wgrad_part(info):
+    return [p for p in info["kernel"].split("+") if p.endswith("_wgrad") or "_wgrad_split" in p][0]
+
+
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 5, 6])
 def test_linear_backward_every_tile(variant):
-    """Each tile shape of the backward GEMMs (bf16 128x128 and 256x256, fp32
-    64x64 and 64x128), grouped and chain."""
+    """Each tile shape of the backward GEMMs (bf16 128x128 and 256x256
+    register-staged, the same two direct-to-LDS with transposing fragment
+    reads, fp32 64x64 and 64x128), grouped and chain. The direct-to-LDS
+    tiles take widths that are multiples of 8 values, still ragged against
+    every tile and with batch tails."""
     dtype = "fp32" if variant in (3, 6) else "bf16"
     say(f"[linear bwd variant] {variant}")
-    ms = _linear_members([(700, 300, 260), (129, 64, 33), (257, 9, 520)], dtype, seed=510 + variant)
+    shapes = [(700, 296, 264), (129, 64, 32), (257, 8, 520)] if variant in (4, 5) else \
+        [(700, 300, 260), (129, 64, 33), (257, 9, 520)]
+    ms = _linear_members(shapes, dtype, seed=510 + variant)
     for mode in ["grouped", "chain"]:
-        _run_linear_bwd(ms, dtype, mode, variant=variant)
+        info = _run_linear_bwd(ms, dtype, mode, variant=variant)
+        assert ("dma" in _wgrad_part(info)) == (variant in (4, 5)), info
         _check_linear_bwd(ms, dtype, f"variant {variant} {mode}")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 @pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
-def test_linear_backward_split_reduction(dtype, mode):
+@pytest.mark.parametrize("aligned", [False, True])
+def test_linear_backward_split_reduction(dtype, mode, aligned):
     """Members with long batches only: dW (and db) reduce over the batch in
     fp32 splits summed by one more launch; ragged widths, one member without
-    db beside members with it."""
-    say(f"[linear bwd split] {dtype} {mode}")
-    ms = _linear_members([(8192, 256, 512), (4096, 100, 72), (6000, 64, 136)], dtype, seed=525)
+    db beside members with it. Aligned widths (multiples of 8 values) take
+    the direct-to-LDS dW tiles in bf16."""
+    say(f"[linear bwd split] {dtype} {mode} aligned={aligned}")
+    shapes = [(8192, 256, 512), (4096, 104, 72), (6000, 64, 136)] if aligned else \
+        [(8192, 256, 512), (4096, 100, 72), (6000, 64, 136)]
+    ms = _linear_members(shapes, dtype, seed=525)
     info = _run_linear_bwd(ms, dtype, mode)
     if info is not None:
         assert "_split" in info["kernel"] and info["launches"] == 4, info   # + the split reduction
+        assert ("dma" in _wgrad_part(info)) == (aligned and dtype == "bf16"), info
     _check_linear_bwd(ms, dtype, f"split {dtype} {mode}")
     for m in ms:
         m["db"] = None
@@ -319,3 +335,133 @@ def test_towers_backward_chain_of_groups():
         _, r_dw1, r_db1 = ORC.linear_backward(synth.exact64(t.x), synth.exact64(t.w1), dh64)
         assert_close(host64(dw1[i]), r_dw1, "bf16", f"tower {i} dW1")
         assert_close(host64(db1[i][None, :])[0], r_db1, "bf16", f"tower {i} db1")
+
+
+# ------------------------------------------------------------------ full-size backward op-groups
+def _dw_sampled(x64, w64, dy64, ns):
+    """dW rows ns and db[ns] of a whole batch: the oracle on dY's columns ns."""
+    _, dw_s, db_s = ORC.linear_backward(x64, w64[ns], np.ascontiguousarray(dy64[:, ns]))
+    return dw_s, db_s
+
+
+def _sample(n, k, seed):
+    g = synth.rng(seed)
+    return np.unique(np.concatenate([[0, n - 1], g.choice(n, size=min(n, k), replace=False)])).astype(np.int64)
+
+
+@pytest.mark.timeout(300)
+def test_large_group_backward_full_size_sampled():
+    """large_group's training backward at full size (32 members, batch 16384,
+    K = 1024, N in {256, 512, 1024}) as the benchmark runs it: tanh, LayerNorm
+    and Linear backward plans, one grouped launch set each. Per operator, the
+    oracle is fed the GPU's stored inputs: dX on sampled rows, dW / db on
+    sampled output rows over the whole batch, dgamma / dbeta over every row."""
+    say("[large_group bwd] G=32 B=16384 K=1024 bf16")
+    wl = synth.large_group(0)
+    ms = wl.members
+    bf = torch.bfloat16
+    xs, ws, bs = [dev(m.x) for m in ms], [dev(m.w) for m in ms], [dev(m.b) for m in ms]
+    gs, bes = [dev(g) for g in wl.gammas], [dev(b) for b in wl.betas]
+    y = [torch.empty((m.M, m.N), dtype=bf, device="cuda") for m in ms]
+    z = [torch.empty_like(v) for v in y]
+    B.optimus_plan_linear(xs, ws, bs, y, "none").execute()
+    B.optimus_plan_layernorm(y, z, gs, bes, wl.eps, "none").execute()
+    gen = torch.Generator(device="cuda").manual_seed(2)
+    dt_ = [torch.randn(v.shape, generator=gen, device="cuda").to(bf) for v in z]
+    dz, dy = [torch.empty_like(v) for v in z], [torch.empty_like(v) for v in y]
+    dx, dw, db = [torch.empty_like(x) for x in xs], [torch.empty_like(w) for w in ws], [torch.empty_like(b) for b in bs]
+    dgm, dbt = [torch.empty_like(g) for g in gs], [torch.empty_like(g) for g in gs]
+    torch.cuda.synchronize()
+    plans = [B.optimus_plan_act_backward(z, dt_, dz, "tanh"),
+             B.optimus_plan_layernorm_backward(y, dz, dy, gs, dgm, dbt, wl.eps),
+             B.optimus_plan_linear_backward(xs, ws, dy, dx, dw, db)]
+    lin_info = plans[2].info()
+    say(f"  linear backward plan: {lin_info['kernel']} launches={lin_info['launches']}")
+    for p in plans:
+        p.execute("grouped")
+    torch.cuda.synchronize()
+    rows = _sample(16384, 40, seed=63)
+    for i, m in enumerate(ms):
+        say(f"  member {i} N={m.N}")
+        z64, dt64 = host64(z[i]), host64(dt_[i])
+        assert_close(host64(dz[i])[rows], ORC.act_backward(z64[rows], dt64[rows], "tanh"), "bf16", f"member {i} dtanh")
+        y64, dz64 = host64(y[i]), host64(dz[i])
+        g64 = synth.exact64(wl.gammas[i])
+        r_dy, r_dg, r_db = ORC.layernorm_backward(y64, g64, dz64, wl.eps)
+        dy64 = host64(dy[i])
+        assert_close(dy64[rows], r_dy[rows], "bf16", f"member {i} LayerNorm dX")
+        assert_close(host64(dgm[i][None, :])[0], r_dg, "bf16", f"member {i} dgamma")
+        assert_close(host64(dbt[i][None, :])[0], r_db, "bf16", f"member {i} dbeta")
+        x64, w64 = synth.exact64(m.x), synth.exact64(m.w)
+        r_dx = ORC.linear_backward(x64[rows], w64, dy64[rows])[0]
+        assert_close(host64(dx[i])[rows], r_dx, "bf16", f"member {i} dX")
+        ns = _sample(m.N, 6, seed=64 + i)
+        r_dw, r_dbs = _dw_sampled(x64, w64, dy64, ns)
+        assert_close(host64(dw[i])[ns], r_dw, "bf16", f"member {i} dW rows")
+        assert_close(host64(db[i][None, :])[0][ns], r_dbs, "bf16", f"member {i} db")
+
+
+@pytest.mark.timeout(300)
+def test_towers_backward_full_size_sampled():
+    """The towers group's training backward at full size (26 towers, batch
+    4096) as the benchmark runs it: LayerNorm, layer 2, relu (in place) and
+    layer 1 backward plans; per operator against the oracle fed the GPU's
+    stored inputs, on sampled rows (dW / db: sampled output rows over the
+    whole batch; dgamma: every row)."""
+    say("[towers bwd] 26 towers B=4096 bf16")
+    wl = synth.towers(0)
+    T = wl.towers
+    bf = torch.bfloat16
+    xs = [dev(t.x) for t in T]
+    w1, b1, w2, b2 = ([dev(getattr(t, a)) for t in T] for a in ("w1", "b1", "w2", "b2"))
+    gm = [dev(t.gamma) for t in T]
+    hp = [torch.empty((4096, 512), dtype=bf, device="cuda") for _ in T]
+    h = [torch.empty_like(v) for v in hp]
+    o = [torch.empty((4096, 256), dtype=bf, device="cuda") for _ in T]
+    B.optimus_plan_linear(xs, w1, b1, hp, "none").execute()
+    B.optimus_plan_pointwise(hp, h, "relu").execute()
+    B.optimus_plan_linear(h, w2, b2, o, "none").execute()
+    gen = torch.Generator(device="cuda").manual_seed(1)
+    dz = [torch.randn(v.shape, generator=gen, device="cuda").to(bf) for v in o]
+    do, dh = [torch.empty_like(v) for v in o], [torch.empty_like(v) for v in h]
+    dx = [torch.empty_like(x) for x in xs]
+    dw1, dw2 = [torch.empty_like(w) for w in w1], [torch.empty_like(w) for w in w2]
+    db1, db2 = [torch.empty_like(b) for b in b1], [torch.empty_like(b) for b in b2]
+    dgm, dbt = [torch.empty_like(g) for g in gm], [torch.empty_like(g) for g in gm]
+    torch.cuda.synchronize()
+    ln_b = B.optimus_plan_layernorm_backward(o, dz, do, gm, dgm, dbt, wl.eps)
+    ln_b.execute("grouped")
+    l2_b = B.optimus_plan_linear_backward(h, w2, do, dh, dw2, db2)
+    l2_b.execute("grouped")
+    torch.cuda.synchronize()
+    dh_lin = [host64(v) for v in dh]   # layer 2's dX before the in-place relu backward
+    relu_b = B.optimus_plan_act_backward(hp, dh, dh, "relu")
+    l1_b = B.optimus_plan_linear_backward(xs, w1, dh, dx, dw1, db1)
+    say(f"  layer 2: {l2_b.info()['kernel']}; layer 1: {l1_b.info()['kernel']}")
+    relu_b.execute("grouped")
+    l1_b.execute("grouped")
+    torch.cuda.synchronize()
+    rows = _sample(4096, 48, seed=65)
+    for i, t in enumerate(T):
+        o64, dz64 = host64(o[i]), host64(dz[i])
+        r_do, r_dg, r_dbt = ORC.layernorm_backward(o64, synth.exact64(t.gamma), dz64, wl.eps)
+        do64 = host64(do[i])
+        assert_close(do64[rows], r_do[rows], "bf16", f"tower {i} LayerNorm dX")
+        assert_close(host64(dgm[i][None, :])[0], r_dg, "bf16", f"tower {i} dgamma")
+        assert_close(host64(dbt[i][None, :])[0], r_dbt, "bf16", f"tower {i} dbeta")
+        h64, w2_64 = host64(h[i]), synth.exact64(t.w2)
+        assert_close(dh_lin[i][rows], ORC.linear_backward(h64[rows], w2_64, do64[rows])[0], "bf16", f"tower {i} dH")
+        ns = _sample(256, 6, seed=66 + i)
+        r_dw2, r_db2 = _dw_sampled(h64, w2_64, do64, ns)
+        assert_close(host64(dw2[i])[ns], r_dw2, "bf16", f"tower {i} dW2 rows")
+        assert_close(host64(db2[i][None, :])[0][ns], r_db2, "bf16", f"tower {i} db2")
+        dhp64 = host64(dh[i])
+        assert_close(dhp64[rows], ORC.act_backward(host64(hp[i])[rows], dh_lin[i][rows], "relu"), "bf16",
+                     f"tower {i} drelu")
+        x64, w1_64 = synth.exact64(t.x), synth.exact64(t.w1)
+        assert_close(host64(dx[i])[rows], ORC.linear_backward(x64[rows], w1_64, dhp64[rows])[0], "bf16",
+                     f"tower {i} dX")
+        ns = _sample(512, 6, seed=92 + i)
+        r_dw1, r_db1 = _dw_sampled(x64, w1_64, dhp64, ns)
+        assert_close(host64(dw1[i])[ns], r_dw1, "bf16", f"tower {i} dW1 rows")
+        assert_close(host64(db1[i][None, :])[0][ns], r_db1, "bf16", f"tower {i} db1")
