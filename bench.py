@@ -467,18 +467,21 @@ def copy_probe():
 def plan_kernels(label):
     """(a substring of the kernel's name, its source file) for every kernel one
     execution of a plan launches, in order: the scaled fp8 quantize is an amax
-    launch then the convert launch; a Linear backward the transpose of W, the
-    dX GEMM, the dW GEMM (its transposing instance, template argument 3) and,
-    when its batch is split, the reduction; a LayerNorm backward its row kernel
+    launch then the convert launch; a Linear backward the transpose of W
+    (unless dX reads W as it lies), the dX GEMM, the dW GEMM (its transposing
+    instance, template argument 3) and, when its batch is split, the reduction; a LayerNorm backward its row kernel
     then the finalize of dgamma / dbeta."""
     if label.startswith("grouped_quantize_fp8_scaled"):
         return [("grouped_fp8_amax_kernel", "kernels_fp8.hip"), ("grouped_quantize_fp8_scaled_kernel", "kernels_fp8.hip")]
     if "_dgrad" in label or "_wgrad" in label:
         ks = []
         for part in label.split("+"):
-            if part.endswith("_dgrad"):
-                # both GEMM kernels end their template arguments with the
-                # operand layout: 0 for dX, 3 (both transposed) for dW
+            # both GEMM kernels end their template arguments with the operand
+            # layout: 0 for dX over a transposed copy of W, 2 for dX reading W
+            # as it lies, 3 (both reduction-major) for dW
+            if part.endswith("_dgrad_direct"):
+                ks.append(("0, 2>(optimus::DevLinear", "kernels_gemm.hip"))
+            elif part.endswith("_dgrad"):
                 ks.append(("grouped_transpose_kernel", "kernels_gemm.hip"))
                 ks.append(("0, 0>(optimus::DevLinear", "kernels_gemm.hip"))
             else:

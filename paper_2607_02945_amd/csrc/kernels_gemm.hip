@@ -733,50 +733,62 @@ struct DmaLoads {
 // long streams through the batch: every tile starts at step 0, so the tiles
 // of one member that run side by side share both.
 template <int TR>
-__device__ __forceinline__ int dma_rot(const GemmTile& tile, int nk) { return TR ? 0 : tile.mb % nk; }
+__device__ __forceinline__ int dma_rot(const GemmTile& tile, int nk) { return TR == 3 ? 0 : tile.mb % nk; }
+
+// This lane's first staged row and (swizzled) element offset of its chunk,
+// per operand: row-major operands stage 8 rows of 128 bytes per DMA
+// instruction, reduction-major ones RPI rows of RB bytes.
+struct DmaLanes {
+  int lrx, kchx, lrw, kchw;
+};
 
 template <int BM, int BN, int NW, int TR>
-__device__ __forceinline__ DmaLoads dma_loads(const DevLinear& d, int m0, int n0, int kbeg, int kend, int k0, int lr,
-                                              int kch) {
+__device__ __forceinline__ DmaLoads dma_loads(const DevLinear& d, int m0, int n0, int kbeg, int kend, int k0,
+                                              const DmaLanes& ln) {
+  constexpr bool TX = (TR & 1) != 0, TW = (TR & 2) != 0;
   DmaLoads L;
-  if constexpr (TR != 0) {
-    // rows are reduction steps [kbeg, kend) starting at the tile's first
-    // column; the record count ends at the last valid column of the last
-    // row, so rows past kend and chunks past the last column read as zero
+  // reduction-major: rows are reduction steps [kbeg, kend) starting at the
+  // tile's first column; the record count ends at the last valid column of
+  // the last row, so rows past kend and chunks past the last column read as
+  // zero. Row-major: the record count ends at the tile's last valid row and
+  // chunks past K are sent out of range.
+  if constexpr (TX) {
     constexpr int RPI = 1024 / (BM * 2);
-    const int rows = kend - kbeg;
     L.xp = (const bf16_t*)d.x + (int64_t)kbeg * d.ldx + m0;
-    L.wp = (const bf16_t*)d.w + (int64_t)kbeg * d.ldw + n0;
-    L.xbytes = (uint32_t)(((int64_t)(rows - 1) * d.ldx + (d.M - m0)) * 2);
-    L.wbytes = (uint32_t)(((int64_t)(rows - 1) * d.ldw + (d.N - n0)) * 2);
-    L.sx = (uint32_t)(((int64_t)(k0 + lr) * d.ldx + kch) * 2);
-    L.sw = (uint32_t)(((int64_t)(k0 + lr) * d.ldw + kch) * 2);
+    L.xbytes = (uint32_t)(((int64_t)(kend - kbeg - 1) * d.ldx + (d.M - m0)) * 2);
+    L.sx = (uint32_t)(((int64_t)(k0 + ln.lrx) * d.ldx + ln.kchx) * 2);
     L.xrow = (uint32_t)(NW * RPI * d.ldx * 2);
-    L.wrow = (uint32_t)(NW * RPI * d.ldw * 2);
-    L.k0 = k0;
-    return L;
+  } else {
+    const int Mr = d.M - m0;
+    L.xp = (const bf16_t*)d.x + (int64_t)m0 * d.ldx;
+    L.xbytes = (uint32_t)((Mr < BM ? Mr : BM) * d.ldx * 2);
+    L.sx = k0 + ln.kchx < d.K ? (uint32_t)((ln.lrx * d.ldx + ln.kchx) * 2) : kOutOfRange;
+    L.xrow = (uint32_t)(NW * 8 * d.ldx * 2);
   }
-  const int Mr = d.M - m0, Nr = d.N - n0;
-  L.xp = (const bf16_t*)d.x + (int64_t)m0 * d.ldx;
-  L.wp = (const bf16_t*)d.w + (int64_t)n0 * d.ldw;
-  L.xbytes = (uint32_t)((Mr < BM ? Mr : BM) * d.ldx * 2);
-  L.wbytes = (uint32_t)((Nr < BN ? Nr : BN) * d.ldw * 2);
-  const bool kin = k0 + kch < d.K;
-  L.sx = kin ? (uint32_t)((lr * d.ldx + kch) * 2) : kOutOfRange;
-  L.sw = kin ? (uint32_t)((lr * d.ldw + kch) * 2) : kOutOfRange;
-  L.xrow = (uint32_t)(NW * 8 * d.ldx * 2);
-  L.wrow = (uint32_t)(NW * 8 * d.ldw * 2);
+  if constexpr (TW) {
+    constexpr int RPI = 1024 / (BN * 2);
+    L.wp = (const bf16_t*)d.w + (int64_t)kbeg * d.ldw + n0;
+    L.wbytes = (uint32_t)(((int64_t)(kend - kbeg - 1) * d.ldw + (d.N - n0)) * 2);
+    L.sw = (uint32_t)(((int64_t)(k0 + ln.lrw) * d.ldw + ln.kchw) * 2);
+    L.wrow = (uint32_t)(NW * RPI * d.ldw * 2);
+  } else {
+    const int Nr = d.N - n0;
+    L.wp = (const bf16_t*)d.w + (int64_t)n0 * d.ldw;
+    L.wbytes = (uint32_t)((Nr < BN ? Nr : BN) * d.ldw * 2);
+    L.sw = k0 + ln.kchw < d.K ? (uint32_t)((ln.lrw * d.ldw + ln.kchw) * 2) : kOutOfRange;
+    L.wrow = (uint32_t)(NW * 8 * d.ldw * 2);
+  }
   L.k0 = k0;
   return L;
 }
 
-// The reduction range of a work item: all of K, or (transposed operands with
-// a split reduction) split tile.pad of it.
+// The reduction range of a work item: all of K, or (both operands
+// reduction-major, a split reduction) split tile.pad of it.
 template <int TR>
 __device__ __forceinline__ void dma_krange(const DevLinear& d, const GemmTile& tile, int& kbeg, int& kend) {
   kbeg = 0;
   kend = d.K;
-  if constexpr (TR != 0) {
+  if constexpr (TR == 3) {
     if (d.ws) {
       kbeg = tile.pad * d.kchunk;
       kend = min(d.K, kbeg + d.kchunk);
@@ -787,7 +799,7 @@ __device__ __forceinline__ void dma_krange(const DevLinear& d, const GemmTile& t
 // The first K step's loads of work item t (k0 < 0 past the end or for a padding entry).
 template <int BM, int BN, int NW, int TR>
 __device__ __forceinline__ DmaLoads dma_first(const DevLinear* __restrict__ descs, const GemmTile* __restrict__ tiles,
-                                              int t, int num_tiles, int lr, int kch) {
+                                              int t, int num_tiles, const DmaLanes& ln) {
   DmaLoads L;
   L.k0 = -1;
   if (t >= num_tiles) return L;
@@ -797,7 +809,7 @@ __device__ __forceinline__ DmaLoads dma_first(const DevLinear* __restrict__ desc
   int kbeg, kend;
   dma_krange<TR>(d, tile, kbeg, kend);
   const int nk = (kend - kbeg + 63) / 64;
-  return dma_loads<BM, BN, NW, TR>(d, tile.mb * BM, tile.nb * BN, kbeg, kend, dma_rot<TR>(tile, nk) * 64, lr, kch);
+  return dma_loads<BM, BN, NW, TR>(d, tile.mb * BM, tile.nb * BN, kbeg, kend, dma_rot<TR>(tile, nk) * 64, ln);
 }
 
 template <int BM, int BN, int WM, int WN, int ACT, int TR = 0>
@@ -807,9 +819,11 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   using S = DmaShape<BM, BN, WM, WN>;
   constexpr int NW = S::NW, A = ACT & 7;
   constexpr bool LN = (ACT & 8) != 0;  // the row LayerNorm is fused into the epilogue
-  // TR = 3: x and w both stored reduction-major (the weight gradient
-  // dW = dY^T X: x = dY, w = X); no bias, activation or LayerNorm
-  static_assert(TR == 0 || (TR == 3 && ACT == 0 && BM == BN), "transposed instances: both operands, no epilogue ops");
+  // TR bit 0: x stored reduction-major, bit 1: w. TR = 3 is the weight
+  // gradient dW = dY^T X (x = dY, w = X), TR = 2 the input gradient
+  // dX = dY W read straight from W; no bias, activation or LayerNorm
+  constexpr bool TX = (TR & 1) != 0, TW = (TR & 2) != 0;
+  static_assert(TR == 0 || ((TR == 3 || TR == 2) && ACT == 0 && BM == BN), "transposed instances: no epilogue ops");
   extern __shared__ __align__(16) char smem[];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
   float* sBias = (float*)(smem + S::BIAS);
@@ -818,11 +832,18 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   float* red = sBeta + BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN, l32 = lane & 31, lh = lane >> 5;
-  // this lane's first staged row and its (swizzled) chunk; each further DMA
-  // instruction of the wave is NW * 8 rows (reduction-major: NW * RPI rows)
-  // further down, with the same swizzle
-  const int lr = TR ? wave * S::RPI + lane / S::CPR : wave * 8 + (lane >> 3);
-  const int kch = TR ? ((lane % S::CPR) ^ (4 * (lr & 3))) << 3 : ((lane & 7) ^ swz(lr)) << 3;
+  // this lane's first staged row and its (swizzled) chunk per operand; each
+  // further DMA instruction of the wave is NW * 8 rows (reduction-major:
+  // NW * RPI rows) further down, with the same swizzle
+  DmaLanes ln;
+  {
+    const int lrn = wave * 8 + (lane >> 3), kchn = ((lane & 7) ^ swz(lrn)) << 3;
+    const int lrt = wave * S::RPI + lane / S::CPR, kcht = ((lane % S::CPR) ^ (4 * (lrt & 3))) << 3;
+    ln.lrx = TX ? lrt : lrn;
+    ln.kchx = TX ? kcht : kchn;
+    ln.lrw = TW ? lrt : lrn;
+    ln.kchw = TW ? kcht : kchn;
+  }
 
   int t = blockIdx.x;
   if ((gridDim.x & 7) == 0) t = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
@@ -833,8 +854,8 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     return q < S::XI ? wave * 8 * 128 + q * NW * 8 * 128 : S::XBYTES + wave * 8 * 128 + (q - S::XI) * NW * 8 * 128;
   };
   auto gofs = [&](const DmaLoads& L, int q) {
-    if constexpr (TR != 0) return q < S::XI ? L.sx + q * L.xrow : L.sw + (q - S::XI) * L.wrow;
-    return q < S::XI ? L.sx + q * L.xrow + L.k0 * 2 : L.sw + (q - S::XI) * L.wrow + L.k0 * 2;
+    // reduction-major offsets already hold the step's first row
+    return q < S::XI ? L.sx + q * L.xrow + (TX ? 0 : L.k0 * 2) : L.sw + (q - S::XI) * L.wrow + (TW ? 0 : L.k0 * 2);
   };
   // every load of one K step into `stage`
   auto issue_all = [&](const DmaLoads& L, int stage) {
@@ -845,7 +866,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
 
   int sbase = 0;  // stage holding the current tile's first K step
   {
-    const DmaLoads L = dma_first<BM, BN, NW, TR>(descs, tiles, t, num_tiles, lr, kch);
+    const DmaLoads L = dma_first<BM, BN, NW, TR>(descs, tiles, t, num_tiles, ln);
     if (L.k0 >= 0) issue_all(L, 0);
   }
 
@@ -853,7 +874,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     const GemmTile tile = tiles[t];
     if (tile.member < 0) {
       // padding (only at the end of the list): nothing was loaded for it
-      const DmaLoads L = dma_first<BM, BN, NW, TR>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
+      const DmaLoads L = dma_first<BM, BN, NW, TR>(descs, tiles, t + gridDim.x, num_tiles, ln);
       if (L.k0 >= 0) issue_all(L, sbase);
       continue;
     }
@@ -866,7 +887,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     // reduction-major x: the tiles of the first column block also sum each x
     // row over the reduction (db beside dW), from the fragments that the
     // waves of the first wave column read anyway
-    const bool rsum = TR != 0 && d.xsum && tile.nb == 0 && wn == 0;
+    const bool rsum = TX && d.xsum && tile.nb == 0 && wn == 0;
     float rs[S::FM];
 #pragma unroll
     for (int i = 0; i < S::FM; ++i) rs[i] = 0.f;
@@ -888,36 +909,36 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       const char* swp = sxp + S::XBYTES;
       u32x4 a[2][S::FN], b[2][S::FM];
       auto frag = [&](int kc, int set) {
-        if constexpr (TR != 0) {
-          // lane 16 g + s: reduction rows 16 kc + 8 (g / 2) + s / 4 (+ 4 for
-          // the second read), values 4 (s mod 4) .. + 3 of the fragment's 16
-          // columns [16 (g mod 2), + 16); the reads hand lane l the eight
-          // reduction values 8 (l / 32) .. + 7 of fragment row l mod 32
-          const int s16 = lane & 15, t4 = s16 >> 2;
-          const int kr = kc * 16 + 8 * lh + t4;
-          const int cl = 2 * ((lane >> 4) & 1) + ((s16 & 3) >> 1);  // chunk within the 32-column fragment
-          const int lo = kr * S::RB + cl * 16 + 8 * (s16 & 1);
-          auto tr = [&](const char* base, int rowbase) {
-            const char* p = base + lo + (((rowbase >> 5) ^ t4) << 6);
-            const u32x2 v0 = lds_read_tr16(p), v1 = lds_read_tr16(p + 4 * S::RB);
-            return u32x4{v0.x, v0.y, v1.x, v1.y};
-          };
+        // reduction-major: lane 16 g + s reads reduction rows 16 kc +
+        // 8 (g / 2) + s / 4 (+ 4 for the second read), values 4 (s mod 4) ..
+        // + 3 of the fragment's 16 columns [16 (g mod 2), + 16); the reads
+        // hand lane l the eight reduction values 8 (l / 32) .. + 7 of
+        // fragment row l mod 32, the row-major read's layout
+        const int s16 = lane & 15, t4 = s16 >> 2;
+        const int kr = kc * 16 + 8 * lh + t4;
+        const int cl = 2 * ((lane >> 4) & 1) + ((s16 & 3) >> 1);  // chunk within the 32-column fragment
+        const int lo = kr * S::RB + cl * 16 + 8 * (s16 & 1);
+        auto tr = [&](const char* base, int rowbase) {
+          const char* p = base + lo + (((rowbase >> 5) ^ t4) << 6);
+          const u32x2 v0 = lds_read_tr16(p), v1 = lds_read_tr16(p + 4 * S::RB);
+          return u32x4{v0.x, v0.y, v1.x, v1.y};
+        };
+        const int lc = kc * 2 + lh;
 #pragma unroll
-          for (int j = 0; j < S::FN; ++j) a[set][j] = tr(swp, wn * S::TN + j * 32);
-#pragma unroll
-          for (int i = 0; i < S::FM; ++i) b[set][i] = tr(sxp, wm * S::TM + i * 32);
-        } else {
-          const int lc = kc * 2 + lh;
-#pragma unroll
-          for (int j = 0; j < S::FN; ++j) {
-            const int row = wn * S::TN + j * 32 + l32;
+        for (int j = 0; j < S::FN; ++j) {
+          const int row = wn * S::TN + j * 32 + l32;
+          if constexpr (TW)
+            a[set][j] = tr(swp, wn * S::TN + j * 32);
+          else
             a[set][j] = *(const u32x4*)(swp + row * 128 + ((lc ^ swz(row)) << 4));
-          }
+        }
 #pragma unroll
-          for (int i = 0; i < S::FM; ++i) {
-            const int row = wm * S::TM + i * 32 + l32;
+        for (int i = 0; i < S::FM; ++i) {
+          const int row = wm * S::TM + i * 32 + l32;
+          if constexpr (TX)
+            b[set][i] = tr(sxp, wm * S::TM + i * 32);
+          else
             b[set][i] = *(const u32x4*)(sxp + row * 128 + ((lc ^ swz(row)) << 4));
-          }
         }
       };
       const bool go = L.k0 >= 0;
@@ -935,7 +956,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
         for (int i = 0; i < S::FM; ++i)
 #pragma unroll
           for (int j = 0; j < S::FN; ++j) Mfma<bf16_t>::run(a[kc & 1][j], b[kc & 1][i], acc[i][j]);
-        if constexpr (TR != 0) {
+        if constexpr (TX) {
           if (rsum) {
 #pragma unroll
             for (int i = 0; i < S::FM; ++i)
@@ -969,9 +990,9 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       DmaLoads L;
       if (kb + 1 < nk) {
         const int q = kb + 1 + rot;
-        L = dma_loads<BM, BN, NW, TR>(d, m0, n0, kbeg, kend, (q >= nk ? q - nk : q) * S::BK, lr, kch);
+        L = dma_loads<BM, BN, NW, TR>(d, m0, n0, kbeg, kend, (q >= nk ? q - nk : q) * S::BK, ln);
       } else {
-        L = dma_first<BM, BN, NW, TR>(descs, tiles, t + gridDim.x, num_tiles, lr, kch);
+        L = dma_first<BM, BN, NW, TR>(descs, tiles, t + gridDim.x, num_tiles, ln);
       }
       step(stage, L, stage ^ 1);
       if (kb == 0 && tid < BN) {
@@ -984,7 +1005,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     }
     __syncthreads();  // every wave is done with the last stage (staging) and the bias is written
     if constexpr (LN) ln_rows<BM, BN, WM, WN>(acc, sBias, sGamma, sBeta, red, d);
-    if constexpr (TR != 0) {
+    if constexpr (TR == 3) {
       if (rsum) {
         // lanes l and l + 32 hold the two halves of row l mod 32's sum
 #pragma unroll
@@ -1032,7 +1053,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
     // address is one lane base plus constants and every bound a per-tile
     // scalar, so nothing lane-dependent stays live across the tile loop.
     // (A split reduction has written its partial tile instead.)
-    if (!(TR != 0 && d.ws)) {
+    if (!(TR == 3 && d.ws)) {
       constexpr int RPP = 64 / S::CPRW;  // staged rows per store pass
       // opaque copies: computed here, per tile, instead of being hoisted out
       // of the tile loop and kept live across the K loop
@@ -1501,6 +1522,18 @@ static bool gemm_dma_trans_ok(const optimus_linear_desc* d, int32_t G) {
   return true;
 }
 
+// dX read straight from W on the direct-to-LDS tiles (template argument 2):
+// x = dY row-major as in the forward, w = W [K_red][N] reduction-major; both
+// widths multiples of 8 values, rows 16-byte aligned, offsets below 2^31.
+bool gemm_dma_wt_ok(const optimus_linear_desc* d, int32_t G) {
+  for (int g = 0; g < G; ++g) {
+    if (d[g].N % 8 || d[g].K % 8 || d[g].ldx % 8 || d[g].ldw % 8 || ((uintptr_t)d[g].x & 15) || ((uintptr_t)d[g].w & 15))
+      return false;
+    if (256 * d[g].ldx * 2 >= (int64_t)1 << 31 || (d[g].K + 128) * d[g].ldw * 2 >= (int64_t)1 << 31) return false;
+  }
+  return true;
+}
+
 int gemm_ln_max_n(optimus_dtype dt) { return dt == OPTIMUS_F32 ? 128 : 256; }
 
 GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln) {
@@ -1630,6 +1663,8 @@ static hipError_t launch_dma_trans(int tr, const DevLinear* descs, const GemmTil
   using S = DmaShape<BM, BN, WM, WN>;
   if (tr == 3)
     OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 0, 3>), S::LDS_BYTES, S::NT)
+  else if (tr == 2)
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 0, 2>), S::LDS_BYTES, S::NT)
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

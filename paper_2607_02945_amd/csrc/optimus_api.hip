@@ -679,9 +679,38 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
   std::vector<optimus_linear_desc> dx_shape, dw_shape;  // (M', N', K') for the tile picker
   std::vector<TransposeItem> tps;  // W -> W^T tiles, member by member
   std::vector<int> tp_end;  // per dX member: end of its transpose tiles
+  // dX straight from W (no transpose, no scratch copy) when every dX member
+  // allows the direct-to-LDS tiles to read W as it lies, reduction-major
+  bool direct = false;
+  GemmConfig dx_cfg{};
+  if (dt == OPTIMUS_BF16) {
+    std::vector<optimus_linear_desc> sh;
+    for (int g = 0; g < G; ++g)
+      if (d[g].dx) {
+        optimus_linear_desc e{};
+        e.M = d[g].M; e.N = d[g].K; e.K = d[g].N;
+        e.x = d[g].dy; e.ldx = d[g].lddy; e.w = d[g].w; e.ldw = d[g].ldw;
+        sh.push_back(e);
+      }
+    if (!sh.empty() && gemm_dma_wt_ok(sh.data(), (int32_t)sh.size())) {
+      dx_cfg = gemm_pick_config(dt, sh.data(), (int32_t)sh.size(), false);
+      direct = dx_cfg.variant == 4 || dx_cfg.variant == 5;
+    }
+  }
   for (int g = 0; g < G; ++g) {
     const optimus_linear_grad_desc& m = d[g];
-    if (m.dx) {
+    if (m.dx && direct) {
+      DevLinear o{};
+      o.x = m.dy; o.ldx = m.lddy; o.w = m.w; o.ldw = m.ldw; o.y = m.dx; o.ldy = m.lddx;
+      o.M = (int32_t)m.M; o.N = (int32_t)m.K; o.K = (int32_t)m.N;
+      const bool vout = m.lddx % VEC == 0 && aligned16(m.dx);
+      o.vec = 1 | 4 | (vout ? 2 : 0);
+      o.inv_n = 1.0f / (float)m.K;
+      dxs.push_back(o);
+      dx_ids.push_back(g);
+      hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
+      hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K);
+    } else if (m.dx) {
       // dX = dY . W as a forward GEMM on W^T [K][N'] (N' = N rounded up to 8
       // values), transposed into plan scratch by the first launch
       DevLinear o{};
@@ -732,7 +761,11 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
   hp.chain_launches = 0;
   std::string name;
   hp.tp_chain.assign(G, RowLaunch{});
-  if (!dxs.empty()) {
+  if (!dxs.empty() && direct) {
+    GemmSet& gs = hp.gs[hp.n_gs++];
+    build_gemm_set(hp, gs, dx_cfg, 2, dxs, dx_ids, G, OPTIMUS_ACT_NONE, false);
+    name = std::string(gs.cfg.name) + "_dgrad_direct";
+  } else if (!dxs.empty()) {
     // the transposes of W, then dX on the forward kernels (direct-to-LDS when
     // dY rows and N are 16-byte multiples)
     const size_t toff = hp.blob.add(tps.data(), tps.size() * sizeof(TransposeItem));

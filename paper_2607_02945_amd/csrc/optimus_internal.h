@@ -133,6 +133,9 @@ int gemm_ln_max_n(optimus_dtype dt);
 // reduction-major (dW = dY^T . X, with db from d.xsum).
 hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, const DevLinear* descs,
                        const GemmTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream, int tr = 0);
+// Whether every member of a dX group (x = dY [M][K_red], w = W [K_red][N])
+// can run on the direct-to-LDS tiles reading W as it lies (no transpose).
+bool gemm_dma_wt_ok(const optimus_linear_desc* d, int32_t G);
 // Tile shape for the backward GEMMs with both operands reduction-major
 // (direct-to-LDS where every member allows it, else register-staged).
 // split_k: the set's K will be split (dW over the batch), so prefer the large

@@ -107,10 +107,17 @@ def test_linear_backward(dtype, mode):
     ms = _linear_members(SHAPES, dtype, seed=500)
     info = _run_linear_bwd(ms, dtype, mode)
     if info is not None:
-        # W transposed, dX, dW (+ db), and the reduction when dW's batch is split
-        n = 4 if "_split" in info["kernel"] else 3
+        n = _launches(info)
         assert info["kind"] == 7 and info["launches"] == n and info["chain_launches"] == n * len(ms), info
     _check_linear_bwd(ms, dtype, f"{dtype} {mode}")
+
+
+def _launches(info):
+    """Launches of a Linear backward plan with dX and dW: the transpose of W
+    (unless dX reads W as it lies), dX, dW and, when dW's batch is split,
+    the reduction."""
+    k = info["kernel"]
+    return 1 + ("_dgrad_direct" not in k) + 1 + ("_split" in k)
 
 
 def _wgrad_part(info):
@@ -132,6 +139,7 @@ def test_linear_backward_every_tile(variant):
     for mode in ["grouped", "chain"]:
         info = _run_linear_bwd(ms, dtype, mode, variant=variant)
         assert ("dma" in _wgrad_part(info)) == (variant in (4, 5)), info
+        assert ("_dgrad_direct" in info["kernel"]) == (variant in (4, 5)), info   # W read as it lies
         _check_linear_bwd(ms, dtype, f"variant {variant} {mode}")
 
 
@@ -149,7 +157,7 @@ def test_linear_backward_split_reduction(dtype, mode, aligned):
     ms = _linear_members(shapes, dtype, seed=525)
     info = _run_linear_bwd(ms, dtype, mode)
     if info is not None:
-        assert "_split" in info["kernel"] and info["launches"] == 4, info   # + the split reduction
+        assert "_split" in info["kernel"] and info["launches"] == _launches(info), info
         assert ("dma" in _wgrad_part(info)) == (aligned and dtype == "bf16"), info
     _check_linear_bwd(ms, dtype, f"split {dtype} {mode}")
     for m in ms:
