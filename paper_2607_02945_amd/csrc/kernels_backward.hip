@@ -92,9 +92,12 @@ __global__ __launch_bounds__(kRowThreads) void grouped_act_backward_kernel(const
 // Each lane keeps its columns' dgamma / dbeta sums over the rows it handles;
 // at the end of the tile they are added into sPart ([2][cols] in LDS) and the
 // tile's partial row leaves in one coalesced pass.
+// gamma is staged in LDS as fp32 (sGamma, [cols], filled by the caller) and
+// read where it is used, which keeps the kernel at 128 registers (four waves
+// per SIMD).
 template <typename T, int MAXC>
 __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile& rt, int lane, int wave,
-                                             float* sPart) {
+                                             float* sPart, const float* sGamma) {
   constexpr int VEC = Elem<T>::VEC;
   const int L = d.lanes;
   const int rpw = 64 / L;
@@ -102,17 +105,18 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
   const int li = lane & (L - 1);
   const int cpr = d.cols / VEC;
   const bool params = d.want_params != 0;
-  float gm[MAXC][VEC];
-#pragma unroll
-  for (int j = 0; j < MAXC; ++j) {
+  auto gamma_of = [&](int j, float (&gm)[VEC]) {
     const int c = j * L + li;
-    if (d.gamma && c < cpr) {
-      Elem<T>::unpack(ld16((const char*)d.gamma + (int64_t)c * 16), gm[j]);
-    } else {
+    const f32x4* p = (const f32x4*)(sGamma + (c < cpr ? c : 0) * VEC);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) gm[j][e] = 1.f;
+    for (int h = 0; h < VEC / 4; ++h) {
+      const f32x4 v = p[h];
+      gm[4 * h] = v.x;
+      gm[4 * h + 1] = v.y;
+      gm[4 * h + 2] = v.z;
+      gm[4 * h + 3] = v.w;
     }
-  }
+  };
   float accG[MAXC][VEC], accB[MAXC][VEC];
 #pragma unroll
   for (int j = 0; j < MAXC; ++j)
@@ -136,31 +140,38 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
   };
   fetch(rt.row0 + wave * rpw + sub);
   // every lane of the wave runs the loop the same number of times (the
-  // lane-group sums need all 64); rows past the tile contribute nothing
+  // lane-group sums need all 64); rows past the tile contribute nothing.
+  // The current row stays packed (cx, cg) and is unpacked in each pass, so
+  // that it and the prefetched next row fit in registers together.
   for (int base = rt.row0; base < end; base += rpb) {
     const int r = base + wave * rpw + sub;
     const bool valid = r < end;
-    float x[MAXC][VEC], g[MAXC][VEC];
+    u32x4 cx[MAXC], cg[MAXC];
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
-      Elem<T>::unpack(rx[j], x[j]);
-      Elem<T>::unpack(rg[j], g[j]);
+      cx[j] = rx[j];
+      cg[j] = rg[j];
     }
     if (base + rpb < end) fetch(r + rpb);
     float s = 0.f;
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j)
+    for (int j = 0; j < MAXC; ++j) {
+      float x[VEC];
+      Elem<T>::unpack(cx[j], x);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) s += x[j][e];
+      for (int e = 0; e < VEC; ++e) s += x[e];
+    }
     const float mean = group_sum(s, L) * d.inv_cols;
     float q = 0.f;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
       const bool in = valid && (j * L + li) < cpr;
+      float x[VEC];
+      Elem<T>::unpack(cx[j], x);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        x[j][e] -= mean;
-        q += in ? x[j][e] * x[j][e] : 0.f;
+        const float t = x[e] - mean;
+        q += in ? t * t : 0.f;
       }
     }
     const float rstd = __builtin_amdgcn_rsqf(group_sum(q, L) * d.inv_cols + d.eps);
@@ -168,11 +179,14 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
       const bool in = valid && (j * L + li) < cpr;
+      float x[VEC], g[VEC], gm[VEC];
+      Elem<T>::unpack(cx[j], x);
+      Elem<T>::unpack(cg[j], g);
+      gamma_of(j, gm);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float xh = x[j][e] * rstd;
-        const float gg = g[j][e] * gm[j][e];
-        x[j][e] = xh;
+        const float xh = (x[e] - mean) * rstd;
+        const float gg = g[e] * gm[e];
         sg += in ? gg : 0.f;
         sgx += in ? gg * xh : 0.f;
       }
@@ -184,12 +198,16 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
     for (int j = 0; j < MAXC; ++j) {
       const int c = j * L + li;
       if (valid && c < cpr) {
-        float o[VEC];
+        float x[VEC], g[VEC], gm[VEC], o[VEC];
+        Elem<T>::unpack(cx[j], x);
+        Elem<T>::unpack(cg[j], g);
+        gamma_of(j, gm);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          o[e] = rstd * (g[j][e] * gm[j][e] - mg - x[j][e] * mgx);
-          accG[j][e] += g[j][e] * x[j][e];
-          accB[j][e] += g[j][e];
+          const float xh = (x[e] - mean) * rstd;
+          o[e] = rstd * (g[e] * gm[e] - mg - xh * mgx);
+          accG[j][e] += g[e] * xh;
+          accB[j][e] += g[e];
         }
         st16_nt(orow + (int64_t)c * 16, Elem<T>::pack(o));
       }
@@ -275,25 +293,27 @@ __device__ __forceinline__ void lnb_rows_scalar(const DevRowsGrad& d, const RowT
 }
 
 template <typename T>
-__global__ __launch_bounds__(kRowThreads) void grouped_layernorm_backward_kernel(
+__global__ __launch_bounds__(kRowThreads, 4) void grouped_layernorm_backward_kernel(
     const DevRowsGrad* __restrict__ descs, const RowTile* __restrict__ tiles, int32_t num_tiles) {
-  // [2][cols] for the widest row the 16-byte path holds: 64 lanes x the
-  // chunks per lane x the values per chunk
+  // [2][cols] partials and [cols] gamma for the widest row the 16-byte path
+  // holds: 64 lanes x the chunks per lane x the values per chunk
   constexpr int MAXCOLS = 64 * kLnChunksPerLane * Elem<T>::VEC;
-  __shared__ float sPart[2 * MAXCOLS];
+  __shared__ __align__(16) float sPart[2 * MAXCOLS];
+  __shared__ __align__(16) float sGamma[MAXCOLS];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
     const RowTile rt = tiles[t];
+    if (rt.member < 0) continue;  // padding of a block with fewer segments
     const DevRowsGrad d = descs[rt.member];
     if (d.vec && d.lanes > 0) {
       const bool params = d.want_params != 0;
-      if (params) {
+      if (params)
         for (int i = tid; i < 2 * d.cols; i += kRowThreads) sPart[i] = 0.f;
-        __syncthreads();
-      }
-      lnb_rows_vec<T, kLnChunksPerLane>(d, rt, lane, wave, sPart);
+      for (int i = tid; i < d.cols; i += kRowThreads) sGamma[i] = d.gamma ? Elem<T>::load1(d.gamma, i) : 1.f;
+      __syncthreads();
+      lnb_rows_vec<T, kLnChunksPerLane>(d, rt, lane, wave, sPart, sGamma);
+      __syncthreads();  // every wave is done with sGamma and has added into sPart
       if (params) {
-        __syncthreads();
         float* out = d.part + (int64_t)(d.part0 + rt.pad) * 2 * d.cols;
         for (int i = tid; i < 2 * d.cols; i += kRowThreads) out[i] = sPart[i];
         __syncthreads();  // sPart is cleared by the next tile
@@ -305,20 +325,49 @@ __global__ __launch_bounds__(kRowThreads) void grouped_layernorm_backward_kernel
 }
 
 // ===================================================================== finalize
+// One item is kFinCols columns of one member: the four waves of a block take
+// every fourth partial row each (four loads in flight per lane), then the
+// four sums meet in LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void grad_finalize_kernel(const GradFinItem* __restrict__ items, int32_t num_items) {
+  __shared__ float red[2][4][kFinCols];
+  const int cl = threadIdx.x % kFinCols, pg = threadIdx.x / kFinCols;
   for (int t = blockIdx.x; t < num_items; t += gridDim.x) {
     const GradFinItem it = items[t];
-    const int c = it.c0 + threadIdx.x;
-    if (c >= it.cols) continue;
+    const int c = it.c0 + cl;
     float sg = 0.f, sb = 0.f;
-    for (int p = 0; p < it.nparts; ++p) {
-      const float* row = it.part + (int64_t)p * 2 * it.cols;
-      sg += row[c];
-      sb += row[it.cols + c];
+    if (c < it.cols) {
+      const int64_t stride = 2 * (int64_t)it.cols;
+      const float* base = it.part + c;
+      int p = pg;
+      for (; p + 12 < it.nparts; p += 16) {
+        float g[4], b[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          g[u] = base[(int64_t)(p + 4 * u) * stride];
+          b[u] = base[(int64_t)(p + 4 * u) * stride + it.cols];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          sg += g[u];
+          sb += b[u];
+        }
+      }
+      for (; p < it.nparts; p += 4) {
+        sg += base[(int64_t)p * stride];
+        sb += base[(int64_t)p * stride + it.cols];
+      }
     }
-    if (it.dgamma) Elem<T>::store1(it.dgamma, c, sg);
-    if (it.dbeta) Elem<T>::store1(it.dbeta, c, sb);
+    red[0][pg][cl] = sg;
+    red[1][pg][cl] = sb;
+    __syncthreads();
+    if (pg == 0 && c < it.cols) {
+      const float g = (red[0][0][cl] + red[0][1][cl]) + (red[0][2][cl] + red[0][3][cl]);
+      const float b = (red[1][0][cl] + red[1][1][cl]) + (red[1][2][cl] + red[1][3][cl]);
+      if (it.dgamma) Elem<T>::store1(it.dgamma, c, g);
+      if (it.dbeta) Elem<T>::store1(it.dbeta, c, b);
+    }
+    __syncthreads();  // red is rewritten by the next item
   }
 }
 
@@ -356,6 +405,17 @@ hipError_t layernorm_backward_launch(optimus_dtype dt, const DevRowsGrad* descs,
     hipLaunchKernelGGL(grouped_layernorm_backward_kernel<float>, dim3(grid), dim3(kRowThreads), 0, stream, descs,
                        tiles, num_tiles);
   return hipGetLastError();
+}
+
+int layernorm_backward_resident_per_cu(optimus_dtype dt) {
+  const void* k = dt == OPTIMUS_BF16 ? (const void*)grouped_layernorm_backward_kernel<bf16_t>
+                                     : (const void*)grouped_layernorm_backward_kernel<float>;
+  int b = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k, kRowThreads, 0) != hipSuccess || b < 1) {
+    (void)hipGetLastError();
+    return 2;
+  }
+  return b;
 }
 
 hipError_t grad_finalize_launch(optimus_dtype dt, const GradFinItem* items, int32_t num_items, int32_t grid,

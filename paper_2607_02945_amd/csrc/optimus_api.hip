@@ -969,22 +969,63 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
     hp.bytes += (double)s * (3.0 * m.rows * m.cols + (m.gamma ? m.cols : 0) + (m.dgamma ? m.cols : 0) +
                              (m.dbeta ? m.cols : 0));
   }
+  // The per-op chain launches each member over at most kGradMaxTilesPerMember
+  // row tiles (hp.rows_chain). The grouped launch gives every resident
+  // workgroup one contiguous, equal share of all members' row bytes, cut at
+  // member boundaries into segments: the work is balanced to a row, and a
+  // member has one dgamma / dbeta partial row per segment (about one per
+  // workgroup that touches it), not per tile. Segment r of workgroup b sits
+  // at index r * B + b (the kernel walks t = b, b + B, ...), padded with
+  // member -1.
   std::vector<int> ntiles;
-  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember);
-  // partial rows: one per tile (16-byte path) or per wave (per-value path)
-  int64_t part_rows = 0;
-  std::vector<int> nparts(G, 0);
+  std::vector<RowTile> chain_tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember);
+  std::vector<int> nseg(G, 0);
+  std::vector<RowTile> tiles;
+  int64_t B = 1;
+  {
+    double total = 0.0;
+    for (const auto& m : members) total += (double)m.rows * m.cols * (double)s;
+    constexpr double kMinSegmentBytes = 64.0 * 1024.0;  // smaller shares only add partial rows
+    const int64_t resident = (int64_t)device_cu_count() * layernorm_backward_resident_per_cu(dt);
+    B = std::max<int64_t>(1, std::min<int64_t>(resident, (int64_t)(total / kMinSegmentBytes)));
+    std::vector<std::vector<RowTile>> per_block((size_t)B);
+    double cum = 0.0;
+    int64_t blk = 0;
+    for (int g = 0; g < G; ++g) {
+      const double rb = (double)members[g].cols * (double)s;
+      int64_t r = 0;
+      while (r < members[g].rows) {
+        const double end = total * (double)(blk + 1) / (double)B;
+        int64_t k = members[g].rows - r;
+        if (blk + 1 < B) k = std::min<int64_t>(k, std::max<int64_t>(1, (int64_t)std::ceil((end - cum) / rb)));
+        per_block[(size_t)blk].push_back(RowTile{g, (int32_t)r, (int32_t)k, nseg[g]++});
+        r += k;
+        cum += (double)k * rb;
+        while (blk + 1 < B && cum >= total * (double)(blk + 1) / (double)B) ++blk;
+      }
+    }
+    size_t rounds = 0;
+    for (const auto& v : per_block) rounds = std::max(rounds, v.size());
+    tiles.assign(rounds * (size_t)B, RowTile{-1, 0, 0, 0});
+    for (int64_t bb = 0; bb < B; ++bb)
+      for (size_t r = 0; r < per_block[(size_t)bb].size(); ++r) tiles[r * (size_t)B + (size_t)bb] = per_block[(size_t)bb][r];
+  }
+  // partial rows: one per segment or chain tile (16-byte path), per wave of
+  // one (per-value path); room for the larger of the two layouts
+  std::vector<int> nparts(G, 0), nparts_chain(G, 0);
+  std::vector<int64_t> part_rows(G, 0);
   for (int g = 0; g < G; ++g) {
     if (!members[g].want_params) continue;
-    members[g].part0 = (int32_t)part_rows;
-    nparts[g] = ntiles[g] * (members[g].vec ? 1 : kGradWavesPerBlock);
-    part_rows += nparts[g];
+    const int k = members[g].vec ? 1 : kGradWavesPerBlock;
+    nparts[g] = nseg[g] * k;
+    nparts_chain[g] = ntiles[g] * k;
+    part_rows[g] = std::max(nparts[g], nparts_chain[g]);
   }
   int64_t part_floats = 0;  // offsets in floats of each member's first partial row
   std::vector<int64_t> part_off(G, 0);
   for (int g = 0; g < G; ++g) {
     part_off[g] = part_floats;
-    if (members[g].want_params) part_floats += (int64_t)nparts[g] * 2 * members[g].cols;
+    if (members[g].want_params) part_floats += part_rows[g] * 2 * members[g].cols;
   }
   // the kernel addresses partial row p of a member at part + p * 2 * cols: give
   // each member its own base so rows of different widths do not overlap
@@ -996,34 +1037,42 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
   const size_t doff = hp.blob.add(members.data(), members.size() * sizeof(DevRowsGrad));
   for (int g = 0; g < G; ++g) hp.table_fixups.push_back(doff + g * sizeof(DevRowsGrad) + offsetof(DevRowsGrad, part));
   const size_t toff = hp.blob.add(tiles.data(), tiles.size() * sizeof(RowTile));
+  const size_t ctoff = hp.blob.add(chain_tiles.data(), chain_tiles.size() * sizeof(RowTile));
   for (auto& c : hp.rows_chain) {
     c.descs_off = doff;
-    c.tiles_off = toff;
+    c.tiles_off = ctoff;
   }
-  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
-  // finalize items: 256 columns each
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), (int32_t)B};
+  // finalize items: kFinCols columns each, for the grouped layout, then for the chain's
   std::vector<GradFinItem> fin;
+  auto add_fin = [&](int g, int np) {
+    if (members[g].want_params)
+      for (int c0 = 0; c0 < members[g].cols; c0 += kFinCols)
+        fin.push_back(GradFinItem{(const float*)(uintptr_t)(part_off_blob + (size_t)part_off[g] * sizeof(float)),
+                                  d[g].dgamma, d[g].dbeta, members[g].cols, np, c0, 0});
+  };
+  for (int g = 0; g < G; ++g) add_fin(g, nparts[g]);
+  const int32_t n_fin_grouped = (int32_t)fin.size();
   hp.fin_chain.assign(G, RowLaunch{});
   for (int g = 0; g < G; ++g) {
     const int first = (int)fin.size();
-    if (members[g].want_params)
-      for (int c0 = 0; c0 < members[g].cols; c0 += 256)
-        fin.push_back(GradFinItem{(const float*)(uintptr_t)(part_off_blob + (size_t)part_off[g] * sizeof(float)),
-                                  d[g].dgamma, d[g].dbeta, members[g].cols, nparts[g], c0, 0});
+    add_fin(g, nparts_chain[g]);
     hp.fin_chain[g] = RowLaunch{0, 0, first, (int)fin.size() - first, 0};
   }
   const size_t foff = hp.blob.add(fin.data(), fin.size() * sizeof(GradFinItem));
   for (size_t i = 0; i < fin.size(); ++i) hp.table_fixups.push_back(foff + i * sizeof(GradFinItem) + offsetof(GradFinItem, part));
   const int32_t fin_cap = device_cu_count() * 4;
-  hp.fin = RowLaunch{foff, foff, 0, (int32_t)fin.size(), (int32_t)std::max<int64_t>(1, std::min<int64_t>((int64_t)fin.size(), fin_cap))};
+  hp.fin = RowLaunch{foff, foff, 0, n_fin_grouped, std::max<int32_t>(1, std::min<int32_t>(n_fin_grouped, fin_cap))};
   for (auto& c : hp.fin_chain) {
     c.descs_off = c.tiles_off = foff;
     c.grid = std::max(1, std::min(c.num_tiles, fin_cap));
   }
-  hp.work_items = (int64_t)tiles.size();
+  int64_t segs = 0;
+  for (int g = 0; g < G; ++g) segs += nseg[g];
+  hp.work_items = segs;
   hp.grid = hp.rows.grid;
   hp.block = kRowThreads;
-  hp.launches = fin.empty() ? 1 : 2;
+  hp.launches = n_fin_grouped == 0 ? 1 : 2;
   hp.chain_launches = 0;
   for (int g = 0; g < G; ++g) hp.chain_launches += 1 + (hp.fin_chain[g].num_tiles > 0 ? 1 : 0);
   hp.kernel = dt == OPTIMUS_F32 ? "grouped_layernorm_backward_f32" : "grouped_layernorm_backward_bf16";

@@ -189,7 +189,8 @@ struct DevRowsGrad {
   int32_t want_params;  // dgamma / dbeta wanted
 };
 
-// Finalize: columns [c0, c0 + 256) of one member, the sum of its partial rows.
+// Finalize: columns [c0, c0 + kFinCols) of one member, the sum of its partial rows.
+constexpr int kFinCols = 64;
 struct GradFinItem {
   const float* part;  // first partial row of the member ([2][cols] each)
   void* dgamma;
@@ -198,6 +199,8 @@ struct GradFinItem {
 };
 
 constexpr int kGradWavesPerBlock = 4;  // partial rows per tile on the per-value path
+// Workgroups of the LayerNorm-backward kernel resident on one CU.
+int layernorm_backward_resident_per_cu(optimus_dtype dt);
 hipError_t act_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs, const RowTile* tiles,
                                int32_t num_tiles, int32_t grid, hipStream_t stream);
 hipError_t layernorm_backward_launch(optimus_dtype dt, const DevRowsGrad* descs, const RowTile* tiles,
