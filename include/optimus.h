@@ -307,6 +307,21 @@ optimus_status optimus_grouped_linear_backward(const optimus_linear_grad_desc* d
 optimus_status optimus_grouped_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
                                                   optimus_stream_t stream);
 
+/* Grouped backward of the fused LayerNorm + activation (the forward's
+ * optimus_grouped_layernorm with an epilogue activation: out = act(gamma *
+ * xhat + beta)), two launches as optimus_grouped_layernorm_backward. Here
+ * d[g].dy is dL/d(out), the activation output's gradient; the activation's
+ * input gamma * xhat + beta is recomputed from x, so no forward output is
+ * read and no intermediate gradient is stored: dx, dgamma and dbeta are the
+ * LayerNorm's, of dL/dz = dy * act'(z). The backward graph's activation and
+ * LayerNorm groups of Table 1 in one pass. beta: G device pointers ([cols]
+ * each, the member's dtype) or NULL (all 0); a NULL entry means 0. act =
+ * NONE is optimus_grouped_layernorm_backward. Errors as there, plus
+ * OPTIMUS_ERR_UNSUPPORTED for an unknown activation. */
+optimus_status optimus_grouped_layernorm_act_backward(const optimus_layernorm_grad_desc* d, const void* const* beta,
+                                                      int32_t G, optimus_dtype dt, optimus_act act,
+                                                      optimus_stream_t stream);
+
 /* Grouped activation backward, one launch. Exact in-place (dx == dy) is allowed. */
 optimus_status optimus_grouped_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt,
                                             optimus_act act, optimus_stream_t stream);
@@ -339,6 +354,8 @@ optimus_status optimus_plan_linear_backward(const optimus_linear_grad_desc* d, i
                                             optimus_plan* out);
 optimus_status optimus_plan_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
                                                optimus_plan* out);
+optimus_status optimus_plan_layernorm_act_backward(const optimus_layernorm_grad_desc* d, const void* const* beta,
+                                                   int32_t G, optimus_dtype dt, optimus_act act, optimus_plan* out);
 optimus_status optimus_plan_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
                                          optimus_plan* out);
 optimus_status optimus_plan_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,

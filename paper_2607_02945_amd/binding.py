@@ -86,6 +86,7 @@ EXPORTS = [
     "optimus_grouped_dequantize_fp8", "optimus_grouped_linear_backward", "optimus_grouped_layernorm_backward",
     "optimus_grouped_act_backward", "optimus_plan_linear_backward", "optimus_plan_layernorm_backward",
     "optimus_plan_act_backward", "optimus_validate_linear_backward", "optimus_validate_layernorm_backward",
+    "optimus_grouped_layernorm_act_backward", "optimus_plan_layernorm_act_backward",
     "optimus_validate_act_backward",
     "optimus_plan_linear", "optimus_plan_linear_layernorm", "optimus_plan_layernorm", "optimus_plan_pointwise",
     "optimus_plan_split_op_cat", "optimus_plan_quantize_fp8", "optimus_plan_dequantize_fp8",
@@ -131,6 +132,10 @@ def lib() -> ctypes.CDLL:
             "optimus_grouped_linear_backward": (st, [P(LinearGradDesc), c_i32, ctypes.c_int, c_vp]),
             "optimus_grouped_layernorm_backward": (st, [P(LayerNormGradDesc), c_i32, ctypes.c_int, c_vp]),
             "optimus_grouped_act_backward": (st, [P(ActGradDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
+            "optimus_grouped_layernorm_act_backward": (st, [P(LayerNormGradDesc), P(c_vp), c_i32, ctypes.c_int,
+                                                            ctypes.c_int, c_vp]),
+            "optimus_plan_layernorm_act_backward": (st, [P(LayerNormGradDesc), P(c_vp), c_i32, ctypes.c_int,
+                                                         ctypes.c_int, P(c_vp)]),
             "optimus_plan_linear_backward": (st, [P(LinearGradDesc), c_i32, ctypes.c_int, P(c_vp)]),
             "optimus_plan_layernorm_backward": (st, [P(LayerNormGradDesc), c_i32, ctypes.c_int, P(c_vp)]),
             "optimus_plan_act_backward": (st, [P(ActGradDesc), c_i32, ctypes.c_int, ctypes.c_int, P(c_vp)]),
@@ -380,6 +385,14 @@ def optimus_grouped_layernorm_backward(xs, dys, dxs, gammas=None, dgammas=None, 
     check(lib().optimus_grouped_layernorm_backward(d, len(xs), dtype_code(xs[0]) if xs else BF16, _stream(stream)))
 
 
+def optimus_grouped_layernorm_act_backward(xs, dys, dxs, gammas=None, betas=None, dgammas=None, dbetas=None,
+                                           eps=1e-5, act="none", stream=None) -> None:
+    d = layernorm_grad_descs(xs, dys, dxs, gammas, dgammas, dbetas, eps)
+    G = len(xs)
+    check(lib().optimus_grouped_layernorm_act_backward(d, _ptrs(betas, G), G, dtype_code(xs[0]) if xs else BF16,
+                                                       _act(act), _stream(stream)))
+
+
 def optimus_grouped_act_backward(xs, dys, dxs, act, stream=None) -> None:
     d = act_grad_descs(xs, dys, dxs)
     check(lib().optimus_grouped_act_backward(d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
@@ -460,6 +473,15 @@ def optimus_plan_linear_backward(xs, ws, dys, dxs=None, dws=None, dbs=None) -> P
     d = linear_grad_descs(xs, ws, dys, dxs, dws, dbs)
     return _plan(lib().optimus_plan_linear_backward, d, len(dys), dtype_code(dys[0]) if dys else BF16,
                  keep=(xs, ws, list(dys), dxs, dws, dbs))
+
+
+def optimus_plan_layernorm_act_backward(xs, dys, dxs, gammas=None, betas=None, dgammas=None, dbetas=None, eps=1e-5,
+                                        act="none") -> Plan:
+    d = layernorm_grad_descs(xs, dys, dxs, gammas, dgammas, dbetas, eps)
+    G = len(xs)
+    return _plan(lib().optimus_plan_layernorm_act_backward, d, _ptrs(betas, G), G,
+                 dtype_code(xs[0]) if xs else BF16, _act(act),
+                 keep=(list(xs), list(dys), list(dxs), gammas, betas, dgammas, dbetas))
 
 
 def optimus_plan_layernorm_backward(xs, dys, dxs, gammas=None, dgammas=None, dbetas=None, eps=1e-5) -> Plan:

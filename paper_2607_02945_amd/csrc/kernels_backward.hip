@@ -92,12 +92,13 @@ __global__ __launch_bounds__(kRowThreads) void grouped_act_backward_kernel(const
 // Each lane keeps its columns' dgamma / dbeta sums over the rows it handles;
 // at the end of the tile they are added into sPart ([2][cols] in LDS) and the
 // tile's partial row leaves in one coalesced pass.
-// gamma is staged in LDS as fp32 (sGamma, [cols], filled by the caller) and
-// read where it is used, which keeps the kernel at 128 registers (four waves
-// per SIMD).
-template <typename T, int MAXC>
+// gamma (and beta) are staged in LDS as fp32 (sGamma, sBeta: [cols], filled
+// by the caller) and read where they are used. ACT != 0: the backward of the
+// fused LayerNorm + activation -- the incoming gradient is the activation
+// output's, and is multiplied by act'(gamma * xhat + beta), recomputed here.
+template <typename T, int MAXC, int ACT>
 __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile& rt, int lane, int wave,
-                                             float* sPart, const float* sGamma) {
+                                             float* sPart, const float* sGamma, const float* sBeta) {
   constexpr int VEC = Elem<T>::VEC;
   const int L = d.lanes;
   const int rpw = 64 / L;
@@ -105,9 +106,9 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
   const int li = lane & (L - 1);
   const int cpr = d.cols / VEC;
   const bool params = d.want_params != 0;
-  auto gamma_of = [&](int j, float (&gm)[VEC]) {
+  auto param_of = [&](const float* src, int j, float (&gm)[VEC]) {
     const int c = j * L + li;
-    const f32x4* p = (const f32x4*)(sGamma + (c < cpr ? c : 0) * VEC);
+    const f32x4* p = (const f32x4*)(src + (c < cpr ? c : 0) * VEC);
 #pragma unroll
     for (int h = 0; h < VEC / 4; ++h) {
       const f32x4 v = p[h];
@@ -115,6 +116,16 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
       gm[4 * h + 1] = v.y;
       gm[4 * h + 2] = v.z;
       gm[4 * h + 3] = v.w;
+    }
+  };
+  auto gamma_of = [&](int j, float (&gm)[VEC]) { param_of(sGamma, j, gm); };
+  // the gradient entering the LayerNorm: dy, or dy * act'(gamma xhat + beta)
+  auto grad_in = [&](int j, const float (&gm)[VEC], const float (&xh)[VEC], float (&g)[VEC]) {
+    if constexpr (ACT != 0) {
+      float be[VEC];
+      param_of(sBeta, j, be);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) g[e] *= act_grad<ACT>(gm[e] * xh[e] + be[e]);
     }
   };
   float accG[MAXC][VEC], accB[MAXC][VEC];
@@ -179,16 +190,18 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
       const bool in = valid && (j * L + li) < cpr;
-      float x[VEC], g[VEC], gm[VEC];
+      float x[VEC], g[VEC], gm[VEC], xh[VEC];
       Elem<T>::unpack(cx[j], x);
       Elem<T>::unpack(cg[j], g);
       gamma_of(j, gm);
 #pragma unroll
+      for (int e = 0; e < VEC; ++e) xh[e] = (x[e] - mean) * rstd;
+      grad_in(j, gm, xh, g);
+#pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float xh = (x[e] - mean) * rstd;
         const float gg = g[e] * gm[e];
         sg += in ? gg : 0.f;
-        sgx += in ? gg * xh : 0.f;
+        sgx += in ? gg * xh[e] : 0.f;
       }
     }
     const float mg = group_sum(sg, L) * d.inv_cols;
@@ -198,15 +211,17 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
     for (int j = 0; j < MAXC; ++j) {
       const int c = j * L + li;
       if (valid && c < cpr) {
-        float x[VEC], g[VEC], gm[VEC], o[VEC];
+        float x[VEC], g[VEC], gm[VEC], o[VEC], xh[VEC];
         Elem<T>::unpack(cx[j], x);
         Elem<T>::unpack(cg[j], g);
         gamma_of(j, gm);
 #pragma unroll
+        for (int e = 0; e < VEC; ++e) xh[e] = (x[e] - mean) * rstd;
+        grad_in(j, gm, xh, g);
+#pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          const float xh = (x[e] - mean) * rstd;
-          o[e] = rstd * (g[e] * gm[e] - mg - xh * mgx);
-          accG[j][e] += g[e] * xh;
+          o[e] = rstd * (g[e] * gm[e] - mg - xh[e] * mgx);
+          accG[j][e] += g[e] * xh[e];
           accB[j][e] += g[e];
         }
         st16_nt(orow + (int64_t)c * 16, Elem<T>::pack(o));
@@ -244,7 +259,7 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
 // Any shape, any alignment: one wave per row, four passes over global memory;
 // the wave's dgamma / dbeta sums go to its own partial row (written by its
 // first row, added to by the next ones: only this wave touches it).
-template <typename T>
+template <typename T, int ACT>
 __device__ __forceinline__ void lnb_rows_scalar(const DevRowsGrad& d, const RowTile& rt, int lane, int wave) {
   const int end = rt.row0 + rt.nrows;
   const bool params = d.want_params != 0;
@@ -262,11 +277,23 @@ __device__ __forceinline__ void lnb_rows_scalar(const DevRowsGrad& d, const RowT
       q += t * t;
     }
     const float rstd = __builtin_amdgcn_rsqf(group_sum(q, 64) * d.inv_cols + d.eps);
+    // the gradient entering the LayerNorm at column c (ACT: times act' of
+    // the recomputed activation input)
+    auto grad_in = [&](int c, float xh) {
+      float g = Elem<T>::load1(d.dy, go + c);
+      if constexpr (ACT != 0) {
+        const float gm = d.gamma ? Elem<T>::load1(d.gamma, c) : 1.f;
+        const float be = d.beta ? Elem<T>::load1(d.beta, c) : 0.f;
+        g *= act_grad<ACT>(gm * xh + be);
+      }
+      return g;
+    };
     float sg = 0.f, sgx = 0.f;
     for (int c = lane; c < d.cols; c += 64) {
-      const float gg = Elem<T>::load1(d.dy, go + c) * (d.gamma ? Elem<T>::load1(d.gamma, c) : 1.f);
+      const float xh = (Elem<T>::load1(d.x, xo + c) - mean) * rstd;
+      const float gg = grad_in(c, xh) * (d.gamma ? Elem<T>::load1(d.gamma, c) : 1.f);
       sg += gg;
-      sgx += gg * (Elem<T>::load1(d.x, xo + c) - mean) * rstd;
+      sgx += gg * xh;
     }
     const float mg = group_sum(sg, 64) * d.inv_cols;
     const float mgx = group_sum(sgx, 64) * d.inv_cols;
@@ -274,7 +301,7 @@ __device__ __forceinline__ void lnb_rows_scalar(const DevRowsGrad& d, const RowT
     // dx may overwrite dy in place
     for (int c = lane; c < d.cols; c += 64) {
       const float xh = (Elem<T>::load1(d.x, xo + c) - mean) * rstd;
-      const float gy = Elem<T>::load1(d.dy, go + c);
+      const float gy = grad_in(c, xh);
       const float gg = gy * (d.gamma ? Elem<T>::load1(d.gamma, c) : 1.f);
       Elem<T>::store1(d.dx, oo + c, rstd * (gg - mg - xh * mgx));
       if (params) {
@@ -292,14 +319,15 @@ __device__ __forceinline__ void lnb_rows_scalar(const DevRowsGrad& d, const RowT
   }
 }
 
-template <typename T>
-__global__ __launch_bounds__(kRowThreads, 4) void grouped_layernorm_backward_kernel(
+template <typename T, int ACT>
+__global__ __launch_bounds__(kRowThreads) void grouped_layernorm_backward_kernel(
     const DevRowsGrad* __restrict__ descs, const RowTile* __restrict__ tiles, int32_t num_tiles) {
   // [2][cols] partials and [cols] gamma for the widest row the 16-byte path
   // holds: 64 lanes x the chunks per lane x the values per chunk
   constexpr int MAXCOLS = 64 * kLnChunksPerLane * Elem<T>::VEC;
   __shared__ __align__(16) float sPart[2 * MAXCOLS];
   __shared__ __align__(16) float sGamma[MAXCOLS];
+  __shared__ __align__(16) float sBeta[ACT != 0 ? MAXCOLS : 4];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
     const RowTile rt = tiles[t];
@@ -310,8 +338,10 @@ __global__ __launch_bounds__(kRowThreads, 4) void grouped_layernorm_backward_ker
       if (params)
         for (int i = tid; i < 2 * d.cols; i += kRowThreads) sPart[i] = 0.f;
       for (int i = tid; i < d.cols; i += kRowThreads) sGamma[i] = d.gamma ? Elem<T>::load1(d.gamma, i) : 1.f;
+      if constexpr (ACT != 0)
+        for (int i = tid; i < d.cols; i += kRowThreads) sBeta[i] = d.beta ? Elem<T>::load1(d.beta, i) : 0.f;
       __syncthreads();
-      lnb_rows_vec<T, kLnChunksPerLane>(d, rt, lane, wave, sPart, sGamma);
+      lnb_rows_vec<T, kLnChunksPerLane, ACT>(d, rt, lane, wave, sPart, sGamma, sBeta);
       __syncthreads();  // every wave is done with sGamma and has added into sPart
       if (params) {
         float* out = d.part + (int64_t)(d.part0 + rt.pad) * 2 * d.cols;
@@ -319,7 +349,7 @@ __global__ __launch_bounds__(kRowThreads, 4) void grouped_layernorm_backward_ker
         __syncthreads();  // sPart is cleared by the next tile
       }
     } else {
-      lnb_rows_scalar<T>(d, rt, lane, wave);
+      lnb_rows_scalar<T, ACT>(d, rt, lane, wave);
     }
   }
 }
@@ -395,21 +425,26 @@ hipError_t act_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsG
   return hipGetLastError();
 }
 
-hipError_t layernorm_backward_launch(optimus_dtype dt, const DevRowsGrad* descs, const RowTile* tiles,
-                                     int32_t num_tiles, int32_t grid, hipStream_t stream) {
+hipError_t layernorm_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs,
+                                     const RowTile* tiles, int32_t num_tiles, int32_t grid, hipStream_t stream) {
   if (num_tiles <= 0) return hipSuccess;
-  if (dt == OPTIMUS_BF16)
-    hipLaunchKernelGGL(grouped_layernorm_backward_kernel<bf16_t>, dim3(grid), dim3(kRowThreads), 0, stream, descs,
-                       tiles, num_tiles);
-  else
-    hipLaunchKernelGGL(grouped_layernorm_backward_kernel<float>, dim3(grid), dim3(kRowThreads), 0, stream, descs,
-                       tiles, num_tiles);
+  if (dt == OPTIMUS_BF16) {
+    OPTIMUS_BWD_ACT_SWITCH(act, hipLaunchKernelGGL((grouped_layernorm_backward_kernel<bf16_t, A>), dim3(grid),
+                                                   dim3(kRowThreads), 0, stream, descs, tiles, num_tiles));
+  } else {
+    OPTIMUS_BWD_ACT_SWITCH(act, hipLaunchKernelGGL((grouped_layernorm_backward_kernel<float, A>), dim3(grid),
+                                                   dim3(kRowThreads), 0, stream, descs, tiles, num_tiles));
+  }
   return hipGetLastError();
 }
 
-int layernorm_backward_resident_per_cu(optimus_dtype dt) {
-  const void* k = dt == OPTIMUS_BF16 ? (const void*)grouped_layernorm_backward_kernel<bf16_t>
-                                     : (const void*)grouped_layernorm_backward_kernel<float>;
+int layernorm_backward_resident_per_cu(optimus_dtype dt, optimus_act act) {
+  const void* k = nullptr;
+  if (dt == OPTIMUS_BF16) {
+    OPTIMUS_BWD_ACT_SWITCH(act, k = (const void*)grouped_layernorm_backward_kernel<bf16_t, A>);
+  } else {
+    OPTIMUS_BWD_ACT_SWITCH(act, k = (const void*)grouped_layernorm_backward_kernel<float, A>);
+  }
   int b = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k, kRowThreads, 0) != hipSuccess || b < 1) {
     (void)hipGetLastError();

@@ -962,17 +962,22 @@ static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRo
   return tiles;
 }
 
+// act != NONE: the backward of the fused LayerNorm + activation (beta: G
+// pointers or NULL).
 static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
-                                               HostPlan& hp) {
+                                               HostPlan& hp, const void* const* beta = nullptr,
+                                               optimus_act act = OPTIMUS_ACT_NONE) {
   optimus_status st = optimus_validate_layernorm_backward(d, G, dt);
   if (st != OPTIMUS_OK) return st;
-  hp.kind = KIND_LNBWD; hp.dt = dt; hp.act = OPTIMUS_ACT_NONE; hp.G = G;
+  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "grouped_layernorm_act_backward: unknown activation %d", (int)act);
+  hp.kind = KIND_LNBWD; hp.dt = dt; hp.act = act; hp.G = G;
   const size_t s = dtype_size(dt);
   std::vector<DevRowsGrad> members;
   for (int g = 0; g < G; ++g) {
     const optimus_layernorm_grad_desc& m = d[g];
     members.push_back(make_rows_grad(m.x, m.ldx, m.dy, m.lddy, m.dx, m.lddx, m.gamma, m.rows, m.cols, m.eps, dt, true));
     members.back().want_params = (m.dgamma || m.dbeta) ? 1 : 0;
+    members.back().beta = act != OPTIMUS_ACT_NONE && beta ? beta[g] : nullptr;
     hp.bytes += (double)s * (3.0 * m.rows * m.cols + (m.gamma ? m.cols : 0) + (m.dgamma ? m.cols : 0) +
                              (m.dbeta ? m.cols : 0));
   }
@@ -993,7 +998,7 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
     double total = 0.0;
     for (const auto& m : members) total += (double)m.rows * m.cols * (double)s;
     constexpr double kMinSegmentBytes = 64.0 * 1024.0;  // smaller shares only add partial rows
-    const int64_t resident = (int64_t)device_cu_count() * layernorm_backward_resident_per_cu(dt);
+    const int64_t resident = (int64_t)device_cu_count() * layernorm_backward_resident_per_cu(dt, act);
     B = std::max<int64_t>(1, std::min<int64_t>(resident, (int64_t)(total / kMinSegmentBytes)));
     std::vector<std::vector<RowTile>> per_block((size_t)B);
     double cum = 0.0;
@@ -1082,7 +1087,8 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
   hp.launches = n_fin_grouped == 0 ? 1 : 2;
   hp.chain_launches = 0;
   for (int g = 0; g < G; ++g) hp.chain_launches += 1 + (hp.fin_chain[g].num_tiles > 0 ? 1 : 0);
-  hp.kernel = dt == OPTIMUS_F32 ? "grouped_layernorm_backward_f32" : "grouped_layernorm_backward_bf16";
+  static const char* const act_names[] = {"", "_relu", "_sigmoid", "_tanh", "_silu"};
+  hp.kernel = std::string("grouped_layernorm_backward") + act_names[(int)act] + (dt == OPTIMUS_F32 ? "_f32" : "_bf16");
   return OPTIMUS_OK;
 }
 
@@ -1528,7 +1534,7 @@ static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t st
       return act_backward_launch(hp.dt, hp.act, at<DevRowsGrad>(table, hp.rows.descs_off),
                                  at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles, hp.rows.grid, stream);
     case KIND_LNBWD: {
-      hipError_t e = layernorm_backward_launch(hp.dt, at<DevRowsGrad>(table, hp.rows.descs_off),
+      hipError_t e = layernorm_backward_launch(hp.dt, hp.act, at<DevRowsGrad>(table, hp.rows.descs_off),
                                                at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles,
                                                hp.rows.grid, stream);
       if (e != hipSuccess) return e;
@@ -1665,6 +1671,14 @@ extern "C" optimus_status optimus_plan_layernorm_backward(const optimus_layernor
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
+extern "C" optimus_status optimus_plan_layernorm_act_backward(const optimus_layernorm_grad_desc* d,
+                                                              const void* const* beta, int32_t G, optimus_dtype dt,
+                                                              optimus_act act, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_layernorm_backward(d, G, dt, hp, beta, act);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
 extern "C" optimus_status optimus_plan_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt,
                                                     optimus_act act, optimus_plan* out) {
   HostPlan hp;
@@ -1734,7 +1748,7 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
         if (hp.kind == KIND_ACTBWD) {
           e = act_backward_launch(hp.dt, hp.act, ds, ts, c.num_tiles, c.grid, st);
         } else {
-          e = layernorm_backward_launch(hp.dt, ds, ts, c.num_tiles, c.grid, st);
+          e = layernorm_backward_launch(hp.dt, hp.act, ds, ts, c.num_tiles, c.grid, st);
           const RowLaunch& f = hp.fin_chain[g];
           if (e == hipSuccess && f.num_tiles > 0)
             e = grad_finalize_launch(hp.dt, at<GradFinItem>(p->table, f.descs_off) + f.first_tile, f.num_tiles, f.grid,
@@ -1915,6 +1929,13 @@ extern "C" optimus_status optimus_grouped_layernorm_backward(const optimus_layer
                                                              optimus_dtype dt, optimus_stream_t stream) {
   HostPlan hp;
   optimus_status st = build_layernorm_backward(d, G, dt, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_layernorm_act_backward(const optimus_layernorm_grad_desc* d,
+                                                                 const void* const* beta, int32_t G, optimus_dtype dt,
+                                                                 optimus_act act, optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_layernorm_backward(d, G, dt, hp, beta, act);
   return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
 }
 extern "C" optimus_status optimus_grouped_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt,

@@ -187,6 +187,9 @@ struct DevRowsGrad {
   float eps, inv_cols;
   int32_t part0;    // this member's first partial row
   int32_t want_params;  // dgamma / dbeta wanted
+  // fused activation backward (LayerNorm + activation): the activation's
+  // input gamma * xhat + beta is recomputed from x; beta [cols] or NULL (0)
+  const void* beta;
 };
 
 // Finalize: columns [c0, c0 + kFinCols) of one member, the sum of its partial rows.
@@ -200,10 +203,10 @@ struct GradFinItem {
 
 constexpr int kGradWavesPerBlock = 4;  // partial rows per tile on the per-value path
 // Workgroups of the LayerNorm-backward kernel resident on one CU.
-int layernorm_backward_resident_per_cu(optimus_dtype dt);
+int layernorm_backward_resident_per_cu(optimus_dtype dt, optimus_act act);
 hipError_t act_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs, const RowTile* tiles,
                                int32_t num_tiles, int32_t grid, hipStream_t stream);
-hipError_t layernorm_backward_launch(optimus_dtype dt, const DevRowsGrad* descs, const RowTile* tiles,
+hipError_t layernorm_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs, const RowTile* tiles,
                                      int32_t num_tiles, int32_t grid, hipStream_t stream);
 hipError_t grad_finalize_launch(optimus_dtype dt, const GradFinItem* items, int32_t num_items, int32_t grid,
                                 hipStream_t stream);

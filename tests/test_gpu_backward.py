@@ -294,6 +294,69 @@ def test_layernorm_backward_variants(dtype):
     _check_ln_bwd(ms, dtype, "unaligned")
 
 
+# ------------------------------------------------------------------ fused LayerNorm + activation
+def _ref_ln_act_bwd(m, beta64, act, eps):
+    """The oracle composition: the activation's input z = LayerNorm(x) (fp64,
+    from the stored x), dz = dout * act'(z), then the LayerNorm backward."""
+    z = ORC.layernorm(m["x64"], m["g64"], beta64, eps)
+    dz = ORC.act_backward(z, m["dy64"], act)
+    return ORC.layernorm_backward(m["x64"], m["g64"], dz, eps)
+
+
+@pytest.mark.parametrize("act", ACTS)
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
+def test_layernorm_act_backward(act, dtype, mode):
+    """Backward of LayerNorm + activation in one pass (the activation's input
+    recomputed from x) against the oracle's activation backward then
+    LayerNorm backward; register and per-value rows, one member without beta."""
+    say(f"[ln+act bwd] {act} {dtype} {mode}")
+    eps = 1e-5
+    ms = _ln_members(LN_SHAPES, dtype, seed=580)
+    g = synth.rng(581)
+    betas, b64s = [], []
+    for i, m in enumerate(ms):
+        if i == 2:
+            betas.append(None); b64s.append(None)
+            continue
+        b, b64 = _t(g.normal(0.0, 0.3, (1, m["cols"])), dtype)
+        betas.append(b[0]); b64s.append(b64[0])
+    for m in ms:
+        m["dx"] = _empty((m["rows"], m["cols"]), dtype)
+        m["dg"] = torch.full((m["cols"],), float("nan"), dtype=synth.DTYPES[dtype], device="cuda")
+        m["db"] = torch.full((m["cols"],), float("nan"), dtype=synth.DTYPES[dtype], device="cuda")
+    args = ([m["x"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms], [m["gamma"] for m in ms], betas,
+            [m["dg"] for m in ms], [m["db"] for m in ms], eps, act)
+    if mode == "oneshot":
+        B.optimus_grouped_layernorm_act_backward(*args)
+    else:
+        p = B.optimus_plan_layernorm_act_backward(*args)
+        info = p.info()
+        assert info["kind"] == 8 and info["launches"] == 2 and (act == "none") == ("_" + act not in info["kernel"])
+        p.execute(mode)
+        p.execute(mode)
+        torch.cuda.synchronize()
+        p.close()
+    torch.cuda.synchronize()
+    for i, m in enumerate(ms):
+        rdx, rdg, rdb = _ref_ln_act_bwd(m, b64s[i], act, eps)
+        assert_close(host64(m["dx"]), rdx, dtype, f"{act} member {i} dx")
+        assert_close(host64(m["dg"][None, :])[0], rdg, dtype, f"{act} member {i} dgamma")
+        assert_close(host64(m["db"][None, :])[0], rdb, dtype, f"{act} member {i} dbeta")
+
+
+def test_layernorm_act_backward_in_place_no_params():
+    """dx over dy (one pass reads the whole row first), no dgamma / dbeta, no gamma."""
+    say("[ln+act bwd in place]")
+    ms = _ln_members(LN_SHAPES[:3], "bf16", seed=585, gamma=False)
+    refs = [_ref_ln_act_bwd(m, None, "silu", 1e-5)[0] for m in ms]
+    B.optimus_grouped_layernorm_act_backward([m["x"] for m in ms], [m["dy"] for m in ms], [m["dy"] for m in ms],
+                                             None, None, None, None, 1e-5, "silu")
+    torch.cuda.synchronize()
+    for i, m in enumerate(ms):
+        assert_close(host64(m["dy"]), refs[i], "bf16", f"in place member {i} dx")
+
+
 # ------------------------------------------------------------------ a training step's backward
 def test_towers_backward_chain_of_groups():
     """The towers group's backward (LayerNorm, layer 2, relu, layer 1) as
@@ -360,10 +423,12 @@ def _sample(n, k, seed):
 @pytest.mark.timeout(300)
 def test_large_group_backward_full_size_sampled():
     """large_group's training backward at full size (32 members, batch 16384,
-    K = 1024, N in {256, 512, 1024}) as the benchmark runs it: tanh, LayerNorm
-    and Linear backward plans, one grouped launch set each. Per operator, the
-    oracle is fed the GPU's stored inputs: dX on sampled rows, dW / db on
-    sampled output rows over the whole batch, dgamma / dbeta over every row."""
+    K = 1024, N in {256, 512, 1024}) as the benchmark runs it: the LayerNorm +
+    tanh backward in one pass, then the Linear backward. Per operator, the
+    oracle is fed the GPU's stored inputs: the tanh input recomputed in fp64
+    from y, then tanh and LayerNorm backward (dX on sampled rows, dgamma /
+    dbeta over every row); the Linear's dX on sampled rows, dW / db on
+    sampled output rows over the whole batch."""
     say("[large_group bwd] G=32 B=16384 K=1024 bf16")
     wl = synth.large_group(0)
     ms = wl.members
@@ -371,19 +436,16 @@ def test_large_group_backward_full_size_sampled():
     xs, ws, bs = [dev(m.x) for m in ms], [dev(m.w) for m in ms], [dev(m.b) for m in ms]
     gs, bes = [dev(g) for g in wl.gammas], [dev(b) for b in wl.betas]
     y = [torch.empty((m.M, m.N), dtype=bf, device="cuda") for m in ms]
-    z = [torch.empty_like(v) for v in y]
     B.optimus_plan_linear(xs, ws, bs, y, "none").execute()
-    B.optimus_plan_layernorm(y, z, gs, bes, wl.eps, "none").execute()
     gen = torch.Generator(device="cuda").manual_seed(2)
-    dt_ = [torch.randn(v.shape, generator=gen, device="cuda").to(bf) for v in z]
-    dz, dy = [torch.empty_like(v) for v in z], [torch.empty_like(v) for v in y]
+    dt_ = [torch.randn(v.shape, generator=gen, device="cuda").to(bf) for v in y]
+    dy = [torch.empty_like(v) for v in y]
     dx, dw, db = [torch.empty_like(x) for x in xs], [torch.empty_like(w) for w in ws], [torch.empty_like(b) for b in bs]
     dgm, dbt = [torch.empty_like(g) for g in gs], [torch.empty_like(g) for g in gs]
     torch.cuda.synchronize()
-    plans = [B.optimus_plan_act_backward(z, dt_, dz, "tanh"),
-             B.optimus_plan_layernorm_backward(y, dz, dy, gs, dgm, dbt, wl.eps),
+    plans = [B.optimus_plan_layernorm_act_backward(y, dt_, dy, gs, bes, dgm, dbt, wl.eps, "tanh"),
              B.optimus_plan_linear_backward(xs, ws, dy, dx, dw, db)]
-    lin_info = plans[2].info()
+    lin_info = plans[1].info()
     say(f"  linear backward plan: {lin_info['kernel']} launches={lin_info['launches']}")
     for p in plans:
         p.execute("grouped")
@@ -391,10 +453,9 @@ def test_large_group_backward_full_size_sampled():
     rows = _sample(16384, 40, seed=63)
     for i, m in enumerate(ms):
         say(f"  member {i} N={m.N}")
-        z64, dt64 = host64(z[i]), host64(dt_[i])
-        assert_close(host64(dz[i])[rows], ORC.act_backward(z64[rows], dt64[rows], "tanh"), "bf16", f"member {i} dtanh")
-        y64, dz64 = host64(y[i]), host64(dz[i])
-        g64 = synth.exact64(wl.gammas[i])
+        y64, dt64 = host64(y[i]), host64(dt_[i])
+        g64, b64 = synth.exact64(wl.gammas[i]), synth.exact64(wl.betas[i])
+        dz64 = ORC.act_backward(ORC.layernorm(y64, g64, b64, wl.eps), dt64, "tanh")
         r_dy, r_dg, r_db = ORC.layernorm_backward(y64, g64, dz64, wl.eps)
         dy64 = host64(dy[i])
         assert_close(dy64[rows], r_dy[rows], "bf16", f"member {i} LayerNorm dX")
