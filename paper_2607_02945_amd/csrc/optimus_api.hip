@@ -557,7 +557,49 @@ static int32_t row_grid(int64_t tiles) {
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(tiles, cap));
 }
 
-// Row-wise plan over `members` (LayerNorm or pointwise), member-major tiles.
+// Balanced row segments for a grouped row launch of `resident` workgroups:
+// every workgroup gets one contiguous, equal share of all members' row bytes
+// (rows[g] rows of row_bytes[g] each, members in order), cut at member
+// boundaries into segments (pad = the segment's index within its member,
+// nseg[g] of them). Segment r of workgroup b sits at index r * B + b (the
+// kernels walk t = b, b + B, ...), padded with member -1; shares below 64 KB
+// take fewer workgroups. Returns B, the launch's grid.
+static int64_t balanced_row_segments(const std::vector<int64_t>& rows, const std::vector<double>& row_bytes,
+                                     int64_t resident, std::vector<RowTile>& tiles, std::vector<int>& nseg) {
+  const size_t G = rows.size();
+  double total = 0.0;
+  for (size_t g = 0; g < G; ++g) total += (double)rows[g] * row_bytes[g];
+  constexpr double kMinSegmentBytes = 64.0 * 1024.0;
+  const int64_t B = std::max<int64_t>(1, std::min<int64_t>(resident, (int64_t)(total / kMinSegmentBytes)));
+  std::vector<std::vector<RowTile>> per_block((size_t)B);
+  nseg.assign(G, 0);
+  double cum = 0.0;
+  int64_t blk = 0;
+  for (size_t g = 0; g < G; ++g) {
+    const double rb = row_bytes[g];
+    int64_t r = 0;
+    while (r < rows[g]) {
+      const double end = total * (double)(blk + 1) / (double)B;
+      int64_t k = rows[g] - r;
+      if (blk + 1 < B) k = std::min<int64_t>(k, std::max<int64_t>(1, (int64_t)std::ceil((end - cum) / rb)));
+      per_block[(size_t)blk].push_back(RowTile{(int)g, (int32_t)r, (int32_t)k, nseg[g]++});
+      r += k;
+      cum += (double)k * rb;
+      while (blk + 1 < B && cum >= total * (double)(blk + 1) / (double)B) ++blk;
+    }
+  }
+  size_t rounds = 0;
+  for (const auto& v : per_block) rounds = std::max(rounds, v.size());
+  tiles.assign(rounds * (size_t)B, RowTile{-1, 0, 0, 0});
+  for (int64_t bb = 0; bb < B; ++bb)
+    for (size_t r = 0; r < per_block[(size_t)bb].size(); ++r) tiles[r * (size_t)B + (size_t)bb] = per_block[(size_t)bb][r];
+  return B;
+}
+
+// Row-wise plan over `members` (LayerNorm or pointwise), member-major tiles
+// of about kRowTileBytes. (Balanced per-workgroup segments, as the LayerNorm
+// backward uses, measured slower here: 268 against 253 us for large_group's
+// LayerNorm + tanh. The hardware spreads the small tiles better.)
 static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool layernorm, size_t s) {
   std::vector<RowTile> tiles;
   hp.rows_chain.clear();
@@ -982,45 +1024,24 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
                              (m.dbeta ? m.cols : 0));
   }
   // The per-op chain launches each member over at most kGradMaxTilesPerMember
-  // row tiles (hp.rows_chain). The grouped launch gives every resident
-  // workgroup one contiguous, equal share of all members' row bytes, cut at
-  // member boundaries into segments: the work is balanced to a row, and a
+  // row tiles (hp.rows_chain). The grouped launch takes balanced row
+  // segments (balanced_row_segments): the work is balanced to a row, and a
   // member has one dgamma / dbeta partial row per segment (about one per
-  // workgroup that touches it), not per tile. Segment r of workgroup b sits
-  // at index r * B + b (the kernel walks t = b, b + B, ...), padded with
-  // member -1.
+  // workgroup that touches it), not per tile.
   std::vector<int> ntiles;
   std::vector<RowTile> chain_tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember);
-  std::vector<int> nseg(G, 0);
+  std::vector<int> nseg;
   std::vector<RowTile> tiles;
-  int64_t B = 1;
+  int64_t B;
   {
-    double total = 0.0;
-    for (const auto& m : members) total += (double)m.rows * m.cols * (double)s;
-    constexpr double kMinSegmentBytes = 64.0 * 1024.0;  // smaller shares only add partial rows
-    const int64_t resident = (int64_t)device_cu_count() * layernorm_backward_resident_per_cu(dt, act);
-    B = std::max<int64_t>(1, std::min<int64_t>(resident, (int64_t)(total / kMinSegmentBytes)));
-    std::vector<std::vector<RowTile>> per_block((size_t)B);
-    double cum = 0.0;
-    int64_t blk = 0;
-    for (int g = 0; g < G; ++g) {
-      const double rb = (double)members[g].cols * (double)s;
-      int64_t r = 0;
-      while (r < members[g].rows) {
-        const double end = total * (double)(blk + 1) / (double)B;
-        int64_t k = members[g].rows - r;
-        if (blk + 1 < B) k = std::min<int64_t>(k, std::max<int64_t>(1, (int64_t)std::ceil((end - cum) / rb)));
-        per_block[(size_t)blk].push_back(RowTile{g, (int32_t)r, (int32_t)k, nseg[g]++});
-        r += k;
-        cum += (double)k * rb;
-        while (blk + 1 < B && cum >= total * (double)(blk + 1) / (double)B) ++blk;
-      }
+    std::vector<int64_t> rows;
+    std::vector<double> rb;
+    for (const auto& m : members) {
+      rows.push_back(m.rows);
+      rb.push_back((double)m.cols * (double)s);
     }
-    size_t rounds = 0;
-    for (const auto& v : per_block) rounds = std::max(rounds, v.size());
-    tiles.assign(rounds * (size_t)B, RowTile{-1, 0, 0, 0});
-    for (int64_t bb = 0; bb < B; ++bb)
-      for (size_t r = 0; r < per_block[(size_t)bb].size(); ++r) tiles[r * (size_t)B + (size_t)bb] = per_block[(size_t)bb][r];
+    B = balanced_row_segments(rows, rb, (int64_t)device_cu_count() * layernorm_backward_resident_per_cu(dt, act),
+                              tiles, nseg);
   }
   // partial rows: one per segment or chain tile (16-byte path), per wave of
   // one (per-value path); room for the larger of the two layouts
