@@ -185,11 +185,12 @@ def build_copy(name, wl, torch, B):
         dgm, dbt = [torch.empty_like(g) for g in gm], [torch.empty_like(g) for g in gm]
         torch.cuda.synchronize()
         ln_b = B.optimus_plan_layernorm_backward(o, dz, do, gm, dgm, dbt, wl.eps)
-        l2_b = B.optimus_plan_linear_backward(h, w2, do, dh, dw2, db2)
-        relu_b = B.optimus_plan_act_backward(hp, dh, dh, "relu")
+        # layer 2's dX leaves with the relu backward applied (d of the
+        # pre-activation hp), as the forward fuses the relu into layer 1
+        l2_b = B.optimus_plan_linear_act_backward(h, w2, do, dh, dw2, db2, hp, "relu")
         l1_b = B.optimus_plan_linear_backward(xs, w1, dh, dx, dw1, db1)
-        og.grouped = [(ln_b, "grouped"), (l2_b, "grouped"), (relu_b, "grouped"), (l1_b, "grouped")]
-        og.chain = [(ln_b, "chain"), (l2_b, "chain"), (relu_b, "chain"), (l1_b, "chain")]
+        og.grouped = [(ln_b, "grouped"), (l2_b, "grouped"), (l1_b, "grouped")]
+        og.chain = [(ln_b, "chain"), (l2_b, "chain"), (l1_b, "chain")]
         og.keep = (xs, w1, b1, w2, b2, gm, hp, h, o, dz, do, dh, dx, dw1, dw2, db1, db2, dgm, dbt)
     elif name == "large_group_bwd":
         # backward of Linear -> LayerNorm -> tanh over the 32 wide members: the
@@ -260,7 +261,9 @@ def describe(name, wl):
     if name == "towers_bwd":
         return {"workload": name, "towers": wl.G, "batch": wl.towers[0].x.shape[0],
                 "backward_of": "Linear(in_g->512)+relu, Linear(512->256), LayerNorm",
-                "grads": "dX, dW, db of both layers, dgamma, dbeta", "seed": 0}
+                "grads": "dX, dW, db of both layers, dgamma, dbeta",
+                "launches": "LayerNorm backward, layer 2 backward with the relu backward in its dX, layer 1 backward",
+                "seed": 0}
     if name == "large_group_bwd":
         return {"workload": name, "G": wl.G, "batch": wl.members[0].M, "K": sorted({m.K for m in wl.members}),
                 "N": sorted({m.N for m in wl.members}), "backward_of": "Linear -> LayerNorm -> tanh",
@@ -483,11 +486,14 @@ def plan_kernels(label):
             # both GEMM kernels end their template arguments with the operand
             # layout: 0 for dX over a transposed copy of W, 2 for dX reading W
             # as it lies, 3 (both reduction-major) for dW
-            if part.endswith("_dgrad_direct"):
-                ks.append(("0, 2>(optimus::DevLinear", "kernels_gemm.hip"))
-            elif part.endswith("_dgrad"):
+            # (with a fused activation backward the dX part ends in its name)
+            if "_dgrad_direct" in part:
+                ks.append((", 2>(optimus::DevLinear", "kernels_gemm.hip"))
+            elif "_dgrad" in part:
                 ks.append(("grouped_transpose_kernel", "kernels_gemm.hip"))
                 ks.append(("0, 0>(optimus::DevLinear", "kernels_gemm.hip"))
+                if not part.endswith("_dgrad"):
+                    ks.append(("grouped_act_backward_kernel", "kernels_backward.hip"))
             else:
                 ks.append(("0, 3>(optimus::DevLinear", "kernels_gemm.hip"))
                 if "_split" in part:

@@ -307,6 +307,23 @@ optimus_status optimus_grouped_linear_backward(const optimus_linear_grad_desc* d
 optimus_status optimus_grouped_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
                                                   optimus_stream_t stream);
 
+/* Grouped Linear backward with the activation backward of the layer below
+ * fused into dX: for a member whose input x = act(a) is an activation's
+ * output, dX leaves as dL/da = (dY W) * act'(a) instead of dL/dx, which
+ * saves the activation backward's pass over dX (Table 1's backward groups,
+ * the Linear's and the activation's, in one launch set). act_x: G device
+ * pointers to a [M][K] (the member's dtype; entries of members without dx
+ * are ignored), ld_act_x: G row strides (>= K). dW and db are those of
+ * optimus_grouped_linear_backward. Where the input-gradient GEMM cannot read W
+ * directly (widths not multiples of 8 values, unaligned rows) the plan adds
+ * one grouped activation-backward launch over dX instead. act = NONE is
+ * optimus_grouped_linear_backward. Errors as there, plus
+ * OPTIMUS_ERR_INVALID_ARG for a NULL act_x / ld_act_x or ld_act_x < K and
+ * OPTIMUS_ERR_UNSUPPORTED for an unknown activation. */
+optimus_status optimus_grouped_linear_act_backward(const optimus_linear_grad_desc* d, const void* const* act_x,
+                                                   const int64_t* ld_act_x, int32_t G, optimus_dtype dt,
+                                                   optimus_act act, optimus_stream_t stream);
+
 /* Grouped backward of the fused LayerNorm + activation (the forward's
  * optimus_grouped_layernorm with an epilogue activation: out = act(gamma *
  * xhat + beta)), two launches as optimus_grouped_layernorm_backward. Here
@@ -354,6 +371,9 @@ optimus_status optimus_plan_linear_backward(const optimus_linear_grad_desc* d, i
                                             optimus_plan* out);
 optimus_status optimus_plan_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G, optimus_dtype dt,
                                                optimus_plan* out);
+optimus_status optimus_plan_linear_act_backward(const optimus_linear_grad_desc* d, const void* const* act_x,
+                                                const int64_t* ld_act_x, int32_t G, optimus_dtype dt, optimus_act act,
+                                                optimus_plan* out);
 optimus_status optimus_plan_layernorm_act_backward(const optimus_layernorm_grad_desc* d, const void* const* beta,
                                                    int32_t G, optimus_dtype dt, optimus_act act, optimus_plan* out);
 optimus_status optimus_plan_act_backward(const optimus_act_grad_desc* d, int32_t G, optimus_dtype dt, optimus_act act,

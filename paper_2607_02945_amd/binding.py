@@ -87,6 +87,7 @@ EXPORTS = [
     "optimus_grouped_act_backward", "optimus_plan_linear_backward", "optimus_plan_layernorm_backward",
     "optimus_plan_act_backward", "optimus_validate_linear_backward", "optimus_validate_layernorm_backward",
     "optimus_grouped_layernorm_act_backward", "optimus_plan_layernorm_act_backward",
+    "optimus_grouped_linear_act_backward", "optimus_plan_linear_act_backward",
     "optimus_validate_act_backward",
     "optimus_plan_linear", "optimus_plan_linear_layernorm", "optimus_plan_layernorm", "optimus_plan_pointwise",
     "optimus_plan_split_op_cat", "optimus_plan_quantize_fp8", "optimus_plan_dequantize_fp8",
@@ -134,6 +135,10 @@ def lib() -> ctypes.CDLL:
             "optimus_grouped_act_backward": (st, [P(ActGradDesc), c_i32, ctypes.c_int, ctypes.c_int, c_vp]),
             "optimus_grouped_layernorm_act_backward": (st, [P(LayerNormGradDesc), P(c_vp), c_i32, ctypes.c_int,
                                                             ctypes.c_int, c_vp]),
+            "optimus_grouped_linear_act_backward": (st, [P(LinearGradDesc), P(c_vp), P(ctypes.c_int64), c_i32,
+                                                         ctypes.c_int, ctypes.c_int, c_vp]),
+            "optimus_plan_linear_act_backward": (st, [P(LinearGradDesc), P(c_vp), P(ctypes.c_int64), c_i32,
+                                                      ctypes.c_int, ctypes.c_int, P(c_vp)]),
             "optimus_plan_layernorm_act_backward": (st, [P(LayerNormGradDesc), P(c_vp), c_i32, ctypes.c_int,
                                                          ctypes.c_int, P(c_vp)]),
             "optimus_plan_linear_backward": (st, [P(LinearGradDesc), c_i32, ctypes.c_int, P(c_vp)]),
@@ -383,6 +388,27 @@ def optimus_grouped_layernorm_backward(xs, dys, dxs, gammas=None, dgammas=None, 
                                        stream=None) -> None:
     d = layernorm_grad_descs(xs, dys, dxs, gammas, dgammas, dbetas, eps)
     check(lib().optimus_grouped_layernorm_backward(d, len(xs), dtype_code(xs[0]) if xs else BF16, _stream(stream)))
+
+
+def _act_inputs(act_x, G):
+    """Pointers and row strides of the activation inputs (entries may be None)."""
+    ptrs = (c_vp * max(G, 1))(*[_ptr(a) for a in act_x])
+    lds = (ctypes.c_int64 * max(G, 1))(*[(a.stride(0) if a is not None else 1) for a in act_x])
+    return ptrs, lds
+
+
+def optimus_grouped_linear_act_backward(xs, ws, dys, dxs, dws, dbs, act_x, act, stream=None) -> None:
+    d = linear_grad_descs(xs, ws, dys, dxs, dws, dbs)
+    ptrs, lds = _act_inputs(act_x, len(xs))
+    check(lib().optimus_grouped_linear_act_backward(d, ptrs, lds, len(xs), dtype_code(xs[0]) if xs else BF16,
+                                                    _act(act), _stream(stream)))
+
+
+def optimus_plan_linear_act_backward(xs, ws, dys, dxs, dws, dbs, act_x, act) -> "Plan":
+    d = linear_grad_descs(xs, ws, dys, dxs, dws, dbs)
+    ptrs, lds = _act_inputs(act_x, len(xs))
+    return _plan(lib().optimus_plan_linear_act_backward, d, ptrs, lds, len(xs), dtype_code(xs[0]) if xs else BF16,
+                 _act(act), keep=(list(xs), list(ws), list(dys), dxs, dws, dbs, list(act_x)))
 
 
 def optimus_grouped_layernorm_act_backward(xs, dys, dxs, gammas=None, betas=None, dgammas=None, dbetas=None,

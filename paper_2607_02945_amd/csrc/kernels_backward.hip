@@ -12,26 +12,6 @@
 
 namespace optimus {
 
-// Derivative of one activation at its input, in the same hardware
-// exponential / reciprocal forms as the forward activations.
-template <int ACT>
-__device__ __forceinline__ float act_grad(float x) {
-  if constexpr (ACT == OPTIMUS_ACT_RELU) {
-    return x > 0.f ? 1.f : 0.f;
-  } else if constexpr (ACT == OPTIMUS_ACT_SIGMOID) {
-    const float s = fast_rcp(1.f + fast_exp(-x));
-    return s * (1.f - s);
-  } else if constexpr (ACT == OPTIMUS_ACT_TANH) {
-    const float t = 1.f - 2.f * fast_rcp(fast_exp(2.f * x) + 1.f);
-    return 1.f - t * t;
-  } else if constexpr (ACT == OPTIMUS_ACT_SILU) {
-    const float s = fast_rcp(1.f + fast_exp(-x));
-    return s + x * s * (1.f - s);
-  } else {
-    return 1.f;
-  }
-}
-
 // ===================================================================== activation
 template <typename T, int ACT>
 __global__ __launch_bounds__(kRowThreads) void grouped_act_backward_kernel(const DevRowsGrad* __restrict__ descs,

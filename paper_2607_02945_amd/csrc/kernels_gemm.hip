@@ -823,7 +823,11 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   // gradient dW = dY^T X (x = dY, w = X), TR = 2 the input gradient
   // dX = dY W read straight from W; no bias, activation or LayerNorm
   constexpr bool TX = (TR & 1) != 0, TW = (TR & 2) != 0;
-  static_assert(TR == 0 || ((TR == 3 || TR == 2) && ACT == 0 && BM == BN), "transposed instances: no epilogue ops");
+  static_assert(TR == 0 || ((TR == 3 && ACT == 0) || (TR == 2 && ACT < 8)) && BM == BN,
+                "transposed instances: no bias or LayerNorm; TR = 2 may fuse an activation backward");
+  // the epilogue's forward activation (TR = 0), or the activation whose
+  // backward multiplies the stored input gradient (TR = 2, by act'(d.ax))
+  constexpr int AF = TR == 0 ? A : 0, AG = TR == 2 ? A : 0;
   extern __shared__ __align__(16) char smem[];
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
   float* sBias = (float*)(smem + S::BIAS);
@@ -1069,6 +1073,8 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       const int tc = wcol0 + lc * 8;  // tile column of this lane's stores
       const bool col_in = tc < Nr, col_vec = (d.vec & 2) != 0 && tc + 8 <= Nr;
       bf16_t* ybase = (bf16_t*)d.y + (int64_t)(m0 + wrow0) * d.ldy + n0 + tc + (int64_t)lrow * d.ldy;
+      const bf16_t* abase = nullptr;
+      if constexpr (AG != 0) abase = (const bf16_t*)d.ax + (int64_t)(m0 + wrow0 + lrow) * d.ldax + n0 + tc;
       // this lane's bias values, all read before the first staging write
       // (a fused LayerNorm has already added them)
       f32x4 bias[S::FN][4];
@@ -1093,10 +1099,10 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
               o2 += bv.z;
               o3 += bv.w;
             }
-            o0 = act_apply<A>(o0);
-            o1 = act_apply<A>(o1);
-            o2 = act_apply<A>(o2);
-            o3 = act_apply<A>(o3);
+            o0 = act_apply<AF>(o0);
+            o1 = act_apply<AF>(o1);
+            o2 = act_apply<AF>(o2);
+            o3 = act_apply<AF>(o3);
             *(u32x2*)(wput + (4 * j + q) * 16) = u32x2{pack_bf16x2(o0, o1), pack_bf16x2(o2, o3)};
           }
         }
@@ -1107,7 +1113,27 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
           const int lim = Mr - (wrow0 + h * S::HR + r * RPP);  // rows of this pass inside the tile
           if (lrow < lim && col_in) {
             bf16_t* yp = ybase + (int64_t)(h * S::HR + r * RPP) * d.ldy;
-            if (col_vec) {
+            if constexpr (AG != 0) {
+              // dX * act'(ax): the stored value times the derivative at the
+              // activation's input, rounded once more to bf16
+              const bf16_t* ap = abase + (int64_t)(h * S::HR + r * RPP) * d.ldax;
+              if (col_vec && (d.vec & 8)) {
+                float g[8], a[8];
+                Elem<bf16_t>::unpack(v, g);
+                Elem<bf16_t>::unpack(ld16_nt(ap), a);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) g[e] *= act_grad<AG>(a[e]);
+                st16_nt(yp, Elem<bf16_t>::pack(g));
+              } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                  if (tc + e < Nr) {
+                    const float g = bf16_to_f32((uint16_t)(v[e >> 1] >> (16 * (e & 1))));
+                    ((OPTIMUS_GLOBAL uint16_t*)yp)[e] =
+                        f32_to_bf16(g * act_grad<AG>(bf16_to_f32(((const OPTIMUS_GLOBAL uint16_t*)ap)[e])));
+                  }
+              }
+            } else if (col_vec) {
               st16_nt(yp, v);  // y is not read again by this launch
             } else {
 #pragma unroll
@@ -1658,14 +1684,21 @@ static hipError_t launch_trans(int tr, const DevLinear* descs, const GemmTile* t
 }
 
 template <int BM, int BN, int WM, int WN>
-static hipError_t launch_dma_trans(int tr, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
-                                   hipStream_t stream, int* occ) {
+static hipError_t launch_dma_trans(int tr, optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n,
+                                   int32_t grid, hipStream_t stream, int* occ) {
   using S = DmaShape<BM, BN, WM, WN>;
   if (tr == 3)
     OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 0, 3>), S::LDS_BYTES, S::NT)
-  else if (tr == 2)
-    OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 0, 2>), S::LDS_BYTES, S::NT)
-  else
+  else if (tr == 2) {
+    switch (act) {
+      case OPTIMUS_ACT_NONE: OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 0, 2>), S::LDS_BYTES, S::NT); break;
+      case OPTIMUS_ACT_RELU: OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 1, 2>), S::LDS_BYTES, S::NT); break;
+      case OPTIMUS_ACT_SIGMOID: OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 2, 2>), S::LDS_BYTES, S::NT); break;
+      case OPTIMUS_ACT_TANH: OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 3, 2>), S::LDS_BYTES, S::NT); break;
+      case OPTIMUS_ACT_SILU: OPTIMUS_LAUNCH_ONE((grouped_gemm_dma_kernel<BM, BN, WM, WN, 4, 2>), S::LDS_BYTES, S::NT); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -1696,13 +1729,13 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
                                 const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
                                 hipStream_t stream, int* occ) {
   if (tr) {
-    if (ln || act != OPTIMUS_ACT_NONE) return hipErrorInvalidValue;
+    if (ln || (act != OPTIMUS_ACT_NONE && tr != 2)) return hipErrorInvalidValue;
     switch (cfg.variant) {
       case 1: return launch_trans<bf16_t, 128, 128, 64, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
       case 2: return launch_trans<bf16_t, 256, 256, 64, 2, 4, 2>(tr, descs, tiles, n, grid, stream, occ);
       case 3: return launch_trans<float, 64, 64, 32, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
-      case 4: return launch_dma_trans<256, 256, 2, 4>(tr, descs, tiles, n, grid, stream, occ);
-      case 5: return launch_dma_trans<128, 128, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
+      case 4: return launch_dma_trans<256, 256, 2, 4>(tr, act, descs, tiles, n, grid, stream, occ);
+      case 5: return launch_dma_trans<128, 128, 2, 2>(tr, act, descs, tiles, n, grid, stream, occ);
       case 6: return launch_trans<float, 64, 128, 64, 2, 2, 2>(tr, descs, tiles, n, grid, stream, occ);
       default: return hipErrorInvalidValue;
     }

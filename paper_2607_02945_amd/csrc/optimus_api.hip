@@ -440,6 +440,7 @@ struct RowLaunch {
 struct GemmSet {
   GemmConfig cfg{};
   int tr = 0;
+  optimus_act act = OPTIMUS_ACT_NONE;  // the instance's epilogue activation (TR = 2: its backward)
   size_t descs_off = 0, tiles_off = 0;
   int32_t num_tiles = 0, grid = 0;
   int64_t real_tiles = 0;
@@ -633,6 +634,7 @@ static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int
   const int n = (int)descs.size();
   gs.cfg = cfg;
   gs.tr = tr;
+  gs.act = act;
   std::vector<int> order(n);
   for (int i = 0; i < n; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return descs[a].K > descs[b].K; });
@@ -712,11 +714,31 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
 //   dW: x[m'][k'] = dY[k'][m'] and w[n'][k'] = X[k'][n'] (both
 //       reduction-major), y = dW, M' = N, N' = K, K' = M; the row sums of x
 //       over k' are db.
+static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, int64_t lddy, void* dx, int64_t lddx,
+                                  const void* gamma, int64_t rows, int64_t cols, float eps, optimus_dtype dt,
+                                  bool layernorm);
+static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
+                                           std::vector<int>& ntiles, int64_t max_tiles = 0);
+
+// act != NONE: dX leaves with the activation backward of the layer below
+// applied, dX * act'(act_x[g]) (act_x [M][K], row stride ld_act_x[g]).
 static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
-                                            HostPlan& hp) {
+                                            HostPlan& hp, optimus_act act = OPTIMUS_ACT_NONE,
+                                            const void* const* act_x = nullptr, const int64_t* ld_act_x = nullptr) {
   optimus_status st = optimus_validate_linear_backward(d, G, dt);
   if (st != OPTIMUS_OK) return st;
-  hp.kind = KIND_LINBWD; hp.dt = dt; hp.act = OPTIMUS_ACT_NONE; hp.G = G;
+  const char* what = "grouped_linear_act_backward";
+  if (!act_ok(act)) return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: unknown activation %d", what, (int)act);
+  if (act != OPTIMUS_ACT_NONE) {
+    if (!act_x || !ld_act_x) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: act_x or ld_act_x is NULL", what);
+    for (int g = 0; g < G; ++g) {
+      if (!d[g].dx) continue;
+      if (!act_x[g] && d[g].M > 0 && d[g].K > 0)
+        return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d: act_x is NULL", what, g);
+      if (ld_act_x[g] < d[g].K) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d: ld_act_x < K", what, g);
+    }
+  }
+  hp.kind = KIND_LINBWD; hp.dt = dt; hp.act = act; hp.G = G;
   const size_t s = dtype_size(dt);
   const int VEC = dt == OPTIMUS_F32 ? 4 : 8;
   std::vector<DevLinear> dxs, dws;
@@ -750,6 +772,11 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       o.M = (int32_t)m.M; o.N = (int32_t)m.K; o.K = (int32_t)m.N;
       const bool vout = m.lddx % VEC == 0 && aligned16(m.dx);
       o.vec = 1 | 4 | (vout ? 2 : 0);
+      if (act != OPTIMUS_ACT_NONE) {  // fused into the epilogue
+        o.ax = act_x[g];
+        o.ldax = ld_act_x[g];
+        o.vec |= (o.ldax % VEC == 0 && aligned16(o.ax)) ? 8 : 0;
+      }
       o.inv_n = 1.0f / (float)m.K;
       dxs.push_back(o);
       dx_ids.push_back(g);
@@ -806,10 +833,11 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
   hp.chain_launches = 0;
   std::string name;
   hp.tp_chain.assign(G, RowLaunch{});
+  static const char* const act_names[] = {"", "_relu", "_sigmoid", "_tanh", "_silu"};
   if (!dxs.empty() && direct) {
     GemmSet& gs = hp.gs[hp.n_gs++];
-    build_gemm_set(hp, gs, dx_cfg, 2, dxs, dx_ids, G, OPTIMUS_ACT_NONE, false);
-    name = std::string(gs.cfg.name) + "_dgrad_direct";
+    build_gemm_set(hp, gs, dx_cfg, 2, dxs, dx_ids, G, act, false);
+    name = std::string(gs.cfg.name) + "_dgrad_direct" + act_names[(int)act];
   } else if (!dxs.empty()) {
     // the transposes of W, then dX on the forward kernels (direct-to-LDS when
     // dY rows and N are 16-byte multiples)
@@ -828,7 +856,26 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
                    OPTIMUS_ACT_NONE, false);
     for (size_t i = 0; i < dxs.size(); ++i)
       hp.scratch_fixups.push_back(gs.descs_off + i * sizeof(DevLinear) + offsetof(DevLinear, w));
-    name = std::string(gs.cfg.name) + "_dgrad";
+    name = std::string(gs.cfg.name) + "_dgrad" + act_names[(int)act];
+    if (act != OPTIMUS_ACT_NONE) {
+      // no fused epilogue on these tiles: one grouped activation-backward
+      // launch over dX in place, x = act_x (members without dX get no rows)
+      std::vector<DevRowsGrad> rm;
+      for (int g = 0; g < G; ++g) {
+        const bool has = d[g].dx != nullptr;
+        rm.push_back(make_rows_grad(has ? act_x[g] : nullptr, has ? ld_act_x[g] : 1, d[g].dx, d[g].lddx, d[g].dx,
+                                    d[g].lddx, nullptr, has ? d[g].M : 0, d[g].K, 0.f, dt, false));
+      }
+      std::vector<int> nt;
+      std::vector<RowTile> rt = grad_row_tiles(hp, rm, s, nt);
+      const size_t roff = hp.blob.add(rm.data(), rm.size() * sizeof(DevRowsGrad));
+      const size_t rtoff = hp.blob.add(rt.data(), rt.size() * sizeof(RowTile));
+      for (auto& c : hp.rows_chain) {
+        c.descs_off = roff;
+        c.tiles_off = rtoff;
+      }
+      hp.rows = RowLaunch{roff, rtoff, 0, (int32_t)rt.size(), row_grid((int64_t)rt.size())};
+    }
   }
   hp.red_chain.assign(G, RowLaunch{});
   if (!dws.empty()) {
@@ -951,7 +998,9 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
   }
   for (const RowLaunch& c : hp.red_chain) hp.chain_launches += c.num_tiles > 0 ? 1 : 0;
   for (const RowLaunch& c : hp.tp_chain) hp.chain_launches += c.num_tiles > 0 ? 1 : 0;
-  hp.launches = std::max(hp.n_gs, 1) + (hp.red.num_tiles > 0 ? 1 : 0) + (hp.tp.num_tiles > 0 ? 1 : 0);
+  for (const RowLaunch& c : hp.rows_chain) hp.chain_launches += c.num_tiles > 0 ? 1 : 0;
+  hp.launches = std::max(hp.n_gs, 1) + (hp.red.num_tiles > 0 ? 1 : 0) + (hp.tp.num_tiles > 0 ? 1 : 0) +
+                (hp.rows.num_tiles > 0 ? 1 : 0);
   hp.grid = hp.n_gs ? hp.gs[0].grid : 0;
   hp.block = hp.n_gs ? hp.gs[0].cfg.threads : 0;
   hp.kernel = name.empty() ? "grouped_linear_backward_empty" : name;
@@ -983,7 +1032,7 @@ static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, in
 // partial row of dgamma / dbeta that the finalize reads back).
 static constexpr int64_t kGradMaxTilesPerMember = 64;
 static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
-                                           std::vector<int>& ntiles, int64_t max_tiles = 0) {
+                                           std::vector<int>& ntiles, int64_t max_tiles) {
   std::vector<RowTile> tiles;
   hp.rows_chain.clear();
   ntiles.assign(members.size(), 0);
@@ -1571,8 +1620,15 @@ static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t st
       }
       for (int i = 0; i < hp.n_gs; ++i) {
         const GemmSet& g = hp.gs[i];
-        hipError_t e = gemm_launch(g.cfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(table, g.descs_off),
+        hipError_t e = gemm_launch(g.cfg, hp.dt, g.act, hp.g_ln, at<DevLinear>(table, g.descs_off),
                                    at<GemmTile>(table, g.tiles_off), g.num_tiles, g.grid, stream, g.tr);
+        if (e != hipSuccess) return e;
+      }
+      if (hp.kind == KIND_LINBWD && hp.rows.num_tiles > 0) {
+        // the activation backward of the layer below, over dX in place
+        hipError_t e = act_backward_launch(hp.dt, hp.act, at<DevRowsGrad>(table, hp.rows.descs_off),
+                                           at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles, hp.rows.grid,
+                                           stream);
         if (e != hipSuccess) return e;
       }
       return splitk_reduce_launch(hp.dt, at<SplitReduceItem>(table, hp.red.descs_off), hp.red.num_tiles, hp.red.grid,
@@ -1692,6 +1748,14 @@ extern "C" optimus_status optimus_plan_layernorm_backward(const optimus_layernor
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
+extern "C" optimus_status optimus_plan_linear_act_backward(const optimus_linear_grad_desc* d, const void* const* act_x,
+                                                           const int64_t* ld_act_x, int32_t G, optimus_dtype dt,
+                                                           optimus_act act, optimus_plan* out) {
+  HostPlan hp;
+  optimus_status st = build_linear_backward(d, G, dt, hp, act, act_x, ld_act_x);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
 extern "C" optimus_status optimus_plan_layernorm_act_backward(const optimus_layernorm_grad_desc* d,
                                                               const void* const* beta, int32_t G, optimus_dtype dt,
                                                               optimus_act act, optimus_plan* out) {
@@ -1787,8 +1851,13 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
           const GemmSet& gs = hp.gs[i];
           const RowLaunch& c = gs.chain[g];
           if (c.num_tiles > 0)
-            e = gemm_launch(gs.cfg, hp.dt, hp.act, hp.g_ln, at<DevLinear>(p->table, gs.descs_off),
+            e = gemm_launch(gs.cfg, hp.dt, gs.act, hp.g_ln, at<DevLinear>(p->table, gs.descs_off),
                             at<GemmTile>(p->table, gs.tiles_off) + c.first_tile, c.num_tiles, c.grid, st, gs.tr);
+        }
+        if (e == hipSuccess && hp.kind == KIND_LINBWD && hp.rows.num_tiles > 0 && hp.rows_chain[g].num_tiles > 0) {
+          const RowLaunch& c = hp.rows_chain[g];
+          e = act_backward_launch(hp.dt, hp.act, at<DevRowsGrad>(p->table, c.descs_off),
+                                  at<RowTile>(p->table, c.tiles_off) + c.first_tile, c.num_tiles, c.grid, st);
         }
         if (e == hipSuccess && !hp.red_chain.empty() && hp.red_chain[g].num_tiles > 0) {
           const RowLaunch& r = hp.red_chain[g];
@@ -1950,6 +2019,14 @@ extern "C" optimus_status optimus_grouped_layernorm_backward(const optimus_layer
                                                              optimus_dtype dt, optimus_stream_t stream) {
   HostPlan hp;
   optimus_status st = build_layernorm_backward(d, G, dt, hp);
+  return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
+}
+extern "C" optimus_status optimus_grouped_linear_act_backward(const optimus_linear_grad_desc* d,
+                                                              const void* const* act_x, const int64_t* ld_act_x,
+                                                              int32_t G, optimus_dtype dt, optimus_act act,
+                                                              optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_linear_backward(d, G, dt, hp, act, act_x, ld_act_x);
   return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
 }
 extern "C" optimus_status optimus_grouped_layernorm_act_backward(const optimus_layernorm_grad_desc* d,

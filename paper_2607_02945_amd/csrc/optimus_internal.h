@@ -34,6 +34,11 @@ struct DevLinear {
   // when not split
   float* ws;
   int32_t kchunk, splits;
+  // input gradient with the activation backward of the layer below fused in
+  // (dX = (dY W) * act'(ax), the instance's activation): ax [M][N] is that
+  // activation's input, row stride ldax; vec bit 3 = ax rows 16-B loadable
+  const void* ax;
+  int64_t ldax;
 };
 
 // Sum of the split partials of one member over rows [row0, row0 + nrows):

@@ -294,6 +294,44 @@ def test_layernorm_backward_variants(dtype):
     _check_ln_bwd(ms, dtype, "unaligned")
 
 
+# ------------------------------------------------------------------ fused dX activation backward
+@pytest.mark.parametrize("act", ["relu", "tanh", "silu"])
+@pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
+@pytest.mark.parametrize("aligned", [True, False])
+def test_linear_act_backward(act, mode, aligned):
+    """dX with the activation backward of the layer below fused in: the
+    input gradient times act'(a), a the activation's input [M][K]; against
+    the oracle's Linear backward then activation backward. Aligned groups
+    fuse it into the dX epilogue, others add one activation-backward launch."""
+    say(f"[linear+act bwd] {act} {mode} aligned={aligned}")
+    shapes = [(700, 296, 264), (129, 64, 32), (257, 8, 520)] if aligned else [(300, 200, 136), (64, 17, 40)]
+    ms = _linear_members(shapes, "bf16", seed=590)
+    g = synth.rng(591)
+    acts = [_t(g.standard_normal((m["M"], m["K"])), "bf16") for m in ms]
+    for m in ms:
+        m["dx"] = _empty((m["M"], m["K"]), "bf16")
+        m["dw"] = _empty((m["N"], m["K"]), "bf16")
+        m["db"] = torch.full((m["N"],), float("nan"), dtype=torch.bfloat16, device="cuda")
+    args = ([m["x"] for m in ms], [m["w"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms],
+            [m["dw"] for m in ms], [m["db"] for m in ms], [a[0] for a in acts], act)
+    if mode == "oneshot":
+        B.optimus_grouped_linear_act_backward(*args)
+    else:
+        p = B.optimus_plan_linear_act_backward(*args)
+        info = p.info()
+        n = _launches(info) + (0 if aligned else 1)
+        assert ("_dgrad_direct_" + act in info["kernel"]) == aligned and info["launches"] == n, info
+        p.execute(mode)
+        torch.cuda.synchronize()
+        p.close()
+    torch.cuda.synchronize()
+    for i, m in enumerate(ms):
+        rdx, rdw, rdb = ORC.linear_backward(m["x64"], m["w64"], m["dy64"])
+        assert_close(host64(m["dx"]), ORC.act_backward(acts[i][1], rdx, act), "bf16", f"{act} member {i} dx")
+        assert_close(host64(m["dw"]), rdw, "bf16", f"{act} member {i} dw")
+        assert_close(host64(m["db"][None, :])[0], rdb, "bf16", f"{act} member {i} db")
+
+
 # ------------------------------------------------------------------ fused LayerNorm + activation
 def _ref_ln_act_bwd(m, beta64, act, eps):
     """The oracle composition: the activation's input z = LayerNorm(x) (fp64,
@@ -473,10 +511,10 @@ def test_large_group_backward_full_size_sampled():
 @pytest.mark.timeout(300)
 def test_towers_backward_full_size_sampled():
     """The towers group's training backward at full size (26 towers, batch
-    4096) as the benchmark runs it: LayerNorm, layer 2, relu (in place) and
-    layer 1 backward plans; per operator against the oracle fed the GPU's
-    stored inputs, on sampled rows (dW / db: sampled output rows over the
-    whole batch; dgamma: every row)."""
+    4096) as the benchmark runs it: LayerNorm backward, layer 2 backward with
+    the relu backward fused into its dX, layer 1 backward; per operator
+    against the oracle fed the GPU's stored inputs, on sampled rows (dW / db:
+    sampled output rows over the whole batch; dgamma: every row)."""
     say("[towers bwd] 26 towers B=4096 bf16")
     wl = synth.towers(0)
     T = wl.towers
@@ -499,16 +537,11 @@ def test_towers_backward_full_size_sampled():
     dgm, dbt = [torch.empty_like(g) for g in gm], [torch.empty_like(g) for g in gm]
     torch.cuda.synchronize()
     ln_b = B.optimus_plan_layernorm_backward(o, dz, do, gm, dgm, dbt, wl.eps)
-    ln_b.execute("grouped")
-    l2_b = B.optimus_plan_linear_backward(h, w2, do, dh, dw2, db2)
-    l2_b.execute("grouped")
-    torch.cuda.synchronize()
-    dh_lin = [host64(v) for v in dh]   # layer 2's dX before the in-place relu backward
-    relu_b = B.optimus_plan_act_backward(hp, dh, dh, "relu")
+    l2_b = B.optimus_plan_linear_act_backward(h, w2, do, dh, dw2, db2, hp, "relu")   # dX leaves as d(hp)
     l1_b = B.optimus_plan_linear_backward(xs, w1, dh, dx, dw1, db1)
     say(f"  layer 2: {l2_b.info()['kernel']}; layer 1: {l1_b.info()['kernel']}")
-    relu_b.execute("grouped")
-    l1_b.execute("grouped")
+    for p in (ln_b, l2_b, l1_b):
+        p.execute("grouped")
     torch.cuda.synchronize()
     rows = _sample(4096, 48, seed=65)
     for i, t in enumerate(T):
@@ -519,14 +552,14 @@ def test_towers_backward_full_size_sampled():
         assert_close(host64(dgm[i][None, :])[0], r_dg, "bf16", f"tower {i} dgamma")
         assert_close(host64(dbt[i][None, :])[0], r_dbt, "bf16", f"tower {i} dbeta")
         h64, w2_64 = host64(h[i]), synth.exact64(t.w2)
-        assert_close(dh_lin[i][rows], ORC.linear_backward(h64[rows], w2_64, do64[rows])[0], "bf16", f"tower {i} dH")
         ns = _sample(256, 6, seed=66 + i)
         r_dw2, r_db2 = _dw_sampled(h64, w2_64, do64, ns)
         assert_close(host64(dw2[i])[ns], r_dw2, "bf16", f"tower {i} dW2 rows")
         assert_close(host64(db2[i][None, :])[0][ns], r_db2, "bf16", f"tower {i} db2")
         dhp64 = host64(dh[i])
-        assert_close(dhp64[rows], ORC.act_backward(host64(hp[i])[rows], dh_lin[i][rows], "relu"), "bf16",
-                     f"tower {i} drelu")
+        r_dh = ORC.linear_backward(h64[rows], w2_64, do64[rows])[0]
+        assert_close(dhp64[rows], ORC.act_backward(host64(hp[i])[rows], r_dh, "relu"), "bf16",
+                     f"tower {i} layer-2 dX with the relu backward")
         x64, w1_64 = synth.exact64(t.x), synth.exact64(t.w1)
         assert_close(host64(dx[i])[rows], ORC.linear_backward(x64[rows], w1_64, dhp64[rows])[0], "bf16",
                      f"tower {i} dX")
