@@ -781,7 +781,9 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       dxs.push_back(o);
       dx_ids.push_back(g);
       hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
-      hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K);
+      // dY, W and dX, plus the activation input the fused epilogue reads
+      hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K *
+                               (act != OPTIMUS_ACT_NONE ? 2.0 : 1.0));
     } else if (m.dx) {
       // dX = dY . W as a forward GEMM on W^T [K][N'] (N' = N rounded up to 8
       // values), transposed into plan scratch by the first launch
@@ -807,7 +809,9 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       sh.x = m.dy; sh.ldx = m.lddy; sh.w = (const void*)(uintptr_t)256; sh.ldw = ldt;  // W^T: 256-byte aligned
       dx_shape.push_back(sh);
       hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
-      hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K);
+      // dY, W and dX; the separate activation backward reads a and dX and writes dX
+      hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K *
+                               (act != OPTIMUS_ACT_NONE ? 4.0 : 1.0));
     }
     if (m.dw) {
       DevLinear o{};
