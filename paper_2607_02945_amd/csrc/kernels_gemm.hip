@@ -1086,6 +1086,18 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
       }
 #pragma unroll
       for (int h = 0; h < S::NH; ++h) {
+        // AG: this pass's activation-input chunks go out before the staging,
+        // so their latency overlaps it and the wave barrier
+        u32x4 av[S::HR / RPP];
+        if constexpr (AG != 0) {
+#pragma unroll
+          for (int r = 0; r < S::HR / RPP; ++r) {
+            const int lim = Mr - (wrow0 + h * S::HR + r * RPP);
+            av[r] = (lrow < lim && col_vec && (d.vec & 8))
+                        ? ld16_nt(abase + (int64_t)(h * S::HR + r * RPP) * d.ldax)
+                        : u32x4{0u, 0u, 0u, 0u};
+          }
+        }
 #pragma unroll
         for (int j = 0; j < S::FN; ++j) {
 #pragma unroll
@@ -1120,7 +1132,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
               if (col_vec && (d.vec & 8)) {
                 float g[8], a[8];
                 Elem<bf16_t>::unpack(v, g);
-                Elem<bf16_t>::unpack(ld16_nt(ap), a);
+                Elem<bf16_t>::unpack(av[r], a);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) g[e] *= act_grad<AG>(a[e]);
                 st16_nt(yp, Elem<bf16_t>::pack(g));
