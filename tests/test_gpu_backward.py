@@ -332,6 +332,27 @@ def test_linear_act_backward(act, mode, aligned):
         assert_close(host64(m["db"][None, :])[0], rdb, "bf16", f"{act} member {i} db")
 
 
+def test_linear_act_backward_unaligned_activation_input():
+    """Aligned dY / W / dX with the activation input starting one value off
+    16-byte alignment (and a padded row stride): the fused epilogue's
+    per-value path."""
+    say("[linear+act bwd unaligned a]")
+    ms = _linear_members([(700, 296, 264), (129, 64, 32)], "bf16", seed=595)
+    g = synth.rng(596)
+    acts = [_t(g.standard_normal((m["M"], m["K"])), "bf16", pad=3, off=1) for m in ms]
+    for m in ms:
+        m["dx"] = _empty((m["M"], m["K"]), "bf16")
+    p = B.optimus_plan_linear_act_backward([m["x"] for m in ms], [m["w"] for m in ms], [m["dy"] for m in ms],
+                                           [m["dx"] for m in ms], None, None, [a[0] for a in acts], "silu")
+    assert "_dgrad_direct_silu" in p.info()["kernel"], p.info()
+    p.execute("grouped")
+    torch.cuda.synchronize()
+    p.close()
+    for i, m in enumerate(ms):
+        rdx = ORC.linear_backward(m["x64"], m["w64"], m["dy64"])[0]
+        assert_close(host64(m["dx"]), ORC.act_backward(acts[i][1], rdx, "silu"), "bf16", f"member {i} dx")
+
+
 # ------------------------------------------------------------------ fused LayerNorm + activation
 def _ref_ln_act_bwd(m, beta64, act, eps):
     """The oracle composition: the activation's input z = LayerNorm(x) (fp64,
