@@ -314,7 +314,9 @@ optimus_status optimus_grouped_layernorm_backward(const optimus_layernorm_grad_d
  * the Linear's and the activation's, in one launch set). act_x: G device
  * pointers to a [M][K] (the member's dtype; entries of members without dx
  * are ignored), ld_act_x: G row strides (>= K). dW and db are those of
- * optimus_grouped_linear_backward. Where the input-gradient GEMM cannot read W
+ * optimus_grouped_linear_backward. act_x may be the member's dx itself (in
+ * place: every value is read before it is written) and must not overlap any
+ * other output (OPTIMUS_ERR_ALIASING). Where the input-gradient GEMM cannot read W
  * directly (widths not multiples of 8 values, unaligned rows) the plan adds
  * one grouped activation-backward launch over dX instead. act = NONE is
  * optimus_grouped_linear_backward. Errors as there, plus

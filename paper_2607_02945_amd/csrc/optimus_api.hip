@@ -737,6 +737,19 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
         return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d: act_x is NULL", what, g);
       if (ld_act_x[g] < d[g].K) return fail(OPTIMUS_ERR_INVALID_ARG, "%s: member %d: ld_act_x < K", what, g);
     }
+    // act_x is read while dX, dW and db are written: it may be a member's dX
+    // itself (each value is read before it is written), no other output
+    std::vector<Region> regs;
+    const size_t es = dtype_size(dt);
+    for (int g = 0; g < G; ++g) {
+      if (!d[g].dx || d[g].M <= 0 || d[g].K <= 0) continue;
+      regs.push_back(region(act_x[g], ld_act_x[g], d[g].M, d[g].K, es, g, false));
+      regs.push_back(region(d[g].dx, d[g].lddx, d[g].M, d[g].K, es, g, true));
+      if (d[g].dw) regs.push_back(region(d[g].dw, d[g].lddw, d[g].N, d[g].K, es, g, true));
+      if (d[g].db) regs.push_back(region(d[g].db, d[g].N, 1, d[g].N, es, g, true));
+    }
+    st = check_aliasing(regs, true, what);
+    if (st != OPTIMUS_OK) return st;
   }
   hp.kind = KIND_LINBWD; hp.dt = dt; hp.act = act; hp.G = G;
   const size_t s = dtype_size(dt);

@@ -258,6 +258,17 @@ def test_backward_validation():
     assert B.optimus_validate_linear_backward(a, G, B.BF16) == ALIASING
     a, G = arr(B.LinearGradDesc, lg(), lg(x=7 * MB, w=8 * MB, dy=9 * MB, dx=10 * MB, dw=11 * MB, db=6 * MB))
     assert B.optimus_validate_linear_backward(a, G, B.BF16) == ALIASING   # two members' db
+    # Linear with a fused activation backward: act_x checks (all before any device call)
+    f = B.lib().optimus_grouped_linear_act_backward
+    a, G = arr(B.LinearGradDesc, lg())
+    ptrs = lambda *p: (ctypes.c_void_p * 1)(*p)
+    lds = lambda *v: (ctypes.c_int64 * 1)(*v)
+    assert f(a, ptrs(5 * MB + 96), lds(48), G, B.BF16, 1, None) == ALIASING     # over dW
+    assert f(a, ptrs(6 * MB), lds(48), G, B.BF16, 1, None) == ALIASING          # over db
+    assert f(a, ptrs(None), lds(48), G, B.BF16, 1, None) == INVALID             # NULL act_x
+    assert f(a, ptrs(13 * MB), lds(47), G, B.BF16, 1, None) == INVALID          # ld < K
+    assert f(a, None, None, G, B.BF16, 3, None) == INVALID                       # no arrays
+    assert f(a, ptrs(13 * MB), lds(48), G, B.BF16, 9, None) == UNSUPPORTED      # unknown activation
     # LayerNorm: rows 64, cols 48
     ln = lambda **kw: B.LayerNormGradDesc(*[kw.get(k, v) for k, v in [
         ("x", 1 * MB), ("ldx", 48), ("gamma", 2 * MB), ("dy", 3 * MB), ("lddy", 48), ("dx", 4 * MB), ("lddx", 48),
