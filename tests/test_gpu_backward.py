@@ -299,19 +299,31 @@ def test_layernorm_backward_variants(dtype):
 @pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
 @pytest.mark.parametrize("aligned", [True, False])
 def test_linear_act_backward(act, mode, aligned):
+    _linear_act_backward_case(act, mode, aligned, "bf16")
+
+
+@pytest.mark.parametrize("act", ["sigmoid", "silu"])
+@pytest.mark.parametrize("mode", ["grouped", "chain"])
+def test_linear_act_backward_fp32(act, mode):
+    """fp32 groups never take the direct-to-LDS dX: the plan adds the grouped
+    activation-backward launch over dX."""
+    _linear_act_backward_case(act, mode, False, "fp32")
+
+
+def _linear_act_backward_case(act, mode, aligned, dtype):
     """dX with the activation backward of the layer below fused in: the
     input gradient times act'(a), a the activation's input [M][K]; against
     the oracle's Linear backward then activation backward. Aligned groups
     fuse it into the dX epilogue, others add one activation-backward launch."""
-    say(f"[linear+act bwd] {act} {mode} aligned={aligned}")
+    say(f"[linear+act bwd] {act} {mode} aligned={aligned} {dtype}")
     shapes = [(700, 296, 264), (129, 64, 32), (257, 8, 520)] if aligned else [(300, 200, 136), (64, 17, 40)]
-    ms = _linear_members(shapes, "bf16", seed=590)
+    ms = _linear_members(shapes, dtype, seed=590)
     g = synth.rng(591)
-    acts = [_t(g.standard_normal((m["M"], m["K"])), "bf16") for m in ms]
+    acts = [_t(g.standard_normal((m["M"], m["K"])), dtype) for m in ms]
     for m in ms:
-        m["dx"] = _empty((m["M"], m["K"]), "bf16")
-        m["dw"] = _empty((m["N"], m["K"]), "bf16")
-        m["db"] = torch.full((m["N"],), float("nan"), dtype=torch.bfloat16, device="cuda")
+        m["dx"] = _empty((m["M"], m["K"]), dtype)
+        m["dw"] = _empty((m["N"], m["K"]), dtype)
+        m["db"] = torch.full((m["N"],), float("nan"), dtype=synth.DTYPES[dtype], device="cuda")
     args = ([m["x"] for m in ms], [m["w"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms],
             [m["dw"] for m in ms], [m["db"] for m in ms], [a[0] for a in acts], act)
     if mode == "oneshot":
@@ -327,9 +339,9 @@ def test_linear_act_backward(act, mode, aligned):
     torch.cuda.synchronize()
     for i, m in enumerate(ms):
         rdx, rdw, rdb = ORC.linear_backward(m["x64"], m["w64"], m["dy64"])
-        assert_close(host64(m["dx"]), ORC.act_backward(acts[i][1], rdx, act), "bf16", f"{act} member {i} dx")
-        assert_close(host64(m["dw"]), rdw, "bf16", f"{act} member {i} dw")
-        assert_close(host64(m["db"][None, :])[0], rdb, "bf16", f"{act} member {i} db")
+        assert_close(host64(m["dx"]), ORC.act_backward(acts[i][1], rdx, act), dtype, f"{act} member {i} dx")
+        assert_close(host64(m["dw"]), rdw, dtype, f"{act} member {i} dw")
+        assert_close(host64(m["db"][None, :])[0], rdb, dtype, f"{act} member {i} db")
 
 
 def test_linear_act_backward_unaligned_activation_input():
