@@ -167,6 +167,26 @@ def test_linear_backward_split_reduction(dtype, mode, aligned):
     _check_linear_bwd(ms2, dtype, f"split, no db {dtype} {mode}", want=("dx", "dw"))
 
 
+@pytest.mark.parametrize("splits", [1, 2, 3, 5, 7])
+def test_linear_backward_pinned_split_counts(splits):
+    """dW on the direct-to-LDS tiles with the batch split 1..7 ways (pinned),
+    ragged batches so that the last split is shorter, db from the split row
+    sums; the same results for every count."""
+    say(f"[linear bwd splits={splits}]")
+    ms = _linear_members([(5000, 256, 264), (3001, 64, 520)], "bf16", seed=600)
+    old = os.environ.get("OPTIMUS_WGRAD_SPLITS")
+    os.environ["OPTIMUS_WGRAD_SPLITS"] = str(splits)
+    try:
+        info = _run_linear_bwd(ms, "bf16", "grouped")
+    finally:
+        if old is None:
+            del os.environ["OPTIMUS_WGRAD_SPLITS"]
+        else:
+            os.environ["OPTIMUS_WGRAD_SPLITS"] = old
+    assert ("_split%d" % splits in info["kernel"]) == (splits > 1) and "dma" in _wgrad_part(info), info
+    _check_linear_bwd(ms, "bf16", f"splits {splits}")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_linear_backward_strided_and_partial(dtype):
     """Row strides above the row lengths everywhere (the 16-byte paths), then
