@@ -1,28 +1,37 @@
 """Benchmark: microseconds per op-group of the grouped launches vs the per-op launch chain.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload launch_bound]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload large_group]
 
 One step = one pass of the workload's op-group (every grouped launch of the
-group, e.g. grouped Linear + fused sigmoid for `launch_bound`) over one batch
-of seeded synthetic input that is already resident in HBM. Inputs are
-rotated over enough copies that each step reads data no longer held in the
-256 MB last-level cache. Prints one JSON line.
+group, e.g. grouped Linear then grouped LayerNorm + tanh for `large_group`)
+over one batch of seeded synthetic input that is already resident in HBM.
+Inputs are rotated over enough copies that each step reads data no longer held
+in the 256 MB last-level cache. Prints one JSON line.
 
-`value` is the mean time of the timed steps between one pair of HIP events.
-Then every launch of the op-group is run `--steps` times back to back over
-the same rotating inputs between one more pair of events; the slowest is the
-dominant kernel, whose mean launch duration divides its algorithmic flops or
-bytes for `roofline` (a plan of several launches -- the scaled fp8 quantize --
-counts them together, `roofline.kernels`), and `other_kernels` lists the rest (e.g. the grouped
-LayerNorm after a grouped Linear). `traffic` is the HBM bytes per launch from
-the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary when that was taken
-on the current kernel sources.
+Timing protocol. Before anything is timed the op-group runs for at least
+SETTLE_SECONDS (`settle_s`: the clocks ramp over the first tens of
+milliseconds of load), then W untimed warm-up steps (`warmup`, as requested),
+then K steps between one pair of HIP events on the launch stream: `value` is
+their mean. Every launch of the op-group is then timed the same way (settle,
+W warm-up launches, K launches back to back between one event pair); the
+slowest is the dominant kernel, whose mean launch duration divides its
+algorithmic flops or bytes for `roofline`, and `other_kernels` lists the rest.
+A single-launch op-group's dominant kernel is the op-group itself, so its
+`kernel_us` is `value`. `reps` follows the paper's protocol (Sec. 5.2: 3
+warm-ups, 100 repetitions) with one event pair per step: p10 / median / p90.
+`traffic` is the HBM bytes per launch from the committed rocprofv3 FETCH_SIZE
+/ WRITE_SIZE summary when that was taken on the current kernel sources.
+`plan_us` is the host time to build and upload the op-group's plans (the
+analogue of the paper's compile time; outside every timed region).
 
-Workloads (the seeded groups of paper_2607_02945_amd.synth): launch_bound
-(default; G=256 bf16 Linear + sigmoid, B=2048), tiny_group, split_op_cat,
-towers, large_group, decompose_mm, act_quant (fp8 quantize of 32 saved
-activations, then dequantize), towers_bwd and large_group_bwd (the training
-backward of the towers and large_group op-groups).
+Workloads (the seeded groups of paper_2607_02945_amd.synth): large_group
+(default; G=32 bf16 Linear, B=16384, K=1024, then LayerNorm + tanh),
+large_group_shared (the same members on ONE shared input), tiny_group,
+launch_bound (G=256 bf16 Linear + sigmoid, B=2048; also timed as two launches,
+Linear then grouped sigmoid), split_op_cat, towers, decompose_mm, act_quant
+(fp8 quantize of 32 saved activations, then dequantize), towers_bwd and
+large_group_bwd (the training backward of the towers and large_group
+op-groups).
 """
 from __future__ import annotations
 
@@ -41,7 +50,8 @@ HBM_PEAK_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 CACHE_BYTES = 512 << 20  # rotate inputs over at least this much memory per step cycle
 COPY_BYTES = 1 << 30     # the calibration copy: 1 GiB read and 1 GiB written, far beyond the caches
-WARMUP_SECONDS = 0.3
+SETTLE_SECONDS = 0.3
+PAPER_WARMUP, PAPER_REPS = 3, 100  # the paper's timing protocol (Sec. 5.2)
 LN_FUSE_MAX_N = {"fp32": 128, "bf16": 256}  # widest row the GEMM epilogue can normalise
 
 
@@ -49,12 +59,11 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=None,
-                    help="untimed steps before timing (default: at least 20 and at least 0.3 s of work, "
-                         "so that the clocks have settled)")
-    ap.add_argument("--workload", default="launch_bound",
-                    choices=["launch_bound", "tiny_group", "split_op_cat", "towers", "large_group", "decompose_mm",
-                             "act_quant", "towers_bwd", "large_group_bwd"])
+    ap.add_argument("--warmup", type=int, default=PAPER_WARMUP,
+                    help="untimed steps before each timed run, after the time-based clock settle")
+    ap.add_argument("--workload", default="large_group",
+                    choices=["large_group", "large_group_shared", "launch_bound", "tiny_group", "split_op_cat",
+                             "towers", "decompose_mm", "act_quant", "towers_bwd", "large_group_bwd"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-chain", action="store_true", help="skip timing the per-op launch chain")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -82,6 +91,16 @@ class OpGroup:
         self.horizontal = []   # split-op-cat only: horizontal fusion without the vertical rewrite
         self.tiled = []        # decompose_mm only: the group through the tiled GEMM kernel
         self.unscaled = []     # act_quant only: quantize without the per-tensor scale
+        self.two_launch = []   # launch_bound only: the Linear, then a grouped pointwise launch
+        self.pw_only = []      # launch_bound only: that grouped pointwise launch alone
+        self.plan_s = 0.0      # host time spent building the grouped plans
+
+    def plan(self, fn, *args, **kw):
+        """Build one plan of the optimized program, timing its creation."""
+        t0 = time.perf_counter()
+        p = fn(*args, **kw)
+        self.plan_s += time.perf_counter() - t0
+        return p
 
     def run(self, which, stream=None):
         for plan, mode in getattr(self, which):
@@ -96,14 +115,16 @@ def build_copy(name, wl, torch, B):
     og = OpGroup()
     cu = lambda t: t.to("cuda")
     bf = torch.bfloat16
-    if name in ("launch_bound", "tiny_group", "large_group", "decompose_mm"):
-        xs = [cu(m.x) for m in wl.members]
+    if name in ("launch_bound", "tiny_group", "large_group", "large_group_shared", "decompose_mm"):
+        # members that share one input tensor keep sharing its device copy
+        dev_of = {}
+        xs = [dev_of.setdefault(id(m.x), cu(m.x)) for m in wl.members]
         ws = [cu(m.w) for m in wl.members]
         bs = [None if m.b is None else cu(m.b) for m in wl.members]
         dt = xs[0].dtype
         ys = [torch.empty((m.M, m.N), dtype=dt, device="cuda") for m in wl.members]
         if not wl.ln:
-            lin = B.optimus_plan_linear(xs, ws, bs, ys, wl.act)
+            lin = og.plan(B.optimus_plan_linear, xs, ws, bs, ys, wl.act)
             og.grouped = [(lin, "grouped")]
             if wl.act == "none":
                 og.chain = [(lin, "chain")]
@@ -113,24 +134,26 @@ def build_copy(name, wl, torch, B):
                 lin0 = B.optimus_plan_linear(xs, ws, bs, y1, "none")
                 pw = B.optimus_plan_pointwise(y1, ys, wl.act)
                 og.chain = [(lin0, "chain"), (pw, "chain")]
+                # the same op-group as two grouped launches: Linear, then the
+                # grouped pointwise activation over its outputs
+                og.two_launch = [(lin0, "grouped"), (pw, "grouped")]
             if name == "decompose_mm":
-                # the same group through the tiled MFMA GEMM (the paper's "before")
-                os.environ["OPTIMUS_GEMM_VARIANT"] = "3"
-                try:
-                    og.tiled = [(B.optimus_plan_linear(xs, ws, bs, ys, wl.act), "grouped")]
-                finally:
-                    del os.environ["OPTIMUS_GEMM_VARIANT"]
+                # the same group through the tiled fp32 MFMA GEMM (the paper's "before")
+                og.tiled = [(B.optimus_plan_linear_ex(xs, ws, bs, ys, wl.act, options={"gemm_tile": "f32_64x64"}),
+                             "grouped")]
             og.keep = (xs, ws, bs, ys, y1)
         else:
             zs = [torch.empty_like(y) for y in ys]
             gs = [cu(g) for g in wl.gammas]
             be = [cu(b) for b in wl.betas]
-            lin = B.optimus_plan_linear(xs, ws, bs, ys, "none")
-            ln = B.optimus_plan_layernorm(ys, zs, gs, be, wl.eps, wl.act)
             if max(m.N for m in wl.members) <= LN_FUSE_MAX_N[wl.dtype]:
                 # the LayerNorm rides in the GEMM epilogue: one launch
-                og.grouped = [(B.optimus_plan_linear_layernorm(xs, ws, bs, zs, gs, be, wl.eps, wl.act), "grouped")]
+                og.grouped = [(og.plan(B.optimus_plan_linear_layernorm, xs, ws, bs, zs, gs, be, wl.eps, wl.act),
+                               "grouped")]
+                lin = B.optimus_plan_linear(xs, ws, bs, ys, "none")
             else:
+                lin = og.plan(B.optimus_plan_linear, xs, ws, bs, ys, "none")
+                ln = og.plan(B.optimus_plan_layernorm, ys, zs, gs, be, wl.eps, wl.act)
                 og.grouped = [(lin, "grouped"), (ln, "grouped")]
             z1 = [torch.empty_like(y) for y in ys]
             ln0 = B.optimus_plan_layernorm(ys, z1, gs, be, wl.eps, "none")
@@ -142,7 +165,7 @@ def build_copy(name, wl, torch, B):
         y = torch.empty_like(x)
         gs = [cu(g) for g in wl.gammas]
         bs = [cu(b) for b in wl.betas]
-        soc = B.optimus_plan_split_op_cat(x, y, wl.widths, gs, bs, True, wl.eps, wl.act)
+        soc = og.plan(B.optimus_plan_split_op_cat, x, y, wl.widths, gs, bs, True, wl.eps, wl.act)
         og.grouped = [(soc, "grouped")]
         og.chain = [(soc, "chain")]
         og.horizontal = [(soc, "horizontal")]
@@ -154,8 +177,8 @@ def build_copy(name, wl, torch, B):
         qs = [torch.empty(x.shape, dtype=torch.uint8, device="cuda") for x in xs]
         sc = [torch.ones(1, dtype=torch.float32, device="cuda") for _ in xs]
         ys = [torch.empty_like(x) for x in xs]
-        quant = B.optimus_plan_quantize_fp8(xs, qs, sc, True)
-        dequant = B.optimus_plan_dequantize_fp8(qs, sc, ys)
+        quant = og.plan(B.optimus_plan_quantize_fp8, xs, qs, sc, True)
+        dequant = og.plan(B.optimus_plan_dequantize_fp8, qs, sc, ys)
         og.grouped = [(quant, "grouped"), (dequant, "grouped")]
         og.chain = [(quant, "chain"), (dequant, "chain")]
         qs_u = [torch.empty_like(q) for q in qs]
@@ -184,11 +207,11 @@ def build_copy(name, wl, torch, B):
         db1, db2 = [torch.empty_like(b) for b in b1], [torch.empty_like(b) for b in b2]
         dgm, dbt = [torch.empty_like(g) for g in gm], [torch.empty_like(g) for g in gm]
         torch.cuda.synchronize()
-        ln_b = B.optimus_plan_layernorm_backward(o, dz, do, gm, dgm, dbt, wl.eps)
+        ln_b = og.plan(B.optimus_plan_layernorm_backward, o, dz, do, gm, dgm, dbt, wl.eps)
         # layer 2's dX leaves with the relu backward applied (d of the
         # pre-activation hp), as the forward fuses the relu into layer 1
-        l2_b = B.optimus_plan_linear_act_backward(h, w2, do, dh, dw2, db2, hp, "relu")
-        l1_b = B.optimus_plan_linear_backward(xs, w1, dh, dx, dw1, db1)
+        l2_b = og.plan(B.optimus_plan_linear_act_backward, h, w2, do, dh, dw2, db2, hp, "relu")
+        l1_b = og.plan(B.optimus_plan_linear_backward, xs, w1, dh, dx, dw1, db1)
         og.grouped = [(ln_b, "grouped"), (l2_b, "grouped"), (l1_b, "grouped")]
         og.chain = [(ln_b, "chain"), (l2_b, "chain"), (l1_b, "chain")]
         og.keep = (xs, w1, b1, w2, b2, gm, hp, h, o, dz, do, dh, dx, dw1, dw2, db1, db2, dgm, dbt)
@@ -208,8 +231,8 @@ def build_copy(name, wl, torch, B):
         dx, dw, db = [torch.empty_like(x) for x in xs], [torch.empty_like(w) for w in ws], [torch.empty_like(b) for b in bs]
         dgm, dbt = [torch.empty_like(g) for g in gs], [torch.empty_like(g) for g in gs]
         torch.cuda.synchronize()
-        lnt_b = B.optimus_plan_layernorm_act_backward(y, dt_, dy, gs, bes, dgm, dbt, wl.eps, "tanh")
-        lin_b = B.optimus_plan_linear_backward(xs, ws, dy, dx, dw, db)
+        lnt_b = og.plan(B.optimus_plan_layernorm_act_backward, y, dt_, dy, gs, bes, dgm, dbt, wl.eps, "tanh")
+        lin_b = og.plan(B.optimus_plan_linear_backward, xs, ws, dy, dx, dw, db)
         og.grouped = [(lnt_b, "grouped"), (lin_b, "grouped")]
         og.chain = [(lnt_b, "chain"), (lin_b, "chain")]
         og.keep = (xs, ws, bs, gs, bes, y, dt_, dy, dx, dw, db, dgm, dbt)
@@ -221,11 +244,11 @@ def build_copy(name, wl, torch, B):
         z = [torch.empty_like(v) for v in o]
         w1, b1, w2, b2 = ([cu(getattr(t, a)) for t in T] for a in ("w1", "b1", "w2", "b2"))
         gm, be = [cu(t.gamma) for t in T], [cu(t.beta) for t in T]
-        l1 = B.optimus_plan_linear(xs, w1, b1, h, "relu")
+        l1 = og.plan(B.optimus_plan_linear, xs, w1, b1, h, "relu")
         l2 = B.optimus_plan_linear(h, w2, b2, o, "none")
         ln = B.optimus_plan_layernorm(o, z, gm, be, wl.eps, "none")
         # layer 2 (N = 256) with the LayerNorm in its epilogue: two launches
-        l2ln = B.optimus_plan_linear_layernorm(h, w2, b2, z, gm, be, wl.eps, "none")
+        l2ln = og.plan(B.optimus_plan_linear_layernorm, h, w2, b2, z, gm, be, wl.eps, "none")
         og.grouped = [(l1, "grouped"), (l2ln, "grouped")]
         h0 = [torch.empty_like(v) for v in h]
         l1n = B.optimus_plan_linear(xs, w1, b1, h0, "none")
@@ -248,7 +271,8 @@ def workload_bytes(name, wl):
     if name == "act_quant":
         return sum(x.numel() * (2 + 1 + 2 + 1) for x in wl.xs)
     s = 4 if wl.dtype == "fp32" else 2
-    return sum((m.x.numel() + m.w.numel() + 2 * m.M * m.N) * s for m in wl.members)
+    xb = sum(x.numel() for x in {id(m.x): m.x for m in wl.members}.values())  # a shared input once
+    return (xb + sum(m.w.numel() + 2 * m.M * m.N for m in wl.members)) * s
 
 
 def describe(name, wl):
@@ -275,20 +299,47 @@ def describe(name, wl):
     if name == "decompose_mm":
         return {"workload": name, "G": wl.G, "M": [m.M for m in wl.members], "K": [m.K for m in wl.members],
                 "N": [m.N for m in wl.members], "bias": False, "seed": 0}
-    return {"workload": name, "G": wl.G, "batch": wl.members[0].M,
-            "K": sorted({m.K for m in wl.members}), "N": sorted({m.N for m in wl.members}),
-            "epilogue": ("LayerNorm+" if wl.ln else "") + wl.act, "seed": 0}
+    out = {"workload": name, "G": wl.G, "batch": wl.members[0].M,
+           "K": sorted({m.K for m in wl.members}), "N": sorted({m.N for m in wl.members}),
+           "epilogue": ("LayerNorm+" if wl.ln else "") + wl.act, "seed": 0}
+    if name == "large_group_shared":
+        out["input"] = "one X shared by every member"
+    return out
 
 
 # ---------------------------------------------------------------------- CPU baseline
-def cpu_baseline(name, wl, target_s):
-    """The oracle as it stands, on the host cores, on a bounded sample of the
-    same workload, scaled to microseconds per op-group."""
+def host_cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or ''."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
+def cpu_baseline(name, wl, target_s, threads=None):
+    """The oracle as it stands, on the host cores (all of them, or `threads`),
+    on a bounded sample of the same workload, scaled to microseconds per
+    op-group."""
     import numpy as np
 
     import oracle
     from paper_2607_02945_amd import synth
     orc = oracle.get()
+    all_threads = orc.num_threads()
+    if threads:
+        orc.set_num_threads(threads)
+    try:
+        return _cpu_baseline(orc, np, synth, name, wl, target_s)
+    finally:
+        if threads:
+            orc.set_num_threads(all_threads)
+
+
+def _cpu_baseline(orc, np, synth, name, wl, target_s):
     e = synth.exact64
     t_total, frac_total, reps = 0.0, 0.0, 0
     if name == "split_op_cat":
@@ -353,7 +404,7 @@ def cpu_baseline(name, wl, target_s):
                         for x, w1, b1, w2, b2, g, b in ins]
     else:
         M = wl.members[0].M
-        rows = {"large_group": 64, "decompose_mm": 65536}.get(name, M)
+        rows = {"large_group": 64, "large_group_shared": 64, "decompose_mm": 65536}.get(name, M)
         ins = [(e(m.x[:rows]), e(m.w), e(m.b)) for m in wl.members]
         lns = [(e(g), e(b)) for g, b in zip(wl.gammas, wl.betas)] if wl.ln else None
         # share of the group's work (flops) the sample covers
@@ -376,7 +427,7 @@ def cpu_baseline(name, wl, target_s):
             break
     us = t_total / frac_total * 1e6
     return {"value": round(us, 1), "unit": "µs per op-group", "cores": orc.num_threads(), "kind": "oracle",
-            "sample": f"{sample}, {reps} pass(es), {t_total:.1f} s, fp64 C loops, scaled to one op-group"}
+            "sample": f"{sample}, {reps} pass(es), {t_total:.2f} s, fp64 C loops, scaled to one op-group"}
 
 
 # ---------------------------------------------------------------------- rocprofv3 traffic
@@ -592,25 +643,26 @@ def main():
         else:
             ogs[i % copies].run(which, stream)
 
-    def warm(which, warmup):
-        """W untimed steps, or by default at least 20 and at least WARMUP_SECONDS
-        of work (the clocks ramp up over the first tens of milliseconds)."""
-        if warmup is not None:
-            for i in range(warmup):
-                one(i, which)
-            return warmup
+    def settle(which):
+        """Run `which` for at least SETTLE_SECONDS (the clocks ramp up over the
+        first tens of milliseconds of load); returns the seconds spent."""
         n, t0 = 0, time.perf_counter()
-        while n < 20 or time.perf_counter() - t0 < WARMUP_SECONDS:
+        while n < 10 or time.perf_counter() - t0 < SETTLE_SECONDS:
             for _ in range(10):
                 one(n, which)
                 n += 1
             torch.cuda.synchronize()
-        return n
+        return time.perf_counter() - t0
+
+    settled = {}
 
     def timed(which, steps, warmup):
-        """(ms, wall s) of `steps` back-to-back steps between one pair of HIP
-        events recorded on the launch stream."""
-        warm(which, warmup)
+        """Settle, `warmup` untimed steps, then (ms, wall s) of `steps`
+        back-to-back steps between one pair of HIP events recorded on the
+        launch stream."""
+        settled[which] = settle(which)
+        for i in range(warmup):
+            one(i, which)
         t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         w0 = time.perf_counter()
@@ -621,40 +673,63 @@ def main():
         torch.cuda.synchronize()
         return t_start.elapsed_time(t_end), time.perf_counter() - w0
 
+    def reps_protocol(which):
+        """The paper's protocol: 3 warm-ups, then 100 repetitions each between
+        its own pair of events; p10 / median / p90 in microseconds."""
+        settle(which)
+        for i in range(PAPER_WARMUP):
+            one(i, which)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(PAPER_REPS + 1)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for i in range(PAPER_REPS):
+            one(i, which)
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        us = sorted(ev[i].elapsed_time(ev[i + 1]) * 1000.0 for i in range(PAPER_REPS))
+        q = lambda f: us[min(PAPER_REPS - 1, int(round(f * (PAPER_REPS - 1))))]
+        return {"warmup": PAPER_WARMUP, "reps": PAPER_REPS, "p10_us": round(q(0.1), 3),
+                "median_us": round(q(0.5), 3), "p90_us": round(q(0.9), 3)}
+
     if args.only_plan is not None:
         # one launch of the op-group alone (for rocprofv3 runs that must see
-        # only the dominant kernel): default warm-up, then --steps launches
+        # only the dominant kernel)
         k = args.only_plan
-        warm(k, args.warmup)
-        k_ms = timed(k, args.steps, 0)[0] / args.steps
+        k_ms = timed(k, args.steps, args.warmup)[0] / args.steps
         print(json.dumps({"workload": args.workload, "plan_index": k, "kernel": ogs[0].grouped[k][0].info()["kernel"],
                           "steps": args.steps, "kernel_us": round(k_ms * 1000.0, 3)}), flush=True)
         return
 
-    warmed = warm("grouped", args.warmup)
-    total_ms, wall = timed("grouped", args.steps, 0)
-    # every launch of the op-group alone, launched back to back over the same
-    # inputs: its mean launch duration (one event pair, so no per-launch event
-    # cost); the slowest is the dominant kernel
-    plan_ms = [timed(k, args.steps, 10)[0] / args.steps for k in range(len(ogs[0].grouped))]
+    total_ms, wall = timed("grouped", args.steps, args.warmup)
+    settle_s = settled["grouped"]
+    ms_step = total_ms / args.steps
+    # every launch of the op-group alone, from the same settled state, launched
+    # back to back over the same inputs: its mean launch duration (one event
+    # pair, so no per-launch event cost); the slowest is the dominant kernel.
+    # A single-launch op-group's only launch is the op-group itself.
+    n_plans = len(ogs[0].grouped)
+    plan_ms = [ms_step] if n_plans == 1 else [timed(k, args.steps, args.warmup)[0] / args.steps
+                                              for k in range(n_plans)]
     kd = max(range(len(plan_ms)), key=lambda k: plan_ms[k])
     k_ms = plan_ms[kd]
-    ms_step = total_ms / args.steps
     info = ogs[0].grouped[kd][0].info()
     launches = sum(p.info()["launches"] for p, _ in ogs[0].grouped)
     out = {
         "metric": METRIC, "value": round(ms_step * 1000.0, 3), "unit": "µs", "n_gpus": 1,
-        "steps": args.steps, "warmup": warmed, "ms_per_step": round(ms_step, 6),
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 6),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
         "data": "synthetic (seeded PCG64 draws of the workload's shapes and distributions)",
         "config": describe(args.workload, wl),
-        "launches_per_group": launches, "input_copies": copies, "wall_ms_per_step": round(wall * 1e3 / args.steps, 6),
+        "settle_s": round(settle_s, 3), "launches_per_group": launches, "input_copies": copies,
+        "wall_ms_per_step": round(wall * 1e3 / args.steps, 6),
+        "plan_us": round(ogs[0].plan_s * 1e6, 1),
     }
     # achieved throughput of the whole op-group
     flops = sum(p.info()["flops"] for p, _ in ogs[0].grouped)
     nbytes = sum(p.info()["bytes"] for p, _ in ogs[0].grouped)
     out["group_tflops"] = round(flops / (ms_step * 1e-3) / 1e12, 3)
     out["group_hbm_gbs"] = round(nbytes / (ms_step * 1e-3) / 1e9, 1)
+    out["reps"] = reps_protocol("grouped")
     # roofline of the dominant kernel: algorithmic work per launch / mean launch duration
     ridge = PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
 
@@ -691,31 +766,50 @@ def main():
         out["other_kernels"] = others
     if not args.no_chain:
         csteps = max(5, min(args.steps, 50))
-        c_ms, _ = timed("chain", csteps, 5)
+        c_ms, _ = timed("chain", csteps, args.warmup)
         c_step = c_ms / csteps
         out["chain"] = {"us_per_group": round(c_step * 1000.0, 3),
                         "launches_per_group": sum(p.info()["chain_launches"] for p, m in ogs[0].chain
                                                   if m == "chain") + sum(1 for p, m in ogs[0].chain if m != "chain"),
                         "speedup": round(c_step / ms_step, 2)}
+    if ogs[0].two_launch:
+        # the Linear and the activation as two grouped launches; the grouped
+        # pointwise kernel's own roofline
+        t_ms, _ = timed("two_launch", args.steps, args.warmup)
+        pw_plan = ogs[0].two_launch[1][0]
+        for og in ogs:
+            og.pw_only = [og.two_launch[1]]
+        p_ms, _ = timed("pw_only", args.steps, args.warmup)
+        pinfo = pw_plan.info()
+        pw = roofline(pinfo, p_ms / args.steps)
+        pw.update({"kernel": pinfo["kernel"], "kernel_us": round(p_ms / args.steps * 1000.0, 3),
+                   "algorithmic_bytes": pinfo["bytes"]})
+        out["two_launch"] = {"us_per_group": round(t_ms / args.steps * 1000.0, 3), "launches_per_group": 2,
+                             "pointwise": pw}
     if ogs[0].tiled:
         tsteps = max(5, min(args.steps, 20))
-        t_ms, _ = timed("tiled", tsteps, 2)
+        t_ms, _ = timed("tiled", tsteps, args.warmup)
         t_step = t_ms / tsteps
         out["tiled_gemm"] = {"us_per_group": round(t_step * 1000.0, 3), "kernel": ogs[0].tiled[0][0].info()["kernel"],
                              "speedup": round(t_step / ms_step, 2)}
     if ogs[0].unscaled:
         usteps = max(5, min(args.steps, 50))
-        u_ms, _ = timed("unscaled", usteps, 5)
+        u_ms, _ = timed("unscaled", usteps, args.warmup)
         pinfo = ogs[0].unscaled[0][0].info()
         entry = roofline(pinfo, u_ms / usteps)
         entry.update({"kernel": pinfo["kernel"], "kernel_us": round(u_ms / usteps * 1000.0, 3)})
         out["unscaled_quantize"] = entry
     if ogs[0].horizontal:
         hsteps = max(5, min(args.steps, 50))
-        h_ms, _ = timed("horizontal", hsteps, 2)
+        h_ms, _ = timed("horizontal", hsteps, args.warmup)
         out["horizontal_only"] = {"us_per_group": round(h_ms / hsteps * 1000.0, 3), "launches_per_group": 3}
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(args.workload, wl, args.cpu_seconds)
+        cb = cpu_baseline(args.workload, wl, args.cpu_seconds)
+        one_t = cpu_baseline(args.workload, wl, args.cpu_seconds / 2, threads=1)
+        cb["one_thread"] = {"value": one_t["value"], "unit": one_t["unit"], "cores": 1, "sample": one_t["sample"]}
+        cb["host_cpu"] = host_cpu_model()
+        cb["host_threads"] = os.cpu_count()
+        out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
 
 

@@ -294,10 +294,12 @@ optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_desc* d, int
 optimus_status optimus_grouped_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
                                               optimus_stream_t stream);
 
-/* Grouped Linear backward: two launches for the whole group -- every dX,
- * then every dW (with db) -- on the register-staged grouped GEMM, whose
- * loads transpose W, X and dY through registers into the tile layout the
- * forward uses. */
+/* Grouped Linear backward: one grouped GEMM launch for every dX, then one
+ * for every dW (with db). dX reads W as it lies when every member's widths
+ * are multiples of 8 values and its rows 16-byte aligned; otherwise one more
+ * launch first transposes W into plan-owned scratch. When the planner splits
+ * dW's reduction over the batch, the splits write fp32 partials into
+ * plan-owned scratch and one more launch sums them. */
 optimus_status optimus_grouped_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
                                                optimus_stream_t stream);
 
@@ -317,8 +319,10 @@ optimus_status optimus_grouped_layernorm_backward(const optimus_layernorm_grad_d
  * optimus_grouped_linear_backward. act_x may be the member's dx itself (in
  * place: every value is read before it is written) and must not overlap any
  * other output (OPTIMUS_ERR_ALIASING). Where the input-gradient GEMM cannot read W
- * directly (widths not multiples of 8 values, unaligned rows) the plan adds
- * one grouped activation-backward launch over dX instead. act = NONE is
+ * directly (widths not multiples of 8 values, unaligned rows) the GEMM
+ * writes dY W into plan-owned scratch ([M][K] per member) and one grouped
+ * activation-backward launch reads it with act_x and writes dx, so the
+ * in-place form holds on that path too. act = NONE is
  * optimus_grouped_linear_backward. Errors as there, plus
  * OPTIMUS_ERR_INVALID_ARG for a NULL act_x / ld_act_x or ld_act_x < K and
  * OPTIMUS_ERR_UNSUPPORTED for an unknown activation. */
@@ -363,6 +367,9 @@ optimus_status optimus_plan_layernorm(const optimus_layernorm_desc* d, int32_t G
                                       optimus_act epilogue, optimus_plan* out);
 optimus_status optimus_plan_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt,
                                       optimus_act op, optimus_plan* out);
+/* A split-op-cat plan keeps the pieces' gamma / beta device pointers and
+ * reads the values they point to on every execute (an in-place update of
+ * gamma / beta between executes is seen by the next one). */
 optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
                                          optimus_plan* out);
 /* A scaled quantize plan also owns the 4-byte amax partials of its members
@@ -384,6 +391,61 @@ optimus_status optimus_plan_quantize_fp8(const optimus_fp8_quant_desc* d, int32_
                                          int32_t use_scaling, optimus_plan* out);
 optimus_status optimus_plan_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,
                                            optimus_plan* out);
+
+/* ---------------------------------------------------------------- plan options
+ * Overrides of the planner's own choices, for tests and tuning sweeps. A
+ * zeroed struct, or a NULL pointer, leaves every choice to the planner (the
+ * plain optimus_plan_* functions). The results do not depend on these
+ * choices beyond floating-point summation order.
+ *   gemm_tile          OPTIMUS_TILE_AUTO or one tile kernel for every grouped
+ *                      GEMM of the plan (a Linear backward: dX and dW). A tile
+ *                      that some GEMM of the plan cannot run -- a dtype
+ *                      mismatch, the direct-to-LDS tiles on rows that are not
+ *                      16-byte aligned or K % 8 != 0, a fused LayerNorm wider
+ *                      than the tile, the streaming kernel for K or N > 8 --
+ *                      returns OPTIMUS_ERR_UNSUPPORTED.
+ *   wgrad_splits       Linear backward: 0 = the planner's split count of dW's
+ *                      reduction over the batch, 1..16 = that count
+ *                      (OPTIMUS_ERR_UNSUPPORTED if a split would be empty,
+ *                      INVALID_ARG outside 0..16).
+ *   soc_waves_per_row  split-op-cat: 0 = the planner's choice, 1, 2 or 4
+ *                      waves of the fused kernel per row (a row needing more
+ *                      waves for its registers takes more; INVALID_ARG for
+ *                      other values).
+ *   reserved           must be 0 (INVALID_ARG otherwise). */
+typedef enum {
+  OPTIMUS_TILE_AUTO = 0,
+  OPTIMUS_TILE_BF16_128X64 = 1,      /* register-staged, one LDS stage */
+  OPTIMUS_TILE_BF16_128X128 = 2,     /* register-staged, two LDS stages */
+  OPTIMUS_TILE_BF16_256X256 = 3,     /* register-staged, two LDS stages, 8 waves */
+  OPTIMUS_TILE_F32_64X64 = 4,
+  OPTIMUS_TILE_BF16_DMA_256X256 = 5, /* direct-to-LDS loads, 8 waves */
+  OPTIMUS_TILE_BF16_DMA_128X128 = 6, /* direct-to-LDS loads, 4 waves */
+  OPTIMUS_TILE_F32_64X128 = 7,
+  OPTIMUS_TILE_SKINNY = 8            /* every K and N <= 8: streaming, no MFMA */
+} optimus_gemm_tile;
+
+typedef struct {
+  int32_t gemm_tile;
+  int32_t wgrad_splits;
+  int32_t soc_waves_per_row;
+  int32_t reserved;
+} optimus_plan_options;
+
+optimus_status optimus_plan_linear_ex(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act epilogue,
+                                      const optimus_plan_options* opt, optimus_plan* out);
+optimus_status optimus_plan_linear_layernorm_ex(const optimus_linear_desc* d, const void* const* gamma,
+                                                const void* const* beta, int32_t G, optimus_dtype dt, float eps,
+                                                optimus_act epilogue, const optimus_plan_options* opt,
+                                                optimus_plan* out);
+optimus_status optimus_plan_linear_backward_ex(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
+                                               const optimus_plan_options* opt, optimus_plan* out);
+optimus_status optimus_plan_linear_act_backward_ex(const optimus_linear_grad_desc* d, const void* const* act_x,
+                                                   const int64_t* ld_act_x, int32_t G, optimus_dtype dt,
+                                                   optimus_act act, const optimus_plan_options* opt,
+                                                   optimus_plan* out);
+optimus_status optimus_plan_split_op_cat_ex(const optimus_split_op_cat_desc* d, optimus_dtype dt,
+                                            const optimus_plan_options* opt, optimus_plan* out);
 
 /* Execution modes of a plan.
  *   GROUPED     one launch for the whole group (the optimized program).

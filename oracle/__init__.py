@@ -110,6 +110,8 @@ class Oracle:
                                                 _dp, _dp, ctypes.c_int64, ctypes.c_int64, ctypes.c_double]
         L.oracle_num_threads.restype = ctypes.c_int
         L.oracle_num_threads.argtypes = []
+        L.oracle_set_num_threads.restype = None
+        L.oracle_set_num_threads.argtypes = [ctypes.c_int]
 
     # ------------------------------------------------------------ one operator
     def act_scalar(self, x: float, act) -> float:
@@ -257,6 +259,10 @@ class Oracle:
 
     def num_threads(self) -> int:
         return self.lib.oracle_num_threads()
+
+    def set_num_threads(self, n: int) -> None:
+        """OpenMP threads of the following calls (the CPU baseline's 1-thread run)."""
+        self.lib.oracle_set_num_threads(int(n))
 
     # ------------------------------------------------------------ groups
     # A group is a list of members; grouping changes nothing in the math

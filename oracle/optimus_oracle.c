@@ -397,6 +397,17 @@ void oracle_dequantize_fp8(const uint8_t* q, int64_t ldq, double* y, int64_t ldy
     }
 }
 
+/* Threads for the following parallel loops (n >= 1; no effect without
+ * OpenMP). Results do not depend on it: every loop writes disjoint outputs. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  extern void omp_set_num_threads(int);
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* Number of OpenMP threads the oracle's parallel loops use (1 without OpenMP). */
 int oracle_num_threads(void) {
 #ifdef _OPENMP

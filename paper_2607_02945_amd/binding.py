@@ -14,8 +14,7 @@ from typing import List, Optional, Sequence
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-# OPTIMUS_LIBRARY may name another build of the same library (tuning builds).
-LIBPATH = os.environ.get("OPTIMUS_LIBRARY") or os.path.join(_PKG, "liboptimus.so")
+LIBPATH = os.path.join(_PKG, "liboptimus.so")
 
 F32, BF16 = 0, 1
 ACTS = {"none": 0, "relu": 1, "sigmoid": 2, "tanh": 3, "silu": 4}
@@ -73,6 +72,30 @@ class Fp8DequantDesc(ctypes.Structure):
                 ("cols", c_i64)]
 
 
+class PlanOptions(ctypes.Structure):
+    """optimus_plan_options: gemm_tile (TILES key or OPTIMUS_TILE_* value; 0 = the
+    planner's), wgrad_splits (0 = the planner's), soc_waves_per_row (0 = the planner's)."""
+    _fields_ = [("gemm_tile", c_i32), ("wgrad_splits", c_i32), ("soc_waves_per_row", c_i32), ("reserved", c_i32)]
+
+
+# optimus_gemm_tile values, keyed by the kernel-table index the plan's kernel name reports
+TILES = {"auto": 0, "bf16_128x64": 1, "bf16_128x128": 2, "bf16_256x256": 3, "f32_64x64": 4, "bf16_dma_256x256": 5,
+         "bf16_dma_128x128": 6, "f32_64x128": 7, "skinny": 8}
+
+
+def plan_options(gemm_tile=0, wgrad_splits=0, soc_waves_per_row=0) -> PlanOptions:
+    t = TILES[gemm_tile] if isinstance(gemm_tile, str) else int(gemm_tile)
+    return PlanOptions(t, int(wgrad_splits), int(soc_waves_per_row), 0)
+
+
+def _opts(options):
+    if options is None:
+        return None
+    if isinstance(options, dict):
+        options = plan_options(**options)
+    return ctypes.byref(options)
+
+
 class PlanInfo(ctypes.Structure):
     _fields_ = [("kind", c_i32), ("group_size", c_i32), ("launches", c_i32), ("chain_launches", c_i32),
                 ("work_items", c_i64), ("grid", c_i32), ("block", c_i32), ("flops", ctypes.c_double),
@@ -91,6 +114,8 @@ EXPORTS = [
     "optimus_validate_act_backward",
     "optimus_plan_linear", "optimus_plan_linear_layernorm", "optimus_plan_layernorm", "optimus_plan_pointwise",
     "optimus_plan_split_op_cat", "optimus_plan_quantize_fp8", "optimus_plan_dequantize_fp8",
+    "optimus_plan_linear_ex", "optimus_plan_linear_layernorm_ex", "optimus_plan_linear_backward_ex",
+    "optimus_plan_linear_act_backward_ex", "optimus_plan_split_op_cat_ex",
     "optimus_plan_execute", "optimus_plan_execute_mode", "optimus_plan_destroy", "optimus_plan_get_info",
     "optimus_validate_linear", "optimus_validate_linear_layernorm", "optimus_validate_layernorm",
     "optimus_validate_pointwise", "optimus_validate_split_op_cat", "optimus_validate_quantize_fp8",
@@ -153,6 +178,15 @@ def lib() -> ctypes.CDLL:
             "optimus_plan_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int, P(c_vp)]),
             "optimus_validate_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32]),
             "optimus_validate_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int]),
+            "optimus_plan_linear_ex": (st, [P(LinearDesc), c_i32, ctypes.c_int, ctypes.c_int, P(PlanOptions),
+                                            P(c_vp)]),
+            "optimus_plan_linear_layernorm_ex": (st, [P(LinearDesc), P(c_vp), P(c_vp), c_i32, ctypes.c_int,
+                                                      ctypes.c_float, ctypes.c_int, P(PlanOptions), P(c_vp)]),
+            "optimus_plan_linear_backward_ex": (st, [P(LinearGradDesc), c_i32, ctypes.c_int, P(PlanOptions),
+                                                     P(c_vp)]),
+            "optimus_plan_linear_act_backward_ex": (st, [P(LinearGradDesc), P(c_vp), P(ctypes.c_int64), c_i32,
+                                                         ctypes.c_int, ctypes.c_int, P(PlanOptions), P(c_vp)]),
+            "optimus_plan_split_op_cat_ex": (st, [P(SplitOpCatDesc), ctypes.c_int, P(PlanOptions), P(c_vp)]),
             "optimus_plan_execute": (st, [c_vp, c_vp]),
             "optimus_plan_execute_mode": (st, [c_vp, ctypes.c_int, c_vp]),
             "optimus_plan_destroy": (None, [c_vp]),
@@ -466,6 +500,43 @@ def optimus_plan_linear(xs, ws, biases, ys, act="none") -> Plan:
     d = linear_descs(xs, ws, biases, ys)
     return _plan(lib().optimus_plan_linear, d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
                  keep=(list(xs), list(ws), biases, list(ys)))
+
+
+def optimus_plan_linear_ex(xs, ws, biases, ys, act="none", options=None) -> Plan:
+    """optimus_plan_linear with plan options (a PlanOptions, a dict of its fields, or None)."""
+    d = linear_descs(xs, ws, biases, ys)
+    return _plan(lib().optimus_plan_linear_ex, d, len(xs), dtype_code(xs[0]) if xs else BF16, _act(act),
+                 _opts(options), keep=(list(xs), list(ws), biases, list(ys)))
+
+
+def optimus_plan_linear_layernorm_ex(xs, ws, biases, ys, gammas=None, betas=None, eps=1e-5, act="none",
+                                     options=None) -> Plan:
+    d = linear_descs(xs, ws, biases, ys)
+    G = len(xs)
+    return _plan(lib().optimus_plan_linear_layernorm_ex, d, _ptrs(gammas, G), _ptrs(betas, G), G,
+                 dtype_code(xs[0]) if xs else BF16, float(eps), _act(act), _opts(options),
+                 keep=(list(xs), list(ws), biases, list(ys), gammas, betas))
+
+
+def optimus_plan_linear_backward_ex(xs, ws, dys, dxs=None, dws=None, dbs=None, options=None) -> Plan:
+    d = linear_grad_descs(xs, ws, dys, dxs, dws, dbs)
+    return _plan(lib().optimus_plan_linear_backward_ex, d, len(dys), dtype_code(dys[0]) if dys else BF16,
+                 _opts(options), keep=(xs, ws, list(dys), dxs, dws, dbs))
+
+
+def optimus_plan_linear_act_backward_ex(xs, ws, dys, dxs, dws, dbs, act_x, act, options=None) -> Plan:
+    d = linear_grad_descs(xs, ws, dys, dxs, dws, dbs)
+    ptrs, lds = _act_inputs(act_x, len(xs))
+    return _plan(lib().optimus_plan_linear_act_backward_ex, d, ptrs, lds, len(xs),
+                 dtype_code(xs[0]) if xs else BF16, _act(act), _opts(options),
+                 keep=(list(xs), list(ws), list(dys), dxs, dws, dbs, list(act_x)))
+
+
+def optimus_plan_split_op_cat_ex(inp, out, widths, gammas=None, betas=None, apply_layernorm=True, eps=1e-5,
+                                 act="none", options=None) -> Plan:
+    a = _SocArgs(inp, out, widths, gammas, betas, apply_layernorm, eps, act)
+    return _plan(lib().optimus_plan_split_op_cat_ex, ctypes.byref(a.desc), dtype_code(inp), _opts(options),
+                 keep=(inp, out, gammas, betas))
 
 
 def optimus_plan_linear_layernorm(xs, ws, biases, ys, gammas=None, betas=None, eps=1e-5, act="none") -> Plan:

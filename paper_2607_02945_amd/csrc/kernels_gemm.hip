@@ -16,8 +16,6 @@
 // past N and K past K_g are zero-filled on load and masked on store (the
 // in-kernel form of the pad -> matmul -> slice steps of the paper's pad_mm
 // case study, appendix Sec. 8.2, without materialising any padding).
-#include <stdlib.h>
-
 #include "device_common.h"
 
 namespace optimus {
@@ -1574,7 +1572,7 @@ bool gemm_dma_wt_ok(const optimus_linear_desc* d, int32_t G) {
 
 int gemm_ln_max_n(optimus_dtype dt) { return dt == OPTIMUS_F32 ? 128 : 256; }
 
-GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln) {
+GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln, int pin) {
   int64_t maxN = 0, maxK = 0;
   double tiles256 = 0.0;
   for (int g = 0; g < G; ++g) {
@@ -1585,7 +1583,22 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
   int v;
   const bool dma = dt == OPTIMUS_BF16 && gemm_dma_ok(d, G);
   const bool skinny = !ln && maxN <= kSkinnyMax && maxK <= kSkinnyMax;
-  if (skinny) {
+  if (pin >= 0) {
+    // a pinned tile (plan options): the direct-to-LDS variants need every
+    // member's x / w rows 16-byte aligned and K % 8 == 0, a fused LayerNorm
+    // a tile as wide as the widest row, the streaming kernel K, N <= 8
+    bool ok;
+    if (pin >= kNumVariants)
+      ok = false;
+    else if (pin == 7)
+      ok = skinny;
+    else if ((dt == OPTIMUS_F32) != (pin == 3 || pin == 6))
+      ok = false;
+    else
+      ok = (dt == OPTIMUS_F32 || pin < 4 || dma) && (!ln || kVariants[pin].bn >= maxN);
+    if (!ok) return GemmConfig{0, 0, -1, 0, 0, "unsupported"};
+    v = pin;
+  } else if (skinny) {
     v = 7;
   } else if (dt == OPTIMUS_F32) {
     v = (ln && maxN > 64) ? 6 : 3;
@@ -1598,26 +1611,6 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
   } else {
     // smaller groups need the 128x128 tile to spread over the CUs
     v = dma ? 5 : 1;
-  }
-  // OPTIMUS_GEMM_VARIANT=<n> pins the tile shape (tests and tuning); the
-  // direct-to-LDS variants need every member's x / w rows 16-byte aligned and
-  // K % 8 == 0, and a fused LayerNorm a tile as wide as the widest row.
-  // fp32: 3 and 6 (tiled) and 7 (skinny) in the same way.
-  {
-    const char* f = getenv("OPTIMUS_GEMM_VARIANT");
-    char* end = nullptr;
-    const long want = f ? strtol(f, &end, 10) : -1;
-    if (f && end && *end == 0 && want >= 0 && want < kNumVariants) {
-      const bool is_f32 = want == 3 || want == 6;
-      bool ok;
-      if (want == 7)
-        ok = skinny;
-      else if ((dt == OPTIMUS_F32) != is_f32)
-        ok = false;
-      else
-        ok = (dt == OPTIMUS_F32 || want < 4 || dma) && (!ln || kVariants[want].bn >= maxN);
-      if (ok) v = (int)want;
-    }
   }
   const GemmVariant& k = kVariants[v];
   return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
@@ -1777,8 +1770,8 @@ hipError_t gemm_launch(const GemmConfig& cfg, optimus_dtype dt, optimus_act act,
 // Backward GEMMs (transposed operands): 256x256 from half a tile per CU on,
 // else 128x128, direct-to-LDS when every member allows it, else register-
 // staged; fp32 64x64.
-GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k,
-                                  int tile) {
+GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k, int tile,
+                                  int pin) {
   double tiles256 = 0.0, area = 0.0;
   for (int g = 0; g < G; ++g) {
     tiles256 += (double)((d[g].M + 255) / 256) * (double)((d[g].N + 255) / 256);
@@ -1789,17 +1782,19 @@ GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d
   const double fill256 = area / (tiles256 * 65536.0);
   // a split reduction fills the machine with the large tile's better per-tile rate
   const bool dma = dt == OPTIMUS_BF16 && gemm_dma_trans_ok(d, G);
-  // tile = 256 or 128 asks for that bf16 tile edge; 0 chooses by the fill rule
-  const bool big = tile ? tile == 256 : fill256 >= 0.75 && (split_k || tiles256 >= 0.5 * device_cu_count());
-  int v = dt == OPTIMUS_F32 ? 3 : big ? (dma ? 4 : 2) : (dma ? 5 : 1);
-  // OPTIMUS_GEMM_VARIANT pins the tile as for the forward (1, 2 register-
-  // staged, 4, 5 direct-to-LDS where allowed; fp32 3, 6)
-  const char* f = getenv("OPTIMUS_GEMM_VARIANT");
-  char* end = nullptr;
-  const long want = f ? strtol(f, &end, 10) : -1;
-  const bool ok = dt == OPTIMUS_F32 ? (want == 3 || want == 6)
-                                    : (want == 1 || want == 2 || ((want == 4 || want == 5) && dma));
-  if (f && end && *end == 0 && ok) v = (int)want;
+  int v;
+  if (pin >= 0) {
+    // a pinned tile (plan options): 1, 2 register-staged, 4, 5 direct-to-LDS
+    // where every member allows it; fp32 3, 6
+    const bool ok = dt == OPTIMUS_F32 ? (pin == 3 || pin == 6)
+                                      : (pin == 1 || pin == 2 || ((pin == 4 || pin == 5) && dma));
+    if (!ok) return GemmConfig{0, 0, -1, 0, 0, "unsupported"};
+    v = pin;
+  } else {
+    // tile = 256 or 128 asks for that bf16 tile edge; 0 chooses by the fill rule
+    const bool big = tile ? tile == 256 : fill256 >= 0.75 && (split_k || tiles256 >= 0.5 * device_cu_count());
+    v = dt == OPTIMUS_F32 ? 3 : big ? (dma ? 4 : 2) : (dma ? 5 : 1);
+  }
   const GemmVariant& k = kVariants[v];
   return GemmConfig{k.bm, k.bn, v, k.threads, k.occ, k.name};
 }

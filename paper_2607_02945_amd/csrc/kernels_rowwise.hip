@@ -7,8 +7,6 @@
 // Grouped kernels walk a device table of (member, row range) tiles written by
 // the planner, so one launch serves members of different shapes (Sec. 3.2
 // group fusion: instances keep their own layouts and sizes).
-#include <stdlib.h>
-
 #include "device_common.h"
 
 namespace optimus {
@@ -214,8 +212,8 @@ __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const De
 // piece then turn its sum into the mean (or the centred sum of squares into
 // 1/sqrt(var + eps)) in place, and every chunk reads its piece's statistic
 // back. With one wave per row the row's LDS traffic is private to the wave and
-// needs no workgroup barrier. Piece gamma and beta are staged once per block
-// in LDS as fp32.
+// needs no workgroup barrier. Piece gamma and beta are gathered from each
+// piece's own arrays and staged once per block in LDS as fp32.
 template <typename T, int ACT, int S, int WPR, bool FULL>
 __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc* __restrict__ sp) {
   constexpr int VEC = Elem<T>::VEC;
@@ -234,19 +232,23 @@ __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc*
   float* lb = lg + (size_t)nch * VEC;
   float* part = lb + (size_t)nch * VEC + slot * (RL * S);
   float* stat = lb + (size_t)nch * VEC + SLOTS * (RL * S) + slot * 2 * npc;
+  // each chunk's gamma / beta values from its piece's own arrays (read on
+  // every launch, so the caller may update them between launches)
   for (int c = threadIdx.x; c < nch; c += kSocThreads) {
+    const SocPiece pc = s.pieces[s.chunk_piece[c]];
+    const int64_t e0 = (int64_t)(c - pc.c0) * VEC;  // first element of the chunk within the piece
     float g[VEC], b[VEC];
-    if (s.gamma) {
-      Elem<T>::unpack(ld16((const char*)s.gamma + (int64_t)c * 16), g);
+    if (pc.gamma && (pc.vec & 1)) {
+      Elem<T>::unpack(ld16((const T*)pc.gamma + e0), g);
     } else {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) g[e] = 1.f;
+      for (int e = 0; e < VEC; ++e) g[e] = pc.gamma ? Elem<T>::load1(pc.gamma, e0 + e) : 1.f;
     }
-    if (s.beta) {
-      Elem<T>::unpack(ld16((const char*)s.beta + (int64_t)c * 16), b);
+    if (pc.beta && (pc.vec & 2)) {
+      Elem<T>::unpack(ld16((const T*)pc.beta + e0), b);
     } else {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) b[e] = 0.f;
+      for (int e = 0; e < VEC; ++e) b[e] = pc.beta ? Elem<T>::load1(pc.beta, e0 + e) : 0.f;
     }
 #pragma unroll
     for (int e = 0; e < VEC; e += 4) {
@@ -466,15 +468,10 @@ struct SocShape {
   size_t smem;
 };
 
-// Waves per row: OPTIMUS_SOC_WPR=<1|2|4> pins it (tuning); otherwise 1 (no workgroup barriers).
-static int soc_wpr() {
-  const char* f = getenv("OPTIMUS_SOC_WPR");
-  if (f && (f[0] == '1' || f[0] == '2' || f[0] == '4') && f[1] == 0) return f[0] - '0';
-  return 1;
-}
-
-static SocShape soc_shape(int32_t nchunks, int32_t n_pieces, optimus_dtype dt) {
-  int wpr = soc_wpr();
+// wpr waves per row (1: no workgroup barriers), more where a row would need
+// over 8 chunks per lane in registers.
+static SocShape soc_shape(int32_t nchunks, int32_t n_pieces, optimus_dtype dt, int32_t wpr) {
+  if (wpr != 2 && wpr != 4) wpr = 1;
   // at most 8 chunks per lane in registers
   while (wpr < 4 && (nchunks + 64 * wpr - 1) / (64 * wpr) > 8) wpr *= 2;
   const int per = (nchunks + 64 * wpr - 1) / (64 * wpr);
@@ -529,8 +526,8 @@ static hipError_t soc_allow_lds(const void* k, size_t smem) {
   return hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
 }
 
-int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces) {
-  const SocShape sh = soc_shape(nchunks, n_pieces, dt);
+int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces, int32_t wpr) {
+  const SocShape sh = soc_shape(nchunks, n_pieces, dt, wpr);
   const void* k = soc_kernel(dt, act, sh);
   int n = 0;
   if (k && soc_allow_lds(k, sh.smem) != hipSuccess) return 1;
@@ -538,16 +535,14 @@ int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_
   return n;
 }
 
-int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces) {
-  return 4 / soc_shape(nchunks, n_pieces, dt).wpr;
+int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces, int32_t wpr) {
+  return 4 / soc_shape(nchunks, n_pieces, dt, wpr).wpr;
 }
 
-hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t rows, int32_t nchunks,
-                      int32_t n_pieces, int32_t n_tasks, int32_t grid, hipStream_t stream) {
-  (void)rows;
-  (void)n_tasks;
+hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t nchunks, int32_t n_pieces,
+                      int32_t wpr, int32_t grid, hipStream_t stream) {
   if (nchunks <= 0 || nchunks > kSocMaxChunks || n_pieces > kSocMaxPieces) return hipErrorInvalidValue;
-  const SocShape sh = soc_shape(nchunks, n_pieces, dt);
+  const SocShape sh = soc_shape(nchunks, n_pieces, dt, wpr);
   const void* k = soc_kernel(dt, act, sh);
   if (!k) return hipErrorInvalidValue;
   hipError_t e = soc_allow_lds(k, sh.smem);

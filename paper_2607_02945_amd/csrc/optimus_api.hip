@@ -403,10 +403,40 @@ extern "C" optimus_status optimus_validate_dequantize_fp8(const optimus_fp8_dequ
   return check_aliasing(regs, false, what);
 }
 
+// ===================================================================== plan options
+// The planner's choices a caller may pin (tests, tuning): the GEMM tile
+// variant (-1: the planner's), dW's split count (0: the planner's) and the
+// fused split-op-cat kernel's waves per row.
+struct PlanOpts {
+  int pin = -1;
+  int splits = 0;
+  int wpr = 1;
+};
+
+static optimus_status parse_options(const optimus_plan_options* o, PlanOpts& po) {
+  po = PlanOpts{};
+  if (!o) return OPTIMUS_OK;
+  if (o->reserved != 0) return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: reserved must be 0");
+  if (o->gemm_tile < OPTIMUS_TILE_AUTO || o->gemm_tile > OPTIMUS_TILE_SKINNY)
+    return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: unknown gemm_tile %d", (int)o->gemm_tile);
+  if (o->wgrad_splits < 0 || o->wgrad_splits > 16)
+    return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: wgrad_splits %d outside 0..16", (int)o->wgrad_splits);
+  const int w = o->soc_waves_per_row;
+  if (w != 0 && w != 1 && w != 2 && w != 4)
+    return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: soc_waves_per_row %d is not 0, 1, 2 or 4", w);
+  po.pin = o->gemm_tile - 1;  // OPTIMUS_TILE_* = kernel-table index + 1
+  po.splits = o->wgrad_splits;
+  po.wpr = w ? w : 1;
+  return OPTIMUS_OK;
+}
+
+static optimus_status tile_unsupported(const PlanOpts& po, const char* what) {
+  return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: gemm_tile %d cannot run every member of this group", what, po.pin + 1);
+}
+
 // ===================================================================== host plans
 // A HostPlan is everything a launch needs, built on the host: a byte blob that
-// becomes the device table, offsets into it, device-to-device copies to run
-// after the upload (packing per-piece gamma/beta), and launch parameters.
+// becomes the device table, offsets into it, and launch parameters.
 enum Kind {
   KIND_LINEAR = 0, KIND_LN = 1, KIND_PW = 2, KIND_SOC = 3, KIND_Q8 = 5, KIND_DQ8 = 6, KIND_LINBWD = 7,
   KIND_LNBWD = 8, KIND_ACTBWD = 9
@@ -420,12 +450,6 @@ struct Blob {
     if (p && n) memcpy(bytes.data() + off, p, n);
     return off;
   }
-};
-
-struct D2DCopy {
-  size_t dst_off;
-  const void* src;
-  size_t bytes;
 };
 
 // One kernel launch over a row-wise table (grouped or one member of a chain).
@@ -453,7 +477,6 @@ struct HostPlan {
   optimus_act act;
   int32_t G = 0;
   Blob blob;
-  std::vector<D2DCopy> copies;
   // GEMM
   GemmSet gs[2];       // forward: gs[0]; backward: dX in gs[0], dW (+ db) in gs[1]
   int n_gs = 0;
@@ -466,7 +489,7 @@ struct HostPlan {
   // fused split-op-cat
   bool soc_fused = false;
   size_t soc_off = 0;
-  int32_t soc_rows = 0, soc_nchunks = 0, soc_pieces = 0, soc_tasks = 0, soc_grid = 0;
+  int32_t soc_rows = 0, soc_nchunks = 0, soc_pieces = 0, soc_tasks = 0, soc_grid = 0, soc_wpr = 1;
   // split-op-cat unfused programs (CHAIN / HORIZONTAL) over plan-owned temporaries
   bool soc_has_unfused = false;
   bool soc_apply_ln = false;
@@ -629,6 +652,11 @@ static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool l
 // member-major, M-blocks then N-blocks, padded to a multiple of 8; the
 // persistent grid is no larger than what is resident at once (a workgroup
 // that had to wait for a free slot would start its whole share late).
+// Forward members that read one input (the same x, ldx, M and K: Table 1's
+// batch_linear_lhs) are walked M-block by M-block across all of them, so the
+// tiles that read one x panel sit side by side in the list (the kernel deals
+// contiguous slices of it to each L2); the per-member CHAIN launches then
+// read a member-major copy of the list.
 static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int tr, const std::vector<DevLinear>& descs,
                            const std::vector<int>& ids, int group_size, optimus_act act, bool ln, int splits = 1) {
   const int n = (int)descs.size();
@@ -638,40 +666,61 @@ static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int
   std::vector<int> order(n);
   for (int i = 0; i < n; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return descs[a].K > descs[b].K; });
-  std::vector<GemmTile> tiles;
-  gs.chain.assign(group_size, RowLaunch{});
   const int bm = cfg.bm, bn = cfg.bn;
-  for (int i : order) {
-    const int first = (int)tiles.size();
-    const int64_t mbs = (descs[i].M + bm - 1) / bm, nbs = (descs[i].N + bn - 1) / bn;
+  auto member_tiles = [&](std::vector<GemmTile>& tl, int i, int64_t mb) {
+    const int64_t nbs = (descs[i].N + bn - 1) / bn;
     // split index fastest: measured on the weight gradient, this beats the
     // split-major order (all tiles of one reduction range side by side on
     // one L2) by 3.5 % despite 16 % more HBM reads
-    for (int64_t mb = 0; mb < mbs; ++mb)
-      for (int64_t nb = 0; nb < nbs; ++nb)
-        for (int ks = 0; ks < splits; ++ks) tiles.push_back(GemmTile{i, (int32_t)mb, (int32_t)nb, ks});
+    for (int64_t nb = 0; nb < nbs; ++nb)
+      for (int ks = 0; ks < splits; ++ks) tl.push_back(GemmTile{i, (int32_t)mb, (int32_t)nb, ks});
+  };
+  // member-major list (and the CHAIN ranges)
+  std::vector<GemmTile> chain_tiles;
+  gs.chain.assign(group_size, RowLaunch{});
+  for (int i : order) {
+    const int first = (int)chain_tiles.size();
+    for (int64_t mb = 0; mb < (descs[i].M + bm - 1) / bm; ++mb) member_tiles(chain_tiles, i, mb);
     gs.chain[ids[i]].first_tile = first;
-    gs.chain[ids[i]].num_tiles = (int)tiles.size() - first;
+    gs.chain[ids[i]].num_tiles = (int)chain_tiles.size() - first;
+  }
+  // grouped list: runs of consecutive members (in `order`) sharing x walk
+  // their M-blocks together
+  std::vector<GemmTile> tiles;
+  bool shared = false;
+  for (int a = 0; a < n;) {
+    int b = a + 1;
+    const DevLinear& da = descs[order[a]];
+    while (tr == 0 && b < n) {
+      const DevLinear& db = descs[order[b]];
+      if (db.x != da.x || db.ldx != da.ldx || db.M != da.M || db.K != da.K) break;
+      ++b;
+    }
+    shared = shared || b - a > 1;
+    for (int64_t mb = 0; mb < (da.M + bm - 1) / bm; ++mb)
+      for (int r = a; r < b; ++r) member_tiles(tiles, order[r], mb);
+    a = b;
   }
   gs.real_tiles = (int64_t)tiles.size();
   while (tiles.size() % 8) tiles.push_back(GemmTile{-1, 0, 0, 0});
   gs.descs_off = hp.blob.add(descs.data(), descs.size() * sizeof(DevLinear));
   gs.tiles_off = hp.blob.add(tiles.data(), tiles.size() * sizeof(GemmTile));
   gs.num_tiles = (int32_t)tiles.size();
+  const size_t chain_off = shared ? hp.blob.add(chain_tiles.data(), chain_tiles.size() * sizeof(GemmTile)) : gs.tiles_off;
   const int64_t cap = (int64_t)device_cu_count() * gemm_resident_per_cu(cfg, hp.dt, act, ln, tr);
   int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
   if (grid >= 8) grid -= grid % 8;
   gs.grid = (int32_t)std::max<int64_t>(1, grid);
   for (auto& c : gs.chain) {
     c.descs_off = gs.descs_off;
-    c.tiles_off = gs.tiles_off;
+    c.tiles_off = chain_off;
     c.grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>(c.num_tiles, cap));
   }
 }
 
 static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
                                    HostPlan& hp, bool ln = false, const void* const* gamma = nullptr,
-                                   const void* const* beta = nullptr, float eps = 0.f) {
+                                   const void* const* beta = nullptr, float eps = 0.f, const PlanOpts& po = PlanOpts{}) {
   optimus_status st = validate_linear_impl(d, G, dt, act, ln, gamma, beta, eps);
   if (st != OPTIMUS_OK) return st;
   hp.kind = KIND_LINEAR; hp.dt = dt; hp.act = act; hp.G = G; hp.g_ln = ln;
@@ -692,12 +741,19 @@ static optimus_status build_linear(const optimus_linear_desc* d, int32_t G, opti
     o.eps = eps;
     o.inv_n = 1.0f / (float)m.N;
     hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
-    hp.bytes += (double)s * ((double)m.M * m.K + (double)m.N * m.K + (m.bias ? (double)m.N : 0.0) + (double)m.M * m.N);
+    // an input shared with an earlier member is read once
+    bool seen = false;
+    for (int e = 0; e < g && !seen; ++e)
+      seen = d[e].x == m.x && d[e].ldx == m.ldx && d[e].M == m.M && d[e].K == m.K;
+    hp.bytes += (double)s * ((seen ? 0.0 : (double)m.M * m.K) + (double)m.N * m.K + (m.bias ? (double)m.N : 0.0) +
+                             (double)m.M * m.N);
     if (ln) hp.bytes += (double)s * ((o.gamma ? (double)m.N : 0.0) + (o.beta ? (double)m.N : 0.0));
   }
   std::vector<int> ids(G);
   for (int g = 0; g < G; ++g) ids[g] = g;
-  build_gemm_set(hp, hp.gs[0], gemm_pick_config(dt, d, G, ln), 0, descs, ids, G, act, ln);
+  const GemmConfig cfg = gemm_pick_config(dt, d, G, ln, G > 0 ? po.pin : -1);
+  if (cfg.variant < 0) return tile_unsupported(po, ln ? "plan_linear_layernorm" : "plan_linear");
+  build_gemm_set(hp, hp.gs[0], cfg, 0, descs, ids, G, act, ln);
   hp.n_gs = 1;
   hp.work_items = hp.gs[0].real_tiles;
   hp.grid = hp.gs[0].grid;
@@ -724,7 +780,8 @@ static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRo
 // applied, dX * act'(act_x[g]) (act_x [M][K], row stride ld_act_x[g]).
 static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
                                             HostPlan& hp, optimus_act act = OPTIMUS_ACT_NONE,
-                                            const void* const* act_x = nullptr, const int64_t* ld_act_x = nullptr) {
+                                            const void* const* act_x = nullptr, const int64_t* ld_act_x = nullptr,
+                                            const PlanOpts& po = PlanOpts{}) {
   optimus_status st = optimus_validate_linear_backward(d, G, dt);
   if (st != OPTIMUS_OK) return st;
   const char* what = "grouped_linear_act_backward";
@@ -773,10 +830,14 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
         sh.push_back(e);
       }
     if (!sh.empty() && gemm_dma_wt_ok(sh.data(), (int32_t)sh.size())) {
-      dx_cfg = gemm_pick_config(dt, sh.data(), (int32_t)sh.size(), false);
+      dx_cfg = gemm_pick_config(dt, sh.data(), (int32_t)sh.size(), false, po.pin);
       direct = dx_cfg.variant == 4 || dx_cfg.variant == 5;
     }
   }
+  // without the direct tiles and with an activation backward, dY W goes to
+  // plan scratch (offset, row stride per member) and the activation backward
+  // reads it beside act_x and writes dx: act_x may then be dx itself
+  std::vector<int64_t> g_off(G, -1), g_ld(G, 0);
   for (int g = 0; g < G; ++g) {
     const optimus_linear_grad_desc& m = d[g];
     if (m.dx && direct) {
@@ -806,8 +867,15 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       hp.scratch_bytes = off + (size_t)(m.K * ldt) * s;
       o.x = m.dy; o.ldx = m.lddy; o.w = (const void*)(uintptr_t)off; o.ldw = ldt; o.y = m.dx; o.ldy = m.lddx;
       o.M = (int32_t)m.M; o.N = (int32_t)m.K; o.K = (int32_t)m.N;
+      if (act != OPTIMUS_ACT_NONE) {
+        g_ld[g] = (m.K + VEC - 1) / VEC * VEC;
+        g_off[g] = (int64_t)((hp.scratch_bytes + 255) & ~(size_t)255);
+        hp.scratch_bytes = (size_t)g_off[g] + (size_t)(m.M * g_ld[g]) * s;
+        o.y = (void*)(uintptr_t)g_off[g];
+        o.ldy = g_ld[g];
+      }
       const bool vin = m.N % VEC == 0 && m.lddy % VEC == 0 && aligned16(m.dy);
-      const bool vout = m.lddx % VEC == 0 && aligned16(m.dx);
+      const bool vout = o.ldy % VEC == 0 && aligned16(o.y);
       o.vec = (vin ? 1 : 0) | (vout ? 2 : 0);
       for (int64_t r0 = 0; r0 < m.N; r0 += 64)
         for (int64_t c0 = 0; c0 < m.K; c0 += 64)
@@ -822,7 +890,8 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       sh.x = m.dy; sh.ldx = m.lddy; sh.w = (const void*)(uintptr_t)256; sh.ldw = ldt;  // W^T: 256-byte aligned
       dx_shape.push_back(sh);
       hp.flops += 2.0 * (double)m.M * (double)m.N * (double)m.K;
-      // dY, W and dX; the separate activation backward reads a and dX and writes dX
+      // dY, W and dX; with an activation backward the GEMM writes dY W to
+      // scratch and the activation backward reads it and a, and writes dX
       hp.bytes += (double)s * ((double)m.M * m.N + (double)m.N * m.K + (double)m.M * m.K *
                                (act != OPTIMUS_ACT_NONE ? 4.0 : 1.0));
     }
@@ -868,24 +937,31 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       hp.tp_chain[dx_ids[i]] = RowLaunch{toff, toff, prev, tp_end[i] - prev, std::max(1, std::min(tp_end[i] - prev, cap))};
       prev = tp_end[i];
     }
+    const GemmConfig fcfg = gemm_pick_config(dt, dx_shape.data(), (int32_t)dx_shape.size(), false, po.pin);
+    if (fcfg.variant < 0) return tile_unsupported(po, "plan_linear_backward (dX)");
     GemmSet& gs = hp.gs[hp.n_gs++];
-    build_gemm_set(hp, gs, gemm_pick_config(dt, dx_shape.data(), (int32_t)dx_shape.size(), false), 0, dxs, dx_ids, G,
-                   OPTIMUS_ACT_NONE, false);
-    for (size_t i = 0; i < dxs.size(); ++i)
+    build_gemm_set(hp, gs, fcfg, 0, dxs, dx_ids, G, OPTIMUS_ACT_NONE, false);
+    for (size_t i = 0; i < dxs.size(); ++i) {
       hp.scratch_fixups.push_back(gs.descs_off + i * sizeof(DevLinear) + offsetof(DevLinear, w));
+      if (g_off[dx_ids[i]] >= 0) hp.scratch_fixups.push_back(gs.descs_off + i * sizeof(DevLinear) + offsetof(DevLinear, y));
+    }
     name = std::string(gs.cfg.name) + "_dgrad" + act_names[(int)act];
     if (act != OPTIMUS_ACT_NONE) {
       // no fused epilogue on these tiles: one grouped activation-backward
-      // launch over dX in place, x = act_x (members without dX get no rows)
+      // launch, x = act_x, dy = dY W in scratch, dx (members without dX get
+      // no rows)
       std::vector<DevRowsGrad> rm;
       for (int g = 0; g < G; ++g) {
         const bool has = d[g].dx != nullptr;
-        rm.push_back(make_rows_grad(has ? act_x[g] : nullptr, has ? ld_act_x[g] : 1, d[g].dx, d[g].lddx, d[g].dx,
+        rm.push_back(make_rows_grad(has ? act_x[g] : nullptr, has ? ld_act_x[g] : 1,
+                                    has ? (const void*)(uintptr_t)g_off[g] : nullptr, has ? g_ld[g] : 1, d[g].dx,
                                     d[g].lddx, nullptr, has ? d[g].M : 0, d[g].K, 0.f, dt, false));
       }
       std::vector<int> nt;
       std::vector<RowTile> rt = grad_row_tiles(hp, rm, s, nt);
       const size_t roff = hp.blob.add(rm.data(), rm.size() * sizeof(DevRowsGrad));
+      for (int g = 0; g < G; ++g)
+        if (d[g].dx) hp.scratch_fixups.push_back(roff + g * sizeof(DevRowsGrad) + offsetof(DevRowsGrad, dy));
       const size_t rtoff = hp.blob.add(rt.data(), rt.size() * sizeof(RowTile));
       for (auto& c : hp.rows_chain) {
         c.descs_off = roff;
@@ -939,11 +1015,12 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       return makespan + (sp > 1 ? out_elems * (4.0 * sp + (double)s) / 4.7e12 + 6e-6 : 0.0);
     };
     const int n_dw = (int32_t)dw_shape.size();
-    GemmConfig cfg = gemm_pick_config_trans(dt, dw_shape.data(), n_dw, true);
+    GemmConfig cfg = gemm_pick_config_trans(dt, dw_shape.data(), n_dw, true, 0, po.pin);
+    if (cfg.variant < 0) return tile_unsupported(po, "plan_linear_backward (dW)");
     int splits = 1;
     {
       std::vector<GemmConfig> cands{cfg};
-      if (dt == OPTIMUS_BF16 && !getenv("OPTIMUS_GEMM_VARIANT"))
+      if (dt == OPTIMUS_BF16 && po.pin < 0)
         for (int edge : {256, 128}) {
           const GemmConfig c = gemm_pick_config_trans(dt, dw_shape.data(), n_dw, true, edge);
           if (c.variant != cfg.variant) cands.push_back(c);
@@ -967,12 +1044,11 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
       }
     }
     const int bk = cfg.variant == 3 ? 32 : 64;  // every split but the last a whole number of K steps
-    // OPTIMUS_WGRAD_SPLITS=<n> (1..16) pins the split count (tests and
-    // tuning) where no split comes out empty
-    if (const char* f = getenv("OPTIMUS_WGRAD_SPLITS")) {
-      char* end = nullptr;
-      const long want = strtol(f, &end, 10);
-      if (end && *end == 0 && want >= 1 && want <= 16 && est_of(cfg, (int)want) >= 0.0) splits = (int)want;
+    // a pinned split count (plan options), where no split comes out empty
+    if (po.splits > 0) {
+      if (est_of(cfg, po.splits) < 0.0)
+        return fail(OPTIMUS_ERR_UNSUPPORTED, "plan_linear_backward: wgrad_splits %d leaves a split empty", po.splits);
+      splits = po.splits;
     }
     if (splits > 1) {
       std::vector<SplitReduceItem> red;
@@ -1242,7 +1318,8 @@ static optimus_status build_pointwise(const optimus_pointwise_desc* d, int32_t G
   return OPTIMUS_OK;
 }
 
-static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt, HostPlan& hp) {
+static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt, HostPlan& hp,
+                                         int32_t wpr = 1) {
   optimus_status st = optimus_validate_split_op_cat(d, dt);
   if (st != OPTIMUS_OK) return st;
   hp.kind = KIND_SOC; hp.dt = dt; hp.act = d->act; hp.G = d->n_slices;
@@ -1282,7 +1359,7 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
     std::vector<SocTask> tasks;
     for (int j = 0; j < n; ++j) {
       const int c0 = (int)(off[j] / VEC), c1 = (int)(off[j + 1] / VEC);
-      pieces[j] = SocPiece{c0, c1, (float)(1.0 / (double)d->widths[j]), 0};
+      pieces[j] = SocPiece{c0, c1, (float)(1.0 / (double)d->widths[j]), 0, nullptr, nullptr};
       for (int c = c0; c < c1; ++c) cp[c] = (uint8_t)j;
       for (int c = c0; c < c1; c += run)
         tasks.push_back(SocTask{(int16_t)c, (int16_t)std::min(c1, c + run), (int16_t)j, 0});
@@ -1293,28 +1370,17 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
     soc.rows = (int32_t)rows; soc.D = (int32_t)D; soc.nchunks = (int32_t)nchunks;
     soc.n_pieces = n; soc.n_tasks = (int32_t)tasks.size();
     soc.apply_ln = 1; soc.eps = d->eps;
-    const size_t gam_off = hp.blob.add(nullptr, (size_t)D * s);
-    const size_t bet_off = hp.blob.add(nullptr, (size_t)D * s);
-    // identity affine where a piece has none: packed arrays start as 1 / 0
-    {
-      std::vector<char> ones((size_t)D * s), zeros((size_t)D * s, 0);
-      for (int64_t i = 0; i < D; ++i) {
-        if (dt == OPTIMUS_F32) { float one = 1.f; memcpy(&ones[i * 4], &one, 4); }
-        else { uint16_t one = 0x3f80; memcpy(&ones[i * 2], &one, 2); }
-      }
-      memcpy(hp.blob.bytes.data() + gam_off, ones.data(), ones.size());
-      memcpy(hp.blob.bytes.data() + bet_off, zeros.data(), zeros.size());
-    }
+    // the pieces keep the caller's gamma / beta pointers (read by every launch)
     for (int j = 0; j < n; ++j) {
-      if (d->gamma && d->gamma[j]) hp.copies.push_back(D2DCopy{gam_off + (size_t)off[j] * s, d->gamma[j], (size_t)d->widths[j] * s});
-      if (d->beta && d->beta[j]) hp.copies.push_back(D2DCopy{bet_off + (size_t)off[j] * s, d->beta[j], (size_t)d->widths[j] * s});
+      pieces[j].gamma = d->gamma ? d->gamma[j] : nullptr;
+      pieces[j].beta = d->beta ? d->beta[j] : nullptr;
+      pieces[j].vec = (pieces[j].gamma && aligned16(pieces[j].gamma) ? 1 : 0) |
+                      (pieces[j].beta && aligned16(pieces[j].beta) ? 2 : 0);
     }
     const size_t cp_off = hp.blob.add(cp.data(), cp.size());
     const size_t pc_off = hp.blob.add(pieces.data(), pieces.size() * sizeof(SocPiece));
     const size_t tk_off = hp.blob.add(tasks.data(), tasks.size() * sizeof(SocTask));
     // device pointers inside DevSoc are filled in at upload (relative offsets kept here)
-    soc.gamma = (const void*)(uintptr_t)gam_off;
-    soc.beta = (const void*)(uintptr_t)bet_off;
     soc.chunk_piece = (const uint8_t*)(uintptr_t)cp_off;
     soc.pieces = (const SocPiece*)(uintptr_t)pc_off;
     soc.tasks = (const SocTask*)(uintptr_t)tk_off;
@@ -1325,8 +1391,9 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
     hp.soc_pieces = n;
     hp.soc_tasks = (int32_t)tasks.size();
     // persistent grid: exactly the workgroups that fit at once, each wave walking rows
-    const int64_t resident = (int64_t)device_cu_count() * soc_blocks_per_cu(dt, d->act, (int32_t)nchunks, n);
-    const int rpb = soc_rows_per_block(dt, (int32_t)nchunks, n);
+    hp.soc_wpr = wpr;
+    const int64_t resident = (int64_t)device_cu_count() * soc_blocks_per_cu(dt, d->act, (int32_t)nchunks, n, wpr);
+    const int rpb = soc_rows_per_block(dt, (int32_t)nchunks, n, wpr);
     hp.soc_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((rows + rpb - 1) / rpb, resident));
     hp.work_items = rows;
     hp.grid = hp.soc_grid;
@@ -1569,8 +1636,6 @@ struct optimus_plan_s {
 static void rebase_soc(HostPlan& hp, char* table) {
   if (!hp.soc_fused) return;
   DevSoc* s = (DevSoc*)(hp.blob.bytes.data() + hp.soc_off);
-  s->gamma = table + (uintptr_t)s->gamma;
-  s->beta = table + (uintptr_t)s->beta;
   s->chunk_piece = (const uint8_t*)(table + (uintptr_t)s->chunk_piece);
   s->pieces = (const SocPiece*)(table + (uintptr_t)s->pieces);
   s->tasks = (const SocTask*)(table + (uintptr_t)s->tasks);
@@ -1654,8 +1719,8 @@ static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t st
     case KIND_PW:
     case KIND_SOC:
       if (hp.kind == KIND_SOC && hp.soc_fused)
-        return soc_launch(hp.dt, hp.act, at<DevSoc>(table, hp.soc_off), hp.soc_rows, hp.soc_nchunks, hp.soc_pieces,
-                          hp.soc_tasks, hp.soc_grid, stream);
+        return soc_launch(hp.dt, hp.act, at<DevSoc>(table, hp.soc_off), hp.soc_nchunks, hp.soc_pieces, hp.soc_wpr,
+                          hp.soc_grid, stream);
       if (hp.row_kernel == KIND_LN)
         return layernorm_launch(hp.dt, hp.row_act, at<DevRows>(table, hp.rows.descs_off),
                                 at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles, hp.rows.grid, stream);
@@ -1663,15 +1728,6 @@ static hipError_t launch_grouped(const HostPlan& hp, char* table, hipStream_t st
                               at<RowTile>(table, hp.rows.tiles_off), hp.rows.num_tiles, hp.rows.grid, stream);
   }
   return hipErrorInvalidValue;
-}
-
-static optimus_status upload_copies(const HostPlan& hp, char* table, hipStream_t stream, bool async) {
-  for (const D2DCopy& c : hp.copies) {
-    hipError_t e = async ? hipMemcpyAsync(table + c.dst_off, c.src, c.bytes, hipMemcpyDeviceToDevice, stream)
-                         : hipMemcpy(table + c.dst_off, c.src, c.bytes, hipMemcpyDeviceToDevice);
-    if (e != hipSuccess) return hip_fail(e, "packing per-piece gamma/beta");
-  }
-  return OPTIMUS_OK;
 }
 
 static optimus_status make_plan(HostPlan&& hp, optimus_plan* out) {
@@ -1698,16 +1754,9 @@ static optimus_status make_plan(HostPlan&& hp, optimus_plan* out) {
   rebase_soc(p->hp, p->table);
   rebase_fixups(p->hp, p->table, p->scratch);
   e = hipMemcpy(p->table, p->hp.blob.bytes.data(), p->hp.blob.bytes.size(), hipMemcpyHostToDevice);
-  if (e == hipSuccess) {
-    optimus_status st = upload_copies(p->hp, p->table, nullptr, false);
-    if (st != OPTIMUS_OK) {
-      (void)hipFree(p->table);
-      delete p;
-      return st;
-    }
-  }
   if (e != hipSuccess) {
     (void)hipFree(p->table);
+    if (p->scratch) (void)hipFree(p->scratch);
     delete p;
     return hip_fail(e, "plan: device table upload");
   }
@@ -1715,20 +1764,37 @@ static optimus_status make_plan(HostPlan&& hp, optimus_plan* out) {
   return OPTIMUS_OK;
 }
 
+extern "C" optimus_status optimus_plan_linear_ex(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
+                                                 optimus_act epilogue, const optimus_plan_options* opt,
+                                                 optimus_plan* out) {
+  PlanOpts po;
+  optimus_status st = parse_options(opt, po);
+  if (st != OPTIMUS_OK) return st;
+  HostPlan hp;
+  st = build_linear(d, G, dt, epilogue, hp, false, nullptr, nullptr, 0.f, po);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
 extern "C" optimus_status optimus_plan_linear(const optimus_linear_desc* d, int32_t G, optimus_dtype dt,
                                               optimus_act epilogue, optimus_plan* out) {
+  return optimus_plan_linear_ex(d, G, dt, epilogue, nullptr, out);
+}
+extern "C" optimus_status optimus_plan_linear_layernorm_ex(const optimus_linear_desc* d, const void* const* gamma,
+                                                           const void* const* beta, int32_t G, optimus_dtype dt,
+                                                           float eps, optimus_act epilogue,
+                                                           const optimus_plan_options* opt, optimus_plan* out) {
+  PlanOpts po;
+  optimus_status st = parse_options(opt, po);
+  if (st != OPTIMUS_OK) return st;
   HostPlan hp;
-  optimus_status st = build_linear(d, G, dt, epilogue, hp);
+  st = build_linear(d, G, dt, epilogue, hp, true, gamma, beta, eps, po);
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
 extern "C" optimus_status optimus_plan_linear_layernorm(const optimus_linear_desc* d, const void* const* gamma,
                                                         const void* const* beta, int32_t G, optimus_dtype dt,
                                                         float eps, optimus_act epilogue, optimus_plan* out) {
-  HostPlan hp;
-  optimus_status st = build_linear(d, G, dt, epilogue, hp, true, gamma, beta, eps);
-  if (st != OPTIMUS_OK) return st;
-  return make_plan(std::move(hp), out);
+  return optimus_plan_linear_layernorm_ex(d, gamma, beta, G, dt, eps, epilogue, nullptr, out);
 }
 extern "C" optimus_status optimus_plan_layernorm(const optimus_layernorm_desc* d, int32_t G, optimus_dtype dt,
                                                  optimus_act epilogue, optimus_plan* out) {
@@ -1744,19 +1810,34 @@ extern "C" optimus_status optimus_plan_pointwise(const optimus_pointwise_desc* d
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
+extern "C" optimus_status optimus_plan_split_op_cat_ex(const optimus_split_op_cat_desc* d, optimus_dtype dt,
+                                                       const optimus_plan_options* opt, optimus_plan* out) {
+  PlanOpts po;
+  optimus_status st = parse_options(opt, po);
+  if (st != OPTIMUS_OK) return st;
+  HostPlan hp;
+  st = build_split_op_cat(d, dt, hp, po.wpr);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
 extern "C" optimus_status optimus_plan_split_op_cat(const optimus_split_op_cat_desc* d, optimus_dtype dt,
                                                     optimus_plan* out) {
+  return optimus_plan_split_op_cat_ex(d, dt, nullptr, out);
+}
+extern "C" optimus_status optimus_plan_linear_backward_ex(const optimus_linear_grad_desc* d, int32_t G,
+                                                          optimus_dtype dt, const optimus_plan_options* opt,
+                                                          optimus_plan* out) {
+  PlanOpts po;
+  optimus_status st = parse_options(opt, po);
+  if (st != OPTIMUS_OK) return st;
   HostPlan hp;
-  optimus_status st = build_split_op_cat(d, dt, hp);
+  st = build_linear_backward(d, G, dt, hp, OPTIMUS_ACT_NONE, nullptr, nullptr, po);
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
 extern "C" optimus_status optimus_plan_linear_backward(const optimus_linear_grad_desc* d, int32_t G, optimus_dtype dt,
                                                        optimus_plan* out) {
-  HostPlan hp;
-  optimus_status st = build_linear_backward(d, G, dt, hp);
-  if (st != OPTIMUS_OK) return st;
-  return make_plan(std::move(hp), out);
+  return optimus_plan_linear_backward_ex(d, G, dt, nullptr, out);
 }
 extern "C" optimus_status optimus_plan_layernorm_backward(const optimus_layernorm_grad_desc* d, int32_t G,
                                                           optimus_dtype dt, optimus_plan* out) {
@@ -1765,13 +1846,22 @@ extern "C" optimus_status optimus_plan_layernorm_backward(const optimus_layernor
   if (st != OPTIMUS_OK) return st;
   return make_plan(std::move(hp), out);
 }
+extern "C" optimus_status optimus_plan_linear_act_backward_ex(const optimus_linear_grad_desc* d,
+                                                              const void* const* act_x, const int64_t* ld_act_x,
+                                                              int32_t G, optimus_dtype dt, optimus_act act,
+                                                              const optimus_plan_options* opt, optimus_plan* out) {
+  PlanOpts po;
+  optimus_status st = parse_options(opt, po);
+  if (st != OPTIMUS_OK) return st;
+  HostPlan hp;
+  st = build_linear_backward(d, G, dt, hp, act, act_x, ld_act_x, po);
+  if (st != OPTIMUS_OK) return st;
+  return make_plan(std::move(hp), out);
+}
 extern "C" optimus_status optimus_plan_linear_act_backward(const optimus_linear_grad_desc* d, const void* const* act_x,
                                                            const int64_t* ld_act_x, int32_t G, optimus_dtype dt,
                                                            optimus_act act, optimus_plan* out) {
-  HostPlan hp;
-  optimus_status st = build_linear_backward(d, G, dt, hp, act, act_x, ld_act_x);
-  if (st != OPTIMUS_OK) return st;
-  return make_plan(std::move(hp), out);
+  return optimus_plan_linear_act_backward_ex(d, act_x, ld_act_x, G, dt, act, nullptr, out);
 }
 extern "C" optimus_status optimus_plan_layernorm_act_backward(const optimus_layernorm_grad_desc* d,
                                                               const void* const* beta, int32_t G, optimus_dtype dt,
@@ -1869,7 +1959,7 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
           const RowLaunch& c = gs.chain[g];
           if (c.num_tiles > 0)
             e = gemm_launch(gs.cfg, hp.dt, gs.act, hp.g_ln, at<DevLinear>(p->table, gs.descs_off),
-                            at<GemmTile>(p->table, gs.tiles_off) + c.first_tile, c.num_tiles, c.grid, st, gs.tr);
+                            at<GemmTile>(p->table, c.tiles_off) + c.first_tile, c.num_tiles, c.grid, st, gs.tr);
         }
         if (e == hipSuccess && hp.kind == KIND_LINBWD && hp.rows.num_tiles > 0 && hp.rows_chain[g].num_tiles > 0) {
           const RowLaunch& c = hp.rows_chain[g];
@@ -1968,10 +2058,10 @@ static optimus_status run_oneshot(HostPlan& hp, hipStream_t stream) {
   if (!tl_stage) tl_stage = new Staging();
   Staging& sg = *tl_stage;
   const size_t n = std::max<size_t>(hp.blob.bytes.size(), 256);
-  char* table = nullptr;
-  HIP_TRY(hipMallocAsync((void**)&table, n, stream), "one-shot: device table");
+  // host-side steps first: nothing on the device exists yet if one fails
   if (!sg.ev) HIP_TRY(hipEventCreateWithFlags(&sg.ev, hipEventDisableTiming), "one-shot: event");
   if (sg.pending) HIP_TRY(hipEventSynchronize(sg.ev), "one-shot: staging reuse");
+  sg.pending = false;
   if (sg.cap < n) {
     if (sg.host) (void)hipHostFree(sg.host);
     sg.host = nullptr;
@@ -1979,19 +2069,38 @@ static optimus_status run_oneshot(HostPlan& hp, hipStream_t stream) {
     HIP_TRY(hipHostMalloc(&sg.host, n, hipHostMallocDefault), "one-shot: pinned staging");
     sg.cap = n;
   }
+  // then the stream-ordered device memory, released in stream order on every path
+  char* table = nullptr;
   char* scratch = nullptr;
-  if (hp.scratch_bytes) HIP_TRY(hipMallocAsync((void**)&scratch, hp.scratch_bytes, stream), "one-shot: scratch");
+  auto release = [&]() {
+    if (table) (void)hipFreeAsync(table, stream);
+    if (scratch) (void)hipFreeAsync(scratch, stream);
+  };
+  hipError_t e = hipMallocAsync((void**)&table, n, stream);
+  if (e != hipSuccess) return hip_fail(e, "one-shot: device table");
+  if (hp.scratch_bytes) {
+    e = hipMallocAsync((void**)&scratch, hp.scratch_bytes, stream);
+    if (e != hipSuccess) {
+      scratch = nullptr;
+      release();
+      return hip_fail(e, "one-shot: scratch");
+    }
+  }
   rebase_soc(hp, table);
   rebase_fixups(hp, table, scratch);
   memcpy(sg.host, hp.blob.bytes.data(), hp.blob.bytes.size());
-  HIP_TRY(hipMemcpyAsync(table, sg.host, hp.blob.bytes.size(), hipMemcpyHostToDevice, stream), "one-shot: upload");
-  HIP_TRY(hipEventRecord(sg.ev, stream), "one-shot: event record");
-  sg.pending = true;
-  optimus_status st = upload_copies(hp, table, stream, true);
-  if (st != OPTIMUS_OK) return st;
-  hipError_t e = launch_grouped(hp, table, stream);
-  (void)hipFreeAsync(table, stream);
-  if (scratch) (void)hipFreeAsync(scratch, stream);
+  e = hipMemcpyAsync(table, sg.host, hp.blob.bytes.size(), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) {
+    e = hipEventRecord(sg.ev, stream);
+    // the staging buffer may be in use until the event has passed
+    sg.pending = true;
+  }
+  if (e != hipSuccess) {
+    release();
+    return hip_fail(e, "one-shot: upload");
+  }
+  e = launch_grouped(hp, table, stream);
+  release();
   return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "one-shot: launch");
 }
 

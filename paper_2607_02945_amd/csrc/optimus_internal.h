@@ -91,11 +91,14 @@ struct RowTile {
 };
 
 // Fused split-op-cat: per 16-byte chunk of a row, the piece it belongs to;
-// per reduction task, a run of chunks of one piece.
+// per reduction task, a run of chunks of one piece. Each piece keeps the
+// caller's gamma / beta pointers, which the kernel reads on every launch.
 struct SocPiece {
   int32_t c0, c1;      // chunk range [c0, c1) of the piece
   float inv_width;
-  int32_t pad;
+  int32_t vec;         // bit 0: gamma rows 16-B loadable; bit 1: beta
+  const void* gamma;   // [width] of the group's dtype, or null (1)
+  const void* beta;    // [width], or null (0)
 };
 
 struct SocTask {
@@ -106,8 +109,6 @@ struct SocTask {
 struct DevSoc {
   const void* in;
   void* out;
-  const void* gamma;   // [D] packed per-piece gamma (device, plan-owned), or null
-  const void* beta;    // [D] packed per-piece beta, or null
   const uint8_t* chunk_piece;   // [nchunks]
   const SocPiece* pieces;       // [n_pieces]
   const SocTask* tasks;         // [n_tasks]
@@ -131,7 +132,9 @@ struct GemmConfig {
 
 // ln: the group's LayerNorm is fused into the epilogue, so one tile must hold
 // a whole output row (the picked variant has bn >= every member's N).
-GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln);
+// pin >= 0: that variant (index into the kernel table) if every member can
+// run on it, else a config with variant -1.
+GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool ln, int pin = -1);
 // Widest output row a fused LayerNorm can take for the dtype.
 int gemm_ln_max_n(optimus_dtype dt);
 // tr: 0 forward; 2 = w reduction-major (dX = dY . W); 3 = x and w
@@ -146,7 +149,7 @@ bool gemm_dma_wt_ok(const optimus_linear_desc* d, int32_t G);
 // split_k: the set's K will be split (dW over the batch), so prefer the large
 // tile; tile = 256 or 128 asks for that bf16 tile edge instead of the rule.
 GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d, int32_t G, bool split_k = false,
-                                  int tile = 0);
+                                  int tile = 0, int pin = -1);
 // Workgroups of the instance gemm_launch would run that fit on one CU at once
 // (the HIP runtime's occupancy of its registers and LDS; cfg.occ if the query fails).
 int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, int tr = 0);
@@ -167,12 +170,14 @@ constexpr int kSocThreads = 256;
 constexpr int kSocMaxChunks = 1024;  // 16-byte chunks per row held in registers by two waves (8 per lane)
 constexpr int kSocMaxPieces = 256;
 constexpr int kSocMaxTasks = 128;    // two per lane
-hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t rows, int32_t nchunks,
-                      int32_t n_pieces, int32_t n_tasks, int32_t grid, hipStream_t stream);
+// wpr: waves per row asked for (1, 2 or 4; a row that needs more waves for
+// its registers takes more).
+hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t nchunks, int32_t n_pieces,
+                      int32_t wpr, int32_t grid, hipStream_t stream);
 // Workgroups of the fused split-op-cat kernel resident per CU (occupancy query)
 // and rows one workgroup works on at a time.
-int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces);
-int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces);
+int soc_blocks_per_cu(optimus_dtype dt, optimus_act act, int32_t nchunks, int32_t n_pieces, int32_t wpr);
+int soc_rows_per_block(optimus_dtype dt, int32_t nchunks, int32_t n_pieces, int32_t wpr);
 
 // ------------------------------------------------------------------ backward
 // One member of the LayerNorm / activation backward. Row mapping as for the

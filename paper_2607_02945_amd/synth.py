@@ -18,6 +18,7 @@ Sec. 5.2: many small bf16 operators; Sec. 3.2: split -> LayerNorm -> act -> cat)
   split_op_cat      [8192, 4096] bf16 split into 32 Dirichlet widths, LN_j -> silu, cat
   towers            26 bf16 MLP towers Linear(in_g->512)+relu+Linear(512->256)+LayerNorm, batch 4096
   large_group       G=32 bf16 Linear members, batch 16384, K=1024 -> LayerNorm -> tanh
+  large_group_shared  the same with one input X shared by every member (batch_linear_lhs)
   decompose_mm      the four tall-skinny mm members of the appendix decompose_mm case
                     study ([~2e7, K] x [K, N], K, N in {(8, 8), (4, 2)}), fp32, no bias
   act_quant         G=32 bf16 saved activations [16384, N_g] (large_group's Linear outputs)
@@ -242,6 +243,25 @@ def large_group(seed: int = 0, G: int = 32, M: int = 16384, K: int = 1024) -> Li
     return LinearLNGroup("large_group", "bf16", members, "tanh", True, gammas, betas, 1e-5)
 
 
+def large_group_shared(seed: int = 0, G: int = 32, M: int = 16384, K: int = 1024) -> LinearLNGroup:
+    """large_group with ONE input X [M, K] shared by every member (Table 1's
+    batch_linear_lhs: Linear members on a common left-hand side). Draws:
+    shapes, per member (W, b, gamma, beta), then X once; distributions as
+    large_group."""
+    g = rng(seed)
+    Ns = g.choice([256, 512, 1024], size=G)
+    ws, gammas, betas = [], [], []
+    for N in Ns.tolist():
+        w = to_storage(_normal(g, (N, K), 1.0 / K), "bf16")
+        b = to_storage(_normal(g, (N,), 0.01), "bf16")
+        gammas.append(to_storage(np.ones(N), "bf16"))
+        betas.append(to_storage(np.zeros(N), "bf16"))
+        ws.append((w, b))
+    x = to_storage(g.standard_normal((M, K)), "bf16")
+    members = [LinearMember(x, w, b) for w, b in ws]
+    return LinearLNGroup("large_group_shared", "bf16", members, "tanh", True, gammas, betas, 1e-5)
+
+
 # The four aten.mm shapes of the decompose_mm case study (appendix Sec. 8.2):
 # (M, K, N) of [M, K] x [K, N]; as Linear members the weight is W = [N, K].
 DECOMPOSE_MM_SHAPES = [(18583840, 8, 8), (25247936, 4, 2), (22502112, 8, 8), (17980096, 4, 2)]
@@ -284,6 +304,7 @@ WORKLOADS = {
     "split_op_cat": split_op_cat,
     "towers": towers,
     "large_group": large_group,
+    "large_group_shared": large_group_shared,
     "decompose_mm": decompose_mm,
     "act_quant": act_quant,
 }

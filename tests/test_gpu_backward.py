@@ -2,7 +2,6 @@
 through the C ABI: Linear (dX, dW, db), activation, LayerNorm (dX, dgamma,
 dbeta); inf-normwise relative error per member and output, 1e-5 for fp32 and
 2e-2 for bf16 (fp32 sums, one rounding of each output)."""
-import os
 
 import numpy as np
 import pytest
@@ -35,20 +34,6 @@ def _empty(shape, dtype, pad=0):
     return t[:, :shape[1]] if pad else t
 
 
-def _with_variant(v, fn):
-    old = os.environ.get("OPTIMUS_GEMM_VARIANT")
-    if v is not None:
-        os.environ["OPTIMUS_GEMM_VARIANT"] = str(v)
-    try:
-        return fn()
-    finally:
-        if v is not None:
-            if old is None:
-                del os.environ["OPTIMUS_GEMM_VARIANT"]
-            else:
-                os.environ["OPTIMUS_GEMM_VARIANT"] = old
-
-
 # ------------------------------------------------------------------ Linear
 def _linear_members(shapes, dtype, seed, pad=0):
     g = synth.rng(seed)
@@ -61,25 +46,27 @@ def _linear_members(shapes, dtype, seed, pad=0):
     return ms
 
 
-def _run_linear_bwd(ms, dtype, mode="oneshot", want=("dx", "dw", "db"), variant=None, pad=0):
+def _run_linear_bwd(ms, dtype, mode="oneshot", want=("dx", "dw", "db"), variant=None, pad=0, splits=0):
+    """The one-shot call, or a plan executed in `mode`; a pinned tile variant
+    (kernel-table index) or dW split count goes through the plan options."""
     for m in ms:
         m["dx"] = _empty((m["M"], m["K"]), dtype, pad) if "dx" in want else None
         m["dw"] = _empty((m["N"], m["K"]), dtype, pad) if "dw" in want else None
         m["db"] = torch.full((m["N"],), float("nan"), dtype=synth.DTYPES[dtype], device="cuda") if "db" in want else None
     args = ([m["x"] for m in ms], [m["w"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms],
             [m["dw"] for m in ms], [m["db"] for m in ms])
-
-    def go():
-        if mode == "oneshot":
-            B.optimus_grouped_linear_backward(*args)
-            return None
-        p = B.optimus_plan_linear_backward(*args)
+    opts = None
+    if variant is not None or splits:
+        opts = {"gemm_tile": 0 if variant is None else variant + 1, "wgrad_splits": splits}
+    info = None
+    if mode == "oneshot" and opts is None:
+        B.optimus_grouped_linear_backward(*args)
+    else:
+        p = B.optimus_plan_linear_backward_ex(*args, options=opts)
         info = p.info()
-        p.execute(mode)
+        p.execute("grouped" if mode == "oneshot" else mode)
         torch.cuda.synchronize()
         p.close()
-        return info
-    info = _with_variant(variant, go)
     torch.cuda.synchronize()
     return info
 
@@ -174,17 +161,29 @@ def test_linear_backward_pinned_split_counts(splits):
     sums; the same results for every count."""
     say(f"[linear bwd splits={splits}]")
     ms = _linear_members([(5000, 256, 264), (3001, 64, 520)], "bf16", seed=600)
-    old = os.environ.get("OPTIMUS_WGRAD_SPLITS")
-    os.environ["OPTIMUS_WGRAD_SPLITS"] = str(splits)
-    try:
-        info = _run_linear_bwd(ms, "bf16", "grouped")
-    finally:
-        if old is None:
-            del os.environ["OPTIMUS_WGRAD_SPLITS"]
-        else:
-            os.environ["OPTIMUS_WGRAD_SPLITS"] = old
+    info = _run_linear_bwd(ms, "bf16", "grouped", splits=splits)
     assert ("_split%d" % splits in info["kernel"]) == (splits > 1) and "dma" in _wgrad_part(info), info
     _check_linear_bwd(ms, "bf16", f"splits {splits}")
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("variant", [4, 5])
+def test_direct_to_lds_backward_every_element_multi_tile(variant):
+    """The backward's direct-to-LDS instances (dX reading W as it lies, dW
+    with both operands reduction-major) with at least two tiles per
+    persistent workgroup: a group of long batches and narrow outputs gives dX
+    many tiles, a group of wide weights and a short batch gives dW many
+    (its split pinned to 1, so every tile runs the plain epilogue); ragged
+    batches; every element of dX, dW and db against the oracle."""
+    say(f"[linear bwd dma multi-tile] variant {variant}")
+    e = 1024 if variant == 4 else 512
+    groups = {"dX": [(4096, 64, e)] * 7 + [(4000, 72, e - 8)],
+              "dW": [(136, e, 1024)] * 31 + [(130, e - 8, 1016)]}
+    for what, shapes in groups.items():
+        ms = _linear_members(shapes, "bf16", seed=540 + variant + (1 if what == "dW" else 0))
+        info = _run_linear_bwd(ms, "bf16", "grouped", variant=variant, splits=1)
+        assert "_dgrad_direct" in info["kernel"] and "dma" in _wgrad_part(info), info
+        _check_linear_bwd(ms, "bf16", f"variant {variant} multi-tile {what}")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
@@ -385,6 +384,39 @@ def test_linear_act_backward_unaligned_activation_input():
         assert_close(host64(m["dx"]), ORC.act_backward(acts[i][1], rdx, "silu"), "bf16", f"member {i} dx")
 
 
+@pytest.mark.parametrize("dtype,aligned", [("fp32", False), ("bf16", False), ("bf16", True)])
+@pytest.mark.parametrize("mode", ["oneshot", "grouped", "chain"])
+def test_linear_act_backward_in_place(dtype, aligned, mode):
+    """act_x is the member's dx itself (the activation input is overwritten by
+    its gradient): fp32 and unaligned bf16 groups compute dY W into plan
+    scratch before the activation backward reads it beside act_x; aligned
+    bf16 groups read act_x in the dX epilogue. Against the oracle's Linear
+    backward then activation backward on the original activation input."""
+    say(f"[linear+act bwd in place] {dtype} aligned={aligned} {mode}")
+    shapes = [(700, 296, 264), (129, 64, 32)] if aligned else [(300, 200, 136), (64, 17, 40), (513, 33, 9)]
+    ms = _linear_members(shapes, dtype, seed=597)
+    g = synth.rng(598)
+    acts = [_t(g.standard_normal((m["M"], m["K"])), dtype) for m in ms]
+    for m, a in zip(ms, acts):
+        m["dx"] = a[0]  # the activation input's storage receives dL/da
+        m["dw"] = _empty((m["N"], m["K"]), dtype)
+    args = ([m["x"] for m in ms], [m["w"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms],
+            [m["dw"] for m in ms], None, [m["dx"] for m in ms], "tanh")
+    if mode == "oneshot":
+        B.optimus_grouped_linear_act_backward(*args)
+    else:
+        p = B.optimus_plan_linear_act_backward(*args)
+        assert ("_dgrad_direct_tanh" in p.info()["kernel"]) == aligned, p.info()
+        p.execute(mode)
+        torch.cuda.synchronize()
+        p.close()
+    torch.cuda.synchronize()
+    for i, m in enumerate(ms):
+        rdx, rdw, _ = ORC.linear_backward(m["x64"], m["w64"], m["dy64"])
+        assert_close(host64(m["dx"]), ORC.act_backward(acts[i][1], rdx, "tanh"), dtype, f"member {i} dx in place")
+        assert_close(host64(m["dw"]), rdw, dtype, f"member {i} dw")
+
+
 # ------------------------------------------------------------------ fused LayerNorm + activation
 def _ref_ln_act_bwd(m, beta64, act, eps):
     """The oracle composition: the activation's input z = LayerNorm(x) (fp64,
@@ -506,9 +538,12 @@ def _dw_sampled(x64, w64, dy64, ns):
     return dw_s, db_s
 
 
-def _sample(n, k, seed):
+def _sample(n, k, seed, block=256):
+    """k random rows of n, both edge rows, and one random row of every
+    `block`-row block (every M-block of the GEMM tiles)."""
     g = synth.rng(seed)
-    return np.unique(np.concatenate([[0, n - 1], g.choice(n, size=min(n, k), replace=False)])).astype(np.int64)
+    per_block = [b + g.integers(0, min(block, n - b)) for b in range(0, n, block)]
+    return np.unique(np.concatenate([[0, n - 1], per_block, g.choice(n, size=min(n, k), replace=False)])).astype(np.int64)
 
 
 @pytest.mark.timeout(300)

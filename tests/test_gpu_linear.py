@@ -1,5 +1,4 @@
 """Grouped Linear on the GPU against the fp64 oracle (through the C ABI)."""
-import os
 
 import numpy as np
 import pytest
@@ -37,25 +36,18 @@ def _members(shapes, dtype, seed, integer=False, strided=False, bias=True):
 
 
 def _run(ms, dtype, act, mode="oneshot", variant=None):
+    """One group through the one-shot call, or a plan executed in `mode`; a
+    pinned tile variant (kernel-table index) goes through the plan options."""
     ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, _ in ms]
     xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
-    old = os.environ.get("OPTIMUS_GEMM_VARIANT")
-    if variant is not None:
-        os.environ["OPTIMUS_GEMM_VARIANT"] = str(variant)
-    try:
-        if mode == "oneshot":
-            B.optimus_grouped_linear(xs, ws, bs, ys, act)
-        else:
-            p = B.optimus_plan_linear(xs, ws, bs, ys, act)
-            p.execute(mode)
-            torch.cuda.synchronize()
-            p.close()
-    finally:
-        if variant is not None:
-            if old is None:
-                del os.environ["OPTIMUS_GEMM_VARIANT"]
-            else:
-                os.environ["OPTIMUS_GEMM_VARIANT"] = old
+    if mode == "oneshot" and variant is None:
+        B.optimus_grouped_linear(xs, ws, bs, ys, act)
+    else:
+        opts = None if variant is None else {"gemm_tile": variant + 1}
+        p = B.optimus_plan_linear_ex(xs, ws, bs, ys, act, options=opts)
+        p.execute("grouped" if mode == "oneshot" else mode)
+        torch.cuda.synchronize()
+        p.close()
     return ys
 
 
@@ -82,7 +74,7 @@ def test_every_bf16_tile_variant(variant):
     say(f"[linear variant] {variant}")
     shapes = [(513, 300, 72), (256, 256, 1024), (31, 7, 40), (700, 520, 136)]
     ms = _members(shapes, "bf16", seed=11 + variant)
-    for mode in ["oneshot", "grouped", "chain"]:
+    for mode in ["grouped", "chain"]:
         ys = _run(ms, "bf16", "tanh", mode=mode, variant=variant)
         _check(ms, ys, "bf16", "tanh", f"variant {variant} {mode}")
 
@@ -232,3 +224,28 @@ def test_skinny_against_tiled_kernel():
     for v in (3, 7):
         ys = _run(ms, "fp32", "none", variant=v)
         _check(ms, ys, "fp32", "none", f"variant {v}")
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("variant", [4, 5])
+def test_direct_to_lds_tiles_every_element_multi_tile(variant):
+    """Each direct-to-LDS forward tile (256x256 8 waves, 128x128 4 waves) on a
+    group with at least two tiles per persistent workgroup, so every
+    workgroup prefetches a next tile's first K step during its last one and
+    stages epilogues back to back; ragged tails in M and N, K of one to
+    several steps; every output element against the oracle."""
+    say(f"[linear dma multi-tile] variant {variant}")
+    if variant == 4:
+        shapes = [(4096, 1024, 64)] * 6 + [(4000, 1000, 72), (3900, 1016, 136)]
+    else:
+        shapes = [(4096, 512, 64)] * 6 + [(4000, 500, 72), (3900, 504, 136)]
+    ms = _members(shapes, "bf16", seed=120 + variant)
+    ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, _ in ms]
+    p = B.optimus_plan_linear_ex([m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms], ys, "silu",
+                                 options={"gemm_tile": variant + 1})
+    info = p.info()
+    assert info["work_items"] >= 2 * info["grid"], info
+    p.execute()
+    torch.cuda.synchronize()
+    p.close()
+    _check(ms, ys, "bf16", "silu", f"variant {variant} multi-tile")

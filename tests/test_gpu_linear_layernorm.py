@@ -1,6 +1,5 @@
 """Grouped Linear with the row LayerNorm fused into the GEMM epilogue, on the
 GPU against the fp64 oracle composition (through the C ABI)."""
-import os
 
 import numpy as np
 import pytest
@@ -31,29 +30,22 @@ def _members(shapes, dtype, seed, params=True, bias=True):
 
 
 def _run(ms, act, eps=1e-5, mode="oneshot", variant=None):
+    """The one-shot call, or a plan executed in `mode`; a pinned tile variant
+    (kernel-table index) goes through the plan options."""
     xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
     gs, es = [m[3] for m in ms], [m[4] for m in ms]
     ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, *_ in ms]
-    old = os.environ.get("OPTIMUS_GEMM_VARIANT")
-    if variant is not None:
-        os.environ["OPTIMUS_GEMM_VARIANT"] = str(variant)
-    try:
-        if mode == "oneshot":
-            B.optimus_grouped_linear_layernorm(xs, ws, bs, ys, gs, es, eps, act)
-            kernel = None
-        else:
-            p = B.optimus_plan_linear_layernorm(xs, ws, bs, ys, gs, es, eps, act)
-            kernel = p.info()["kernel"]
-            assert p.info()["kind"] == 4
-            p.execute(mode)
-            torch.cuda.synchronize()
-            p.close()
-    finally:
-        if variant is not None:
-            if old is None:
-                del os.environ["OPTIMUS_GEMM_VARIANT"]
-            else:
-                os.environ["OPTIMUS_GEMM_VARIANT"] = old
+    if mode == "oneshot" and variant is None:
+        B.optimus_grouped_linear_layernorm(xs, ws, bs, ys, gs, es, eps, act)
+        kernel = None
+    else:
+        opts = None if variant is None else {"gemm_tile": variant + 1}
+        p = B.optimus_plan_linear_layernorm_ex(xs, ws, bs, ys, gs, es, eps, act, options=opts)
+        kernel = p.info()["kernel"]
+        assert p.info()["kind"] == 4
+        p.execute("grouped" if mode == "oneshot" else mode)
+        torch.cuda.synchronize()
+        p.close()
     return ys, kernel
 
 
@@ -151,3 +143,26 @@ def test_rows_too_wide_are_rejected():
     assert ei.value.name == "UNSUPPORTED"
     assert torch.count_nonzero(ys[0]) == 0
     B.optimus_grouped_linear_layernorm([], [], [], [], None, None, 1e-5, "none")
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("variant", [4, 5])
+def test_direct_to_lds_layernorm_every_element_multi_tile(variant):
+    """The fused LayerNorm epilogue on each direct-to-LDS tile with at least
+    two tiles per persistent workgroup (whole rows per tile: N <= the tile's
+    width), a ragged row count and a narrower member; every element against
+    the oracle's fused composition."""
+    bn = {4: 256, 5: 128}[variant]
+    shapes = [(16384, bn, 64)] * 6 + [(16000, bn - 8, 72), (15000, bn // 2, 136)]
+    say(f"[linear+ln dma multi-tile] variant {variant}")
+    ms = _members(shapes, "bf16", seed=160 + variant)
+    xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
+    gs, es = [m[3] for m in ms], [m[4] for m in ms]
+    ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, *_ in ms]
+    p = B.optimus_plan_linear_layernorm_ex(xs, ws, bs, ys, gs, es, 1e-5, "tanh", options={"gemm_tile": variant + 1})
+    info = p.info()
+    assert info["work_items"] >= 2 * info["grid"], info
+    p.execute()
+    torch.cuda.synchronize()
+    p.close()
+    _check(ms, ys, "bf16", "tanh", f"variant {variant} multi-tile")

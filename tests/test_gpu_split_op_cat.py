@@ -135,3 +135,56 @@ def test_wide_row_falls_back_to_grouped_layernorm():
     assert p.info()["kernel"] == "split_op_cat_as_grouped_layernorm"
     _check_pieces(y, x, widths, gms, bts, "tanh", "bf16", "wide")
     p.close()
+
+
+@pytest.mark.parametrize("widths", [None, [8, 24, 40, 8, 48]])
+def test_plan_reads_updated_affine_parameters(widths):
+    """A plan keeps the pieces' gamma / beta pointers: after an in-place update
+    of every piece's parameters (as an optimizer step makes) the next execute
+    of the same plan applies the new values. Both executes against the
+    oracle. Dirichlet widths and short pieces (the per-value gather path is
+    taken for parameters that start off 16-byte alignment)."""
+    say(f"[soc updated params] widths={widths}")
+    if widths is None:
+        widths = synth.dirichlet_widths(synth.rng(52), 32, 4096)
+    x, gms, bts = _case(300, widths, "bf16", seed=53)
+    if len(widths) == 5:  # parameters one value past 16-byte alignment
+        g = synth.rng(54)
+        gms, bts = [], []
+        for w in widths:
+            for lst, v in ((gms, g.uniform(0.5, 1.5, w)), (bts, g.standard_normal(w) * 0.3)):
+                buf = torch.zeros(w + 1, dtype=torch.bfloat16, device="cuda")
+                buf[1:] = dev(synth.to_storage(v, "bf16"))
+                lst.append(buf[1:])
+    y = torch.full_like(x, float("nan"))
+    p = B.optimus_plan_split_op_cat(x, y, widths, gms, bts, True, 1e-5, "silu")
+    assert p.info()["kernel"].startswith("split_op_cat_fused"), p.info()
+    p.execute()
+    torch.cuda.synchronize()
+    _check_pieces(y, x, widths, gms, bts, "silu", "bf16", "first execute")
+    g = synth.rng(55)
+    for gm, bt in zip(gms, bts):
+        gm.copy_(dev(synth.to_storage(g.uniform(-2.0, 2.0, gm.shape[0]), "bf16")))
+        bt.copy_(dev(synth.to_storage(g.standard_normal(bt.shape[0]), "bf16")))
+    y.fill_(float("nan"))
+    p.execute()
+    torch.cuda.synchronize()
+    _check_pieces(y, x, widths, gms, bts, "silu", "bf16", "after the parameter update")
+    p.close()
+
+
+@pytest.mark.parametrize("wpr", [1, 2, 4])
+def test_pinned_waves_per_row(wpr):
+    """The fused kernel with 1, 2 or 4 waves per row (plan options), bf16 and
+    fp32, against the oracle."""
+    say(f"[soc waves per row] {wpr}")
+    widths = synth.dirichlet_widths(synth.rng(56), 32, 4096)
+    for dtype in ["bf16", "fp32"]:
+        x, gms, bts = _case(123, widths, dtype, seed=57)
+        y = torch.full_like(x, float("nan"))
+        p = B.optimus_plan_split_op_cat_ex(x, y, widths, gms, bts, True, 1e-5, "silu",
+                                           options={"soc_waves_per_row": wpr})
+        p.execute()
+        torch.cuda.synchronize()
+        _check_pieces(y, x, widths, gms, bts, "silu", dtype, f"wpr {wpr}")
+        p.close()

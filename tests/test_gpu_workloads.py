@@ -18,9 +18,12 @@ pytestmark = pytest.mark.gpu
 ORC = oracle.get()
 
 
-def _sample_rows(M, n, seed):
+def _sample_rows(M, n, seed, block=256):
+    """n random rows of M, both edge rows, and one random row of every
+    `block`-row block (so every M-block of the GEMM's tiles is compared)."""
     g = synth.rng(seed)
-    rows = np.unique(np.concatenate([[0, M - 1], g.choice(M, size=min(M, n), replace=False)]))
+    per_block = [b + g.integers(0, min(block, M - b)) for b in range(0, M, block)]
+    rows = np.unique(np.concatenate([[0, M - 1], per_block, g.choice(M, size=min(M, n), replace=False)]))
     return rows.astype(np.int64)
 
 
@@ -158,7 +161,7 @@ def test_large_group_full_size_sampled_rows():
     p1.execute()
     p2.execute()
     torch.cuda.synchronize()
-    rows = _sample_rows(16384, 48, seed=62)
+    rows = _sample_rows(16384, 16, seed=62)
     for i, m in enumerate(wl.members):
         lin = ORC.linear_rows(synth.exact64(m.x), synth.exact64(m.w), synth.exact64(m.b), rows)
         yh = host64(ys[i])
@@ -168,6 +171,49 @@ def test_large_group_full_size_sampled_rows():
                      f"member {i} layernorm+tanh (per op)")
         assert_close(host64(zs[i])[rows], ORC.layernorm(lin, g64, b64, wl.eps, "tanh"), "bf16",
                      f"member {i} end to end")
+
+
+def test_large_group_shared_input_full_size_sampled_rows():
+    """The large group's 32 members on ONE shared input X [16384, 1024]
+    (batch_linear_lhs), the Linear then LayerNorm + tanh as the benchmark
+    runs them; one row of every 256-row M-block and the edges, per operator
+    and end to end. The tile list walks M-blocks across members, the CHAIN
+    launches a member-major copy of it."""
+    say("[workload large_group_shared] G=32 B=16384 K=1024 bf16, one X")
+    wl = synth.large_group_shared(0)
+    x = dev(wl.members[0].x)
+    xs = [x] * wl.G
+    ws = [dev(m.w) for m in wl.members]
+    bs = [dev(m.b) for m in wl.members]
+    ys = [torch.empty((m.M, m.N), dtype=torch.bfloat16, device="cuda") for m in wl.members]
+    zs = [torch.empty_like(y) for y in ys]
+    gs = [dev(g) for g in wl.gammas]
+    be = [dev(b) for b in wl.betas]
+    p1 = B.optimus_plan_linear(xs, ws, bs, ys, "none")
+    p2 = B.optimus_plan_layernorm(ys, zs, gs, be, wl.eps, "tanh")
+    p1.execute()
+    p2.execute()
+    torch.cuda.synchronize()
+    rows = _sample_rows(16384, 16, seed=67)
+    x64 = synth.exact64(wl.members[0].x)
+    lins = []
+    for i, m in enumerate(wl.members):
+        lin = ORC.linear_rows(x64, synth.exact64(m.w), synth.exact64(m.b), rows)
+        lins.append(lin)
+        yh = host64(ys[i])
+        assert_close(yh[rows], lin, "bf16", f"member {i} linear")
+        g64, b64 = synth.exact64(wl.gammas[i]), synth.exact64(wl.betas[i])
+        assert_close(host64(zs[i])[rows], ORC.layernorm(yh[rows], g64, b64, wl.eps, "tanh"), "bf16",
+                     f"member {i} layernorm+tanh (per op)")
+        assert_close(host64(zs[i])[rows], ORC.layernorm(lin, g64, b64, wl.eps, "tanh"), "bf16",
+                     f"member {i} end to end")
+    # the per-member chain over the member-major tile list: the same outputs
+    y2 = [torch.full_like(y, float("nan")) for y in ys]
+    p3 = B.optimus_plan_linear(xs, ws, bs, y2, "none")
+    p3.execute("chain")
+    torch.cuda.synchronize()
+    for i in range(wl.G):
+        assert_close(host64(y2[i])[rows], lins[i], "bf16", f"member {i} linear, chain")
 
 
 def test_decompose_mm_full_size_sampled_rows():
