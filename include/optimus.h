@@ -289,6 +289,24 @@ optimus_status optimus_split_op_cat(const optimus_split_op_cat_desc* d, optimus_
 optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
                                             int32_t use_scaling, optimus_stream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * optimus_grouped_quantize_fp8 with the group's descriptor table and amax
+ * partials placed in a library-owned static device array of
+ * OPTIMUS_NOALLOC_SCRATCH_BYTES per GPU (held until the process ends)
+ * instead of stream-ordered allocations; the table goes up with one
+ * hipMemcpyAsync from host memory. Arguments, results and errors as
+ * optimus_grouped_quantize_fp8, bit for bit; a group whose table and
+ * partials exceed OPTIMUS_NOALLOC_SCRATCH_BYTES returns
+ * OPTIMUS_ERR_UNSUPPORTED with nothing launched. Every call on one GPU uses
+ * that GPU's one array: calls on the same stream are ordered, but calls that
+ * may overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller. The array needs no clearing between calls (every
+ * amax partial is written before it is read). */
+#define OPTIMUS_NOALLOC_SCRATCH_BYTES (4u << 20)
+optimus_status optimus_grouped_quantize_fp8_noalloc(const optimus_fp8_quant_desc* d, int32_t G, optimus_dtype dt,
+                                                    int32_t use_scaling, optimus_stream_t stream);
+
 /* Grouped fp8 dequantize: y = fp32(value(q) * scale) rounded to the group's
  * dtype (nearest even for bf16); NaN codes give NaN. */
 optimus_status optimus_grouped_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G, optimus_dtype dt,

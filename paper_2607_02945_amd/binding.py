@@ -115,7 +115,7 @@ EXPORTS = [
     "optimus_plan_linear", "optimus_plan_linear_layernorm", "optimus_plan_layernorm", "optimus_plan_pointwise",
     "optimus_plan_split_op_cat", "optimus_plan_quantize_fp8", "optimus_plan_dequantize_fp8",
     "optimus_plan_linear_ex", "optimus_plan_linear_layernorm_ex", "optimus_plan_linear_backward_ex",
-    "optimus_plan_linear_act_backward_ex", "optimus_plan_split_op_cat_ex",
+    "optimus_plan_linear_act_backward_ex", "optimus_plan_split_op_cat_ex", "optimus_grouped_quantize_fp8_noalloc",
     "optimus_plan_execute", "optimus_plan_execute_mode", "optimus_plan_destroy", "optimus_plan_get_info",
     "optimus_validate_linear", "optimus_validate_linear_layernorm", "optimus_validate_layernorm",
     "optimus_validate_pointwise", "optimus_validate_split_op_cat", "optimus_validate_quantize_fp8",
@@ -174,6 +174,7 @@ def lib() -> ctypes.CDLL:
             "optimus_validate_act_backward": (st, [P(ActGradDesc), c_i32, ctypes.c_int, ctypes.c_int]),
             "optimus_grouped_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32, c_vp]),
             "optimus_grouped_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int, c_vp]),
+            "optimus_grouped_quantize_fp8_noalloc": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32, c_vp]),
             "optimus_plan_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32, P(c_vp)]),
             "optimus_plan_dequantize_fp8": (st, [P(Fp8DequantDesc), c_i32, ctypes.c_int, P(c_vp)]),
             "optimus_validate_quantize_fp8": (st, [P(Fp8QuantDesc), c_i32, ctypes.c_int, c_i32]),
@@ -404,6 +405,14 @@ def optimus_grouped_quantize_fp8(xs, qs, scales=None, use_scaling=True, stream=N
     d = fp8_quant_descs(xs, qs, scales)
     check(lib().optimus_grouped_quantize_fp8(d, len(xs), dtype_code(xs[0]) if xs else BF16, int(use_scaling),
                                              _stream(stream)))
+
+
+def optimus_grouped_quantize_fp8_noalloc(xs, qs, scales=None, use_scaling=True, stream=None) -> None:
+    """optimus_grouped_quantize_fp8 with no device allocation: the table and amax
+    partials live in the library's static per-GPU scratch array."""
+    d = fp8_quant_descs(xs, qs, scales)
+    check(lib().optimus_grouped_quantize_fp8_noalloc(d, len(xs), dtype_code(xs[0]) if xs else BF16,
+                                                     int(use_scaling), _stream(stream)))
 
 
 def optimus_grouped_dequantize_fp8(qs, scales, ys, stream=None) -> None:

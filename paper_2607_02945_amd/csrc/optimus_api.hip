@@ -15,6 +15,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <cstddef>
 #include <string>
@@ -2174,6 +2175,64 @@ extern "C" optimus_status optimus_grouped_quantize_fp8(const optimus_fp8_quant_d
   optimus_status st = build_quantize_fp8(d, G, dt, use_scaling, hp);
   return st != OPTIMUS_OK ? st : run_oneshot(hp, (hipStream_t)stream);
 }
+// ===================================================================== no-allocation entry point
+// The table (and any plan scratch after it) of a call that may not allocate
+// lives in this array: one copy per GPU, for the life of the process. Host
+// code never passes the array's name to a kernel; it uses the device address
+// hipGetSymbolAddress returns, looked up once per device with that device
+// current.
+static __device__ __align__(256) char scratch[OPTIMUS_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+static optimus_status noalloc_scratch(char** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev), "noalloc: current device");
+  if (dev < 0 || dev >= kMaxDevices) return fail(OPTIMUS_ERR_UNSUPPORTED, "noalloc: device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "noalloc: scratch address");
+    if (!p) return fail(OPTIMUS_ERR_HIP, "noalloc: scratch address is NULL");
+    g_scratch_ptr[dev] = (char*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return OPTIMUS_OK;
+}
+
+// One grouped execution with the table, then the plan scratch, in the
+// static array: no device or pinned allocation. The blob is host memory the
+// copy reads before the enqueue returns (pageable source).
+static optimus_status run_noalloc(HostPlan& hp, hipStream_t stream, const char* what) {
+  if (hp.G == 0) return OPTIMUS_OK;
+  const size_t table = (std::max<size_t>(hp.blob.bytes.size(), 256) + 255) & ~(size_t)255;
+  const size_t need = table + hp.scratch_bytes;
+  if (need > (size_t)OPTIMUS_NOALLOC_SCRATCH_BYTES)
+    return fail(OPTIMUS_ERR_UNSUPPORTED, "%s: the group needs %zu bytes of scratch, above the %u-byte limit", what,
+                need, (unsigned)OPTIMUS_NOALLOC_SCRATCH_BYTES);
+  char* base = nullptr;
+  optimus_status st = noalloc_scratch(&base);
+  if (st != OPTIMUS_OK) return st;
+  rebase_soc(hp, base);
+  rebase_fixups(hp, base, hp.scratch_bytes ? base + table : nullptr);
+  HIP_TRY(hipMemcpyAsync(base, hp.blob.bytes.data(), hp.blob.bytes.size(), hipMemcpyHostToDevice, stream),
+          "noalloc: table upload");
+  hipError_t e = launch_grouped(hp, base, stream);
+  return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "noalloc: launch");
+}
+
+extern "C" optimus_status optimus_grouped_quantize_fp8_noalloc(const optimus_fp8_quant_desc* d, int32_t G,
+                                                               optimus_dtype dt, int32_t use_scaling,
+                                                               optimus_stream_t stream) {
+  HostPlan hp;
+  optimus_status st = build_quantize_fp8(d, G, dt, use_scaling, hp);
+  return st != OPTIMUS_OK ? st : run_noalloc(hp, (hipStream_t)stream, "grouped_quantize_fp8_noalloc");
+}
+
 extern "C" optimus_status optimus_grouped_dequantize_fp8(const optimus_fp8_dequant_desc* d, int32_t G,
                                                          optimus_dtype dt, optimus_stream_t stream) {
   HostPlan hp;
