@@ -238,7 +238,7 @@ def test_direct_to_lds_tiles_every_element_multi_tile(variant):
     if variant == 4:
         shapes = [(4096, 1024, 64)] * 6 + [(4000, 1000, 72), (3900, 1016, 136)]
     else:
-        shapes = [(4096, 512, 64)] * 6 + [(4000, 500, 72), (3900, 504, 136)]
+        shapes = [(4096, 512, 64)] * 7 + [(4000, 500, 72), (3900, 504, 136)]
     ms = _members(shapes, "bf16", seed=120 + variant)
     ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, _ in ms]
     p = B.optimus_plan_linear_ex([m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms], ys, "silu",

@@ -153,7 +153,7 @@ def test_direct_to_lds_layernorm_every_element_multi_tile(variant):
     width), a ragged row count and a narrower member; every element against
     the oracle's fused composition."""
     bn = {4: 256, 5: 128}[variant]
-    shapes = [(16384, bn, 64)] * 6 + [(16000, bn - 8, 72), (15000, bn // 2, 136)]
+    shapes = [(16384, bn, 64)] * 8 + [(16000, bn - 8, 72), (15000, bn // 2, 136)]
     say(f"[linear+ln dma multi-tile] variant {variant}")
     ms = _members(shapes, "bf16", seed=160 + variant)
     xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
