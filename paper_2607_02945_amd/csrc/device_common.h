@@ -124,6 +124,25 @@ __device__ __forceinline__ float act_apply(float x) {
   }
 }
 
+// The activations whose exponent argument is a fixed multiple of the input
+// (sigmoid: 2^(-x log2 e); tanh: 2^(2 x log2 e)) can take that product
+// directly: act_in_scale is the multiple (1 for the others) and
+// act_scaled_in(u) = act_apply(u / act_in_scale).
+template <int ACT>
+__device__ __forceinline__ constexpr float act_in_scale() {
+  return ACT == OPTIMUS_ACT_SIGMOID ? -1.4426950408889634f : ACT == OPTIMUS_ACT_TANH ? 2.8853900817779268f : 1.f;
+}
+template <int ACT>
+__device__ __forceinline__ float act_scaled_in(float u) {
+  if constexpr (ACT == OPTIMUS_ACT_SIGMOID) {
+    return fast_rcp(1.f + __builtin_amdgcn_exp2f(u));
+  } else if constexpr (ACT == OPTIMUS_ACT_TANH) {
+    return 1.f - 2.f * fast_rcp(__builtin_amdgcn_exp2f(u) + 1.f);
+  } else {
+    return act_apply<ACT>(u);
+  }
+}
+
 // Derivative of one activation at its input, in the same hardware
 // exponential / reciprocal forms as the forward activations.
 template <int ACT>

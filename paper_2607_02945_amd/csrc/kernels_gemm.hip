@@ -439,8 +439,6 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
 #pragma unroll
       for (int e = 0; e < VEC; ++e) xs[i][e] = 0.f;
 
-    load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
-
     f32x16 acc[S::FM][S::FN];
 #pragma unroll
     for (int i = 0; i < S::FM; ++i)
@@ -535,9 +533,13 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
       }
     };
 
+    // the first K step's operand loads go out before the tile's bias (and
+    // LayerNorm parameter) loads, whose values are written to LDS: that
+    // write waits for them, and the operand loads then fly meanwhile
     const int nk = (kend - kbeg + BK - 1) / BK;
     if constexpr (STAGES == 2) {
       gload(kbeg);
+      load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
       lstore(0);
       __syncthreads();
       for (int kb = 0; kb < nk; ++kb) {
@@ -549,11 +551,13 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
     } else {
       for (int kb = 0; kb < nk; ++kb) {
         gload(kbeg + kb * BK);
+        if (kb == 0) load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
         lstore(0);
         __syncthreads();
         compute(0);
         __syncthreads();
       }
+      if (nk == 0) load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
     }
 
     if constexpr (TX) {

@@ -27,19 +27,30 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
   const int sub = lane / L;
   const int li = lane & (L - 1);
   const int cpr = d.cols / VEC;
-
-  // gamma / beta stay packed (unpacked where used): registers set the occupancy
-  u32x4 gp[MAXC], bp[MAXC];
-  {
-    float one[VEC], zero[VEC];
+  // gamma / beta unpacked once per tile into fp32 registers; for sigmoid and
+  // tanh they also carry the activation's input scale (act_scaled_in), so
+  // that the affine step yields the exponent's argument directly
+  constexpr float ks = act_in_scale<ACT>();
+  float gf[MAXC][VEC], bf[MAXC][VEC];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) { one[e] = 1.f; zero[e] = 0.f; }
-    const u32x4 ones = Elem<T>::pack(one), zeros = Elem<T>::pack(zero);
+  for (int j = 0; j < MAXC; ++j) {
+    const int c = j * L + li;
+    if (d.gamma && c < cpr) {
+      Elem<T>::unpack(ld16((const char*)d.gamma + (int64_t)c * 16), gf[j]);
+    } else {
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-      const int c = j * L + li;
-      gp[j] = (d.gamma && c < cpr) ? ld16((const char*)d.gamma + (int64_t)c * 16) : ones;
-      bp[j] = (d.beta && c < cpr) ? ld16((const char*)d.beta + (int64_t)c * 16) : zeros;
+      for (int e = 0; e < VEC; ++e) gf[j][e] = 1.f;
+    }
+    if (d.beta && c < cpr) {
+      Elem<T>::unpack(ld16((const char*)d.beta + (int64_t)c * 16), bf[j]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) bf[j][e] = 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      gf[j][e] *= ks;
+      bf[j][e] *= ks;
     }
   }
   const int rpb = 4 * rpw;
@@ -90,13 +101,9 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
     for (int j = 0; j < MAXC; ++j) {
       const int c = j * L + li;
       if (valid && c < cpr) {
-        float g[VEC], b[VEC], o[VEC];
-        u32x4 gj = gp[j], bj = bp[j];
-        __asm__ volatile("" : "+v"(gj), "+v"(bj));  // unpack here, not hoisted out of the row loop
-        Elem<T>::unpack(gj, g);
-        Elem<T>::unpack(bj, b);
+        float o[VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) o[e] = act_apply<ACT>(x[j][e] * (rstd * g[e]) + b[e]);
+        for (int e = 0; e < VEC; ++e) o[e] = act_scaled_in<ACT>(x[j][e] * (rstd * gf[j][e]) + bf[j][e]);
         st16_nt(yr + (int64_t)c * 16, Elem<T>::pack(o));
       }
     }
@@ -145,8 +152,9 @@ __global__ __launch_bounds__(kRowThreads) void grouped_layernorm_kernel(const De
 
 // ===================================================================== pointwise
 // Same row/lane mapping as the LayerNorm kernel, without the reductions; a
-// lane group loops over the row's chunks (any row length), four loads in
-// flight per lane.
+// lane group loops over the row's chunks (any row length), kPwInflight loads
+// in flight per lane.
+constexpr int kPwInflight = 4;  // eight was faster on 1.25 GB but slower on 134 MB
 template <typename T, int ACT>
 __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const DevRows* __restrict__ descs,
                                                                         const RowTile* __restrict__ tiles,
@@ -163,14 +171,14 @@ __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const De
       for (int r = rt.row0 + wave * rpw + sub; r < end; r += 4 * rpw) {
         const char* xr = (const char*)d.x + (int64_t)r * d.ldx * sizeof(T);
         char* yr = (char*)d.y + (int64_t)r * d.ldy * sizeof(T);
-        // four chunks per lane in flight, then the rest one at a time
+        // kPwInflight chunks per lane in flight, then the rest one at a time
         int c = li;
-        for (; c + 3 * L < cpr; c += 4 * L) {
-          u32x4 rv[4];
+        for (; c + (kPwInflight - 1) * L < cpr; c += kPwInflight * L) {
+          u32x4 rv[kPwInflight];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) rv[u] = ld16_nt(xr + (int64_t)(c + u * L) * 16);
+          for (int u = 0; u < kPwInflight; ++u) rv[u] = ld16_nt(xr + (int64_t)(c + u * L) * 16);
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
+          for (int u = 0; u < kPwInflight; ++u) {
             float v[VEC];
             Elem<T>::unpack(rv[u], v);
 #pragma unroll

@@ -1302,6 +1302,7 @@ static optimus_status build_layernorm(const optimus_layernorm_desc* d, int32_t G
   return OPTIMUS_OK;
 }
 
+static constexpr int64_t kPwWideRow = 4096;  // elements per re-viewed row of a contiguous pointwise member
 static optimus_status build_pointwise(const optimus_pointwise_desc* d, int32_t G, optimus_dtype dt, optimus_act act,
                                       HostPlan& hp) {
   optimus_status st = optimus_validate_pointwise(d, G, dt, act);
@@ -1311,7 +1312,17 @@ static optimus_status build_pointwise(const optimus_pointwise_desc* d, int32_t G
   std::vector<DevRows> members;
   for (int g = 0; g < G; ++g) {
     const optimus_pointwise_desc& m = d[g];
-    members.push_back(make_rows(m.x, m.ldx, m.y, m.ldy, nullptr, nullptr, m.rows, m.cols, 0.f, dt, false));
+    // an elementwise map ignores the row structure: a member whose rows are
+    // contiguous (ld == cols) and shorter than the wide row is re-viewed as
+    // rows of kPwWideRow elements, so that every lane keeps several 16-byte
+    // loads in flight instead of one per narrow row
+    int64_t rows = m.rows, cols = m.cols;
+    const int64_t total = m.rows * m.cols;
+    if (m.ldx == m.cols && m.ldy == m.cols && m.cols < kPwWideRow && total % kPwWideRow == 0) {
+      rows = total / kPwWideRow;
+      cols = kPwWideRow;
+    }
+    members.push_back(make_rows(m.x, cols, m.y, cols, nullptr, nullptr, rows, cols, 0.f, dt, false));
     hp.bytes += (double)s * 2.0 * m.rows * m.cols;
   }
   build_rows(hp, members, false, s);
