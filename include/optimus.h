@@ -440,7 +440,8 @@ typedef enum {
   OPTIMUS_TILE_BF16_DMA_256X256 = 5, /* direct-to-LDS loads, 8 waves */
   OPTIMUS_TILE_BF16_DMA_128X128 = 6, /* direct-to-LDS loads, 4 waves */
   OPTIMUS_TILE_F32_64X128 = 7,
-  OPTIMUS_TILE_SKINNY = 8            /* every K and N <= 8: streaming, no MFMA */
+  OPTIMUS_TILE_SKINNY = 8,           /* every K and N <= 8: streaming, no MFMA */
+  OPTIMUS_TILE_F32_32X128 = 9        /* 4 waves across the 128 columns */
 } optimus_gemm_tile;
 
 typedef struct {

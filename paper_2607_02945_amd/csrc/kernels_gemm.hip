@@ -1524,7 +1524,8 @@ struct GemmVariant {
 // 3: fp32 64x64; 4-5: direct-to-LDS (bf16, aligned rows, K % 8 == 0):
 // 256x256 8 waves, 128x128 4 waves; 6: fp32 64x128 (a fused LayerNorm over
 // fp32 rows of 65 to 128 columns); 7: skinny members (every K, N <= 8), fp32 or
-// bf16, streamed with no MFMA.
+// bf16, streamed with no MFMA; 8: fp32 32x128, 4 waves across the columns
+// (groups with fewer 64-row tiles than CUs).
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
     {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
@@ -1534,6 +1535,7 @@ static const GemmVariant kVariants[] = {
     {128, 128, 256, 2, "grouped_gemm_dma_bf16_128x128x64_w2x2"},
     {64, 128, 256, 1, "grouped_gemm_f32_64x128x64_w2x2_s2"},
     {kSkinnyRows, kSkinnyMax, 256, 4, "grouped_gemm_skinny"},
+    {32, 128, 256, 2, "grouped_gemm_f32_32x128x64_w1x4_s2"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
 
@@ -1596,7 +1598,7 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
       ok = false;
     else if (pin == 7)
       ok = skinny;
-    else if ((dt == OPTIMUS_F32) != (pin == 3 || pin == 6))
+    else if ((dt == OPTIMUS_F32) != (pin == 3 || pin == 6 || pin == 8))
       ok = false;
     else
       ok = (dt == OPTIMUS_F32 || pin < 4 || dma) && (!ln || kVariants[pin].bn >= maxN);
@@ -1606,6 +1608,13 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     v = 7;
   } else if (dt == OPTIMUS_F32) {
     v = (ln && maxN > 64) ? 6 : 3;
+    // a group of fewer 64-row tiles than CUs: 32-row tiles double the
+    // workgroups and halve each one's serial MFMA work (the small fp32
+    // groups are latency bound: 15.7 -> 10.8 us for tiny_group's eight
+    // members of 512 rows)
+    double tiles64 = 0.0;
+    for (int g = 0; g < G; ++g) tiles64 += (double)((d[g].M + 63) / 64) * (double)((d[g].N + 127) / 128);
+    if (maxN > 64 && maxN <= 128 && tiles64 < device_cu_count()) v = 8;
   } else if (maxN <= 64 && maxK <= 64) {
     v = 0;
   } else if (tiles256 >= 0.5 * device_cu_count() || (ln && maxN > 128)) {
@@ -1757,6 +1766,7 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
     case 4: return launch_dma<256, 256, 2, 4>(act, ln, descs, tiles, n, grid, stream, occ);
     case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 8: return launch_shape<float, 32, 128, 64, 1, 4, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 7:
       if (ln) return hipErrorInvalidValue;
       return dt == OPTIMUS_F32 ? launch_skinny<float>(act, descs, tiles, n, grid, stream, occ)
