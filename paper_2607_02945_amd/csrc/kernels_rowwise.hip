@@ -12,6 +12,11 @@
 namespace optimus {
 
 // ===================================================================== LayerNorm
+#ifndef OPTIMUS_LN_DEPTH
+#define OPTIMUS_LN_DEPTH 2
+#endif
+constexpr int kLnDepth = OPTIMUS_LN_DEPTH;  // row slots loaded ahead of the one being computed
+
 // A row of one member is handled by a group of L lanes (L = power of two set
 // per member by the planner, so that L * MAXC chunks of 16 bytes cover the
 // row); a wave handles 64 / L rows at a time and the four waves of a block
@@ -55,10 +60,10 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
   }
   const int rpb = 4 * rpw;
   const int end = rt.row0 + rt.nrows;
-  // The next two row slots' chunks are loaded while the current one is
-  // computed (two deep: 8 more registers, 6 waves per SIMD instead of 7, but
-  // twice the rows in flight per wave; 1.5 % faster on 1024-wide rows).
-  u32x4 raw[MAXC], raw2[MAXC];
+  // The next kLnDepth row slots' chunks are loaded while the current one is
+  // computed (a ring of row registers, rotated by register moves).
+  constexpr int PF = kLnDepth;
+  u32x4 ring[PF][MAXC];
   auto fetch = [&](u32x4 (&dst)[MAXC], int r) {
     const char* xr = (const char*)d.x + (int64_t)r * d.ldx * sizeof(T);
 #pragma unroll
@@ -67,18 +72,19 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
       dst[j] = (r < end && c < cpr) ? ld16_nt(xr + (int64_t)c * 16) : u32x4{0u, 0u, 0u, 0u};
     }
   };
-  fetch(raw, rt.row0 + wave * rpw + sub);
-  fetch(raw2, rt.row0 + wave * rpw + sub + rpb);
+#pragma unroll
+  for (int p = 0; p < PF; ++p) fetch(ring[p], rt.row0 + wave * rpw + sub + p * rpb);
   for (int base = rt.row0; base < end; base += rpb) {
     const int r = base + wave * rpw + sub;
     const bool valid = r < end;
     float x[MAXC][VEC];
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
-      Elem<T>::unpack(raw[j], x[j]);  // zero where out of range
-      raw[j] = raw2[j];
+      Elem<T>::unpack(ring[0][j], x[j]);  // zero where out of range
+#pragma unroll
+      for (int p = 0; p + 1 < PF; ++p) ring[p][j] = ring[p + 1][j];
     }
-    if (base + 2 * rpb < end) fetch(raw2, r + 2 * rpb);
+    if (base + PF * rpb < end) fetch(ring[PF - 1], r + PF * rpb);
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j)
@@ -463,6 +469,27 @@ hipError_t pointwise_launch(optimus_dtype dt, optimus_act act, const DevRows* de
                                                stream, descs, tiles, num_tiles));
   }
   return hipGetLastError();
+}
+
+// Workgroups of the LayerNorm (or pointwise) instance for (dt, act) that the
+// runtime reports resident on one CU: persistent row grids are sized by it
+// (a grid past it leaves late workgroups to start their whole share after
+// the first ones finish).
+int rowwise_blocks_per_cu(optimus_dtype dt, optimus_act act, bool layernorm) {
+  const void* k = nullptr;
+  auto pick = [&](auto tag) -> hipError_t {
+    using T = decltype(tag);
+    OPTIMUS_ACT_SWITCH(act, k = layernorm ? (const void*)grouped_layernorm_kernel<T, A>
+                                          : (const void*)grouped_pointwise_kernel<T, A>);
+    return hipSuccess;
+  };
+  if ((dt == OPTIMUS_BF16 ? pick(bf16_t{}) : pick(float{})) != hipSuccess || !k) return 4;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kRowThreads, 0) != hipSuccess || n < 1) {
+    (void)hipGetLastError();
+    return 4;
+  }
+  return n;
 }
 
 template <typename T, int ACT, int S, int WPR, bool FULL>

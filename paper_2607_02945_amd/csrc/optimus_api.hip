@@ -418,7 +418,7 @@ static optimus_status parse_options(const optimus_plan_options* o, PlanOpts& po)
   po = PlanOpts{};
   if (!o) return OPTIMUS_OK;
   if (o->reserved != 0) return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: reserved must be 0");
-  if (o->gemm_tile < OPTIMUS_TILE_AUTO || o->gemm_tile > OPTIMUS_TILE_F32_32X128)
+  if (o->gemm_tile < OPTIMUS_TILE_AUTO || o->gemm_tile > OPTIMUS_TILE_BF16_DMA_128X64)
     return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: unknown gemm_tile %d", (int)o->gemm_tile);
   if (o->wgrad_splits < 0 || o->wgrad_splits > 16)
     return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: wgrad_splits %d outside 0..16", (int)o->wgrad_splits);
@@ -577,8 +577,12 @@ static void add_row_tiles(std::vector<RowTile>& tiles, int member, const DevRows
     tiles.push_back(RowTile{member, (int32_t)r0, (int32_t)std::min<int64_t>(per, r.rows - r0), 0});
 }
 
-static int32_t row_grid(int64_t tiles) {
-  const int64_t cap = (int64_t)device_cu_count() * 8;
+// Persistent row grid: no more workgroups than are resident at once
+// (per_cu: the kernel instance's occupancy; one past it starts late with a
+// whole share: large_group's LayerNorm + tanh took 237 us at 8 per CU
+// requested, 229 us at the 5 that fit).
+static int32_t row_grid(int64_t tiles, int per_cu) {
+  const int64_t cap = (int64_t)device_cu_count() * std::max(1, std::min(per_cu, 8));
   return (int32_t)std::max<int64_t>(1, std::min<int64_t>(tiles, cap));
 }
 
@@ -625,7 +629,9 @@ static int64_t balanced_row_segments(const std::vector<int64_t>& rows, const std
 // of about kRowTileBytes. (Balanced per-workgroup segments, as the LayerNorm
 // backward uses, measured slower here: 268 against 253 us for large_group's
 // LayerNorm + tanh. The hardware spreads the small tiles better.)
-static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool layernorm, size_t s) {
+static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool layernorm, size_t s,
+                       optimus_act act) {
+  const int per_cu = rowwise_blocks_per_cu(hp.dt, act, layernorm);
   std::vector<RowTile> tiles;
   hp.rows_chain.clear();
   for (size_t g = 0; g < members.size(); ++g) {
@@ -638,9 +644,9 @@ static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool l
   for (auto& c : hp.rows_chain) {
     c.descs_off = doff;
     c.tiles_off = toff;
-    c.grid = row_grid(c.num_tiles);
+    c.grid = row_grid(c.num_tiles, per_cu);
   }
-  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size(), per_cu)};
   hp.row_kernel = layernorm ? KIND_LN : KIND_PW;
   hp.work_items = (int64_t)tiles.size();
   hp.grid = hp.rows.grid;
@@ -775,7 +781,7 @@ static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, in
                                   const void* gamma, int64_t rows, int64_t cols, float eps, optimus_dtype dt,
                                   bool layernorm);
 static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
-                                           std::vector<int>& ntiles, int64_t max_tiles = 0);
+                                           std::vector<int>& ntiles, int64_t max_tiles, int per_cu);
 
 // act != NONE: dX leaves with the activation backward of the layer below
 // applied, dX * act'(act_x[g]) (act_x [M][K], row stride ld_act_x[g]).
@@ -959,7 +965,7 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
                                     d[g].lddx, nullptr, has ? d[g].M : 0, d[g].K, 0.f, dt, false));
       }
       std::vector<int> nt;
-      std::vector<RowTile> rt = grad_row_tiles(hp, rm, s, nt);
+      std::vector<RowTile> rt = grad_row_tiles(hp, rm, s, nt, 0, act_backward_blocks_per_cu(dt, act));
       const size_t roff = hp.blob.add(rm.data(), rm.size() * sizeof(DevRowsGrad));
       for (int g = 0; g < G; ++g)
         if (d[g].dx) hp.scratch_fixups.push_back(roff + g * sizeof(DevRowsGrad) + offsetof(DevRowsGrad, dy));
@@ -968,7 +974,8 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
         c.descs_off = roff;
         c.tiles_off = rtoff;
       }
-      hp.rows = RowLaunch{roff, rtoff, 0, (int32_t)rt.size(), row_grid((int64_t)rt.size())};
+      hp.rows = RowLaunch{roff, rtoff, 0, (int32_t)rt.size(),
+                          row_grid((int64_t)rt.size(), act_backward_blocks_per_cu(dt, act))};
     }
   }
   hp.red_chain.assign(G, RowLaunch{});
@@ -1126,7 +1133,7 @@ static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, in
 // partial row of dgamma / dbeta that the finalize reads back).
 static constexpr int64_t kGradMaxTilesPerMember = 64;
 static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
-                                           std::vector<int>& ntiles, int64_t max_tiles) {
+                                           std::vector<int>& ntiles, int64_t max_tiles, int per_cu) {
   std::vector<RowTile> tiles;
   hp.rows_chain.clear();
   ntiles.assign(members.size(), 0);
@@ -1142,7 +1149,7 @@ static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRo
       tiles.push_back(RowTile{(int)g, (int32_t)r0, (int32_t)std::min<int64_t>(per, m.rows - r0), 0});
     for (int t = first; t < (int)tiles.size(); ++t) tiles[t].pad = t - first;
     ntiles[g] = (int)tiles.size() - first;
-    hp.rows_chain.push_back(RowLaunch{0, 0, first, ntiles[g], row_grid(ntiles[g])});
+    hp.rows_chain.push_back(RowLaunch{0, 0, first, ntiles[g], row_grid(ntiles[g], per_cu)});
   }
   return tiles;
 }
@@ -1172,7 +1179,8 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
   // member has one dgamma / dbeta partial row per segment (about one per
   // workgroup that touches it), not per tile.
   std::vector<int> ntiles;
-  std::vector<RowTile> chain_tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember);
+  std::vector<RowTile> chain_tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember,
+                                                    layernorm_backward_resident_per_cu(dt, act));
   std::vector<int> nseg;
   std::vector<RowTile> tiles;
   int64_t B;
@@ -1269,14 +1277,15 @@ static optimus_status build_act_backward(const optimus_act_grad_desc* d, int32_t
     hp.bytes += (double)s * 3.0 * m.rows * m.cols;
   }
   std::vector<int> ntiles;
-  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles);
+  const int per_cu = act_backward_blocks_per_cu(dt, act);
+  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles, 0, per_cu);
   const size_t doff = hp.blob.add(members.data(), members.size() * sizeof(DevRowsGrad));
   const size_t toff = hp.blob.add(tiles.data(), tiles.size() * sizeof(RowTile));
   for (auto& c : hp.rows_chain) {
     c.descs_off = doff;
     c.tiles_off = toff;
   }
-  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size(), per_cu)};
   hp.work_items = (int64_t)tiles.size();
   hp.grid = hp.rows.grid;
   hp.block = kRowThreads;
@@ -1297,7 +1306,7 @@ static optimus_status build_layernorm(const optimus_layernorm_desc* d, int32_t G
     members.push_back(make_rows(m.x, m.ldx, m.y, m.ldy, m.gamma, m.beta, m.rows, m.cols, m.eps, dt, true));
     hp.bytes += (double)s * (2.0 * m.rows * m.cols + (m.gamma ? m.cols : 0) + (m.beta ? m.cols : 0));
   }
-  build_rows(hp, members, true, s);
+  build_rows(hp, members, true, s, act);
   hp.kernel = dt == OPTIMUS_F32 ? "grouped_layernorm_f32" : "grouped_layernorm_bf16";
   return OPTIMUS_OK;
 }
@@ -1325,7 +1334,7 @@ static optimus_status build_pointwise(const optimus_pointwise_desc* d, int32_t G
     members.push_back(make_rows(m.x, cols, m.y, cols, nullptr, nullptr, rows, cols, 0.f, dt, false));
     hp.bytes += (double)s * 2.0 * m.rows * m.cols;
   }
-  build_rows(hp, members, false, s);
+  build_rows(hp, members, false, s, act);
   hp.kernel = dt == OPTIMUS_F32 ? "grouped_pointwise_f32" : "grouped_pointwise_bf16";
   return OPTIMUS_OK;
 }
@@ -1354,7 +1363,7 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
   if (!d->apply_layernorm) {
     // same activation on every piece: split and concat vanish into one pointwise pass over [rows, D]
     std::vector<DevRows> m{make_rows(d->in, d->ldin, d->out, d->ldout, nullptr, nullptr, rows, D, 0.f, dt, false)};
-    build_rows(hp, m, false, s);
+    build_rows(hp, m, false, s, d->act);
     hp.row_act = d->act;
     hp.kernel = "split_op_cat_as_pointwise";
   } else if (vec && nchunks <= kSocMaxChunks && n <= kSocMaxPieces && n <= kSocMaxTasks) {
@@ -1419,7 +1428,7 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
       m.push_back(make_rows((const char*)d->in + off[j] * s, d->ldin, (char*)d->out + off[j] * s, d->ldout,
                             d->gamma ? d->gamma[j] : nullptr, d->beta ? d->beta[j] : nullptr, rows, d->widths[j],
                             d->eps, dt, true));
-    build_rows(hp, m, true, s);
+    build_rows(hp, m, true, s, d->act);
     hp.row_act = d->act;
     hp.kernel = "split_op_cat_as_grouped_layernorm";
   }
@@ -2006,26 +2015,32 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
   const int n = hp.G;
   hipError_t e = hipSuccess;
   if (mode == OPTIMUS_EXEC_HORIZONTAL) {
-    const int32_t T = hp.soc_piece_tiles_total, grid = row_grid(T);
+    const int ln_cu = rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, ln_on);
+    const int32_t T = hp.soc_piece_tiles_total, grid = row_grid(T, ln_cu);
     e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tl, T, grid, st)
               : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tl, T, grid, st);
-    if (e == hipSuccess) e = pointwise_launch(hp.dt, hp.act, act, tl, T, grid, st);
-    if (e == hipSuccess) e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, grid, st);
+    const int32_t pgrid = row_grid(T, rowwise_blocks_per_cu(hp.dt, hp.act, false));
+    const int32_t cgrid = row_grid(T, rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, false));
+    if (e == hipSuccess) e = pointwise_launch(hp.dt, hp.act, act, tl, T, pgrid, st);
+    if (e == hipSuccess) e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, cgrid, st);
   } else {
+    const int ln_cu = rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, ln_on);
+    const int pw_cu = rowwise_blocks_per_cu(hp.dt, hp.act, false);
+    const int cat_cu = rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, false);
     for (int j = 0; j < n && e == hipSuccess; ++j) {
       const RowTile* tj = tl + hp.soc_piece_first[j];
       const int32_t cnt = hp.soc_piece_count[j];
-      e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt), st)
-                : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt), st);
+      e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt, ln_cu), st)
+                : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt, ln_cu), st);
     }
     for (int j = 0; j < n && e == hipSuccess; ++j) {
       const RowTile* tj = tl + hp.soc_piece_first[j];
       const int32_t cnt = hp.soc_piece_count[j];
-      e = pointwise_launch(hp.dt, hp.act, act, tj, cnt, row_grid(cnt), st);
+      e = pointwise_launch(hp.dt, hp.act, act, tj, cnt, row_grid(cnt, pw_cu), st);
     }
     if (e == hipSuccess) {
       const int32_t T = hp.soc_piece_tiles_total;
-      e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, row_grid(T), st);
+      e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, row_grid(T, cat_cu), st);
     }
   }
   return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "execute: split-op-cat unfused launch");
