@@ -1536,7 +1536,6 @@ static const GemmVariant kVariants[] = {
     {64, 128, 256, 1, "grouped_gemm_f32_64x128x64_w2x2_s2"},
     {kSkinnyRows, kSkinnyMax, 256, 4, "grouped_gemm_skinny"},
     {32, 128, 256, 2, "grouped_gemm_f32_32x128x64_w1x4_s2"},
-    {128, 64, 256, 3, "grouped_gemm_dma_bf16_128x64x64_w4x1"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
 
@@ -1602,8 +1601,7 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     else if ((dt == OPTIMUS_F32) != (pin == 3 || pin == 6 || pin == 8))
       ok = false;
     else
-      ok = (dt == OPTIMUS_F32 || pin < 4 || ((pin == 4 || pin == 5 || pin == 9) && dma)) &&
-           (!ln || kVariants[pin].bn >= maxN);
+      ok = (dt == OPTIMUS_F32 || pin < 4 || dma) && (!ln || kVariants[pin].bn >= maxN);
     if (!ok) return GemmConfig{0, 0, -1, 0, 0, "unsupported"};
     v = pin;
   } else if (skinny) {
@@ -1769,7 +1767,6 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
     case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 8: return launch_shape<float, 32, 128, 64, 1, 4, 2>(act, ln, descs, tiles, n, grid, stream, occ);
-    case 9: return launch_dma<128, 64, 4, 1>(act, ln, descs, tiles, n, grid, stream, occ);
     case 7:
       if (ln) return hipErrorInvalidValue;
       return dt == OPTIMUS_F32 ? launch_skinny<float>(act, descs, tiles, n, grid, stream, occ)
