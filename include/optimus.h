@@ -441,7 +441,8 @@ typedef enum {
   OPTIMUS_TILE_BF16_DMA_128X128 = 6, /* direct-to-LDS loads, 4 waves */
   OPTIMUS_TILE_F32_64X128 = 7,
   OPTIMUS_TILE_SKINNY = 8,           /* every K and N <= 8: streaming, no MFMA */
-  OPTIMUS_TILE_F32_32X128 = 9        /* 4 waves across the 128 columns */
+  OPTIMUS_TILE_F32_32X128 = 9,       /* 4 waves across the 128 columns */
+  OPTIMUS_TILE_BF16_STREAM = 10      /* every K, N <= 64 (multiples of 8, aligned rows): 512-row streams */
 } optimus_gemm_tile;
 
 typedef struct {

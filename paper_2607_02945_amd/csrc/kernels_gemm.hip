@@ -1163,6 +1163,135 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_dma_kernel(const Dev
   }
 }
 
+// ===================================================================== streaming members
+// Every member has K <= 64 and N <= 64 values (bf16, N and K multiples of 8,
+// 16-byte aligned rows): a member's whole weight is one K step of at most
+// 64 x 64, so a tile's work is its x rows in and its y rows out -- a
+// streaming pass over the batch rather than a tiled contraction. A work item
+// is kStreamRows rows of one member. The block stages the member's weight
+// and bias in LDS once per item (the MFMA A operand is w,
+// v_mfma_f32_32x32x16_bf16, so a lane ends with four consecutive columns of
+// one row); each wave then walks 32-row slabs of the item: a slab's x rows
+// are loaded whole (coalesced 16-byte pieces: loading them straight into
+// the MFMA B layout, 32 rows x 32 bytes per instruction, was 30 % slower)
+// and turned into B operands through the wave's own LDS slice, the loads of
+// the next two slabs are in flight while the current slab is multiplied and
+// stored, and the result leaves through the same slice in whole 16-byte
+// pieces of rows. Within an item the waves never wait for each other.
+constexpr int kStreamRows = 512;  // 4 waves x 4 slabs of 32 rows (256: +1 %, 1024: +10 %)
+constexpr int kStreamPitch = 144; // staged row bytes: 64 bf16 + 16 (distinct bank groups for the 8-row passes)
+constexpr int kStreamWave = 32 * kStreamPitch;             // a wave's staging slice
+constexpr int kStreamW = 4 * kStreamWave;                  // then the weight [64][kStreamPitch] and fp32 bias [64]
+constexpr size_t kStreamLds = kStreamW + 64 * kStreamPitch + 64 * sizeof(float);
+
+template <int ACT>
+__global__ __launch_bounds__(256, 4) void grouped_gemm_stream_kernel(const DevLinear* __restrict__ descs,
+                                                                     const GemmTile* __restrict__ tiles,
+                                                                     int32_t num_tiles) {
+  extern __shared__ __align__(16) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, lh = lane >> 5;
+  char* stg = smem + wave * kStreamWave;
+  char* sw = smem + kStreamW;                           // w rows n, 64 k values each (zero past N, K)
+  float* sbias = (float*)(sw + 64 * kStreamPitch);
+  for (int t = blockIdx.x; t < num_tiles; t += gridDim.x) {
+    const GemmTile tile = tiles[t];
+    if (tile.member < 0) continue;
+    const DevLinear& d = descs[tile.member];
+    const int KC = (d.K + 15) >> 4, NB = (d.N + 31) >> 5;
+    const int row0 = tile.mb * kStreamRows;
+    const int rows = min(kStreamRows, d.M - row0);
+    const int nslab = (rows + 31) >> 5;
+    const bf16_t* xb = (const bf16_t*)d.x + (int64_t)row0 * d.ldx;
+    // a slab's x rows in whole-row order: load i of lane l is 16-byte chunk
+    // (l + 64 i) % 8 of slab row (l + 64 i) / 8
+    auto xload = [&](int sl, u32x4 (&b)[4]) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int idx = lane + 64 * i, r = sl * 32 + (idx >> 3), c = idx & 7;
+        b[i] = (r < rows && 8 * c < d.K) ? ld16_nt(xb + (int64_t)r * d.ldx + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+      }
+    };
+    // the first slab's x loads go out first, then the block's weight and bias
+    // two slabs ahead in flight (2.5 % faster than one)
+    u32x4 bx[4], bn[4], bn2[4];
+    if (wave + 4 < nslab) xload(wave + 4, bn);
+    if (wave < nslab) xload(wave, bx);
+    __syncthreads();  // every wave is done with the previous item's weight and bias
+    {
+      // 64 rows x 8 chunks of 16 bytes, two per thread
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int idx = tid + 256 * i, n = idx >> 3, c = idx & 7;
+        const u32x4 v = (n < d.N && 8 * c < d.K) ? ld16((const bf16_t*)d.w + (int64_t)n * d.ldw + 8 * c)
+                                                 : u32x4{0u, 0u, 0u, 0u};
+        *(u32x4*)(sw + n * kStreamPitch + 16 * c) = v;
+      }
+      if (tid < 64) sbias[tid] = (d.bias && tid < d.N) ? Elem<bf16_t>::load1(d.bias, tid) : 0.f;
+    }
+    __syncthreads();
+    for (int sl = wave; sl < nslab; sl += 4) {
+      if (sl + 8 < nslab) xload(sl + 8, bn2);
+      // the slab through this wave's LDS slice into the MFMA B layout
+      // (lane l: row l % 32, k values 16 kc + 8 (l / 32), + 8)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int idx = lane + 64 * i;
+        *(u32x4*)(stg + (idx >> 3) * kStreamPitch + 16 * (idx & 7)) = bx[i];
+      }
+      lds_wave_sync();
+      u32x4 xf[4];
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) xf[kc] = *(const u32x4*)(stg + l32 * kStreamPitch + 32 * kc + 16 * lh);
+      f32x16 acc[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) {
+        if (kc < KC) {
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            if (j < NB) {
+              // A operand: w[32 j + l32][16 kc + 8 lh, + 8)
+              const u32x4 a = *(const u32x4*)(sw + (32 * j + l32) * kStreamPitch + 32 * kc + 16 * lh);
+              Mfma<bf16_t>::run(a, xf[kc], acc[j]);
+            }
+        }
+      }
+      // bias + activation + rounding into this wave's staging slice: lane
+      // (l32, lh) holds row l32, columns 32 j + 8 q + 4 lh + (0..3)
+      char* put = stg + l32 * kStreamPitch + lh * 8;
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 bv = *(const f32x4*)(sbias + 32 * j + 8 * q + 4 * lh);
+          const float o0 = act_apply<ACT>(acc[j][q * 4 + 0] + bv.x), o1 = act_apply<ACT>(acc[j][q * 4 + 1] + bv.y);
+          const float o2 = act_apply<ACT>(acc[j][q * 4 + 2] + bv.z), o3 = act_apply<ACT>(acc[j][q * 4 + 3] + bv.w);
+          *(u32x2*)(put + (32 * j + 8 * q) * 2) = u32x2{pack_bf16x2(o0, o1), pack_bf16x2(o2, o3)};
+        }
+      lds_wave_sync();
+      // whole 16-byte pieces of rows: lane -> row (lane / 8) + 8 p, piece lane % 8
+      const int pr = lane >> 3, pc = lane & 7;
+      bf16_t* yb = (bf16_t*)d.y + (int64_t)(row0 + sl * 32 + pr) * d.ldy + pc * 8;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int r = sl * 32 + p * 8 + pr;
+        const u32x4 v = *(const u32x4*)(stg + (p * 8 + pr) * kStreamPitch + pc * 16);
+        if (r < rows && pc * 8 < d.N) st16_nt(yb + (int64_t)(p * 8) * d.ldy, v);
+      }
+      lds_wave_sync();  // staging read before the next slab overwrites it
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) {
+        bx[kc] = bn[kc];
+        bn[kc] = bn2[kc];
+      }
+    }
+  }
+}
+
 // ===================================================================== skinny members
 // Every member has K <= 8 and N <= 8: a tall-skinny matrix product such as
 // [2e7, 8] x [8, 8], which the paper's decompose_mm rewrite (appendix Sec. 8.2)
@@ -1525,7 +1654,8 @@ struct GemmVariant {
 // 256x256 8 waves, 128x128 4 waves; 6: fp32 64x128 (a fused LayerNorm over
 // fp32 rows of 65 to 128 columns); 7: skinny members (every K, N <= 8), fp32 or
 // bf16, streamed with no MFMA; 8: fp32 32x128, 4 waves across the columns
-// (groups with fewer 64-row tiles than CUs).
+// (groups with fewer 64-row tiles than CUs); 9: streaming bf16 members
+// (every K, N <= 64, multiples of 8, aligned rows; no fused LayerNorm).
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
     {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
@@ -1536,8 +1666,20 @@ static const GemmVariant kVariants[] = {
     {64, 128, 256, 1, "grouped_gemm_f32_64x128x64_w2x2_s2"},
     {kSkinnyRows, kSkinnyMax, 256, 4, "grouped_gemm_skinny"},
     {32, 128, 256, 2, "grouped_gemm_f32_32x128x64_w1x4_s2"},
+    {kStreamRows, 64, 256, 8, "grouped_gemm_stream_bf16"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
+
+// The streaming kernel: bf16 members with K, N <= 64 values, both multiples
+// of 8, and 16-byte aligned x, w, y rows.
+static bool gemm_stream_ok(const optimus_linear_desc* d, int32_t G) {
+  for (int g = 0; g < G; ++g) {
+    if (d[g].K > 64 || d[g].N > 64 || d[g].K % 8 || d[g].N % 8 || d[g].ldx % 8 || d[g].ldw % 8 || d[g].ldy % 8 ||
+        ((uintptr_t)d[g].x & 15) || ((uintptr_t)d[g].w & 15) || ((uintptr_t)d[g].y & 15))
+      return false;
+  }
+  return true;
+}
 
 // The direct-to-LDS kernels address a tile of at most 256 rows through 32-bit
 // buffer offsets below 2^31 (larger offsets mark out-of-range chunks).
@@ -1598,6 +1740,8 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
       ok = false;
     else if (pin == 7)
       ok = skinny;
+    else if (pin == 9)
+      ok = dt == OPTIMUS_BF16 && !ln && gemm_stream_ok(d, G);
     else if ((dt == OPTIMUS_F32) != (pin == 3 || pin == 6 || pin == 8))
       ok = false;
     else
@@ -1616,7 +1760,7 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     for (int g = 0; g < G; ++g) tiles64 += (double)((d[g].M + 63) / 64) * (double)((d[g].N + 127) / 128);
     if (maxN > 64 && maxN <= 128 && tiles64 < device_cu_count()) v = 8;
   } else if (maxN <= 64 && maxK <= 64) {
-    v = 0;
+    v = (!ln && gemm_stream_ok(d, G)) ? 9 : 0;
   } else if (tiles256 >= 0.5 * device_cu_count() || (ln && maxN > 128)) {
     // measured over groups of 64 to 4096 256x256 tiles: the 256x256 tile wins
     // from half a tile per CU on (and is the one that holds rows past 128)
@@ -1653,6 +1797,20 @@ static hipError_t resident_of(const void* kfn, int threads, size_t smem, int* ou
     if (occ) return resident_of((const void*)kfn, (NT), (SMEM), occ);                                              \
     hipLaunchKernelGGL(kfn, dim3(grid), dim3(NT), (SMEM), stream, descs, tiles, n);                                \
   }
+
+static hipError_t launch_stream(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n,
+                                int32_t grid, hipStream_t stream, int* occ) {
+  constexpr size_t smem = kStreamLds;
+  switch (act) {
+    case OPTIMUS_ACT_NONE: OPTIMUS_LAUNCH_ONE((grouped_gemm_stream_kernel<0>), smem, 256); break;
+    case OPTIMUS_ACT_RELU: OPTIMUS_LAUNCH_ONE((grouped_gemm_stream_kernel<1>), smem, 256); break;
+    case OPTIMUS_ACT_SIGMOID: OPTIMUS_LAUNCH_ONE((grouped_gemm_stream_kernel<2>), smem, 256); break;
+    case OPTIMUS_ACT_TANH: OPTIMUS_LAUNCH_ONE((grouped_gemm_stream_kernel<3>), smem, 256); break;
+    case OPTIMUS_ACT_SILU: OPTIMUS_LAUNCH_ONE((grouped_gemm_stream_kernel<4>), smem, 256); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 template <typename T>
 static hipError_t launch_skinny(optimus_act act, const DevLinear* descs, const GemmTile* tiles, int32_t n,
@@ -1767,6 +1925,9 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
     case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 8: return launch_shape<float, 32, 128, 64, 1, 4, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 9:
+      if (ln || dt != OPTIMUS_BF16) return hipErrorInvalidValue;
+      return launch_stream(act, descs, tiles, n, grid, stream, occ);
     case 7:
       if (ln) return hipErrorInvalidValue;
       return dt == OPTIMUS_F32 ? launch_skinny<float>(act, descs, tiles, n, grid, stream, occ)

@@ -249,3 +249,49 @@ def test_direct_to_lds_tiles_every_element_multi_tile(variant):
     torch.cuda.synchronize()
     p.close()
     _check(ms, ys, "bf16", "silu", f"variant {variant} multi-tile")
+
+
+@pytest.mark.parametrize("act", ACTS)
+def test_streaming_small_members(act):
+    """Members with K, N <= 64 (multiples of 8) on the streaming kernel (the
+    planner's choice for such bf16 groups): ragged batches (1, tails inside a
+    32-row slab and a 512-row item, several items), every K and N class, a
+    member without bias; grouped and chain; every element against the oracle."""
+    say(f"[linear streaming] {act}")
+    shapes = [(1, 8, 8), (33, 16, 24), (511, 64, 64), (513, 48, 40), (1000, 24, 16), (2048, 56, 48), (70, 64, 8)]
+    ms = _members(shapes, "bf16", seed=130)
+    ms[1] = (ms[1][0], ms[1][1], None)
+    for mode in ["grouped", "chain"]:
+        xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
+        ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, _ in ms]
+        p = B.optimus_plan_linear(xs, ws, bs, ys, act)
+        assert p.info()["kernel"] == "grouped_gemm_stream_bf16", p.info()
+        p.execute(mode)
+        torch.cuda.synchronize()
+        p.close()
+        _check(ms, ys, "bf16", act, f"streaming {mode}")
+
+
+def test_streaming_strided_and_fallback():
+    """Row strides above the row lengths keep the streaming kernel (16-byte
+    aligned rows); a member with K not a multiple of 8 sends the group to the
+    register-staged 128x64 tile; both against the oracle."""
+    say("[linear streaming strided / fallback]")
+    g = synth.rng(131)
+    x = dev(synth.to_storage(g.standard_normal((300, 72)), "bf16"))[:, 8:40]        # K = 32, ld 72
+    w = dev(synth.to_storage(g.standard_normal((48, 40)) / 6, "bf16"))[:, :32]      # N = 48, ld 40
+    b = dev(synth.to_storage(g.standard_normal(48) * 0.1, "bf16"))
+    ybuf = torch.full((300, 56), float("nan"), dtype=torch.bfloat16, device="cuda")
+    y = ybuf[:, :48]                                                                  # ld 56
+    p = B.optimus_plan_linear([x], [w], [b], [y], "tanh")
+    assert p.info()["kernel"] == "grouped_gemm_stream_bf16", p.info()
+    p.execute()
+    torch.cuda.synchronize()
+    _check([(x, w, b)], [y], "bf16", "tanh", "streaming strided")
+    ms = _members([(400, 32, 32), (200, 16, 12)], "bf16", seed=132)
+    ys = [torch.full((m[0].shape[0], m[1].shape[0]), float("nan"), dtype=torch.bfloat16, device="cuda") for m in ms]
+    p = B.optimus_plan_linear([m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms], ys, "relu")
+    assert p.info()["kernel"].startswith("grouped_gemm_bf16_128x64"), p.info()
+    p.execute()
+    torch.cuda.synchronize()
+    _check(ms, ys, "bf16", "relu", "K not a multiple of 8")
