@@ -101,6 +101,26 @@ __device__ __forceinline__ float chunk_sum<float>(const u32x4& c) {
   return (f[0] + f[1]) + (f[2] + f[3]);
 }
 
+// Sum of the squares of one chunk's values in fp32 (bf16: v_dot2 of each
+// packed pair with itself; the products of two bf16 values are exact in fp32).
+template <typename T>
+__device__ __forceinline__ float chunk_sumsq(const u32x4& c);
+template <>
+__device__ __forceinline__ float chunk_sumsq<bf16_t>(const u32x4& c) {
+  const bf16x8 v = __builtin_bit_cast(bf16x8, c);
+  const bf16x2 p0 = __builtin_shufflevector(v, v, 0, 1), p1 = __builtin_shufflevector(v, v, 2, 3);
+  const bf16x2 p2 = __builtin_shufflevector(v, v, 4, 5), p3 = __builtin_shufflevector(v, v, 6, 7);
+  float a = __builtin_amdgcn_fdot2_f32_bf16(p0, p0, 0.f, false);
+  a = __builtin_amdgcn_fdot2_f32_bf16(p1, p1, a, false);
+  a = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, a, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(p3, p3, a, false);
+}
+template <>
+__device__ __forceinline__ float chunk_sumsq<float>(const u32x4& c) {
+  const f32x4 f = __builtin_bit_cast(f32x4, c);
+  return __builtin_fmaf(f[0], f[0], f[1] * f[1]) + __builtin_fmaf(f[2], f[2], f[3] * f[3]);
+}
+
 // ------------------------------------------------------------------ activations
 // exp via the hardware base-2 exponential; reciprocal via the hardware
 // approximate reciprocal (1 ulp). Large |x| saturates correctly: e^x -> inf
@@ -125,12 +145,16 @@ __device__ __forceinline__ float act_apply(float x) {
 }
 
 // The activations whose exponent argument is a fixed multiple of the input
-// (sigmoid: 2^(-x log2 e); tanh: 2^(2 x log2 e)) can take that product
-// directly: act_in_scale is the multiple (1 for the others) and
-// act_scaled_in(u) = act_apply(u / act_in_scale).
+// (sigmoid and silu: 2^(-x log2 e); tanh: 2^(2 x log2 e)) can take that
+// product directly: act_in_scale is the multiple (1 for the others) and
+// act_scaled_in(u) = act_apply(u / act_in_scale). For silu,
+// x / (1 + e^-x) = u / ((1 + 2^u) * (-log2 e)) with u = -x log2 e, so the
+// scale goes into the denominator's fma.
 template <int ACT>
 __device__ __forceinline__ constexpr float act_in_scale() {
-  return ACT == OPTIMUS_ACT_SIGMOID ? -1.4426950408889634f : ACT == OPTIMUS_ACT_TANH ? 2.8853900817779268f : 1.f;
+  return ACT == OPTIMUS_ACT_SIGMOID || ACT == OPTIMUS_ACT_SILU ? -1.4426950408889634f
+         : ACT == OPTIMUS_ACT_TANH                            ? 2.8853900817779268f
+                                                              : 1.f;
 }
 template <int ACT>
 __device__ __forceinline__ float act_scaled_in(float u) {
@@ -138,9 +162,29 @@ __device__ __forceinline__ float act_scaled_in(float u) {
     return fast_rcp(1.f + __builtin_amdgcn_exp2f(u));
   } else if constexpr (ACT == OPTIMUS_ACT_TANH) {
     return 1.f - 2.f * fast_rcp(__builtin_amdgcn_exp2f(u) + 1.f);
+  } else if constexpr (ACT == OPTIMUS_ACT_SILU) {
+    return u * fast_rcp(__builtin_fmaf(__builtin_amdgcn_exp2f(u), -1.4426950408889634f, -1.4426950408889634f));
   } else {
     return act_apply<ACT>(u);
   }
+}
+
+// d[e] = x[e] - m for the values of one chunk, in fp32.
+template <typename T>
+__device__ __forceinline__ void centred(const u32x4& c, float m, float* d);
+template <>
+__device__ __forceinline__ void centred<bf16_t>(const u32x4& c, float m, float* d) {
+  Elem<bf16_t>::unpack(c, d);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) d[e] -= m;
+}
+template <>
+__device__ __forceinline__ void centred<float>(const u32x4& c, float m, float* d) {
+  const f32x4 f = __builtin_bit_cast(f32x4, c);
+  d[0] = f[0] - m;
+  d[1] = f[1] - m;
+  d[2] = f[2] - m;
+  d[3] = f[3] - m;
 }
 
 // Derivative of one activation at its input, in the same hardware

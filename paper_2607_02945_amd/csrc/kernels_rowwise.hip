@@ -32,9 +32,10 @@ __device__ __forceinline__ void ln_rows_vec(const DevRows& d, const RowTile& rt,
   const int sub = lane / L;
   const int li = lane & (L - 1);
   const int cpr = d.cols / VEC;
-  // gamma / beta unpacked once per tile into fp32 registers; for sigmoid and
-  // tanh they also carry the activation's input scale (act_scaled_in), so
-  // that the affine step yields the exponent's argument directly
+  // gamma / beta unpacked once per tile into fp32 registers; for sigmoid,
+  // silu and tanh they also carry the activation's input scale
+  // (act_scaled_in), so that the affine step yields the exponent's argument
+  // directly
   constexpr float ks = act_in_scale<ACT>();
   float gf[MAXC][VEC], bf[MAXC][VEC];
 #pragma unroll
@@ -217,23 +218,28 @@ __global__ __launch_bounds__(kRowThreads) void grouped_pointwise_kernel(const De
 // and the concat are index arithmetic only. The next row is loaded while the
 // current one is computed.
 //
-// Piece statistics (two passes: sums, then centred squares): the chunk
-// partials of a row go to an LDS array in row order; each of the row's
-// 64 WPR lanes reads back the run of S consecutive chunks starting at chunk
-// (its index in the row) * S, adds them up piece by piece in registers, and
-// adds each piece's run total into that piece's LDS accumulator (ds_add_f32;
-// a piece spanning several lanes gets one add per lane). The lanes that own a
-// piece then turn its sum into the mean (or the centred sum of squares into
-// 1/sqrt(var + eps)) in place, and every chunk reads its piece's statistic
-// back. With one wave per row the row's LDS traffic is private to the wave and
-// needs no workgroup barrier. Piece gamma and beta are gathered from each
-// piece's own arrays and staged once per block in LDS as fp32.
+// Piece statistics take one pass: every chunk contributes its sum and its sum
+// of squares (fp32), written to LDS in row order. Each of the row's 64 WPR
+// lanes then adds up the run of S consecutive chunks starting at chunk
+// (its index in the row) * S, piece by piece: a piece that starts and ends
+// inside the run gets its total written to the piece's slot, and the run's
+// first and last segments are written back over the run's first two entries.
+// The lane that owns a piece then adds, in a fixed order, the segments of
+// the runs the piece spans, so the statistics do not depend on timing. The
+// variance is E[x^2] - mean^2; where that would lose accuracy (a piece whose
+// squared mean exceeds 16 times its variance) the row recomputes the
+// variance from the centred values in a second pass. With one wave per row
+// the row's LDS traffic is private to the wave and needs no workgroup
+// barrier. Piece gamma and beta are gathered from each piece's own arrays
+// and staged once per block in LDS as fp32, times the activation's input
+// scale (act_scaled_in).
 template <typename T, int ACT, int S, int WPR, bool FULL>
 __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc* __restrict__ sp) {
   constexpr int VEC = Elem<T>::VEC;
   constexpr int PACKS = (S + 3) / 4;    // piece ids packed four per register
   constexpr int SLOTS = 4 / WPR;        // rows in flight per block
   constexpr int RL = 64 * WPR;          // lanes per row
+  constexpr int PL = S > 1 ? 1 : 0;     // where a run keeps its last segment
   extern __shared__ __align__(16) char smem[];
   const DevSoc s = *sp;
   // wave, slot and part are uniform across a wave: keep them (and row addresses) scalar
@@ -241,11 +247,16 @@ __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc*
   const int slot = wave / WPR, wr = wave % WPR;
   // FULL: the row is exactly RL * S chunks, so no chunk needs a range check
   const int nch = FULL ? RL * S : s.nchunks, npc = s.n_pieces;
-  // LDS: gamma [nch * VEC] f32 | beta [nch * VEC] f32 | part [SLOTS][RL * S] f32 | stat [SLOTS][2][npc] f32
+  // LDS: gamma [nch * VEC] f32 | beta [nch * VEC] f32 | per slot: part [RL * S] (sum, sum of squares),
+  // acc [2][npc] f32 (piece sums -> mean, squares -> 1/sqrt(var + eps)), flag
+  const int slot_floats = 2 * RL * S + ((2 * npc + 4) & ~3);
   float* lg = (float*)smem;
   float* lb = lg + (size_t)nch * VEC;
-  float* part = lb + (size_t)nch * VEC + slot * (RL * S);
-  float* stat = lb + (size_t)nch * VEC + SLOTS * (RL * S) + slot * 2 * npc;
+  float2* part = (float2*)(lb + (size_t)nch * VEC + slot * slot_floats);
+  float* acc = (float*)(part + RL * S);
+  // one flag per row with one wave per row; one per block otherwise, so every
+  // wave of the block takes the same branch (its barriers are block-wide)
+  int* flag = (int*)(lb + (size_t)nch * VEC + (WPR == 1 ? slot : 0) * slot_floats + 2 * RL * S + 2 * npc);
   // each chunk's gamma / beta values from its piece's own arrays (read on
   // every launch, so the caller may update them between launches)
   for (int c = threadIdx.x; c < nch; c += kSocThreads) {
@@ -264,10 +275,11 @@ __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc*
 #pragma unroll
       for (int e = 0; e < VEC; ++e) b[e] = pc.beta ? Elem<T>::load1(pc.beta, e0 + e) : 0.f;
     }
+    constexpr float ks = act_in_scale<ACT>();
 #pragma unroll
     for (int e = 0; e < VEC; e += 4) {
-      *(f32x4*)(lg + (size_t)c * VEC + e) = f32x4{g[e], g[e + 1], g[e + 2], g[e + 3]};
-      *(f32x4*)(lb + (size_t)c * VEC + e) = f32x4{b[e], b[e + 1], b[e + 2], b[e + 3]};
+      *(f32x4*)(lg + (size_t)c * VEC + e) = f32x4{g[e] * ks, g[e + 1] * ks, g[e + 2] * ks, g[e + 3] * ks};
+      *(f32x4*)(lb + (size_t)c * VEC + e) = f32x4{b[e] * ks, b[e + 1] * ks, b[e + 2] * ks, b[e + 3] * ks};
     }
   }
   __syncthreads();
@@ -294,50 +306,88 @@ __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc*
     rp[j >> 2] |= (uint32_t)(cr < nch ? s.chunk_piece[cr] : 0) << (8 * (j & 3));
   }
   auto piece_of = [](const uint32_t* pk, int j) { return (int)((pk[j >> 2] >> (8 * (j & 3))) & 0xffu); };
-  // the pieces this lane finalises: ls, ls + RL (n_pieces <= 128)
-  const float iw0 = ls < npc ? s.pieces[ls].inv_width : 0.f;
-  const float iw1 = ls + RL < npc ? s.pieces[ls + RL].inv_width : 0.f;
 
-  // Reduce per-chunk partials t[] of the slot's row into per-piece accumulators acc[] (LDS).
-  auto piece_reduce = [&](const float* t, float* acc) {
-#pragma unroll
-    for (int j = 0; j < S; ++j) {
-      const int c = cbase + j * 64 + lane;
-      if (FULL || c < nch) part[c] = t[j];
+  // The pieces this lane owns (ls, ls + RL; n_pieces <= 2 RL) and where their
+  // totals come from: kind 1 = the first segment of run l0, 2 = its last
+  // segment, 3 = a piece inside run l0 (its own slot), 0 = the last segment
+  // of run l0 plus the first segments of runs l0 + 1 .. l1.
+  struct Owned {
+    int p, l0, l1, kind;
+    float w, iw;  // width in values, and its reciprocal
+  };
+  auto owned = [&](int p) {
+    Owned o{p, 0, -1, 0, 1.f, 0.f};
+    if (p < npc) {
+      const SocPiece q = s.pieces[p];
+      o.w = (float)((q.c1 - q.c0) * VEC);
+      o.iw = q.inv_width;
+      o.l0 = q.c0 / S;
+      o.l1 = (q.c1 - 1) / S;
+      if (o.l0 == o.l1) {
+        const int rs = o.l0 * S, re = min(rs + S, nch);
+        o.kind = q.c0 == rs ? 1 : q.c1 == re ? 2 : 3;
+      }
     }
-    row_sync();
+    return o;
+  };
+  const Owned own0 = owned(ls), own1 = owned(ls + RL);
+  auto total = [&](const Owned& o, const float* ix, const float* iy) -> float2 {
+    if (o.kind == 1) return part[o.l0 * S];
+    if (o.kind == 2) return part[o.l0 * S + PL];
+    if (o.kind == 3) return float2{ix[o.p], iy ? iy[o.p] : 0.f};
+    float2 v = part[o.l0 * S + PL];
+    for (int l = o.l0 + 1; l <= o.l1; ++l) {
+      const float2 f = part[l * S];
+      v.x += f.x;
+      v.y += f.y;
+    }
+    return v;
+  };
+
+  // Per-piece totals of the row's chunk pairs in part[] (see above): pieces
+  // inside a run go to ix[p] (and iy[p] unless iy is null).
+  auto run_reduce = [&](float* ix, float* iy) {
     if (run0 < nch) {
-      float run[S];
-      if constexpr (S % 4 == 0) {
+      float2 run[S];
 #pragma unroll
-        for (int k = 0; k < S / 4; ++k) {
-          const f32x4 v = *(const f32x4*)(part + run0 + 4 * k);
-          run[4 * k + 0] = v[0];
-          run[4 * k + 1] = v[1];
-          run[4 * k + 2] = v[2];
-          run[4 * k + 3] = v[3];
+      for (int i = 0; i < S; i += 2) {
+        if constexpr (S > 1) {
+          const f32x4 v = *(const f32x4*)(part + run0 + i);
+          run[i] = float2{v[0], v[1]};
+          run[i + 1] = float2{v[2], v[3]};
+        } else {
+          run[i] = part[run0 + i];
         }
-      } else {
-#pragma unroll
-        for (int i = 0; i < S; ++i) run[i] = part[run0 + i];
       }
       int cur = piece_of(rp, 0);
-      float a = 0.f;
+      float2 a{0.f, 0.f}, first{0.f, 0.f};
+      bool in_first = true;
 #pragma unroll
       for (int i = 0; i < S; ++i) {
         if (FULL || run0 + i < nch) {
           const int p = piece_of(rp, i);
           if (p != cur) {
-            atomicAdd(&acc[cur], a);
-            a = 0.f;
+            if (in_first) {
+              first = a;
+              in_first = false;
+            } else {
+              ix[cur] = a.x;
+              if (iy) iy[cur] = a.y;
+            }
+            a = float2{0.f, 0.f};
             cur = p;
           }
-          a += run[i];
+          a.x += run[i].x;
+          a.y += run[i].y;
         }
       }
-      atomicAdd(&acc[cur], a);
+      if (in_first) first = a;
+      if constexpr (PL) {
+        *(f32x4*)(part + run0) = f32x4{first.x, first.y, a.x, a.y};
+      } else {
+        part[run0] = a;
+      }
     }
-    row_sync();
   };
 
   u32x4 raw[S];
@@ -363,61 +413,87 @@ __global__ __launch_bounds__(kSocThreads) void split_op_cat_kernel(const DevSoc*
     if (row + row_step < s.rows) fetch(row + row_step);
     char* yr = (char*)s.out + (int64_t)row * s.ldout * sizeof(T);
     if (s.apply_ln) {
-      float t[S];
-      // pass 1: piece means
-      for (int p = ls; p < 2 * npc; p += RL) stat[p] = 0.f;
-#pragma unroll
-      for (int j = 0; j < S; ++j) t[j] = chunk_sum<T>(cur[j]);
-      piece_reduce(t, stat);
-      if (ls < npc) stat[ls] *= iw0;
-      if (ls + RL < npc) stat[ls + RL] *= iw1;
-      row_sync();
-      // pass 2: centred squares -> 1/sqrt(var + eps) (the centred values are
-      // recomputed from the packed row below rather than held: registers
-      // decide how many rows are in flight)
+      // one pass: chunk sums and sums of squares
 #pragma unroll
       for (int j = 0; j < S; ++j) {
-        const float m = stat[piece_of(pc, j)];
-        float dx[VEC];
-        Elem<T>::unpack(cur[j], dx);
-        float a = 0.f;
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          dx[e] -= m;
-          a += dx[e] * dx[e];
-        }
-        t[j] = a;
+        const int c = cbase + j * 64 + lane;
+        if (FULL || c < nch) part[c] = float2{chunk_sum<T>(cur[j]), chunk_sumsq<T>(cur[j])};
       }
-      piece_reduce(t, stat + npc);
-      if (ls < npc) stat[npc + ls] = __builtin_amdgcn_rsqf(stat[npc + ls] * iw0 + s.eps);
-      if (ls + RL < npc) stat[npc + ls + RL] = __builtin_amdgcn_rsqf(stat[npc + ls + RL] * iw1 + s.eps);
+      if ((WPR == 1 ? lane : threadIdx.x) == 0) *flag = 0;
       row_sync();
+      run_reduce(acc, acc + npc);
+      row_sync();
+      // owners: mean, E[x^2] - mean^2, and whether that lost accuracy
+      auto finish = [&](const Owned& o) {
+        if (o.p < npc) {
+          const float2 t = total(o, acc, acc + npc);
+          // a correctly rounded division: a constant piece gets its value back exactly
+          const float m = __fdiv_rn(t.x, o.w), m2 = m * m;
+          const float var = t.y * o.iw - m2;
+          if (m2 > 16.f * var) *flag = 1;
+          acc[o.p] = m;
+          acc[npc + o.p] = __builtin_amdgcn_rsqf(fmaxf(var, 0.f) + s.eps);
+        }
+      };
+      finish(own0);
+      finish(own1);
+      row_sync();
+      if (__builtin_amdgcn_readfirstlane(*flag)) {  // the same word for every wave that shares it
+        // second pass for the variance: sums of centred squares (the squared
+        // means are large next to the variance, so E[x^2] - mean^2 cancels)
+#pragma unroll
+        for (int j = 0; j < S; ++j) {
+          const int c = cbase + j * 64 + lane;
+          const float m = acc[piece_of(pc, j)];
+          float dx[VEC];
+          u32x4 cj = cur[j];
+          __asm__ volatile("" : "+v"(cj));  // unpacked here and again below, never held across
+          centred<T>(cj, m, dx);
+          float a = 0.f;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) a += dx[e] * dx[e];
+          if (FULL || c < nch) part[c] = float2{a, 0.f};
+        }
+        row_sync();
+        run_reduce(acc + npc, nullptr);  // inside-run pieces' totals go to the (recomputed) second slot
+        row_sync();
+        auto refinish = [&](const Owned& o) {
+          if (o.p < npc) {
+            const float q = total(o, acc + npc, nullptr).x;
+            acc[npc + o.p] = __builtin_amdgcn_rsqf(q * o.iw + s.eps);
+          }
+        };
+        refinish(own0);
+        refinish(own1);
+        row_sync();
+      }
       // normalise: y = (x - mean) * (rstd * gamma) + beta, then the activation
+      // (gamma and beta carry its input scale)
       if (valid) {
 #pragma unroll
         for (int j = 0; j < S; ++j) {
           const int c = cbase + j * 64 + lane;
           if (FULL || c < nch) {
             const int pj = piece_of(pc, j);
-            const float m = stat[pj], rs = stat[npc + pj];
+            const float m = acc[pj], rs = acc[npc + pj];
             float dx[VEC], o[VEC];
             u32x4 cj = cur[j];
-            __asm__ volatile("" : "+v"(cj));  // unpack again here instead of keeping pass 2's floats live
-            Elem<T>::unpack(cj, dx);
+            __asm__ volatile("" : "+v"(cj));  // unpack at the use instead of keeping floats live
+            centred<T>(cj, m, dx);
 #pragma unroll
             for (int e = 0; e < VEC; e += 4) {
               const f32x4 g = *(const f32x4*)(lg + (size_t)c * VEC + e);
               const f32x4 b = *(const f32x4*)(lb + (size_t)c * VEC + e);
-              o[e + 0] = act_apply<ACT>((dx[e + 0] - m) * (rs * g[0]) + b[0]);
-              o[e + 1] = act_apply<ACT>((dx[e + 1] - m) * (rs * g[1]) + b[1]);
-              o[e + 2] = act_apply<ACT>((dx[e + 2] - m) * (rs * g[2]) + b[2]);
-              o[e + 3] = act_apply<ACT>((dx[e + 3] - m) * (rs * g[3]) + b[3]);
+              o[e + 0] = act_scaled_in<ACT>(dx[e + 0] * (rs * g[0]) + b[0]);
+              o[e + 1] = act_scaled_in<ACT>(dx[e + 1] * (rs * g[1]) + b[1]);
+              o[e + 2] = act_scaled_in<ACT>(dx[e + 2] * (rs * g[2]) + b[2]);
+              o[e + 3] = act_scaled_in<ACT>(dx[e + 3] * (rs * g[3]) + b[3]);
             }
             st16_nt(yr + c * 16, Elem<T>::pack(o));
           }
         }
       }
-      row_sync();  // statistics read before the next row clears them
+      row_sync();  // statistics read before the next row overwrites them
     } else if (valid) {
 #pragma unroll
       for (int j = 0; j < S; ++j) {
@@ -514,7 +590,8 @@ static SocShape soc_shape(int32_t nchunks, int32_t n_pieces, optimus_dtype dt, i
   const int vec = dt == OPTIMUS_F32 ? 4 : 8;
   const int slots = 4 / wpr;
   return SocShape{st, wpr, nchunks == 64 * wpr * st,
-                  (size_t)nchunks * vec * 4 * 2 + (size_t)slots * 64 * wpr * st * 4 + (size_t)slots * 2 * n_pieces * 4};
+                  (size_t)nchunks * vec * 4 * 2 +
+                      (size_t)slots * (2 * 64 * wpr * st + ((2 * n_pieces + 4) & ~3)) * 4};
 }
 
 template <typename T, int ACT, int WPR>

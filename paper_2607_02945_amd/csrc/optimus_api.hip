@@ -490,7 +490,7 @@ struct HostPlan {
   // fused split-op-cat
   bool soc_fused = false;
   size_t soc_off = 0;
-  int32_t soc_rows = 0, soc_nchunks = 0, soc_pieces = 0, soc_tasks = 0, soc_grid = 0, soc_wpr = 1;
+  int32_t soc_rows = 0, soc_nchunks = 0, soc_pieces = 0, soc_grid = 0, soc_wpr = 1;
   // split-op-cat unfused programs (CHAIN / HORIZONTAL) over plan-owned temporaries
   bool soc_has_unfused = false;
   bool soc_apply_ln = false;
@@ -1366,30 +1366,19 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
     build_rows(hp, m, false, s, d->act);
     hp.row_act = d->act;
     hp.kernel = "split_op_cat_as_pointwise";
-  } else if (vec && nchunks <= kSocMaxChunks && n <= kSocMaxPieces && n <= kSocMaxTasks) {
-    // reduction runs: each piece's chunk range cut into runs of at most `run` chunks, <= 128 runs
-    int run = 1;
-    auto count_tasks = [&](int r) {
-      int64_t t = 0;
-      for (int j = 0; j < n; ++j) t += (d->widths[j] / VEC + r - 1) / r;
-      return t;
-    };
-    while (count_tasks(run) > kSocMaxTasks) ++run;  // ends: n <= kSocMaxTasks pieces need n tasks at most
+  } else if (vec && nchunks <= kSocMaxChunks && n <= kSocMaxPieces) {
     std::vector<uint8_t> cp((size_t)nchunks);
     std::vector<SocPiece> pieces(n);
-    std::vector<SocTask> tasks;
     for (int j = 0; j < n; ++j) {
       const int c0 = (int)(off[j] / VEC), c1 = (int)(off[j + 1] / VEC);
       pieces[j] = SocPiece{c0, c1, (float)(1.0 / (double)d->widths[j]), 0, nullptr, nullptr};
       for (int c = c0; c < c1; ++c) cp[c] = (uint8_t)j;
-      for (int c = c0; c < c1; c += run)
-        tasks.push_back(SocTask{(int16_t)c, (int16_t)std::min(c1, c + run), (int16_t)j, 0});
     }
     DevSoc soc{};
     soc.in = d->in; soc.out = d->out;
     soc.ldin = d->ldin; soc.ldout = d->ldout;
     soc.rows = (int32_t)rows; soc.D = (int32_t)D; soc.nchunks = (int32_t)nchunks;
-    soc.n_pieces = n; soc.n_tasks = (int32_t)tasks.size();
+    soc.n_pieces = n;
     soc.apply_ln = 1; soc.eps = d->eps;
     // the pieces keep the caller's gamma / beta pointers (read by every launch)
     for (int j = 0; j < n; ++j) {
@@ -1400,17 +1389,14 @@ static optimus_status build_split_op_cat(const optimus_split_op_cat_desc* d, opt
     }
     const size_t cp_off = hp.blob.add(cp.data(), cp.size());
     const size_t pc_off = hp.blob.add(pieces.data(), pieces.size() * sizeof(SocPiece));
-    const size_t tk_off = hp.blob.add(tasks.data(), tasks.size() * sizeof(SocTask));
     // device pointers inside DevSoc are filled in at upload (relative offsets kept here)
     soc.chunk_piece = (const uint8_t*)(uintptr_t)cp_off;
     soc.pieces = (const SocPiece*)(uintptr_t)pc_off;
-    soc.tasks = (const SocTask*)(uintptr_t)tk_off;
     hp.soc_off = hp.blob.add(&soc, sizeof soc);
     hp.soc_fused = true;
     hp.soc_rows = (int32_t)rows;
     hp.soc_nchunks = (int32_t)nchunks;
     hp.soc_pieces = n;
-    hp.soc_tasks = (int32_t)tasks.size();
     // persistent grid: exactly the workgroups that fit at once, each wave walking rows
     hp.soc_wpr = wpr;
     const int64_t resident = (int64_t)device_cu_count() * soc_blocks_per_cu(dt, d->act, (int32_t)nchunks, n, wpr);
@@ -1659,7 +1645,6 @@ static void rebase_soc(HostPlan& hp, char* table) {
   DevSoc* s = (DevSoc*)(hp.blob.bytes.data() + hp.soc_off);
   s->chunk_piece = (const uint8_t*)(table + (uintptr_t)s->chunk_piece);
   s->pieces = (const SocPiece*)(table + (uintptr_t)s->pieces);
-  s->tasks = (const SocTask*)(table + (uintptr_t)s->tasks);
 }
 
 // Every pointer the planner stored as a blob (or scratch) offset, made a device address.

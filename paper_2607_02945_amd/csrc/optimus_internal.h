@@ -101,22 +101,15 @@ struct SocPiece {
   const void* beta;    // [width], or null (0)
 };
 
-struct SocTask {
-  int16_t c0, c1;      // chunk range summed by one lane
-  int16_t piece, pad;
-};
-
 struct DevSoc {
   const void* in;
   void* out;
   const uint8_t* chunk_piece;   // [nchunks]
   const SocPiece* pieces;       // [n_pieces]
-  const SocTask* tasks;         // [n_tasks]
   int64_t ldin, ldout;
-  int32_t rows, D, nchunks, n_pieces, n_tasks;
+  int32_t rows, D, nchunks, n_pieces;
   int32_t apply_ln;
   float eps;
-  int32_t pad;
 };
 
 // ------------------------------------------------------------------ launchers
@@ -170,8 +163,7 @@ int rowwise_blocks_per_cu(optimus_dtype dt, optimus_act act, bool layernorm);
 
 constexpr int kSocThreads = 256;
 constexpr int kSocMaxChunks = 1024;  // 16-byte chunks per row held in registers by two waves (8 per lane)
-constexpr int kSocMaxPieces = 256;
-constexpr int kSocMaxTasks = 128;    // two per lane
+constexpr int kSocMaxPieces = 128;   // two owned by each lane of a one-wave row
 // wpr: waves per row asked for (1, 2 or 4; a row that needs more waves for
 // its registers takes more).
 hipError_t soc_launch(optimus_dtype dt, optimus_act act, const DevSoc* soc, int32_t nchunks, int32_t n_pieces,

@@ -188,3 +188,79 @@ def test_pinned_waves_per_row(wpr):
         torch.cuda.synchronize()
         _check_pieces(y, x, widths, gms, bts, "silu", dtype, f"wpr {wpr}")
         p.close()
+
+
+def test_statistics_every_segment_kind():
+    """Pieces placed (in 16-byte chunks, eight per reduction run for bf16 rows
+    of 4096) so that a piece's total comes from each possible place: the first
+    segment of a run, a piece inside a run, the last segment of a run, a whole
+    run, and pieces spanning runs. fp32 rows of the same widths take two waves
+    per row with other run boundaries."""
+    say("[soc segment kinds]")
+    widths = [24, 8, 32, 64, 16, 48, 80, 24, 3800]
+    for dtype in ["bf16", "fp32"]:
+        x, gms, bts = _case(97, widths, dtype, seed=58)
+        y = torch.full_like(x, float("nan"))
+        p = B.optimus_plan_split_op_cat(x, y, widths, gms, bts, True, 1e-5, "silu")
+        assert p.info()["kernel"].startswith("split_op_cat_fused"), p.info()
+        p.execute()
+        torch.cuda.synchronize()
+        _check_pieces(y, x, widths, gms, bts, "silu", dtype, "segment kinds")
+        p.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_large_means_take_the_two_pass_variance(dtype):
+    """Pieces whose mean is far above their spread (E[x^2] - mean^2 would
+    cancel in fp32): even rows offset on every piece, odd rows on one piece
+    only, against the oracle. The one-pass variance alone misses the
+    tolerance here (bf16: 1000 + N(0, 9); fp32: 64 + N(0, 1) on a 1/64 grid,
+    where the fp32 sums behind the mean are exact, so that only the variance
+    decides: emulated in numpy, 5e-4 one-pass against 1e-6 two-pass).
+    Constant rows give beta exactly."""
+    say(f"[soc large means] {dtype}")
+    widths = synth.dirichlet_widths(synth.rng(60), 32, 4096)
+    g = synth.rng(61)
+    rows, D = 256, 4096
+    offset, spread = (1000.0, 3.0) if dtype == "bf16" else (64.0, 1.0)
+    v = g.standard_normal((rows, D)) * spread
+    if dtype == "fp32":
+        v = np.round(v * 64.0) / 64.0
+    v[0::2] += offset
+    o5 = sum(widths[:5])
+    v[1::2, o5:o5 + widths[5]] += offset
+    x = dev(synth.to_storage(v, dtype))
+    gms = [dev(synth.to_storage(g.uniform(0.5, 1.5, w), dtype)) for w in widths]
+    bts = [dev(synth.to_storage(g.standard_normal(w) * np.sqrt(0.1), dtype)) for w in widths]
+    y = torch.full_like(x, float("nan"))
+    B.optimus_split_op_cat(x, y, widths, gms, bts, True, 1e-5, "silu")
+    _check_pieces(y, x, widths, gms, bts, "silu", dtype, "large means")
+    # constant rows (zero variance, nonzero mean): y = beta exactly
+    xc = torch.full((33, D), 7.0, dtype=x.dtype, device="cuda")
+    yc = torch.full_like(xc, float("nan"))
+    B.optimus_split_op_cat(xc, yc, widths, gms, bts, True, 1e-5, "none")
+    want = torch.cat(bts).unsqueeze(0).expand(33, D)
+    assert torch.equal(yc, want)
+
+
+def test_bitwise_repeatable():
+    """Piece statistics are summed in a fixed order: repeated executes of one
+    plan and a one-shot call give bit-identical outputs."""
+    say("[soc repeatable]")
+    widths = synth.dirichlet_widths(synth.rng(62), 32, 4096)
+    x, gms, bts = _case(1000, widths, "bf16", seed=63)
+    ys = [torch.full_like(x, float("nan")) for _ in range(3)]
+    p = B.optimus_plan_split_op_cat(x, ys[0], widths, gms, bts, True, 1e-5, "silu")
+    p.execute()
+    torch.cuda.synchronize()
+    first = ys[0].clone()
+    for _ in range(4):
+        ys[0].fill_(float("nan"))
+        p.execute()
+        torch.cuda.synchronize()
+        assert torch.equal(ys[0], first)
+    p.close()
+    B.optimus_split_op_cat(x, ys[1], widths, gms, bts, True, 1e-5, "silu")
+    torch.cuda.synchronize()
+    assert torch.equal(ys[1], first)
+    _check_pieces(first, x, widths, gms, bts, "silu", "bf16", "repeatable")
