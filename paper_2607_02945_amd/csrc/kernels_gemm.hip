@@ -380,7 +380,13 @@ __device__ __forceinline__ void gemm_epilogue(const f32x16 (&acc)[BM / WM / 32][
 // transposed operands of the backward GEMMs). With bit 0 set and d.xsum
 // given, the tiles of the first column block also write the row sums of x
 // over the whole reduction (db beside dW = dY^T X).
-template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES, int ACT, int TR = 0>
+// PRE > 0 (forward, two stages): a tile of at most PRE K steps issues the
+// global loads of all its steps at once into registers, so the steps wait
+// for one load latency instead of one each; with one row of four waves
+// (WM = 1, WN = 4) and a member no wider than half the tile, the two wave
+// pairs then take alternate K steps over the same columns and add their
+// partial sums through LDS before the epilogue (the tile's MFMA time halves).
+template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES, int ACT, int TR = 0, int PRE = 0>
 __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLinear* __restrict__ descs,
                                                                    const GemmTile* __restrict__ tiles,
                                                                    int32_t num_tiles) {
@@ -448,19 +454,19 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     u32x4 rx[NRX], rw[NRW];
-    auto gload = [&](int k0) {
+    auto gload_to = [&](u32x4 (&ox)[NRX], u32x4 (&ow)[NRW], int k0) {
       if constexpr (TX) {
 #pragma unroll
         for (int i = 0; i < LXT; ++i) {
           const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
 #pragma unroll
-          for (int j = 0; j < KB; ++j) rx[i * KB + j] = load_chunk_t<T>(xb, d.ldx, rg * VEC, Mr, k0 + kq * KB + j, kend, vin);
+          for (int j = 0; j < KB; ++j) ox[i * KB + j] = load_chunk_t<T>(xb, d.ldx, rg * VEC, Mr, k0 + kq * KB + j, kend, vin);
         }
       } else {
 #pragma unroll
         for (int i = 0; i < S::LX; ++i) {
           const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-          rx[i] = load_chunk<T>(xb, d.ldx, row, Mr, k0 + c * VEC, kend, vin);
+          ox[i] = load_chunk<T>(xb, d.ldx, row, Mr, k0 + c * VEC, kend, vin);
         }
       }
       if constexpr (TW) {
@@ -468,17 +474,18 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         for (int i = 0; i < LWT; ++i) {
           const int idx = tid + i * NT, kq = idx % (BK / KB), rg = idx / (BK / KB);
 #pragma unroll
-          for (int j = 0; j < KB; ++j) rw[i * KB + j] = load_chunk_t<T>(wb, d.ldw, rg * VEC, Nr, k0 + kq * KB + j, kend, vw);
+          for (int j = 0; j < KB; ++j) ow[i * KB + j] = load_chunk_t<T>(wb, d.ldw, rg * VEC, Nr, k0 + kq * KB + j, kend, vw);
         }
       } else {
 #pragma unroll
         for (int i = 0; i < S::LW; ++i) {
           const int idx = tid + i * NT, row = idx / CPR, c = idx % CPR;
-          rw[i] = load_chunk<T>(wb, d.ldw, row, Nr, k0 + c * VEC, kend, vin);
+          ow[i] = load_chunk<T>(wb, d.ldw, row, Nr, k0 + c * VEC, kend, vin);
         }
       }
     };
-    auto lstore = [&](int stage) {
+    auto gload = [&](int k0) { gload_to(rx, rw, k0); };
+    auto lstore_from = [&](const u32x4 (&rx)[NRX], const u32x4 (&rw)[NRW], int stage) {
       T* sx = sAB + stage * S::STAGE_ELEMS;
       T* sw = sx + BM * LDK;
       if constexpr (TX) {
@@ -515,7 +522,10 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         }
       }
     };
-    auto compute = [&](int stage) {
+    auto lstore = [&](int stage) { lstore_from(rx, rw, stage); };
+    // MFMA over one staged step; wcol: the wave's column block (wn, or the
+    // block it shares under the K split)
+    auto compute = [&](int stage, int wcol) {
       const T* sx = sAB + stage * S::STAGE_ELEMS;
       const T* sw = sx + BM * LDK;
 #pragma unroll
@@ -523,7 +533,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         const int ko = kc * 2 * VEC + lh * VEC;
         u32x4 a[S::FN], b[S::FM];
 #pragma unroll
-        for (int j = 0; j < S::FN; ++j) a[j] = *(const u32x4*)(sw + (wn * S::TN + j * 32 + l32) * LDK + ko);
+        for (int j = 0; j < S::FN; ++j) a[j] = *(const u32x4*)(sw + (wcol * S::TN + j * 32 + l32) * LDK + ko);
 #pragma unroll
         for (int i = 0; i < S::FM; ++i) b[i] = *(const u32x4*)(sx + (wm * S::TM + i * 32 + l32) * LDK + ko);
 #pragma unroll
@@ -537,14 +547,75 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
     // LayerNorm parameter) loads, whose values are written to LDS: that
     // write waits for them, and the operand loads then fly meanwhile
     const int nk = (kend - kbeg + BK - 1) / BK;
-    if constexpr (STAGES == 2) {
+    bool staged = false;  // K loop done by the all-steps-in-flight path
+    if constexpr (PRE > 0 && STAGES == 2 && TR == 0) {
+      if (nk <= PRE) {
+        staged = true;
+        u32x4 px[PRE][NRX], pw[PRE][NRW];
+#pragma unroll
+        for (int s = 0; s < PRE; ++s)
+          if (s < nk) gload_to(px[s], pw[s], kbeg + s * BK);
+        load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
+        if (WM == 1 && WN == 4 && 2 * d.N <= BN && nk > 1) {
+          // K split: wave pair p = wn / 2 takes steps s + p of each staged pair
+          const int pair = wn >> 1;
+#pragma unroll
+          for (int s = 0; s < PRE; s += 2) {
+            if (s < nk) {
+              lstore_from(px[s], pw[s], 0);
+              if (s + 1 < nk) lstore_from(px[s + 1], pw[s + 1], 1);
+              __syncthreads();
+              if (s + pair < nk) compute(pair, wn & 1);
+              __syncthreads();
+            }
+          }
+          // pair 1 hands its sums to pair 0 (same columns) through the operand
+          // area; its own columns, past N, must read as zeros afterwards
+          float* hand = (float*)smem + (wn & 1) * (S::FM * S::FN * 16 * 64);
+          if (pair == 1) {
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+              for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                  hand[((i * S::FN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+                  acc[i][j][r] = 0.f;
+                }
+          }
+          __syncthreads();
+          if (pair == 0) {
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+              for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] += hand[((i * S::FN + j) * 16 + r) * 64 + lane];
+          }
+          __syncthreads();  // hand-over read before the epilogue stages into the same area
+        } else {
+          lstore_from(px[0], pw[0], 0);
+          __syncthreads();
+#pragma unroll
+          for (int s = 0; s < PRE; ++s) {
+            if (s < nk) {
+              compute(s & 1, wn);
+              if (s + 1 < nk) lstore_from(px[s + 1], pw[s + 1], (s + 1) & 1);
+              __syncthreads();
+            }
+          }
+        }
+      }
+    }
+    if (staged) {
+    } else if constexpr (STAGES == 2) {
       gload(kbeg);
       load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
       lstore(0);
       __syncthreads();
       for (int kb = 0; kb < nk; ++kb) {
         if (kb + 1 < nk) gload(kbeg + (kb + 1) * BK);
-        compute(kb & 1);
+        compute(kb & 1, wn);
         if (kb + 1 < nk) lstore((kb + 1) & 1);
         __syncthreads();
       }
@@ -554,7 +625,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
         if (kb == 0) load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
         lstore(0);
         __syncthreads();
-        compute(0);
+        compute(0, wn);
         __syncthreads();
       }
       if (nk == 0) load_col_params<T, BN, LN>(sBias, sGamma, sBeta, d, n0, Nr);
@@ -1826,15 +1897,15 @@ static hipError_t launch_skinny(optimus_act act, const DevLinear* descs, const G
   return hipGetLastError();
 }
 
-template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
+template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES, int PRE = 0>
 static hipError_t launch_shape(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
                                int32_t grid, hipStream_t stream, int* occ) {
   using S = GemmShape<T, BM, BN, BK, WM, WN, STAGES>;
-#define OPTIMUS_GEMM_LAUNCH(A)                                                                     \
-  if (ln)                                                                                          \
-    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, (A) | 8>), S::LDS_BYTES_LN, S::NT) \
-  else                                                                                             \
-    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, (A)>), S::LDS_BYTES, S::NT)
+#define OPTIMUS_GEMM_LAUNCH(A)                                                                                   \
+  if (ln)                                                                                                        \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, (A) | 8, 0, PRE>), S::LDS_BYTES_LN, S::NT) \
+  else                                                                                                           \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_kernel<T, BM, BN, BK, WM, WN, STAGES, (A), 0, PRE>), S::LDS_BYTES, S::NT)
   switch (act) {
     case OPTIMUS_ACT_NONE: OPTIMUS_GEMM_LAUNCH(0); break;
     case OPTIMUS_ACT_RELU: OPTIMUS_GEMM_LAUNCH(1); break;
@@ -1924,7 +1995,7 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
     case 4: return launch_dma<256, 256, 2, 4>(act, ln, descs, tiles, n, grid, stream, occ);
     case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
-    case 8: return launch_shape<float, 32, 128, 64, 1, 4, 2>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 8: return launch_shape<float, 32, 128, 64, 1, 4, 2, 4>(act, ln, descs, tiles, n, grid, stream, occ);
     case 9:
       if (ln || dt != OPTIMUS_BF16) return hipErrorInvalidValue;
       return launch_stream(act, descs, tiles, n, grid, stream, occ);

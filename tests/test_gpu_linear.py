@@ -79,6 +79,21 @@ def test_every_bf16_tile_variant(variant):
         _check(ms, ys, "bf16", "tanh", f"variant {variant} {mode}")
 
 
+@pytest.mark.parametrize("variant", [3, 6, 8])
+def test_every_fp32_tile_variant(variant):
+    """The fp32 tiles, 64x64 (3), 64x128 (6) and 32x128 (8: every K step's
+    loads in flight at once when K <= 256, and the two wave pairs splitting K
+    for members of N <= 64), grouped and chain, against the oracle: one to five
+    K steps, members of N <= 64 with even and odd step counts, a member wider
+    than one tile."""
+    say(f"[linear fp32 variant] {variant}")
+    shapes = [(513, 120, 136), (300, 60, 200), (90, 33, 130), (257, 64, 260), (31, 7, 40), (130, 200, 64)]
+    ms = _members(shapes, "fp32", seed=15 + variant)
+    for mode in ["grouped", "chain"]:
+        ys = _run(ms, "fp32", "sigmoid", mode=mode, variant=variant)
+        _check(ms, ys, "fp32", "sigmoid", f"fp32 variant {variant} {mode}")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_unaligned_k_and_strided_input(dtype):
     say(f"[linear scalar path] {dtype}")

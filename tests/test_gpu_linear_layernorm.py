@@ -173,10 +173,11 @@ def test_direct_to_lds_layernorm_every_element_multi_tile(variant):
 def test_every_fp32_variant(variant):
     """The fp32 tiles that can hold the rows (3: 64x64 for N <= 64; 6: 64x128;
     8: 32x128, the planner's choice for groups of fewer 64-row tiles than
-    CUs), grouped and chain, ragged rows and K, against the oracle's fused
+    CUs, with its K split over the wave pairs for members of N <= 64),
+    grouped and chain, ragged rows and K, against the oracle's fused
     composition."""
     bn = {3: 64, 6: 128, 8: 128}[variant]
-    shapes = [(513, bn, 136), (100, bn - 4, 40), (31, 16, 24), (257, bn // 2, 260)]
+    shapes = [(513, bn, 136), (100, bn - 4, 40), (31, 16, 24), (257, bn // 2, 260), (300, 60, 200), (90, 33, 130)]
     say(f"[linear+ln fp32 variant] {variant}")
     ms = _members(shapes, "fp32", seed=170 + variant)
     for mode in ["grouped", "chain"]:
