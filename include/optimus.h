@@ -73,10 +73,20 @@ extern "C" {
 
 typedef struct ihipStream_t* optimus_stream_t; /* the same type as hipStream_t */
 
-typedef enum { OPTIMUS_F32 = 0, OPTIMUS_BF16 = 1 } optimus_dtype;
+/* The enumerations are int-sized in C; in C++ they take int as their fixed
+ * underlying type (the same size), so that any value a caller passes -- an
+ * unknown dtype or activation included, which the library rejects -- is a
+ * valid value of the type. */
+#ifdef __cplusplus
+#define OPTIMUS_ENUM(tag) enum tag : int
+#else
+#define OPTIMUS_ENUM(tag) enum tag
+#endif
+
+typedef OPTIMUS_ENUM(optimus_dtype_e) { OPTIMUS_F32 = 0, OPTIMUS_BF16 = 1 } optimus_dtype;
 
 /* Activations of Table 1: relu, sigmoid, tanh, and silu = x * sigmoid(x). */
-typedef enum {
+typedef OPTIMUS_ENUM(optimus_act_e) {
   OPTIMUS_ACT_NONE = 0,
   OPTIMUS_ACT_RELU = 1,
   OPTIMUS_ACT_SIGMOID = 2,
@@ -84,7 +94,7 @@ typedef enum {
   OPTIMUS_ACT_SILU = 4
 } optimus_act;
 
-typedef enum {
+typedef OPTIMUS_ENUM(optimus_status_e) {
   OPTIMUS_OK = 0,
   OPTIMUS_ERR_INVALID_ARG = -1,
   OPTIMUS_ERR_UNSUPPORTED = -2,
@@ -431,7 +441,7 @@ optimus_status optimus_plan_dequantize_fp8(const optimus_fp8_dequant_desc* d, in
  *                      waves for its registers takes more; INVALID_ARG for
  *                      other values).
  *   reserved           must be 0 (INVALID_ARG otherwise). */
-typedef enum {
+typedef OPTIMUS_ENUM(optimus_gemm_tile_e) {
   OPTIMUS_TILE_AUTO = 0,
   OPTIMUS_TILE_BF16_128X64 = 1,      /* register-staged, one LDS stage */
   OPTIMUS_TILE_BF16_128X128 = 2,     /* register-staged, two LDS stages */
@@ -481,7 +491,7 @@ optimus_status optimus_plan_split_op_cat_ex(const optimus_split_op_cat_desc* d, 
  *               concat launch (3 launches).
  * CHAIN and HORIZONTAL on a split-op-cat plan use plan-owned temporaries of
  * rows*D elements, allocated on their first use. */
-typedef enum {
+typedef OPTIMUS_ENUM(optimus_exec_mode_e) {
   OPTIMUS_EXEC_GROUPED = 0,
   OPTIMUS_EXEC_CHAIN = 1,
   OPTIMUS_EXEC_HORIZONTAL = 2
