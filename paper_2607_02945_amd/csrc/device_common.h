@@ -215,25 +215,11 @@ __device__ __forceinline__ float act_grad(float x) {
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *(const OPTIMUS_GLOBAL u32x4*)p; }
 __device__ __forceinline__ void st16(void* p, const u32x4& v) { *(OPTIMUS_GLOBAL u32x4*)p = v; }
 // Streaming variants: data touched once (nontemporal hint).
-#ifndef OPTIMUS_NT_LOADS
-#define OPTIMUS_NT_LOADS 1
-#endif
-#ifndef OPTIMUS_NT_STORES
-#define OPTIMUS_NT_STORES 1
-#endif
 __device__ __forceinline__ u32x4 ld16_nt(const void* p) {
-#if OPTIMUS_NT_LOADS
   return __builtin_nontemporal_load((const OPTIMUS_GLOBAL u32x4*)p);
-#else
-  return *(const OPTIMUS_GLOBAL u32x4*)p;
-#endif
 }
 __device__ __forceinline__ void st16_nt(void* p, const u32x4& v) {
-#if OPTIMUS_NT_STORES
   __builtin_nontemporal_store(v, (OPTIMUS_GLOBAL u32x4*)p);
-#else
-  *(OPTIMUS_GLOBAL u32x4*)p = v;
-#endif
 }
 
 // ------------------------------------------------------------------ lane reductions

@@ -70,8 +70,10 @@ __global__ __launch_bounds__(kRowThreads) void grouped_act_backward_kernel(const
 // ===================================================================== LayerNorm
 // 16-byte path: the row's chunks in registers (MAXC per lane), as the forward.
 // Each lane keeps its columns' dgamma / dbeta sums over the rows it handles;
-// at the end of the tile they are added into sPart ([2][cols] in LDS) and the
-// tile's partial row leaves in one coalesced pass.
+// at the end of the tile each wave writes its sums to its own slot sPart
+// ([2][cols] in LDS, one per wave) and the block adds the four slots in a
+// fixed order as the tile's partial row leaves in one coalesced pass, so the
+// sums do not depend on timing.
 // gamma (and beta) are staged in LDS as fp32 (sGamma, sBeta: [cols], filled
 // by the caller) and read where they are used. ACT != 0: the backward of the
 // fused LayerNorm + activation -- the incoming gradient is the activation
@@ -220,6 +222,7 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
           accB[j][e] += __shfl_xor(accB[j][e], off);
         }
     }
+    // the wave's lanes of slot 0 own every column of the row exactly once
     if (sub == 0) {
 #pragma unroll
       for (int j = 0; j < MAXC; ++j) {
@@ -227,8 +230,8 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
         if (c < cpr) {
 #pragma unroll
           for (int e = 0; e < VEC; ++e) {
-            atomicAdd(&sPart[c * VEC + e], accG[j][e]);
-            atomicAdd(&sPart[d.cols + c * VEC + e], accB[j][e]);
+            sPart[c * VEC + e] = accG[j][e];
+            sPart[d.cols + c * VEC + e] = accB[j][e];
           }
         }
       }
@@ -300,12 +303,12 @@ __device__ __forceinline__ void lnb_rows_scalar(const DevRowsGrad& d, const RowT
 }
 
 template <typename T, int ACT>
-__global__ __launch_bounds__(kRowThreads) void grouped_layernorm_backward_kernel(
+__global__ __launch_bounds__(kRowThreads, 3) void grouped_layernorm_backward_kernel(
     const DevRowsGrad* __restrict__ descs, const RowTile* __restrict__ tiles, int32_t num_tiles) {
   // [2][cols] partials and [cols] gamma for the widest row the 16-byte path
   // holds: 64 lanes x the chunks per lane x the values per chunk
   constexpr int MAXCOLS = 64 * kLnChunksPerLane * Elem<T>::VEC;
-  __shared__ __align__(16) float sPart[2 * MAXCOLS];
+  __shared__ __align__(16) float sPart[4][2 * MAXCOLS];  // one [2][cols] slot per wave
   __shared__ __align__(16) float sGamma[MAXCOLS];
   __shared__ __align__(16) float sBeta[ACT != 0 ? MAXCOLS : 4];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -315,18 +318,16 @@ __global__ __launch_bounds__(kRowThreads) void grouped_layernorm_backward_kernel
     const DevRowsGrad d = descs[rt.member];
     if (d.vec && d.lanes > 0) {
       const bool params = d.want_params != 0;
-      if (params)
-        for (int i = tid; i < 2 * d.cols; i += kRowThreads) sPart[i] = 0.f;
       for (int i = tid; i < d.cols; i += kRowThreads) sGamma[i] = d.gamma ? Elem<T>::load1(d.gamma, i) : 1.f;
       if constexpr (ACT != 0)
         for (int i = tid; i < d.cols; i += kRowThreads) sBeta[i] = d.beta ? Elem<T>::load1(d.beta, i) : 0.f;
       __syncthreads();
-      lnb_rows_vec<T, kLnChunksPerLane, ACT>(d, rt, lane, wave, sPart, sGamma, sBeta);
-      __syncthreads();  // every wave is done with sGamma and has added into sPart
+      lnb_rows_vec<T, kLnChunksPerLane, ACT>(d, rt, lane, wave, sPart[wave], sGamma, sBeta);
+      __syncthreads();  // every wave is done with sGamma and has written its slot
       if (params) {
         float* out = d.part + (int64_t)(d.part0 + rt.pad) * 2 * d.cols;
-        for (int i = tid; i < 2 * d.cols; i += kRowThreads) out[i] = sPart[i];
-        __syncthreads();  // sPart is cleared by the next tile
+        for (int i = tid; i < 2 * d.cols; i += kRowThreads) out[i] = ((sPart[0][i] + sPart[1][i]) + sPart[2][i]) + sPart[3][i];
+        __syncthreads();  // the slots are written again by the next tile
       }
     } else {
       lnb_rows_scalar<T, ACT>(d, rt, lane, wave);

@@ -12,10 +12,7 @@
 namespace optimus {
 
 // ===================================================================== LayerNorm
-#ifndef OPTIMUS_LN_DEPTH
-#define OPTIMUS_LN_DEPTH 2
-#endif
-constexpr int kLnDepth = OPTIMUS_LN_DEPTH;  // row slots loaded ahead of the one being computed
+constexpr int kLnDepth = 2;  // row slots loaded ahead of the one being computed
 
 // A row of one member is handled by a group of L lanes (L = power of two set
 // per member by the planner, so that L * MAXC chunks of 16 bytes cover the

@@ -564,10 +564,7 @@ static DevRows make_rows(const void* x, int64_t ldx, void* y, int64_t ldy, const
 
 // Row tiles of one member: about kRowTileBytes of input per tile, a whole
 // number of the block's row slots.
-#ifndef OPTIMUS_ROW_TILE_BYTES
-#define OPTIMUS_ROW_TILE_BYTES 32768
-#endif
-static constexpr int64_t kRowTileBytes = OPTIMUS_ROW_TILE_BYTES;
+static constexpr int64_t kRowTileBytes = 32768;
 static void add_row_tiles(std::vector<RowTile>& tiles, int member, const DevRows& r, size_t s) {
   const int rpb = r.vec ? 4 * (64 / r.lanes) : 4;
   const int64_t row_bytes = std::max<int64_t>(1, (int64_t)r.cols * (int64_t)s);

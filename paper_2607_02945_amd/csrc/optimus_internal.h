@@ -148,12 +148,9 @@ GemmConfig gemm_pick_config_trans(optimus_dtype dt, const optimus_linear_desc* d
 int gemm_resident_per_cu(const GemmConfig& cfg, optimus_dtype dt, optimus_act act, bool ln, int tr = 0);
 
 constexpr int kRowThreads = 256;
-#ifndef OPTIMUS_LN_CHUNKS_PER_LANE
-#define OPTIMUS_LN_CHUNKS_PER_LANE 2
-#endif
 // 16-byte chunks of a row each lane of the LayerNorm kernel holds in registers
 // (rows up to 64 * this many chunks take the register path).
-constexpr int kLnChunksPerLane = OPTIMUS_LN_CHUNKS_PER_LANE;
+constexpr int kLnChunksPerLane = 2;
 hipError_t layernorm_launch(optimus_dtype dt, optimus_act act, const DevRows* descs, const RowTile* tiles,
                             int32_t num_tiles, int32_t grid, hipStream_t stream);
 hipError_t pointwise_launch(optimus_dtype dt, optimus_act act, const DevRows* descs, const RowTile* tiles,

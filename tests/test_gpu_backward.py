@@ -295,6 +295,41 @@ def test_layernorm_backward(dtype, mode):
     _check_ln_bwd(ms, dtype, f"{dtype} {mode}")
 
 
+@pytest.mark.parametrize("act", ["none", "tanh"])
+def test_layernorm_backward_bitwise_repeatable(act):
+    """dgamma / dbeta are summed in a fixed order (per-wave slots added in
+    wave order, then the partial rows in row order): repeated executes of one
+    plan give bit-identical gradients, with and without the fused activation
+    backward; the first execute against the oracle."""
+    say(f"[ln bwd repeatable] {act}")
+    ms = _ln_members([(4000, 256), (2000, 1024), (3000, 136)], "bf16", seed=560)
+    for m in ms:
+        m["dx"] = _empty((m["rows"], m["cols"]), "bf16")
+        m["dg"] = torch.full((m["cols"],), float("nan"), dtype=torch.bfloat16, device="cuda")
+        m["db"] = torch.full((m["cols"],), float("nan"), dtype=torch.bfloat16, device="cuda")
+    args = ([m["x"] for m in ms], [m["dy"] for m in ms], [m["dx"] for m in ms], [m["gamma"] for m in ms])
+    if act == "none":
+        p = B.optimus_plan_layernorm_backward(*args, [m["dg"] for m in ms], [m["db"] for m in ms], 1e-5)
+    else:
+        betas = [torch.zeros_like(m["gamma"]) for m in ms]
+        p = B.optimus_plan_layernorm_act_backward(*args, betas, [m["dg"] for m in ms], [m["db"] for m in ms],
+                                                  1e-5, act)
+    p.execute()
+    torch.cuda.synchronize()
+    first = [(m["dx"].clone(), m["dg"].clone(), m["db"].clone()) for m in ms]
+    if act == "none":
+        _check_ln_bwd(ms, "bf16", "repeatable")
+    for _ in range(4):
+        for m in ms:
+            m["dg"].fill_(float("nan"))
+            m["db"].fill_(float("nan"))
+        p.execute()
+        torch.cuda.synchronize()
+        for m, (dx, dg, db) in zip(ms, first):
+            assert torch.equal(m["dx"], dx) and torch.equal(m["dg"], dg) and torch.equal(m["db"], db)
+    p.close()
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_layernorm_backward_variants(dtype):
     """No gamma, no dgamma/dbeta, in place (dx == dy), strided and unaligned rows, eps 0.5."""
