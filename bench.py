@@ -74,9 +74,14 @@ def parse():
                     help="turn four rocprofv3 --pmc output folders (FETCH_SIZE and WRITE_SIZE of this workload's "
                          "bench run and of --copy-probe) into profiles/<kernel>__<workload>.pmc.json; no GPU needed")
     ap.add_argument("--pmc-command", default="", help="command line recorded in the --pmc-summary output")
-    ap.add_argument("--only-plan", type=int, default=None, metavar="K",
+    ap.add_argument("--pmc-plan", default=None, metavar="K",
+                    help="with --pmc-summary: the launch the counters cover (a plan_index of the bench line's "
+                         "roofline or other_kernels, or 'pw' for launch_bound's grouped pointwise launch); "
+                         "default: the dominant one")
+    ap.add_argument("--only-plan", default=None, metavar="K",
                     help="time only launch K of the op-group (roofline.plan_index of a bench line picks the "
-                         "dominant one), for profiler runs")
+                         "dominant one; 'pw': launch_bound's grouped pointwise launch of the two-launch form), "
+                         "for profiler runs")
     return ap.parse_args()
 
 
@@ -470,8 +475,15 @@ def pmc_summary(args):
     name = args.workload
     line = os.path.join(ROOT, "profiles", "bench", f"bench_{name}.json")
     with open(line) as f:
-        roof = json.loads(f.read().splitlines()[-1])["roofline"]
-    label, plan_index = roof["kernel"], roof["plan_index"]
+        bl = json.loads(f.read().splitlines()[-1])
+    entries = [bl["roofline"]] + bl.get("other_kernels", [])
+    if "two_launch" in bl:
+        entries.append(dict(bl["two_launch"]["pointwise"], plan_index="pw"))
+    want = bl["roofline"]["plan_index"] if args.pmc_plan is None else args.pmc_plan
+    match = [e for e in entries if str(e.get("plan_index")) == str(want)]
+    if not match:
+        raise SystemExit(f"bench.py: no launch with plan_index {want} in {line}")
+    label, plan_index = match[0]["kernel"], match[0]["plan_index"]
     kernel, kernels = kernel_symbol(label), kernel_symbols(label)
     if len(set(kernels)) != len(kernels):
         raise SystemExit(f"bench.py: the kernels of {label} are not told apart by name")
@@ -693,10 +705,18 @@ def main():
 
     if args.only_plan is not None:
         # one launch of the op-group alone (for rocprofv3 runs that must see
-        # only the dominant kernel)
-        k = args.only_plan
+        # only that kernel)
+        if args.only_plan == "pw":
+            if not ogs[0].two_launch:
+                raise SystemExit("bench.py: --only-plan pw needs a workload with a two-launch form")
+            for og in ogs:
+                og.pw_only = [og.two_launch[1]]
+            k, plan = "pw_only", ogs[0].two_launch[1][0]
+        else:
+            k = int(args.only_plan)
+            plan = ogs[0].grouped[k][0]
         k_ms = timed(k, args.steps, args.warmup)[0] / args.steps
-        print(json.dumps({"workload": args.workload, "plan_index": k, "kernel": ogs[0].grouped[k][0].info()["kernel"],
+        print(json.dumps({"workload": args.workload, "plan_index": args.only_plan, "kernel": plan.info()["kernel"],
                           "steps": args.steps, "kernel_us": round(k_ms * 1000.0, 3)}), flush=True)
         return
 
@@ -759,8 +779,9 @@ def main():
         o_ms = plan_ms[k]
         pinfo = plan.info()
         entry = roofline(pinfo, o_ms)
-        entry.update({"kernel": pinfo["kernel"], "kernel_us": round(o_ms * 1000.0, 3),
-                      "algorithmic_bytes": pinfo["bytes"], "algorithmic_flops": pinfo["flops"]})
+        entry.update({"kernel": pinfo["kernel"], "plan_index": k, "kernel_us": round(o_ms * 1000.0, 3),
+                      "algorithmic_bytes": pinfo["bytes"], "algorithmic_flops": pinfo["flops"],
+                      "traffic": traffic_from_profile(pinfo["kernel"], args.workload, k)})
         others.append(entry)
     if others:
         out["other_kernels"] = others
@@ -783,7 +804,7 @@ def main():
         pinfo = pw_plan.info()
         pw = roofline(pinfo, p_ms / args.steps)
         pw.update({"kernel": pinfo["kernel"], "kernel_us": round(p_ms / args.steps * 1000.0, 3),
-                   "algorithmic_bytes": pinfo["bytes"]})
+                   "algorithmic_bytes": pinfo["bytes"], "traffic": traffic_from_profile(pinfo["kernel"], args.workload, "pw")})
         out["two_launch"] = {"us_per_group": round(t_ms / args.steps * 1000.0, 3), "launches_per_group": 2,
                              "pointwise": pw}
     if ogs[0].tiled:

@@ -688,8 +688,13 @@ static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int
     gs.chain[ids[i]].first_tile = first;
     gs.chain[ids[i]].num_tiles = (int)chain_tiles.size() - first;
   }
-  // grouped list: runs of consecutive members (in `order`) sharing x walk
-  // their M-blocks together
+  // grouped list: a run of consecutive members (in `order`) that share x is
+  // walked in groups of kSharedMBlocks M-blocks: for each group, every
+  // member's N-blocks in turn, each over the group's M-blocks. Consecutive
+  // items then share a weight block, and a group's x rows serve every member
+  // while they are in L2 (walking all members' N-blocks per M-block instead
+  // kept x resident but fetched each weight block once per M-block).
+  constexpr int64_t kSharedMBlocks = 8;
   std::vector<GemmTile> tiles;
   bool shared = false;
   for (int a = 0; a < n;) {
@@ -700,9 +705,19 @@ static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int
       if (db.x != da.x || db.ldx != da.ldx || db.M != da.M || db.K != da.K) break;
       ++b;
     }
-    shared = shared || b - a > 1;
-    for (int64_t mb = 0; mb < (da.M + bm - 1) / bm; ++mb)
-      for (int r = a; r < b; ++r) member_tiles(tiles, order[r], mb);
+    const int64_t mbs = (da.M + bm - 1) / bm;
+    if (b - a == 1) {
+      for (int64_t mb = 0; mb < mbs; ++mb) member_tiles(tiles, order[a], mb);
+    } else {
+      shared = true;
+      for (int64_t g0 = 0; g0 < mbs; g0 += kSharedMBlocks)
+        for (int r = a; r < b; ++r) {
+          const int i = order[r];
+          for (int64_t nb = 0; nb < (descs[i].N + bn - 1) / bn; ++nb)
+            for (int64_t mb = g0; mb < std::min(mbs, g0 + kSharedMBlocks); ++mb)
+              tiles.push_back(GemmTile{i, (int32_t)mb, (int32_t)nb, 0});
+        }
+    }
     a = b;
   }
   gs.real_tiles = (int64_t)tiles.size();
