@@ -721,12 +721,36 @@ static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int
     a = b;
   }
   gs.real_tiles = (int64_t)tiles.size();
+  const int64_t cap = (int64_t)device_cu_count() * gemm_resident_per_cu(cfg, hp.dt, act, ln, tr);
+  // The kernels hand XCD x (the hardware deals workgroups round-robin to the
+  // 8 XCDs) the items at positions r * grid + x * grid / 8 + [0, grid / 8) of
+  // round r. Over more than one round, each XCD gets one contiguous eighth of
+  // the list instead of a slice of every round, so the items that share a
+  // weight block (a member's M-blocks) or an x panel stay on one L2, and the
+  // last round's items spread over all XCDs; empty positions are padding.
+  bool dealt = false;
+  {
+    const int64_t T = (int64_t)tiles.size();
+    int64_t g = std::min<int64_t>((T + 7) / 8 * 8, cap);
+    if (g >= 8) g -= g % 8;
+    // (the tiled kernels; the streaming and skinny kernels walk items in plain order)
+    if (tr == 0 && g >= 8 && T > g && cfg.variant != 7 && cfg.variant != 9) {
+      const int64_t per = g / 8, chunk = (T + 7) / 8, rounds = (chunk + per - 1) / per;
+      std::vector<GemmTile> dealt_tiles((size_t)(rounds * g), GemmTile{-1, 0, 0, 0});
+      for (int64_t x = 0; x < 8; ++x)
+        for (int64_t j = 0; j < chunk && x * chunk + j < T; ++j)
+          dealt_tiles[(size_t)((j / per) * g + x * per + j % per)] = tiles[(size_t)(x * chunk + j)];
+      tiles.swap(dealt_tiles);
+      dealt = true;
+    }
+  }
   while (tiles.size() % 8) tiles.push_back(GemmTile{-1, 0, 0, 0});
   gs.descs_off = hp.blob.add(descs.data(), descs.size() * sizeof(DevLinear));
   gs.tiles_off = hp.blob.add(tiles.data(), tiles.size() * sizeof(GemmTile));
   gs.num_tiles = (int32_t)tiles.size();
-  const size_t chain_off = shared ? hp.blob.add(chain_tiles.data(), chain_tiles.size() * sizeof(GemmTile)) : gs.tiles_off;
-  const int64_t cap = (int64_t)device_cu_count() * gemm_resident_per_cu(cfg, hp.dt, act, ln, tr);
+  // the CHAIN launches walk each member's tiles in member order: their own list unless it equals the grouped one
+  const size_t chain_off =
+      shared || dealt ? hp.blob.add(chain_tiles.data(), chain_tiles.size() * sizeof(GemmTile)) : gs.tiles_off;
   int64_t grid = std::min<int64_t>((int64_t)tiles.size(), cap);
   if (grid >= 8) grid -= grid % 8;
   gs.grid = (int32_t)std::max<int64_t>(1, grid);
