@@ -441,7 +441,10 @@ def traffic_from_profile(kernel, name, plan_index):
     kernel and workload, when it was taken on the current kernel sources and
     on the same launch of the op-group (two launches may share a kernel
     label) -- else None."""
-    path = os.path.join(ROOT, "profiles", f"{kernel_symbol(kernel)}__{name}.pmc.json")
+    sym = kernel_symbol(kernel)
+    path = os.path.join(ROOT, "profiles", f"{sym}__{name}__plan{plan_index}.pmc.json")
+    if not os.path.exists(path):
+        path = os.path.join(ROOT, "profiles", f"{sym}__{name}.pmc.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -510,7 +513,10 @@ def pmc_summary(args):
     if len(kernels) > 1:
         out["per_kernel"] = per
         out["note"] = "one execution of the plan is these launches; hbm_bytes_per_launch is their sum"
-    path = os.path.join(ROOT, "profiles", f"{kernel}__{name}.pmc.json")
+    # the dominant launch's summary is <kernel>__<workload>; another launch of
+    # the op-group adds its plan index (two launches may share a kernel)
+    tail = "" if str(plan_index) == str(bl["roofline"]["plan_index"]) else f"__plan{plan_index}"
+    path = os.path.join(ROOT, "profiles", f"{kernel}__{name}{tail}.pmc.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
         f.write("\n")
@@ -581,6 +587,7 @@ def kernel_symbol(label):
                         ("grouped_quantize_fp8", "grouped_quantize_fp8_kernel"),
                         ("grouped_dequantize_fp8", "grouped_dequantize_fp8_kernel"),
                         ("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
+                        ("grouped_gemm_stream", "grouped_gemm_stream_kernel"),
                         ("grouped_gemm", "grouped_gemm_kernel"), ("split_op_cat_fused", "split_op_cat_kernel"),
                         ("grouped_layernorm", "grouped_layernorm_kernel"), ("grouped_pointwise", "grouped_pointwise_kernel")):
         if label.startswith(prefix):
@@ -592,7 +599,8 @@ def kernel_symbol(label):
 # headers): a counter summary is used only while these are unchanged.
 KERNEL_SOURCES = {
     "grouped_gemm_kernel": "kernels_gemm.hip", "grouped_gemm_dma_kernel": "kernels_gemm.hip",
-    "grouped_gemm_skinny_kernel": "kernels_gemm.hip", "split_op_cat_kernel": "kernels_rowwise.hip",
+    "grouped_gemm_skinny_kernel": "kernels_gemm.hip", "grouped_gemm_stream_kernel": "kernels_gemm.hip",
+    "split_op_cat_kernel": "kernels_rowwise.hip",
     "grouped_layernorm_kernel": "kernels_rowwise.hip", "grouped_pointwise_kernel": "kernels_rowwise.hip",
     "grouped_quantize_fp8_scaled_kernel": "kernels_fp8.hip", "grouped_quantize_fp8_kernel": "kernels_fp8.hip",
     "grouped_dequantize_fp8_kernel": "kernels_fp8.hip", "grouped_fp8_amax_kernel": "kernels_fp8.hip",

@@ -728,13 +728,17 @@ static void build_gemm_set(HostPlan& hp, GemmSet& gs, const GemmConfig& cfg, int
   // the list instead of a slice of every round, so the items that share a
   // weight block (a member's M-blocks) or an x panel stay on one L2, and the
   // last round's items spread over all XCDs; empty positions are padding.
+  // Only for members of one K: with K unequal the heavy-first list relies on
+  // every round mixing all XCDs (dealt, one XCD would take all the long items).
   bool dealt = false;
   {
     const int64_t T = (int64_t)tiles.size();
     int64_t g = std::min<int64_t>((T + 7) / 8 * 8, cap);
     if (g >= 8) g -= g % 8;
+    bool one_k = true;
+    for (const DevLinear& dd : descs) one_k = one_k && dd.K == descs[0].K;
     // (the tiled kernels; the streaming and skinny kernels walk items in plain order)
-    if (tr == 0 && g >= 8 && T > g && cfg.variant != 7 && cfg.variant != 9) {
+    if (tr == 0 && one_k && g >= 8 && T > g && cfg.variant != 7 && cfg.variant != 9) {
       const int64_t per = g / 8, chunk = (T + 7) / 8, rounds = (chunk + per - 1) / per;
       std::vector<GemmTile> dealt_tiles((size_t)(rounds * g), GemmTile{-1, 0, 0, 0});
       for (int64_t x = 0; x < 8; ++x)
