@@ -452,7 +452,8 @@ typedef OPTIMUS_ENUM(optimus_gemm_tile_e) {
   OPTIMUS_TILE_F32_64X128 = 7,
   OPTIMUS_TILE_SKINNY = 8,           /* every K and N <= 8: streaming, no MFMA */
   OPTIMUS_TILE_F32_32X128 = 9,       /* 4 waves across the 128 columns */
-  OPTIMUS_TILE_BF16_STREAM = 10      /* every K, N <= 64 (multiples of 8, aligned rows): 512-row streams */
+  OPTIMUS_TILE_BF16_STREAM = 10,     /* every K, N <= 64 (multiples of 8, aligned rows): 512-row streams */
+  OPTIMUS_TILE_F32_16X128 = 11       /* operands loaded straight into MFMA registers, no LDS staging */
 } optimus_gemm_tile;
 
 typedef struct {

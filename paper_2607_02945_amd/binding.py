@@ -80,7 +80,8 @@ class PlanOptions(ctypes.Structure):
 
 # optimus_gemm_tile values, keyed by the kernel-table index the plan's kernel name reports
 TILES = {"auto": 0, "bf16_128x64": 1, "bf16_128x128": 2, "bf16_256x256": 3, "f32_64x64": 4, "bf16_dma_256x256": 5,
-         "bf16_dma_128x128": 6, "f32_64x128": 7, "skinny": 8, "f32_32x128": 9, "bf16_stream": 10}
+         "bf16_dma_128x128": 6, "f32_64x128": 7, "skinny": 8, "f32_32x128": 9, "bf16_stream": 10,
+         "f32_16x128": 11}
 
 
 def plan_options(gemm_tile=0, wgrad_splits=0, soc_waves_per_row=0) -> PlanOptions:

@@ -688,6 +688,202 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
   }
 }
 
+// ===================================================================== 16-row fp32 tiles
+// Small fp32 groups (fewer 32-row tiles than CUs, at most 128 outputs per row)
+// are latency bound: a workgroup's time is its descriptor and operand load
+// latency plus its serial MFMA work. This kernel halves that work per
+// workgroup with 16-row tiles on v_mfma_f32_16x16x4f32, and stages nothing
+// through LDS: each lane loads its MFMA operands straight from global memory
+// as 16-byte chunks of four consecutive k (w row n = lane % 16, x row
+// m = lane % 16, k offset 4 (lane / 16) in a group of 16 k), so the waves of a
+// tile never wait for one another inside the K loop. Instruction e of a group
+// pairs element e of every lane's chunks, i.e. it sums k = 4 q + e over the
+// lane quarters q; the four instructions cover the group's 16 k (a fixed
+// permuted order, the same for both operands). The A operand is the weight
+// tile, so output register r of lane l holds row l % 16 and column
+// 4 (l / 16) + r of its 16-column block: four consecutive columns of a row.
+//
+// The four waves take the tile's 32-column blocks (two MFMA blocks each).
+// When the tile holds fewer columns (N <= 64, or the last block of a wider
+// member), the spare waves split the K range with the waves of the same
+// columns and hand their partial sums over through LDS, added in a fixed
+// order. A wave loads batches of kR16Batch k-groups, the next batch in flight
+// while the current one is multiplied; even and odd k-groups go to separate
+// accumulators, so four independent MFMA chains run per wave. Bias, gamma and
+// beta are read straight into registers beside the first operand loads.
+constexpr int kR16Rows = 16, kR16Cols = 128, kR16Batch = 8;
+
+template <int ACTX>
+__global__ __launch_bounds__(256) void grouped_gemm_rows16_kernel(const DevLinear* __restrict__ descs,
+                                                                 const GemmTile* __restrict__ tiles,
+                                                                 int32_t num_tiles) {
+  constexpr int ACT = ACTX & 7;
+  constexpr bool LN = (ACTX & 8) != 0;
+  constexpr int KB = kR16Batch;
+  __shared__ float hand[3][4][8][64];    // K-split partials: [split - 1][column block][value][lane]
+  __shared__ float red[2][kR16Rows][4];  // fused LayerNorm row partials: [pass][row][column block]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, lq = lane >> 4;
+
+  int vb = blockIdx.x;
+  if ((gridDim.x & 7) == 0) vb = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+
+  for (int t = vb; t < num_tiles; t += gridDim.x) {
+    const GemmTile tile = tiles[t];
+    if (tile.member < 0) continue;
+    const DevLinear d = descs[tile.member];
+    const int m0 = tile.mb * kR16Rows, n0 = tile.nb * kR16Cols;
+    const int Mr = d.M - m0;                     // rows left from the tile's first (may exceed 16)
+    const int Nr = min(d.N - n0, kR16Cols);      // columns in this tile
+    const int ncb = Nr > 64 ? 4 : Nr > 32 ? 2 : 1;  // 32-column blocks in use
+    const int ks = 4 / ncb;                      // waves per column block (K-split ways)
+    const int cb = wave & (ncb - 1), sk = wave / ncb;
+    const int c0 = cb * 32;                      // the wave's first column in the tile
+    const int nkg = (d.K + 15) >> 4;             // k-groups of 16
+    const int per = (nkg + ks - 1) / ks;
+    const int g_beg = min(nkg, sk * per), g_end = min(nkg, g_beg + per);
+    const bool vin = d.vec & 1;
+    const float* xb = (const float*)d.x + (int64_t)m0 * d.ldx;
+    const float* wb = (const float*)d.w + (int64_t)(n0 + c0) * d.ldw;
+    const int wrows = Nr - c0;                   // w rows left from the wave's first column
+
+    u32x4 bufA[KB][3], bufB[KB][3];              // per k-group: w block 0, w block 1, x
+    auto load = [&](u32x4 (&b)[KB][3], int g0) {
+#pragma unroll
+      for (int i = 0; i < KB; ++i) {
+        if (g0 + i < g_end) {
+          const int k = (g0 + i) * 16 + lq * 4;
+          b[i][0] = load_chunk<float>(wb, d.ldw, l16, wrows, k, d.K, vin);
+          b[i][1] = load_chunk<float>(wb, d.ldw, 16 + l16, wrows, k, d.K, vin);
+          b[i][2] = load_chunk<float>(xb, d.ldx, l16, Mr, k, d.K, vin);
+        }
+      }
+    };
+    f32x4 acc[2][2];  // [column block][k-group parity]
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) acc[j][p] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](const u32x4 (&b)[KB][3], int g0) {
+#pragma unroll
+      for (int i = 0; i < KB; ++i) {
+        if (g0 + i < g_end) {
+          const f32x4 w0 = __builtin_bit_cast(f32x4, b[i][0]), w1 = __builtin_bit_cast(f32x4, b[i][1]);
+          const f32x4 xv = __builtin_bit_cast(f32x4, b[i][2]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[0][i & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(w0[e], xv[e], acc[0][i & 1], 0, 0, 0);
+            acc[1][i & 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[e], xv[e], acc[1][i & 1], 0, 0, 0);
+          }
+        }
+      }
+    };
+
+    // this lane's columns: c0 + 16 j + 4 lq + r of the tile
+    const int cl = c0 + lq * 4;
+    float pb[2][4], pg[2][4], pe[2][4];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int c = cl + 16 * j + r;
+        const bool in = c < Nr;
+        pb[j][r] = (d.bias && in) ? Elem<float>::load1(d.bias, n0 + c) : 0.f;
+        if constexpr (LN) {
+          pg[j][r] = in ? (d.gamma ? Elem<float>::load1(d.gamma, c) : 1.f) : 0.f;
+          pe[j][r] = (d.beta && in) ? Elem<float>::load1(d.beta, c) : 0.f;
+        }
+      }
+
+    if (g_beg < g_end) load(bufA, g_beg);
+    for (int g = g_beg; g < g_end; g += 2 * KB) {
+      if (g + KB < g_end) load(bufB, g + KB);
+      compute(bufA, g);
+      if (g + 2 * KB < g_end) load(bufA, g + 2 * KB);
+      if (g + KB < g_end) compute(bufB, g + KB);
+    }
+    f32x4 s[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) s[j] = acc[j][0] + acc[j][1];
+
+    if (ks > 1) {
+      // the K-split waves hand their sums to the first wave of their columns
+      if (sk > 0)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) hand[sk - 1][cb][j * 4 + r][lane] = s[j][r];
+      __syncthreads();
+      if (sk == 0)
+        for (int q = 1; q < ks; ++q)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s[j][r] += hand[q - 1][cb][j * 4 + r][lane];
+    }
+
+    float o[2][4];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[j][r] = s[j][r] + pb[j][r];
+    if constexpr (LN) {
+      // the tile holds whole rows (n0 = 0); columns past N are exact zeros
+      // (zero weights and bias), so they add nothing to the sum
+      float tsum = 0.f;
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) tsum += o[j][r];
+      tsum += __shfl_xor(tsum, 16);
+      tsum += __shfl_xor(tsum, 32);
+      if (sk == 0 && lq == 0) red[0][l16][cb] = tsum;
+      __syncthreads();
+      float mu = 0.f;
+      for (int c = 0; c < ncb; ++c) mu += red[0][l16][c];
+      mu *= d.inv_n;
+      float tsq = 0.f;
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float c = cl + 16 * j + r < Nr ? o[j][r] - mu : 0.f;
+          tsq += c * c;
+        }
+      tsq += __shfl_xor(tsq, 16);
+      tsq += __shfl_xor(tsq, 32);
+      if (sk == 0 && lq == 0) red[1][l16][cb] = tsq;
+      __syncthreads();
+      float var = 0.f;
+      for (int c = 0; c < ncb; ++c) var += red[1][l16][c];
+      const float rs = __builtin_amdgcn_rsqf(var * d.inv_n + d.eps);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[j][r] = (o[j][r] - mu) * rs * pg[j][r] + pe[j][r];
+    }
+    if (sk == 0 && l16 < Mr) {
+      float* yr = (float*)d.y + (int64_t)(m0 + l16) * d.ldy + n0;
+      const bool vout = (d.vec & 2) != 0;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int c = cl + 16 * j;
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = act_apply<ACT>(o[j][r]);
+        if (vout && c + 3 < Nr) {
+          st16(yr + c, __builtin_bit_cast(u32x4, f32x4{v[0], v[1], v[2], v[3]}));
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (c + r < Nr) Elem<float>::store1(yr, c + r, v[r]);
+        }
+      }
+    }
+    __syncthreads();  // hand-over and row partials read before the next tile writes them
+  }
+}
+
 // ===================================================================== direct-to-LDS variant
 // bf16 members whose x and w rows are 16-byte aligned with K % 8 == 0. The K
 // loop stages BK = 64 columns of the x and w tiles straight from global memory
@@ -1726,7 +1922,8 @@ struct GemmVariant {
 // fp32 rows of 65 to 128 columns); 7: skinny members (every K, N <= 8), fp32 or
 // bf16, streamed with no MFMA; 8: fp32 32x128, 4 waves across the columns
 // (groups with fewer 64-row tiles than CUs); 9: streaming bf16 members
-// (every K, N <= 64, multiples of 8, aligned rows; no fused LayerNorm).
+// (every K, N <= 64, multiples of 8, aligned rows; no fused LayerNorm); 10:
+// fp32 16x128, operands loaded straight into MFMA registers (small groups).
 static const GemmVariant kVariants[] = {
     {128, 64, 256, 4, "grouped_gemm_bf16_128x64x64_w4x1_s1"},
     {128, 128, 256, 2, "grouped_gemm_bf16_128x128x64_w2x2_s2"},
@@ -1738,6 +1935,7 @@ static const GemmVariant kVariants[] = {
     {kSkinnyRows, kSkinnyMax, 256, 4, "grouped_gemm_skinny"},
     {32, 128, 256, 2, "grouped_gemm_f32_32x128x64_w1x4_s2"},
     {kStreamRows, 64, 256, 8, "grouped_gemm_stream_bf16"},
+    {kR16Rows, kR16Cols, 256, 2, "grouped_gemm_rows16_f32_16x128_w4"},
 };
 static const int kNumVariants = (int)(sizeof(kVariants) / sizeof(kVariants[0]));
 
@@ -1813,7 +2011,7 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
       ok = skinny;
     else if (pin == 9)
       ok = dt == OPTIMUS_BF16 && !ln && gemm_stream_ok(d, G);
-    else if ((dt == OPTIMUS_F32) != (pin == 3 || pin == 6 || pin == 8))
+    else if ((dt == OPTIMUS_F32) != (pin == 3 || pin == 6 || pin == 8 || pin == 10))
       ok = false;
     else
       ok = (dt == OPTIMUS_F32 || pin < 4 || dma) && (!ln || kVariants[pin].bn >= maxN);
@@ -1823,13 +2021,13 @@ GemmConfig gemm_pick_config(optimus_dtype dt, const optimus_linear_desc* d, int3
     v = 7;
   } else if (dt == OPTIMUS_F32) {
     v = (ln && maxN > 64) ? 6 : 3;
-    // a group of fewer 64-row tiles than CUs: 32-row tiles double the
-    // workgroups and halve each one's serial MFMA work (the small fp32
-    // groups are latency bound: 15.7 -> 10.8 us for tiny_group's eight
-    // members of 512 rows)
-    double tiles64 = 0.0;
-    for (int g = 0; g < G; ++g) tiles64 += (double)((d[g].M + 63) / 64) * (double)((d[g].N + 127) / 128);
-    if (maxN > 64 && maxN <= 128 && tiles64 < device_cu_count()) v = 8;
+    // a group of fewer 32-row tiles than CUs is latency bound: 16-row tiles
+    // with register-direct operands halve each workgroup's serial MFMA work
+    // and spread it over twice the CUs (tiny_group's eight members of 512
+    // rows: 15.7 us on 64-row tiles, 9.2 on 32-row tiles)
+    double tiles32 = 0.0;
+    for (int g = 0; g < G; ++g) tiles32 += (double)((d[g].M + 31) / 32) * (double)((d[g].N + 127) / 128);
+    if (tiles32 < device_cu_count() && maxK <= 1024) v = 10;
   } else if (maxN <= 64 && maxK <= 64) {
     v = (!ln && gemm_stream_ok(d, G)) ? 9 : 0;
   } else if (tiles256 >= 0.5 * device_cu_count() || (ln && maxN > 128)) {
@@ -1918,6 +2116,25 @@ static hipError_t launch_shape(optimus_act act, bool ln, const DevLinear* descs,
   return hipGetLastError();
 }
 
+static hipError_t launch_rows16(optimus_act act, bool ln, const DevLinear* descs, const GemmTile* tiles, int32_t n,
+                               int32_t grid, hipStream_t stream, int* occ) {
+#define OPTIMUS_R16_LAUNCH(A)                                                 \
+  if (ln)                                                                     \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_rows16_kernel<(A) | 8>), 0, 256) \
+  else                                                                        \
+    OPTIMUS_LAUNCH_ONE((grouped_gemm_rows16_kernel<(A)>), 0, 256)
+  switch (act) {
+    case OPTIMUS_ACT_NONE: OPTIMUS_R16_LAUNCH(0); break;
+    case OPTIMUS_ACT_RELU: OPTIMUS_R16_LAUNCH(1); break;
+    case OPTIMUS_ACT_SIGMOID: OPTIMUS_R16_LAUNCH(2); break;
+    case OPTIMUS_ACT_TANH: OPTIMUS_R16_LAUNCH(3); break;
+    case OPTIMUS_ACT_SILU: OPTIMUS_R16_LAUNCH(4); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef OPTIMUS_R16_LAUNCH
+  return hipGetLastError();
+}
+
 // Backward GEMM instances: no bias, no activation, no LayerNorm.
 template <typename T, int BM, int BN, int BK, int WM, int WN, int STAGES>
 static hipError_t launch_trans(int tr, const DevLinear* descs, const GemmTile* tiles, int32_t n, int32_t grid,
@@ -1996,6 +2213,9 @@ static hipError_t gemm_dispatch(const GemmConfig& cfg, optimus_dtype dt, optimus
     case 5: return launch_dma<128, 128, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 6: return launch_shape<float, 64, 128, 64, 2, 2, 2>(act, ln, descs, tiles, n, grid, stream, occ);
     case 8: return launch_shape<float, 32, 128, 64, 1, 4, 2, 4>(act, ln, descs, tiles, n, grid, stream, occ);
+    case 10:
+      if (dt != OPTIMUS_F32) return hipErrorInvalidValue;
+      return launch_rows16(act, ln, descs, tiles, n, grid, stream, occ);
     case 9:
       if (ln || dt != OPTIMUS_BF16) return hipErrorInvalidValue;
       return launch_stream(act, descs, tiles, n, grid, stream, occ);

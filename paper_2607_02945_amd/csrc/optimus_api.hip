@@ -418,7 +418,7 @@ static optimus_status parse_options(const optimus_plan_options* o, PlanOpts& po)
   po = PlanOpts{};
   if (!o) return OPTIMUS_OK;
   if (o->reserved != 0) return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: reserved must be 0");
-  if (o->gemm_tile < OPTIMUS_TILE_AUTO || o->gemm_tile > OPTIMUS_TILE_BF16_STREAM)
+  if (o->gemm_tile < OPTIMUS_TILE_AUTO || o->gemm_tile > OPTIMUS_TILE_F32_16X128)
     return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: unknown gemm_tile %d", (int)o->gemm_tile);
   if (o->wgrad_splits < 0 || o->wgrad_splits > 16)
     return fail(OPTIMUS_ERR_INVALID_ARG, "plan options: wgrad_splits %d outside 0..16", (int)o->wgrad_splits);

@@ -79,13 +79,14 @@ def test_every_bf16_tile_variant(variant):
         _check(ms, ys, "bf16", "tanh", f"variant {variant} {mode}")
 
 
-@pytest.mark.parametrize("variant", [3, 6, 8])
+@pytest.mark.parametrize("variant", [3, 6, 8, 10])
 def test_every_fp32_tile_variant(variant):
-    """The fp32 tiles, 64x64 (3), 64x128 (6) and 32x128 (8: every K step's
+    """The fp32 tiles, 64x64 (3), 64x128 (6), 32x128 (8: every K step's
     loads in flight at once when K <= 256, and the two wave pairs splitting K
-    for members of N <= 64), grouped and chain, against the oracle: one to five
-    K steps, members of N <= 64 with even and odd step counts, a member wider
-    than one tile."""
+    for members of N <= 64) and 16x128 (10: operands straight into MFMA
+    registers in batches of 8 k-groups, spare waves splitting K two or four
+    ways), grouped and chain, against the oracle: one to five K steps, members
+    of N <= 64 with even and odd step counts, a member wider than one tile."""
     say(f"[linear fp32 variant] {variant}")
     shapes = [(513, 120, 136), (300, 60, 200), (90, 33, 130), (257, 64, 260), (31, 7, 40), (130, 200, 64)]
     ms = _members(shapes, "fp32", seed=15 + variant)

@@ -63,8 +63,9 @@ CASES = {
     "bf16_rows_64_one_step": ([(900, 64, 64), (130, 48, 16), (33, 16, 40)], "bf16", "grouped_gemm_bf16_128x64"),
     "bf16_unaligned_k": ([(400, 256, 100), (77, 250, 13)], "bf16", "grouped_gemm_bf16_256x256"),
     "bf16_unaligned_k_128": ([(400, 128, 100), (77, 90, 13)], "bf16", "grouped_gemm_bf16_128x128"),
-    "fp32_rows_64": ([(512, 64, 64), (512, 64, 256), (100, 33, 40)], "fp32", "grouped_gemm_f32_64x64"),
-    "fp32_rows_128_few_tiles": ([(512, 128, 128), (512, 64, 256), (150, 100, 24)], "fp32", "grouped_gemm_f32_32x128"),
+    "fp32_rows_64": ([(8192, 64, 64), (4096, 64, 256), (100, 33, 40)], "fp32", "grouped_gemm_f32_64x64"),
+    "fp32_rows_64_few_tiles": ([(512, 64, 64), (512, 64, 256), (100, 33, 40)], "fp32", "grouped_gemm_rows16_f32_16x128"),
+    "fp32_rows_128_few_tiles": ([(512, 128, 128), (512, 64, 256), (150, 100, 24)], "fp32", "grouped_gemm_rows16_f32_16x128"),
     "fp32_rows_128": ([(8192, 128, 128), (8192, 64, 72), (150, 100, 24)], "fp32", "grouped_gemm_f32_64x128"),
 }
 
@@ -169,19 +170,20 @@ def test_direct_to_lds_layernorm_every_element_multi_tile(variant):
     _check(ms, ys, "bf16", "tanh", f"variant {variant} multi-tile")
 
 
-@pytest.mark.parametrize("variant", [3, 6, 8])
+@pytest.mark.parametrize("variant", [3, 6, 8, 10])
 def test_every_fp32_variant(variant):
     """The fp32 tiles that can hold the rows (3: 64x64 for N <= 64; 6: 64x128;
-    8: 32x128, the planner's choice for groups of fewer 64-row tiles than
-    CUs, with its K split over the wave pairs for members of N <= 64),
-    grouped and chain, ragged rows and K, against the oracle's fused
-    composition."""
-    bn = {3: 64, 6: 128, 8: 128}[variant]
+    8: 32x128 with its K split over the wave pairs for members of N <= 64;
+    10: 16x128 with register-direct operands, the planner's choice for groups
+    of fewer 32-row tiles than CUs, its spare waves splitting K for members of
+    N <= 64 or <= 32), grouped and chain, ragged rows and K, against the
+    oracle's fused composition."""
+    bn = {3: 64, 6: 128, 8: 128, 10: 128}[variant]
     shapes = [(513, bn, 136), (100, bn - 4, 40), (31, 16, 24), (257, bn // 2, 260), (300, 60, 200), (90, 33, 130)]
     say(f"[linear+ln fp32 variant] {variant}")
     ms = _members(shapes, "fp32", seed=170 + variant)
     for mode in ["grouped", "chain"]:
         ys, name = _run(ms, "tanh", mode=mode, variant=variant)
         assert name.startswith({3: "grouped_gemm_f32_64x64", 6: "grouped_gemm_f32_64x128",
-                                8: "grouped_gemm_f32_32x128"}[variant]), name
+                                8: "grouped_gemm_f32_32x128", 10: "grouped_gemm_rows16_f32_16x128"}[variant]), name
         _check(ms, ys, "fp32", "tanh", f"fp32 variant {variant} {mode}")
