@@ -23,6 +23,9 @@ warm-ups, 100 repetitions) with one event pair per step: p10 / median / p90.
 / WRITE_SIZE summary when that was taken on the current kernel sources.
 `plan_us` is the host time to build and upload the op-group's plans (the
 analogue of the paper's compile time; outside every timed region).
+`torch_eager` times the forward op-groups as PyTorch eager ops, one call per
+member and operator (the vendor BLAS for the Linears): context for `chain`,
+the per-op launches of this library's own kernels; never part of `value`.
 
 Workloads (the seeded groups of paper_2607_02945_amd.synth): large_group
 (default; G=32 bf16 Linear, B=16384, K=1024, then LayerNorm + tanh),
@@ -99,6 +102,7 @@ class OpGroup:
         self.two_launch = []   # launch_bound only: the Linear, then a grouped pointwise launch
         self.pw_only = []      # launch_bound only: that grouped pointwise launch alone
         self.plan_s = 0.0      # host time spent building the grouped plans
+        self.eager = None      # the op-group as PyTorch eager ops, one call per member and operator
 
     def plan(self, fn, *args, **kw):
         """Build one plan of the optimized program, timing its creation."""
@@ -108,6 +112,9 @@ class OpGroup:
         return p
 
     def run(self, which, stream=None):
+        if which == "eager":
+            self.eager()
+            return
         for plan, mode in getattr(self, which):
             plan.execute(mode, stream)
 
@@ -142,6 +149,7 @@ def build_copy(name, wl, torch, B):
                 # the same op-group as two grouped launches: Linear, then the
                 # grouped pointwise activation over its outputs
                 og.two_launch = [(lin0, "grouped"), (pw, "grouped")]
+            og.eager = _eager_linear(torch, xs, ws, bs, None, None, 0.0, wl.act)
             if name == "decompose_mm":
                 # the same group through the tiled fp32 MFMA GEMM (the paper's "before")
                 og.tiled = [(B.optimus_plan_linear_ex(xs, ws, bs, ys, wl.act, options={"gemm_tile": "f32_64x64"}),
@@ -164,6 +172,7 @@ def build_copy(name, wl, torch, B):
             ln0 = B.optimus_plan_layernorm(ys, z1, gs, be, wl.eps, "none")
             pw = B.optimus_plan_pointwise(z1, zs, wl.act)
             og.chain = [(lin, "chain"), (ln0, "chain"), (pw, "chain")]
+            og.eager = _eager_linear(torch, xs, ws, bs, gs, be, wl.eps, wl.act)
             og.keep = (xs, ws, bs, ys, zs, gs, be, z1)
     elif name == "split_op_cat":
         x = cu(wl.x)
@@ -174,6 +183,13 @@ def build_copy(name, wl, torch, B):
         og.grouped = [(soc, "grouped")]
         og.chain = [(soc, "chain")]
         og.horizontal = [(soc, "horizontal")]
+        F = torch.nn.functional
+        act = _torch_act(torch, wl.act)
+
+        def eager():
+            pieces = x.split(list(wl.widths), dim=1)
+            return torch.cat([act(F.layer_norm(p, (p.shape[1],), g, b, wl.eps)) for p, g, b in zip(pieces, gs, bs)], dim=1)
+        og.eager = eager
         og.keep = (x, y, gs, bs)
     elif name == "act_quant":
         # forward: the saved activations to E4M3 codes with per-tensor scales;
@@ -259,8 +275,36 @@ def build_copy(name, wl, torch, B):
         l1n = B.optimus_plan_linear(xs, w1, b1, h0, "none")
         relu = B.optimus_plan_pointwise(h0, h, "relu")
         og.chain = [(l1n, "chain"), (relu, "chain"), (l2, "chain"), (ln, "chain")]
+        F = torch.nn.functional
+
+        def eager():
+            return [F.layer_norm(F.linear(torch.relu(F.linear(x, a, c)), w, v), (w.shape[0],), g, e, wl.eps)
+                    for x, a, c, w, v, g, e in zip(xs, w1, b1, w2, b2, gm, be)]
+        og.eager = eager
         og.keep = (xs, h, o, z, w1, b1, w2, b2, gm, be, h0)
     return og
+
+
+def _torch_act(torch, act):
+    return {"none": lambda t: t, "relu": torch.relu, "sigmoid": torch.sigmoid, "tanh": torch.tanh,
+            "silu": torch.nn.functional.silu}[act]
+
+
+def _eager_linear(torch, xs, ws, bs, gs, be, eps, act):
+    """The Linear group (+ LayerNorm) + activation as PyTorch eager ops, one
+    call per member and operator (the vendor BLAS for the Linear)."""
+    F = torch.nn.functional
+    a = _torch_act(torch, act)
+
+    def eager():
+        out = []
+        for i, (x, w, b) in enumerate(zip(xs, ws, bs)):
+            t = F.linear(x, w, b)
+            if gs is not None:
+                t = F.layer_norm(t, (w.shape[0],), gs[i], be[i], eps)
+            out.append(a(t))
+        return out
+    return eager
 
 
 def workload_bytes(name, wl):
@@ -801,6 +845,15 @@ def main():
                         "launches_per_group": sum(p.info()["chain_launches"] for p, m in ogs[0].chain
                                                   if m == "chain") + sum(1 for p, m in ogs[0].chain if m != "chain"),
                         "speedup": round(c_step / ms_step, 2)}
+    if ogs[0].eager is not None and not args.no_chain:
+        # the same op-group as PyTorch eager ops (context: what the model ran
+        # before the rewrite, with the vendor BLAS for its Linears)
+        esteps = max(5, min(args.steps, 50))
+        e_ms, _ = timed("eager", esteps, args.warmup)
+        e_step = e_ms / esteps
+        out["torch_eager"] = {"us_per_group": round(e_step * 1000.0, 3), "speedup": round(e_step / ms_step, 2),
+                              "ops": "torch.nn.functional per member and operator (linear, layer_norm, activation; "
+                                     "split and cat for split-op-cat)"}
     if ogs[0].two_launch:
         # the Linear and the activation as two grouped launches; the grouped
         # pointwise kernel's own roofline
