@@ -632,6 +632,7 @@ def kernel_symbol(label):
                         ("grouped_dequantize_fp8", "grouped_dequantize_fp8_kernel"),
                         ("grouped_gemm_dma", "grouped_gemm_dma_kernel"), ("grouped_gemm_skinny", "grouped_gemm_skinny_kernel"),
                         ("grouped_gemm_stream", "grouped_gemm_stream_kernel"),
+                        ("grouped_gemm_rows16", "grouped_gemm_rows16_kernel"),
                         ("grouped_gemm", "grouped_gemm_kernel"), ("split_op_cat_fused", "split_op_cat_kernel"),
                         ("grouped_layernorm", "grouped_layernorm_kernel"), ("grouped_pointwise", "grouped_pointwise_kernel")):
         if label.startswith(prefix):
@@ -644,6 +645,7 @@ def kernel_symbol(label):
 KERNEL_SOURCES = {
     "grouped_gemm_kernel": "kernels_gemm.hip", "grouped_gemm_dma_kernel": "kernels_gemm.hip",
     "grouped_gemm_skinny_kernel": "kernels_gemm.hip", "grouped_gemm_stream_kernel": "kernels_gemm.hip",
+    "grouped_gemm_rows16_kernel": "kernels_gemm.hip",
     "split_op_cat_kernel": "kernels_rowwise.hip",
     "grouped_layernorm_kernel": "kernels_rowwise.hip", "grouped_pointwise_kernel": "kernels_rowwise.hip",
     "grouped_quantize_fp8_scaled_kernel": "kernels_fp8.hip", "grouped_quantize_fp8_kernel": "kernels_fp8.hip",
