@@ -419,21 +419,6 @@ hipError_t layernorm_backward_launch(optimus_dtype dt, optimus_act act, const De
   return hipGetLastError();
 }
 
-int act_backward_blocks_per_cu(optimus_dtype dt, optimus_act act) {
-  const void* k = nullptr;
-  if (dt == OPTIMUS_BF16) {
-    OPTIMUS_BWD_ACT_SWITCH(act, k = (const void*)grouped_act_backward_kernel<bf16_t, A>);
-  } else {
-    OPTIMUS_BWD_ACT_SWITCH(act, k = (const void*)grouped_act_backward_kernel<float, A>);
-  }
-  int b = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k, kRowThreads, 0) != hipSuccess || b < 1) {
-    (void)hipGetLastError();
-    return 4;
-  }
-  return b;
-}
-
 int layernorm_backward_resident_per_cu(optimus_dtype dt, optimus_act act) {
   const void* k = nullptr;
   if (dt == OPTIMUS_BF16) {

@@ -472,19 +472,4 @@ hipError_t fp8_dequantize_launch(optimus_dtype dt, const DevFp8* descs, const Fp
   return hipGetLastError();
 }
 
-int fp8_blocks_per_cu(optimus_dtype dt, int kernel) {
-  const bool b = dt == OPTIMUS_BF16;
-  const void* k = kernel == 1   ? (b ? (const void*)grouped_quantize_fp8_scaled_kernel<bf16_t>
-                                     : (const void*)grouped_quantize_fp8_scaled_kernel<float>)
-                  : kernel == 0 ? (b ? (const void*)grouped_quantize_fp8_kernel<bf16_t>
-                                     : (const void*)grouped_quantize_fp8_kernel<float>)
-                  : kernel == 3 ? (b ? (const void*)grouped_fp8_amax_kernel<bf16_t>
-                                     : (const void*)grouped_fp8_amax_kernel<float>)
-                                : (b ? (const void*)grouped_dequantize_fp8_kernel<bf16_t>
-                                     : (const void*)grouped_dequantize_fp8_kernel<float>);
-  int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kFp8Threads, 0) != hipSuccess || n < 1) n = 4;
-  return n;
-}
-
 }  // namespace optimus

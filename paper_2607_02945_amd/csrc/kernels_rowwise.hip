@@ -544,27 +544,6 @@ hipError_t pointwise_launch(optimus_dtype dt, optimus_act act, const DevRows* de
   return hipGetLastError();
 }
 
-// Workgroups of the LayerNorm (or pointwise) instance for (dt, act) that the
-// runtime reports resident on one CU: persistent row grids are sized by it
-// (a grid past it leaves late workgroups to start their whole share after
-// the first ones finish).
-int rowwise_blocks_per_cu(optimus_dtype dt, optimus_act act, bool layernorm) {
-  const void* k = nullptr;
-  auto pick = [&](auto tag) -> hipError_t {
-    using T = decltype(tag);
-    OPTIMUS_ACT_SWITCH(act, k = layernorm ? (const void*)grouped_layernorm_kernel<T, A>
-                                          : (const void*)grouped_pointwise_kernel<T, A>);
-    return hipSuccess;
-  };
-  if ((dt == OPTIMUS_BF16 ? pick(bf16_t{}) : pick(float{})) != hipSuccess || !k) return 4;
-  int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kRowThreads, 0) != hipSuccess || n < 1) {
-    (void)hipGetLastError();
-    return 4;
-  }
-  return n;
-}
-
 template <typename T, int ACT, int S, int WPR, bool FULL>
 static const void* soc_kernel_ptr() {
   return (const void*)split_op_cat_kernel<T, ACT, S, WPR, FULL>;

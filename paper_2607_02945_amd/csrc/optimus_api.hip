@@ -574,13 +574,15 @@ static void add_row_tiles(std::vector<RowTile>& tiles, int member, const DevRows
     tiles.push_back(RowTile{member, (int32_t)r0, (int32_t)std::min<int64_t>(per, r.rows - r0), 0});
 }
 
-// Persistent row grid: no more workgroups than are resident at once
-// (per_cu: the kernel instance's occupancy; one past it starts late with a
-// whole share: large_group's LayerNorm + tanh took 237 us at 8 per CU
-// requested, 229 us at the 5 that fit).
-static int32_t row_grid(int64_t tiles, int per_cu) {
-  const int64_t cap = (int64_t)device_cu_count() * std::max(1, std::min(per_cu, 8));
-  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(tiles, cap));
+// Row-wise grids: one workgroup per tile. The hardware dispatcher refills a
+// CU as soon as one of its workgroups ends, so short-lived workgroups keep
+// every CU streaming to the end of the launch; a persistent grid of the
+// resident workgroups, each walking its share of tiles, left the CUs that
+// finished early idle (large_group's LayerNorm + tanh: 229 us persistent,
+// 237 us with more workgroups than fit, 209 us with one per 32 KB tile; the
+// fp8 codec's dequantize 171 -> 163 us).
+static int32_t row_grid(int64_t tiles) {
+  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(tiles, (int64_t)1 << 30));
 }
 
 // Balanced row segments for a grouped row launch of `resident` workgroups:
@@ -628,7 +630,6 @@ static int64_t balanced_row_segments(const std::vector<int64_t>& rows, const std
 // LayerNorm + tanh. The hardware spreads the small tiles better.)
 static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool layernorm, size_t s,
                        optimus_act act) {
-  const int per_cu = rowwise_blocks_per_cu(hp.dt, act, layernorm);
   std::vector<RowTile> tiles;
   hp.rows_chain.clear();
   for (size_t g = 0; g < members.size(); ++g) {
@@ -641,9 +642,9 @@ static void build_rows(HostPlan& hp, const std::vector<DevRows>& members, bool l
   for (auto& c : hp.rows_chain) {
     c.descs_off = doff;
     c.tiles_off = toff;
-    c.grid = row_grid(c.num_tiles, per_cu);
+    c.grid = row_grid(c.num_tiles);
   }
-  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size(), per_cu)};
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
   hp.row_kernel = layernorm ? KIND_LN : KIND_PW;
   hp.work_items = (int64_t)tiles.size();
   hp.grid = hp.rows.grid;
@@ -821,7 +822,7 @@ static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, in
                                   const void* gamma, int64_t rows, int64_t cols, float eps, optimus_dtype dt,
                                   bool layernorm);
 static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
-                                           std::vector<int>& ntiles, int64_t max_tiles, int per_cu);
+                                           std::vector<int>& ntiles, int64_t max_tiles);
 
 // act != NONE: dX leaves with the activation backward of the layer below
 // applied, dX * act'(act_x[g]) (act_x [M][K], row stride ld_act_x[g]).
@@ -1005,7 +1006,7 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
                                     d[g].lddx, nullptr, has ? d[g].M : 0, d[g].K, 0.f, dt, false));
       }
       std::vector<int> nt;
-      std::vector<RowTile> rt = grad_row_tiles(hp, rm, s, nt, 0, act_backward_blocks_per_cu(dt, act));
+      std::vector<RowTile> rt = grad_row_tiles(hp, rm, s, nt, 0);
       const size_t roff = hp.blob.add(rm.data(), rm.size() * sizeof(DevRowsGrad));
       for (int g = 0; g < G; ++g)
         if (d[g].dx) hp.scratch_fixups.push_back(roff + g * sizeof(DevRowsGrad) + offsetof(DevRowsGrad, dy));
@@ -1014,8 +1015,7 @@ static optimus_status build_linear_backward(const optimus_linear_grad_desc* d, i
         c.descs_off = roff;
         c.tiles_off = rtoff;
       }
-      hp.rows = RowLaunch{roff, rtoff, 0, (int32_t)rt.size(),
-                          row_grid((int64_t)rt.size(), act_backward_blocks_per_cu(dt, act))};
+      hp.rows = RowLaunch{roff, rtoff, 0, (int32_t)rt.size(), row_grid((int64_t)rt.size())};
     }
   }
   hp.red_chain.assign(G, RowLaunch{});
@@ -1173,7 +1173,7 @@ static DevRowsGrad make_rows_grad(const void* x, int64_t ldx, const void* dy, in
 // partial row of dgamma / dbeta that the finalize reads back).
 static constexpr int64_t kGradMaxTilesPerMember = 64;
 static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRowsGrad>& members, size_t s,
-                                           std::vector<int>& ntiles, int64_t max_tiles, int per_cu) {
+                                           std::vector<int>& ntiles, int64_t max_tiles) {
   std::vector<RowTile> tiles;
   hp.rows_chain.clear();
   ntiles.assign(members.size(), 0);
@@ -1189,7 +1189,7 @@ static std::vector<RowTile> grad_row_tiles(HostPlan& hp, const std::vector<DevRo
       tiles.push_back(RowTile{(int)g, (int32_t)r0, (int32_t)std::min<int64_t>(per, m.rows - r0), 0});
     for (int t = first; t < (int)tiles.size(); ++t) tiles[t].pad = t - first;
     ntiles[g] = (int)tiles.size() - first;
-    hp.rows_chain.push_back(RowLaunch{0, 0, first, ntiles[g], row_grid(ntiles[g], per_cu)});
+    hp.rows_chain.push_back(RowLaunch{0, 0, first, ntiles[g], row_grid(ntiles[g])});
   }
   return tiles;
 }
@@ -1219,8 +1219,7 @@ static optimus_status build_layernorm_backward(const optimus_layernorm_grad_desc
   // member has one dgamma / dbeta partial row per segment (about one per
   // workgroup that touches it), not per tile.
   std::vector<int> ntiles;
-  std::vector<RowTile> chain_tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember,
-                                                    layernorm_backward_resident_per_cu(dt, act));
+  std::vector<RowTile> chain_tiles = grad_row_tiles(hp, members, s, ntiles, kGradMaxTilesPerMember);
   std::vector<int> nseg;
   std::vector<RowTile> tiles;
   int64_t B;
@@ -1317,15 +1316,14 @@ static optimus_status build_act_backward(const optimus_act_grad_desc* d, int32_t
     hp.bytes += (double)s * 3.0 * m.rows * m.cols;
   }
   std::vector<int> ntiles;
-  const int per_cu = act_backward_blocks_per_cu(dt, act);
-  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles, 0, per_cu);
+  std::vector<RowTile> tiles = grad_row_tiles(hp, members, s, ntiles, 0);
   const size_t doff = hp.blob.add(members.data(), members.size() * sizeof(DevRowsGrad));
   const size_t toff = hp.blob.add(tiles.data(), tiles.size() * sizeof(RowTile));
   for (auto& c : hp.rows_chain) {
     c.descs_off = doff;
     c.tiles_off = toff;
   }
-  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size(), per_cu)};
+  hp.rows = RowLaunch{doff, toff, 0, (int32_t)tiles.size(), row_grid((int64_t)tiles.size())};
   hp.work_items = (int64_t)tiles.size();
   hp.grid = hp.rows.grid;
   hp.block = kRowThreads;
@@ -1568,16 +1566,11 @@ static void fp8_items(const Fp8Geom& g, int member, int64_t rows, int64_t budget
   }
 }
 
-static int32_t fp8_grid(int64_t items, optimus_dtype dt, int kernel) {
-  const int64_t cap = (int64_t)device_cu_count() * fp8_blocks_per_cu(dt, kernel);
-  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(items, cap));
-}
 
 // Shared by quantize and dequantize: the member table and item lists.
 // Grouped: (scaled: the amax items, then) the convert items, member order.
 // CHAIN: per member, its own items.
-static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vector<Fp8Geom>& geo, bool scaled,
-                      int kernel) {
+static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vector<Fp8Geom>& geo, bool scaled) {
   const int G = (int)members.size();
   std::vector<std::vector<Fp8Item>> conv(G), amax(G);
   int32_t nslots = 0;
@@ -1597,21 +1590,22 @@ static void build_fp8(HostPlan& hp, std::vector<DevFp8>& members, const std::vec
     }
   }
   std::vector<Fp8Item> items;
-  auto add = [&](const std::vector<Fp8Item>& v, int kern) {
+  // one workgroup per item, as for the row-wise grids
+  auto add = [&](const std::vector<Fp8Item>& v) {
     const int32_t first = (int32_t)items.size();
     items.insert(items.end(), v.begin(), v.end());
-    return RowLaunch{0, 0, first, (int32_t)v.size(), fp8_grid((int64_t)v.size(), hp.dt, kern)};
+    return RowLaunch{0, 0, first, (int32_t)v.size(), row_grid((int64_t)v.size())};
   };
   std::vector<Fp8Item> all_a, all_c;
   for (int g = 0; g < G; ++g) all_a.insert(all_a.end(), amax[g].begin(), amax[g].end());
   for (int g = 0; g < G; ++g) all_c.insert(all_c.end(), conv[g].begin(), conv[g].end());
-  hp.q_amax = scaled ? add(all_a, 3) : RowLaunch{};
-  hp.q_grouped = add(all_c, kernel);
+  hp.q_amax = scaled ? add(all_a) : RowLaunch{};
+  hp.q_grouped = add(all_c);
   hp.q_chain.clear();
   hp.q_chain_amax.clear();
   for (int g = 0; g < G; ++g) {
-    if (scaled) hp.q_chain_amax.push_back(add(amax[g], 3));
-    hp.q_chain.push_back(add(conv[g], kernel));
+    if (scaled) hp.q_chain_amax.push_back(add(amax[g]));
+    hp.q_chain.push_back(add(conv[g]));
   }
   hp.q_scaled = scaled;
   hp.q_descs_off = hp.blob.add(members.data(), members.size() * sizeof(DevFp8));
@@ -1641,7 +1635,7 @@ static optimus_status build_quantize_fp8(const optimus_fp8_quant_desc* d, int32_
     geo.push_back(fp8_geom(m.x, m.ldx, m.q, m.ldq, m.cols, dt));
     hp.bytes += (double)m.rows * m.cols * (double)(s + 1) + (use_scaling ? 4.0 : 0.0);
   }
-  build_fp8(hp, members, geo, use_scaling != 0, use_scaling ? 1 : 0);
+  build_fp8(hp, members, geo, use_scaling != 0);
   hp.kernel = std::string(use_scaling ? "grouped_quantize_fp8_scaled_" : "grouped_quantize_fp8_") +
               (dt == OPTIMUS_F32 ? "f32" : "bf16");
   return OPTIMUS_OK;
@@ -1664,7 +1658,7 @@ static optimus_status build_dequantize_fp8(const optimus_fp8_dequant_desc* d, in
     geo.push_back(fp8_geom(m.y, m.ldy, m.q, m.ldq, m.cols, dt));
     hp.bytes += (double)m.rows * m.cols * (double)(s + 1) + (m.scale ? 4.0 : 0.0);
   }
-  build_fp8(hp, members, geo, false, 2);
+  build_fp8(hp, members, geo, false);
   hp.kernel = std::string("grouped_dequantize_fp8_") + (dt == OPTIMUS_F32 ? "f32" : "bf16");
   return OPTIMUS_OK;
 }
@@ -2040,32 +2034,26 @@ extern "C" optimus_status optimus_plan_execute_mode(optimus_plan p, optimus_exec
   const int n = hp.G;
   hipError_t e = hipSuccess;
   if (mode == OPTIMUS_EXEC_HORIZONTAL) {
-    const int ln_cu = rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, ln_on);
-    const int32_t T = hp.soc_piece_tiles_total, grid = row_grid(T, ln_cu);
+    const int32_t T = hp.soc_piece_tiles_total, grid = row_grid(T);
     e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tl, T, grid, st)
               : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tl, T, grid, st);
-    const int32_t pgrid = row_grid(T, rowwise_blocks_per_cu(hp.dt, hp.act, false));
-    const int32_t cgrid = row_grid(T, rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, false));
-    if (e == hipSuccess) e = pointwise_launch(hp.dt, hp.act, act, tl, T, pgrid, st);
-    if (e == hipSuccess) e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, cgrid, st);
+    if (e == hipSuccess) e = pointwise_launch(hp.dt, hp.act, act, tl, T, grid, st);
+    if (e == hipSuccess) e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, grid, st);
   } else {
-    const int ln_cu = rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, ln_on);
-    const int pw_cu = rowwise_blocks_per_cu(hp.dt, hp.act, false);
-    const int cat_cu = rowwise_blocks_per_cu(hp.dt, OPTIMUS_ACT_NONE, false);
     for (int j = 0; j < n && e == hipSuccess; ++j) {
       const RowTile* tj = tl + hp.soc_piece_first[j];
       const int32_t cnt = hp.soc_piece_count[j];
-      e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt, ln_cu), st)
-                : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt, ln_cu), st);
+      e = ln_on ? layernorm_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt), st)
+                : pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, ln, tj, cnt, row_grid(cnt), st);
     }
     for (int j = 0; j < n && e == hipSuccess; ++j) {
       const RowTile* tj = tl + hp.soc_piece_first[j];
       const int32_t cnt = hp.soc_piece_count[j];
-      e = pointwise_launch(hp.dt, hp.act, act, tj, cnt, row_grid(cnt, pw_cu), st);
+      e = pointwise_launch(hp.dt, hp.act, act, tj, cnt, row_grid(cnt), st);
     }
     if (e == hipSuccess) {
       const int32_t T = hp.soc_piece_tiles_total;
-      e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, row_grid(T, cat_cu), st);
+      e = pointwise_launch(hp.dt, OPTIMUS_ACT_NONE, cat, tl, T, row_grid(T), st);
     }
   }
   return e == hipSuccess ? OPTIMUS_OK : hip_fail(e, "execute: split-op-cat unfused launch");

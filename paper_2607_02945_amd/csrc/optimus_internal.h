@@ -155,8 +155,6 @@ hipError_t layernorm_launch(optimus_dtype dt, optimus_act act, const DevRows* de
                             int32_t num_tiles, int32_t grid, hipStream_t stream);
 hipError_t pointwise_launch(optimus_dtype dt, optimus_act act, const DevRows* descs, const RowTile* tiles,
                             int32_t num_tiles, int32_t grid, hipStream_t stream);
-// Workgroups of the LayerNorm (layernorm) or pointwise instance resident per CU.
-int rowwise_blocks_per_cu(optimus_dtype dt, optimus_act act, bool layernorm);
 
 constexpr int kSocThreads = 256;
 constexpr int kSocMaxChunks = 1024;  // 16-byte chunks per row held in registers by two waves (8 per lane)
@@ -205,8 +203,6 @@ struct GradFinItem {
 constexpr int kGradWavesPerBlock = 4;  // partial rows per tile on the per-value path
 // Workgroups of the LayerNorm-backward kernel resident on one CU.
 int layernorm_backward_resident_per_cu(optimus_dtype dt, optimus_act act);
-// Workgroups of the activation-backward instance resident on one CU.
-int act_backward_blocks_per_cu(optimus_dtype dt, optimus_act act);
 hipError_t act_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs, const RowTile* tiles,
                                int32_t num_tiles, int32_t grid, hipStream_t stream);
 hipError_t layernorm_backward_launch(optimus_dtype dt, optimus_act act, const DevRowsGrad* descs, const RowTile* tiles,
@@ -247,9 +243,6 @@ hipError_t fp8_quantize_launch(optimus_dtype dt, const DevFp8* descs, const Fp8I
                                int32_t grid, const uint32_t* slots, hipStream_t stream);
 hipError_t fp8_dequantize_launch(optimus_dtype dt, const DevFp8* descs, const Fp8Item* items, int32_t num_items,
                                  int32_t grid, hipStream_t stream);
-// Workgroups of a codec kernel resident per CU (occupancy query); kernel:
-// 0 quantize, 1 scaled convert, 2 dequantize, 3 amax.
-int fp8_blocks_per_cu(optimus_dtype dt, int kernel);
 
 int device_cu_count();
 
