@@ -31,7 +31,8 @@ Workloads (the seeded groups of paper_2607_02945_amd.synth): large_group
 (default; G=32 bf16 Linear, B=16384, K=1024, then LayerNorm + tanh),
 large_group_shared (the same members on ONE shared input), tiny_group,
 launch_bound (G=256 bf16 Linear + sigmoid, B=2048; also timed as two launches,
-Linear then grouped sigmoid), split_op_cat, towers, decompose_mm, act_quant
+Linear then grouped sigmoid: `separate_act`, as large_group is with Linear,
+LayerNorm, then grouped tanh), split_op_cat, towers, decompose_mm, act_quant
 (fp8 quantize of 32 saved activations, then dequantize), towers_bwd and
 large_group_bwd (the training backward of the towers and large_group
 op-groups).
@@ -79,11 +80,11 @@ def parse():
     ap.add_argument("--pmc-command", default="", help="command line recorded in the --pmc-summary output")
     ap.add_argument("--pmc-plan", default=None, metavar="K",
                     help="with --pmc-summary: the launch the counters cover (a plan_index of the bench line's "
-                         "roofline or other_kernels, or 'pw' for launch_bound's grouped pointwise launch); "
+                         "roofline or other_kernels, or 'pw' for the grouped pointwise launch of separate_act); "
                          "default: the dominant one")
     ap.add_argument("--only-plan", default=None, metavar="K",
                     help="time only launch K of the op-group (roofline.plan_index of a bench line picks the "
-                         "dominant one; 'pw': launch_bound's grouped pointwise launch of the two-launch form), "
+                         "dominant one; 'pw': the grouped pointwise launch of the separate-activation form), "
                          "for profiler runs")
     return ap.parse_args()
 
@@ -99,8 +100,8 @@ class OpGroup:
         self.horizontal = []   # split-op-cat only: horizontal fusion without the vertical rewrite
         self.tiled = []        # decompose_mm only: the group through the tiled GEMM kernel
         self.unscaled = []     # act_quant only: quantize without the per-tensor scale
-        self.two_launch = []   # launch_bound only: the Linear, then a grouped pointwise launch
-        self.pw_only = []      # launch_bound only: that grouped pointwise launch alone
+        self.separate = []     # the activation as its own grouped pointwise launch, after the Linear (+ LayerNorm)
+        self.pw_only = []      # that grouped pointwise launch alone
         self.plan_s = 0.0      # host time spent building the grouped plans
         self.eager = None      # the op-group as PyTorch eager ops, one call per member and operator
 
@@ -148,7 +149,7 @@ def build_copy(name, wl, torch, B):
                 og.chain = [(lin0, "chain"), (pw, "chain")]
                 # the same op-group as two grouped launches: Linear, then the
                 # grouped pointwise activation over its outputs
-                og.two_launch = [(lin0, "grouped"), (pw, "grouped")]
+                og.separate = [(lin0, "grouped"), (pw, "grouped")]
             og.eager = _eager_linear(torch, xs, ws, bs, None, None, 0.0, wl.act)
             if name == "decompose_mm":
                 # the same group through the tiled fp32 MFMA GEMM (the paper's "before")
@@ -172,6 +173,11 @@ def build_copy(name, wl, torch, B):
             ln0 = B.optimus_plan_layernorm(ys, z1, gs, be, wl.eps, "none")
             pw = B.optimus_plan_pointwise(z1, zs, wl.act)
             og.chain = [(lin, "chain"), (ln0, "chain"), (pw, "chain")]
+            if len(og.grouped) == 2:
+                # rows too wide for the GEMM epilogue: also time the op-group
+                # as three grouped launches, Linear, LayerNorm, then the
+                # activation as a grouped pointwise pass over the whole group
+                og.separate = [(lin, "grouped"), (ln0, "grouped"), (pw, "grouped")]
             og.eager = _eager_linear(torch, xs, ws, bs, gs, be, wl.eps, wl.act)
             og.keep = (xs, ws, bs, ys, zs, gs, be, z1)
     elif name == "split_op_cat":
@@ -524,8 +530,8 @@ def pmc_summary(args):
     with open(line) as f:
         bl = json.loads(f.read().splitlines()[-1])
     entries = [bl["roofline"]] + bl.get("other_kernels", [])
-    if "two_launch" in bl:
-        entries.append(dict(bl["two_launch"]["pointwise"], plan_index="pw"))
+    if "separate_act" in bl:
+        entries.append(dict(bl["separate_act"]["pointwise"], plan_index="pw"))
     want = bl["roofline"]["plan_index"] if args.pmc_plan is None else args.pmc_plan
     match = [e for e in entries if str(e.get("plan_index")) == str(want)]
     if not match:
@@ -761,11 +767,11 @@ def main():
         # one launch of the op-group alone (for rocprofv3 runs that must see
         # only that kernel)
         if args.only_plan == "pw":
-            if not ogs[0].two_launch:
-                raise SystemExit("bench.py: --only-plan pw needs a workload with a two-launch form")
+            if not ogs[0].separate:
+                raise SystemExit("bench.py: --only-plan pw needs a workload with a separate activation launch")
             for og in ogs:
-                og.pw_only = [og.two_launch[1]]
-            k, plan = "pw_only", ogs[0].two_launch[1][0]
+                og.pw_only = [og.separate[-1]]
+            k, plan = "pw_only", ogs[0].separate[-1][0]
         else:
             k = int(args.only_plan)
             plan = ogs[0].grouped[k][0]
@@ -856,20 +862,21 @@ def main():
         out["torch_eager"] = {"us_per_group": round(e_step * 1000.0, 3), "speedup": round(e_step / ms_step, 2),
                               "ops": "torch.nn.functional per member and operator (linear, layer_norm, activation; "
                                      "split and cat for split-op-cat)"}
-    if ogs[0].two_launch:
-        # the Linear and the activation as two grouped launches; the grouped
-        # pointwise kernel's own roofline
-        t_ms, _ = timed("two_launch", args.steps, args.warmup)
-        pw_plan = ogs[0].two_launch[1][0]
+    if ogs[0].separate:
+        # the activation as its own grouped launch after the Linear (and the
+        # LayerNorm); the grouped pointwise kernel's own roofline
+        t_ms, _ = timed("separate", args.steps, args.warmup)
+        pw_plan = ogs[0].separate[-1][0]
         for og in ogs:
-            og.pw_only = [og.two_launch[1]]
+            og.pw_only = [og.separate[-1]]
         p_ms, _ = timed("pw_only", args.steps, args.warmup)
         pinfo = pw_plan.info()
         pw = roofline(pinfo, p_ms / args.steps)
         pw.update({"kernel": pinfo["kernel"], "kernel_us": round(p_ms / args.steps * 1000.0, 3),
                    "algorithmic_bytes": pinfo["bytes"], "traffic": traffic_from_profile(pinfo["kernel"], args.workload, "pw")})
-        out["two_launch"] = {"us_per_group": round(t_ms / args.steps * 1000.0, 3), "launches_per_group": 2,
-                             "pointwise": pw}
+        out["separate_act"] = {"us_per_group": round(t_ms / args.steps * 1000.0, 3),
+                               "launches_per_group": sum(p.info()["launches"] for p, _ in ogs[0].separate),
+                               "pointwise": pw}
     if ogs[0].tiled:
         tsteps = max(5, min(args.steps, 20))
         t_ms, _ = timed("tiled", tsteps, args.warmup)
