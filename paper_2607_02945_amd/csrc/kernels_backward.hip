@@ -77,7 +77,12 @@ __global__ __launch_bounds__(kRowThreads) void grouped_act_backward_kernel(const
 // gamma (and beta) are staged in LDS as fp32 (sGamma, sBeta: [cols], filled
 // by the caller) and read where they are used. ACT != 0: the backward of the
 // fused LayerNorm + activation -- the incoming gradient is the activation
-// output's, and is multiplied by act'(gamma * xhat + beta), recomputed here.
+// output's, and is multiplied by act'(gamma * xhat + beta), recomputed here
+// once per value: the pass that forms the row sums leaves the products in
+// the wave's slot sPart (free until the tile's sums are written there) and
+// the output pass reads them back (the derivative is two transcendentals per
+// value; large_group's LayerNorm + tanh backward 454 -> 413 us). Keeping
+// xhat there too saved nothing.
 template <typename T, int MAXC, int ACT>
 __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile& rt, int lane, int wave,
                                              float* sPart, const float* sGamma, const float* sBeta) {
@@ -168,6 +173,8 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
       }
     }
     const float rstd = __builtin_amdgcn_rsqf(group_sum(q, L) * d.inv_cols + d.eps);
+    // this lane's products g * act' of chunk j, element group h (ACT != 0)
+    auto gslot = [&](int j, int h) { return (f32x4*)sPart + (j * (VEC / 4) + h) * 64 + lane; };
     float sg = 0.f, sgx = 0.f;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
@@ -179,6 +186,10 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
 #pragma unroll
       for (int e = 0; e < VEC; ++e) xh[e] = (x[e] - mean) * rstd;
       grad_in(j, gm, xh, g);
+      if constexpr (ACT != 0) {
+#pragma unroll
+        for (int h = 0; h < VEC / 4; ++h) *gslot(j, h) = f32x4{g[4 * h], g[4 * h + 1], g[4 * h + 2], g[4 * h + 3]};
+      }
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
         const float gg = g[e] * gm[e];
@@ -195,11 +206,21 @@ __device__ __forceinline__ void lnb_rows_vec(const DevRowsGrad& d, const RowTile
       if (valid && c < cpr) {
         float x[VEC], g[VEC], gm[VEC], o[VEC], xh[VEC];
         Elem<T>::unpack(cx[j], x);
-        Elem<T>::unpack(cg[j], g);
         gamma_of(j, gm);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) xh[e] = (x[e] - mean) * rstd;
-        grad_in(j, gm, xh, g);
+        if constexpr (ACT != 0) {
+#pragma unroll
+          for (int h = 0; h < VEC / 4; ++h) {
+            const f32x4 v = *gslot(j, h);
+            g[4 * h] = v.x;
+            g[4 * h + 1] = v.y;
+            g[4 * h + 2] = v.z;
+            g[4 * h + 3] = v.w;
+          }
+        } else {
+          Elem<T>::unpack(cg[j], g);
+        }
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
           o[e] = rstd * (g[e] * gm[e] - mg - xh[e] * mgx);
