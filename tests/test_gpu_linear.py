@@ -85,10 +85,13 @@ def test_every_fp32_tile_variant(variant):
     loads in flight at once when K <= 256, and the two wave pairs splitting K
     for members of N <= 64) and 16x128 (10: operands straight into MFMA
     registers in batches of 8 k-groups, spare waves splitting K two or four
-    ways), grouped and chain, against the oracle: one to five K steps, members
-    of N <= 64 with even and odd step counts, a member wider than one tile."""
+    ways), grouped and chain, against the oracle: one to ten K steps (38
+    k-groups: the 16-row kernel's batch loop turns over more than once),
+    members of N <= 64 with even and odd step counts, a member wider than one
+    tile."""
     say(f"[linear fp32 variant] {variant}")
-    shapes = [(513, 120, 136), (300, 60, 200), (90, 33, 130), (257, 64, 260), (31, 7, 40), (130, 200, 64)]
+    shapes = [(513, 120, 136), (300, 60, 200), (90, 33, 130), (257, 64, 260), (31, 7, 40), (130, 200, 64),
+              (40, 100, 600)]
     ms = _members(shapes, "fp32", seed=15 + variant)
     for mode in ["grouped", "chain"]:
         ys = _run(ms, "fp32", "sigmoid", mode=mode, variant=variant)

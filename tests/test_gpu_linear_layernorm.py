@@ -179,7 +179,8 @@ def test_every_fp32_variant(variant):
     N <= 64 or <= 32), grouped and chain, ragged rows and K, against the
     oracle's fused composition."""
     bn = {3: 64, 6: 128, 8: 128, 10: 128}[variant]
-    shapes = [(513, bn, 136), (100, bn - 4, 40), (31, 16, 24), (257, bn // 2, 260), (300, 60, 200), (90, 33, 130)]
+    shapes = [(513, bn, 136), (100, bn - 4, 40), (31, 16, 24), (257, bn // 2, 260), (300, 60, 200), (90, 33, 130),
+              (40, bn - 28, 600)]
     say(f"[linear+ln fp32 variant] {variant}")
     ms = _members(shapes, "fp32", seed=170 + variant)
     for mode in ["grouped", "chain"]:
