@@ -24,6 +24,8 @@ warm-ups, 100 repetitions) with one event pair per step: p10 / median / p90.
 `plan_us` is the host time to build and upload the op-group's plans (the
 analogue of the paper's compile time; outside every timed region). `warm`
 repeats the op-group on one copy (caches may hold its inputs): secondary.
+`graph` replays the op-group and the chain from HIP graphs (one per input
+copy): the host's launch cost drops out of both.
 `torch_eager` times the forward op-groups as PyTorch eager ops, one call per
 member and operator (the vendor BLAS for the Linears): context for `chain`,
 the per-op launches of this library's own kernels; never part of `value`.
@@ -710,7 +712,26 @@ def main():
         og.run("grouped", stream)
     torch.cuda.synchronize()
 
+    graphs = {}
+
+    def capture(which):
+        """One HIP graph per input copy holding the op-group's launches in
+        mode `which` (plans launch kernels only, so they can be recorded)."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        out = []
+        for og in ogs:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                og.run(which)
+            out.append(g)
+        torch.cuda.synchronize()
+        graphs["graph_" + which] = out
+
     def one(i, which):
+        if which in graphs:
+            graphs[which][i % copies].replay()
+            return
         if which == "warm":
             ogs[0].run("grouped", stream)
             return
@@ -861,6 +882,17 @@ def main():
                         "launches_per_group": sum(p.info()["chain_launches"] for p, m in ogs[0].chain
                                                   if m == "chain") + sum(1 for p, m in ogs[0].chain if m != "chain"),
                         "speedup": round(c_step / ms_step, 2)}
+        # both forms replayed from HIP graphs: no host cost per launch, so
+        # what remains of the chain's cost is the GPU's per-launch overhead
+        capture("chain")
+        capture("grouped")
+        gc_ms, _ = timed("graph_chain", csteps, args.warmup)
+        gg_ms, _ = timed("graph_grouped", args.steps, args.warmup)
+        g_step = gg_ms / args.steps
+        out["graph"] = {"us_per_group": round(g_step * 1000.0, 3),
+                        "chain_us_per_group": round(gc_ms / csteps * 1000.0, 3),
+                        "chain_speedup": round(gc_ms / csteps / g_step, 2)}
+        graphs.clear()
     if ogs[0].eager is not None and not args.no_chain:
         # the same op-group as PyTorch eager ops (context: what the model ran
         # before the rewrite, with the vendor BLAS for its Linears)
