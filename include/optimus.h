@@ -498,6 +498,11 @@ typedef OPTIMUS_ENUM(optimus_exec_mode_e) {
   OPTIMUS_EXEC_HORIZONTAL = 2
 } optimus_exec_mode;
 
+/* An execution only enqueues kernel launches on `stream`: no host
+ * synchronization, copies or fills. It can therefore be recorded into a HIP
+ * graph and replayed; a CHAIN or HORIZONTAL split-op-cat plan must have run
+ * once in that mode before it is recorded (its temporaries are allocated on
+ * first use). The plan and every tensor it names must outlive the graph. */
 optimus_status optimus_plan_execute(optimus_plan plan, optimus_stream_t stream);
 optimus_status optimus_plan_execute_mode(optimus_plan plan, optimus_exec_mode mode, optimus_stream_t stream);
 void optimus_plan_destroy(optimus_plan plan);
