@@ -710,7 +710,10 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
 // order. A wave loads batches of kR16Batch k-groups, the next batch in flight
 // while the current one is multiplied; even and odd k-groups go to separate
 // accumulators, so four independent MFMA chains run per wave. Bias, gamma and
-// beta are read straight into registers beside the first operand loads.
+// beta are read once per column, by the first kR16Cols threads after the
+// first operand batch is on its way, and reach the lanes through LDS after
+// the K loop (one 4-byte load per value and lane had doubled the memory
+// instructions ahead of the first MFMA).
 constexpr int kR16Rows = 16, kR16Cols = 128, kR16Batch = 8;
 
 template <int ACTX>
@@ -722,6 +725,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_rows16_kernel(const DevLinea
   constexpr int KB = kR16Batch;
   __shared__ float hand[3][4][8][64];    // K-split partials: [split - 1][column block][value][lane]
   __shared__ float red[2][kR16Rows][4];  // fused LayerNorm row partials: [pass][row][column block]
+  __shared__ __align__(16) float par[3][kR16Cols];  // the tile's bias, gamma, beta (0, 1, 0 where absent)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, lq = lane >> 4;
 
@@ -781,21 +785,17 @@ __global__ __launch_bounds__(256) void grouped_gemm_rows16_kernel(const DevLinea
 
     // this lane's columns: c0 + 16 j + 4 lq + r of the tile
     const int cl = c0 + lq * 4;
-    float pb[2][4], pg[2][4], pe[2][4];
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int c = cl + 16 * j + r;
-        const bool in = c < Nr;
-        pb[j][r] = (d.bias && in) ? Elem<float>::load1(d.bias, n0 + c) : 0.f;
-        if constexpr (LN) {
-          pg[j][r] = in ? (d.gamma ? Elem<float>::load1(d.gamma, c) : 1.f) : 0.f;
-          pe[j][r] = (d.beta && in) ? Elem<float>::load1(d.beta, c) : 0.f;
-        }
-      }
 
     if (g_beg < g_end) load(bufA, g_beg);
+    // thread tid < kR16Cols: column tid's parameters (zero past the member's columns)
+    float qb = 0.f, qg = 0.f, qe = 0.f;
+    if (tid < kR16Cols && tid < Nr) {
+      qb = d.bias ? Elem<float>::load1(d.bias, n0 + tid) : 0.f;
+      if constexpr (LN) {
+        qg = d.gamma ? Elem<float>::load1(d.gamma, tid) : 1.f;
+        qe = d.beta ? Elem<float>::load1(d.beta, tid) : 0.f;
+      }
+    }
     for (int g = g_beg; g < g_end; g += 2 * KB) {
       if (g + KB < g_end) load(bufB, g + KB);
       compute(bufA, g);
@@ -806,20 +806,34 @@ __global__ __launch_bounds__(256) void grouped_gemm_rows16_kernel(const DevLinea
 #pragma unroll
     for (int j = 0; j < 2; ++j) s[j] = acc[j][0] + acc[j][1];
 
-    if (ks > 1) {
-      // the K-split waves hand their sums to the first wave of their columns
-      if (sk > 0)
+    if (tid < kR16Cols) {
+      par[0][tid] = qb;
+      if constexpr (LN) {
+        par[1][tid] = qg;
+        par[2][tid] = qe;
+      }
+    }
+    // the K-split waves hand their sums to the first wave of their columns
+    if (ks > 1 && sk > 0)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) hand[sk - 1][cb][j * 4 + r][lane] = s[j][r];
+    __syncthreads();
+    if (ks > 1 && sk == 0)
+      for (int q = 1; q < ks; ++q)
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) hand[sk - 1][cb][j * 4 + r][lane] = s[j][r];
-      __syncthreads();
-      if (sk == 0)
-        for (int q = 1; q < ks; ++q)
+          for (int r = 0; r < 4; ++r) s[j][r] += hand[q - 1][cb][j * 4 + r][lane];
+    f32x4 pb[2], pg[2], pe[2];
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) s[j][r] += hand[q - 1][cb][j * 4 + r][lane];
+    for (int j = 0; j < 2; ++j) {
+      pb[j] = *(const f32x4*)&par[0][cl + 16 * j];
+      if constexpr (LN) {
+        pg[j] = *(const f32x4*)&par[1][cl + 16 * j];
+        pe[j] = *(const f32x4*)&par[2][cl + 16 * j];
+      }
     }
 
     float o[2][4];
