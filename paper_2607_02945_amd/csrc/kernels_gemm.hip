@@ -692,7 +692,7 @@ __global__ __launch_bounds__(WM* WN * 64) void grouped_gemm_kernel(const DevLine
 // Small fp32 groups (fewer 32-row tiles than CUs, at most 128 outputs per row)
 // are latency bound: a workgroup's time is its descriptor and operand load
 // latency plus its serial MFMA work. This kernel halves that work per
-// workgroup with 16-row tiles on v_mfma_f32_16x16x4f32, and stages nothing
+// workgroup with 16-row tiles on v_mfma_f32_16x16x4f32, and stages no operand
 // through LDS: each lane loads its MFMA operands straight from global memory
 // as 16-byte chunks of four consecutive k (w row n = lane % 16, x row
 // m = lane % 16, k offset 4 (lane / 16) in a group of 16 k), so the waves of a
@@ -725,7 +725,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_rows16_kernel(const DevLinea
   constexpr int KB = kR16Batch;
   __shared__ float hand[3][4][8][64];    // K-split partials: [split - 1][column block][value][lane]
   __shared__ float red[2][kR16Rows][4];  // fused LayerNorm row partials: [pass][row][column block]
-  __shared__ __align__(16) float par[3][kR16Cols];  // the tile's bias, gamma, beta (0, 1, 0 where absent)
+  __shared__ __align__(16) float par[3][kR16Cols];  // the tile's bias, gamma, beta per column; 0 past N
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, lq = lane >> 4;
 
