@@ -291,6 +291,28 @@ def test_streaming_small_members(act):
         _check(ms, ys, "bf16", act, f"streaming {mode}")
 
 
+def test_streaming_reordered_item_list():
+    """More streaming items than CUs: the planner orders them by bytes per row
+    and reverses every other device-width of the list, so the grouped list is
+    no longer member-major and the per-member chain launches walk their own
+    copy. Both modes, every element against the oracle."""
+    say("[linear streaming] reordered item list")
+    g = synth.rng(131)
+    dims = [8, 16, 24, 32, 40, 48, 56, 64]
+    shapes = [(int(g.choice([300, 512, 700])), int(g.choice(dims)), int(g.choice(dims))) for _ in range(300)]
+    ms = _members(shapes, "bf16", seed=132)
+    xs, ws, bs = [m[0] for m in ms], [m[1] for m in ms], [m[2] for m in ms]
+    for mode in ["grouped", "chain"]:
+        ys = [torch.full((x.shape[0], w.shape[0]), float("nan"), dtype=x.dtype, device="cuda") for x, w, _ in ms]
+        p = B.optimus_plan_linear(xs, ws, bs, ys, "sigmoid")
+        info = p.info()
+        assert info["kernel"] == "grouped_gemm_stream_bf16" and info["work_items"] > 256, info
+        p.execute(mode)
+        torch.cuda.synchronize()
+        p.close()
+        _check(ms, ys, "bf16", "sigmoid", f"streaming reordered {mode}")
+
+
 def test_streaming_strided_and_fallback():
     """Row strides above the row lengths keep the streaming kernel (16-byte
     aligned rows); a member with K not a multiple of 8 sends the group to the
